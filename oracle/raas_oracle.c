@@ -1,0 +1,376 @@
+/*
+ * CPU oracle for page-based RaaS decode (TEST INFRASTRUCTURE ONLY).
+ *
+ * A plain, slow, fp64 reference of what the decode path computes, written
+ * from the paper (arXiv 2502.11147): Algorithm 1 (RaaS Algorithm) for the
+ * order of a decode step, Section 3.2 for the top-r / LRU timestamp rule and
+ * prefill pinning, Section 3.3 for page granularity and the Quest-style
+ * representative score. Only tests, the smoke check and the benchmark's CPU
+ * baseline may call it; the product path never does. It shares no code with
+ * the HIP path.
+ *
+ * One kvm (KV manager) holds the cache of one unit: one sequence, one layer,
+ * one KV head, with the G query heads that share that KV head.
+ *
+ * Readings of points the paper leaves open (each is marked where it is used):
+ *  R1 representative key: per-channel min and max of the page's keys, score
+ *     = sum_c max(q_c*kmax_c, q_c*kmin_c), an upper bound on q.k for every key
+ *     of the page (Quest's criterion, Section 3.3 adopts Quest's strategy).
+ *  R2 GQA: one decision per unit; page score = max over the G query heads.
+ *  R3 prefill longer than the budget: pin the first min(P_pages, S-1) pages
+ *     and drop the rest (policy PIN_HEAD), or refuse (policy ERROR).
+ *  R4 a partial last prefill page is not topped up by decode tokens.
+ *  R5 a new page's timestamp is the clock at its creation; the clock is the
+ *     token's absolute position.
+ *  R6 ties of the oldest timestamp go to the smallest logical page id.
+ *  R7 "top-r": n = #evictable pages, k = floor(r*n); the pages strictly above
+ *     the (n-k)-th smallest score are refreshed (k = n: all; k = 0: none).
+ *     Only decode (evictable) pages take part; the current tail page counts.
+ *  R8 eviction is eager, in Algorithm 1's order: after the refresh, when the
+ *     next token has no room (tail page full and no free slot).
+ *  R9 softmax scale 1/sqrt(d); attention covers every resident token.
+ */
+#include <math.h>
+#include <stdint.h>
+#include <stdlib.h>
+#include <string.h>
+
+#define ORC_OK 0
+#define ORC_E_INVALID (-1)
+#define ORC_E_BUDGET (-2)
+#define ORC_E_STATE (-3)
+#define ORC_E_INTERNAL (-10)
+
+enum { FREE = 0, PINNED = 1, EVICTABLE = 2 };
+enum { POLICY_PIN_HEAD = 0, POLICY_ERROR = 1 };
+
+typedef struct {
+    int G, d, ps, S, policy;
+    double r;
+    /* per page slot */
+    int *state, *lid, *fill, *ts;
+    double *K, *V;       /* [S][ps][d] */
+    double *kmin, *kmax; /* [S][d] representative keys (R1) */
+    /* per unit */
+    int tail, next_lid, clock, prefilled;
+    /* diagnostics of the last decode step */
+    double *score; /* [S], NaN where the slot is not evictable */
+    double theta;  /* the threshold; -inf when every page was refreshed, NaN when none */
+    int n_evictable, k_refreshed, evicted;
+} orc_kvm;
+
+orc_kvm* orc_new(int G, int d, int ps, int S, double r, int policy) {
+    if (G < 1 || d < 1 || ps < 1 || S < 2 || !(r >= 0.0 && r <= 1.0)) return NULL;
+    if (policy != POLICY_PIN_HEAD && policy != POLICY_ERROR) return NULL;
+    orc_kvm* m = (orc_kvm*)calloc(1, sizeof(orc_kvm));
+    m->G = G; m->d = d; m->ps = ps; m->S = S; m->r = r; m->policy = policy;
+    m->state = (int*)calloc((size_t)S, sizeof(int));
+    m->lid = (int*)calloc((size_t)S, sizeof(int));
+    m->fill = (int*)calloc((size_t)S, sizeof(int));
+    m->ts = (int*)calloc((size_t)S, sizeof(int));
+    m->K = (double*)calloc((size_t)S * ps * d, sizeof(double));
+    m->V = (double*)calloc((size_t)S * ps * d, sizeof(double));
+    m->kmin = (double*)calloc((size_t)S * d, sizeof(double));
+    m->kmax = (double*)calloc((size_t)S * d, sizeof(double));
+    m->score = (double*)calloc((size_t)S, sizeof(double));
+    for (int s = 0; s < S; ++s) {
+        m->state[s] = FREE;
+        m->lid[s] = -1;
+        m->ts[s] = -1;
+        m->score[s] = NAN;
+    }
+    m->tail = -1;
+    m->evicted = -1;
+    m->theta = NAN;
+    return m;
+}
+
+void orc_free(orc_kvm* m) {
+    if (!m) return;
+    free(m->state); free(m->lid); free(m->fill); free(m->ts);
+    free(m->K); free(m->V); free(m->kmin); free(m->kmax); free(m->score);
+    free(m);
+}
+
+static void page_reset_representative(orc_kvm* m, int s) {
+    for (int c = 0; c < m->d; ++c) {
+        m->kmin[(size_t)s * m->d + c] = INFINITY;
+        m->kmax[(size_t)s * m->d + c] = -INFINITY;
+    }
+}
+
+/* write one token into slot s at its next position and widen the page's
+ * per-channel min/max (R1) */
+static void page_store_token(orc_kvm* m, int s, const double* k, const double* v) {
+    const int d = m->d;
+    size_t off = ((size_t)s * m->ps + m->fill[s]) * d;
+    for (int c = 0; c < d; ++c) {
+        m->K[off + c] = k[c];
+        m->V[off + c] = v[c];
+        if (k[c] < m->kmin[(size_t)s * d + c]) m->kmin[(size_t)s * d + c] = k[c];
+        if (k[c] > m->kmax[(size_t)s * d + c]) m->kmax[(size_t)s * d + c] = k[c];
+    }
+    m->fill[s] += 1;
+}
+
+/* kvm.store_cache(K, V, -, "prefill"): store the prefill tokens' K/V in
+ * pages and mark them non-evictable (Algorithm 1; Section 3.1 keeps every
+ * prefill token). K, V: [P][d]. */
+int orc_prefill(orc_kvm* m, const double* K, const double* V, int P) {
+    if (!m || P < 0 || (P > 0 && (!K || !V))) return ORC_E_INVALID;
+    if (m->prefilled) return ORC_E_STATE;
+    const int ps = m->ps;
+    int pages = (P + ps - 1) / ps;
+    int keep = pages;
+    if (keep > m->S - 1) { /* R3: at least one slot stays for decode pages */
+        if (m->policy == POLICY_ERROR) return ORC_E_BUDGET;
+        keep = m->S - 1;
+    }
+    for (int p = 0; p < keep; ++p) {
+        m->state[p] = PINNED;
+        m->lid[p] = p;
+        m->ts[p] = -1;
+        m->fill[p] = 0;
+        page_reset_representative(m, p);
+        for (int t = p * ps; t < P && t < (p + 1) * ps; ++t)
+            page_store_token(m, p, K + (size_t)t * m->d, V + (size_t)t * m->d);
+    }
+    m->next_lid = pages;
+    m->tail = -1; /* R4: decode tokens start a fresh page */
+    m->clock = P; /* R5 */
+    m->prefilled = 1;
+    return ORC_OK;
+}
+
+/* kvm.load_cache + "K = K_old::K_new" + attention(Q, K, V) (Algorithm 1):
+ * exact softmax attention of each of the G queries over every resident
+ * token plus the new one (R9). out: [G][d]. */
+static void attention(const orc_kvm* m, const double* q, const double* k_new, const double* v_new,
+                      double* out) {
+    const int G = m->G, d = m->d, ps = m->ps;
+    const double scale = 1.0 / sqrt((double)d);
+    int n_old = 0;
+    for (int s = 0; s < m->S; ++s)
+        if (m->state[s] != FREE) n_old += m->fill[s];
+    const int n = n_old + 1;
+    double* Kc = (double*)malloc(sizeof(double) * (size_t)n * d);
+    double* Vc = (double*)malloc(sizeof(double) * (size_t)n * d);
+    double* logit = (double*)malloc(sizeof(double) * (size_t)n);
+    int i = 0;
+    for (int s = 0; s < m->S; ++s) { /* K_old, V_old */
+        if (m->state[s] == FREE) continue;
+        for (int t = 0; t < m->fill[s]; ++t, ++i) {
+            memcpy(Kc + (size_t)i * d, m->K + ((size_t)s * ps + t) * d, sizeof(double) * d);
+            memcpy(Vc + (size_t)i * d, m->V + ((size_t)s * ps + t) * d, sizeof(double) * d);
+        }
+    }
+    memcpy(Kc + (size_t)i * d, k_new, sizeof(double) * d); /* :: K_new */
+    memcpy(Vc + (size_t)i * d, v_new, sizeof(double) * d);
+    for (int j = 0; j < G; ++j) {
+        const double* qj = q + (size_t)j * d;
+        double mx = -INFINITY;
+        for (int t = 0; t < n; ++t) {
+            double acc = 0.0;
+            for (int c = 0; c < d; ++c) acc += qj[c] * Kc[(size_t)t * d + c];
+            logit[t] = acc * scale;
+            if (logit[t] > mx) mx = logit[t];
+        }
+        double den = 0.0;
+        for (int c = 0; c < d; ++c) out[(size_t)j * d + c] = 0.0;
+        for (int t = 0; t < n; ++t) {
+            double p = exp(logit[t] - mx);
+            den += p;
+            for (int c = 0; c < d; ++c) out[(size_t)j * d + c] += p * Vc[(size_t)t * d + c];
+        }
+        for (int c = 0; c < d; ++c) out[(size_t)j * d + c] /= den;
+    }
+    free(Kc); free(Vc); free(logit);
+}
+
+static int cmp_double(const void* a, const void* b) {
+    double x = *(const double*)a, y = *(const double*)b;
+    return (x > y) - (x < y);
+}
+
+/* kvm.is_full(): the next token has no room (R8) */
+static int is_full(const orc_kvm* m) {
+    if (m->tail >= 0 && m->fill[m->tail] < m->ps) return 0;
+    for (int s = 0; s < m->S; ++s)
+        if (m->state[s] == FREE) return 0;
+    return 1;
+}
+
+/*
+ * One decode step of one unit: attention, then kvm.store_cache(.., "decode")
+ * = store K_new/V_new, give the top-r pages the latest timestamp, and evict
+ * the oldest page when the cache is full (Algorithm 1, Section 3.3).
+ *
+ * q: [G][d]; k_new, v_new: [d]; out: [G][d] or NULL (attention skipped).
+ * injected: NULL, or per-slot page scores that replace the representative
+ * scores (used to drive the retention policy directly in tests).
+ */
+int orc_decode(orc_kvm* m, const double* q, const double* k_new, const double* v_new, double* out,
+               const double* injected) {
+    if (!m) return ORC_E_INVALID;
+    if (!m->prefilled) return ORC_E_STATE;
+    if (!injected && (!q || !k_new || !v_new)) return ORC_E_INVALID;
+    const int G = m->G, d = m->d, S = m->S;
+    const int c = m->clock;
+
+    if (out) attention(m, q, k_new, v_new, out);
+
+    /* store K_new, V_new: into the tail page, or a fresh page taken from the
+     * lowest free slot when the tail is full or absent (Section 3.3) */
+    if (m->tail < 0 || m->fill[m->tail] == m->ps) {
+        int s = -1;
+        for (int i = 0; i < S; ++i)
+            if (m->state[i] == FREE) { s = i; break; }
+        if (s < 0) return ORC_E_INTERNAL; /* eager eviction leaves a free slot */
+        m->state[s] = EVICTABLE;
+        m->lid[s] = m->next_lid++;
+        m->fill[s] = 0;
+        m->ts[s] = c; /* R5 */
+        page_reset_representative(m, s);
+        m->tail = s;
+    }
+    if (k_new && v_new) {
+        page_store_token(m, m->tail, k_new, v_new);
+    } else {
+        m->fill[m->tail] += 1; /* retention-only run: no payload */
+    }
+
+    /* one representative score per evictable page (R1, R2) */
+    int n = 0;
+    for (int s = 0; s < S; ++s) {
+        m->score[s] = NAN;
+        if (m->state[s] != EVICTABLE) continue;
+        ++n;
+        if (injected) {
+            m->score[s] = injected[s];
+            continue;
+        }
+        double best = -INFINITY;
+        for (int j = 0; j < G; ++j) {
+            double acc = 0.0;
+            for (int ch = 0; ch < d; ++ch) {
+                double a = q[(size_t)j * d + ch] * m->kmax[(size_t)s * d + ch];
+                double b = q[(size_t)j * d + ch] * m->kmin[(size_t)s * d + ch];
+                acc += (a > b) ? a : b;
+            }
+            if (acc > best) best = acc;
+        }
+        m->score[s] = best;
+    }
+
+    /* new timestamps to the pages with the top-r scores (R7) */
+    int k = (int)floor(m->r * (double)n);
+    m->n_evictable = n;
+    m->k_refreshed = k;
+    m->theta = NAN;
+    if (k > 0) {
+        double theta = -INFINITY;
+        if (k < n) {
+            double* sorted = (double*)malloc(sizeof(double) * (size_t)n);
+            int i = 0;
+            for (int s = 0; s < S; ++s)
+                if (m->state[s] == EVICTABLE) sorted[i++] = m->score[s];
+            qsort(sorted, (size_t)n, sizeof(double), cmp_double);
+            theta = sorted[n - k - 1]; /* the (n-k)-th smallest */
+            free(sorted);
+        }
+        m->theta = theta;
+        for (int s = 0; s < S; ++s)
+            if (m->state[s] == EVICTABLE && m->score[s] > theta) m->ts[s] = c;
+    }
+
+    /* if kvm.is_full(): evict the page with the oldest timestamp (R6, R8) */
+    m->evicted = -1;
+    if (is_full(m)) {
+        int v = -1;
+        for (int s = 0; s < S; ++s) {
+            if (m->state[s] != EVICTABLE) continue;
+            if (v < 0 || m->ts[s] < m->ts[v] || (m->ts[s] == m->ts[v] && m->lid[s] < m->lid[v])) v = s;
+        }
+        if (v < 0) return ORC_E_INTERNAL;
+        m->evicted = m->lid[v];
+        m->state[v] = FREE;
+        m->lid[v] = -1;
+        m->ts[v] = -1;
+        m->fill[v] = 0;
+        if (m->tail == v) m->tail = -1;
+    }
+    m->clock = c + 1;
+    return ORC_OK;
+}
+
+/* page table (lid or -1), timestamps (-1 for pinned and free), state, fill */
+void orc_state(const orc_kvm* m, int* page_table, int* ts, int* state, int* fill, int* unit) {
+    for (int s = 0; s < m->S; ++s) {
+        if (page_table) page_table[s] = (m->state[s] == FREE) ? -1 : m->lid[s];
+        if (ts) ts[s] = (m->state[s] == EVICTABLE) ? m->ts[s] : -1;
+        if (state) state[s] = m->state[s];
+        if (fill) fill[s] = m->fill[s];
+    }
+    if (unit) {
+        unit[0] = m->tail;
+        unit[1] = m->next_lid;
+        unit[2] = m->clock;
+        unit[3] = m->evicted;
+        unit[4] = m->n_evictable;
+        unit[5] = m->k_refreshed;
+    }
+}
+
+/* per-slot scores of the last step (NaN where not evictable) and the threshold */
+void orc_last_scores(const orc_kvm* m, double* score, double* theta) {
+    if (score) memcpy(score, m->score, sizeof(double) * (size_t)m->S);
+    if (theta) *theta = m->theta;
+}
+
+/* the resident keys / values in slot order, for tests: [S][ps][d] */
+void orc_pages(const orc_kvm* m, double* K, double* V, double* kmin, double* kmax) {
+    size_t n = (size_t)m->S * m->ps * m->d;
+    if (K) memcpy(K, m->K, sizeof(double) * n);
+    if (V) memcpy(V, m->V, sizeof(double) * n);
+    if (kmin) memcpy(kmin, m->kmin, sizeof(double) * (size_t)m->S * m->d);
+    if (kmax) memcpy(kmax, m->kmax, sizeof(double) * (size_t)m->S * m->d);
+}
+
+/*
+ * One decode step for n independent units (OpenMP across units only). The
+ * inputs are float32 (values of the workload's dtype, widened exactly).
+ * q: [n][G][d]; k, v: [n][d]; out: [n][G][d] fp64 or NULL.
+ */
+int orc_decode_batch(orc_kvm** ms, int n, const float* q, const float* k, const float* v,
+                     double* out) {
+    int status = ORC_OK;
+#pragma omp parallel for schedule(dynamic, 1)
+    for (int u = 0; u < n; ++u) {
+        orc_kvm* m = ms[u];
+        const int G = m->G, d = m->d;
+        double* qd = (double*)malloc(sizeof(double) * (size_t)(G + 2) * d);
+        double* kd = qd + (size_t)G * d;
+        double* vd = kd + d;
+        for (int i = 0; i < G * d; ++i) qd[i] = (double)q[(size_t)u * G * d + i];
+        for (int i = 0; i < d; ++i) {
+            kd[i] = (double)k[(size_t)u * d + i];
+            vd[i] = (double)v[(size_t)u * d + i];
+        }
+        int rc = orc_decode(m, qd, kd, vd, out ? out + (size_t)u * G * d : NULL, NULL);
+        if (rc != ORC_OK) {
+#pragma omp critical
+            status = rc;
+        }
+        free(qd);
+    }
+    return status;
+}
+
+int orc_threads(void) {
+#ifdef _OPENMP
+    extern int omp_get_max_threads(void);
+    return omp_get_max_threads();
+#else
+    return 1;
+#endif
+}

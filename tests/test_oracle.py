@@ -1,0 +1,183 @@
+"""The CPU oracle against what the paper and the mathematics fix (no GPU).
+
+The checks live in ``pins.py``. They run here against the committed oracle,
+and against copies of it with one planted mistake each, every one of which
+must be caught by at least one check.
+"""
+from __future__ import annotations
+
+import json
+import os
+
+import numpy as np
+import pytest
+
+import oracle
+import pins
+import synth
+from oracle.history import HistoryLRU
+
+GOLDEN = os.path.join(os.path.dirname(__file__), "golden")
+
+
+@pytest.mark.parametrize("check", pins.ALL_CHECKS, ids=lambda c: c.__name__)
+def test_oracle_pin(check, oracle_lib):
+    check(oracle_lib)
+
+
+# (name, [(original text, replacement)]) -- each a plausible slip in the oracle
+MUTANTS = [
+    ("score_uses_min", [("acc += (a > b) ? a : b;", "acc += (a < b) ? a : b;")]),
+    ("no_softmax_scale", [("const double scale = 1.0 / sqrt((double)d);", "const double scale = 1.0;")]),
+    ("refresh_ties_at_threshold", [("m->score[s] > theta) m->ts[s] = c;", "m->score[s] >= theta) m->ts[s] = c;")]),
+    ("order_statistic_off_by_one", [("theta = sorted[n - k - 1];", "theta = sorted[n - k];")]),
+    ("tie_break_newest", [("m->lid[s] < m->lid[v]", "m->lid[s] > m->lid[v]")]),
+    ("new_page_unstamped", [("m->ts[s] = c; /* R5 */", "m->ts[s] = -1; /* R5 */")]),
+    ("prefill_fills_cache", [("keep = m->S - 1;", "keep = m->S;")]),
+    ("pinned_not_attended", [("if (m->state[s] != FREE) n_old += m->fill[s];",
+                              "if (m->state[s] == EVICTABLE) n_old += m->fill[s];"),
+                             ("        if (m->state[s] == FREE) continue;\n        for (int t = 0; t < m->fill[s]; ++t, ++i) {",
+                              "        if (m->state[s] != EVICTABLE) continue;\n        for (int t = 0; t < m->fill[s]; ++t, ++i) {")]),
+    ("kmax_not_widened", [("if (k[c] > m->kmax[(size_t)s * d + c]) m->kmax[(size_t)s * d + c] = k[c];", "")]),
+    ("evicted_tail_kept", [("if (m->tail == v) m->tail = -1;", "")]),
+    ("top_r_rounds_up", [("int k = (int)floor(m->r * (double)n);", "int k = (int)ceil(m->r * (double)n);")]),
+    ("pinned_pages_scored", [("        m->score[s] = NAN;\n        if (m->state[s] != EVICTABLE) continue;",
+                              "        m->score[s] = NAN;\n        if (m->state[s] == FREE) continue;")]),
+    ("softmax_sign", [("double p = exp(logit[t] - mx);", "double p = exp(mx - logit[t]);")]),
+    ("gqa_last_head_only", [("if (acc > best) best = acc;", "best = acc;")]),
+]
+
+
+@pytest.mark.parametrize("name,edits", MUTANTS, ids=[m[0] for m in MUTANTS])
+def test_planted_mistake_is_caught(name, edits, tmp_path):
+    src = open(oracle.SRC).read()
+    for old, new in edits:
+        assert src.count(old) == 1, (name, old)
+        src = src.replace(old, new)
+    path = tmp_path / ("mutant_%s.c" % name)
+    path.write_text(src)
+    lib = oracle.build(str(path), str(tmp_path / ("libmutant_%s.so" % name)), force=True)
+    caught = []
+    for check in pins.ALL_CHECKS:
+        try:
+            check(lib)
+        except (AssertionError, oracle.OracleError, ValueError, KeyError, IndexError):
+            caught.append(check.__name__)
+    assert caught, "planted mistake %s went unnoticed" % name
+
+
+def _golden():
+    with open(os.path.join(GOLDEN, "retention_worked_example.json")) as f:
+        return json.load(f)
+
+
+def test_golden_worked_example_oracle(oracle_lib):
+    g = _golden()
+    ps, S, P = g["page_size"], g["slots"], g["prefill_len"]
+    m = oracle.Kvm(1, 2, ps, S, r=g["r"], lib=oracle_lib)
+    assert m.prefill(np.zeros((P, 2)), np.zeros((P, 2))) == 0
+    for step in g["steps"]:
+        st = m.state()
+        assert st["clock"] == step["clock"]
+        slot_lid = {s: int(st["page_table"][s]) for s in range(S) if st["state"][s] == oracle.EVICTABLE}
+        new = pins._new_slot(st, ps)
+        if new is not None:
+            slot_lid[new] = st["next_lid"]
+        assert sorted(slot_lid.values()) == sorted(int(x) for x in step["scores"])
+        sc = np.zeros(S)
+        for s, lid in slot_lid.items():
+            sc[s] = step["scores"][str(lid)]
+        m.decode_with_scores(sc)
+        st = m.state()
+        assert st["evicted"] == step["evicted"], step
+        assert st["page_table"].tolist() == step["page_table"], step
+        assert st["ts"].tolist() == step["ts"], step
+
+
+def test_golden_worked_example_history():
+    g = _golden()
+    h = HistoryLRU(g["page_size"], g["slots"], g["r"], g["prefill_len"])
+    for step in g["steps"]:
+        ev = h.decode(lambda lid: step["scores"][str(lid)])
+        assert (ev if ev is not None else -1) == step["evicted"]
+        assert h.resident_lids() == sorted(x for x in step["page_table"] if x >= 0)
+
+
+def test_generator_philox_known_answers(synth_lib):
+    """Philox4x32-10 against the known-answer vectors published with the
+    Random123 library (Salmon et al., SC 2011)."""
+    kat = [
+        ([0, 0, 0, 0], [0, 0], [0x6627E8D5, 0xE169C58D, 0xBC57AC4C, 0x9B00DBD8]),
+        ([0xFFFFFFFF] * 4, [0xFFFFFFFF] * 2, [0x408F276D, 0x41C83B0E, 0xA20BC7C6, 0x6D5451FD]),
+        ([0x243F6A88, 0x85A308D3, 0x13198A2E, 0x03707344], [0xA4093822, 0x299F31D0],
+         [0xD16CFE09, 0x94FDCCEB, 0x5001E420, 0x24126EA1]),
+    ]
+    for ctr, key, want in kat:
+        assert synth_lib.philox4x32_10(ctr, key) == want
+
+
+def test_generator_statistics_and_milestones(synth_lib):
+    """Shape of the synthetic inputs: N(0,1) values exactly representable in
+    the dtype, and queries inside a milestone window at cos 0.8 to the
+    milestone key (one active milestone)."""
+    w = synth.get_workload("tiny-f32")
+    q, k, v = synth.steps(w, 0, 0, 0, 200)
+    assert abs(float(k.std()) - 1.0) < 0.05 and abs(float(k.mean())) < 0.05
+    wb = synth.get_workload("llama8b-b1-L1024")
+    qb, kb, vb = synth.steps(wb, 0, 0, 0, 4)
+    bits = qb.view(np.uint32)
+    assert np.all(bits & 0xFFFF == 0)  # bf16-representable
+    # tiny-f32: milestones at decode steps 31, 63, ...; window 64
+    assert synth.active_milestones(w, 0, 0, 0, 0, 31) == []
+    assert synth.active_milestones(w, 0, 0, 0, 0, 32) == [31]
+    assert synth.active_milestones(w, 0, 0, 0, 0, 95) == [31, 63]
+    assert synth.active_milestones(w, 0, 0, 0, 0, 96) == [63, 95]
+    # one active milestone at step 32: every query head at cos 0.8 to k_31
+    q, k, _ = synth.steps(w, 0, 0, 31, 2)
+    km = k[0, 0, 0].astype(np.float64)
+    for j in range(w.group):
+        qj = q[1, 0, j].astype(np.float64)
+        cos = qj @ km / np.linalg.norm(qj) / np.linalg.norm(km)
+        assert abs(cos - 0.8) < 1e-5
+    assert synth.active_milestones(w, 0, 0, 0, 0, 0) == []
+    # stress workload: heavy-tailed keys (excess kurtosis well above 0)
+    ws = synth.get_workload("llama8b-b128-ps32-L512").replace(batch=2)
+    _, ks, vs = synth.steps(ws, 0, 0, 0, 64)
+    kk = ks.astype(np.float64).ravel()
+    vv = vs.astype(np.float64).ravel()
+    kurt_k = np.mean((kk - kk.mean()) ** 4) / np.var(kk) ** 2 - 3
+    kurt_v = np.mean((vv - vv.mean()) ** 4) / np.var(vv) ** 2 - 3
+    assert kurt_k > 0.5 and abs(kurt_v) < 0.3
+
+
+def test_generator_random_access(synth_lib):
+    """Any window of steps regenerates to the same values."""
+    w = synth.get_workload("llama8b-b1-L1024")
+    a = synth.steps(w, 7, 0, 100, 10)
+    b = synth.steps(w, 7, 0, 105, 3)
+    for x, y in zip(a, b):
+        assert np.array_equal(x[5:8], y)
+    c = synth.steps(w, 8, 0, 105, 3)
+    assert not np.array_equal(a[0][5:8], c[0])
+
+
+def test_oracle_batch_matches_single(oracle_lib):
+    """The OpenMP batch entry gives the per-unit results."""
+    rng = np.random.default_rng(0)
+    G, d, ps, S, P, n = 2, 8, 4, 4, 6, 5
+    a = [oracle.Kvm(G, d, ps, S) for _ in range(n)]
+    b = [oracle.Kvm(G, d, ps, S) for _ in range(n)]
+    for u in range(n):
+        K = rng.standard_normal((P, d)).astype(np.float32)
+        V = rng.standard_normal((P, d)).astype(np.float32)
+        a[u].prefill(K, V)
+        b[u].prefill(K, V)
+    for t in range(30):
+        q = rng.standard_normal((n, G, d)).astype(np.float32)
+        k = rng.standard_normal((n, d)).astype(np.float32)
+        v = rng.standard_normal((n, d)).astype(np.float32)
+        out = oracle.decode_batch(a, q, k, v)
+        for u in range(n):
+            o1 = b[u].decode(q[u], k[u], v[u])
+            assert np.array_equal(o1, out[u])
+            assert a[u].state()["page_table"].tolist() == b[u].state()["page_table"].tolist()
