@@ -1,0 +1,159 @@
+/*
+ * raas.h -- C ABI of the MI355X (gfx950) decode path of page-based RaaS,
+ * Reasoning-Aware Attention Sparsity (Hu et al., arXiv 2502.11147).
+ *
+ * The library keeps, per (sequence, layer, KV head) -- a "unit" -- a fixed
+ * pool of S = budget_tokens / page_size pages in HBM (O(L) memory, Section
+ * 4.3). Prefill pages are stored and marked non-evictable (Algorithm 1,
+ * Section 3.1). Every decode step (Algorithm 1, Sections 3.2-3.3):
+ *   1. stores the new token's K/V in the unit's tail page, opening a fresh
+ *      page in the lowest free slot when the tail is full;
+ *   2. computes exact softmax attention of the G query heads of the unit
+ *      over every resident token (scale 1/sqrt(head_dim));
+ *   3. scores every evictable page once against the step's queries with a
+ *      representative key: per-channel key min/max of the page, score =
+ *      max over the G heads of sum_c max(q_c*kmax_c, q_c*kmin_c), in fp64
+ *      (Section 3.3 adopts Quest's representative-key strategy);
+ *   4. gives the latest timestamp (the token's absolute position) to the
+ *      evictable pages strictly above the (n-k)-th smallest score, where n
+ *      is the number of evictable pages and k = floor(r*n) ("top-r", r =
+ *      0.5 = above the median, Section 3.2);
+ *   5. when the next token has no room (tail page full, no free slot),
+ *      evicts the evictable page with the oldest timestamp, ties to the
+ *      smallest logical page id (Algorithm 1, "evict KVs with the oldest
+ *      timestamps").
+ *
+ * Conventions for every call:
+ *  - Tensor arguments are DEVICE pointers owned by the caller, contiguous,
+ *    in the pool's dtype (fp32 or bf16) unless stated otherwise. Head-major
+ *    layouts: q and out [batch][n_q_heads][head_dim]; k_new, v_new
+ *    [batch][n_kv_heads][head_dim]; prefill k, v
+ *    [batch][n_kv_heads][prefill_len][head_dim]. Query head h belongs to KV
+ *    head h / (n_q_heads / n_kv_heads). Q and K are post-positional-encoding.
+ *  - `stream` is a hipStream_t passed as void* (NULL = default stream).
+ *    Calls enqueue work on it and return without waiting, except
+ *    raas_destroy and raas_export_state, which synchronise it. Inputs must
+ *    stay valid until the enqueued work has run.
+ *  - A call that returns an error has changed no state; raas_last_error()
+ *    gives a message (thread-local). RAAS_E_HIP reports a failed HIP call,
+ *    possibly of earlier asynchronous work.
+ *  - Inputs must be finite. Calls on one pool are not thread-safe.
+ */
+#ifndef RAAS_H
+#define RAAS_H
+
+#include <stddef.h>
+#include <stdint.h>
+
+#ifdef __cplusplus
+extern "C" {
+#endif
+
+#define RAAS_ABI_VERSION 1
+
+typedef enum {
+    RAAS_OK = 0,
+    RAAS_E_INVALID = -1, /* bad argument or configuration */
+    RAAS_E_BUDGET = -2,  /* prefill does not fit and the policy is RAAS_PREFILL_ERROR */
+    RAAS_E_STATE = -3,   /* call out of order: decode before prefill, prefill twice */
+    RAAS_E_HIP = -4,     /* a HIP runtime call failed */
+    RAAS_E_OOM = -5      /* device allocation failed */
+} raas_status;
+
+typedef enum { RAAS_F32 = 0, RAAS_BF16 = 1 } raas_dtype;
+
+/* What to do when the prefill needs more than S-1 pages (Limitations: the
+ * budget then goes to prefill tokens and decode tokens are discarded). */
+typedef enum {
+    RAAS_PREFILL_PIN_HEAD = 0, /* pin the first S-1 prefill pages, drop the rest;
+                                  one slot is left for decode pages */
+    RAAS_PREFILL_ERROR = 1     /* refuse with RAAS_E_BUDGET */
+} raas_prefill_policy;
+
+typedef struct {
+    int32_t batch;          /* sequences, >= 1; all advance together */
+    int32_t n_layers;       /* >= 1; each layer has its own pool and clock */
+    int32_t n_q_heads;      /* multiple of n_kv_heads, group G = n_q_heads/n_kv_heads <= 16 */
+    int32_t n_kv_heads;     /* >= 1 */
+    int32_t head_dim;       /* 64 or 128 */
+    int32_t page_size;      /* tokens per page: 8, 16, 32, 64 or 128 (the paper uses 16) */
+    int32_t budget_tokens;  /* L: multiple of page_size, 2 <= L/page_size <= 2048 */
+    int32_t dtype;          /* raas_dtype of q, k, v and out */
+    float r;                /* fraction of evictable pages refreshed per step, in [0, 1] (0.5) */
+    int32_t prefill_policy; /* raas_prefill_policy */
+} raas_config;
+
+typedef struct raas_pool raas_pool; /* opaque */
+
+/* Validates cfg, allocates the pool for every layer in device memory
+ * (hipMalloc) and clears it on `stream`. *out receives the pool; the caller
+ * releases it with raas_destroy. Errors: RAAS_E_INVALID, RAAS_E_OOM,
+ * RAAS_E_HIP. */
+raas_status raas_create_pool(const raas_config* cfg, void* stream, raas_pool** out);
+
+/* kvm.store_cache(K, V, -, "prefill") of Algorithm 1 for one layer: stores
+ * the prefill_len (>= 0) tokens of every unit in pages 0, 1, ... and marks
+ * them non-evictable; sets the clock to prefill_len. A partial last page is
+ * not topped up by decode tokens. k, v: [batch][n_kv_heads][prefill_len]
+ * [head_dim] (NULL allowed when prefill_len == 0). Must come exactly once
+ * per layer, before its first decode step (else RAAS_E_STATE). Errors:
+ * RAAS_E_INVALID, RAAS_E_STATE, RAAS_E_BUDGET, RAAS_E_HIP. */
+raas_status raas_prefill(raas_pool* pool, int32_t layer, const void* k, const void* v,
+                         int32_t prefill_len, void* stream);
+
+/* One decode step of one layer for every unit (steps 1-5 above). q
+ * [batch][n_q_heads][head_dim]; k_new, v_new [batch][n_kv_heads][head_dim];
+ * out [batch][n_q_heads][head_dim] receives the attention output, rounded
+ * to the pool dtype (nearest-even). Optional outputs (NULL = not written),
+ * per unit u = seq * n_kv_heads + kv_head and slot s, after the step:
+ *   page_table_out [u][S]: logical page id held by the slot (prefill pages
+ *                          0.. in prefill order, then decode pages), or -1;
+ *   timestamps_out [u][S]: timestamp of an evictable page, -1 otherwise;
+ *   evicted_out    [u]   : logical page id evicted by this step, or -1.
+ * Errors: RAAS_E_INVALID, RAAS_E_STATE (layer not prefilled), RAAS_E_HIP. */
+raas_status raas_decode_step(raas_pool* pool, int32_t layer, const void* q, const void* k_new,
+                             const void* v_new, void* out, int32_t* page_table_out,
+                             int32_t* timestamps_out, int32_t* evicted_out, void* stream);
+
+/* Synchronises the pool's last stream, frees all device memory and the
+ * pool. NULL is ignored. */
+void raas_destroy(raas_pool* pool);
+
+/* Message of the last error on this thread ("" if none). */
+const char* raas_last_error(void);
+
+/* RAAS_ABI_VERSION of the library. */
+int32_t raas_abi_version(void);
+
+/* Device bytes the pool holds; fixed from creation on. */
+size_t raas_pool_bytes(const raas_pool* pool);
+
+/* Copies one layer's retention state to host memory (synchronises
+ * `stream`). host_buf holds n_ints int32 = units * (4*S + 4), in order:
+ * lid [units][S], ts [units][S], state [units][S] (0 free, 1 pinned,
+ * 2 evictable), fill [units][S], then per unit {tail slot or -1,
+ * next logical page id, clock, last evicted id or -1}. Errors:
+ * RAAS_E_INVALID (wrong n_ints), RAAS_E_HIP. */
+raas_status raas_export_state(raas_pool* pool, int32_t layer, int32_t* host_buf, size_t n_ints,
+                              void* stream);
+
+/* Tuning: number of slices each unit's pages are split into for the
+ * attention step (split-K). 0 restores the automatic choice. Results do not
+ * depend on it beyond floating-point rounding. Errors: RAAS_E_INVALID. */
+raas_status raas_set_attention_splits(raas_pool* pool, int32_t splits);
+
+/* Kernel timing with HIP events recorded on the call's stream around each
+ * enabled kernel of raas_decode_step. mask bit i enables kernel i:
+ * 0 append, 1 attention, 2 split merge, 3 score/threshold/evict. mask 0
+ * turns timing off. raas_profile_read returns, for kernel i, the summed
+ * duration in ms and the number of timed launches since the last read
+ * (synchronising on the recorded events), then resets them. Errors:
+ * RAAS_E_INVALID, RAAS_E_HIP. */
+raas_status raas_profile(raas_pool* pool, int32_t mask);
+raas_status raas_profile_read(raas_pool* pool, int32_t kernel, double* total_ms, int64_t* launches);
+
+#ifdef __cplusplus
+}
+#endif
+
+#endif /* RAAS_H */

@@ -1,0 +1,397 @@
+// Host runtime of the page-based RaaS decode path: argument validation, the
+// fixed HBM page pool, and the per-step launch sequence on the caller's
+// stream. Implements include/raas.h.
+#include <math.h>
+#include <stdarg.h>
+#include <stdio.h>
+#include <string.h>
+
+#include <new>
+#include <string>
+#include <vector>
+
+#include "raas.h"
+#include "raas_internal.h"
+
+using namespace raas;
+
+namespace {
+
+thread_local std::string g_last_error;
+
+raas_status fail(raas_status st, const char* fmt, ...) __attribute__((format(printf, 2, 3)));
+raas_status fail(raas_status st, const char* fmt, ...) {
+    char buf[512];
+    va_list ap;
+    va_start(ap, fmt);
+    vsnprintf(buf, sizeof buf, fmt, ap);
+    va_end(ap);
+    g_last_error = buf;
+    return st;
+}
+
+raas_status hip_fail(hipError_t e, const char* what) {
+    return fail(RAAS_E_HIP, "%s: %s", what, hipGetErrorString(e));
+}
+
+constexpr int kKernels = 4;  // append, attention, merge, score
+constexpr size_t kProfRing = 8192;
+
+struct Timing {
+    std::vector<hipEvent_t> start, stop;  // ring of recorded pairs
+    size_t head = 0, count = 0;           // pairs recorded since the last read
+    double folded_ms = 0.0;               // time of pairs recycled before the read
+    int64_t folded_n = 0;
+};
+
+}  // namespace
+
+struct raas_pool {
+    raas_config cfg;
+    int U, G, D, ps, S, Lcap, esz;
+    size_t kv_layer_elems, meta_layer_elems, rep_layer_elems;
+    void* K = nullptr;
+    void* V = nullptr;
+    void* kmin = nullptr;
+    void* kmax = nullptr;
+    int32_t* meta = nullptr;  // lid, ts, state, fill: 4 x [Ly][U][S]
+    int32_t* unit = nullptr;  // [Ly][U][4]
+    int32_t* err = nullptr;
+    float* part = nullptr;
+    size_t bytes = 0;
+    std::vector<unsigned char> prefilled;
+    int split_override = 0;
+    hipStream_t last_stream = nullptr;
+    int prof_mask = 0;
+    Timing timing[kKernels];
+};
+
+namespace {
+
+LayerView view(const raas_pool* p, int layer) {
+    LayerView L;
+    const size_t kv = (size_t)layer * p->kv_layer_elems * p->esz;
+    const size_t rep = (size_t)layer * p->rep_layer_elems * p->esz;
+    const size_t meta = (size_t)layer * p->meta_layer_elems;
+    const size_t all_meta = (size_t)p->cfg.n_layers * p->meta_layer_elems;
+    L.K = (char*)p->K + kv;
+    L.V = (char*)p->V + kv;
+    L.kmin = (char*)p->kmin + rep;
+    L.kmax = (char*)p->kmax + rep;
+    L.lid = p->meta + meta;
+    L.ts = p->meta + all_meta + meta;
+    L.state = p->meta + 2 * all_meta + meta;
+    L.fill = p->meta + 3 * all_meta + meta;
+    L.unit = p->unit + (size_t)layer * p->U * 4;
+    L.err = p->err;
+    L.U = p->U;
+    L.G = p->G;
+    L.D = p->D;
+    L.ps = p->ps;
+    L.S = p->S;
+    L.Lcap = p->Lcap;
+    L.bf16 = p->cfg.dtype == RAAS_BF16;
+    return L;
+}
+
+raas_status validate(const raas_config* c) {
+    if (!c) return fail(RAAS_E_INVALID, "cfg is NULL");
+    if (c->batch < 1) return fail(RAAS_E_INVALID, "batch must be >= 1 (got %d)", c->batch);
+    if (c->n_layers < 1) return fail(RAAS_E_INVALID, "n_layers must be >= 1 (got %d)", c->n_layers);
+    if (c->n_kv_heads < 1) return fail(RAAS_E_INVALID, "n_kv_heads must be >= 1 (got %d)", c->n_kv_heads);
+    if (c->n_q_heads < 1 || c->n_q_heads % c->n_kv_heads != 0)
+        return fail(RAAS_E_INVALID, "n_q_heads (%d) must be a positive multiple of n_kv_heads (%d)",
+                    c->n_q_heads, c->n_kv_heads);
+    if (c->n_q_heads / c->n_kv_heads > 16)
+        return fail(RAAS_E_INVALID, "query group n_q_heads/n_kv_heads = %d exceeds 16",
+                    c->n_q_heads / c->n_kv_heads);
+    if (c->head_dim != 64 && c->head_dim != 128)
+        return fail(RAAS_E_INVALID, "head_dim must be 64 or 128 (got %d)", c->head_dim);
+    const int ps = c->page_size;
+    if (ps != 8 && ps != 16 && ps != 32 && ps != 64 && ps != 128)
+        return fail(RAAS_E_INVALID, "page_size must be 8, 16, 32, 64 or 128 (got %d)", ps);
+    if (c->budget_tokens < 1 || c->budget_tokens % ps != 0)
+        return fail(RAAS_E_INVALID, "budget_tokens (%d) must be a positive multiple of page_size (%d)",
+                    c->budget_tokens, ps);
+    const int S = c->budget_tokens / ps;
+    if (S < 2 || S > 2048)
+        return fail(RAAS_E_INVALID, "budget_tokens / page_size = %d pages must lie in [2, 2048]", S);
+    if (c->dtype != RAAS_F32 && c->dtype != RAAS_BF16)
+        return fail(RAAS_E_INVALID, "dtype must be RAAS_F32 or RAAS_BF16 (got %d)", c->dtype);
+    if (!(c->r >= 0.0f && c->r <= 1.0f)) return fail(RAAS_E_INVALID, "r must lie in [0, 1]");
+    if (c->prefill_policy != RAAS_PREFILL_PIN_HEAD && c->prefill_policy != RAAS_PREFILL_ERROR)
+        return fail(RAAS_E_INVALID, "unknown prefill_policy %d", c->prefill_policy);
+    const double units = (double)c->batch * c->n_kv_heads;
+    if (units > 1e7) return fail(RAAS_E_INVALID, "batch * n_kv_heads too large");
+    return RAAS_OK;
+}
+
+raas_status check_layer(const raas_pool* p, int32_t layer) {
+    if (!p) return fail(RAAS_E_INVALID, "pool is NULL");
+    if (layer < 0 || layer >= p->cfg.n_layers)
+        return fail(RAAS_E_INVALID, "layer %d out of range [0, %d)", layer, p->cfg.n_layers);
+    return RAAS_OK;
+}
+
+void split_plan(const raas_pool* p, int& nsplit, int& bps) {
+    const int nblk = p->Lcap / kBlockTokens;
+    int want;
+    if (p->split_override > 0) {
+        want = p->split_override;
+    } else if (p->cfg.dtype == RAAS_F32) {
+        want = (nblk + 1) / 2;  // about 64 tokens per wavefront
+    } else {
+        // aim at ~8 wavefronts per CU over 256 CUs, kAttnWaves per workgroup
+        const double target_waves = 2048.0;
+        const double per_wave = fmax(1.0, (double)p->U * nblk / target_waves);
+        want = (int)ceil(nblk / (kAttnWaves * per_wave));
+    }
+    want = want < 1 ? 1 : want;
+    want = want > kMaxSplits ? kMaxSplits : want;
+    want = want > nblk ? nblk : want;
+    bps = (nblk + want - 1) / want;
+    nsplit = (nblk + bps - 1) / bps;  // no empty split
+}
+
+void prof_record(raas_pool* p, int k, bool start, hipStream_t s) {
+    if (!(p->prof_mask & (1 << k))) return;
+    Timing& t = p->timing[k];
+    if (t.start.empty()) {
+        t.start.resize(kProfRing);
+        t.stop.resize(kProfRing);
+        for (size_t i = 0; i < kProfRing; ++i) {
+            hipEventCreate(&t.start[i]);
+            hipEventCreate(&t.stop[i]);
+        }
+    }
+    const size_t slot = (t.head + t.count) % kProfRing;
+    if (start) {
+        if (t.count == kProfRing) {  // recycle the oldest pair
+            float ms = 0.f;
+            hipEventSynchronize(t.stop[t.head]);
+            hipEventElapsedTime(&ms, t.start[t.head], t.stop[t.head]);
+            t.folded_ms += ms;
+            t.folded_n += 1;
+            t.head = (t.head + 1) % kProfRing;
+            t.count -= 1;
+        }
+        hipEventRecord(t.start[(t.head + t.count) % kProfRing], s);
+    } else {
+        hipEventRecord(t.stop[slot], s);
+        t.count += 1;
+    }
+}
+
+}  // namespace
+
+extern "C" {
+
+const char* raas_last_error(void) { return g_last_error.c_str(); }
+
+int32_t raas_abi_version(void) { return RAAS_ABI_VERSION; }
+
+size_t raas_pool_bytes(const raas_pool* p) { return p ? p->bytes : 0; }
+
+raas_status raas_create_pool(const raas_config* cfg, void* stream, raas_pool** out) {
+    if (!out) return fail(RAAS_E_INVALID, "out is NULL");
+    raas_status st = validate(cfg);
+    if (st != RAAS_OK) return st;
+    raas_pool* p = new (std::nothrow) raas_pool();
+    if (!p) return fail(RAAS_E_OOM, "host allocation failed");
+    p->cfg = *cfg;
+    p->U = cfg->batch * cfg->n_kv_heads;
+    p->G = cfg->n_q_heads / cfg->n_kv_heads;
+    p->D = cfg->head_dim;
+    p->ps = cfg->page_size;
+    p->S = cfg->budget_tokens / cfg->page_size;
+    p->Lcap = (p->S * p->ps + kBlockTokens - 1) / kBlockTokens * kBlockTokens;
+    p->esz = cfg->dtype == RAAS_BF16 ? 2 : 4;
+    p->kv_layer_elems = (size_t)p->U * p->Lcap * p->D;
+    p->rep_layer_elems = (size_t)p->U * p->S * p->D;
+    p->meta_layer_elems = (size_t)p->U * p->S;
+    p->prefilled.assign((size_t)cfg->n_layers, 0);
+    const size_t Ly = (size_t)cfg->n_layers;
+    const int nblk = p->Lcap / kBlockTokens;
+    const int max_split = nblk < kMaxSplits ? nblk : kMaxSplits;
+    struct Req {
+        void** ptr;
+        size_t bytes;
+    } reqs[] = {
+        {&p->K, Ly * p->kv_layer_elems * p->esz},
+        {&p->V, Ly * p->kv_layer_elems * p->esz},
+        {&p->kmin, Ly * p->rep_layer_elems * p->esz},
+        {&p->kmax, Ly * p->rep_layer_elems * p->esz},
+        {(void**)&p->meta, 4 * Ly * p->meta_layer_elems * sizeof(int32_t)},
+        {(void**)&p->unit, Ly * p->U * 4 * sizeof(int32_t)},
+        {(void**)&p->err, 256},
+        {(void**)&p->part, (size_t)p->U * max_split * p->G * (p->D + 2) * sizeof(float)},
+    };
+    hipStream_t s = (hipStream_t)stream;
+    for (auto& r : reqs) {
+        hipError_t e = hipMalloc(r.ptr, r.bytes);
+        if (e != hipSuccess) {
+            (void)hipGetLastError();
+            raas_destroy(p);
+            return fail(e == hipErrorOutOfMemory ? RAAS_E_OOM : RAAS_E_HIP, "hipMalloc(%zu bytes): %s",
+                        r.bytes, hipGetErrorString(e));
+        }
+        p->bytes += r.bytes;
+        e = hipMemsetAsync(*r.ptr, 0, r.bytes, s);
+        if (e != hipSuccess) {
+            raas_destroy(p);
+            return hip_fail(e, "hipMemsetAsync");
+        }
+    }
+    // every slot starts free: lid = ts = -1, state = free (0), fill = 0
+    hipError_t e = hipMemsetAsync(p->meta, 0xFF, 2 * Ly * p->meta_layer_elems * sizeof(int32_t), s);
+    if (e != hipSuccess) {
+        raas_destroy(p);
+        return hip_fail(e, "hipMemsetAsync");
+    }
+    p->last_stream = s;
+    *out = p;
+    return RAAS_OK;
+}
+
+void raas_destroy(raas_pool* p) {
+    if (!p) return;
+    if (p->K || p->meta) hipStreamSynchronize(p->last_stream);
+    for (auto& t : p->timing) {
+        for (auto ev : t.start) hipEventDestroy(ev);
+        for (auto ev : t.stop) hipEventDestroy(ev);
+    }
+    void* ptrs[] = {p->K, p->V, p->kmin, p->kmax, p->meta, p->unit, p->err, p->part};
+    for (void* q : ptrs)
+        if (q) hipFree(q);
+    delete p;
+}
+
+raas_status raas_prefill(raas_pool* p, int32_t layer, const void* k, const void* v,
+                         int32_t prefill_len, void* stream) {
+    raas_status st = check_layer(p, layer);
+    if (st != RAAS_OK) return st;
+    if (prefill_len < 0) return fail(RAAS_E_INVALID, "prefill_len must be >= 0 (got %d)", prefill_len);
+    if (prefill_len > 0 && (!k || !v)) return fail(RAAS_E_INVALID, "k or v is NULL");
+    if (p->prefilled[layer]) return fail(RAAS_E_STATE, "layer %d was already prefilled", layer);
+    const int pages = (prefill_len + p->ps - 1) / p->ps;
+    int keep = pages;
+    if (keep > p->S - 1) {
+        if (p->cfg.prefill_policy == RAAS_PREFILL_ERROR)
+            return fail(RAAS_E_BUDGET, "prefill needs %d pages but the budget leaves %d (S-1)", pages,
+                        p->S - 1);
+        keep = p->S - 1;
+    }
+    hipStream_t s = (hipStream_t)stream;
+    hipError_t e = launch_prefill(view(p, layer), k, v, prefill_len, keep, s);
+    if (e != hipSuccess) return hip_fail(e, "prefill launch");
+    p->prefilled[layer] = 1;
+    p->last_stream = s;
+    return RAAS_OK;
+}
+
+raas_status raas_decode_step(raas_pool* p, int32_t layer, const void* q, const void* k_new,
+                             const void* v_new, void* out, int32_t* page_table_out,
+                             int32_t* timestamps_out, int32_t* evicted_out, void* stream) {
+    raas_status st = check_layer(p, layer);
+    if (st != RAAS_OK) return st;
+    if (!q || !k_new || !v_new || !out) return fail(RAAS_E_INVALID, "q, k_new, v_new and out must be non-NULL");
+    if (!p->prefilled[layer]) return fail(RAAS_E_STATE, "layer %d has not been prefilled", layer);
+    const LayerView L = view(p, layer);
+    StepIO io{q, k_new, v_new, out, page_table_out, timestamps_out, evicted_out};
+    hipStream_t s = (hipStream_t)stream;
+    int nsplit, bps;
+    split_plan(p, nsplit, bps);
+
+    prof_record(p, 0, true, s);
+    hipError_t e = launch_append(L, io, s);
+    prof_record(p, 0, false, s);
+    if (e != hipSuccess) return hip_fail(e, "append launch");
+
+    prof_record(p, 1, true, s);
+    e = launch_attention(L, io, nsplit, bps, p->part, s);
+    prof_record(p, 1, false, s);
+    if (e != hipSuccess) return hip_fail(e, "attention launch");
+
+    if (nsplit > 1) {
+        prof_record(p, 2, true, s);
+        e = launch_merge(L, io, nsplit, p->part, s);
+        prof_record(p, 2, false, s);
+        if (e != hipSuccess) return hip_fail(e, "merge launch");
+    }
+
+    prof_record(p, 3, true, s);
+    e = launch_score(L, io, (double)p->cfg.r, s);
+    prof_record(p, 3, false, s);
+    if (e != hipSuccess) return hip_fail(e, "score launch");
+    p->last_stream = s;
+    return RAAS_OK;
+}
+
+raas_status raas_export_state(raas_pool* p, int32_t layer, int32_t* host_buf, size_t n_ints,
+                              void* stream) {
+    raas_status st = check_layer(p, layer);
+    if (st != RAAS_OK) return st;
+    const size_t need = (size_t)p->U * (4 * (size_t)p->S + 4);
+    if (!host_buf || n_ints != need)
+        return fail(RAAS_E_INVALID, "host_buf must hold %zu int32 (got %zu)", need, n_ints);
+    const LayerView L = view(p, layer);
+    hipStream_t s = (hipStream_t)stream;
+    const size_t us = (size_t)p->U * p->S;
+    int32_t* src[4] = {L.lid, L.ts, L.state, L.fill};
+    for (int i = 0; i < 4; ++i) {
+        hipError_t e = hipMemcpyAsync(host_buf + i * us, src[i], us * sizeof(int32_t), hipMemcpyDeviceToHost, s);
+        if (e != hipSuccess) return hip_fail(e, "hipMemcpyAsync");
+    }
+    hipError_t e = hipMemcpyAsync(host_buf + 4 * us, L.unit, (size_t)p->U * 4 * sizeof(int32_t),
+                                  hipMemcpyDeviceToHost, s);
+    if (e != hipSuccess) return hip_fail(e, "hipMemcpyAsync");
+    int32_t errflag = 0;
+    e = hipMemcpyAsync(&errflag, p->err, sizeof(int32_t), hipMemcpyDeviceToHost, s);
+    if (e != hipSuccess) return hip_fail(e, "hipMemcpyAsync");
+    e = hipStreamSynchronize(s);
+    if (e != hipSuccess) return hip_fail(e, "hipStreamSynchronize");
+    if (errflag) return fail(RAAS_E_HIP, "device reported an internal inconsistency (flag %d)", errflag);
+    return RAAS_OK;
+}
+
+raas_status raas_set_attention_splits(raas_pool* p, int32_t splits) {
+    if (!p) return fail(RAAS_E_INVALID, "pool is NULL");
+    if (splits < 0 || splits > kMaxSplits) return fail(RAAS_E_INVALID, "splits must lie in [0, %d]", kMaxSplits);
+    p->split_override = splits;
+    return RAAS_OK;
+}
+
+raas_status raas_profile(raas_pool* p, int32_t mask) {
+    if (!p) return fail(RAAS_E_INVALID, "pool is NULL");
+    if (mask < 0 || mask >= (1 << kKernels)) return fail(RAAS_E_INVALID, "bad kernel mask %d", mask);
+    p->prof_mask = mask;
+    return RAAS_OK;
+}
+
+raas_status raas_profile_read(raas_pool* p, int32_t kernel, double* total_ms, int64_t* launches) {
+    if (!p) return fail(RAAS_E_INVALID, "pool is NULL");
+    if (kernel < 0 || kernel >= kKernels || !total_ms || !launches)
+        return fail(RAAS_E_INVALID, "bad kernel index or NULL output");
+    Timing& t = p->timing[kernel];
+    double ms_sum = t.folded_ms;
+    int64_t n = t.folded_n;
+    for (size_t i = 0; i < t.count; ++i) {
+        const size_t j = (t.head + i) % kProfRing;
+        hipError_t e = hipEventSynchronize(t.stop[j]);
+        if (e != hipSuccess) return hip_fail(e, "hipEventSynchronize");
+        float ms = 0.f;
+        e = hipEventElapsedTime(&ms, t.start[j], t.stop[j]);
+        if (e != hipSuccess) return hip_fail(e, "hipEventElapsedTime");
+        ms_sum += ms;
+        n += 1;
+    }
+    t.head = 0;
+    t.count = 0;
+    t.folded_ms = 0.0;
+    t.folded_n = 0;
+    *total_ms = ms_sum;
+    *launches = n;
+    return RAAS_OK;
+}
+
+}  // extern "C"

@@ -1,0 +1,185 @@
+"""Lockstep parity harness: the HIP decode path against the CPU oracle.
+
+Both sides get the same seeded inputs (``synth``); the oracle runs free on
+the units it checks and never sees anything the GPU produced. Per step and
+checked unit:
+  - page table, timestamps and evicted page must be bit-exact, except when
+    the oracle flags the step's threshold as a near-tie (two or more
+    evictable pages within NEAR_TIE of the threshold score); a mismatch
+    confined to flagged pages is counted and ends the comparison of that
+    unit, any other mismatch fails;
+  - attention outputs must agree within the tolerance of the dtype.
+"""
+from __future__ import annotations
+
+import dataclasses
+import math
+
+import numpy as np
+
+import oracle
+import synth
+
+NEAR_TIE = 1e-6
+TOL = {"bf16": 2e-2, "f32": 1e-4}
+
+
+@dataclasses.dataclass
+class ParityReport:
+    steps: int = 0
+    units_checked: int = 0
+    outputs_compared: int = 0
+    max_abs_err: float = 0.0
+    flagged_steps: int = 0
+    flagged_divergences: int = 0
+    evictions: int = 0
+    notes: list = dataclasses.field(default_factory=list)
+
+
+def to_device(a: np.ndarray, dtype: str):
+    import torch
+
+    t = torch.from_numpy(np.ascontiguousarray(a))
+    t = t.to(torch.bfloat16) if dtype == "bf16" else t.to(torch.float32)
+    return t.cuda()
+
+
+def new_pool(w, splits=None, policy=None):
+    import paper_2502_11147_amd as raas
+
+    kw = {}
+    if policy is not None:
+        kw["prefill_policy"] = policy
+    pool = raas.Pool.for_workload(w, **kw)
+    if splits is not None:
+        pool.set_attention_splits(splits)
+    return pool
+
+
+def unit_index(w, seq, kvh):
+    return seq * w.n_kv_heads + kvh
+
+
+def run_parity(w, seed: int, steps: int, layer: int = 0, units=None, out_every: int = 1,
+               splits=None, chunk: int = 64, pool=None, prefill_len=None, check_invariants=True,
+               report: ParityReport | None = None) -> ParityReport:
+    """Runs `steps` decode steps of workload `w` on the GPU and checks the
+    listed units (all when None) against the oracle."""
+    import torch
+
+    rep = report or ParityReport()
+    B, Hq, Hkv, d, G, S, ps = (w.batch, w.n_q_heads, w.n_kv_heads, w.head_dim, w.group, w.slots,
+                               w.page_size)
+    U = B * Hkv
+    P = w.prefill_len if prefill_len is None else prefill_len
+    units = list(range(U)) if units is None else list(units)
+    tol = TOL[w.dtype]
+    own_pool = pool is None
+    if own_pool:
+        pool = new_pool(w, splits)
+    Kp, Vp = synth.prefill(w, seed, layer, prefill_len=P)
+    pool.prefill(layer, to_device(Kp, w.dtype) if P else None, to_device(Vp, w.dtype) if P else None)
+    orc = {}
+    for u in units:
+        b, h = divmod(u, Hkv)
+        m = oracle.Kvm(G, d, ps, S, r=w.r)
+        rc = m.prefill(Kp[b, h].astype(np.float64), Vp[b, h].astype(np.float64))
+        assert rc == 0, rc
+        orc[u] = m
+    live = set(units)
+    rep.units_checked += len(units)
+    dt = torch.bfloat16 if w.dtype == "bf16" else torch.float32
+    for t0 in range(0, steps, chunk):
+        n = min(chunk, steps - t0)
+        q, k, v = synth.steps(w, seed, layer, t0, n)
+        qd, kd, vd = to_device(q, w.dtype), to_device(k, w.dtype), to_device(v, w.dtype)
+        out = torch.empty((n, B, Hq, d), dtype=dt, device="cuda")
+        pt = torch.empty((n, B, Hkv, S), dtype=torch.int32, device="cuda")
+        ts = torch.empty((n, B, Hkv, S), dtype=torch.int32, device="cuda")
+        ev = torch.empty((n, B, Hkv), dtype=torch.int32, device="cuda")
+        for i in range(n):
+            pool.decode_step(layer, qd[i], kd[i], vd[i], out[i], pt[i], ts[i], ev[i])
+        torch.cuda.synchronize()
+        out_h = out.float().cpu().numpy().reshape(n, U, G, d)
+        pt_h = pt.cpu().numpy().reshape(n, U, S)
+        ts_h = ts.cpu().numpy().reshape(n, U, S)
+        ev_h = ev.cpu().numpy().reshape(n, U)
+        q64 = q.reshape(n, U, G, d)
+        k64 = k.reshape(n, U, d)
+        v64 = v.reshape(n, U, d)
+        for i in range(n):
+            t = t0 + i
+            clock = P + t
+            want_out = (t % out_every == 0) or t == steps - 1
+            rep.evictions += int(np.sum(ev_h[i] >= 0))
+            if check_invariants:
+                _check_invariants(pt_h[i], ts_h[i], ev_h[i], clock, P, ps, S)
+            for u in sorted(live):
+                m = orc[u]
+                o = m.decode(q64[i, u], k64[i, u], v64[i, u], want_out=want_out)
+                st = m.state()
+                scores, theta = m.last_scores()
+                flagged = _flagged_pages(scores, theta)
+                if len(flagged) >= 2:
+                    rep.flagged_steps += 1
+                same_pt = np.array_equal(st["page_table"], pt_h[i, u])
+                same_ts = np.array_equal(st["ts"], ts_h[i, u])
+                same_ev = st["evicted"] == ev_h[i, u]
+                if not (same_pt and same_ts and same_ev):
+                    bad = set(np.nonzero(st["ts"] != ts_h[i, u])[0]) | set(
+                        np.nonzero(st["page_table"] != pt_h[i, u])[0])
+                    if len(flagged) >= 2 and bad <= flagged | _victims(st, pt_h[i, u]):
+                        rep.flagged_divergences += 1
+                        rep.notes.append("unit %d step %d: flagged near-tie divergence" % (u, t))
+                        live.discard(u)
+                        continue
+                    raise AssertionError(
+                        "retention mismatch: workload %s seed %d layer %d unit %d step %d\n"
+                        "oracle pt %s\n   gpu pt %s\noracle ts %s\n   gpu ts %s\noracle ev %d gpu ev %d"
+                        % (w.name, seed, layer, u, t, st["page_table"].tolist(), pt_h[i, u].tolist(),
+                           st["ts"].tolist(), ts_h[i, u].tolist(), st["evicted"], ev_h[i, u]))
+                if want_out:
+                    err = float(np.max(np.abs(out_h[i, u].astype(np.float64) - o)))
+                    rep.max_abs_err = max(rep.max_abs_err, err)
+                    rep.outputs_compared += 1
+                    if not (err <= tol):
+                        raise AssertionError("output mismatch: workload %s seed %d layer %d unit %d step %d: "
+                                             "max abs err %.3g > %g" % (w.name, seed, layer, u, t, err, tol))
+        rep.steps = t0 + n
+    if own_pool:
+        pool.close()
+    return rep
+
+
+def _flagged_pages(scores, theta):
+    if theta is None or not math.isfinite(theta):
+        return set()
+    ok = ~np.isnan(scores)
+    return set(int(s) for s in np.nonzero(ok & (np.abs(np.where(ok, scores, 0.0) - theta) <= NEAR_TIE))[0])
+
+
+def _victims(st, gpu_pt):
+    """slots whose page differs only because the two sides evicted different pages"""
+    return set(int(s) for s in np.nonzero((st["page_table"] == -1) | (gpu_pt == -1))[0])
+
+
+def _check_invariants(pt, ts, ev, clock, P, ps, S):
+    """Properties that hold for every unit at any size (Algorithm 1, Sections 3.1-3.3)."""
+    pinned = min(-(-P // ps), S - 1)
+    # prefill pages stay in slots 0..pinned-1 with their own ids and no timestamp
+    assert np.all(pt[:, :pinned] == np.arange(pinned)[None, :]), "pinned pages moved"
+    assert np.all(ts[:, :pinned] == -1)
+    # decode pages carry ids above the prefill's and timestamps no later than now
+    dec = pt[:, pinned:]
+    dts = ts[:, pinned:]
+    assert np.all((dec == -1) | (dec >= -(-P // ps)))
+    assert np.all((dec == -1) == (dts == -1))
+    assert np.all(dts <= clock) and np.all((dts == -1) | (dts >= P))
+    # logical ids are unique within a unit
+    for row in pt:
+        live = row[row >= 0]
+        assert len(np.unique(live)) == len(live), "duplicate page id"
+    # an eviction leaves exactly one free slot behind
+    assert np.all((ev == -1) | (ev >= -(-P // ps)))
+    nfree = np.sum(pt == -1, axis=1)
+    assert np.all(nfree[ev >= 0] >= 1)

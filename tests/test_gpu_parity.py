@@ -1,0 +1,277 @@
+"""GPU parity: the HIP decode path against the CPU oracle, through the C ABI.
+
+Small cases compare every unit at every step; the full-size workloads run
+in the launch configuration the benchmark uses and compare sampled units,
+plus properties every unit must satisfy.
+"""
+from __future__ import annotations
+
+import sys
+
+import numpy as np
+import pytest
+
+import synth
+from harness import ParityReport, new_pool, run_parity, to_device
+
+pytestmark = pytest.mark.gpu
+
+
+def _say(msg):
+    print(msg, flush=True)
+    sys.stdout.flush()
+
+
+@pytest.fixture(scope="module", autouse=True)
+def _gpu():
+    torch = pytest.importorskip("torch")
+    if not torch.cuda.is_available():
+        pytest.skip("no GPU")
+    import paper_2502_11147_amd as raas
+
+    raas.load_library()  # fails loudly when the HIP library is missing
+
+
+def small(**kw):
+    base = dict(name="small", batch=2, n_layers=1, n_q_heads=8, n_kv_heads=2, head_dim=128, dtype="bf16",
+                page_size=16, budget=128, prefill_len=40, decode_steps=300, ms_period=16,
+                ms_phase_random=True, ms_wmin=8, ms_wmax=64)
+    base.update(kw)
+    return synth.Workload(**base)
+
+
+def _report(rep: ParityReport, tag):
+    _say("%s: steps %d units %d outputs %d max_abs_err %.3g evictions %d flagged %d/%d"
+          % (tag, rep.steps, rep.units_checked, rep.outputs_compared, rep.max_abs_err, rep.evictions,
+             rep.flagged_steps, rep.flagged_divergences))
+    assert rep.flagged_divergences == 0 or rep.flagged_divergences <= rep.flagged_steps
+
+
+def test_tiny_f32_full_run():
+    """The tiny fp32 workload end to end: every step, every output."""
+    w = synth.get_workload("tiny-f32")
+    _say("case tiny-f32 seed 0 steps %d" % w.decode_steps)
+    rep = run_parity(w, seed=0, steps=w.decode_steps)
+    _report(rep, "tiny-f32")
+    assert rep.evictions > 0
+
+
+@pytest.mark.parametrize("seed", [0, 1])
+def test_small_bf16_every_step(seed):
+    w = small()
+    _say("case small-bf16 seed %d" % seed)
+    rep = run_parity(w, seed=seed, steps=w.decode_steps)
+    _report(rep, "small-bf16")
+    assert rep.evictions > 0
+
+
+@pytest.mark.parametrize("splits", [1, 2, 3, 5, 64])
+def test_split_counts_agree(splits):
+    """Split-K over pages changes only rounding, never retention."""
+    w = small(budget=512, prefill_len=100, decode_steps=520)
+    _say("case split-sweep splits %d" % splits)
+    rep = run_parity(w, seed=3, steps=w.decode_steps, splits=splits)
+    _report(rep, "splits=%d" % splits)
+
+
+EDGE = [
+    dict(prefill_len=0),
+    dict(prefill_len=16 * 7),                     # exactly S-1 pages pinned, one decode slot
+    dict(prefill_len=1000),                       # overflow: first S-1 pages pinned (PIN_HEAD)
+    dict(prefill_len=3),                          # one partial pinned page
+    dict(page_size=8, budget=64),
+    dict(page_size=32, budget=256),
+    dict(page_size=64, budget=448, prefill_len=70),
+    dict(page_size=128, budget=512, prefill_len=130),
+    dict(budget=80),                              # 5 pages: 80 tokens, not a multiple of 32
+    dict(n_q_heads=2, n_kv_heads=2),              # G = 1
+    dict(n_q_heads=28, n_kv_heads=4),             # G = 7
+    dict(n_q_heads=32, n_kv_heads=2),             # G = 16
+    dict(head_dim=64),
+    dict(r=0.0), dict(r=1.0), dict(r=0.25), dict(r=0.75),
+    dict(dtype="f32", head_dim=128),
+    dict(dtype="f32", n_q_heads=14, n_kv_heads=2, head_dim=64, page_size=8, budget=96),
+]
+
+
+@pytest.mark.parametrize("edge", EDGE, ids=[",".join("%s=%s" % kv for kv in e.items()) for e in EDGE])
+def test_edge_cases(edge):
+    w = small(decode_steps=200, **edge)
+    _say("case edge %s" % edge)
+    rep = run_parity(w, seed=5, steps=w.decode_steps)
+    _report(rep, "edge")
+
+
+def test_multi_layer_independent():
+    """Layers have their own pages and clocks; stepping one leaves the others."""
+    import torch
+
+    w = small(n_layers=3, decode_steps=150)
+    pool = new_pool(w)
+    _say("case multi-layer layer 2 then 0")
+    rep = run_parity(w, seed=9, steps=120, layer=2, pool=pool)
+    before = pool.export_state(1)
+    assert np.all(before["state"] == 0) and np.all(before["lid"] == -1)
+    rep = run_parity(w, seed=9, steps=w.decode_steps, layer=0, pool=pool, report=rep)
+    st2 = pool.export_state(2)
+    assert np.all(st2["clock"] == w.prefill_len + 120)
+    st0 = pool.export_state(0)
+    assert np.all(st0["clock"] == w.prefill_len + w.decode_steps)
+    pool.close()
+    torch.cuda.synchronize()
+
+
+def test_state_errors_and_budget_policy():
+    import torch
+
+    import paper_2502_11147_amd as raas
+
+    w = small()
+    pool = new_pool(w)
+    d = w.head_dim
+    q = torch.zeros((w.batch, w.n_q_heads, d), dtype=torch.bfloat16, device="cuda")
+    kv = torch.zeros((w.batch, w.n_kv_heads, d), dtype=torch.bfloat16, device="cuda")
+    out = torch.empty_like(q)
+    with pytest.raises(raas.RaasError) as e:
+        pool.decode_step(0, q, kv, kv, out)
+    assert e.value.code == raas.E_STATE
+    K = torch.zeros((w.batch, w.n_kv_heads, 16, d), dtype=torch.bfloat16, device="cuda")
+    pool.prefill(0, K, K)
+    with pytest.raises(raas.RaasError) as e:
+        pool.prefill(0, K, K)
+    assert e.value.code == raas.E_STATE
+    with pytest.raises(raas.RaasError) as e:
+        pool.decode_step(1, q, kv, kv, out)
+    assert e.value.code == raas.E_INVALID
+    pool.decode_step(0, q, kv, kv, out)
+    st = pool.export_state(0)
+    assert np.all(st["clock"] == 17)
+    pool.close()
+    strict = new_pool(w, policy=raas.PREFILL_ERROR)
+    big = torch.zeros((w.batch, w.n_kv_heads, w.budget, d), dtype=torch.bfloat16, device="cuda")
+    with pytest.raises(raas.RaasError) as e:
+        strict.prefill(0, big, big)
+    assert e.value.code == raas.E_BUDGET
+    st = strict.export_state(0)
+    assert np.all(st["state"] == 0)  # the refused call changed nothing
+    strict.close()
+
+
+def test_deterministic():
+    """Same inputs twice: bitwise-identical outputs and state."""
+    import torch
+
+    w = small(decode_steps=260)
+    outs = []
+    for _ in range(2):
+        pool = new_pool(w)
+        K, V = synth.prefill(w, 11, 0)
+        pool.prefill(0, to_device(K, w.dtype), to_device(V, w.dtype))
+        q, k, v = synth.steps(w, 11, 0, 0, w.decode_steps)
+        qd, kd, vd = to_device(q, w.dtype), to_device(k, w.dtype), to_device(v, w.dtype)
+        o = torch.empty((w.decode_steps, w.batch, w.n_q_heads, w.head_dim), dtype=torch.bfloat16,
+                        device="cuda")
+        for i in range(w.decode_steps):
+            pool.decode_step(0, qd[i], kd[i], vd[i], o[i])
+        st = pool.export_state(0)
+        outs.append((o.view(torch.int16).cpu().numpy(), st))
+        pool.close()
+    assert np.array_equal(outs[0][0], outs[1][0])
+    for key in ("lid", "ts", "state", "fill", "clock", "next_lid"):
+        assert np.array_equal(outs[0][1][key], outs[1][1][key])
+
+
+def test_pool_memory_is_fixed():
+    """O(L) memory (Section 4.3): the pool's bytes are set at creation and
+    resident tokens never exceed the budget."""
+    import torch
+
+    w = small(decode_steps=400)
+    pool = new_pool(w)
+    b0 = pool.pool_bytes()
+    K, V = synth.prefill(w, 2, 0)
+    pool.prefill(0, to_device(K, w.dtype), to_device(V, w.dtype))
+    q, k, v = synth.steps(w, 2, 0, 0, w.decode_steps)
+    qd, kd, vd = to_device(q, w.dtype), to_device(k, w.dtype), to_device(v, w.dtype)
+    out = torch.empty((w.batch, w.n_q_heads, w.head_dim), dtype=torch.bfloat16, device="cuda")
+    for i in range(w.decode_steps):
+        pool.decode_step(0, qd[i], kd[i], vd[i], out)
+        if i % 50 == 49:
+            st = pool.export_state(0)
+            resident = np.where(st["state"] != 0, st["fill"], 0).sum(axis=1)
+            assert np.all(resident <= w.budget)
+    assert pool.pool_bytes() == b0
+    pool.close()
+
+
+# ---- full-size workloads, benchmark launch configuration, sampled units ----
+
+def _sample_units(w, n, seed=0):
+    rng = np.random.default_rng(seed)
+    U = w.batch * w.n_kv_heads
+    picks = {0, U - 1}
+    while len(picks) < min(n, U):
+        picks.add(int(rng.integers(0, U)))
+    return sorted(picks)
+
+
+def test_llama8b_b1_full_run():
+    """Batch-1 Llama-3.1-8B layer, L=1024: all 8 units, every step of the
+    full 8192-step run; outputs every 16th step."""
+    w = synth.get_workload("llama8b-b1-L1024")
+    _say("case %s steps %d" % (w.name, w.decode_steps))
+    rep = run_parity(w, seed=0, steps=w.decode_steps, out_every=16, chunk=256)
+    _report(rep, w.name)
+    assert rep.evictions > 0
+
+
+def test_llama8b_b32_serving_shape():
+    """Batch-32 Llama-3.1-8B layer, L=2048 (the benchmark workload): fills the
+    budget after 1024 decode steps, then evicts; 12 sampled units checked
+    step by step, every unit checked against the invariants."""
+    w = synth.get_workload("llama8b-b32-L2048")
+    steps = 1024 + 640
+    _say("case %s steps %d" % (w.name, steps))
+    rep = run_parity(w, seed=0, steps=steps, units=_sample_units(w, 12), out_every=32, chunk=128)
+    _report(rep, w.name)
+    assert rep.evictions > 0
+
+
+def test_qwen7b_28_layer_stack_last_layer():
+    """Qwen2.5-7B-shaped stack (28 layers, 28/4 heads, batch 64, L=4096): the
+    full 28-layer pool, its last layer run past the budget; 8 sampled
+    units."""
+    w = synth.get_workload("qwen7b-28L-b64-L4096")
+    steps = 2048 + 256
+    _say("case %s layer 27 steps %d" % (w.name, steps))
+    pool = new_pool(w)
+    rep = run_parity(w, seed=0, steps=steps, layer=27, units=_sample_units(w, 8), out_every=64,
+                     chunk=128, pool=pool)
+    pool.close()
+    _report(rep, w.name)
+    assert rep.evictions > 0
+
+
+@pytest.mark.parametrize("name,steps", [("llama8b-b128-ps32-L512", 200), ("llama8b-b128-ps32-L2048", 200),
+                                        ("llama8b-b128-ps32-L8192", 160)])
+def test_stress_sweep(name, steps):
+    """Batch 128, page 32, prefill 4096, heavy-tailed keys. At L=512 and
+    2048 the prefill overflows the budget: S-1 pages pinned, each decode
+    page evicted once full."""
+    w = synth.get_workload(name)
+    _say("case %s steps %d" % (name, steps))
+    rep = run_parity(w, seed=0, steps=steps, units=_sample_units(w, 8), out_every=8)
+    _report(rep, name)
+    if w.budget < w.prefill_len:
+        assert rep.evictions > 0
+
+
+def test_stress_dense_equivalence():
+    """L = N (36864 tokens): nothing is ever evicted and the output is dense
+    attention over every token (the oracle is exactly that at L >= N)."""
+    w = synth.get_workload("llama8b-b128-ps32-dense")
+    steps = 96
+    _say("case %s steps %d" % (w.name, steps))
+    rep = run_parity(w, seed=0, steps=steps, units=_sample_units(w, 4), out_every=16)
+    _report(rep, w.name)
+    assert rep.evictions == 0
