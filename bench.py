@@ -31,7 +31,7 @@ if ROOT not in sys.path:
     sys.path.insert(0, ROOT)
 
 HBM_PEAK_GBS = 8000.0  # MI355X HBM3E
-KERNEL_ATTENTION = 1
+KERNEL_STEP, KERNEL_EPILOGUE = 0, 1
 
 
 def parse():
@@ -76,22 +76,16 @@ def resident_schedule(st, ps, S, n):
 
 
 def step_bytes(w, resident, n_ev):
-    """Algorithmic HBM bytes of one whole decode step for all units: K+V of the
-    resident tokens, the representative keys of evictable pages, q read twice
-    (attention and scoring) and out written, the new K/V read and stored,
-    the tail page's representative keys updated, and per-slot state."""
+    """Algorithmic HBM bytes of one whole decode step, all units: K+V of the
+    resident tokens; the representative keys (per-channel min and max) of the
+    evictable pages; q read for the attention and for the scores, out
+    written; the new K and V read once and stored once; the tail page's
+    min/max read and written; per slot, state/timestamp/id/fill read and
+    state/timestamp written (24 B)."""
     e = 2 if w.dtype == "bf16" else 4
-    d, G, S, U = w.head_dim, w.group, w.slots, w.batch * w.n_kv_heads
-    per_unit = (resident * 2 * d * e + n_ev * 2 * d * e + 3 * G * d * e + 4 * d * e + 4 * d * e + 16 * S)
+    d, G, S = w.head_dim, w.group, w.slots
+    per_unit = (resident * 2 * d * e + n_ev * 2 * d * e + 3 * G * d * e + 4 * d * e + 4 * d * e + 24 * S)
     return per_unit.sum(axis=-1)
-
-
-def attention_bytes(w, resident):
-    """Algorithmic bytes of one attention launch: K+V of every resident token,
-    q read, out written."""
-    e = 2 if w.dtype == "bf16" else 4
-    d, G, U = w.head_dim, w.group, w.batch * w.n_kv_heads
-    return resident.sum(axis=-1) * 2 * d * e + 2 * U * G * d * e
 
 
 def cpu_baseline(w, seed, ring_np, budget_s):
@@ -180,28 +174,51 @@ def main():
     run(0, fill)
     run(fill, args.warmup)
     torch.cuda.synchronize()
+
+    # one kernel per step (the step kernel runs the epilogue) or two?
+    pool.profile(1 << KERNEL_EPILOGUE)
+    run(fill + args.warmup, 1)
+    fused = pool.profile_read(KERNEL_EPILOGUE)[1] == 0
+    pool.profile(0)
+    t_start = fill + args.warmup + 1
     st = pool.export_state(0)
     res = resident_schedule(st, w.page_size, S, args.steps)
     n_ev0 = (st["state"] == 2).sum(axis=1)
 
-    pool.profile(1 << KERNEL_ATTENTION)
-    pool.profile_read(KERNEL_ATTENTION)
+    # timed region: HIP events on the launch stream (torch's current stream)
+    # around all K steps; with two kernels per step, the library also times
+    # each kernel on every 16th step
+    ev0, ev1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
     torch.cuda.synchronize()
     t0 = time.perf_counter()
-    run(fill + args.warmup, args.steps)
+    ev0.record()
+    if fused:
+        run(t_start, args.steps)
+    else:
+        for i0 in range(0, args.steps, 16):
+            pool.profile((1 << KERNEL_STEP) | (1 << KERNEL_EPILOGUE))
+            run(t_start + i0, 1)
+            pool.profile(0)
+            run(t_start + i0 + 1, min(16, args.steps - i0) - 1)
+    ev1.record()
     torch.cuda.synchronize()
     elapsed = time.perf_counter() - t0
-    attn_ms, attn_n = pool.profile_read(KERNEL_ATTENTION)
-    pool.profile(0)
+    span_ms = ev0.elapsed_time(ev1)
+    step_ms, step_n = pool.profile_read(KERNEL_STEP)
+    epi_ms, epi_n = pool.profile_read(KERNEL_EPILOGUE)
     st_end = pool.export_state(0)
     pool.close()
 
     ms_per_step = elapsed * 1e3 / args.steps
     tokens_per_s = w.batch * args.steps / elapsed
-    attn_avg_s = attn_ms / 1e3 / max(attn_n, 1)
-    attn_bytes = float(np.mean(attention_bytes(w, res)))
-    achieved = attn_bytes / attn_avg_s / 1e9
+    # step kernel's average duration: the event span over the K launches when
+    # it is the only kernel of the step, else the sampled per-kernel events
+    step_avg_s = span_ms / 1e3 / args.steps if fused else step_ms / 1e3 / max(step_n, 1)
     step_b = float(np.mean(step_bytes(w, res, n_ev0[None, :])))
+    # bytes of the step kernel alone: everything but what the epilogue kernel moves
+    e = 2 if w.dtype == "bf16" else 4
+    kernel_b = step_b if fused else step_b - U * w.group * w.head_dim * e - 24 * U * S
+    achieved = kernel_b / step_avg_s / 1e9
     line = {
         "metric": "decode tokens/s per GPU at batch B, budget L; achieved HBM GB/s vs peak",
         "value": round(tokens_per_s, 1),
@@ -210,6 +227,7 @@ def main():
         "steps": args.steps,
         "warmup": args.warmup,
         "ms_per_step": round(ms_per_step, 5),
+        "ms_per_step_events": round(span_ms / args.steps, 5),
         "higher_is_better": True,
         "scaling": "weak",
         "vs_baseline": None,
@@ -224,19 +242,21 @@ def main():
         },
         "step_hbm_gbs_algorithmic": round(step_b / (elapsed / args.steps) / 1e9, 1),
         "roofline": {
-            "kernel": "k_attn_bf16" if w.dtype == "bf16" else "k_attn_f32",
+            "kernel": ("k_step_bf16" if w.dtype == "bf16" else "k_step_f32") + ("" if fused else " (+k_epilogue)"),
             "bound": "hbm",
             "achieved": round(achieved, 1),
             "peak": HBM_PEAK_GBS,
             "unit": "GB/s",
             "frac": round(achieved / HBM_PEAK_GBS, 4),
             "traffic": None,
-            "bytes_per_launch": attn_bytes,
-            "avg_launch_us": round(attn_avg_s * 1e6, 3),
-            "launches_timed": attn_n,
+            "bytes_per_launch": kernel_b,
+            "avg_launch_us": round(step_avg_s * 1e6, 3),
+            "launches_timed": args.steps if fused else step_n,
+            "timing": "event span over the timed launches" if fused else "per-launch events, every 16th step",
+            "epilogue_kernel_avg_us": round(epi_ms * 1e3 / epi_n, 3) if epi_n else None,
         },
     }
-    assert np.all(st_end["clock"] == w.prefill_len + fill + args.warmup + args.steps)
+    assert np.all(st_end["clock"] == w.prefill_len + t_start + args.steps)
     if not args.no_cpu_baseline:
         line["cpu_baseline"] = cpu_baseline(w, args.seed, ring_np, args.cpu_seconds)
     print(json.dumps(line), flush=True)

@@ -37,7 +37,9 @@
  *  - A call that returns an error has changed no state; raas_last_error()
  *    gives a message (thread-local). RAAS_E_HIP reports a failed HIP call,
  *    possibly of earlier asynchronous work.
- *  - Inputs must be finite. Calls on one pool are not thread-safe.
+ *  - Inputs must be finite. Calls on one pool are not thread-safe and must
+ *    be ordered (one stream, or synchronised between streams): they share
+ *    the pool's state and per-step scratch buffers.
  */
 #ifndef RAAS_H
 #define RAAS_H
@@ -144,11 +146,13 @@ raas_status raas_set_attention_splits(raas_pool* pool, int32_t splits);
 
 /* Kernel timing with HIP events recorded on the call's stream around each
  * enabled kernel of raas_decode_step. mask bit i enables kernel i:
- * 0 append, 1 attention, 2 split merge, 3 score/threshold/evict. mask 0
- * turns timing off. raas_profile_read returns, for kernel i, the summed
- * duration in ms and the number of timed launches since the last read
- * (synchronising on the recorded events), then resets them. Errors:
- * RAAS_E_INVALID, RAAS_E_HIP. */
+ * 0 the step kernel (attention, append, page scores, and the epilogue when a
+ * single workgroup covers a unit), 1 the epilogue kernel (split merge,
+ * refresh, eviction; launched when a unit is split over several
+ * workgroups, and for fp32 pools). mask 0 turns timing off.
+ * raas_profile_read returns, for kernel i, the summed duration in ms and the
+ * number of timed launches since the last read (synchronising on the
+ * recorded events), then resets them. Errors: RAAS_E_INVALID, RAAS_E_HIP. */
 raas_status raas_profile(raas_pool* pool, int32_t mask);
 raas_status raas_profile_read(raas_pool* pool, int32_t kernel, double* total_ms, int64_t* launches);
 

@@ -9,19 +9,26 @@ namespace raas {
 
 enum SlotState : int32_t { kFree = 0, kPinned = 1, kEvictable = 2 };
 
-// Per-unit record: [tail slot or -1, next logical page id, clock, last evicted id]
-enum UnitField : int { kTail = 0, kNextLid = 1, kClock = 2, kEvicted = 3 };
+// Per-unit record, kUnitFields int32 each:
+//  tail      slot of the page receiving decode tokens, or -1
+//  next_lid  logical id the next fresh page gets
+//  clock     absolute position of the next token
+//  evicted   logical id evicted by the last step, or -1
+//  next_slot slot the next token goes to (the tail, or the lowest free slot)
+//  next_fill its position in that page (0: the page is opened by that token)
+enum UnitField : int { kTail = 0, kNextLid = 1, kClock = 2, kEvicted = 3, kNextSlot = 4, kNextFill = 5 };
+constexpr int kUnitFields = 8;
 
 // Tokens of one attention block: two 16-row MFMA tiles.
 constexpr int kBlockTokens = 32;
-// Waves per attention workgroup.
-constexpr int kAttnWaves = 4;
 // Upper bound on attention splits per unit (sizes the partials buffer).
 constexpr int kMaxSplits = 64;
+// LDS a step workgroup may use.
+constexpr size_t kMaxLds = 60 * 1024;
 
 // One layer of the pool, as the kernels see it. Unit u = seq * n_kv_heads + kv_head.
 struct LayerView {
-    void* K;         // [U][Lcap][D] in the block-swizzled (bf16) or plain (fp32) layout
+    void* K;         // [U][Lcap][D] block-swizzled (bf16) or plain (fp32)
     void* V;         // [U][Lcap][D] likewise
     void* kmin;      // [U][S][D] per-page per-channel key minimum, pool dtype
     void* kmax;      // [U][S][D] per-page per-channel key maximum
@@ -29,10 +36,13 @@ struct LayerView {
     int32_t* ts;     // [U][S] timestamp, -1 unless evictable
     int32_t* state;  // [U][S] SlotState
     int32_t* fill;   // [U][S] tokens in the page
-    int32_t* unit;   // [U][4] UnitField
+    int32_t* unit;   // [U][kUnitFields]
     int32_t* err;    // device flag, nonzero after an internal inconsistency
+    double* score;   // [U][S] page scores (split path)
+    float* part;     // [U][nsplit][G][D+2] partial attention (split path)
     int U, G, D, ps, S, Lcap;
-    int bf16;        // 1: bf16 pool, 0: fp32 pool
+    int nsplit, bps;  // attention splits per unit, 32-token blocks per split
+    int bf16;         // 1: bf16 pool, 0: fp32 pool
 };
 
 struct StepIO {
@@ -45,14 +55,23 @@ struct StepIO {
     int32_t* evicted_out;
 };
 
+// Launch plan of one decode step.
+struct StepPlan {
+    int waves;       // wavefronts per step workgroup (bf16)
+    int nsplit, bps; // splits per unit and blocks per split
+    bool fused;      // true: the step workgroup also runs the epilogue (nsplit == 1, bf16)
+    size_t lds;      // dynamic LDS of the step kernel
+};
+
+StepPlan plan_step(int U, int G, int D, int S, int Lcap, bool bf16, int split_override);
+
 // Launchers (asynchronous on `stream`; return the launch status).
 hipError_t launch_prefill(const LayerView& L, const void* k, const void* v, int P, int keep_pages,
                           hipStream_t stream);
-hipError_t launch_append(const LayerView& L, const StepIO& io, hipStream_t stream);
-hipError_t launch_attention(const LayerView& L, const StepIO& io, int nsplit, int blocks_per_split,
-                            float* partials, hipStream_t stream);
-hipError_t launch_merge(const LayerView& L, const StepIO& io, int nsplit, const float* partials,
-                        hipStream_t stream);
-hipError_t launch_score(const LayerView& L, const StepIO& io, double r, hipStream_t stream);
+// The step kernel: attention, page scores, append; plus the epilogue when fused.
+hipError_t launch_step(const LayerView& L, const StepIO& io, const StepPlan& plan, double r,
+                       hipStream_t stream);
+// The epilogue kernel of the split path: merge, refresh, evict, state out.
+hipError_t launch_epilogue(const LayerView& L, const StepIO& io, double r, hipStream_t stream);
 
 }  // namespace raas

@@ -4,16 +4,22 @@
 // Pool layout in HBM, per unit (sequence, layer, KV head): a contiguous run of
 // Lcap = roundup(S * page_size, 32) token rows for K and for V. Token t of
 // slot s sits at row s * page_size + t. Rows are grouped in blocks of 32; in a
-// bf16 pool each block is stored in the order the attention kernel's MFMA
-// operands are loaded, so that every 16-byte-per-lane load of a wavefront
-// reads 1 KiB of consecutive bytes:
+// bf16 pool each block is stored in the order the attention MFMA operands
+// are loaded, so that every 16-byte-per-lane load of a wavefront reads 1 KiB
+// of consecutive bytes:
 //   K block: [2 row tiles][D/32 k-steps][4 lane groups][16 rows][8 channels],
 //            tile q, row i holding token 8*(i/4) + 4*q + i%4, lane group a
 //            channels 32*ks + 8*a .. +8;
 //   V block: [D/16 channel tiles][4 token octets][16 channels][8 tokens],
-//            i.e. V transposed so a lane reads 8 consecutive tokens of one
-//            channel.
+//            V transposed so a lane reads 8 consecutive tokens of one channel.
 // An fp32 pool keeps plain [row][channel] order.
+//
+// One decode step is one launch of a step kernel (attention over the
+// resident pages with the new token substituted in registers, the append of
+// that token, the page scores) whose workgroup, when one workgroup covers a
+// whole unit, also runs the epilogue (top-r refresh, eviction, next target
+// slot, state out). When a unit is split over several workgroups, or the pool
+// is fp32, the epilogue is a second kernel that also merges the splits.
 #include <math.h>
 
 #include "raas_internal.h"
@@ -65,14 +71,17 @@ __device__ __forceinline__ size_t v_off(int t, int c) {
     return (size_t)b * 32 * D + (size_t)nb * 512 + (16 * a + i) * 8 + j;
 }
 
-__device__ __forceinline__ bf16x8 ld_bf16x8(const uint16_t* p) {
-    return __builtin_bit_cast(bf16x8, *reinterpret_cast<const u32x4*>(p));
-}
+__device__ __forceinline__ u32x4 ld4(const void* p) { return *reinterpret_cast<const u32x4*>(p); }
+__device__ __forceinline__ void st4(void* p, u32x4 x) { *reinterpret_cast<u32x4*>(p) = x; }
 
 __device__ __forceinline__ float wave_sum(float v) {
 #pragma unroll
     for (int off = 32; off >= 1; off >>= 1) v += __shfl_xor(v, off);
     return v;
+}
+
+__device__ __forceinline__ uint16_t u16_at(const u32x4& x, int e) {
+    return (uint16_t)((x[e >> 1] >> ((e & 1) * 16)) & 0xFFFFu);
 }
 
 // ---------------------------------------------------------------------------
@@ -90,11 +99,13 @@ __global__ void k_prefill_meta(LayerView L, int P, int keep_pages) {
         L.fill[base + s] = pin ? min(L.ps, P - s * L.ps) : 0;
     }
     if (threadIdx.x == 0) {
-        int32_t* U4 = L.unit + 4 * (size_t)u;
+        int32_t* U4 = L.unit + (size_t)u * kUnitFields;
         U4[kTail] = -1;
         U4[kNextLid] = (P + L.ps - 1) / L.ps;
         U4[kClock] = P;
         U4[kEvicted] = -1;
+        U4[kNextSlot] = keep_pages;  // lowest free slot; decode starts a fresh page
+        U4[kNextFill] = 0;
     }
 }
 
@@ -111,8 +122,7 @@ __global__ void k_prefill_bf16(LayerView L, const uint16_t* __restrict__ k,
         const int u = (int)(tid / ((size_t)keep_tok * (D / 8)));
         const int rem = (int)(tid - (size_t)u * keep_tok * (D / 8));
         const int t = rem / (D / 8), ch = rem % (D / 8);
-        const u32x4 x = *reinterpret_cast<const u32x4*>(k + ((size_t)u * P + t) * D + ch * 8);
-        *reinterpret_cast<u32x4*>(K + (size_t)u * L.Lcap * D + k_off<D>(t, ch * 8)) = x;
+        st4(K + (size_t)u * L.Lcap * D + k_off<D>(t, ch * 8), ld4(k + ((size_t)u * P + t) * D + ch * 8));
     } else if (tid - nK < nV) {
         const size_t r = tid - nK;
         const int u = (int)(r / ((size_t)octets * D));
@@ -126,8 +136,7 @@ __global__ void k_prefill_bf16(LayerView L, const uint16_t* __restrict__ k,
             const uint32_t hi = (t1 < keep_tok) ? v[((size_t)u * P + t1) * D + c] : 0u;
             w[j / 2] = lo | (hi << 16);
         }
-        u32x4 x = {w[0], w[1], w[2], w[3]};
-        *reinterpret_cast<u32x4*>(V + (size_t)u * L.Lcap * D + v_off<D>(8 * g, c)) = x;
+        st4(V + (size_t)u * L.Lcap * D + v_off<D>(8 * g, c), u32x4{w[0], w[1], w[2], w[3]});
     }
 }
 
@@ -142,158 +151,379 @@ __global__ void k_prefill_f32(LayerView L, const float* __restrict__ k, const fl
     const int t = rem / (D / 4), ch = rem % (D / 4);
     const size_t src = ((size_t)u * P + t) * D + ch * 4;
     const size_t dst = ((size_t)u * L.Lcap + t) * D + ch * 4;
-    *reinterpret_cast<float4*>((float*)L.K + dst) = *reinterpret_cast<const float4*>(k + src);
-    *reinterpret_cast<float4*>((float*)L.V + dst) = *reinterpret_cast<const float4*>(v + src);
+    st4((float*)L.K + dst, ld4(k + src));
+    st4((float*)L.V + dst, ld4(v + src));
 }
 
 // ---------------------------------------------------------------------------
-// Append (Algorithm 1, "store K_new and V_new"; Section 3.3 pages): one
-// wavefront per unit. When the tail page is full or absent the lowest free
-// slot becomes a fresh evictable page stamped with the clock. Eviction at the
-// end of the previous step guarantees a free slot in that case.
+// Epilogue of a step, for one unit, run by every thread of one workgroup.
+// Slot state is in LDS with the page the step opened already marked
+// evictable; s_score holds the score of every evictable page.
+//  - Top-r refresh (Algorithm 1; Section 3.2): with n evictable pages and
+//    k = floor(r*n), page p gets ts = clock when at least n-k evictable
+//    pages score strictly less, i.e. exactly the pages above the (n-k)-th
+//    smallest score.
+//  - Eviction (Algorithm 1, "if kvm.is_full(): evict KVs with the oldest
+//    timestamps"): when the tail page is full and no slot is free, the
+//    evictable page with the smallest (timestamp, logical id) is freed.
+//  - The next token's target: the tail page if it has room, else the lowest
+//    free slot (a fresh page).
 
-template <typename T, int D>
-__global__ __launch_bounds__(64) void k_append(LayerView L, const T* __restrict__ k_new,
-                                               const T* __restrict__ v_new) {
-    const int u = blockIdx.x, lane = threadIdx.x;
-    const int S = L.S, ps = L.ps;
+struct EpiShared {
+    int cnt_ev, cnt_free, min_free, victim;
+    unsigned long long min_key;
+};
+
+__device__ void load_slots(const LayerView& L, int u, double* s_score, int* s_state, int* s_ts, int* s_lid) {
+    const int S = L.S;
     const size_t base = (size_t)u * S;
-    int32_t* U4 = L.unit + 4 * (size_t)u;
-    int tail = U4[kTail];
-    int f = (tail >= 0) ? L.fill[base + tail] : ps;
-    if (f == ps) {
-        int s = -1;
-        for (int b0 = 0; b0 < S; b0 += 64) {
-            const int s_ = b0 + lane;
-            const bool fr = (s_ < S) && L.state[base + s_] == kFree;
-            const unsigned long long m = __ballot(fr);
-            if (m) {
-                s = b0 + __builtin_ctzll(m);
-                break;
-            }
+    const int32_t* U4 = L.unit + (size_t)u * kUnitFields;
+    const int ns = U4[kNextSlot];
+    const bool opened = U4[kNextFill] == 0;
+    for (int s = threadIdx.x; s < S; s += blockDim.x) {
+        int st = L.state[base + s], t = L.ts[base + s], id = L.lid[base + s];
+        if (s == ns && opened) {
+            st = kEvictable;
+            t = U4[kClock];
+            id = U4[kNextLid];
         }
-        if (s < 0) {  // cannot happen: the previous step evicted when full
-            if (lane == 0) atomicOr(L.err, 1);
-            return;
-        }
-        if (lane == 0) {
-            const int nl = U4[kNextLid];
-            L.state[base + s] = kEvictable;
-            L.lid[base + s] = nl;
-            L.ts[base + s] = U4[kClock];
-            U4[kNextLid] = nl + 1;
-            U4[kTail] = s;
-        }
-        tail = s;
-        f = 0;
+        s_state[s] = st;
+        s_ts[s] = t;
+        s_lid[s] = id;
+        s_score[s] = INFINITY;  // scored below when evictable; never ranks under a real score
     }
-    const T* kn = k_new + (size_t)u * D;
-    const T* vn = v_new + (size_t)u * D;
-    const int row = tail * ps + f;
-    T* kmin = (T*)L.kmin + (base + tail) * D;
-    T* kmax = (T*)L.kmax + (base + tail) * D;
-    for (int c = lane; c < D; c += 64) {
-        const T x = kn[c];
-        if (f == 0) {
-            kmin[c] = x;
-            kmax[c] = x;
-        } else {
-            if (to_f<T>(x) < to_f<T>(kmin[c])) kmin[c] = x;
-            if (to_f<T>(x) > to_f<T>(kmax[c])) kmax[c] = x;
+}
+
+__device__ void retention(const LayerView& L, const StepIO& io, int u, double r, const double* s_score,
+                          int* s_state, int* s_ts, const int* s_lid, EpiShared& e) {
+    const int S = L.S, ps = L.ps, tid = threadIdx.x, nt = blockDim.x;
+    const size_t base = (size_t)u * S;
+    int32_t* U4 = L.unit + (size_t)u * kUnitFields;
+    const int clock = U4[kClock], ns = U4[kNextSlot], nf = U4[kNextFill], next_lid = U4[kNextLid];
+    const bool opened = nf == 0;
+    if (tid == 0) {
+        e.cnt_ev = 0;
+        e.cnt_free = 0;
+        e.min_free = S;
+        e.victim = -1;
+        e.min_key = ~0ull;
+    }
+    __syncthreads();
+    int ev = 0, fr = 0;
+    for (int s = tid; s < S; s += nt) {
+        ev += (s_state[s] == kEvictable);
+        fr += (s_state[s] == kFree);
+    }
+    if (ev) atomicAdd(&e.cnt_ev, ev);
+    if (fr) atomicAdd(&e.cnt_free, fr);
+    __syncthreads();
+    const int n = e.cnt_ev, nfree = e.cnt_free;
+    const int k = (int)floor(r * (double)n);
+    if (k > 0) {
+        // gsz consecutive threads rank one page; non-evictable slots score +inf
+        int gsz = 1;
+        while (gsz < 16 && gsz * 2 * S <= nt) gsz *= 2;
+        const int sub = tid & (gsz - 1);
+        const int rounds = (S * gsz + nt - 1) / nt;
+        for (int rd = 0; rd < rounds; ++rd) {
+            const int p = (rd * nt + tid) / gsz;
+            const double sp = p < S ? s_score[p] : -INFINITY;
+            int less = 0;
+#pragma unroll 8
+            for (int o = sub; o < S; o += gsz) less += s_score[o] < sp;
+            for (int off = 1; off < gsz; off <<= 1) less += __shfl_xor(less, off);
+            if (p < S && sub == 0 && s_state[p] == kEvictable && less >= n - k) s_ts[p] = clock;
         }
     }
-    if constexpr (sizeof(T) == 2) {
-        uint16_t* Ku = (uint16_t*)L.K + (size_t)u * L.Lcap * D;
-        uint16_t* Vu = (uint16_t*)L.V + (size_t)u * L.Lcap * D;
-        if (lane < D / 8)
-            *reinterpret_cast<u32x4*>(Ku + k_off<D>(row, lane * 8)) =
-                *reinterpret_cast<const u32x4*>((const uint16_t*)kn + lane * 8);
-        for (int c = lane; c < D; c += 64) Vu[v_off<D>(row, c)] = ((const uint16_t*)vn)[c];
-    } else {
-        float* Ku = (float*)L.K + ((size_t)u * L.Lcap + row) * D;
-        float* Vu = (float*)L.V + ((size_t)u * L.Lcap + row) * D;
-        for (int c = lane; c < D; c += 64) {
-            Ku[c] = (float)kn[c];
-            Vu[c] = (float)vn[c];
+    __syncthreads();
+    const int fill_tail = nf + 1;
+    const bool full = (fill_tail == ps) && nfree == 0;
+    if (full) {
+        unsigned long long best = ~0ull;
+        for (int s = tid; s < S; s += nt) {
+            if (s_state[s] != kEvictable) continue;
+            const unsigned long long key = ((unsigned long long)(uint32_t)s_ts[s] << 32) | (uint32_t)s_lid[s];
+            best = key < best ? key : best;
         }
+        if (best != ~0ull) atomicMin(&e.min_key, best);
+        __syncthreads();
+        for (int s = tid; s < S; s += nt) {
+            if (s_state[s] == kEvictable && (uint32_t)s_lid[s] == (uint32_t)(e.min_key & 0xFFFFFFFFull))
+                e.victim = s;
+        }
+        __syncthreads();
     }
-    if (lane == 0) L.fill[base + tail] = f + 1;
+    const int victim = e.victim;
+    const int evicted = victim >= 0 ? s_lid[victim] : -1;
+    if (full && victim < 0 && tid == 0) atomicOr(L.err, 2);
+    const bool tail_gone = victim == ns;
+    const int tail_fill = tail_gone ? 0 : fill_tail;
+    const bool need_free = tail_gone || tail_fill == ps;
+    if (need_free) {
+        int lo = S;
+        for (int s = tid; s < S; s += nt)
+            if (s_state[s] == kFree || s == victim) lo = min(lo, s);
+        if (lo < S) atomicMin(&e.min_free, lo);
+    }
+    __syncthreads();
+    const int next_slot = need_free ? e.min_free : ns;
+    if (need_free && next_slot >= S && tid == 0) atomicOr(L.err, 4);
+    for (int s = tid; s < S; s += nt) {
+        const bool gone = s == victim;
+        const int st = gone ? kFree : s_state[s];
+        const int t = gone ? -1 : s_ts[s];
+        const int id = gone ? -1 : s_lid[s];
+        L.state[base + s] = st;
+        L.ts[base + s] = t;
+        if (s == ns || gone) {
+            L.lid[base + s] = id;
+            L.fill[base + s] = gone ? 0 : fill_tail;
+        }
+        if (io.page_table_out) io.page_table_out[base + s] = (st == kFree) ? -1 : id;
+        if (io.timestamps_out) io.timestamps_out[base + s] = (st == kEvictable) ? t : -1;
+    }
+    if (tid == 0) {
+        U4[kTail] = tail_gone ? -1 : ns;
+        U4[kNextLid] = next_lid + (opened ? 1 : 0);
+        U4[kClock] = clock + 1;
+        U4[kEvicted] = evicted;
+        U4[kNextSlot] = next_slot < S ? next_slot : 0;
+        U4[kNextFill] = need_free ? 0 : tail_fill;
+        if (io.evicted_out) io.evicted_out[u] = evicted;
+    }
 }
 
 // ---------------------------------------------------------------------------
-// Attention over every resident token (Algorithm 1, attention(Q, K_old::K_new,
-// V_old::V_new)), split-K over 32-token blocks.
-//
-// bf16 pools: one workgroup of kAttnWaves wavefronts per (unit, split); each
-// wavefront holds the unit's whole GQA query group and walks blocks
-// round-robin. Per block: QK^T as two 16x16x32 bf16 MFMA tiles per 32
-// channels (rows = tokens, columns = query heads, G <= 16 of the 16 used),
-// online softmax in base 2 with one cross-lane max per block, and PV as
-// D/16 MFMAs of V^T (rows = channels) times P^T (columns = heads). A lane
-// owns one head (its column) in both products, so no data moves between
-// lanes except the block max. Partial (max, sum, acc) of the wavefronts are
-// merged through LDS; with several splits the workgroup writes a partial
-// that k_merge combines.
+// Page scores (Section 3.3, Quest's representative keys): for each evictable
+// page, max over the G query heads of sum_c max(q_c*kmax_c, q_c*kmin_c), in
+// fp64. With q+ = max(q, 0) and q- = min(q, 0) the selected product is
+// q+*kmax + q-*kmin, one of the two terms being an exact zero; products of
+// bf16 or fp32 values are exact in fp64, so each fused multiply-add rounds
+// exactly as an add of the exact product. Four lanes per page: each sums
+// D/4 consecutive channels in order, the quarters combine through a fixed
+// xor tree, so equal pages score equal. The page the step writes to has its
+// min/max widened by the new key here, and stored back.
 
 template <int D>
-__global__ __launch_bounds__(kAttnWaves * 64) void k_attn_bf16(LayerView L, const uint16_t* __restrict__ q,
-                                                           float* __restrict__ part,
-                                                           uint16_t* __restrict__ out, int nsplit,
-                                                           int bps, float scale_log2) {
-    constexpr int KS = D / 32, NB = D / 16, BLK = 32 * D;
-    __shared__ float s_m[kAttnWaves][16];
-    __shared__ float s_l[kAttnWaves][16];
-    __shared__ __align__(16) float s_o[kAttnWaves][16][D + 4];
+struct ScoreFrag {
+    u32x4 kx[D / 32], kn[D / 32];  // D/4 bf16 channels of kmax and kmin
+};
 
-    const int lane = threadIdx.x & 63, w = threadIdx.x >> 6;
-    const int grp = lane >> 4, col = lane & 15;
-    const int u = blockIdx.x / nsplit, split = blockIdx.x - (blockIdx.x / nsplit) * nsplit;
+template <int D>
+__device__ __forceinline__ void score_load(const LayerView& L, int u, int p, int qtr, bool act,
+                                           ScoreFrag<D>& f) {
+    const size_t off = ((size_t)u * L.S + p) * D + qtr * (D / 4);
+    const uint16_t* kx = (const uint16_t*)L.kmax + off;
+    const uint16_t* kn = (const uint16_t*)L.kmin + off;
+#pragma unroll
+    for (int i = 0; i < D / 32; ++i) {
+        f.kx[i] = act ? ld4(kx + 8 * i) : u32x4{0u, 0u, 0u, 0u};
+        f.kn[i] = act ? ld4(kn + 8 * i) : u32x4{0u, 0u, 0u, 0u};
+    }
+}
+
+template <int D>
+__device__ __forceinline__ double score_compute(const LayerView& L, int u, int p, int qtr, bool act,
+                                                ScoreFrag<D>& f, bool is_tail, bool opened,
+                                                const uint16_t* __restrict__ k_new, const double* s_qp,
+                                                const double* s_qn) {
+    const int G = L.G;
+    if (act && is_tail) {
+        const uint16_t* kn_src = k_new + qtr * (D / 4);
+#pragma unroll
+        for (int i = 0; i < D / 32; ++i) {
+            const u32x4 x = ld4(kn_src + 8 * i);
+            if (opened) {
+                f.kx[i] = x;
+                f.kn[i] = x;
+            } else {
+                u32x4 mx, mn;
+#pragma unroll
+                for (int h = 0; h < 4; ++h) {
+                    uint32_t a = 0, b = 0;
+#pragma unroll
+                    for (int half = 0; half < 2; ++half) {
+                        const uint16_t xv = (uint16_t)(x[h] >> (16 * half));
+                        const uint16_t hv = (uint16_t)(f.kx[i][h] >> (16 * half));
+                        const uint16_t lv = (uint16_t)(f.kn[i][h] >> (16 * half));
+                        a |= (uint32_t)(bf2f(xv) > bf2f(hv) ? xv : hv) << (16 * half);
+                        b |= (uint32_t)(bf2f(xv) < bf2f(lv) ? xv : lv) << (16 * half);
+                    }
+                    mx[h] = a;
+                    mn[h] = b;
+                }
+                f.kx[i] = mx;
+                f.kn[i] = mn;
+            }
+            const size_t off = ((size_t)u * L.S + p) * D + qtr * (D / 4) + 8 * i;
+            st4((uint16_t*)L.kmax + off, f.kx[i]);
+            st4((uint16_t*)L.kmin + off, f.kn[i]);
+        }
+    }
+    const int c0 = qtr * (D / 4);
+    double best = -INFINITY;
+#pragma unroll 1
+    for (int j = 0; j < G; ++j) {
+        const double* qp = s_qp + (size_t)j * D + c0;
+        const double* qn = s_qn + (size_t)j * D + c0;
+        double a = 0.0;
+#pragma unroll
+        for (int i = 0; i < D / 32; ++i) {
+#pragma unroll
+            for (int e = 0; e < 8; ++e) {
+                a = fma(qp[8 * i + e], (double)bf2f(u16_at(f.kx[i], e)), a);
+                a = fma(qn[8 * i + e], (double)bf2f(u16_at(f.kn[i], e)), a);
+            }
+        }
+        a += __shfl_xor(a, 1);
+        a += __shfl_xor(a, 2);
+        best = a > best ? a : best;
+    }
+    return best;
+}
+
+// ---------------------------------------------------------------------------
+// Step kernel, bf16 pools: attention over every resident token (Algorithm 1,
+// attention(Q, K_old::K_new, V_old::V_new)), split-K over 32-token blocks.
+// One workgroup of NW wavefronts per (unit, split); each wavefront holds the
+// unit's whole GQA query group and walks blocks round-robin. Per block: QK^T
+// as two 16x16x32 bf16 MFMA tiles per 32 channels (rows = tokens, columns =
+// query heads, G <= 16 of the 16 used), online softmax in base 2 with one
+// cross-lane max per block, and PV as D/16 MFMAs of V^T (rows = channels)
+// times P^T (columns = heads). A lane owns one head (its column) in both
+// products, so no data moves between lanes except the block max. The new
+// token is not in the pool when the block is read: its K/V come from the
+// step's inputs, substituted in registers, and the wavefront 0 of the
+// owning workgroup stores it.
+
+template <int D, int NW>
+__global__ __launch_bounds__(NW * 64) void k_step_bf16(LayerView L, StepIO io, float scale_log2, double r,
+                                                       int fused) {
+    constexpr int KS = D / 32, NB = D / 16, BLK = 32 * D;
+    extern __shared__ __align__(16) unsigned char smem[];
+    __shared__ float s_m[NW][16];
+    __shared__ float s_l[NW][16];
+    __shared__ EpiShared epi;
+
     const int G = L.G, S = L.S, ps = L.ps;
+    double* s_qp = reinterpret_cast<double*>(smem);      // [G][D]
+    double* s_qn = s_qp + (size_t)G * D;                  // [G][D]
+    float* s_o = reinterpret_cast<float*>(s_qn + (size_t)G * D);  // [NW][G][D+4]
+    double* s_score = reinterpret_cast<double*>(s_o + (size_t)NW * G * (D + 4));  // [S], fused only
+    int* s_state = reinterpret_cast<int*>(s_score + S);  // [S], fused only
+    int* s_ts = s_state + S;
+    int* s_lid = s_ts + S;
+
+    const int tid = threadIdx.x, lane = tid & 63, w = tid >> 6;
+    const int grp = lane >> 4, col = lane & 15;
+    const int nsplit = L.nsplit;
+    const int u = blockIdx.x / nsplit, split = blockIdx.x - (blockIdx.x / nsplit) * nsplit;
+    const size_t base = (size_t)u * S;
+    const int32_t* U4 = L.unit + (size_t)u * kUnitFields;
+    const int ns = U4[kNextSlot], nf = U4[kNextFill];
+    const bool opened = nf == 0;
+    const int row_new = ns * ps + nf, b_new = row_new >> 5, tt_new = row_new & 31;
     const int nblk = L.Lcap / 32;
-    const int b0 = split * bps;
-    const int b1 = min(nblk, b0 + bps);
+    const int b0 = split * L.bps;
+    const int b1 = min(nblk, b0 + L.bps);
+    const int sl0 = min(S, (32 * b0 + ps - 1) / ps), sl1 = min(S, (32 * b1 + ps - 1) / ps);
+    const uint16_t* qg = (const uint16_t*)io.q + (size_t)u * G * D;
+    const uint16_t* kn_g = (const uint16_t*)io.k_new + (size_t)u * D;
+    const uint16_t* vn_g = (const uint16_t*)io.v_new + (size_t)u * D;
     const uint16_t* Ku = (const uint16_t*)L.K + (size_t)u * L.Lcap * D;
     const uint16_t* Vu = (const uint16_t*)L.V + (size_t)u * L.Lcap * D;
-    const int32_t* fu = L.fill + (size_t)u * S;
+    const int32_t* fu = L.fill + base;
+
+    for (int i = tid; i < G * D; i += NW * 64) {
+        const double x = (double)bf2f(qg[i]);
+        s_qp[i] = x > 0.0 ? x : 0.0;
+        s_qn[i] = x < 0.0 ? x : 0.0;
+    }
+    if (fused) load_slots(L, u, s_score, s_state, s_ts, s_lid);
 
     bf16x8 qv[KS];
 #pragma unroll
     for (int ks = 0; ks < KS; ++ks) {
-        if (col < G) {
-            qv[ks] = ld_bf16x8(q + ((size_t)u * G + col) * D + 32 * ks + 8 * grp);
-        } else {
-            qv[ks] = __builtin_bit_cast(bf16x8, u32x4{0u, 0u, 0u, 0u});
-        }
+        const u32x4 x = (col < G) ? ld4(qg + (size_t)col * D + 32 * ks + 8 * grp) : u32x4{0u, 0u, 0u, 0u};
+        qv[ks] = __builtin_bit_cast(bf16x8, x);
     }
     float m_run = -INFINITY, l_run = 0.0f;
     f32x4 acc[NB];
 #pragma unroll
     for (int nb = 0; nb < NB; ++nb) acc[nb] = f32x4{0.f, 0.f, 0.f, 0.f};
 
-    for (int b = b0 + w; b < b1; b += kAttnWaves) {
-        // tokens 8*grp .. 8*grp+7 of the block lie in one page (page_size % 8 == 0)
+    // valid tokens among this lane's 8 rows of block b (they lie in one page: page_size % 8 == 0)
+    auto valid_rows = [&](int b) {
         const int t0 = 32 * b + 8 * grp;
         const int slot = t0 / ps;
-        const int pos0 = t0 - slot * ps;
-        const int f = (slot < S) ? fu[slot] : 0;
-        const int nv = min(max(f - pos0, 0), 8);
-        if (__ballot(nv > 0) == 0ull) continue;
-
+        const int f = (slot < S) ? (slot == ns ? nf + 1 : fu[slot]) : 0;
+        return min(max(f - (t0 - slot * ps), 0), 8);
+    };
+    // next block of this wavefront at or after b holding a resident token
+    auto next_block = [&](int b, int& nv) {
+        for (; b < b1; b += NW) {
+            nv = valid_rows(b);
+            if (__ballot(nv > 0) != 0ull) return b;
+        }
+        return b1;
+    };
+    auto load_block = [&](int b, u32x4 (&kr)[2][KS], u32x4 (&vr)[NB]) {
         const uint16_t* Kb = Ku + (size_t)b * BLK + lane * 8;
         const uint16_t* Vb = Vu + (size_t)b * BLK + lane * 8;
-        bf16x8 kr[2][KS], vr[NB];
 #pragma unroll
         for (int qq = 0; qq < 2; ++qq)
 #pragma unroll
-            for (int ks = 0; ks < KS; ++ks) kr[qq][ks] = ld_bf16x8(Kb + (qq * KS + ks) * 512);
+            for (int ks = 0; ks < KS; ++ks) kr[qq][ks] = ld4(Kb + (qq * KS + ks) * 512);
 #pragma unroll
-        for (int nb = 0; nb < NB; ++nb) vr[nb] = ld_bf16x8(Vb + nb * 512);
+        for (int nb = 0; nb < NB; ++nb) vr[nb] = ld4(Vb + nb * 512);
+    };
+
+    int nv_next = 0;
+    int b = next_block(b0 + w, nv_next);
+    u32x4 kr_next[2][KS], vr_next[NB];
+    if (b < b1) load_block(b, kr_next, vr_next);
+    while (b < b1) {
+        const int nv = nv_next;
+        u32x4 kr[2][KS], vr[NB];
+#pragma unroll
+        for (int qq = 0; qq < 2; ++qq)
+#pragma unroll
+            for (int ks = 0; ks < KS; ++ks) kr[qq][ks] = kr_next[qq][ks];
+#pragma unroll
+        for (int nb = 0; nb < NB; ++nb) vr[nb] = vr_next[nb];
+        const int bn = next_block(b + NW, nv_next);
+        if (bn < b1) load_block(bn, kr_next, vr_next);
+
+        if (b == b_new) {  // the new token: K/V from the inputs
+            const int i_new = 4 * (tt_new >> 3) + (tt_new & 3), q_new = (tt_new >> 2) & 1;
+            if (col == i_new) {
+#pragma unroll
+                for (int ks = 0; ks < KS; ++ks) {
+                    const u32x4 x = ld4(kn_g + 32 * ks + 8 * grp);
+                    if (q_new == 0) kr[0][ks] = x; else kr[1][ks] = x;
+                }
+            }
+            if (grp == (tt_new >> 3)) {
+                const int j_new = tt_new & 7;
+#pragma unroll
+                for (int nb = 0; nb < NB; ++nb) {
+                    const uint32_t val = vn_g[16 * nb + col];
+#pragma unroll
+                    for (int h = 0; h < 4; ++h) {
+                        if ((j_new >> 1) == h) {
+                            const int sh = (j_new & 1) * 16;
+                            vr[nb][h] = (vr[nb][h] & ~(0xFFFFu << sh)) | (val << sh);
+                        }
+                    }
+                }
+            }
+        }
 
         f32x4 s0 = {0.f, 0.f, 0.f, 0.f}, s1 = {0.f, 0.f, 0.f, 0.f};
 #pragma unroll
         for (int ks = 0; ks < KS; ++ks) {
-            s0 = __builtin_amdgcn_mfma_f32_16x16x32_bf16(kr[0][ks], qv[ks], s0, 0, 0, 0);
-            s1 = __builtin_amdgcn_mfma_f32_16x16x32_bf16(kr[1][ks], qv[ks], s1, 0, 0, 0);
+            s0 = __builtin_amdgcn_mfma_f32_16x16x32_bf16(__builtin_bit_cast(bf16x8, kr[0][ks]), qv[ks], s0, 0, 0, 0);
+            s1 = __builtin_amdgcn_mfma_f32_16x16x32_bf16(__builtin_bit_cast(bf16x8, kr[1][ks]), qv[ks], s1, 0, 0, 0);
         }
         // x[j]: scaled logit of token 8*grp + j for head `col` (base 2)
         float x[8];
@@ -315,21 +545,30 @@ __global__ __launch_bounds__(kAttnWaves * 64) void k_attn_bf16(LayerView L, cons
             for (int nb = 0; nb < NB; ++nb) acc[nb] *= alpha;
             m_run = m_new;
         }
-        float p[8], psum = 0.0f;
-#pragma unroll
-        for (int j = 0; j < 8; ++j) {
-            p[j] = __builtin_amdgcn_exp2f(x[j] - m_run);
-            psum += p[j];
-        }
-        l_run += psum;
+        float psum = 0.0f;
         bf16x8 pb;
 #pragma unroll
-        for (int j = 0; j < 8; ++j) pb[j] = (__bf16)p[j];
+        for (int j = 0; j < 8; ++j) {
+            const float p = __builtin_amdgcn_exp2f(x[j] - m_run);
+            psum += p;
+            pb[j] = (__bf16)p;
+        }
+        l_run += psum;
 #pragma unroll
         for (int nb = 0; nb < NB; ++nb)
-            acc[nb] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(vr[nb], pb, acc[nb], 0, 0, 0);
+            acc[nb] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(__builtin_bit_cast(bf16x8, vr[nb]), pb, acc[nb], 0, 0, 0);
+        b = bn;
     }
 
+    // append: store the new token in the pool (Algorithm 1, "Store K_new and V_new")
+    if (w == 0 && b_new >= b0 && b_new < b1) {
+        uint16_t* Kw = (uint16_t*)L.K + (size_t)u * L.Lcap * D;
+        uint16_t* Vw = (uint16_t*)L.V + (size_t)u * L.Lcap * D;
+        if (lane < D / 8) st4(Kw + k_off<D>(row_new, lane * 8), ld4(kn_g + lane * 8));
+        for (int c = lane; c < D; c += 64) Vw[v_off<D>(row_new, c)] = vn_g[c];
+    }
+
+    // park this wavefront's partial attention in LDS
     l_run += __shfl_xor(l_run, 16);
     l_run += __shfl_xor(l_run, 32);
     if (grp == 0) {
@@ -339,26 +578,42 @@ __global__ __launch_bounds__(kAttnWaves * 64) void k_attn_bf16(LayerView L, cons
     if (col < G) {
 #pragma unroll
         for (int nb = 0; nb < NB; ++nb)
-            *reinterpret_cast<f32x4*>(&s_o[w][col][16 * nb + 4 * grp]) = acc[nb];
+            *reinterpret_cast<f32x4*>(&s_o[((size_t)w * G + col) * (D + 4) + 16 * nb + 4 * grp]) = acc[nb];
     }
+
+    // page scores of the slots whose first row lies in this workgroup's blocks
+    __syncthreads();  // s_qp / s_qn staged
+    const int qtr = lane & 3;
+    for (int first = sl0 + 16 * w; first < sl1; first += 16 * NW) {
+        const int p = first + (lane >> 2);
+        const bool act = p < sl1 && (p == ns || L.state[base + p] == kEvictable);
+        ScoreFrag<D> frag;
+        score_load<D>(L, u, p, qtr, act && !(p == ns && opened), frag);
+        const double sc = score_compute<D>(L, u, p, qtr, act, frag, p == ns, opened, kn_g, s_qp, s_qn);
+        if (act && qtr == 0) {
+            if (fused) s_score[p] = sc;
+            else L.score[base + p] = sc;
+        }
+    }
+
     __syncthreads();
-    for (int idx = threadIdx.x; idx < G * D; idx += kAttnWaves * 64) {
+    for (int idx = tid; idx < G * D; idx += NW * 64) {
         const int h = idx / D, c = idx - (idx / D) * D;
         float M = -INFINITY;
 #pragma unroll
-        for (int ww = 0; ww < kAttnWaves; ++ww) M = fmaxf(M, s_m[ww][h]);
+        for (int ww = 0; ww < NW; ++ww) M = fmaxf(M, s_m[ww][h]);
         float O = 0.0f, Ls = 0.0f;
 #pragma unroll
-        for (int ww = 0; ww < kAttnWaves; ++ww) {
+        for (int ww = 0; ww < NW; ++ww) {
             const float mw = s_m[ww][h];
             const float wt = (mw == -INFINITY) ? 0.0f : __builtin_amdgcn_exp2f(mw - M);
-            O += wt * s_o[ww][h][c];
+            O += wt * s_o[((size_t)ww * G + h) * (D + 4) + c];
             Ls += wt * s_l[ww][h];
         }
-        if (nsplit == 1) {
-            out[((size_t)u * G + h) * D + c] = f2bf(O / Ls);
+        if (fused) {
+            ((uint16_t*)io.out)[((size_t)u * G + h) * D + c] = f2bf(O / Ls);
         } else {
-            float* pp = part + (((size_t)u * nsplit + split) * G + h) * (D + 2);
+            float* pp = L.part + (((size_t)u * nsplit + split) * G + h) * (D + 2);
             pp[c] = O;
             if (c == 0) {
                 pp[D] = M;
@@ -366,23 +621,32 @@ __global__ __launch_bounds__(kAttnWaves * 64) void k_attn_bf16(LayerView L, cons
             }
         }
     }
+    if (fused) retention(L, io, u, r, s_score, s_state, s_ts, s_lid, epi);
 }
 
-// fp32 pools: one wavefront per (unit, split), one token at a time, lanes
-// across channels; online softmax per head in fp32.
+// Step kernel, fp32 pools: one wavefront per (unit, split), one token at a
+// time, lanes across channels, online softmax per head in fp32; one lane per
+// page for the scores, summing the channels in order.
 template <int D>
-__global__ __launch_bounds__(64) void k_attn_f32(LayerView L, const float* __restrict__ q,
-                                                 float* __restrict__ part, float* __restrict__ out,
-                                                 int nsplit, int tps, float scale_log2) {
+__global__ __launch_bounds__(64) void k_step_f32(LayerView L, StepIO io, float scale_log2) {
     constexpr int DPL = D / 64;
     const int lane = threadIdx.x;
+    const int nsplit = L.nsplit;
     const int u = blockIdx.x / nsplit, split = blockIdx.x - (blockIdx.x / nsplit) * nsplit;
     const int G = L.G, S = L.S, ps = L.ps;
-    const int t0 = split * tps;
-    const int t1 = min(S * ps, t0 + tps);
+    const size_t base = (size_t)u * S;
+    const int32_t* U4 = L.unit + (size_t)u * kUnitFields;
+    const int ns = U4[kNextSlot], nf = U4[kNextFill];
+    const bool opened = nf == 0;
+    const int row_new = ns * ps + nf;
+    const int t0 = split * L.bps * 32;
+    const int t1 = min(S * ps, t0 + L.bps * 32);
     const float* Ku = (const float*)L.K + (size_t)u * L.Lcap * D;
     const float* Vu = (const float*)L.V + (size_t)u * L.Lcap * D;
-    const int32_t* fu = L.fill + (size_t)u * S;
+    const float* qg = (const float*)io.q + (size_t)u * G * D;
+    const float* kn_g = (const float*)io.k_new + (size_t)u * D;
+    const float* vn_g = (const float*)io.v_new + (size_t)u * D;
+    const int32_t* fu = L.fill + base;
 
     float qr[16][DPL], m[16], l[16], acc[16][DPL];
 #pragma unroll
@@ -391,18 +655,19 @@ __global__ __launch_bounds__(64) void k_attn_f32(LayerView L, const float* __res
         l[j] = 0.0f;
 #pragma unroll
         for (int i = 0; i < DPL; ++i) {
-            qr[j][i] = (j < G) ? q[((size_t)u * G + j) * D + lane + 64 * i] : 0.0f;
+            qr[j][i] = (j < G) ? qg[(size_t)j * D + lane + 64 * i] : 0.0f;
             acc[j][i] = 0.0f;
         }
     }
     for (int t = t0; t < t1; ++t) {
         const int slot = t / ps;
-        if (t - slot * ps >= fu[slot]) continue;
+        const int f = (slot == ns) ? nf + 1 : fu[slot];
+        if (t - slot * ps >= f) continue;
         float kr[DPL], vr[DPL];
 #pragma unroll
         for (int i = 0; i < DPL; ++i) {
-            kr[i] = Ku[(size_t)t * D + lane + 64 * i];
-            vr[i] = Vu[(size_t)t * D + lane + 64 * i];
+            kr[i] = (t == row_new) ? kn_g[lane + 64 * i] : Ku[(size_t)t * D + lane + 64 * i];
+            vr[i] = (t == row_new) ? vn_g[lane + 64 * i] : Vu[(size_t)t * D + lane + 64 * i];
         }
 #pragma unroll
         for (int j = 0; j < 16; ++j) {
@@ -423,196 +688,147 @@ __global__ __launch_bounds__(64) void k_attn_f32(LayerView L, const float* __res
 #pragma unroll
     for (int j = 0; j < 16; ++j) {
         if (j >= G) break;
-        if (nsplit == 1) {
+        float* pp = L.part + (((size_t)u * nsplit + split) * G + j) * (D + 2);
 #pragma unroll
-            for (int i = 0; i < DPL; ++i) out[((size_t)u * G + j) * D + lane + 64 * i] = acc[j][i] / l[j];
-        } else {
-            float* pp = part + (((size_t)u * nsplit + split) * G + j) * (D + 2);
+        for (int i = 0; i < DPL; ++i) pp[lane + 64 * i] = acc[j][i];
+        if (lane == 0) {
+            pp[D] = m[j];
+            pp[D + 1] = l[j];
+        }
+    }
+    if (row_new >= t0 && row_new < t1) {  // append
+        float* Kw = (float*)L.K + ((size_t)u * L.Lcap + row_new) * D;
+        float* Vw = (float*)L.V + ((size_t)u * L.Lcap + row_new) * D;
+        for (int c = lane; c < D; c += 64) {
+            Kw[c] = kn_g[c];
+            Vw[c] = vn_g[c];
+        }
+    }
+    // page scores: pages whose first row lies in this split
+    const int sl0 = min(S, (t0 + ps - 1) / ps), sl1 = min(S, (t1 + ps - 1) / ps);
+    for (int p = sl0 + lane; p < sl1; p += 64) {
+        const bool tail = p == ns;
+        if (!(tail || L.state[base + p] == kEvictable)) continue;
+        float* kx = (float*)L.kmax + (base + p) * D;
+        float* kn = (float*)L.kmin + (base + p) * D;
+        double best = -INFINITY;
+        double accj[16];
 #pragma unroll
-            for (int i = 0; i < DPL; ++i) pp[lane + 64 * i] = acc[j][i];
-            if (lane == 0) {
-                pp[D] = m[j];
-                pp[D + 1] = l[j];
+        for (int j = 0; j < 16; ++j) accj[j] = 0.0;
+        for (int c = 0; c < D; ++c) {
+            float hi = kx[c], lo = kn[c];
+            if (tail) {
+                const float x = kn_g[c];
+                hi = opened ? x : fmaxf(hi, x);
+                lo = opened ? x : fminf(lo, x);
+                kx[c] = hi;
+                kn[c] = lo;
+            }
+#pragma unroll
+            for (int j = 0; j < 16; ++j) {
+                if (j < G) {
+                    const double qd = (double)qg[(size_t)j * D + c];
+                    const double a = qd * (double)hi, b = qd * (double)lo;
+                    accj[j] += a > b ? a : b;
+                }
             }
         }
+#pragma unroll
+        for (int j = 0; j < 16; ++j)
+            if (j < G) best = accj[j] > best ? accj[j] : best;
+        L.score[base + p] = best;
     }
 }
 
-// Split-K merge: out = sum_s 2^(M_s - M) O_s / sum_s 2^(M_s - M) L_s.
+// Epilogue kernel of the split path: merges the splits' partial attention
+// (out = sum_s 2^(M_s - M) O_s / sum_s 2^(M_s - M) L_s), then refresh,
+// eviction and state out for the unit.
 template <typename T>
-__global__ __launch_bounds__(256) void k_merge(LayerView L, const float* __restrict__ part,
-                                               T* __restrict__ out, int nsplit) {
-    const int u = blockIdx.x, G = L.G, D = L.D;
+__global__ __launch_bounds__(256) void k_epilogue(LayerView L, StepIO io, double r) {
+    extern __shared__ __align__(16) unsigned char smem[];
+    __shared__ EpiShared epi;
+    const int S = L.S, G = L.G, D = L.D, nsplit = L.nsplit;
+    double* s_score = reinterpret_cast<double*>(smem);
+    int* s_state = reinterpret_cast<int*>(s_score + S);
+    int* s_ts = s_state + S;
+    int* s_lid = s_ts + S;
+    const int u = blockIdx.x;
+    const size_t base = (size_t)u * S;
+    load_slots(L, u, s_score, s_state, s_ts, s_lid);
+    __syncthreads();
+    for (int s = threadIdx.x; s < S; s += blockDim.x)
+        if (s_state[s] == kEvictable) s_score[s] = L.score[base + s];
+    __syncthreads();
     for (int idx = threadIdx.x; idx < G * D; idx += blockDim.x) {
         const int h = idx / D, c = idx - (idx / D) * D;
         float M = -INFINITY;
         for (int s = 0; s < nsplit; ++s)
-            M = fmaxf(M, part[(((size_t)u * nsplit + s) * G + h) * (D + 2) + D]);
+            M = fmaxf(M, L.part[(((size_t)u * nsplit + s) * G + h) * (D + 2) + D]);
         float O = 0.0f, Ls = 0.0f;
         for (int s = 0; s < nsplit; ++s) {
-            const float* pp = part + (((size_t)u * nsplit + s) * G + h) * (D + 2);
+            const float* pp = L.part + (((size_t)u * nsplit + s) * G + h) * (D + 2);
             const float ms = pp[D];
             const float wt = (ms == -INFINITY) ? 0.0f : __builtin_amdgcn_exp2f(ms - M);
             O += wt * pp[c];
             Ls += wt * pp[D + 1];
         }
-        out[((size_t)u * G + h) * D + c] = from_f<T>(O / Ls);
+        ((T*)io.out)[((size_t)u * G + h) * D + c] = from_f<T>(O / Ls);
     }
-}
-
-// ---------------------------------------------------------------------------
-// Score, threshold, refresh, evict (Algorithm 1, store_cache; Sections
-// 3.2-3.3): one workgroup per unit.
-//  - Each evictable page gets max over the G query heads of
-//    sum_c max(q_c*kmax_c, q_c*kmin_c), accumulated in fp64 (products of
-//    bf16 or fp32 values are exact in fp64); 16 lanes per page, each summing
-//    D/16 channels in order, then a fixed xor tree, so equal pages score
-//    equal.
-//  - With n evictable pages and k = floor(r*n), page p is refreshed (ts =
-//    clock) when at least n-k evictable pages score strictly less than it:
-//    exactly the pages above the (n-k)-th smallest score.
-//  - When the tail page is full and no slot is free, the evictable page with
-//    the smallest (timestamp, logical id) is freed.
-template <typename T, int D>
-__global__ __launch_bounds__(256) void k_score(LayerView L, const T* __restrict__ q, StepIO io,
-                                               double r) {
-    extern __shared__ __align__(16) unsigned char smem[];
-    const int S = L.S, G = L.G;
-    double* s_q = reinterpret_cast<double*>(smem);  // [G][D]
-    double* s_score = s_q + (size_t)G * D;          // [S]
-    int* s_ts = reinterpret_cast<int*>(s_score + S); // [S]
-    int* s_state = s_ts + S;                        // [S]
-    __shared__ int s_cnt[2];
-    __shared__ unsigned long long s_min;
-    __shared__ int s_victim;
-
-    const int u = blockIdx.x, tid = threadIdx.x;
-    const size_t base = (size_t)u * S;
-    int32_t* U4 = L.unit + 4 * (size_t)u;
-    const int clock = U4[kClock];
-    for (int i = tid; i < G * D; i += 256) s_q[i] = (double)to_f<T>(q[(size_t)u * G * D + i]);
-    for (int s = tid; s < S; s += 256) {
-        s_state[s] = L.state[base + s];
-        s_ts[s] = L.ts[base + s];
-    }
-    if (tid == 0) {
-        s_cnt[0] = 0;
-        s_cnt[1] = 0;
-        s_min = ~0ull;
-        s_victim = -1;
-    }
-    __syncthreads();
-
-    constexpr int DPL = D / 16;
-    const int g = tid >> 4, li = tid & 15;
-    const T* kmax_u = (const T*)L.kmax + base * D;
-    const T* kmin_u = (const T*)L.kmin + base * D;
-    for (int p0 = 0; p0 < S; p0 += 16) {
-        const int p = p0 + g;
-        const bool act = (p < S) && s_state[p] == kEvictable;
-        double kx[DPL], kn[DPL];
-#pragma unroll
-        for (int e = 0; e < DPL; ++e) {
-            kx[e] = act ? (double)to_f<T>(kmax_u[(size_t)p * D + li * DPL + e]) : 0.0;
-            kn[e] = act ? (double)to_f<T>(kmin_u[(size_t)p * D + li * DPL + e]) : 0.0;
-        }
-        double best = -INFINITY;
-        for (int j = 0; j < G; ++j) {
-            const double* qj = s_q + (size_t)j * D + li * DPL;
-            double a = 0.0;
-#pragma unroll
-            for (int e = 0; e < DPL; ++e) {
-                const double hi = qj[e] * kx[e];
-                const double lo = qj[e] * kn[e];
-                a += (hi > lo) ? hi : lo;
-            }
-            a += __shfl_xor(a, 8);
-            a += __shfl_xor(a, 4);
-            a += __shfl_xor(a, 2);
-            a += __shfl_xor(a, 1);
-            best = (a > best) ? a : best;
-        }
-        if (act && li == 0) s_score[p] = best;
-    }
-    int ev = 0, fr = 0;
-    for (int s = tid; s < S; s += 256) {
-        ev += (s_state[s] == kEvictable);
-        fr += (s_state[s] == kFree);
-    }
-    if (ev) atomicAdd(&s_cnt[0], ev);
-    if (fr) atomicAdd(&s_cnt[1], fr);
-    __syncthreads();
-
-    const int n = s_cnt[0], nfree = s_cnt[1];
-    const int k = (int)floor(r * (double)n);
-    if (k > 0) {
-        for (int p = tid; p < S; p += 256) {
-            if (s_state[p] != kEvictable) continue;
-            const double sp = s_score[p];
-            int less = 0;
-            for (int o = 0; o < S; ++o) less += (s_state[o] == kEvictable && s_score[o] < sp);
-            if (less >= n - k) s_ts[p] = clock;
-        }
-    }
-    __syncthreads();
-
-    const int tail = U4[kTail];
-    const bool full = tail >= 0 && L.fill[base + tail] == L.ps && nfree == 0;
-    int evicted = -1;
-    if (full) {
-        unsigned long long best = ~0ull;
-        for (int s = tid; s < S; s += 256) {
-            if (s_state[s] != kEvictable) continue;
-            const unsigned long long key =
-                ((unsigned long long)(uint32_t)s_ts[s] << 32) | (uint32_t)L.lid[base + s];
-            best = key < best ? key : best;
-        }
-        if (best != ~0ull) atomicMin(&s_min, best);
-        __syncthreads();
-        for (int s = tid; s < S; s += 256) {
-            if (s_state[s] != kEvictable) continue;
-            const unsigned long long key =
-                ((unsigned long long)(uint32_t)s_ts[s] << 32) | (uint32_t)L.lid[base + s];
-            if (key == s_min) s_victim = s;
-        }
-        __syncthreads();
-        const int v = s_victim;
-        if (v >= 0) {
-            evicted = (int)(s_min & 0xFFFFFFFFull);
-            if (tid == 0) {
-                s_state[v] = kFree;
-                s_ts[v] = -1;
-            }
-        } else if (tid == 0) {
-            atomicOr(L.err, 2);
-        }
-        __syncthreads();
-        if (v >= 0 && tid == 0) {
-            L.lid[base + v] = -1;
-            L.fill[base + v] = 0;
-            if (tail == v) U4[kTail] = -1;
-        }
-    }
-    for (int s = tid; s < S; s += 256) {
-        L.ts[base + s] = s_ts[s];
-        L.state[base + s] = s_state[s];
-        if (io.page_table_out)
-            io.page_table_out[base + s] = (s_state[s] == kFree) ? -1 : L.lid[base + s];
-        if (io.timestamps_out) io.timestamps_out[base + s] = (s_state[s] == kEvictable) ? s_ts[s] : -1;
-    }
-    if (tid == 0) {
-        U4[kClock] = clock + 1;
-        U4[kEvicted] = evicted;
-        if (io.evicted_out) io.evicted_out[u] = evicted;
-    }
+    retention(L, io, u, r, s_score, s_state, s_ts, s_lid, epi);
 }
 
 inline unsigned grid1d(size_t n, int block) { return (unsigned)((n + block - 1) / block); }
 
+size_t step_lds(int G, int D, int S, int NW, bool fused) {
+    size_t b = (size_t)16 * G * D + (size_t)NW * G * (D + 4) * 4;
+    if (fused) b += (size_t)S * (8 + 12);
+    return b;
+}
+
+template <int D, int NW>
+hipError_t launch_step_bf16(const LayerView& L, const StepIO& io, const StepPlan& pl, float sl2, double r,
+                            hipStream_t s) {
+    hipLaunchKernelGGL((k_step_bf16<D, NW>), dim3((unsigned)(L.U * pl.nsplit)), dim3(NW * 64), pl.lds, s, L, io,
+                       sl2, r, pl.fused ? 1 : 0);
+    return hipGetLastError();
+}
+
 }  // namespace
 
 // ---------------------------------------------------------------------------
-// launchers
+
+StepPlan plan_step(int U, int G, int D, int S, int Lcap, bool bf16, int split_override) {
+    StepPlan pl{};
+    const int nblk = Lcap / kBlockTokens;
+    int want;
+    if (!bf16) {
+        pl.waves = 1;
+        want = split_override > 0 ? split_override : (nblk + 1) / 2;
+    } else {
+        pl.waves = 2;
+        for (int nw : {8, 4, 2}) {
+            if (step_lds(G, D, S, nw, false) <= kMaxLds) {
+                pl.waves = nw;
+                break;
+            }
+        }
+        if (split_override > 0) {
+            want = split_override;
+        } else {
+            // about 2048 wavefronts in flight over the 256 CUs
+            const double per_wave = fmax(1.0, (double)U * nblk / 2048.0);
+            want = (int)ceil(nblk / (pl.waves * per_wave));
+        }
+    }
+    want = want < 1 ? 1 : want;
+    want = want > kMaxSplits ? kMaxSplits : want;
+    want = want > nblk ? nblk : want;
+    pl.bps = (nblk + want - 1) / want;
+    pl.nsplit = (nblk + pl.bps - 1) / pl.bps;
+    pl.fused = bf16 && pl.nsplit == 1 && step_lds(G, D, S, pl.waves, true) <= kMaxLds;
+    pl.lds = bf16 ? step_lds(G, D, S, pl.waves, pl.fused) : 0;
+    return pl;
+}
 
 hipError_t launch_prefill(const LayerView& L, const void* k, const void* v, int P, int keep_pages,
                           hipStream_t stream) {
@@ -636,76 +852,36 @@ hipError_t launch_prefill(const LayerView& L, const void* k, const void* v, int 
     return hipGetLastError();
 }
 
-hipError_t launch_append(const LayerView& L, const StepIO& io, hipStream_t stream) {
-    if (L.bf16) {
+hipError_t launch_step(const LayerView& L, const StepIO& io, const StepPlan& pl, double r, hipStream_t s) {
+    const float sl2 = (float)(1.4426950408889634 / sqrt((double)L.D));
+    if (!L.bf16) {
+        const dim3 grid((unsigned)(L.U * pl.nsplit));
         if (L.D == 128)
-            hipLaunchKernelGGL((k_append<uint16_t, 128>), dim3(L.U), dim3(64), 0, stream, L,
-                               (const uint16_t*)io.k_new, (const uint16_t*)io.v_new);
+            hipLaunchKernelGGL(k_step_f32<128>, grid, dim3(64), 0, s, L, io, sl2);
         else
-            hipLaunchKernelGGL((k_append<uint16_t, 64>), dim3(L.U), dim3(64), 0, stream, L,
-                               (const uint16_t*)io.k_new, (const uint16_t*)io.v_new);
-    } else {
-        if (L.D == 128)
-            hipLaunchKernelGGL((k_append<float, 128>), dim3(L.U), dim3(64), 0, stream, L,
-                               (const float*)io.k_new, (const float*)io.v_new);
-        else
-            hipLaunchKernelGGL((k_append<float, 64>), dim3(L.U), dim3(64), 0, stream, L,
-                               (const float*)io.k_new, (const float*)io.v_new);
+            hipLaunchKernelGGL(k_step_f32<64>, grid, dim3(64), 0, s, L, io, sl2);
+        return hipGetLastError();
     }
-    return hipGetLastError();
+    if (L.D == 128) {
+        switch (pl.waves) {
+            case 8: return launch_step_bf16<128, 8>(L, io, pl, sl2, r, s);
+            case 4: return launch_step_bf16<128, 4>(L, io, pl, sl2, r, s);
+            default: return launch_step_bf16<128, 2>(L, io, pl, sl2, r, s);
+        }
+    }
+    switch (pl.waves) {
+        case 8: return launch_step_bf16<64, 8>(L, io, pl, sl2, r, s);
+        case 4: return launch_step_bf16<64, 4>(L, io, pl, sl2, r, s);
+        default: return launch_step_bf16<64, 2>(L, io, pl, sl2, r, s);
+    }
 }
 
-hipError_t launch_attention(const LayerView& L, const StepIO& io, int nsplit, int bps,
-                            float* partials, hipStream_t stream) {
-    const float scale_log2 = (float)(1.4426950408889634 / sqrt((double)L.D));
-    const dim3 grid((unsigned)(L.U * nsplit));
-    if (L.bf16) {
-        if (L.D == 128)
-            hipLaunchKernelGGL(k_attn_bf16<128>, grid, dim3(kAttnWaves * 64), 0, stream, L,
-                               (const uint16_t*)io.q, partials, (uint16_t*)io.out, nsplit, bps, scale_log2);
-        else
-            hipLaunchKernelGGL(k_attn_bf16<64>, grid, dim3(kAttnWaves * 64), 0, stream, L,
-                               (const uint16_t*)io.q, partials, (uint16_t*)io.out, nsplit, bps, scale_log2);
-    } else {
-        const int tps = bps * 32;
-        if (L.D == 128)
-            hipLaunchKernelGGL(k_attn_f32<128>, grid, dim3(64), 0, stream, L, (const float*)io.q,
-                               partials, (float*)io.out, nsplit, tps, scale_log2);
-        else
-            hipLaunchKernelGGL(k_attn_f32<64>, grid, dim3(64), 0, stream, L, (const float*)io.q,
-                               partials, (float*)io.out, nsplit, tps, scale_log2);
-    }
-    return hipGetLastError();
-}
-
-hipError_t launch_merge(const LayerView& L, const StepIO& io, int nsplit, const float* partials,
-                        hipStream_t stream) {
+hipError_t launch_epilogue(const LayerView& L, const StepIO& io, double r, hipStream_t stream) {
+    const size_t shm = (size_t)L.S * (8 + 12);
     if (L.bf16)
-        hipLaunchKernelGGL(k_merge<uint16_t>, dim3(L.U), dim3(256), 0, stream, L, partials,
-                           (uint16_t*)io.out, nsplit);
+        hipLaunchKernelGGL(k_epilogue<uint16_t>, dim3(L.U), dim3(256), shm, stream, L, io, r);
     else
-        hipLaunchKernelGGL(k_merge<float>, dim3(L.U), dim3(256), 0, stream, L, partials,
-                           (float*)io.out, nsplit);
-    return hipGetLastError();
-}
-
-hipError_t launch_score(const LayerView& L, const StepIO& io, double r, hipStream_t stream) {
-    const size_t shm = (size_t)L.G * L.D * sizeof(double) + (size_t)L.S * (sizeof(double) + 2 * sizeof(int));
-    if (L.bf16) {
-        if (L.D == 128)
-            hipLaunchKernelGGL((k_score<uint16_t, 128>), dim3(L.U), dim3(256), shm, stream, L,
-                               (const uint16_t*)io.q, io, r);
-        else
-            hipLaunchKernelGGL((k_score<uint16_t, 64>), dim3(L.U), dim3(256), shm, stream, L,
-                               (const uint16_t*)io.q, io, r);
-    } else {
-        if (L.D == 128)
-            hipLaunchKernelGGL((k_score<float, 128>), dim3(L.U), dim3(256), shm, stream, L,
-                               (const float*)io.q, io, r);
-        else
-            hipLaunchKernelGGL((k_score<float, 64>), dim3(L.U), dim3(256), shm, stream, L,
-                               (const float*)io.q, io, r);
-    }
+        hipLaunchKernelGGL(k_epilogue<float>, dim3(L.U), dim3(256), shm, stream, L, io, r);
     return hipGetLastError();
 }
 

@@ -34,7 +34,7 @@ raas_status hip_fail(hipError_t e, const char* what) {
     return fail(RAAS_E_HIP, "%s: %s", what, hipGetErrorString(e));
 }
 
-constexpr int kKernels = 4;  // append, attention, merge, score
+constexpr int kKernels = 2;  // step kernel, epilogue kernel
 constexpr size_t kProfRing = 8192;
 
 struct Timing {
@@ -55,9 +55,10 @@ struct raas_pool {
     void* kmin = nullptr;
     void* kmax = nullptr;
     int32_t* meta = nullptr;  // lid, ts, state, fill: 4 x [Ly][U][S]
-    int32_t* unit = nullptr;  // [Ly][U][4]
+    int32_t* unit = nullptr;  // [Ly][U][kUnitFields]
     int32_t* err = nullptr;
-    float* part = nullptr;
+    float* part = nullptr;    // [U][splits][G][D+2], scratch of one step
+    double* score = nullptr;  // [U][S], scratch of one step
     size_t bytes = 0;
     std::vector<unsigned char> prefilled;
     int split_override = 0;
@@ -82,8 +83,12 @@ LayerView view(const raas_pool* p, int layer) {
     L.ts = p->meta + all_meta + meta;
     L.state = p->meta + 2 * all_meta + meta;
     L.fill = p->meta + 3 * all_meta + meta;
-    L.unit = p->unit + (size_t)layer * p->U * 4;
+    L.unit = p->unit + (size_t)layer * p->U * kUnitFields;
     L.err = p->err;
+    L.score = p->score;
+    L.part = p->part;
+    L.nsplit = 1;
+    L.bps = p->Lcap / kBlockTokens;
     L.U = p->U;
     L.G = p->G;
     L.D = p->D;
@@ -131,26 +136,6 @@ raas_status check_layer(const raas_pool* p, int32_t layer) {
     if (layer < 0 || layer >= p->cfg.n_layers)
         return fail(RAAS_E_INVALID, "layer %d out of range [0, %d)", layer, p->cfg.n_layers);
     return RAAS_OK;
-}
-
-void split_plan(const raas_pool* p, int& nsplit, int& bps) {
-    const int nblk = p->Lcap / kBlockTokens;
-    int want;
-    if (p->split_override > 0) {
-        want = p->split_override;
-    } else if (p->cfg.dtype == RAAS_F32) {
-        want = (nblk + 1) / 2;  // about 64 tokens per wavefront
-    } else {
-        // aim at ~8 wavefronts per CU over 256 CUs, kAttnWaves per workgroup
-        const double target_waves = 2048.0;
-        const double per_wave = fmax(1.0, (double)p->U * nblk / target_waves);
-        want = (int)ceil(nblk / (kAttnWaves * per_wave));
-    }
-    want = want < 1 ? 1 : want;
-    want = want > kMaxSplits ? kMaxSplits : want;
-    want = want > nblk ? nblk : want;
-    bps = (nblk + want - 1) / want;
-    nsplit = (nblk + bps - 1) / bps;  // no empty split
 }
 
 void prof_record(raas_pool* p, int k, bool start, hipStream_t s) {
@@ -222,9 +207,10 @@ raas_status raas_create_pool(const raas_config* cfg, void* stream, raas_pool** o
         {&p->kmin, Ly * p->rep_layer_elems * p->esz},
         {&p->kmax, Ly * p->rep_layer_elems * p->esz},
         {(void**)&p->meta, 4 * Ly * p->meta_layer_elems * sizeof(int32_t)},
-        {(void**)&p->unit, Ly * p->U * 4 * sizeof(int32_t)},
+        {(void**)&p->unit, Ly * p->U * kUnitFields * sizeof(int32_t)},
         {(void**)&p->err, 256},
         {(void**)&p->part, (size_t)p->U * max_split * p->G * (p->D + 2) * sizeof(float)},
+        {(void**)&p->score, (size_t)p->U * p->S * sizeof(double)},
     };
     hipStream_t s = (hipStream_t)stream;
     for (auto& r : reqs) {
@@ -260,7 +246,7 @@ void raas_destroy(raas_pool* p) {
         for (auto ev : t.start) hipEventDestroy(ev);
         for (auto ev : t.stop) hipEventDestroy(ev);
     }
-    void* ptrs[] = {p->K, p->V, p->kmin, p->kmax, p->meta, p->unit, p->err, p->part};
+    void* ptrs[] = {p->K, p->V, p->kmin, p->kmax, p->meta, p->unit, p->err, p->part, p->score};
     for (void* q : ptrs)
         if (q) hipFree(q);
     delete p;
@@ -296,33 +282,23 @@ raas_status raas_decode_step(raas_pool* p, int32_t layer, const void* q, const v
     if (st != RAAS_OK) return st;
     if (!q || !k_new || !v_new || !out) return fail(RAAS_E_INVALID, "q, k_new, v_new and out must be non-NULL");
     if (!p->prefilled[layer]) return fail(RAAS_E_STATE, "layer %d has not been prefilled", layer);
-    const LayerView L = view(p, layer);
+    LayerView L = view(p, layer);
     StepIO io{q, k_new, v_new, out, page_table_out, timestamps_out, evicted_out};
     hipStream_t s = (hipStream_t)stream;
-    int nsplit, bps;
-    split_plan(p, nsplit, bps);
+    const StepPlan pl = plan_step(p->U, p->G, p->D, p->S, p->Lcap, p->cfg.dtype == RAAS_BF16, p->split_override);
+    L.nsplit = pl.nsplit;
+    L.bps = pl.bps;
 
     prof_record(p, 0, true, s);
-    hipError_t e = launch_append(L, io, s);
+    hipError_t e = launch_step(L, io, pl, (double)p->cfg.r, s);
     prof_record(p, 0, false, s);
-    if (e != hipSuccess) return hip_fail(e, "append launch");
-
-    prof_record(p, 1, true, s);
-    e = launch_attention(L, io, nsplit, bps, p->part, s);
-    prof_record(p, 1, false, s);
-    if (e != hipSuccess) return hip_fail(e, "attention launch");
-
-    if (nsplit > 1) {
-        prof_record(p, 2, true, s);
-        e = launch_merge(L, io, nsplit, p->part, s);
-        prof_record(p, 2, false, s);
-        if (e != hipSuccess) return hip_fail(e, "merge launch");
+    if (e != hipSuccess) return hip_fail(e, "step launch");
+    if (!pl.fused) {
+        prof_record(p, 1, true, s);
+        e = launch_epilogue(L, io, (double)p->cfg.r, s);
+        prof_record(p, 1, false, s);
+        if (e != hipSuccess) return hip_fail(e, "epilogue launch");
     }
-
-    prof_record(p, 3, true, s);
-    e = launch_score(L, io, (double)p->cfg.r, s);
-    prof_record(p, 3, false, s);
-    if (e != hipSuccess) return hip_fail(e, "score launch");
     p->last_stream = s;
     return RAAS_OK;
 }
@@ -342,8 +318,8 @@ raas_status raas_export_state(raas_pool* p, int32_t layer, int32_t* host_buf, si
         hipError_t e = hipMemcpyAsync(host_buf + i * us, src[i], us * sizeof(int32_t), hipMemcpyDeviceToHost, s);
         if (e != hipSuccess) return hip_fail(e, "hipMemcpyAsync");
     }
-    hipError_t e = hipMemcpyAsync(host_buf + 4 * us, L.unit, (size_t)p->U * 4 * sizeof(int32_t),
-                                  hipMemcpyDeviceToHost, s);
+    std::vector<int32_t> unit((size_t)p->U * kUnitFields);
+    hipError_t e = hipMemcpyAsync(unit.data(), L.unit, unit.size() * sizeof(int32_t), hipMemcpyDeviceToHost, s);
     if (e != hipSuccess) return hip_fail(e, "hipMemcpyAsync");
     int32_t errflag = 0;
     e = hipMemcpyAsync(&errflag, p->err, sizeof(int32_t), hipMemcpyDeviceToHost, s);
@@ -351,6 +327,8 @@ raas_status raas_export_state(raas_pool* p, int32_t layer, int32_t* host_buf, si
     e = hipStreamSynchronize(s);
     if (e != hipSuccess) return hip_fail(e, "hipStreamSynchronize");
     if (errflag) return fail(RAAS_E_HIP, "device reported an internal inconsistency (flag %d)", errflag);
+    for (int u = 0; u < p->U; ++u)
+        for (int f = 0; f < 4; ++f) host_buf[4 * us + 4 * (size_t)u + f] = unit[(size_t)u * kUnitFields + f];
     return RAAS_OK;
 }
 
