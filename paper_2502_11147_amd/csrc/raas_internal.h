@@ -16,15 +16,16 @@ enum SlotState : int32_t { kFree = 0, kPinned = 1, kEvictable = 2 };
 //  evicted   logical id evicted by the last step, or -1
 //  next_slot slot the next token goes to (the tail, or the lowest free slot)
 //  next_fill its position in that page (0: the page is opened by that token)
-enum UnitField : int { kTail = 0, kNextLid = 1, kClock = 2, kEvicted = 3, kNextSlot = 4, kNextFill = 5 };
+//  pinned    number of pinned prefill pages (slots 0 .. pinned-1)
+enum UnitField : int { kTail = 0, kNextLid = 1, kClock = 2, kEvicted = 3, kNextSlot = 4, kNextFill = 5, kPinnedPages = 6 };
 constexpr int kUnitFields = 8;
 
 // Tokens of one attention block: two 16-row MFMA tiles.
 constexpr int kBlockTokens = 32;
 // Upper bound on attention splits per unit (sizes the partials buffer).
 constexpr int kMaxSplits = 64;
-// LDS a step workgroup may use.
-constexpr size_t kMaxLds = 60 * 1024;
+// Dynamic LDS a step workgroup may use (gfx950 has 160 KiB per workgroup).
+constexpr size_t kMaxLds = 144 * 1024;
 
 // One layer of the pool, as the kernels see it. Unit u = seq * n_kv_heads + kv_head.
 struct LayerView {
@@ -63,7 +64,9 @@ struct StepPlan {
     size_t lds;      // dynamic LDS of the step kernel
 };
 
-StepPlan plan_step(int U, int G, int D, int S, int Lcap, bool bf16, int split_override);
+StepPlan plan_step(int U, int G, int D, int S, int Lcap, int ps, int pinned, bool bf16, int split_override);
+// Lets the step kernels use more than the default dynamic LDS.
+hipError_t allow_large_lds();
 
 // Launchers (asynchronous on `stream`; return the launch status).
 hipError_t launch_prefill(const LayerView& L, const void* k, const void* v, int P, int keep_pages,

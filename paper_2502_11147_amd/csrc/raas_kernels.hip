@@ -22,6 +22,8 @@
 // is fp32, the epilogue is a second kernel that also merges the splits.
 #include <math.h>
 
+#include <algorithm>
+
 #include "raas_internal.h"
 
 namespace raas {
@@ -106,6 +108,7 @@ __global__ void k_prefill_meta(LayerView L, int P, int keep_pages) {
         U4[kEvicted] = -1;
         U4[kNextSlot] = keep_pages;  // lowest free slot; decode starts a fresh page
         U4[kNextFill] = 0;
+        U4[kPinnedPages] = keep_pages;
     }
 }
 
@@ -169,23 +172,27 @@ __global__ void k_prefill_f32(LayerView L, const float* __restrict__ k, const fl
 //  - The next token's target: the tail page if it has room, else the lowest
 //    free slot (a fresh page).
 
-struct EpiShared {
-    int cnt_ev, cnt_free, min_free, victim;
-    unsigned long long min_key;
+// The unit record as read once at the start of a step.
+struct UnitRec {
+    int ns, nf, clock, next_lid;
+    __device__ bool opened() const { return nf == 0; }
 };
 
-__device__ void load_slots(const LayerView& L, int u, double* s_score, int* s_state, int* s_ts, int* s_lid) {
+__device__ __forceinline__ UnitRec read_unit(const LayerView& L, int u) {
+    const int32_t* U4 = L.unit + (size_t)u * kUnitFields;
+    return UnitRec{U4[kNextSlot], U4[kNextFill], U4[kClock], U4[kNextLid]};
+}
+
+__device__ void load_slots(const LayerView& L, int u, const UnitRec& ur, double* s_score, int* s_state,
+                           int* s_ts, int* s_lid) {
     const int S = L.S;
     const size_t base = (size_t)u * S;
-    const int32_t* U4 = L.unit + (size_t)u * kUnitFields;
-    const int ns = U4[kNextSlot];
-    const bool opened = U4[kNextFill] == 0;
     for (int s = threadIdx.x; s < S; s += blockDim.x) {
         int st = L.state[base + s], t = L.ts[base + s], id = L.lid[base + s];
-        if (s == ns && opened) {
+        if (s == ur.ns && ur.opened()) {
             st = kEvictable;
-            t = U4[kClock];
-            id = U4[kNextLid];
+            t = ur.clock;
+            id = ur.next_lid;
         }
         s_state[s] = st;
         s_ts[s] = t;
@@ -194,150 +201,52 @@ __device__ void load_slots(const LayerView& L, int u, double* s_score, int* s_st
     }
 }
 
-__device__ void retention(const LayerView& L, const StepIO& io, int u, double r, const double* s_score,
-                          int* s_state, int* s_ts, const int* s_lid, EpiShared& e) {
-    const int S = L.S, ps = L.ps, tid = threadIdx.x, nt = blockDim.x;
-    const size_t base = (size_t)u * S;
-    int32_t* U4 = L.unit + (size_t)u * kUnitFields;
-    const int clock = U4[kClock], ns = U4[kNextSlot], nf = U4[kNextFill], next_lid = U4[kNextLid];
-    const bool opened = nf == 0;
-    if (tid == 0) {
-        e.cnt_ev = 0;
-        e.cnt_free = 0;
-        e.min_free = S;
-        e.victim = -1;
-        e.min_key = ~0ull;
-    }
-    __syncthreads();
-    int ev = 0, fr = 0;
-    for (int s = tid; s < S; s += nt) {
-        ev += (s_state[s] == kEvictable);
-        fr += (s_state[s] == kFree);
-    }
-    if (ev) atomicAdd(&e.cnt_ev, ev);
-    if (fr) atomicAdd(&e.cnt_free, fr);
-    __syncthreads();
-    const int n = e.cnt_ev, nfree = e.cnt_free;
-    const int k = (int)floor(r * (double)n);
-    if (k > 0) {
-        // gsz consecutive threads rank one page; non-evictable slots score +inf
-        int gsz = 1;
-        while (gsz < 16 && gsz * 2 * S <= nt) gsz *= 2;
-        const int sub = tid & (gsz - 1);
-        const int rounds = (S * gsz + nt - 1) / nt;
-        for (int rd = 0; rd < rounds; ++rd) {
-            const int p = (rd * nt + tid) / gsz;
-            const double sp = p < S ? s_score[p] : -INFINITY;
-            int less = 0;
-#pragma unroll 8
-            for (int o = sub; o < S; o += gsz) less += s_score[o] < sp;
-            for (int off = 1; off < gsz; off <<= 1) less += __shfl_xor(less, off);
-            if (p < S && sub == 0 && s_state[p] == kEvictable && less >= n - k) s_ts[p] = clock;
-        }
-    }
-    __syncthreads();
-    const int fill_tail = nf + 1;
-    const bool full = (fill_tail == ps) && nfree == 0;
-    if (full) {
-        unsigned long long best = ~0ull;
-        for (int s = tid; s < S; s += nt) {
-            if (s_state[s] != kEvictable) continue;
-            const unsigned long long key = ((unsigned long long)(uint32_t)s_ts[s] << 32) | (uint32_t)s_lid[s];
-            best = key < best ? key : best;
-        }
-        if (best != ~0ull) atomicMin(&e.min_key, best);
-        __syncthreads();
-        for (int s = tid; s < S; s += nt) {
-            if (s_state[s] == kEvictable && (uint32_t)s_lid[s] == (uint32_t)(e.min_key & 0xFFFFFFFFull))
-                e.victim = s;
-        }
-        __syncthreads();
-    }
-    const int victim = e.victim;
-    const int evicted = victim >= 0 ? s_lid[victim] : -1;
-    if (full && victim < 0 && tid == 0) atomicOr(L.err, 2);
-    const bool tail_gone = victim == ns;
-    const int tail_fill = tail_gone ? 0 : fill_tail;
-    const bool need_free = tail_gone || tail_fill == ps;
-    if (need_free) {
-        int lo = S;
-        for (int s = tid; s < S; s += nt)
-            if (s_state[s] == kFree || s == victim) lo = min(lo, s);
-        if (lo < S) atomicMin(&e.min_free, lo);
-    }
-    __syncthreads();
-    const int next_slot = need_free ? e.min_free : ns;
-    if (need_free && next_slot >= S && tid == 0) atomicOr(L.err, 4);
-    for (int s = tid; s < S; s += nt) {
-        const bool gone = s == victim;
-        const int st = gone ? kFree : s_state[s];
-        const int t = gone ? -1 : s_ts[s];
-        const int id = gone ? -1 : s_lid[s];
-        L.state[base + s] = st;
-        L.ts[base + s] = t;
-        if (s == ns || gone) {
-            L.lid[base + s] = id;
-            L.fill[base + s] = gone ? 0 : fill_tail;
-        }
-        if (io.page_table_out) io.page_table_out[base + s] = (st == kFree) ? -1 : id;
-        if (io.timestamps_out) io.timestamps_out[base + s] = (st == kEvictable) ? t : -1;
-    }
-    if (tid == 0) {
-        U4[kTail] = tail_gone ? -1 : ns;
-        U4[kNextLid] = next_lid + (opened ? 1 : 0);
-        U4[kClock] = clock + 1;
-        U4[kEvicted] = evicted;
-        U4[kNextSlot] = next_slot < S ? next_slot : 0;
-        U4[kNextFill] = need_free ? 0 : tail_fill;
-        if (io.evicted_out) io.evicted_out[u] = evicted;
-    }
-}
-
 // ---------------------------------------------------------------------------
 // Page scores (Section 3.3, Quest's representative keys): for each evictable
 // page, max over the G query heads of sum_c max(q_c*kmax_c, q_c*kmin_c), in
 // fp64. With q+ = max(q, 0) and q- = min(q, 0) the selected product is
 // q+*kmax + q-*kmin, one of the two terms being an exact zero; products of
-// bf16 or fp32 values are exact in fp64, so each fused multiply-add rounds
-// exactly as an add of the exact product. Four lanes per page: each sums
-// D/4 consecutive channels in order, the quarters combine through a fixed
-// xor tree, so equal pages score equal. The page the step writes to has its
-// min/max widened by the new key here, and stored back.
+// bf16 values are exact in fp64, so each fused multiply-add rounds exactly as
+// an add of the exact product. Eight lanes per page: lane part p sums D/8
+// consecutive channels in order, the eight parts combine through a fixed xor
+// tree, so equal pages score equal. A wavefront scores 8 pages per pass; its
+// passes are interleaved with its attention blocks, each pass's keys loading
+// while the previous block computes. The page the step writes to has its
+// min/max widened by the new key and stored back.
 
 template <int D>
 struct ScoreFrag {
-    u32x4 kx[D / 32], kn[D / 32];  // D/4 bf16 channels of kmax and kmin
+    static constexpr int SV = D / 64;  // 16-byte vectors per array per lane (D/8 bf16 channels)
+    u32x4 kx[SV], kn[SV];
 };
 
 template <int D>
-__device__ __forceinline__ void score_load(const LayerView& L, int u, int p, int qtr, bool act,
-                                           ScoreFrag<D>& f) {
-    const size_t off = ((size_t)u * L.S + p) * D + qtr * (D / 4);
+__device__ __forceinline__ void score_issue(const LayerView& L, int u, int p, int part, bool load,
+                                            ScoreFrag<D>& f) {
+    const size_t off = ((size_t)u * L.S + p) * D + part * (D / 8);
     const uint16_t* kx = (const uint16_t*)L.kmax + off;
     const uint16_t* kn = (const uint16_t*)L.kmin + off;
 #pragma unroll
-    for (int i = 0; i < D / 32; ++i) {
-        f.kx[i] = act ? ld4(kx + 8 * i) : u32x4{0u, 0u, 0u, 0u};
-        f.kn[i] = act ? ld4(kn + 8 * i) : u32x4{0u, 0u, 0u, 0u};
+    for (int i = 0; i < ScoreFrag<D>::SV; ++i) {
+        f.kx[i] = load ? ld4(kx + 8 * i) : u32x4{0u, 0u, 0u, 0u};
+        f.kn[i] = load ? ld4(kn + 8 * i) : u32x4{0u, 0u, 0u, 0u};
     }
 }
 
 template <int D>
-__device__ __forceinline__ double score_compute(const LayerView& L, int u, int p, int qtr, bool act,
-                                                ScoreFrag<D>& f, bool is_tail, bool opened,
-                                                const uint16_t* __restrict__ k_new, const double* s_qp,
-                                                const double* s_qn) {
+__device__ __forceinline__ double score_finish(const LayerView& L, int u, int p, int part, bool act,
+                                               ScoreFrag<D>& f, bool is_tail, bool opened,
+                                               const uint16_t* __restrict__ k_new, const double2* q2) {
+    constexpr int SV = ScoreFrag<D>::SV;
     const int G = L.G;
     if (act && is_tail) {
-        const uint16_t* kn_src = k_new + qtr * (D / 4);
 #pragma unroll
-        for (int i = 0; i < D / 32; ++i) {
-            const u32x4 x = ld4(kn_src + 8 * i);
+        for (int i = 0; i < SV; ++i) {
+            const u32x4 x = ld4(k_new + part * (D / 8) + 8 * i);
             if (opened) {
                 f.kx[i] = x;
                 f.kn[i] = x;
             } else {
-                u32x4 mx, mn;
 #pragma unroll
                 for (int h = 0; h < 4; ++h) {
                     uint32_t a = 0, b = 0;
@@ -349,66 +258,204 @@ __device__ __forceinline__ double score_compute(const LayerView& L, int u, int p
                         a |= (uint32_t)(bf2f(xv) > bf2f(hv) ? xv : hv) << (16 * half);
                         b |= (uint32_t)(bf2f(xv) < bf2f(lv) ? xv : lv) << (16 * half);
                     }
-                    mx[h] = a;
-                    mn[h] = b;
+                    f.kx[i][h] = a;
+                    f.kn[i][h] = b;
                 }
-                f.kx[i] = mx;
-                f.kn[i] = mn;
             }
-            const size_t off = ((size_t)u * L.S + p) * D + qtr * (D / 4) + 8 * i;
+            const size_t off = ((size_t)u * L.S + p) * D + part * (D / 8) + 8 * i;
             st4((uint16_t*)L.kmax + off, f.kx[i]);
             st4((uint16_t*)L.kmin + off, f.kn[i]);
         }
     }
-    const int c0 = qtr * (D / 4);
+    const int c0 = part * (D / 8);
     double best = -INFINITY;
 #pragma unroll 1
     for (int j = 0; j < G; ++j) {
-        const double* qp = s_qp + (size_t)j * D + c0;
-        const double* qn = s_qn + (size_t)j * D + c0;
+        const double2* qj = q2 + (size_t)j * D + c0;
         double a = 0.0;
+        // the keys stay packed: widening them once for all heads would need 4x the registers
 #pragma unroll
-        for (int i = 0; i < D / 32; ++i) {
+        for (int i = 0; i < SV; ++i) asm volatile("" : "+v"(f.kx[i]), "+v"(f.kn[i]));
+#pragma unroll
+        for (int i = 0; i < SV; ++i) {
+            __builtin_amdgcn_sched_barrier(0);  // keep each octet's q reads next to their use
 #pragma unroll
             for (int e = 0; e < 8; ++e) {
-                a = fma(qp[8 * i + e], (double)bf2f(u16_at(f.kx[i], e)), a);
-                a = fma(qn[8 * i + e], (double)bf2f(u16_at(f.kn[i], e)), a);
+                const double2 qq = qj[8 * i + e];
+                a = fma(qq.x, (double)bf2f(u16_at(f.kx[i], e)), a);
+                a = fma(qq.y, (double)bf2f(u16_at(f.kn[i], e)), a);
             }
         }
         a += __shfl_xor(a, 1);
         a += __shfl_xor(a, 2);
+        a += __shfl_xor(a, 4);
         best = a > best ? a : best;
     }
     return best;
 }
 
+// Results of the retention policy for one step, computed by the retention
+// wavefront and applied to the pool once the attention has read it.
+struct RetShared {
+    int victim, evicted, next_slot, next_fill, tail_after, errs;
+};
+
+// Retention policy of one unit, run by one wavefront (Algorithm 1,
+// store_cache; Sections 3.2-3.3) on the slot state in LDS, the opened page
+// already marked evictable and s_score holding every evictable page's score
+// (+inf elsewhere):
+//  - top-r refresh: with n evictable pages and k = floor(r*n), page p gets
+//    ts = clock when at least n-k evictable pages score strictly less, i.e.
+//    exactly the pages above the (n-k)-th smallest score;
+//  - eviction ("if kvm.is_full(): evict KVs with the oldest timestamps"):
+//    when the tail page is full and no slot is free, the evictable page with
+//    the smallest (timestamp, logical id) is freed;
+//  - the next token's target: the tail page if it has room, else the lowest
+//    free slot (a fresh page).
+__device__ void retention_wave(const LayerView& L, const UnitRec& ur, double r, const double* s_score,
+                               int* s_state, int* s_ts, const int* s_lid, RetShared& out) {
+    const int S = L.S, ps = L.ps, lane = threadIdx.x & 63;
+    int n = 0, nfree = 0;
+    for (int s0 = 0; s0 < S; s0 += 64) {
+        const int s = s0 + lane;
+        const int st = s < S ? s_state[s] : -1;
+        n += __popcll(__ballot(st == kEvictable));
+        nfree += __popcll(__ballot(st == kFree));
+    }
+    const int k = (int)floor(r * (double)n);
+    if (k > 0) {
+        for (int s0 = 0; s0 < S; s0 += 64) {
+            const int p = s0 + lane;
+            if (p < S && s_state[p] == kEvictable) {
+                const double sp = s_score[p];
+                int less = 0;
+#pragma unroll 8
+                for (int o = 0; o < S; ++o) less += s_score[o] < sp;
+                if (less >= n - k) s_ts[p] = ur.clock;
+            }
+        }
+    }
+    const int fill_tail = ur.nf + 1;
+    const bool full = fill_tail == ps && nfree == 0;
+    int victim = -1;
+    if (full) {
+        unsigned long long best = ~0ull;
+        for (int s0 = 0; s0 < S; s0 += 64) {
+            const int s = s0 + lane;
+            if (s < S && s_state[s] == kEvictable) {
+                const unsigned long long key = ((unsigned long long)(uint32_t)s_ts[s] << 32) | (uint32_t)s_lid[s];
+                best = key < best ? key : best;
+            }
+        }
+#pragma unroll
+        for (int off = 32; off >= 1; off >>= 1) {
+            const unsigned long long o = __shfl_xor(best, off);
+            best = o < best ? o : best;
+        }
+        for (int s0 = 0; s0 < S; s0 += 64) {
+            const int s = s0 + lane;
+            const bool hit = s < S && s_state[s] == kEvictable &&
+                             (uint32_t)s_lid[s] == (uint32_t)(best & 0xFFFFFFFFull);
+            const unsigned long long m = __ballot(hit);
+            if (m) {
+                victim = s0 + __builtin_ctzll(m);
+                break;
+            }
+        }
+    }
+    const bool tail_gone = victim == ur.ns;
+    const int tail_fill = tail_gone ? 0 : fill_tail;
+    const bool need_free = tail_gone || tail_fill == ps;
+    int next_slot = ur.ns;
+    if (need_free) {
+        next_slot = S;
+        for (int s0 = 0; s0 < S; s0 += 64) {
+            const int s = s0 + lane;
+            const unsigned long long m = __ballot(s < S && (s_state[s] == kFree || s == victim));
+            if (m) {
+                next_slot = s0 + __builtin_ctzll(m);
+                break;
+            }
+        }
+    }
+    if (lane == 0) {
+        out.victim = victim;
+        out.evicted = victim >= 0 ? s_lid[victim] : -1;
+        out.next_slot = next_slot < S ? next_slot : 0;
+        out.next_fill = need_free ? 0 : tail_fill;
+        out.tail_after = tail_gone ? -1 : ur.ns;
+        out.errs = (full && victim < 0 ? 2 : 0) | (need_free && next_slot >= S ? 4 : 0);
+    }
+    if (victim >= 0 && lane == 0) {
+        s_state[victim] = kFree;
+        s_ts[victim] = -1;
+    }
+}
+
+// Writes the step's retention results to the pool and the optional outputs.
+__device__ void retention_store(const LayerView& L, const StepIO& io, int u, const UnitRec& ur,
+                                const int* s_state, const int* s_ts, const int* s_lid, const RetShared& rs,
+                                int first, int stride) {
+    const int S = L.S;
+    const size_t base = (size_t)u * S;
+    for (int s = first; s < S; s += stride) {
+        const bool gone = s == rs.victim;
+        const int st = s_state[s];
+        const int id = gone ? -1 : s_lid[s];
+        if (st == kEvictable || gone) L.ts[base + s] = s_ts[s];
+        if (s == ur.ns || gone) {
+            L.state[base + s] = st;
+            L.lid[base + s] = id;
+            L.fill[base + s] = gone ? 0 : ur.nf + 1;
+        }
+        if (io.page_table_out) io.page_table_out[base + s] = (st == kFree) ? -1 : id;
+        if (io.timestamps_out) io.timestamps_out[base + s] = (st == kEvictable) ? s_ts[s] : -1;
+    }
+    if (first == 0) {
+        int32_t* U4 = L.unit + (size_t)u * kUnitFields;
+        U4[kTail] = rs.tail_after;
+        U4[kNextLid] = ur.next_lid + (ur.opened() ? 1 : 0);
+        U4[kClock] = ur.clock + 1;
+        U4[kEvicted] = rs.evicted;
+        U4[kNextSlot] = rs.next_slot;
+        U4[kNextFill] = rs.next_fill;
+        if (io.evicted_out) io.evicted_out[u] = rs.evicted;
+        if (rs.errs) atomicOr(L.err, rs.errs);
+    }
+}
+
 // ---------------------------------------------------------------------------
-// Step kernel, bf16 pools: attention over every resident token (Algorithm 1,
-// attention(Q, K_old::K_new, V_old::V_new)), split-K over 32-token blocks.
-// One workgroup of NW wavefronts per (unit, split); each wavefront holds the
-// unit's whole GQA query group and walks blocks round-robin. Per block: QK^T
-// as two 16x16x32 bf16 MFMA tiles per 32 channels (rows = tokens, columns =
-// query heads, G <= 16 of the 16 used), online softmax in base 2 with one
+// Step kernel, bf16 pools. One workgroup of NW wavefronts per (unit, split).
+//
+// Attention (Algorithm 1, attention(Q, K_old::K_new, V_old::V_new)) over
+// every resident token, split-K over 32-token blocks. Each wavefront holds
+// the unit's whole GQA query group and walks blocks round-robin, loading the
+// next block while it computes the current one. Per block: QK^T as two
+// 16x16x32 bf16 MFMA tiles per 32 channels (rows = tokens, columns = query
+// heads, G <= 16 of the 16 used), online softmax in base 2 with one
 // cross-lane max per block, and PV as D/16 MFMAs of V^T (rows = channels)
 // times P^T (columns = heads). A lane owns one head (its column) in both
 // products, so no data moves between lanes except the block max. The new
 // token is not in the pool when the block is read: its K/V come from the
-// step's inputs, substituted in registers, and the wavefront 0 of the
-// owning workgroup stores it.
+// step's inputs, substituted in registers, and the owning wavefront stores
+// it. Page-score passes ride along with the blocks. When one workgroup
+// covers the unit (fused), wavefront 0 runs the retention policy while the
+// others merge the wavefronts' partial outputs, and the state goes out only
+// after the attention has read the pool.
 
 template <int D, int NW>
-__global__ __launch_bounds__(NW * 64) void k_step_bf16(LayerView L, StepIO io, float scale_log2, double r,
+__global__ __launch_bounds__(NW * 64) __attribute__((amdgpu_waves_per_eu(1, 2))) void k_step_bf16(
+    LayerView L, StepIO io, float scale_log2, double r,
                                                        int fused) {
     constexpr int KS = D / 32, NB = D / 16, BLK = 32 * D;
     extern __shared__ __align__(16) unsigned char smem[];
     __shared__ float s_m[NW][16];
     __shared__ float s_l[NW][16];
-    __shared__ EpiShared epi;
+    __shared__ RetShared ret;
 
     const int G = L.G, S = L.S, ps = L.ps;
-    double* s_qp = reinterpret_cast<double*>(smem);      // [G][D]
-    double* s_qn = s_qp + (size_t)G * D;                  // [G][D]
-    float* s_o = reinterpret_cast<float*>(s_qn + (size_t)G * D);  // [NW][G][D+4]
+    double2* s_q2 = reinterpret_cast<double2*>(smem);  // [G][D] (q+, q-)
+    float* s_o = reinterpret_cast<float*>(s_q2 + (size_t)G * D);  // [NW][G][D+4]
     double* s_score = reinterpret_cast<double*>(s_o + (size_t)NW * G * (D + 4));  // [S], fused only
     int* s_state = reinterpret_cast<int*>(s_score + S);  // [S], fused only
     int* s_ts = s_state + S;
@@ -419,38 +466,22 @@ __global__ __launch_bounds__(NW * 64) void k_step_bf16(LayerView L, StepIO io, f
     const int nsplit = L.nsplit;
     const int u = blockIdx.x / nsplit, split = blockIdx.x - (blockIdx.x / nsplit) * nsplit;
     const size_t base = (size_t)u * S;
-    const int32_t* U4 = L.unit + (size_t)u * kUnitFields;
-    const int ns = U4[kNextSlot], nf = U4[kNextFill];
-    const bool opened = nf == 0;
+    const UnitRec ur = read_unit(L, u);
+    const int ns = ur.ns, nf = ur.nf;
+    const bool opened = ur.opened();
+    const int pinned = L.unit[(size_t)u * kUnitFields + kPinnedPages];
     const int row_new = ns * ps + nf, b_new = row_new >> 5, tt_new = row_new & 31;
     const int nblk = L.Lcap / 32;
     const int b0 = split * L.bps;
     const int b1 = min(nblk, b0 + L.bps);
-    const int sl0 = min(S, (32 * b0 + ps - 1) / ps), sl1 = min(S, (32 * b1 + ps - 1) / ps);
+    // pages scored here: those whose first row lies in this workgroup's blocks, pinned ones excepted
+    const int sl0 = max(pinned, min(S, (32 * b0 + ps - 1) / ps)), sl1 = min(S, (32 * b1 + ps - 1) / ps);
     const uint16_t* qg = (const uint16_t*)io.q + (size_t)u * G * D;
     const uint16_t* kn_g = (const uint16_t*)io.k_new + (size_t)u * D;
     const uint16_t* vn_g = (const uint16_t*)io.v_new + (size_t)u * D;
     const uint16_t* Ku = (const uint16_t*)L.K + (size_t)u * L.Lcap * D;
     const uint16_t* Vu = (const uint16_t*)L.V + (size_t)u * L.Lcap * D;
     const int32_t* fu = L.fill + base;
-
-    for (int i = tid; i < G * D; i += NW * 64) {
-        const double x = (double)bf2f(qg[i]);
-        s_qp[i] = x > 0.0 ? x : 0.0;
-        s_qn[i] = x < 0.0 ? x : 0.0;
-    }
-    if (fused) load_slots(L, u, s_score, s_state, s_ts, s_lid);
-
-    bf16x8 qv[KS];
-#pragma unroll
-    for (int ks = 0; ks < KS; ++ks) {
-        const u32x4 x = (col < G) ? ld4(qg + (size_t)col * D + 32 * ks + 8 * grp) : u32x4{0u, 0u, 0u, 0u};
-        qv[ks] = __builtin_bit_cast(bf16x8, x);
-    }
-    float m_run = -INFINITY, l_run = 0.0f;
-    f32x4 acc[NB];
-#pragma unroll
-    for (int nb = 0; nb < NB; ++nb) acc[nb] = f32x4{0.f, 0.f, 0.f, 0.f};
 
     // valid tokens among this lane's 8 rows of block b (they lie in one page: page_size % 8 == 0)
     auto valid_rows = [&](int b) {
@@ -482,6 +513,54 @@ __global__ __launch_bounds__(NW * 64) void k_step_bf16(LayerView L, StepIO io, f
     int b = next_block(b0 + w, nv_next);
     u32x4 kr_next[2][KS], vr_next[NB];
     if (b < b1) load_block(b, kr_next, vr_next);
+
+    // stage (q+, q-) and the slot state
+    for (int i = tid; i < G * D; i += NW * 64) {
+        const double x = (double)bf2f(qg[i]);
+        s_q2[i] = double2{x > 0.0 ? x : 0.0, x < 0.0 ? x : 0.0};
+    }
+    if (fused) load_slots(L, u, ur, s_score, s_state, s_ts, s_lid);
+
+    // score passes of this wavefront: 8 pages each, page = first + (lane >> 3)
+    const int part = lane & 7;
+    auto pass_page = [&](int pass) { return sl0 + 8 * (pass * NW + w) + (lane >> 3); };
+    auto pass_act = [&](int p) { return p < sl1 && (p == ns || L.state[base + p] == kEvictable); };
+    const int npass = (sl1 - sl0 - 8 * w > 0) ? (sl1 - sl0 - 8 * w + 8 * NW - 1) / (8 * NW) : 0;
+    int pass = 0;
+    ScoreFrag<D> frag;
+    bool act_cur = false;
+    if (npass > 0) {
+        const int p = pass_page(0);
+        act_cur = pass_act(p);
+        score_issue<D>(L, u, p, part, act_cur && !(p == ns && opened), frag);
+    }
+    auto score_step = [&]() {
+        const int p = pass_page(pass);
+        const double sc = score_finish<D>(L, u, p, part, act_cur, frag, p == ns, opened, kn_g, s_q2);
+        if (act_cur && part == 0) {
+            if (fused) s_score[p] = sc;
+            else L.score[base + p] = sc;
+        }
+        ++pass;
+        if (pass < npass) {
+            const int pn = pass_page(pass);
+            act_cur = pass_act(pn);
+            score_issue<D>(L, u, pn, part, act_cur && !(pn == ns && opened), frag);
+        }
+    };
+
+    bf16x8 qv[KS];
+#pragma unroll
+    for (int ks = 0; ks < KS; ++ks) {
+        const u32x4 x = (col < G) ? ld4(qg + (size_t)col * D + 32 * ks + 8 * grp) : u32x4{0u, 0u, 0u, 0u};
+        qv[ks] = __builtin_bit_cast(bf16x8, x);
+    }
+    float m_run = -INFINITY, l_run = 0.0f;
+    f32x4 acc[NB];
+#pragma unroll
+    for (int nb = 0; nb < NB; ++nb) acc[nb] = f32x4{0.f, 0.f, 0.f, 0.f};
+    __syncthreads();  // (q+, q-) and the slot state staged
+
     while (b < b1) {
         const int nv = nv_next;
         u32x4 kr[2][KS], vr[NB];
@@ -517,6 +596,11 @@ __global__ __launch_bounds__(NW * 64) void k_step_bf16(LayerView L, StepIO io, f
                     }
                 }
             }
+            // append: store the new token in the pool (Algorithm 1, "Store K_new and V_new")
+            uint16_t* Kw = (uint16_t*)L.K + (size_t)u * L.Lcap * D;
+            uint16_t* Vw = (uint16_t*)L.V + (size_t)u * L.Lcap * D;
+            if (lane < D / 8) st4(Kw + k_off<D>(row_new, lane * 8), ld4(kn_g + lane * 8));
+            for (int c = lane; c < D; c += 64) Vw[v_off<D>(row_new, c)] = vn_g[c];
         }
 
         f32x4 s0 = {0.f, 0.f, 0.f, 0.f}, s1 = {0.f, 0.f, 0.f, 0.f};
@@ -549,24 +633,18 @@ __global__ __launch_bounds__(NW * 64) void k_step_bf16(LayerView L, StepIO io, f
         bf16x8 pb;
 #pragma unroll
         for (int j = 0; j < 8; ++j) {
-            const float p = __builtin_amdgcn_exp2f(x[j] - m_run);
-            psum += p;
-            pb[j] = (__bf16)p;
+            const float pj = __builtin_amdgcn_exp2f(x[j] - m_run);
+            psum += pj;
+            pb[j] = (__bf16)pj;
         }
         l_run += psum;
 #pragma unroll
         for (int nb = 0; nb < NB; ++nb)
             acc[nb] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(__builtin_bit_cast(bf16x8, vr[nb]), pb, acc[nb], 0, 0, 0);
+        if (pass < npass) score_step();  // this block's registers are free again
         b = bn;
     }
-
-    // append: store the new token in the pool (Algorithm 1, "Store K_new and V_new")
-    if (w == 0 && b_new >= b0 && b_new < b1) {
-        uint16_t* Kw = (uint16_t*)L.K + (size_t)u * L.Lcap * D;
-        uint16_t* Vw = (uint16_t*)L.V + (size_t)u * L.Lcap * D;
-        if (lane < D / 8) st4(Kw + k_off<D>(row_new, lane * 8), ld4(kn_g + lane * 8));
-        for (int c = lane; c < D; c += 64) Vw[v_off<D>(row_new, c)] = vn_g[c];
-    }
+    while (pass < npass) score_step();  // passes left when the wavefront ran out of blocks
 
     // park this wavefront's partial attention in LDS
     l_run += __shfl_xor(l_run, 16);
@@ -580,48 +658,41 @@ __global__ __launch_bounds__(NW * 64) void k_step_bf16(LayerView L, StepIO io, f
         for (int nb = 0; nb < NB; ++nb)
             *reinterpret_cast<f32x4*>(&s_o[((size_t)w * G + col) * (D + 4) + 16 * nb + 4 * grp]) = acc[nb];
     }
+    __syncthreads();  // attention done, partials parked, scores in
 
-    // page scores of the slots whose first row lies in this workgroup's blocks
-    __syncthreads();  // s_qp / s_qn staged
-    const int qtr = lane & 3;
-    for (int first = sl0 + 16 * w; first < sl1; first += 16 * NW) {
-        const int p = first + (lane >> 2);
-        const bool act = p < sl1 && (p == ns || L.state[base + p] == kEvictable);
-        ScoreFrag<D> frag;
-        score_load<D>(L, u, p, qtr, act && !(p == ns && opened), frag);
-        const double sc = score_compute<D>(L, u, p, qtr, act, frag, p == ns, opened, kn_g, s_qp, s_qn);
-        if (act && qtr == 0) {
-            if (fused) s_score[p] = sc;
-            else L.score[base + p] = sc;
-        }
-    }
-
-    __syncthreads();
-    for (int idx = tid; idx < G * D; idx += NW * 64) {
-        const int h = idx / D, c = idx - (idx / D) * D;
-        float M = -INFINITY;
+    if (fused && w == 0) retention_wave(L, ur, r, s_score, s_state, s_ts, s_lid, ret);
+    // merge the wavefronts' partial outputs (wavefront 0 joins when not busy with retention)
+    const int m_first = fused ? tid - 64 : tid, m_threads = fused ? (NW - 1) * 64 : NW * 64;
+    if (m_first >= 0) {
+        for (int idx = m_first; idx < G * D; idx += m_threads) {
+            const int h = idx / D, c = idx - (idx / D) * D;
+            float M = -INFINITY;
 #pragma unroll
-        for (int ww = 0; ww < NW; ++ww) M = fmaxf(M, s_m[ww][h]);
-        float O = 0.0f, Ls = 0.0f;
+            for (int ww = 0; ww < NW; ++ww) M = fmaxf(M, s_m[ww][h]);
+            float O = 0.0f, Ls = 0.0f;
 #pragma unroll
-        for (int ww = 0; ww < NW; ++ww) {
-            const float mw = s_m[ww][h];
-            const float wt = (mw == -INFINITY) ? 0.0f : __builtin_amdgcn_exp2f(mw - M);
-            O += wt * s_o[((size_t)ww * G + h) * (D + 4) + c];
-            Ls += wt * s_l[ww][h];
-        }
-        if (fused) {
-            ((uint16_t*)io.out)[((size_t)u * G + h) * D + c] = f2bf(O / Ls);
-        } else {
-            float* pp = L.part + (((size_t)u * nsplit + split) * G + h) * (D + 2);
-            pp[c] = O;
-            if (c == 0) {
-                pp[D] = M;
-                pp[D + 1] = Ls;
+            for (int ww = 0; ww < NW; ++ww) {
+                const float mw = s_m[ww][h];
+                const float wt = (mw == -INFINITY) ? 0.0f : __builtin_amdgcn_exp2f(mw - M);
+                O += wt * s_o[((size_t)ww * G + h) * (D + 4) + c];
+                Ls += wt * s_l[ww][h];
+            }
+            if (fused) {
+                ((uint16_t*)io.out)[((size_t)u * G + h) * D + c] = f2bf(O / Ls);
+            } else {
+                float* pp = L.part + (((size_t)u * nsplit + split) * G + h) * (D + 2);
+                pp[c] = O;
+                if (c == 0) {
+                    pp[D] = M;
+                    pp[D + 1] = Ls;
+                }
             }
         }
     }
-    if (fused) retention(L, io, u, r, s_score, s_state, s_ts, s_lid, epi);
+    if (fused) {
+        __syncthreads();  // retention decided
+        retention_store(L, io, u, ur, s_state, s_ts, s_lid, ret, tid, NW * 64);
+    }
 }
 
 // Step kernel, fp32 pools: one wavefront per (unit, split), one token at a
@@ -741,12 +812,13 @@ __global__ __launch_bounds__(64) void k_step_f32(LayerView L, StepIO io, float s
 }
 
 // Epilogue kernel of the split path: merges the splits' partial attention
-// (out = sum_s 2^(M_s - M) O_s / sum_s 2^(M_s - M) L_s), then refresh,
-// eviction and state out for the unit.
+// (out = sum_s 2^(M_s - M) O_s / sum_s 2^(M_s - M) L_s) while wavefront 0
+// runs the retention policy on the scores the splits wrote; then the state
+// goes out.
 template <typename T>
 __global__ __launch_bounds__(256) void k_epilogue(LayerView L, StepIO io, double r) {
     extern __shared__ __align__(16) unsigned char smem[];
-    __shared__ EpiShared epi;
+    __shared__ RetShared ret;
     const int S = L.S, G = L.G, D = L.D, nsplit = L.nsplit;
     double* s_score = reinterpret_cast<double*>(smem);
     int* s_state = reinterpret_cast<int*>(s_score + S);
@@ -754,11 +826,13 @@ __global__ __launch_bounds__(256) void k_epilogue(LayerView L, StepIO io, double
     int* s_lid = s_ts + S;
     const int u = blockIdx.x;
     const size_t base = (size_t)u * S;
-    load_slots(L, u, s_score, s_state, s_ts, s_lid);
+    const UnitRec ur = read_unit(L, u);
+    load_slots(L, u, ur, s_score, s_state, s_ts, s_lid);
     __syncthreads();
     for (int s = threadIdx.x; s < S; s += blockDim.x)
         if (s_state[s] == kEvictable) s_score[s] = L.score[base + s];
     __syncthreads();
+    if (threadIdx.x < 64) retention_wave(L, ur, r, s_score, s_state, s_ts, s_lid, ret);
     for (int idx = threadIdx.x; idx < G * D; idx += blockDim.x) {
         const int h = idx / D, c = idx - (idx / D) * D;
         float M = -INFINITY;
@@ -774,14 +848,17 @@ __global__ __launch_bounds__(256) void k_epilogue(LayerView L, StepIO io, double
         }
         ((T*)io.out)[((size_t)u * G + h) * D + c] = from_f<T>(O / Ls);
     }
-    retention(L, io, u, r, s_score, s_state, s_ts, s_lid, epi);
+    __syncthreads();
+    retention_store(L, io, u, ur, s_state, s_ts, s_lid, ret, threadIdx.x, blockDim.x);
 }
 
 inline unsigned grid1d(size_t n, int block) { return (unsigned)((n + block - 1) / block); }
 
+// LDS of the step kernel: (q+, q-) pairs in fp64, the attention wavefronts'
+// partial outputs, and the fused epilogue's slot arrays
 size_t step_lds(int G, int D, int S, int NW, bool fused) {
     size_t b = (size_t)16 * G * D + (size_t)NW * G * (D + 4) * 4;
-    if (fused) b += (size_t)S * (8 + 12);
+    if (fused) b += (size_t)S * 20;
     return b;
 }
 
@@ -797,7 +874,9 @@ hipError_t launch_step_bf16(const LayerView& L, const StepIO& io, const StepPlan
 
 // ---------------------------------------------------------------------------
 
-StepPlan plan_step(int U, int G, int D, int S, int Lcap, bool bf16, int split_override) {
+StepPlan plan_step(int U, int G, int D, int S, int Lcap, int ps, int pinned, bool bf16, int split_override) {
+    (void)ps;
+    (void)pinned;
     StepPlan pl{};
     const int nblk = Lcap / kBlockTokens;
     int want;
@@ -815,9 +894,9 @@ StepPlan plan_step(int U, int G, int D, int S, int Lcap, bool bf16, int split_ov
         if (split_override > 0) {
             want = split_override;
         } else {
-            // about 2048 wavefronts in flight over the 256 CUs
-            const double per_wave = fmax(1.0, (double)U * nblk / 2048.0);
-            want = (int)ceil(nblk / (pl.waves * per_wave));
+            // one workgroup per CU over the 256 CUs
+            const double per_wave = fmax(1.0, (double)U * nblk / (256.0 * pl.waves));
+            want = (int)ceil(nblk / (pl.waves * per_wave) - 1e-9);
         }
     }
     want = want < 1 ? 1 : want;
@@ -828,6 +907,22 @@ StepPlan plan_step(int U, int G, int D, int S, int Lcap, bool bf16, int split_ov
     pl.fused = bf16 && pl.nsplit == 1 && step_lds(G, D, S, pl.waves, true) <= kMaxLds;
     pl.lds = bf16 ? step_lds(G, D, S, pl.waves, pl.fused) : 0;
     return pl;
+}
+
+hipError_t allow_large_lds() {
+    const int bytes = (int)kMaxLds;
+    hipError_t e = hipSuccess;
+    auto set = [&](const void* f) {
+        hipError_t r = hipFuncSetAttribute(f, hipFuncAttributeMaxDynamicSharedMemorySize, bytes);
+        if (r != hipSuccess) e = r;
+    };
+    set((const void*)k_step_bf16<128, 8>);
+    set((const void*)k_step_bf16<128, 4>);
+    set((const void*)k_step_bf16<128, 2>);
+    set((const void*)k_step_bf16<64, 8>);
+    set((const void*)k_step_bf16<64, 4>);
+    set((const void*)k_step_bf16<64, 2>);
+    return e;
 }
 
 hipError_t launch_prefill(const LayerView& L, const void* k, const void* v, int P, int keep_pages,

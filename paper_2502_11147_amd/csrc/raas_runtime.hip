@@ -61,6 +61,7 @@ struct raas_pool {
     double* score = nullptr;  // [U][S], scratch of one step
     size_t bytes = 0;
     std::vector<unsigned char> prefilled;
+    std::vector<int> pinned;  // pinned prefill pages of each layer
     int split_override = 0;
     hipStream_t last_stream = nullptr;
     int prof_mask = 0;
@@ -195,6 +196,7 @@ raas_status raas_create_pool(const raas_config* cfg, void* stream, raas_pool** o
     p->rep_layer_elems = (size_t)p->U * p->S * p->D;
     p->meta_layer_elems = (size_t)p->U * p->S;
     p->prefilled.assign((size_t)cfg->n_layers, 0);
+    p->pinned.assign((size_t)cfg->n_layers, 0);
     const size_t Ly = (size_t)cfg->n_layers;
     const int nblk = p->Lcap / kBlockTokens;
     const int max_split = nblk < kMaxSplits ? nblk : kMaxSplits;
@@ -213,6 +215,11 @@ raas_status raas_create_pool(const raas_config* cfg, void* stream, raas_pool** o
         {(void**)&p->score, (size_t)p->U * p->S * sizeof(double)},
     };
     hipStream_t s = (hipStream_t)stream;
+    hipError_t ea = allow_large_lds();
+    if (ea != hipSuccess) {
+        raas_destroy(p);
+        return hip_fail(ea, "hipFuncSetAttribute");
+    }
     for (auto& r : reqs) {
         hipError_t e = hipMalloc(r.ptr, r.bytes);
         if (e != hipSuccess) {
@@ -271,6 +278,7 @@ raas_status raas_prefill(raas_pool* p, int32_t layer, const void* k, const void*
     hipError_t e = launch_prefill(view(p, layer), k, v, prefill_len, keep, s);
     if (e != hipSuccess) return hip_fail(e, "prefill launch");
     p->prefilled[layer] = 1;
+    p->pinned[layer] = keep;
     p->last_stream = s;
     return RAAS_OK;
 }
@@ -285,7 +293,8 @@ raas_status raas_decode_step(raas_pool* p, int32_t layer, const void* q, const v
     LayerView L = view(p, layer);
     StepIO io{q, k_new, v_new, out, page_table_out, timestamps_out, evicted_out};
     hipStream_t s = (hipStream_t)stream;
-    const StepPlan pl = plan_step(p->U, p->G, p->D, p->S, p->Lcap, p->cfg.dtype == RAAS_BF16, p->split_override);
+    const StepPlan pl = plan_step(p->U, p->G, p->D, p->S, p->Lcap, p->ps, p->pinned[layer], p->cfg.dtype == RAAS_BF16,
+                                  p->split_override);
     L.nsplit = pl.nsplit;
     L.bps = pl.bps;
 
