@@ -424,34 +424,47 @@ __device__ void retention_store(const LayerView& L, const StepIO& io, int u, con
     }
 }
 
+// Workgroup barrier that waits for this wavefront's LDS traffic only: loads
+// already issued to global memory stay in flight across it.
+__device__ __forceinline__ void lds_barrier() {
+    __atomic_signal_fence(__ATOMIC_SEQ_CST);
+    __builtin_amdgcn_s_waitcnt(0xC07F);  // lgkmcnt(0); vmcnt and expcnt left at their maxima
+    __builtin_amdgcn_s_barrier();
+    __atomic_signal_fence(__ATOMIC_SEQ_CST);
+}
+
 // ---------------------------------------------------------------------------
 // Step kernel, bf16 pools. One workgroup of NW wavefronts per (unit, split).
 //
 // Attention (Algorithm 1, attention(Q, K_old::K_new, V_old::V_new)) over
 // every resident token, split-K over 32-token blocks. Each wavefront holds
-// the unit's whole GQA query group and walks blocks round-robin, loading the
-// next block while it computes the current one. Per block: QK^T as two
-// 16x16x32 bf16 MFMA tiles per 32 channels (rows = tokens, columns = query
-// heads, G <= 16 of the 16 used), online softmax in base 2 with one
-// cross-lane max per block, and PV as D/16 MFMAs of V^T (rows = channels)
-// times P^T (columns = heads). A lane owns one head (its column) in both
-// products, so no data moves between lanes except the block max. The new
-// token is not in the pool when the block is read: its K/V come from the
-// step's inputs, substituted in registers, and the owning wavefront stores
-// it. Page-score passes ride along with the blocks. When one workgroup
-// covers the unit (fused), wavefront 0 runs the retention policy while the
-// others merge the wavefronts' partial outputs, and the state goes out only
-// after the attention has read the pool.
+// the unit's whole GQA query group; it takes one block statically, then
+// claims further blocks from a counter in LDS, so the wavefronts that the
+// memory system serves faster take more blocks. The next block loads while
+// the current one computes. Per block: QK^T as two 16x16x32 bf16 MFMA tiles
+// per 32 channels (rows = tokens, columns = query heads, G <= 16 of the 16
+// used), online softmax in base 2 with one cross-lane max per block, and PV
+// as D/16 MFMAs of V^T (rows = channels) times P^T (columns = heads). A lane
+// owns one head (its column) in both products, so no data moves between
+// lanes except the block max. The new token is not in the pool when the
+// block is read: its K/V come from the step's inputs, substituted in
+// registers, and the wavefront holding that block stores it.
+//
+// Page-score passes ride along with the first blocks. Once every wavefront
+// has finished its passes (a workgroup barrier), wavefront 0 runs the
+// retention policy when one workgroup covers the unit (fused), then goes on
+// claiming blocks. The state reaches the pool only after the attention has
+// read it; the wavefronts' partial outputs merge at the end.
 
 template <int D, int NW>
 __global__ __launch_bounds__(NW * 64) __attribute__((amdgpu_waves_per_eu(1, 2))) void k_step_bf16(
-    LayerView L, StepIO io, float scale_log2, double r,
-                                                       int fused) {
+    LayerView L, StepIO io, float scale_log2, double r, int fused) {
     constexpr int KS = D / 32, NB = D / 16, BLK = 32 * D;
     extern __shared__ __align__(16) unsigned char smem[];
     __shared__ float s_m[NW][16];
     __shared__ float s_l[NW][16];
     __shared__ RetShared ret;
+    __shared__ int s_next;  // next unclaimed block
 
     const int G = L.G, S = L.S, ps = L.ps;
     double2* s_q2 = reinterpret_cast<double2*>(smem);  // [G][D] (q+, q-)
@@ -483,20 +496,14 @@ __global__ __launch_bounds__(NW * 64) __attribute__((amdgpu_waves_per_eu(1, 2)))
     const uint16_t* Vu = (const uint16_t*)L.V + (size_t)u * L.Lcap * D;
     const int32_t* fu = L.fill + base;
 
-    // valid tokens among this lane's 8 rows of block b (they lie in one page: page_size % 8 == 0)
-    auto valid_rows = [&](int b) {
-        const int t0 = 32 * b + 8 * grp;
-        const int slot = t0 / ps;
-        const int f = (slot < S) ? (slot == ns ? nf + 1 : fu[slot]) : 0;
-        return min(max(f - (t0 - slot * ps), 0), 8);
+    // fill of the page holding this lane's 8 rows of block b (page_size % 8 == 0)
+    auto row_fill = [&](int b) {
+        const int slot = (32 * b + 8 * grp) / ps;
+        return (slot < S) ? (slot == ns ? nf + 1 : fu[slot]) : 0;
     };
-    // next block of this wavefront at or after b holding a resident token
-    auto next_block = [&](int b, int& nv) {
-        for (; b < b1; b += NW) {
-            nv = valid_rows(b);
-            if (__ballot(nv > 0) != 0ull) return b;
-        }
-        return b1;
+    auto valid_rows = [&](int b, int f) {
+        const int t0 = 32 * b + 8 * grp;
+        return min(max(f - (t0 - (t0 / ps) * ps), 0), 8);
     };
     auto load_block = [&](int b, u32x4 (&kr)[2][KS], u32x4 (&vr)[NB]) {
         const uint16_t* Kb = Ku + (size_t)b * BLK + lane * 8;
@@ -509,31 +516,41 @@ __global__ __launch_bounds__(NW * 64) __attribute__((amdgpu_waves_per_eu(1, 2)))
         for (int nb = 0; nb < NB; ++nb) vr[nb] = ld4(Vb + nb * 512);
     };
 
-    int nv_next = 0;
-    int b = next_block(b0 + w, nv_next);
-    u32x4 kr_next[2][KS], vr_next[NB];
-    if (b < b1) load_block(b, kr_next, vr_next);
-
-    // stage (q+, q-) and the slot state
+    // staging loads first, so that waiting for them leaves the block loads in flight
     for (int i = tid; i < G * D; i += NW * 64) {
         const double x = (double)bf2f(qg[i]);
         s_q2[i] = double2{x > 0.0 ? x : 0.0, x < 0.0 ? x : 0.0};
     }
     if (fused) load_slots(L, u, ur, s_score, s_state, s_ts, s_lid);
+    if (tid == 0) s_next = b0 + 2 * NW;  // claims start after the two static blocks of every wavefront
+
+    int b = b0 + w;  // first and second blocks (b0 + w + NW): static
+    int f_next = 0;
+    u32x4 kr_next[2][KS], vr_next[NB];
+    if (b < b1) {
+        f_next = row_fill(b);
+        load_block(b, kr_next, vr_next);
+    }
+    bf16x8 qv[KS];
+#pragma unroll
+    for (int ks = 0; ks < KS; ++ks) {
+        const u32x4 x = (col < G) ? ld4(qg + (size_t)col * D + 32 * ks + 8 * grp) : u32x4{0u, 0u, 0u, 0u};
+        qv[ks] = __builtin_bit_cast(bf16x8, x);
+    }
+    float m_run = -INFINITY, l_run = 0.0f;
+    f32x4 acc[NB];
+#pragma unroll
+    for (int nb = 0; nb < NB; ++nb) acc[nb] = f32x4{0.f, 0.f, 0.f, 0.f};
 
     // score passes of this wavefront: 8 pages each, page = first + (lane >> 3)
     const int part = lane & 7;
     auto pass_page = [&](int pass) { return sl0 + 8 * (pass * NW + w) + (lane >> 3); };
     auto pass_act = [&](int p) { return p < sl1 && (p == ns || L.state[base + p] == kEvictable); };
     const int npass = (sl1 - sl0 - 8 * w > 0) ? (sl1 - sl0 - 8 * w + 8 * NW - 1) / (8 * NW) : 0;
+    const int npass_all = (sl1 - sl0 + 8 * NW - 1) / (8 * NW);  // passes of wavefront 0, the most
     int pass = 0;
     ScoreFrag<D> frag;
     bool act_cur = false;
-    if (npass > 0) {
-        const int p = pass_page(0);
-        act_cur = pass_act(p);
-        score_issue<D>(L, u, p, part, act_cur && !(p == ns && opened), frag);
-    }
     auto score_step = [&]() {
         const int p = pass_page(pass);
         const double sc = score_finish<D>(L, u, p, part, act_cur, frag, p == ns, opened, kn_g, s_q2);
@@ -548,21 +565,26 @@ __global__ __launch_bounds__(NW * 64) __attribute__((amdgpu_waves_per_eu(1, 2)))
             score_issue<D>(L, u, pn, part, act_cur && !(pn == ns && opened), frag);
         }
     };
+    // retention policy once every wavefront's scores are in LDS
+    bool decided = false;
+    auto scores_done = [&]() {
+        lds_barrier();
+        if (fused && w == 0) retention_wave(L, ur, r, s_score, s_state, s_ts, s_lid, ret);
+        decided = true;
+    };
 
-    bf16x8 qv[KS];
-#pragma unroll
-    for (int ks = 0; ks < KS; ++ks) {
-        const u32x4 x = (col < G) ? ld4(qg + (size_t)col * D + 32 * ks + 8 * grp) : u32x4{0u, 0u, 0u, 0u};
-        qv[ks] = __builtin_bit_cast(bf16x8, x);
-    }
-    float m_run = -INFINITY, l_run = 0.0f;
-    f32x4 acc[NB];
-#pragma unroll
-    for (int nb = 0; nb < NB; ++nb) acc[nb] = f32x4{0.f, 0.f, 0.f, 0.f};
-    __syncthreads();  // (q+, q-) and the slot state staged
-
+    // after the first block: the staging is visible and the score passes start
+    auto staged = [&]() {
+        lds_barrier();  // (q+, q-), slot state and the block counter staged
+        if (npass > 0) {
+            const int p = pass_page(0);
+            act_cur = pass_act(p);
+            score_issue<D>(L, u, p, part, act_cur && !(p == ns && opened), frag);
+        }
+    };
+    int it = 0;
     while (b < b1) {
-        const int nv = nv_next;
+        const int f_cur = f_next;
         u32x4 kr[2][KS], vr[NB];
 #pragma unroll
         for (int qq = 0; qq < 2; ++qq)
@@ -570,81 +592,96 @@ __global__ __launch_bounds__(NW * 64) __attribute__((amdgpu_waves_per_eu(1, 2)))
             for (int ks = 0; ks < KS; ++ks) kr[qq][ks] = kr_next[qq][ks];
 #pragma unroll
         for (int nb = 0; nb < NB; ++nb) vr[nb] = vr_next[nb];
-        const int bn = next_block(b + NW, nv_next);
-        if (bn < b1) load_block(bn, kr_next, vr_next);
-
-        if (b == b_new) {  // the new token: K/V from the inputs
-            const int i_new = 4 * (tt_new >> 3) + (tt_new & 3), q_new = (tt_new >> 2) & 1;
-            if (col == i_new) {
+        int bn = b + NW;
+        if (it > 0) {
+            if (lane == 0) bn = atomicAdd(&s_next, 1);  // one claim per wavefront
+            bn = __builtin_amdgcn_readfirstlane(bn);
+        }
+        if (bn < b1) {
+            f_next = row_fill(bn);
+            load_block(bn, kr_next, vr_next);
+        }
+        const int nv = valid_rows(b, f_cur);
+        if (__ballot(nv > 0) != 0ull) {
+            if (b == b_new) {  // the new token: K/V from the inputs
+                const int i_new = 4 * (tt_new >> 3) + (tt_new & 3), q_new = (tt_new >> 2) & 1;
+                if (col == i_new) {
 #pragma unroll
-                for (int ks = 0; ks < KS; ++ks) {
-                    const u32x4 x = ld4(kn_g + 32 * ks + 8 * grp);
-                    if (q_new == 0) kr[0][ks] = x; else kr[1][ks] = x;
+                    for (int ks = 0; ks < KS; ++ks) {
+                        const u32x4 x = ld4(kn_g + 32 * ks + 8 * grp);
+                        if (q_new == 0) kr[0][ks] = x; else kr[1][ks] = x;
+                    }
                 }
-            }
-            if (grp == (tt_new >> 3)) {
-                const int j_new = tt_new & 7;
+                if (grp == (tt_new >> 3)) {
+                    const int j_new = tt_new & 7;
 #pragma unroll
-                for (int nb = 0; nb < NB; ++nb) {
-                    const uint32_t val = vn_g[16 * nb + col];
+                    for (int nb = 0; nb < NB; ++nb) {
+                        const uint32_t val = vn_g[16 * nb + col];
 #pragma unroll
-                    for (int h = 0; h < 4; ++h) {
-                        if ((j_new >> 1) == h) {
-                            const int sh = (j_new & 1) * 16;
-                            vr[nb][h] = (vr[nb][h] & ~(0xFFFFu << sh)) | (val << sh);
+                        for (int h = 0; h < 4; ++h) {
+                            if ((j_new >> 1) == h) {
+                                const int sh = (j_new & 1) * 16;
+                                vr[nb][h] = (vr[nb][h] & ~(0xFFFFu << sh)) | (val << sh);
+                            }
                         }
                     }
                 }
+                // append: store the new token in the pool (Algorithm 1, "Store K_new and V_new")
+                uint16_t* Kw = (uint16_t*)L.K + (size_t)u * L.Lcap * D;
+                uint16_t* Vw = (uint16_t*)L.V + (size_t)u * L.Lcap * D;
+                if (lane < D / 8) st4(Kw + k_off<D>(row_new, lane * 8), ld4(kn_g + lane * 8));
+                for (int c = lane; c < D; c += 64) Vw[v_off<D>(row_new, c)] = vn_g[c];
             }
-            // append: store the new token in the pool (Algorithm 1, "Store K_new and V_new")
-            uint16_t* Kw = (uint16_t*)L.K + (size_t)u * L.Lcap * D;
-            uint16_t* Vw = (uint16_t*)L.V + (size_t)u * L.Lcap * D;
-            if (lane < D / 8) st4(Kw + k_off<D>(row_new, lane * 8), ld4(kn_g + lane * 8));
-            for (int c = lane; c < D; c += 64) Vw[v_off<D>(row_new, c)] = vn_g[c];
-        }
 
-        f32x4 s0 = {0.f, 0.f, 0.f, 0.f}, s1 = {0.f, 0.f, 0.f, 0.f};
+            f32x4 s0 = {0.f, 0.f, 0.f, 0.f}, s1 = {0.f, 0.f, 0.f, 0.f};
 #pragma unroll
-        for (int ks = 0; ks < KS; ++ks) {
-            s0 = __builtin_amdgcn_mfma_f32_16x16x32_bf16(__builtin_bit_cast(bf16x8, kr[0][ks]), qv[ks], s0, 0, 0, 0);
-            s1 = __builtin_amdgcn_mfma_f32_16x16x32_bf16(__builtin_bit_cast(bf16x8, kr[1][ks]), qv[ks], s1, 0, 0, 0);
+            for (int ks = 0; ks < KS; ++ks) {
+                s0 = __builtin_amdgcn_mfma_f32_16x16x32_bf16(__builtin_bit_cast(bf16x8, kr[0][ks]), qv[ks], s0, 0, 0, 0);
+                s1 = __builtin_amdgcn_mfma_f32_16x16x32_bf16(__builtin_bit_cast(bf16x8, kr[1][ks]), qv[ks], s1, 0, 0, 0);
+            }
+            // x[j]: scaled logit of token 8*grp + j for head `col` (base 2)
+            float x[8];
+#pragma unroll
+            for (int v = 0; v < 4; ++v) {
+                x[v] = (v < nv) ? s0[v] * scale_log2 : -INFINITY;
+                x[4 + v] = (4 + v < nv) ? s1[v] * scale_log2 : -INFINITY;
+            }
+            float mb = x[0];
+#pragma unroll
+            for (int j = 1; j < 8; ++j) mb = fmaxf(mb, x[j]);
+            mb = fmaxf(mb, __shfl_xor(mb, 16));
+            mb = fmaxf(mb, __shfl_xor(mb, 32));
+            const float m_new = fmaxf(m_run, mb);
+            if (__ballot(m_new > m_run) != 0ull) {
+                const float alpha = __builtin_amdgcn_exp2f(m_run - m_new);
+                l_run *= alpha;
+#pragma unroll
+                for (int nb = 0; nb < NB; ++nb) acc[nb] *= alpha;
+                m_run = m_new;
+            }
+            float psum = 0.0f;
+            bf16x8 pb;
+#pragma unroll
+            for (int j = 0; j < 8; ++j) {
+                const float pj = __builtin_amdgcn_exp2f(x[j] - m_run);
+                psum += pj;
+                pb[j] = (__bf16)pj;
+            }
+            l_run += psum;
+#pragma unroll
+            for (int nb = 0; nb < NB; ++nb)
+                acc[nb] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(__builtin_bit_cast(bf16x8, vr[nb]), pb, acc[nb], 0, 0, 0);
         }
-        // x[j]: scaled logit of token 8*grp + j for head `col` (base 2)
-        float x[8];
-#pragma unroll
-        for (int v = 0; v < 4; ++v) {
-            x[v] = (v < nv) ? s0[v] * scale_log2 : -INFINITY;
-            x[4 + v] = (4 + v < nv) ? s1[v] * scale_log2 : -INFINITY;
-        }
-        float mb = x[0];
-#pragma unroll
-        for (int j = 1; j < 8; ++j) mb = fmaxf(mb, x[j]);
-        mb = fmaxf(mb, __shfl_xor(mb, 16));
-        mb = fmaxf(mb, __shfl_xor(mb, 32));
-        const float m_new = fmaxf(m_run, mb);
-        if (__ballot(m_new > m_run) != 0ull) {
-            const float alpha = __builtin_amdgcn_exp2f(m_run - m_new);
-            l_run *= alpha;
-#pragma unroll
-            for (int nb = 0; nb < NB; ++nb) acc[nb] *= alpha;
-            m_run = m_new;
-        }
-        float psum = 0.0f;
-        bf16x8 pb;
-#pragma unroll
-        for (int j = 0; j < 8; ++j) {
-            const float pj = __builtin_amdgcn_exp2f(x[j] - m_run);
-            psum += pj;
-            pb[j] = (__bf16)pj;
-        }
-        l_run += psum;
-#pragma unroll
-        for (int nb = 0; nb < NB; ++nb)
-            acc[nb] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(__builtin_bit_cast(bf16x8, vr[nb]), pb, acc[nb], 0, 0, 0);
-        if (pass < npass) score_step();  // this block's registers are free again
+        // this block's registers are free again
+        if (it == 0) staged();
+        else if (pass < npass) score_step();
+        if (it == npass_all) scores_done();
+        ++it;
         b = bn;
     }
+    if (it == 0) staged();
     while (pass < npass) score_step();  // passes left when the wavefront ran out of blocks
+    if (!decided) scores_done();
 
     // park this wavefront's partial attention in LDS
     l_run += __shfl_xor(l_run, 16);
@@ -658,41 +695,34 @@ __global__ __launch_bounds__(NW * 64) __attribute__((amdgpu_waves_per_eu(1, 2)))
         for (int nb = 0; nb < NB; ++nb)
             *reinterpret_cast<f32x4*>(&s_o[((size_t)w * G + col) * (D + 4) + 16 * nb + 4 * grp]) = acc[nb];
     }
-    __syncthreads();  // attention done, partials parked, scores in
+    lds_barrier();  // partials parked, retention decided
 
-    if (fused && w == 0) retention_wave(L, ur, r, s_score, s_state, s_ts, s_lid, ret);
-    // merge the wavefronts' partial outputs (wavefront 0 joins when not busy with retention)
-    const int m_first = fused ? tid - 64 : tid, m_threads = fused ? (NW - 1) * 64 : NW * 64;
-    if (m_first >= 0) {
-        for (int idx = m_first; idx < G * D; idx += m_threads) {
-            const int h = idx / D, c = idx - (idx / D) * D;
-            float M = -INFINITY;
+    // merge the wavefronts' partial outputs
+    for (int idx = tid; idx < G * D; idx += NW * 64) {
+        const int h = idx / D, c = idx - (idx / D) * D;
+        float M = -INFINITY;
 #pragma unroll
-            for (int ww = 0; ww < NW; ++ww) M = fmaxf(M, s_m[ww][h]);
-            float O = 0.0f, Ls = 0.0f;
+        for (int ww = 0; ww < NW; ++ww) M = fmaxf(M, s_m[ww][h]);
+        float O = 0.0f, Ls = 0.0f;
 #pragma unroll
-            for (int ww = 0; ww < NW; ++ww) {
-                const float mw = s_m[ww][h];
-                const float wt = (mw == -INFINITY) ? 0.0f : __builtin_amdgcn_exp2f(mw - M);
-                O += wt * s_o[((size_t)ww * G + h) * (D + 4) + c];
-                Ls += wt * s_l[ww][h];
-            }
-            if (fused) {
-                ((uint16_t*)io.out)[((size_t)u * G + h) * D + c] = f2bf(O / Ls);
-            } else {
-                float* pp = L.part + (((size_t)u * nsplit + split) * G + h) * (D + 2);
-                pp[c] = O;
-                if (c == 0) {
-                    pp[D] = M;
-                    pp[D + 1] = Ls;
-                }
+        for (int ww = 0; ww < NW; ++ww) {
+            const float mw = s_m[ww][h];
+            const float wt = (mw == -INFINITY) ? 0.0f : __builtin_amdgcn_exp2f(mw - M);
+            O += wt * s_o[((size_t)ww * G + h) * (D + 4) + c];
+            Ls += wt * s_l[ww][h];
+        }
+        if (fused) {
+            ((uint16_t*)io.out)[((size_t)u * G + h) * D + c] = f2bf(O / Ls);
+        } else {
+            float* pp = L.part + (((size_t)u * nsplit + split) * G + h) * (D + 2);
+            pp[c] = O;
+            if (c == 0) {
+                pp[D] = M;
+                pp[D + 1] = Ls;
             }
         }
     }
-    if (fused) {
-        __syncthreads();  // retention decided
-        retention_store(L, io, u, ur, s_state, s_ts, s_lid, ret, tid, NW * 64);
-    }
+    if (fused) retention_store(L, io, u, ur, s_state, s_ts, s_lid, ret, tid, NW * 64);
 }
 
 // Step kernel, fp32 pools: one wavefront per (unit, split), one token at a
