@@ -45,7 +45,116 @@ def parse():
     ap.add_argument("--splits", type=int, default=0, help="attention splits per unit (0 = automatic)")
     ap.add_argument("--cpu-seconds", type=float, default=15.0, help="budget of the CPU oracle sample")
     ap.add_argument("--no-cpu-baseline", action="store_true")
+    ap.add_argument("--copy-calibration", action="store_true",
+                    help="run only a plain streaming kernel of known size (counter calibration)")
+    ap.add_argument("--traffic-summary", metavar="DIR", default=None,
+                    help="turn rocprofv3 --pmc output under DIR/{fetch,write,copy_fetch,copy_write} "
+                         "into the stored traffic profile of --workload")
     return ap.parse_args()
+
+
+COPY_BYTES = 1 << 30  # bytes read (and written) by one calibration launch
+PROFILES = os.path.join(ROOT, "profiles")
+
+
+def traffic_profile_path(kernel, workload):
+    return os.path.join(PROFILES, "traffic_%s_%s.json" % (kernel, workload))
+
+
+def copy_calibration():
+    """A plain streaming kernel of known size: negation of 2^30 bytes of bf16
+    into a second buffer (each byte read once, written once). What FETCH_SIZE
+    and WRITE_SIZE read for it scales them to bytes."""
+    import torch
+
+    assert torch.cuda.is_available(), "needs a GPU"
+    n = COPY_BYTES // 2
+    src = torch.ones(n, dtype=torch.bfloat16, device="cuda")
+    dst = torch.empty_like(src)
+    for _ in range(5):
+        torch.neg(src, out=dst)
+    torch.cuda.synchronize()
+    print(json.dumps({"copy_calibration": "neg", "bytes_read": COPY_BYTES, "bytes_written": COPY_BYTES,
+                      "launches": 5}), flush=True)
+
+
+def _counter_rows(d, counter):
+    import csv
+    import glob
+
+    files = sorted(glob.glob(os.path.join(d, "**", "*counter_collection.csv"), recursive=True))
+    if not files:
+        raise SystemExit("no counter_collection.csv under %s" % d)
+    rows = []
+    for f in files:
+        with open(f) as fh:
+            for r in csv.DictReader(fh):
+                if r["Counter_Name"] == counter:
+                    rows.append(r)
+    rows.sort(key=lambda r: int(r["Dispatch_Id"]))
+    return rows
+
+
+def traffic_summary(args):
+    """Per-launch FETCH_SIZE and WRITE_SIZE of the step kernel over the last
+    --steps dispatches (the timed steps of a bench run with the same flags),
+    scaled by the factor that makes the same counters read the known size of
+    the calibration kernel. Writes the stored traffic profile."""
+    import synth
+    from paper_2502_11147_amd import build as hip_build
+
+    w = synth.get_workload(args.workload or synth.workloads.HEADLINE)
+    kernel = "k_step_bf16" if w.dtype == "bf16" else "k_step_f32"
+    out = {"kernel": kernel, "workload": w.name, "kernel_digest": hip_build.kernel_digest()}
+    for counter, sub, csub in (("FETCH_SIZE", "fetch", "copy_fetch"), ("WRITE_SIZE", "write", "copy_write")):
+        rows = [r for r in _counter_rows(os.path.join(args.traffic_summary, sub), counter)
+                if kernel in r["Kernel_Name"]]
+        rows = rows[-args.steps:]
+        if len(rows) < args.steps:
+            raise SystemExit("%s: %d %s dispatches, want %d" % (counter, len(rows), kernel, args.steps))
+        kib = float(np.mean([float(r["Counter_Value"]) for r in rows]))
+        crow = [r for r in _counter_rows(os.path.join(args.traffic_summary, csub), counter)
+                if "neg" in r["Kernel_Name"]]
+        if not crow:
+            raise SystemExit("%s: no calibration dispatches" % counter)
+        ckib = float(np.median([float(r["Counter_Value"]) for r in crow]))
+        factor = COPY_BYTES / (ckib * 1024.0)
+        key = counter.lower()
+        out[key + "_kib_per_launch"] = round(kib, 3)
+        out[key + "_calibration_kib"] = round(ckib, 3)
+        out[key + "_factor"] = round(factor, 5)
+        out[key + "_bytes_per_launch"] = round(kib * 1024.0 * factor)
+        out[key + "_launches"] = len(rows)
+    out["traffic_bytes_per_launch"] = out["fetch_size_bytes_per_launch"] + out["write_size_bytes_per_launch"]
+    flags = "--workload %s --steps %d --warmup %d --no-cpu-baseline" % (w.name, args.steps, args.warmup)
+    out["commands"] = [
+        "timeout -s KILL 300 rocprofv3 --pmc FETCH_SIZE --output-format csv -d DIR/fetch -- python3 bench.py " + flags,
+        "timeout -s KILL 300 rocprofv3 --pmc WRITE_SIZE --output-format csv -d DIR/write -- python3 bench.py " + flags,
+        "timeout -s KILL 120 rocprofv3 --pmc FETCH_SIZE --output-format csv -d DIR/copy_fetch -- python3 bench.py --copy-calibration",
+        "timeout -s KILL 120 rocprofv3 --pmc WRITE_SIZE --output-format csv -d DIR/copy_write -- python3 bench.py --copy-calibration",
+        "python3 bench.py --traffic-summary DIR " + flags,
+    ]
+    os.makedirs(PROFILES, exist_ok=True)
+    path = traffic_profile_path(kernel, w.name)
+    with open(path, "w") as f:
+        json.dump(out, f, indent=1)
+        f.write("\n")
+    print(json.dumps(out), flush=True)
+
+
+def stored_traffic(kernel, workload):
+    """HBM bytes per launch from the stored counter profile, or None when
+    there is none or the kernels have changed since it was taken."""
+    from paper_2502_11147_amd import build as hip_build
+
+    path = traffic_profile_path(kernel, workload)
+    if not os.path.exists(path):
+        return None, "no stored counter profile"
+    with open(path) as f:
+        prof = json.load(f)
+    if prof.get("kernel_digest") != hip_build.kernel_digest():
+        return None, "kernel sources changed since the counters were taken"
+    return float(prof["traffic_bytes_per_launch"]), os.path.relpath(path, ROOT)
 
 
 def resident_schedule(st, ps, S, n):
@@ -78,13 +187,12 @@ def resident_schedule(st, ps, S, n):
 def step_bytes(w, resident, n_ev):
     """Algorithmic HBM bytes of one whole decode step, all units: K+V of the
     resident tokens; the representative keys (per-channel min and max) of the
-    evictable pages; q read for the attention and for the scores, out
-    written; the new K and V read once and stored once; the tail page's
-    min/max read and written; per slot, state/timestamp/id/fill read and
-    state/timestamp written (24 B)."""
+    evictable pages; q read once, out written once; the new K and V read once
+    and stored once; the tail page's min/max read and written; per slot,
+    state/timestamp/id/fill read and state/timestamp written (24 B)."""
     e = 2 if w.dtype == "bf16" else 4
     d, G, S = w.head_dim, w.group, w.slots
-    per_unit = (resident * 2 * d * e + n_ev * 2 * d * e + 3 * G * d * e + 4 * d * e + 4 * d * e + 24 * S)
+    per_unit = (resident * 2 * d * e + n_ev * 2 * d * e + 2 * G * d * e + 4 * d * e + 4 * d * e + 24 * S)
     return per_unit.sum(axis=-1)
 
 
@@ -136,11 +244,17 @@ def cpu_baseline(w, seed, ring_np, budget_s):
 
 def main():
     args = parse()
+    if args.traffic_summary:
+        traffic_summary(args)
+        return
     if args.gpus != 1:
         print("bench.py runs on one GPU: this decode path has no multi-GPU mode "
               "(units are independent; see the design notes on sharding). Got --gpus %d." % args.gpus,
               file=sys.stderr)
         sys.exit(2)
+    if args.copy_calibration:
+        copy_calibration()
+        return
     import torch
 
     import paper_2502_11147_amd as raas
@@ -219,6 +333,8 @@ def main():
     e = 2 if w.dtype == "bf16" else 4
     kernel_b = step_b if fused else step_b - U * w.group * w.head_dim * e - 24 * U * S
     achieved = kernel_b / step_avg_s / 1e9
+    kname = "k_step_bf16" if w.dtype == "bf16" else "k_step_f32"
+    traffic, traffic_src = stored_traffic(kname, w.name) if fused else (None, "two kernels per step")
     line = {
         "metric": "decode tokens/s per GPU at batch B, budget L; achieved HBM GB/s vs peak",
         "value": round(tokens_per_s, 1),
@@ -242,13 +358,14 @@ def main():
         },
         "step_hbm_gbs_algorithmic": round(step_b / (elapsed / args.steps) / 1e9, 1),
         "roofline": {
-            "kernel": ("k_step_bf16" if w.dtype == "bf16" else "k_step_f32") + ("" if fused else " (+k_epilogue)"),
+            "kernel": kname + ("" if fused else " (+k_epilogue)"),
             "bound": "hbm",
             "achieved": round(achieved, 1),
             "peak": HBM_PEAK_GBS,
             "unit": "GB/s",
             "frac": round(achieved / HBM_PEAK_GBS, 4),
-            "traffic": None,
+            "traffic": None if traffic is None else round(traffic),
+            "traffic_source": traffic_src,
             "bytes_per_launch": kernel_b,
             "avg_launch_us": round(step_avg_s * 1e6, 3),
             "launches_timed": args.steps if fused else step_n,

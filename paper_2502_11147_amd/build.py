@@ -1,6 +1,7 @@
 """Compiles the HIP sources of the decode path into ``libraas.so`` (gfx950)."""
 from __future__ import annotations
 
+import hashlib
 import os
 import subprocess
 
@@ -20,6 +21,17 @@ def hipcc_command(out: str) -> list[str]:
         "-Xclang", "-target-feature", "-Xclang", "-packed-fp32-ops",
         "-I", INCLUDE, "-I", CSRC, *SOURCES, "-o", out,
     ]
+
+
+def kernel_digest() -> str:
+    """sha256 over the kernel sources and the compile flags: identifies the
+    kernels that a stored hardware-counter measurement was taken on."""
+    h = hashlib.sha256()
+    for p in (os.path.join(CSRC, "raas_kernels.hip"), os.path.join(CSRC, "raas_internal.h")):
+        with open(p, "rb") as f:
+            h.update(f.read())
+    h.update(" ".join(a for a in hipcc_command("lib") if not os.path.isabs(a) and a not in ("-I", "-o", "lib")).encode())
+    return h.hexdigest()
 
 
 def build(verbose: bool = False) -> str:
