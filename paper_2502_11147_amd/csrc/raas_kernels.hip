@@ -214,6 +214,15 @@ __device__ void load_slots(const LayerView& L, int u, const UnitRec& ur, double*
 // while the previous block computes. The page the step writes to has its
 // min/max widened by the new key and stored back.
 
+// LDS slot of element i = head * D + channel of the fp64 (q+, q-) array: one
+// 16-byte pad after each D/8 channels, so that the eight lanes scoring a
+// page, which read channels D/8 apart, fall on different LDS banks.
+template <int D>
+__device__ __forceinline__ int qpad_index(int i) {
+    const int h = i / D, c = i - (i / D) * D;
+    return h * (D + 8) + c + c / (D / 8);
+}
+
 template <int D>
 struct ScoreFrag {
     static constexpr int SV = D / 64;  // 16-byte vectors per array per lane (D/8 bf16 channels)
@@ -271,7 +280,7 @@ __device__ __forceinline__ double score_finish(const LayerView& L, int u, int p,
     double best = -INFINITY;
 #pragma unroll 1
     for (int j = 0; j < G; ++j) {
-        const double2* qj = q2 + (size_t)j * D + c0;
+        const double2* qj = q2 + (size_t)j * (D + 8) + c0 + part;  // padded rows: see qpad_index
         double a = 0.0;
         // the keys stay packed: widening them once for all heads would need 4x the registers
 #pragma unroll
@@ -433,6 +442,97 @@ __device__ __forceinline__ void lds_barrier() {
     __atomic_signal_fence(__ATOMIC_SEQ_CST);
 }
 
+// One 32-token block of attention for the GQA group held by this wavefront:
+// QK^T as two 16x16x32 bf16 MFMA tiles per 32 channels (rows = tokens,
+// columns = query heads), online softmax in base 2 with one cross-lane max,
+// PV as D/16 MFMAs of V^T times P^T. nv: valid rows among this lane's eight.
+template <int D>
+__device__ __forceinline__ void attend_block(const u32x4 (&kr)[2][D / 32], const u32x4 (&vr)[D / 16], int nv,
+                                             const bf16x8 (&qv)[D / 32], float scale_log2, float& m_run,
+                                             float& l_run, f32x4 (&acc)[D / 16]) {
+    constexpr int KS = D / 32, NB = D / 16;
+    f32x4 s0 = {0.f, 0.f, 0.f, 0.f}, s1 = {0.f, 0.f, 0.f, 0.f};
+#pragma unroll
+    for (int ks = 0; ks < KS; ++ks) {
+        s0 = __builtin_amdgcn_mfma_f32_16x16x32_bf16(__builtin_bit_cast(bf16x8, kr[0][ks]), qv[ks], s0, 0, 0, 0);
+        s1 = __builtin_amdgcn_mfma_f32_16x16x32_bf16(__builtin_bit_cast(bf16x8, kr[1][ks]), qv[ks], s1, 0, 0, 0);
+    }
+    // x[j]: scaled logit of token 8*grp + j for head `col` (base 2)
+    float x[8];
+#pragma unroll
+    for (int v = 0; v < 4; ++v) {
+        x[v] = (v < nv) ? s0[v] * scale_log2 : -INFINITY;
+        x[4 + v] = (4 + v < nv) ? s1[v] * scale_log2 : -INFINITY;
+    }
+    float mb = x[0];
+#pragma unroll
+    for (int j = 1; j < 8; ++j) mb = fmaxf(mb, x[j]);
+    mb = fmaxf(mb, __shfl_xor(mb, 16));
+    mb = fmaxf(mb, __shfl_xor(mb, 32));
+    const float m_new = fmaxf(m_run, mb);
+    if (__ballot(m_new > m_run) != 0ull) {
+        const float alpha = __builtin_amdgcn_exp2f(m_run - m_new);
+        l_run *= alpha;
+#pragma unroll
+        for (int nb = 0; nb < NB; ++nb) acc[nb] *= alpha;
+        m_run = m_new;
+    }
+    float psum = 0.0f;
+    bf16x8 pb;
+#pragma unroll
+    for (int j = 0; j < 8; ++j) {
+        const float pj = __builtin_amdgcn_exp2f(x[j] - m_run);
+        psum += pj;
+        pb[j] = (__bf16)pj;
+    }
+    l_run += psum;
+#pragma unroll
+    for (int nb = 0; nb < NB; ++nb)
+        acc[nb] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(__builtin_bit_cast(bf16x8, vr[nb]), pb, acc[nb], 0, 0, 0);
+}
+
+// Block sharing. A unit's last nsh full pinned blocks are its shared blocks:
+// the decode step never writes them, so any workgroup may read them while
+// the unit's own workgroup (its owner) writes the unit's state. The owner
+// takes its other blocks first and then claims shared blocks from a counter
+// in memory; waves whose own unit is done claim shared blocks of other units
+// from the same counters. A helper parks its block's partial attention in
+// memory (slot c of the unit), the owner its merged partial (slot nsh), and
+// each adds its block count to the unit's done counter; whoever completes
+// the count merges the slots and writes the output. Counters come in two
+// sets by clock parity: a step uses one and its owner clears the unit's
+// record in the other for the next step. Nothing waits on another workgroup.
+
+__device__ __forceinline__ int32_t* coord_rec(const LayerView& L, int parity, int u) {
+    return L.coord + ((size_t)parity * L.U + u) * kCoordFields;
+}
+
+// partial slot s of unit u: [G][D+4] floats, channels then (max, sum) of each head
+__device__ __forceinline__ float* shared_slot(const LayerView& L, int u, int s) {
+    return L.part + ((size_t)u * (L.nsh + 1) + s) * L.G * (L.D + 4);
+}
+
+// Output of unit u from its owner's slot and the slots of the blocks helpers
+// took (mask bits); called after the done count completed and an acquire.
+__device__ void finish_shared(const LayerView& L, const StepIO& io, int u, uint64_t mask, int first, int stride) {
+    const int G = L.G, D = L.D, nsh = L.nsh;
+    for (int idx = first; idx < G * D; idx += stride) {
+        const int h = idx / D, c = idx - (idx / D) * D;
+        const float* po = shared_slot(L, u, nsh) + (size_t)h * (D + 4);
+        float M = po[D];
+        for (uint64_t m = mask; m; m &= m - 1) M = fmaxf(M, shared_slot(L, u, __builtin_ctzll(m))[(size_t)h * (D + 4) + D]);
+        const float wo = (po[D] == -INFINITY) ? 0.0f : __builtin_amdgcn_exp2f(po[D] - M);
+        float O = wo * po[c], Ls = wo * po[D + 1];
+        for (uint64_t m = mask; m; m &= m - 1) {
+            const float* ph = shared_slot(L, u, __builtin_ctzll(m)) + (size_t)h * (D + 4);
+            const float wt = __builtin_amdgcn_exp2f(ph[D] - M);  // a helper's block has 32 valid rows
+            O += wt * ph[c];
+            Ls += wt * ph[D + 1];
+        }
+        ((uint16_t*)io.out)[((size_t)u * G + h) * D + c] = f2bf(O / Ls);
+    }
+}
+
 // ---------------------------------------------------------------------------
 // Step kernel, bf16 pools. One workgroup of NW wavefronts per (unit, split).
 //
@@ -464,11 +564,13 @@ __global__ __launch_bounds__(NW * 64) __attribute__((amdgpu_waves_per_eu(1, 2)))
     __shared__ float s_m[NW][16];
     __shared__ float s_l[NW][16];
     __shared__ RetShared ret;
-    __shared__ int s_next;  // next unclaimed block
+    __shared__ int s_next;  // next unclaimed block index
+    __shared__ int s_sh;    // shared blocks the owner's wavefronts took
+    __shared__ int s_last;  // the owner completed the unit's done count
 
     const int G = L.G, S = L.S, ps = L.ps;
-    double2* s_q2 = reinterpret_cast<double2*>(smem);  // [G][D] (q+, q-)
-    float* s_o = reinterpret_cast<float*>(s_q2 + (size_t)G * D);  // [NW][G][D+4]
+    double2* s_q2 = reinterpret_cast<double2*>(smem);  // [G][D+8] (q+, q-), padded: qpad_index
+    float* s_o = reinterpret_cast<float*>(s_q2 + (size_t)G * (D + 8));  // [NW][G][D+4]
     double* s_score = reinterpret_cast<double*>(s_o + (size_t)NW * G * (D + 4));  // [S], fused only
     int* s_state = reinterpret_cast<int*>(s_score + S);  // [S], fused only
     int* s_ts = s_state + S;
@@ -479,32 +581,18 @@ __global__ __launch_bounds__(NW * 64) __attribute__((amdgpu_waves_per_eu(1, 2)))
     const int nsplit = L.nsplit;
     const int u = blockIdx.x / nsplit, split = blockIdx.x - (blockIdx.x / nsplit) * nsplit;
     const size_t base = (size_t)u * S;
-    const UnitRec ur = read_unit(L, u);
-    const int ns = ur.ns, nf = ur.nf;
-    const bool opened = ur.opened();
-    const int pinned = L.unit[(size_t)u * kUnitFields + kPinnedPages];
-    const int row_new = ns * ps + nf, b_new = row_new >> 5, tt_new = row_new & 31;
     const int nblk = L.Lcap / 32;
     const int b0 = split * L.bps;
     const int b1 = min(nblk, b0 + L.bps);
-    // pages scored here: those whose first row lies in this workgroup's blocks, pinned ones excepted
-    const int sl0 = max(pinned, min(S, (32 * b0 + ps - 1) / ps)), sl1 = min(S, (32 * b1 + ps - 1) / ps);
+    // block sharing (fused only): block index i < nown maps to a block outside
+    // the shared range [sh0, sh0 + nsh), which the owner claims from memory last
+    const int nsh = L.nsh, sh0 = L.sh0, nown = (b1 - b0) - nsh;
     const uint16_t* qg = (const uint16_t*)io.q + (size_t)u * G * D;
     const uint16_t* kn_g = (const uint16_t*)io.k_new + (size_t)u * D;
     const uint16_t* vn_g = (const uint16_t*)io.v_new + (size_t)u * D;
     const uint16_t* Ku = (const uint16_t*)L.K + (size_t)u * L.Lcap * D;
     const uint16_t* Vu = (const uint16_t*)L.V + (size_t)u * L.Lcap * D;
     const int32_t* fu = L.fill + base;
-
-    // fill of the page holding this lane's 8 rows of block b (page_size % 8 == 0)
-    auto row_fill = [&](int b) {
-        const int slot = (32 * b + 8 * grp) / ps;
-        return (slot < S) ? (slot == ns ? nf + 1 : fu[slot]) : 0;
-    };
-    auto valid_rows = [&](int b, int f) {
-        const int t0 = 32 * b + 8 * grp;
-        return min(max(f - (t0 - (t0 / ps) * ps), 0), 8);
-    };
     auto load_block = [&](int b, u32x4 (&kr)[2][KS], u32x4 (&vr)[NB]) {
         const uint16_t* Kb = Ku + (size_t)b * BLK + lane * 8;
         const uint16_t* Vb = Vu + (size_t)b * BLK + lane * 8;
@@ -516,27 +604,66 @@ __global__ __launch_bounds__(NW * 64) __attribute__((amdgpu_waves_per_eu(1, 2)))
         for (int nb = 0; nb < NB; ++nb) vr[nb] = ld4(Vb + nb * 512);
     };
 
-    // staging loads first, so that waiting for them leaves the block loads in flight
-    for (int i = tid; i < G * D; i += NW * 64) {
-        const double x = (double)bf2f(qg[i]);
-        s_q2[i] = double2{x > 0.0 ? x : 0.0, x < 0.0 ? x : 0.0};
-    }
-    if (fused) load_slots(L, u, ur, s_score, s_state, s_ts, s_lid);
-    if (tid == 0) s_next = b0 + 2 * NW;  // claims start after the two static blocks of every wavefront
-
-    int b = b0 + w;  // first and second blocks (b0 + w + NW): static
-    int f_next = 0;
+    // the first block's K/V and the queries go out before anything else:
+    // the first block depends on no state (claim index w is static)
+    int b = (w < nown) ? b0 + (w < sh0 ? w : w + nsh) : b1;
     u32x4 kr_next[2][KS], vr_next[NB];
-    if (b < b1) {
-        f_next = row_fill(b);
-        load_block(b, kr_next, vr_next);
-    }
+    if (b < b1) load_block(b, kr_next, vr_next);
     bf16x8 qv[KS];
 #pragma unroll
     for (int ks = 0; ks < KS; ++ks) {
         const u32x4 x = (col < G) ? ld4(qg + (size_t)col * D + 32 * ks + 8 * grp) : u32x4{0u, 0u, 0u, 0u};
         qv[ks] = __builtin_bit_cast(bf16x8, x);
     }
+
+    const UnitRec ur = read_unit(L, u);
+    const int ns = ur.ns, nf = ur.nf;
+    const bool opened = ur.opened();
+    const int pinned = L.unit[(size_t)u * kUnitFields + kPinnedPages];
+    const int row_new = ns * ps + nf, b_new = row_new >> 5, tt_new = row_new & 31;
+    const int par = ur.clock & 1;
+    int32_t* co = coord_rec(L, par, u);
+    if (split == 0 && tid < kCoordFields) coord_rec(L, par ^ 1, u)[tid] = 0;  // the next step's record
+    int my_sh = 0;  // shared blocks this wavefront took (lane 0)
+    // the block of claim index i, or b1 when none is left
+    auto take = [&](int i) -> int {
+        if (i < nown) return b0 + (i < sh0 ? i : i + nsh);
+        if (nsh == 0) return b1;
+        const int c = __hip_atomic_fetch_add(co + kClaim, 1, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+        if (c >= nsh) return b1;
+        ++my_sh;
+        return sh0 + c;
+    };
+    if (w >= nown) {  // fewer own blocks than wavefronts: the first block is a claim
+        if (lane == 0) b = take(w);
+        b = __builtin_amdgcn_readfirstlane(b);
+        if (b < b1) load_block(b, kr_next, vr_next);
+    }
+    // pages scored here: those whose first row lies in this workgroup's blocks, pinned ones excepted
+    const int sl0 = max(pinned, min(S, (32 * b0 + ps - 1) / ps)), sl1 = min(S, (32 * b1 + ps - 1) / ps);
+
+    // fill of the page holding this lane's 8 rows of block b (page_size % 8 == 0)
+    auto row_fill = [&](int b) {
+        const int slot = (32 * b + 8 * grp) / ps;
+        return (slot < S) ? (slot == ns ? nf + 1 : fu[slot]) : 0;
+    };
+    auto valid_rows = [&](int b, int f) {
+        const int t0 = 32 * b + 8 * grp;
+        return min(max(f - (t0 - (t0 / ps) * ps), 0), 8);
+    };
+    int f_next = (b < b1) ? row_fill(b) : 0;
+
+    // staging for the scores and the epilogue
+    for (int i = tid; i < G * D; i += NW * 64) {
+        const double x = (double)bf2f(qg[i]);
+        s_q2[qpad_index<D>(i)] = double2{x > 0.0 ? x : 0.0, x < 0.0 ? x : 0.0};
+    }
+    if (fused) load_slots(L, u, ur, s_score, s_state, s_ts, s_lid);
+    if (tid == 0) {
+        s_next = 2 * NW;  // claims start after the two static blocks of every wavefront
+        s_sh = 0;
+    }
+
     float m_run = -INFINITY, l_run = 0.0f;
     f32x4 acc[NB];
 #pragma unroll
@@ -592,11 +719,9 @@ __global__ __launch_bounds__(NW * 64) __attribute__((amdgpu_waves_per_eu(1, 2)))
             for (int ks = 0; ks < KS; ++ks) kr[qq][ks] = kr_next[qq][ks];
 #pragma unroll
         for (int nb = 0; nb < NB; ++nb) vr[nb] = vr_next[nb];
-        int bn = b + NW;
-        if (it > 0) {
-            if (lane == 0) bn = atomicAdd(&s_next, 1);  // one claim per wavefront
-            bn = __builtin_amdgcn_readfirstlane(bn);
-        }
+        int bn = b1;
+        if (lane == 0) bn = take(it == 0 ? w + NW : atomicAdd(&s_next, 1));  // one claim per wavefront
+        bn = __builtin_amdgcn_readfirstlane(bn);
         if (bn < b1) {
             f_next = row_fill(bn);
             load_block(bn, kr_next, vr_next);
@@ -633,44 +758,7 @@ __global__ __launch_bounds__(NW * 64) __attribute__((amdgpu_waves_per_eu(1, 2)))
                 for (int c = lane; c < D; c += 64) Vw[v_off<D>(row_new, c)] = vn_g[c];
             }
 
-            f32x4 s0 = {0.f, 0.f, 0.f, 0.f}, s1 = {0.f, 0.f, 0.f, 0.f};
-#pragma unroll
-            for (int ks = 0; ks < KS; ++ks) {
-                s0 = __builtin_amdgcn_mfma_f32_16x16x32_bf16(__builtin_bit_cast(bf16x8, kr[0][ks]), qv[ks], s0, 0, 0, 0);
-                s1 = __builtin_amdgcn_mfma_f32_16x16x32_bf16(__builtin_bit_cast(bf16x8, kr[1][ks]), qv[ks], s1, 0, 0, 0);
-            }
-            // x[j]: scaled logit of token 8*grp + j for head `col` (base 2)
-            float x[8];
-#pragma unroll
-            for (int v = 0; v < 4; ++v) {
-                x[v] = (v < nv) ? s0[v] * scale_log2 : -INFINITY;
-                x[4 + v] = (4 + v < nv) ? s1[v] * scale_log2 : -INFINITY;
-            }
-            float mb = x[0];
-#pragma unroll
-            for (int j = 1; j < 8; ++j) mb = fmaxf(mb, x[j]);
-            mb = fmaxf(mb, __shfl_xor(mb, 16));
-            mb = fmaxf(mb, __shfl_xor(mb, 32));
-            const float m_new = fmaxf(m_run, mb);
-            if (__ballot(m_new > m_run) != 0ull) {
-                const float alpha = __builtin_amdgcn_exp2f(m_run - m_new);
-                l_run *= alpha;
-#pragma unroll
-                for (int nb = 0; nb < NB; ++nb) acc[nb] *= alpha;
-                m_run = m_new;
-            }
-            float psum = 0.0f;
-            bf16x8 pb;
-#pragma unroll
-            for (int j = 0; j < 8; ++j) {
-                const float pj = __builtin_amdgcn_exp2f(x[j] - m_run);
-                psum += pj;
-                pb[j] = (__bf16)pj;
-            }
-            l_run += psum;
-#pragma unroll
-            for (int nb = 0; nb < NB; ++nb)
-                acc[nb] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(__builtin_bit_cast(bf16x8, vr[nb]), pb, acc[nb], 0, 0, 0);
+            attend_block<D>(kr, vr, nv, qv, scale_log2, m_run, l_run, acc);
         }
         // this block's registers are free again
         if (it == 0) staged();
@@ -683,6 +771,7 @@ __global__ __launch_bounds__(NW * 64) __attribute__((amdgpu_waves_per_eu(1, 2)))
     while (pass < npass) score_step();  // passes left when the wavefront ran out of blocks
     if (!decided) scores_done();
 
+    if (lane == 0 && my_sh > 0) atomicAdd(&s_sh, my_sh);
     // park this wavefront's partial attention in LDS
     l_run += __shfl_xor(l_run, 16);
     l_run += __shfl_xor(l_run, 32);
@@ -697,7 +786,9 @@ __global__ __launch_bounds__(NW * 64) __attribute__((amdgpu_waves_per_eu(1, 2)))
     }
     lds_barrier();  // partials parked, retention decided
 
-    // merge the wavefronts' partial outputs
+    // merge the wavefronts' partial outputs; when helpers took shared
+    // blocks, into the owner's slot in memory
+    const bool via_memory = fused && nsh > 0 && s_sh != nsh;
     for (int idx = tid; idx < G * D; idx += NW * 64) {
         const int h = idx / D, c = idx - (idx / D) * D;
         float M = -INFINITY;
@@ -711,7 +802,14 @@ __global__ __launch_bounds__(NW * 64) __attribute__((amdgpu_waves_per_eu(1, 2)))
             O += wt * s_o[((size_t)ww * G + h) * (D + 4) + c];
             Ls += wt * s_l[ww][h];
         }
-        if (fused) {
+        if (via_memory) {
+            float* po = shared_slot(L, u, nsh) + (size_t)h * (D + 4);
+            po[c] = O;
+            if (c == 0) {
+                po[D] = M;
+                po[D + 1] = Ls;
+            }
+        } else if (fused) {
             ((uint16_t*)io.out)[((size_t)u * G + h) * D + c] = f2bf(O / Ls);
         } else {
             float* pp = L.part + (((size_t)u * nsplit + split) * G + h) * (D + 2);
@@ -723,6 +821,106 @@ __global__ __launch_bounds__(NW * 64) __attribute__((amdgpu_waves_per_eu(1, 2)))
         }
     }
     if (fused) retention_store(L, io, u, ur, s_state, s_ts, s_lid, ret, tid, NW * 64);
+    if (nsh == 0) return;
+
+    if (via_memory) {  // add the owner's blocks to the done count; the last contributor merges
+        // every wavefront's slot stores complete (vmcnt 0) before the barrier,
+        // so the one release below writes all of them back
+        __builtin_amdgcn_s_waitcnt(0x0F70);
+        __syncthreads();
+        if (tid == 0) {
+            const int mine = nown + s_sh;
+            __builtin_amdgcn_fence(__ATOMIC_RELEASE, "agent");
+            const int old = __hip_atomic_fetch_add(co + kDone, mine, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+            if (old + mine == nblk) __builtin_amdgcn_fence(__ATOMIC_ACQUIRE, "agent");
+            s_last = old + mine == nblk;
+        }
+        __syncthreads();
+        if (s_last) {
+            const uint64_t mask = __hip_atomic_load((uint64_t*)(co + kMaskLo), __ATOMIC_RELAXED,
+                                                    __HIP_MEMORY_SCOPE_AGENT);
+            finish_shared(L, io, u, mask, tid, NW * 64);
+        }
+    }
+
+    // help: take shared blocks of the units with the most left unclaimed
+    const unsigned rot = (unsigned)(((size_t)blockIdx.x * NW + w) * 2654435761u % (unsigned)L.U);
+    for (;;) {
+        unsigned long long best = 0;
+        for (int v0 = 0; v0 < L.U; v0 += 64) {
+            const int v = v0 + lane;
+            if (v < L.U) {
+                const int cl = __hip_atomic_load(coord_rec(L, par, v) + kClaim, __ATOMIC_RELAXED,
+                                                 __HIP_MEMORY_SCOPE_AGENT);
+                if (cl < nsh) {
+                    const unsigned dist = ((unsigned)v + (unsigned)L.U - rot) % (unsigned)L.U;
+                    const unsigned long long key = ((unsigned long long)(nsh - cl) << 32) | (0xFFFFFFFFu - dist);
+                    best = key > best ? key : best;
+                }
+            }
+        }
+#pragma unroll
+        for (int off = 32; off >= 1; off >>= 1) {
+            const unsigned long long o = __shfl_xor(best, off);
+            best = o > best ? o : best;
+        }
+        if (best == 0) break;
+        const int u2 = (int)((rot + (0xFFFFFFFFu - (unsigned)(best & 0xFFFFFFFFull))) % (unsigned)L.U);
+        int32_t* co2 = coord_rec(L, par, u2);
+        int c = nsh;
+        if (lane == 0) c = __hip_atomic_fetch_add(co2 + kClaim, 1, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+        c = __builtin_amdgcn_readfirstlane(c);
+        if (c >= nsh) continue;
+
+        // shared block sh0 + c of unit u2: full pinned rows, nothing to substitute
+        const size_t boff = (size_t)u2 * L.Lcap * D + (size_t)(sh0 + c) * BLK + lane * 8;
+        const uint16_t* Kb = (const uint16_t*)L.K + boff;
+        const uint16_t* Vb = (const uint16_t*)L.V + boff;
+        u32x4 kr[2][KS], vr[NB];
+#pragma unroll
+        for (int qq = 0; qq < 2; ++qq)
+#pragma unroll
+            for (int ks = 0; ks < KS; ++ks) kr[qq][ks] = ld4(Kb + (qq * KS + ks) * 512);
+#pragma unroll
+        for (int nb = 0; nb < NB; ++nb) vr[nb] = ld4(Vb + nb * 512);
+        const uint16_t* q2 = (const uint16_t*)io.q + (size_t)u2 * G * D;
+        bf16x8 qh[KS];
+#pragma unroll
+        for (int ks = 0; ks < KS; ++ks) {
+            const u32x4 x = (col < G) ? ld4(q2 + (size_t)col * D + 32 * ks + 8 * grp) : u32x4{0u, 0u, 0u, 0u};
+            qh[ks] = __builtin_bit_cast(bf16x8, x);
+        }
+        float mh = -INFINITY, lh = 0.0f;
+        f32x4 ah[NB];
+#pragma unroll
+        for (int nb = 0; nb < NB; ++nb) ah[nb] = f32x4{0.f, 0.f, 0.f, 0.f};
+        attend_block<D>(kr, vr, 8, qh, scale_log2, mh, lh, ah);
+        lh += __shfl_xor(lh, 16);
+        lh += __shfl_xor(lh, 32);
+        float* ph = shared_slot(L, u2, c);
+        if (col < G) {
+#pragma unroll
+            for (int nb = 0; nb < NB; ++nb)
+                *reinterpret_cast<f32x4*>(&ph[(size_t)col * (D + 4) + 16 * nb + 4 * grp]) = ah[nb];
+            if (grp == 0) {
+                ph[(size_t)col * (D + 4) + D] = mh;
+                ph[(size_t)col * (D + 4) + D + 1] = lh;
+            }
+        }
+        int last = 0;
+        if (lane == 0) {
+            __hip_atomic_fetch_or((uint64_t*)(co2 + kMaskLo), 1ull << c, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+            __builtin_amdgcn_fence(__ATOMIC_RELEASE, "agent");  // the slot and the mask bit, then the count
+            last = __hip_atomic_fetch_add(co2 + kDone, 1, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT) + 1 == nblk;
+            if (last) __builtin_amdgcn_fence(__ATOMIC_ACQUIRE, "agent");
+        }
+        last = __builtin_amdgcn_readfirstlane(last);
+        if (last) {
+            const uint64_t mask = __hip_atomic_load((uint64_t*)(co2 + kMaskLo), __ATOMIC_RELAXED,
+                                                    __HIP_MEMORY_SCOPE_AGENT);
+            finish_shared(L, io, u2, mask, lane, 64);
+        }
+    }
 }
 
 // Step kernel, fp32 pools: one wavefront per (unit, split), one token at a
@@ -887,7 +1085,7 @@ inline unsigned grid1d(size_t n, int block) { return (unsigned)((n + block - 1) 
 // LDS of the step kernel: (q+, q-) pairs in fp64, the attention wavefronts'
 // partial outputs, and the fused epilogue's slot arrays
 size_t step_lds(int G, int D, int S, int NW, bool fused) {
-    size_t b = (size_t)16 * G * D + (size_t)NW * G * (D + 4) * 4;
+    size_t b = (size_t)16 * G * (D + 8) + (size_t)NW * G * (D + 4) * 4;
     if (fused) b += (size_t)S * 20;
     return b;
 }
@@ -904,9 +1102,9 @@ hipError_t launch_step_bf16(const LayerView& L, const StepIO& io, const StepPlan
 
 // ---------------------------------------------------------------------------
 
-StepPlan plan_step(int U, int G, int D, int S, int Lcap, int ps, int pinned, bool bf16, int split_override) {
+StepPlan plan_step(int U, int G, int D, int S, int Lcap, int ps, int full_rows, bool bf16, int split_override,
+                   int share_override) {
     (void)ps;
-    (void)pinned;
     StepPlan pl{};
     const int nblk = Lcap / kBlockTokens;
     int want;
@@ -936,6 +1134,21 @@ StepPlan plan_step(int U, int G, int D, int S, int Lcap, int ps, int pinned, boo
     pl.nsplit = (nblk + pl.bps - 1) / pl.bps;
     pl.fused = bf16 && pl.nsplit == 1 && step_lds(G, D, S, pl.waves, true) <= kMaxLds;
     pl.lds = bf16 ? step_lds(G, D, S, pl.waves, pl.fused) : 0;
+    // block sharing: the last full pinned blocks of every unit, while a
+    // helper's scan of the per-unit counters stays short; off unless asked
+    // for (a helper's block costs more latency than it saves at the end of
+    // a step)
+    pl.nsh = 0;
+    pl.sh0 = 0;
+    if (pl.fused && U <= 4096) {
+        const int pb = full_rows / kBlockTokens;
+        int n = share_override >= 0 ? share_override : 0;
+        n = std::min(std::min(n, pb), kMaxShared);
+        if (n > 0) {
+            pl.nsh = n;
+            pl.sh0 = pb - n;
+        }
+    }
     return pl;
 }
 
