@@ -204,23 +204,26 @@ __device__ void load_slots(const LayerView& L, int u, const UnitRec& ur, double*
 // ---------------------------------------------------------------------------
 // Page scores (Section 3.3, Quest's representative keys): for each evictable
 // page, max over the G query heads of sum_c max(q_c*kmax_c, q_c*kmin_c), in
-// fp64. With q+ = max(q, 0) and q- = min(q, 0) the selected product is
-// q+*kmax + q-*kmin, one of the two terms being an exact zero; products of
-// bf16 values are exact in fp64, so each fused multiply-add rounds exactly as
-// an add of the exact product. Eight lanes per page: lane part p sums D/8
-// consecutive channels in order, the eight parts combine through a fixed xor
-// tree, so equal pages score equal. A wavefront scores 8 pages per pass; its
-// passes are interleaved with its attention blocks, each pass's keys loading
-// while the previous block computes. The page the step writes to has its
-// min/max widened by the new key and stored back.
+// fp64. The larger product is q_c times kmax_c when q_c > 0 and kmin_c
+// otherwise (both are zero when q_c = 0), so each channel takes one selected
+// key and one fused multiply-add; products of bf16 values are exact in fp64,
+// so each multiply-add rounds exactly as an add of the exact product. Eight
+// lanes per page: lane part p sums D/8 consecutive channels in two chains
+// (even and odd channels), the eight parts combine through a fixed xor tree,
+// so equal pages score equal. A wavefront scores 8 pages per pass; its passes
+// are interleaved with its attention blocks, each pass's keys loading while
+// the previous block computes. The page the step writes to has its min/max
+// widened by the new key and stored back.
 
-// LDS slot of element i = head * D + channel of the fp64 (q+, q-) array: one
+// LDS slot of element i = head * D + channel of the fp64 query array: a
 // 16-byte pad after each D/8 channels, so that the eight lanes scoring a
-// page, which read channels D/8 apart, fall on different LDS banks.
+// page, which read channel pairs D/8 apart, fall on different LDS banks and
+// every pair stays 16-byte aligned.
+constexpr int qpad_row(int D) { return D + 16; }
 template <int D>
 __device__ __forceinline__ int qpad_index(int i) {
     const int h = i / D, c = i - (i / D) * D;
-    return h * (D + 8) + c + c / (D / 8);
+    return h * qpad_row(D) + c + 2 * (c / (D / 8));
 }
 
 template <int D>
@@ -245,7 +248,7 @@ __device__ __forceinline__ void score_issue(const LayerView& L, int u, int p, in
 template <int D>
 __device__ __forceinline__ double score_finish(const LayerView& L, int u, int p, int part, bool act,
                                                ScoreFrag<D>& f, bool is_tail, bool opened,
-                                               const uint16_t* __restrict__ k_new, const double2* q2) {
+                                               const uint16_t* __restrict__ k_new, const double* qd) {
     constexpr int SV = ScoreFrag<D>::SV;
     const int G = L.G;
     if (act && is_tail) {
@@ -277,24 +280,30 @@ __device__ __forceinline__ double score_finish(const LayerView& L, int u, int p,
         }
     }
     const int c0 = part * (D / 8);
+    // the keys widened to fp32 once for all heads (exact for bf16)
+    float kxf[D / 8], knf[D / 8];
+#pragma unroll
+    for (int i = 0; i < SV; ++i)
+#pragma unroll
+        for (int e = 0; e < 8; ++e) {
+            kxf[8 * i + e] = bf2f(u16_at(f.kx[i], e));
+            knf[8 * i + e] = bf2f(u16_at(f.kn[i], e));
+        }
     double best = -INFINITY;
 #pragma unroll 1
     for (int j = 0; j < G; ++j) {
-        const double2* qj = q2 + (size_t)j * (D + 8) + c0 + part;  // padded rows: see qpad_index
-        double a = 0.0;
-        // the keys stay packed: widening them once for all heads would need 4x the registers
+        const double* qj = qd + (size_t)j * qpad_row(D) + c0 + 2 * part;  // see qpad_index
+        double a0 = 0.0, a1 = 0.0;  // even and odd channels
+        // keep the fp64 widening inside the loop: hoisted, it needs twice the registers
 #pragma unroll
-        for (int i = 0; i < SV; ++i) asm volatile("" : "+v"(f.kx[i]), "+v"(f.kn[i]));
+        for (int c = 0; c < D / 8; ++c) asm volatile("" : "+v"(kxf[c]), "+v"(knf[c]));
 #pragma unroll
-        for (int i = 0; i < SV; ++i) {
-            __builtin_amdgcn_sched_barrier(0);  // keep each octet's q reads next to their use
-#pragma unroll
-            for (int e = 0; e < 8; ++e) {
-                const double2 qq = qj[8 * i + e];
-                a = fma(qq.x, (double)bf2f(u16_at(f.kx[i], e)), a);
-                a = fma(qq.y, (double)bf2f(u16_at(f.kn[i], e)), a);
-            }
+        for (int c = 0; c < D / 8; c += 2) {
+            const double2 qq = *reinterpret_cast<const double2*>(qj + c);
+            a0 = fma(qq.x, (double)(qq.x > 0.0 ? kxf[c] : knf[c]), a0);
+            a1 = fma(qq.y, (double)(qq.y > 0.0 ? kxf[c + 1] : knf[c + 1]), a1);
         }
+        double a = a0 + a1;
         a += __shfl_xor(a, 1);
         a += __shfl_xor(a, 2);
         a += __shfl_xor(a, 4);
@@ -569,8 +578,8 @@ __global__ __launch_bounds__(NW * 64) __attribute__((amdgpu_waves_per_eu(1, 2)))
     __shared__ int s_last;  // the owner completed the unit's done count
 
     const int G = L.G, S = L.S, ps = L.ps;
-    double2* s_q2 = reinterpret_cast<double2*>(smem);  // [G][D+8] (q+, q-), padded: qpad_index
-    float* s_o = reinterpret_cast<float*>(s_q2 + (size_t)G * (D + 8));  // [NW][G][D+4]
+    double* s_qd = reinterpret_cast<double*>(smem);  // [G][D+16] q in fp64, padded: qpad_index
+    float* s_o = reinterpret_cast<float*>(s_qd + (size_t)G * qpad_row(D));  // [NW][G][D+4]
     double* s_score = reinterpret_cast<double*>(s_o + (size_t)NW * G * (D + 4));  // [S], fused only
     int* s_state = reinterpret_cast<int*>(s_score + S);  // [S], fused only
     int* s_ts = s_state + S;
@@ -656,7 +665,7 @@ __global__ __launch_bounds__(NW * 64) __attribute__((amdgpu_waves_per_eu(1, 2)))
     // staging for the scores and the epilogue
     for (int i = tid; i < G * D; i += NW * 64) {
         const double x = (double)bf2f(qg[i]);
-        s_q2[qpad_index<D>(i)] = double2{x > 0.0 ? x : 0.0, x < 0.0 ? x : 0.0};
+        s_qd[qpad_index<D>(i)] = x;
     }
     if (fused) load_slots(L, u, ur, s_score, s_state, s_ts, s_lid);
     if (tid == 0) {
@@ -680,7 +689,7 @@ __global__ __launch_bounds__(NW * 64) __attribute__((amdgpu_waves_per_eu(1, 2)))
     bool act_cur = false;
     auto score_step = [&]() {
         const int p = pass_page(pass);
-        const double sc = score_finish<D>(L, u, p, part, act_cur, frag, p == ns, opened, kn_g, s_q2);
+        const double sc = score_finish<D>(L, u, p, part, act_cur, frag, p == ns, opened, kn_g, s_qd);
         if (act_cur && part == 0) {
             if (fused) s_score[p] = sc;
             else L.score[base + p] = sc;
@@ -702,7 +711,7 @@ __global__ __launch_bounds__(NW * 64) __attribute__((amdgpu_waves_per_eu(1, 2)))
 
     // after the first block: the staging is visible and the score passes start
     auto staged = [&]() {
-        lds_barrier();  // (q+, q-), slot state and the block counter staged
+        lds_barrier();  // fp64 queries, slot state and the block counter staged
         if (npass > 0) {
             const int p = pass_page(0);
             act_cur = pass_act(p);
@@ -1082,10 +1091,10 @@ __global__ __launch_bounds__(256) void k_epilogue(LayerView L, StepIO io, double
 
 inline unsigned grid1d(size_t n, int block) { return (unsigned)((n + block - 1) / block); }
 
-// LDS of the step kernel: (q+, q-) pairs in fp64, the attention wavefronts'
+// LDS of the step kernel: the queries in fp64, the attention wavefronts'
 // partial outputs, and the fused epilogue's slot arrays
 size_t step_lds(int G, int D, int S, int NW, bool fused) {
-    size_t b = (size_t)16 * G * (D + 8) + (size_t)NW * G * (D + 4) * 4;
+    size_t b = (size_t)8 * G * qpad_row(D) + (size_t)NW * G * (D + 4) * 4;
     if (fused) b += (size_t)S * 20;
     return b;
 }
