@@ -55,6 +55,7 @@ struct LayerView {
     int U, G, D, ps, S, Lcap;
     int nsplit, bps;  // attention splits per unit, 32-token blocks per split
     int nsh, sh0;     // shared blocks per unit and the first of them (0: no sharing)
+    int rev;          // 1: this step visits blocks and page groups in descending order
     int bf16;         // 1: bf16 pool, 0: fp32 pool
 };
 

@@ -183,22 +183,27 @@ __device__ __forceinline__ UnitRec read_unit(const LayerView& L, int u) {
     return UnitRec{U4[kNextSlot], U4[kNextFill], U4[kClock], U4[kNextLid]};
 }
 
+// Stages slot s (state, timestamp, logical id as read from the pool) in LDS,
+// with the page the step opens already marked evictable.
+__device__ __forceinline__ void stage_slot(const UnitRec& ur, int s, int st, int t, int id, double* s_score,
+                                           int* s_state, int* s_ts, int* s_lid) {
+    if (s == ur.ns && ur.opened()) {
+        st = kEvictable;
+        t = ur.clock;
+        id = ur.next_lid;
+    }
+    s_state[s] = st;
+    s_ts[s] = t;
+    s_lid[s] = id;
+    s_score[s] = INFINITY;  // scored below when evictable; never ranks under a real score
+}
+
 __device__ void load_slots(const LayerView& L, int u, const UnitRec& ur, double* s_score, int* s_state,
-                           int* s_ts, int* s_lid) {
+                           int* s_ts, int* s_lid, int first = 0) {
     const int S = L.S;
     const size_t base = (size_t)u * S;
-    for (int s = threadIdx.x; s < S; s += blockDim.x) {
-        int st = L.state[base + s], t = L.ts[base + s], id = L.lid[base + s];
-        if (s == ur.ns && ur.opened()) {
-            st = kEvictable;
-            t = ur.clock;
-            id = ur.next_lid;
-        }
-        s_state[s] = st;
-        s_ts[s] = t;
-        s_lid[s] = id;
-        s_score[s] = INFINITY;  // scored below when evictable; never ranks under a real score
-    }
+    for (int s = threadIdx.x + first; s < S; s += blockDim.x)
+        stage_slot(ur, s, L.state[base + s], L.ts[base + s], L.lid[base + s], s_score, s_state, s_ts, s_lid);
 }
 
 // ---------------------------------------------------------------------------
@@ -613,22 +618,37 @@ __global__ __launch_bounds__(NW * 64) __attribute__((amdgpu_waves_per_eu(1, 2)))
         for (int nb = 0; nb < NB; ++nb) vr[nb] = ld4(Vb + nb * 512);
     };
 
-    // the first block's K/V and the queries go out before anything else:
-    // the first block depends on no state (claim index w is static)
-    int b = (w < nown) ? b0 + (w < sh0 ? w : w + nsh) : b1;
-    u32x4 kr_next[2][KS], vr_next[NB];
-    if (b < b1) load_block(b, kr_next, vr_next);
+    // Loads complete in issue order, so the small reads go out first: the
+    // unit record, this thread's staging elements and slot, the first
+    // block's fill and the queries; then the first block (its index w is
+    // static), which the staging below no longer waits for.
+    const int32_t* U4 = L.unit + (size_t)u * kUnitFields;
+    const UnitRec ur{U4[kNextSlot], U4[kNextFill], U4[kClock], U4[kNextLid]};
+    const int pinned = U4[kPinnedPages];
+    // claim index i of the own blocks, ascending or (L.rev) descending
+    auto blk_of = [&](int i) {
+        const int j = L.rev ? nown - 1 - i : i;
+        return b0 + (j < sh0 ? j : j + nsh);
+    };
+    int b = (w < nown) ? blk_of(w) : b1;
+    const int slot_first = (32 * b + 8 * grp) / ps;
+    const int fill_first = (b < b1 && slot_first < S) ? fu[slot_first] : 0;
+    // unconditional (clamped) reads: a read under a branch draws its first
+    // use into the branch, with a wait for it ahead of the block loads
+    const uint16_t q_first = qg[tid < G * D ? tid : 0];
+    const int s_first = tid < S ? tid : 0;
+    const int st_first = L.state[base + s_first], ts_first = L.ts[base + s_first], lid_first = L.lid[base + s_first];
     bf16x8 qv[KS];
 #pragma unroll
     for (int ks = 0; ks < KS; ++ks) {
         const u32x4 x = (col < G) ? ld4(qg + (size_t)col * D + 32 * ks + 8 * grp) : u32x4{0u, 0u, 0u, 0u};
         qv[ks] = __builtin_bit_cast(bf16x8, x);
     }
+    u32x4 kr_next[2][KS], vr_next[NB];
+    if (b < b1) load_block(b, kr_next, vr_next);
 
-    const UnitRec ur = read_unit(L, u);
     const int ns = ur.ns, nf = ur.nf;
     const bool opened = ur.opened();
-    const int pinned = L.unit[(size_t)u * kUnitFields + kPinnedPages];
     const int row_new = ns * ps + nf, b_new = row_new >> 5, tt_new = row_new & 31;
     const int par = ur.clock & 1;
     int32_t* co = coord_rec(L, par, u);
@@ -636,7 +656,7 @@ __global__ __launch_bounds__(NW * 64) __attribute__((amdgpu_waves_per_eu(1, 2)))
     int my_sh = 0;  // shared blocks this wavefront took (lane 0)
     // the block of claim index i, or b1 when none is left
     auto take = [&](int i) -> int {
-        if (i < nown) return b0 + (i < sh0 ? i : i + nsh);
+        if (i < nown) return blk_of(i);
         if (nsh == 0) return b1;
         const int c = __hip_atomic_fetch_add(co + kClaim, 1, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
         if (c >= nsh) return b1;
@@ -660,14 +680,16 @@ __global__ __launch_bounds__(NW * 64) __attribute__((amdgpu_waves_per_eu(1, 2)))
         const int t0 = 32 * b + 8 * grp;
         return min(max(f - (t0 - (t0 / ps) * ps), 0), 8);
     };
-    int f_next = (b < b1) ? row_fill(b) : 0;
+    int f_next = 0;
+    if (b < b1) f_next = (w < nown) ? (slot_first < S ? (slot_first == ns ? nf + 1 : fill_first) : 0) : row_fill(b);
 
     // staging for the scores and the epilogue
-    for (int i = tid; i < G * D; i += NW * 64) {
-        const double x = (double)bf2f(qg[i]);
-        s_qd[qpad_index<D>(i)] = x;
+    if (tid < G * D) s_qd[qpad_index<D>(tid)] = (double)bf2f(q_first);
+    for (int i = tid + NW * 64; i < G * D; i += NW * 64) s_qd[qpad_index<D>(i)] = (double)bf2f(qg[i]);
+    if (fused) {
+        if (tid < S) stage_slot(ur, tid, st_first, ts_first, lid_first, s_score, s_state, s_ts, s_lid);
+        load_slots(L, u, ur, s_score, s_state, s_ts, s_lid, NW * 64);
     }
-    if (fused) load_slots(L, u, ur, s_score, s_state, s_ts, s_lid);
     if (tid == 0) {
         s_next = 2 * NW;  // claims start after the two static blocks of every wavefront
         s_sh = 0;
@@ -680,7 +702,11 @@ __global__ __launch_bounds__(NW * 64) __attribute__((amdgpu_waves_per_eu(1, 2)))
 
     // score passes of this wavefront: 8 pages each, page = first + (lane >> 3)
     const int part = lane & 7;
-    auto pass_page = [&](int pass) { return sl0 + 8 * (pass * NW + w) + (lane >> 3); };
+    const int ngroups = (sl1 - sl0 + 7) / 8;  // 8-page groups, in the step's direction
+    auto pass_page = [&](int pass) {
+        const int g = pass * NW + w;
+        return sl0 + 8 * (L.rev ? ngroups - 1 - g : g) + (lane >> 3);
+    };
     auto pass_act = [&](int p) { return p < sl1 && (p == ns || L.state[base + p] == kEvictable); };
     const int npass = (sl1 - sl0 - 8 * w > 0) ? (sl1 - sl0 - 8 * w + 8 * NW - 1) / (8 * NW) : 0;
     const int npass_all = (sl1 - sl0 + 8 * NW - 1) / (8 * NW);  // passes of wavefront 0, the most

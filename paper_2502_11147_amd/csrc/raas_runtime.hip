@@ -64,6 +64,7 @@ struct raas_pool {
     std::vector<unsigned char> prefilled;
     std::vector<int> pinned;  // pinned prefill pages of each layer
     std::vector<int> full_rows;  // rows of full pinned pages of each layer
+    std::vector<unsigned char> descending;  // traversal direction of each layer's next step
     int split_override = 0;
     int share_override = -1;
     hipStream_t last_stream = nullptr;
@@ -94,6 +95,7 @@ LayerView view(const raas_pool* p, int layer) {
     L.coord = p->coord + (size_t)layer * 2 * p->U * kCoordFields;
     L.nsh = 0;
     L.sh0 = 0;
+    L.rev = 0;
     L.nsplit = 1;
     L.bps = p->Lcap / kBlockTokens;
     L.U = p->U;
@@ -204,6 +206,7 @@ raas_status raas_create_pool(const raas_config* cfg, void* stream, raas_pool** o
     p->prefilled.assign((size_t)cfg->n_layers, 0);
     p->pinned.assign((size_t)cfg->n_layers, 0);
     p->full_rows.assign((size_t)cfg->n_layers, 0);
+    p->descending.assign((size_t)cfg->n_layers, 0);
     const size_t Ly = (size_t)cfg->n_layers;
     const int nblk = p->Lcap / kBlockTokens;
     const int max_split = nblk < kMaxSplits ? nblk : kMaxSplits;
@@ -314,6 +317,10 @@ raas_status raas_decode_step(raas_pool* p, int32_t layer, const void* q, const v
     L.bps = pl.bps;
     L.nsh = pl.nsh;
     L.sh0 = pl.sh0;
+    // Successive steps of a layer read its pool in opposite directions, so a
+    // step starts with the blocks the previous one read last, the likeliest
+    // to be still in the GPU's memory-side cache.
+    L.rev = p->descending[layer];
 
     prof_record(p, 0, true, s);
     hipError_t e = launch_step(L, io, pl, (double)p->cfg.r, s);
@@ -325,6 +332,7 @@ raas_status raas_decode_step(raas_pool* p, int32_t layer, const void* q, const v
         prof_record(p, 1, false, s);
         if (e != hipSuccess) return hip_fail(e, "epilogue launch");
     }
+    p->descending[layer] ^= 1;
     p->last_stream = s;
     return RAAS_OK;
 }
