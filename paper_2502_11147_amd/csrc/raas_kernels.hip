@@ -253,7 +253,7 @@ __device__ __forceinline__ void score_issue(const LayerView& L, int u, int p, in
 template <int D>
 __device__ __forceinline__ double score_finish(const LayerView& L, int u, int p, int part, bool act,
                                                ScoreFrag<D>& f, bool is_tail, bool opened,
-                                               const uint16_t* __restrict__ k_new, const double* qd) {
+                                               const uint16_t* k_new, const double* qd) {
     constexpr int SV = ScoreFrag<D>::SV;
     const int G = L.G;
     if (act && is_tail) {
@@ -581,6 +581,8 @@ __global__ __launch_bounds__(NW * 64) __attribute__((amdgpu_waves_per_eu(1, 2)))
     __shared__ int s_next;  // next unclaimed block index
     __shared__ int s_sh;    // shared blocks the owner's wavefronts took
     __shared__ int s_last;  // the owner completed the unit's done count
+    __shared__ __align__(16) uint16_t s_kn[D];  // the new token's key and value, staged so that
+    __shared__ __align__(16) uint16_t s_vn[D];  // no read in the block loop waits on memory
 
     const int G = L.G, S = L.S, ps = L.ps;
     double* s_qd = reinterpret_cast<double*>(smem);  // [G][D+16] q in fp64, padded: qpad_index
@@ -636,6 +638,8 @@ __global__ __launch_bounds__(NW * 64) __attribute__((amdgpu_waves_per_eu(1, 2)))
     // unconditional (clamped) reads: a read under a branch draws its first
     // use into the branch, with a wait for it ahead of the block loads
     const uint16_t q_first = qg[tid < G * D ? tid : 0];
+    const int t_new = tid < D / 8 ? tid : 0;
+    const u32x4 kn_first = ld4(kn_g + 8 * t_new), vn_first = ld4(vn_g + 8 * t_new);
     const int s_first = tid < S ? tid : 0;
     const int st_first = L.state[base + s_first], ts_first = L.ts[base + s_first], lid_first = L.lid[base + s_first];
     bf16x8 qv[KS];
@@ -686,6 +690,10 @@ __global__ __launch_bounds__(NW * 64) __attribute__((amdgpu_waves_per_eu(1, 2)))
     // staging for the scores and the epilogue
     if (tid < G * D) s_qd[qpad_index<D>(tid)] = (double)bf2f(q_first);
     for (int i = tid + NW * 64; i < G * D; i += NW * 64) s_qd[qpad_index<D>(i)] = (double)bf2f(qg[i]);
+    if (tid < D / 8) {
+        st4(&s_kn[8 * tid], kn_first);
+        st4(&s_vn[8 * tid], vn_first);
+    }
     if (fused) {
         if (tid < S) stage_slot(ur, tid, st_first, ts_first, lid_first, s_score, s_state, s_ts, s_lid);
         load_slots(L, u, ur, s_score, s_state, s_ts, s_lid, NW * 64);
@@ -694,6 +702,9 @@ __global__ __launch_bounds__(NW * 64) __attribute__((amdgpu_waves_per_eu(1, 2)))
         s_next = 2 * NW;  // claims start after the two static blocks of every wavefront
         s_sh = 0;
     }
+    // the staging is visible: the first block is still in flight, and every
+    // wavefront reaches this point after the same short reads
+    lds_barrier();
 
     float m_run = -INFINITY, l_run = 0.0f;
     f32x4 acc[NB];
@@ -715,7 +726,7 @@ __global__ __launch_bounds__(NW * 64) __attribute__((amdgpu_waves_per_eu(1, 2)))
     bool act_cur = false;
     auto score_step = [&]() {
         const int p = pass_page(pass);
-        const double sc = score_finish<D>(L, u, p, part, act_cur, frag, p == ns, opened, kn_g, s_qd);
+        const double sc = score_finish<D>(L, u, p, part, act_cur, frag, p == ns, opened, s_kn, s_qd);
         if (act_cur && part == 0) {
             if (fused) s_score[p] = sc;
             else L.score[base + p] = sc;
@@ -735,9 +746,8 @@ __global__ __launch_bounds__(NW * 64) __attribute__((amdgpu_waves_per_eu(1, 2)))
         decided = true;
     };
 
-    // after the first block: the staging is visible and the score passes start
+    // after the first block: the first pass's keys start loading
     auto staged = [&]() {
-        lds_barrier();  // fp64 queries, slot state and the block counter staged
         if (npass > 0) {
             const int p = pass_page(0);
             act_cur = pass_act(p);
@@ -768,7 +778,7 @@ __global__ __launch_bounds__(NW * 64) __attribute__((amdgpu_waves_per_eu(1, 2)))
                 if (col == i_new) {
 #pragma unroll
                     for (int ks = 0; ks < KS; ++ks) {
-                        const u32x4 x = ld4(kn_g + 32 * ks + 8 * grp);
+                        const u32x4 x = ld4(&s_kn[32 * ks + 8 * grp]);
                         if (q_new == 0) kr[0][ks] = x; else kr[1][ks] = x;
                     }
                 }
@@ -776,7 +786,7 @@ __global__ __launch_bounds__(NW * 64) __attribute__((amdgpu_waves_per_eu(1, 2)))
                     const int j_new = tt_new & 7;
 #pragma unroll
                     for (int nb = 0; nb < NB; ++nb) {
-                        const uint32_t val = vn_g[16 * nb + col];
+                        const uint32_t val = s_vn[16 * nb + col];
 #pragma unroll
                         for (int h = 0; h < 4; ++h) {
                             if ((j_new >> 1) == h) {
@@ -789,8 +799,8 @@ __global__ __launch_bounds__(NW * 64) __attribute__((amdgpu_waves_per_eu(1, 2)))
                 // append: store the new token in the pool (Algorithm 1, "Store K_new and V_new")
                 uint16_t* Kw = (uint16_t*)L.K + (size_t)u * L.Lcap * D;
                 uint16_t* Vw = (uint16_t*)L.V + (size_t)u * L.Lcap * D;
-                if (lane < D / 8) st4(Kw + k_off<D>(row_new, lane * 8), ld4(kn_g + lane * 8));
-                for (int c = lane; c < D; c += 64) Vw[v_off<D>(row_new, c)] = vn_g[c];
+                if (lane < D / 8) st4(Kw + k_off<D>(row_new, lane * 8), ld4(&s_kn[lane * 8]));
+                for (int c = lane; c < D; c += 64) Vw[v_off<D>(row_new, c)] = s_vn[c];
             }
 
             attend_block<D>(kr, vr, nv, qv, scale_log2, m_run, l_run, acc);
