@@ -43,8 +43,6 @@ def parse():
     ap.add_argument("--seed", type=int, default=0)
     ap.add_argument("--ring", type=int, default=128, help="distinct input steps staged on device")
     ap.add_argument("--splits", type=int, default=0, help="attention splits per unit (0 = automatic)")
-    ap.add_argument("--share", type=int, default=-1,
-                    help="prompt blocks per unit other workgroups may take over (-1 automatic, 0 off)")
     ap.add_argument("--cpu-seconds", type=float, default=15.0, help="budget of the CPU oracle sample")
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--copy-calibration", action="store_true",
@@ -272,8 +270,6 @@ def main():
     pool = raas.Pool.for_workload(w)
     if args.splits:
         pool.set_attention_splits(args.splits)
-    if args.share >= 0:
-        pool.set_block_sharing(args.share)
     Kp, Vp = synth.prefill(w, args.seed, 0)
     pool.prefill(0, torch.from_numpy(Kp).to(dt).to(dev), torch.from_numpy(Vp).to(dt).to(dev))
     del Kp, Vp
@@ -359,7 +355,6 @@ def main():
             "budget_tokens": w.budget, "prefill_len": w.prefill_len, "r": w.r,
             "resident_tokens_per_unit_avg": float(res.mean()),
             "attention_splits": args.splits or "auto",
-            "shared_blocks": "auto" if args.share < 0 else args.share,
         },
         "step_hbm_gbs_algorithmic": round(step_b / (elapsed / args.steps) / 1e9, 1),
         "roofline": {

@@ -144,17 +144,6 @@ raas_status raas_export_state(raas_pool* pool, int32_t layer, int32_t* host_buf,
  * depend on it beyond floating-point rounding. Errors: RAAS_E_INVALID. */
 raas_status raas_set_attention_splits(raas_pool* pool, int32_t splits);
 
-/* Tuning: blocks of 32 prompt tokens per unit that other workgroups may take
- * over in a step. The last such blocks of every unit's pinned prompt pages
- * (full pages only: the decode step never writes them) are processed last by
- * the unit's own workgroup and can be taken by workgroups that have finished
- * their own unit; the partial results merge exactly like attention splits.
- * blocks < 0 restores the automatic choice, 0 turns sharing off; the value
- * is capped by the pinned prompt blocks and 62. Applies to bf16 pools when
- * one workgroup covers a unit. Results do not depend on it beyond
- * floating-point rounding. Errors: RAAS_E_INVALID. */
-raas_status raas_set_block_sharing(raas_pool* pool, int32_t blocks);
-
 /* Kernel timing with HIP events recorded on the call's stream around each
  * enabled kernel of raas_decode_step. mask bit i enables kernel i:
  * 0 the step kernel (attention, append, page scores, and the epilogue when a

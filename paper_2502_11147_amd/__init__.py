@@ -23,7 +23,7 @@ KERNELS = ("append", "attention", "merge", "score")
 EXPORTS = (
     "raas_create_pool", "raas_prefill", "raas_decode_step", "raas_destroy", "raas_last_error",
     "raas_abi_version", "raas_pool_bytes", "raas_export_state", "raas_set_attention_splits",
-    "raas_set_block_sharing", "raas_profile", "raas_profile_read",
+    "raas_profile", "raas_profile_read",
 )
 
 
@@ -78,8 +78,6 @@ def load_library(path: str = LIB_PATH) -> ctypes.CDLL:
     lib.raas_export_state.restype = i32
     lib.raas_set_attention_splits.argtypes = [vp, i32]
     lib.raas_set_attention_splits.restype = i32
-    lib.raas_set_block_sharing.argtypes = [vp, i32]
-    lib.raas_set_block_sharing.restype = i32
     lib.raas_profile.argtypes = [vp, i32]
     lib.raas_profile.restype = i32
     lib.raas_profile_read.argtypes = [vp, i32, ctypes.POINTER(ctypes.c_double), ctypes.POINTER(ctypes.c_int64)]
@@ -221,10 +219,6 @@ class Pool:
 
     def set_attention_splits(self, splits: int):
         _check(self.lib.raas_set_attention_splits(self._h, splits), "raas_set_attention_splits")
-
-    def set_block_sharing(self, blocks: int):
-        """Blocks per unit other workgroups may take over (-1 automatic, 0 off)."""
-        _check(self.lib.raas_set_block_sharing(self._h, blocks), "raas_set_block_sharing")
 
     def profile(self, mask: int):
         _check(self.lib.raas_profile(self._h, mask), "raas_profile")

@@ -24,15 +24,6 @@ constexpr int kUnitFields = 8;
 constexpr int kBlockTokens = 32;
 // Upper bound on attention splits per unit (sizes the partials buffer).
 constexpr int kMaxSplits = 64;
-// Upper bound on blocks per unit other workgroups may take over (one bit each
-// in a 64-bit mask; the owner's partial takes one more slot).
-constexpr int kMaxShared = 62;
-// Per-unit coordination record of block sharing, int32 each:
-//  claim     shared blocks claimed so far (by the owner or by helpers)
-//  done      blocks whose partial result is final
-//  mask      (two words) bit c set when a helper took shared block c
-enum CoordField : int { kClaim = 0, kDone = 1, kMaskLo = 2 };
-constexpr int kCoordFields = 4;
 // Dynamic LDS a step workgroup may use (gfx950 has 160 KiB per workgroup).
 constexpr size_t kMaxLds = 144 * 1024;
 
@@ -49,12 +40,9 @@ struct LayerView {
     int32_t* unit;   // [U][kUnitFields]
     int32_t* err;    // device flag, nonzero after an internal inconsistency
     double* score;   // [U][S] page scores (split path)
-    float* part;     // [U][nsplit][G][D+2] partial attention (split path), or
-                     // [U][nsh+1][G][D+4] (shared blocks, owner last)
-    int32_t* coord;  // [2][U][kCoordFields] block sharing, by clock parity
+    float* part;     // [U][nsplit][G][D+2] partial attention (split path)
     int U, G, D, ps, S, Lcap;
     int nsplit, bps;  // attention splits per unit, 32-token blocks per split
-    int nsh, sh0;     // shared blocks per unit and the first of them (0: no sharing)
     int rev;          // 1: this step visits blocks and page groups in descending order
     int bf16;         // 1: bf16 pool, 0: fp32 pool
 };
@@ -75,13 +63,9 @@ struct StepPlan {
     int nsplit, bps; // splits per unit and blocks per split
     bool fused;      // true: the step workgroup also runs the epilogue (nsplit == 1, bf16)
     size_t lds;      // dynamic LDS of the step kernel
-    int nsh, sh0;    // block sharing (fused only)
 };
 
-// full_rows: rows of the pinned prompt pages that are full (a multiple of the
-// page size); share_override < 0 automatic, 0 off, > 0 at most that many.
-StepPlan plan_step(int U, int G, int D, int S, int Lcap, int ps, int full_rows, bool bf16, int split_override,
-                   int share_override);
+StepPlan plan_step(int U, int G, int D, int S, int Lcap, int ps, int pinned, bool bf16, int split_override);
 // Lets the step kernels use more than the default dynamic LDS.
 hipError_t allow_large_lds();
 

@@ -505,48 +505,6 @@ __device__ __forceinline__ void attend_block(const u32x4 (&kr)[2][D / 32], const
         acc[nb] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(__builtin_bit_cast(bf16x8, vr[nb]), pb, acc[nb], 0, 0, 0);
 }
 
-// Block sharing. A unit's last nsh full pinned blocks are its shared blocks:
-// the decode step never writes them, so any workgroup may read them while
-// the unit's own workgroup (its owner) writes the unit's state. The owner
-// takes its other blocks first and then claims shared blocks from a counter
-// in memory; waves whose own unit is done claim shared blocks of other units
-// from the same counters. A helper parks its block's partial attention in
-// memory (slot c of the unit), the owner its merged partial (slot nsh), and
-// each adds its block count to the unit's done counter; whoever completes
-// the count merges the slots and writes the output. Counters come in two
-// sets by clock parity: a step uses one and its owner clears the unit's
-// record in the other for the next step. Nothing waits on another workgroup.
-
-__device__ __forceinline__ int32_t* coord_rec(const LayerView& L, int parity, int u) {
-    return L.coord + ((size_t)parity * L.U + u) * kCoordFields;
-}
-
-// partial slot s of unit u: [G][D+4] floats, channels then (max, sum) of each head
-__device__ __forceinline__ float* shared_slot(const LayerView& L, int u, int s) {
-    return L.part + ((size_t)u * (L.nsh + 1) + s) * L.G * (L.D + 4);
-}
-
-// Output of unit u from its owner's slot and the slots of the blocks helpers
-// took (mask bits); called after the done count completed and an acquire.
-__device__ void finish_shared(const LayerView& L, const StepIO& io, int u, uint64_t mask, int first, int stride) {
-    const int G = L.G, D = L.D, nsh = L.nsh;
-    for (int idx = first; idx < G * D; idx += stride) {
-        const int h = idx / D, c = idx - (idx / D) * D;
-        const float* po = shared_slot(L, u, nsh) + (size_t)h * (D + 4);
-        float M = po[D];
-        for (uint64_t m = mask; m; m &= m - 1) M = fmaxf(M, shared_slot(L, u, __builtin_ctzll(m))[(size_t)h * (D + 4) + D]);
-        const float wo = (po[D] == -INFINITY) ? 0.0f : __builtin_amdgcn_exp2f(po[D] - M);
-        float O = wo * po[c], Ls = wo * po[D + 1];
-        for (uint64_t m = mask; m; m &= m - 1) {
-            const float* ph = shared_slot(L, u, __builtin_ctzll(m)) + (size_t)h * (D + 4);
-            const float wt = __builtin_amdgcn_exp2f(ph[D] - M);  // a helper's block has 32 valid rows
-            O += wt * ph[c];
-            Ls += wt * ph[D + 1];
-        }
-        ((uint16_t*)io.out)[((size_t)u * G + h) * D + c] = f2bf(O / Ls);
-    }
-}
-
 // ---------------------------------------------------------------------------
 // Step kernel, bf16 pools. One workgroup of NW wavefronts per (unit, split).
 //
@@ -579,8 +537,6 @@ __global__ __launch_bounds__(NW * 64) __attribute__((amdgpu_waves_per_eu(1, 2)))
     __shared__ float s_l[NW][16];
     __shared__ RetShared ret;
     __shared__ int s_next;  // next unclaimed block index
-    __shared__ int s_sh;    // shared blocks the owner's wavefronts took
-    __shared__ int s_last;  // the owner completed the unit's done count
     __shared__ __align__(16) uint16_t s_kn[D];  // the new token's key and value, staged so that
     __shared__ __align__(16) uint16_t s_vn[D];  // no read in the block loop waits on memory
 
@@ -600,9 +556,7 @@ __global__ __launch_bounds__(NW * 64) __attribute__((amdgpu_waves_per_eu(1, 2)))
     const int nblk = L.Lcap / 32;
     const int b0 = split * L.bps;
     const int b1 = min(nblk, b0 + L.bps);
-    // block sharing (fused only): block index i < nown maps to a block outside
-    // the shared range [sh0, sh0 + nsh), which the owner claims from memory last
-    const int nsh = L.nsh, sh0 = L.sh0, nown = (b1 - b0) - nsh;
+    const int nown = b1 - b0;  // blocks of this workgroup
     const uint16_t* qg = (const uint16_t*)io.q + (size_t)u * G * D;
     const uint16_t* kn_g = (const uint16_t*)io.k_new + (size_t)u * D;
     const uint16_t* vn_g = (const uint16_t*)io.v_new + (size_t)u * D;
@@ -629,8 +583,7 @@ __global__ __launch_bounds__(NW * 64) __attribute__((amdgpu_waves_per_eu(1, 2)))
     const int pinned = U4[kPinnedPages];
     // claim index i of the own blocks, ascending or (L.rev) descending
     auto blk_of = [&](int i) {
-        const int j = L.rev ? nown - 1 - i : i;
-        return b0 + (j < sh0 ? j : j + nsh);
+        return b0 + (L.rev ? nown - 1 - i : i);
     };
     int b = (w < nown) ? blk_of(w) : b1;
     const int slot_first = (32 * b + 8 * grp) / ps;
@@ -654,24 +607,8 @@ __global__ __launch_bounds__(NW * 64) __attribute__((amdgpu_waves_per_eu(1, 2)))
     const int ns = ur.ns, nf = ur.nf;
     const bool opened = ur.opened();
     const int row_new = ns * ps + nf, b_new = row_new >> 5, tt_new = row_new & 31;
-    const int par = ur.clock & 1;
-    int32_t* co = coord_rec(L, par, u);
-    if (split == 0 && tid < kCoordFields) coord_rec(L, par ^ 1, u)[tid] = 0;  // the next step's record
-    int my_sh = 0;  // shared blocks this wavefront took (lane 0)
     // the block of claim index i, or b1 when none is left
-    auto take = [&](int i) -> int {
-        if (i < nown) return blk_of(i);
-        if (nsh == 0) return b1;
-        const int c = __hip_atomic_fetch_add(co + kClaim, 1, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
-        if (c >= nsh) return b1;
-        ++my_sh;
-        return sh0 + c;
-    };
-    if (w >= nown) {  // fewer own blocks than wavefronts: the first block is a claim
-        if (lane == 0) b = take(w);
-        b = __builtin_amdgcn_readfirstlane(b);
-        if (b < b1) load_block(b, kr_next, vr_next);
-    }
+    auto take = [&](int i) { return i < nown ? blk_of(i) : b1; };
     // pages scored here: those whose first row lies in this workgroup's blocks, pinned ones excepted
     const int sl0 = max(pinned, min(S, (32 * b0 + ps - 1) / ps)), sl1 = min(S, (32 * b1 + ps - 1) / ps);
 
@@ -700,7 +637,6 @@ __global__ __launch_bounds__(NW * 64) __attribute__((amdgpu_waves_per_eu(1, 2)))
     }
     if (tid == 0) {
         s_next = 2 * NW;  // claims start after the two static blocks of every wavefront
-        s_sh = 0;
     }
     // the staging is visible: the first block is still in flight, and every
     // wavefront reaches this point after the same short reads
@@ -816,7 +752,6 @@ __global__ __launch_bounds__(NW * 64) __attribute__((amdgpu_waves_per_eu(1, 2)))
     while (pass < npass) score_step();  // passes left when the wavefront ran out of blocks
     if (!decided) scores_done();
 
-    if (lane == 0 && my_sh > 0) atomicAdd(&s_sh, my_sh);
     // park this wavefront's partial attention in LDS
     l_run += __shfl_xor(l_run, 16);
     l_run += __shfl_xor(l_run, 32);
@@ -831,9 +766,7 @@ __global__ __launch_bounds__(NW * 64) __attribute__((amdgpu_waves_per_eu(1, 2)))
     }
     lds_barrier();  // partials parked, retention decided
 
-    // merge the wavefronts' partial outputs; when helpers took shared
-    // blocks, into the owner's slot in memory
-    const bool via_memory = fused && nsh > 0 && s_sh != nsh;
+    // merge the wavefronts' partial outputs
     for (int idx = tid; idx < G * D; idx += NW * 64) {
         const int h = idx / D, c = idx - (idx / D) * D;
         float M = -INFINITY;
@@ -847,14 +780,7 @@ __global__ __launch_bounds__(NW * 64) __attribute__((amdgpu_waves_per_eu(1, 2)))
             O += wt * s_o[((size_t)ww * G + h) * (D + 4) + c];
             Ls += wt * s_l[ww][h];
         }
-        if (via_memory) {
-            float* po = shared_slot(L, u, nsh) + (size_t)h * (D + 4);
-            po[c] = O;
-            if (c == 0) {
-                po[D] = M;
-                po[D + 1] = Ls;
-            }
-        } else if (fused) {
+        if (fused) {
             ((uint16_t*)io.out)[((size_t)u * G + h) * D + c] = f2bf(O / Ls);
         } else {
             float* pp = L.part + (((size_t)u * nsplit + split) * G + h) * (D + 2);
@@ -866,106 +792,6 @@ __global__ __launch_bounds__(NW * 64) __attribute__((amdgpu_waves_per_eu(1, 2)))
         }
     }
     if (fused) retention_store(L, io, u, ur, s_state, s_ts, s_lid, ret, tid, NW * 64);
-    if (nsh == 0) return;
-
-    if (via_memory) {  // add the owner's blocks to the done count; the last contributor merges
-        // every wavefront's slot stores complete (vmcnt 0) before the barrier,
-        // so the one release below writes all of them back
-        __builtin_amdgcn_s_waitcnt(0x0F70);
-        __syncthreads();
-        if (tid == 0) {
-            const int mine = nown + s_sh;
-            __builtin_amdgcn_fence(__ATOMIC_RELEASE, "agent");
-            const int old = __hip_atomic_fetch_add(co + kDone, mine, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
-            if (old + mine == nblk) __builtin_amdgcn_fence(__ATOMIC_ACQUIRE, "agent");
-            s_last = old + mine == nblk;
-        }
-        __syncthreads();
-        if (s_last) {
-            const uint64_t mask = __hip_atomic_load((uint64_t*)(co + kMaskLo), __ATOMIC_RELAXED,
-                                                    __HIP_MEMORY_SCOPE_AGENT);
-            finish_shared(L, io, u, mask, tid, NW * 64);
-        }
-    }
-
-    // help: take shared blocks of the units with the most left unclaimed
-    const unsigned rot = (unsigned)(((size_t)blockIdx.x * NW + w) * 2654435761u % (unsigned)L.U);
-    for (;;) {
-        unsigned long long best = 0;
-        for (int v0 = 0; v0 < L.U; v0 += 64) {
-            const int v = v0 + lane;
-            if (v < L.U) {
-                const int cl = __hip_atomic_load(coord_rec(L, par, v) + kClaim, __ATOMIC_RELAXED,
-                                                 __HIP_MEMORY_SCOPE_AGENT);
-                if (cl < nsh) {
-                    const unsigned dist = ((unsigned)v + (unsigned)L.U - rot) % (unsigned)L.U;
-                    const unsigned long long key = ((unsigned long long)(nsh - cl) << 32) | (0xFFFFFFFFu - dist);
-                    best = key > best ? key : best;
-                }
-            }
-        }
-#pragma unroll
-        for (int off = 32; off >= 1; off >>= 1) {
-            const unsigned long long o = __shfl_xor(best, off);
-            best = o > best ? o : best;
-        }
-        if (best == 0) break;
-        const int u2 = (int)((rot + (0xFFFFFFFFu - (unsigned)(best & 0xFFFFFFFFull))) % (unsigned)L.U);
-        int32_t* co2 = coord_rec(L, par, u2);
-        int c = nsh;
-        if (lane == 0) c = __hip_atomic_fetch_add(co2 + kClaim, 1, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
-        c = __builtin_amdgcn_readfirstlane(c);
-        if (c >= nsh) continue;
-
-        // shared block sh0 + c of unit u2: full pinned rows, nothing to substitute
-        const size_t boff = (size_t)u2 * L.Lcap * D + (size_t)(sh0 + c) * BLK + lane * 8;
-        const uint16_t* Kb = (const uint16_t*)L.K + boff;
-        const uint16_t* Vb = (const uint16_t*)L.V + boff;
-        u32x4 kr[2][KS], vr[NB];
-#pragma unroll
-        for (int qq = 0; qq < 2; ++qq)
-#pragma unroll
-            for (int ks = 0; ks < KS; ++ks) kr[qq][ks] = ld4(Kb + (qq * KS + ks) * 512);
-#pragma unroll
-        for (int nb = 0; nb < NB; ++nb) vr[nb] = ld4(Vb + nb * 512);
-        const uint16_t* q2 = (const uint16_t*)io.q + (size_t)u2 * G * D;
-        bf16x8 qh[KS];
-#pragma unroll
-        for (int ks = 0; ks < KS; ++ks) {
-            const u32x4 x = (col < G) ? ld4(q2 + (size_t)col * D + 32 * ks + 8 * grp) : u32x4{0u, 0u, 0u, 0u};
-            qh[ks] = __builtin_bit_cast(bf16x8, x);
-        }
-        float mh = -INFINITY, lh = 0.0f;
-        f32x4 ah[NB];
-#pragma unroll
-        for (int nb = 0; nb < NB; ++nb) ah[nb] = f32x4{0.f, 0.f, 0.f, 0.f};
-        attend_block<D>(kr, vr, 8, qh, scale_log2, mh, lh, ah);
-        lh += __shfl_xor(lh, 16);
-        lh += __shfl_xor(lh, 32);
-        float* ph = shared_slot(L, u2, c);
-        if (col < G) {
-#pragma unroll
-            for (int nb = 0; nb < NB; ++nb)
-                *reinterpret_cast<f32x4*>(&ph[(size_t)col * (D + 4) + 16 * nb + 4 * grp]) = ah[nb];
-            if (grp == 0) {
-                ph[(size_t)col * (D + 4) + D] = mh;
-                ph[(size_t)col * (D + 4) + D + 1] = lh;
-            }
-        }
-        int last = 0;
-        if (lane == 0) {
-            __hip_atomic_fetch_or((uint64_t*)(co2 + kMaskLo), 1ull << c, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
-            __builtin_amdgcn_fence(__ATOMIC_RELEASE, "agent");  // the slot and the mask bit, then the count
-            last = __hip_atomic_fetch_add(co2 + kDone, 1, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT) + 1 == nblk;
-            if (last) __builtin_amdgcn_fence(__ATOMIC_ACQUIRE, "agent");
-        }
-        last = __builtin_amdgcn_readfirstlane(last);
-        if (last) {
-            const uint64_t mask = __hip_atomic_load((uint64_t*)(co2 + kMaskLo), __ATOMIC_RELAXED,
-                                                    __HIP_MEMORY_SCOPE_AGENT);
-            finish_shared(L, io, u2, mask, lane, 64);
-        }
-    }
 }
 
 // Step kernel, fp32 pools: one wavefront per (unit, split), one token at a
@@ -1147,8 +973,8 @@ hipError_t launch_step_bf16(const LayerView& L, const StepIO& io, const StepPlan
 
 // ---------------------------------------------------------------------------
 
-StepPlan plan_step(int U, int G, int D, int S, int Lcap, int ps, int full_rows, bool bf16, int split_override,
-                   int share_override) {
+StepPlan plan_step(int U, int G, int D, int S, int Lcap, int ps, int pinned, bool bf16, int split_override) {
+    (void)pinned;
     (void)ps;
     StepPlan pl{};
     const int nblk = Lcap / kBlockTokens;
@@ -1179,21 +1005,6 @@ StepPlan plan_step(int U, int G, int D, int S, int Lcap, int ps, int full_rows, 
     pl.nsplit = (nblk + pl.bps - 1) / pl.bps;
     pl.fused = bf16 && pl.nsplit == 1 && step_lds(G, D, S, pl.waves, true) <= kMaxLds;
     pl.lds = bf16 ? step_lds(G, D, S, pl.waves, pl.fused) : 0;
-    // block sharing: the last full pinned blocks of every unit, while a
-    // helper's scan of the per-unit counters stays short; off unless asked
-    // for (a helper's block costs more latency than it saves at the end of
-    // a step)
-    pl.nsh = 0;
-    pl.sh0 = 0;
-    if (pl.fused && U <= 4096) {
-        const int pb = full_rows / kBlockTokens;
-        int n = share_override >= 0 ? share_override : 0;
-        n = std::min(std::min(n, pb), kMaxShared);
-        if (n > 0) {
-            pl.nsh = n;
-            pl.sh0 = pb - n;
-        }
-    }
     return pl;
 }
 

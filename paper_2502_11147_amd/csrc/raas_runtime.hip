@@ -57,16 +57,13 @@ struct raas_pool {
     int32_t* meta = nullptr;  // lid, ts, state, fill: 4 x [Ly][U][S]
     int32_t* unit = nullptr;  // [Ly][U][kUnitFields]
     int32_t* err = nullptr;
-    float* part = nullptr;    // partial attention, scratch of one step
+    float* part = nullptr;    // [U][splits][G][D+2], scratch of one step
     double* score = nullptr;  // [U][S], scratch of one step
-    int32_t* coord = nullptr; // [Ly][2][U][kCoordFields] block-sharing counters
     size_t bytes = 0;
     std::vector<unsigned char> prefilled;
     std::vector<int> pinned;  // pinned prefill pages of each layer
-    std::vector<int> full_rows;  // rows of full pinned pages of each layer
     std::vector<unsigned char> descending;  // traversal direction of each layer's next step
     int split_override = 0;
-    int share_override = -1;
     hipStream_t last_stream = nullptr;
     int prof_mask = 0;
     Timing timing[kKernels];
@@ -92,9 +89,6 @@ LayerView view(const raas_pool* p, int layer) {
     L.err = p->err;
     L.score = p->score;
     L.part = p->part;
-    L.coord = p->coord + (size_t)layer * 2 * p->U * kCoordFields;
-    L.nsh = 0;
-    L.sh0 = 0;
     L.rev = 0;
     L.nsplit = 1;
     L.bps = p->Lcap / kBlockTokens;
@@ -205,15 +199,10 @@ raas_status raas_create_pool(const raas_config* cfg, void* stream, raas_pool** o
     p->meta_layer_elems = (size_t)p->U * p->S;
     p->prefilled.assign((size_t)cfg->n_layers, 0);
     p->pinned.assign((size_t)cfg->n_layers, 0);
-    p->full_rows.assign((size_t)cfg->n_layers, 0);
     p->descending.assign((size_t)cfg->n_layers, 0);
     const size_t Ly = (size_t)cfg->n_layers;
     const int nblk = p->Lcap / kBlockTokens;
     const int max_split = nblk < kMaxSplits ? nblk : kMaxSplits;
-    const int max_shared = nblk < kMaxShared ? nblk : kMaxShared;
-    // partials: split path [U][splits][G][D+2], shared blocks [U][nsh+1][G][D+4]
-    const size_t part_split = (size_t)max_split * (p->D + 2), part_shared = (size_t)(max_shared + 1) * (p->D + 4);
-    const size_t part_floats = (size_t)p->U * p->G * (part_split > part_shared ? part_split : part_shared);
     struct Req {
         void** ptr;
         size_t bytes;
@@ -225,9 +214,8 @@ raas_status raas_create_pool(const raas_config* cfg, void* stream, raas_pool** o
         {(void**)&p->meta, 4 * Ly * p->meta_layer_elems * sizeof(int32_t)},
         {(void**)&p->unit, Ly * p->U * kUnitFields * sizeof(int32_t)},
         {(void**)&p->err, 256},
-        {(void**)&p->part, part_floats * sizeof(float)},
+        {(void**)&p->part, (size_t)p->U * max_split * p->G * (p->D + 2) * sizeof(float)},
         {(void**)&p->score, (size_t)p->U * p->S * sizeof(double)},
-        {(void**)&p->coord, Ly * 2 * p->U * kCoordFields * sizeof(int32_t)},
     };
     hipStream_t s = (hipStream_t)stream;
     hipError_t ea = allow_large_lds();
@@ -268,7 +256,7 @@ void raas_destroy(raas_pool* p) {
         for (auto ev : t.start) hipEventDestroy(ev);
         for (auto ev : t.stop) hipEventDestroy(ev);
     }
-    void* ptrs[] = {p->K, p->V, p->kmin, p->kmax, p->meta, p->unit, p->err, p->part, p->score, p->coord};
+    void* ptrs[] = {p->K, p->V, p->kmin, p->kmax, p->meta, p->unit, p->err, p->part, p->score};
     for (void* q : ptrs)
         if (q) hipFree(q);
     delete p;
@@ -294,9 +282,6 @@ raas_status raas_prefill(raas_pool* p, int32_t layer, const void* k, const void*
     if (e != hipSuccess) return hip_fail(e, "prefill launch");
     p->prefilled[layer] = 1;
     p->pinned[layer] = keep;
-    // pinned pages are full except a partial last prompt page
-    const int full = (prefill_len / p->ps) * p->ps;
-    p->full_rows[layer] = keep * p->ps < full ? keep * p->ps : full;
     p->last_stream = s;
     return RAAS_OK;
 }
@@ -311,12 +296,10 @@ raas_status raas_decode_step(raas_pool* p, int32_t layer, const void* q, const v
     LayerView L = view(p, layer);
     StepIO io{q, k_new, v_new, out, page_table_out, timestamps_out, evicted_out};
     hipStream_t s = (hipStream_t)stream;
-    const StepPlan pl = plan_step(p->U, p->G, p->D, p->S, p->Lcap, p->ps, p->full_rows[layer],
-                                  p->cfg.dtype == RAAS_BF16, p->split_override, p->share_override);
+    const StepPlan pl = plan_step(p->U, p->G, p->D, p->S, p->Lcap, p->ps, p->pinned[layer],
+                                  p->cfg.dtype == RAAS_BF16, p->split_override);
     L.nsplit = pl.nsplit;
     L.bps = pl.bps;
-    L.nsh = pl.nsh;
-    L.sh0 = pl.sh0;
     // Successive steps of a layer read its pool in opposite directions, so a
     // step starts with the blocks the previous one read last, the likeliest
     // to be still in the GPU's memory-side cache.
@@ -370,12 +353,6 @@ raas_status raas_set_attention_splits(raas_pool* p, int32_t splits) {
     if (!p) return fail(RAAS_E_INVALID, "pool is NULL");
     if (splits < 0 || splits > kMaxSplits) return fail(RAAS_E_INVALID, "splits must lie in [0, %d]", kMaxSplits);
     p->split_override = splits;
-    return RAAS_OK;
-}
-
-raas_status raas_set_block_sharing(raas_pool* p, int32_t blocks) {
-    if (!p) return fail(RAAS_E_INVALID, "pool is NULL");
-    p->share_override = blocks < 0 ? -1 : blocks;
     return RAAS_OK;
 }
 

@@ -44,7 +44,7 @@ def to_device(a: np.ndarray, dtype: str):
     return t.cuda()
 
 
-def new_pool(w, splits=None, policy=None, share=None):
+def new_pool(w, splits=None, policy=None):
     import paper_2502_11147_amd as raas
 
     kw = {}
@@ -53,8 +53,6 @@ def new_pool(w, splits=None, policy=None, share=None):
     pool = raas.Pool.for_workload(w, **kw)
     if splits is not None:
         pool.set_attention_splits(splits)
-    if share is not None:
-        pool.set_block_sharing(share)
     return pool
 
 
@@ -64,7 +62,7 @@ def unit_index(w, seq, kvh):
 
 def run_parity(w, seed: int, steps: int, layer: int = 0, units=None, out_every: int = 1,
                splits=None, chunk: int = 64, pool=None, prefill_len=None, check_invariants=True,
-               report: ParityReport | None = None, share=None) -> ParityReport:
+               report: ParityReport | None = None) -> ParityReport:
     """Runs `steps` decode steps of workload `w` on the GPU and checks the
     listed units (all when None) against the oracle."""
     import torch
@@ -78,7 +76,7 @@ def run_parity(w, seed: int, steps: int, layer: int = 0, units=None, out_every: 
     tol = TOL[w.dtype]
     own_pool = pool is None
     if own_pool:
-        pool = new_pool(w, splits, share=share)
+        pool = new_pool(w, splits)
     Kp, Vp = synth.prefill(w, seed, layer, prefill_len=P)
     pool.prefill(layer, to_device(Kp, w.dtype) if P else None, to_device(Vp, w.dtype) if P else None)
     orc = {}

@@ -74,16 +74,6 @@ def test_split_counts_agree(splits):
     _report(rep, "splits=%d" % splits)
 
 
-@pytest.mark.parametrize("share", [0, 1, 5, 62])
-def test_block_sharing_agrees(share):
-    """Prompt blocks taken over by other workgroups change only rounding,
-    never retention. 32 units of 32 blocks, 18 of them full pinned blocks."""
-    w = small(batch=16, budget=1024, prefill_len=600, decode_steps=300)
-    _say("case block-sharing %d" % share)
-    rep = run_parity(w, seed=5, steps=w.decode_steps, share=share)
-    _report(rep, "share=%d" % share)
-
-
 EDGE = [
     dict(prefill_len=0),
     dict(prefill_len=16 * 7),                     # exactly S-1 pages pinned, one decode slot
@@ -169,8 +159,8 @@ def test_state_errors_and_budget_policy():
 
 def test_deterministic():
     """Same inputs twice: bitwise-identical retention state; outputs equal up
-    to the order in which partial sums merge (blocks are claimed dynamically,
-    within a workgroup and across workgroups)."""
+    to the order in which partial sums merge (the wavefronts of a workgroup
+    claim blocks dynamically)."""
     import torch
 
     w = small(decode_steps=260)
