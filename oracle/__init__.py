@@ -25,6 +25,7 @@ LIB_PATH = os.path.join(_HERE, "libraas_oracle.so")
 OK, E_INVALID, E_BUDGET, E_STATE, E_INTERNAL = 0, -1, -2, -3, -10
 FREE, PINNED, EVICTABLE = 0, 1, 2
 PIN_HEAD, ERROR = 0, 1
+AGG_MAX, AGG_SOFTMAX_SUM = 0, 1  # head aggregation of the page score
 
 _libs: dict[str, ctypes.CDLL] = {}
 
@@ -62,6 +63,8 @@ def load(path: str | None = None) -> ctypes.CDLL:
         fp = ctypes.POINTER(ctypes.c_float)
         lib.orc_decode_batch.argtypes = [ctypes.POINTER(vp), ctypes.c_int, fp, fp, fp, dp]
         lib.orc_decode_batch.restype = ctypes.c_int
+        lib.orc_set_variant.argtypes = [vp, ctypes.c_int, ctypes.c_int]
+        lib.orc_set_variant.restype = ctypes.c_int
         lib.orc_threads.argtypes = []
         lib.orc_threads.restype = ctypes.c_int
         _libs[path] = lib
@@ -93,12 +96,16 @@ class Kvm:
     """The KV manager of one unit (sequence, layer, KV head) with G query heads."""
 
     def __init__(self, G: int, d: int, page_size: int, slots: int, r: float = 0.5,
-                 policy: int = PIN_HEAD, lib: str | None = None):
+                 policy: int = PIN_HEAD, lib: str | None = None, aggregation: int = AGG_MAX,
+                 rank_pinned: bool = False):
         self.lib = load(lib)
         self.G, self.d, self.ps, self.S = G, d, page_size, slots
         self._h = self.lib.orc_new(G, d, page_size, slots, float(r), policy)
         if not self._h:
             raise ValueError("invalid oracle configuration")
+        if aggregation != AGG_MAX or rank_pinned:
+            if self.lib.orc_set_variant(self._h, int(aggregation), int(bool(rank_pinned))) != OK:
+                raise ValueError("invalid oracle variant")
 
     def __del__(self):
         h = getattr(self, "_h", None)

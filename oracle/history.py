@@ -18,8 +18,9 @@ import math
 
 class HistoryLRU:
     def __init__(self, page_size: int, slots: int, r: float, prefill_len: int,
-                 pin_head: bool = True):
+                 pin_head: bool = True, rank_pinned: bool = False):
         self.ps, self.S, self.r = page_size, slots, r
+        self.rank_pinned = rank_pinned           # pinned pages take part in the ranking
         pages = -(-prefill_len // page_size)
         keep = min(pages, slots - 1) if pin_head else pages
         if keep > slots - 1:
@@ -38,7 +39,8 @@ class HistoryLRU:
         return len(self.pinned) + len(self.resident) < self.S
 
     def decode(self, score_of):
-        """score_of(lid) -> score of decode page lid at this step."""
+        """score_of(lid) -> score of page lid at this step (decode pages, and
+        pinned pages too when they are ranked)."""
         t = self.step
         if self.tail is None or self.fill[self.tail] == self.ps:
             assert self.capacity_left()
@@ -50,13 +52,15 @@ class HistoryLRU:
             self.used[lid] = []
             self.tail = lid
         self.fill[self.tail] += 1
-        n = len(self.resident)
+        ranked = self.resident + (self.pinned if self.rank_pinned else [])
+        n = len(ranked)
         k = math.floor(self.r * n)
-        scores = {lid: score_of(lid) for lid in self.resident}
+        scores = {lid: score_of(lid) for lid in ranked}
         # "used" = among the k highest scores, counting ties at the cut as
         # not used: a page is used when at least n-k pages score strictly less
+        # (only decode pages have a use to record)
         for lid in self.resident:
-            below = sum(1 for o in self.resident if scores[o] < scores[lid])
+            below = sum(1 for o in ranked if scores[o] < scores[lid])
             if k > 0 and below >= n - k:
                 self.used[lid].append(t)
         evicted = None

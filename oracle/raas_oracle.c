@@ -29,6 +29,17 @@
  *  R8 eviction is eager, in Algorithm 1's order: after the refresh, when the
  *     next token has no room (tail page full and no free slot).
  *  R9 softmax scale 1/sqrt(d); attention covers every resident token.
+ *
+ * Variants of R2 and R7 (off by default; orc_set_variant):
+ *  aggregation 1: a page's score is the sum over the G query heads of that
+ *     head's softmax probability over the ranked pages, the representative
+ *     bound standing for the page's logit: sum_j exp(scale*(b_j(p) - M_j)) /
+ *     sum_p' exp(scale*(b_j(p') - M_j)), M_j the head's largest bound,
+ *     scale 1/sqrt(d). The paper names no such aggregation; the scale in
+ *     particular is a reading and its value is parity unpinned (the pins fix
+ *     the normalisation, a lone page's value and the G = 1 reduction to R2).
+ *  rank_pinned 1: the pinned prompt pages are ranked together with the
+ *     decode pages (n and k count them); only decode pages take timestamps.
  */
 #include <math.h>
 #include <stdint.h>
@@ -46,6 +57,7 @@ enum { POLICY_PIN_HEAD = 0, POLICY_ERROR = 1 };
 
 typedef struct {
     int G, d, ps, S, policy;
+    int aggregation, rank_pinned; /* variants of R2 and R7, 0 by default */
     double r;
     /* per page slot */
     int *state, *lid, *fill, *ts;
@@ -83,6 +95,13 @@ orc_kvm* orc_new(int G, int d, int ps, int S, double r, int policy) {
     m->evicted = -1;
     m->theta = NAN;
     return m;
+}
+
+int orc_set_variant(orc_kvm* m, int aggregation, int rank_pinned) {
+    if (!m || aggregation < 0 || aggregation > 1 || rank_pinned < 0 || rank_pinned > 1) return ORC_E_INVALID;
+    m->aggregation = aggregation;
+    m->rank_pinned = rank_pinned;
+    return ORC_OK;
 }
 
 void orc_free(orc_kvm* m) {
@@ -239,30 +258,59 @@ int orc_decode(orc_kvm* m, const double* q, const double* k_new, const double* v
         m->fill[m->tail] += 1; /* retention-only run: no payload */
     }
 
-    /* one representative score per evictable page (R1, R2) */
+    /* the ranked pages: the decode pages, and the pinned ones too when
+     * rank_pinned (R7) */
+#define RANKED(st) ((st) == EVICTABLE || (m->rank_pinned && (st) == PINNED))
+    /* one representative score per ranked page (R1, R2) */
     int n = 0;
     for (int s = 0; s < S; ++s) {
         m->score[s] = NAN;
-        if (m->state[s] != EVICTABLE) continue;
-        ++n;
-        if (injected) {
-            m->score[s] = injected[s];
-            continue;
-        }
-        double best = -INFINITY;
-        for (int j = 0; j < G; ++j) {
-            double acc = 0.0;
-            for (int ch = 0; ch < d; ++ch) {
-                double a = q[(size_t)j * d + ch] * m->kmax[(size_t)s * d + ch];
-                double b = q[(size_t)j * d + ch] * m->kmin[(size_t)s * d + ch];
-                acc += (a > b) ? a : b;
+        if (RANKED(m->state[s])) ++n;
+    }
+    if (injected) {
+        for (int s = 0; s < S; ++s)
+            if (RANKED(m->state[s])) m->score[s] = injected[s];
+    } else if (n > 0) {
+        /* per-head bounds b_j(p) = sum_c max(q_jc*kmax_pc, q_jc*kmin_pc) */
+        double* bound = (double*)malloc(sizeof(double) * (size_t)S * G);
+        for (int s = 0; s < S; ++s) {
+            if (!RANKED(m->state[s])) continue;
+            for (int j = 0; j < G; ++j) {
+                double acc = 0.0;
+                for (int ch = 0; ch < d; ++ch) {
+                    double a = q[(size_t)j * d + ch] * m->kmax[(size_t)s * d + ch];
+                    double b = q[(size_t)j * d + ch] * m->kmin[(size_t)s * d + ch];
+                    acc += (a > b) ? a : b;
+                }
+                bound[(size_t)s * G + j] = acc;
             }
-            if (acc > best) best = acc;
         }
-        m->score[s] = best;
+        if (m->aggregation == 0) { /* R2: max over the heads */
+            for (int s = 0; s < S; ++s) {
+                if (!RANKED(m->state[s])) continue;
+                double best = -INFINITY;
+                for (int j = 0; j < G; ++j)
+                    if (bound[(size_t)s * G + j] > best) best = bound[(size_t)s * G + j];
+                m->score[s] = best;
+            }
+        } else { /* sum over the heads of each head's softmax over the ranked pages */
+            const double scale = 1.0 / sqrt((double)d);
+            for (int s = 0; s < S; ++s)
+                if (RANKED(m->state[s])) m->score[s] = 0.0;
+            for (int j = 0; j < G; ++j) {
+                double mx = -INFINITY, z = 0.0;
+                for (int s = 0; s < S; ++s)
+                    if (RANKED(m->state[s]) && bound[(size_t)s * G + j] > mx) mx = bound[(size_t)s * G + j];
+                for (int s = 0; s < S; ++s)
+                    if (RANKED(m->state[s])) z += exp(scale * (bound[(size_t)s * G + j] - mx));
+                for (int s = 0; s < S; ++s)
+                    if (RANKED(m->state[s])) m->score[s] += exp(scale * (bound[(size_t)s * G + j] - mx)) / z;
+            }
+        }
+        free(bound);
     }
 
-    /* new timestamps to the pages with the top-r scores (R7) */
+    /* new timestamps to the decode pages among the top-r ranked scores (R7) */
     int k = (int)floor(m->r * (double)n);
     m->n_evictable = n;
     m->k_refreshed = k;
@@ -273,7 +321,7 @@ int orc_decode(orc_kvm* m, const double* q, const double* k_new, const double* v
             double* sorted = (double*)malloc(sizeof(double) * (size_t)n);
             int i = 0;
             for (int s = 0; s < S; ++s)
-                if (m->state[s] == EVICTABLE) sorted[i++] = m->score[s];
+                if (RANKED(m->state[s])) sorted[i++] = m->score[s];
             qsort(sorted, (size_t)n, sizeof(double), cmp_double);
             theta = sorted[n - k - 1]; /* the (n-k)-th smallest */
             free(sorted);
@@ -282,6 +330,7 @@ int orc_decode(orc_kvm* m, const double* q, const double* k_new, const double* v
         for (int s = 0; s < S; ++s)
             if (m->state[s] == EVICTABLE && m->score[s] > theta) m->ts[s] = c;
     }
+#undef RANKED
 
     /* if kvm.is_full(): evict the page with the oldest timestamp (R6, R8) */
     m->evicted = -1;

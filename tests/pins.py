@@ -157,17 +157,19 @@ def check_fifo_special_cases(lib, seed=4):
             assert evicted and evicted == list(range(first, first + len(evicted)))
 
 
-def _drive_both(lib, ps, S, P, r, scores_for, T):
+def _drive_both(lib, ps, S, P, r, scores_for, T, rank_pinned=False):
     """Drive the oracle and the history-replay LRU with the same page scores.
 
-    scores_for(t, n) gives the scores of the n decode pages alive during
-    step t, in increasing logical-id order."""
-    m = oracle.Kvm(1, 2, ps, S, r=r, lib=lib)
+    scores_for(t, n) gives the scores of the n pages ranked during step t
+    (the decode pages alive, and the pinned ones when rank_pinned), in
+    increasing logical-id order."""
+    m = oracle.Kvm(1, 2, ps, S, r=r, lib=lib, rank_pinned=rank_pinned)
     assert m.prefill(np.zeros((P, 2)), np.zeros((P, 2))) == 0
-    h = HistoryLRU(ps, S, r, P)
+    h = HistoryLRU(ps, S, r, P, rank_pinned=rank_pinned)
     for t in range(T):
         st = m.state()
-        slot_lid = {s: int(st["page_table"][s]) for s in range(S) if st["state"][s] == oracle.EVICTABLE}
+        ranked_states = (oracle.EVICTABLE, oracle.PINNED) if rank_pinned else (oracle.EVICTABLE,)
+        slot_lid = {s: int(st["page_table"][s]) for s in range(S) if st["state"][s] in ranked_states}
         new = _new_slot(st, ps)
         if new is not None:
             slot_lid[new] = st["next_lid"]
@@ -224,6 +226,72 @@ def check_random_policy_vs_history(lib, seed=5, cases=80):
         levels = int(rng.integers(2, 6))
         _drive_both(lib, ps, S, P, r,
                     lambda t, n: [float(x) for x in rng.integers(0, levels, size=n)], T)
+
+
+def check_rank_pinned_vs_history(lib, seed=8, cases=60):
+    """Variant: the pinned prompt pages ranked with the decode pages (n and
+    k count them; only decode pages take timestamps). Random scores with
+    ties over pinned and decode pages: oracle and history-replay LRU agree at
+    every step, and the step reports n = pinned + decode pages."""
+    rng = np.random.default_rng(seed)
+    for _ in range(cases):
+        ps = int(rng.integers(1, 4))
+        S = int(rng.integers(3, 9))
+        P = int(rng.integers(1, (S - 1) * ps + 1))
+        r = float(rng.choice([0.5, 0.25, 0.75, 1.0]))
+        T = int(rng.integers(5, 50))
+        levels = int(rng.integers(2, 6))
+        _drive_both(lib, ps, S, P, r,
+                    lambda t, n: [float(x) for x in rng.integers(0, levels, size=n)], T, rank_pinned=True)
+    m = oracle.Kvm(1, 2, 2, 6, r=0.5, lib=lib, rank_pinned=True)
+    assert m.prefill(np.zeros((5, 2)), np.zeros((5, 2))) == 0  # 3 pinned pages
+    for t in range(7):
+        m.decode_with_scores(np.arange(6, dtype=float))
+        st = m.state()
+        pinned = int(np.sum(st["state"] == oracle.PINNED))
+        decode = int(np.sum(st["state"] == oracle.EVICTABLE)) + (st["evicted"] >= 0)
+        assert pinned == 3 and st["n_evictable"] == pinned + decode, (t, st)
+
+
+def check_softmax_sum_invariants(lib, seed=9):
+    """Variant: a page's score is the sum over the G heads of each head's
+    softmax probability over the ranked pages. Then (i) the ranked scores
+    sum to G at every step; (ii) a lone ranked page scores exactly G; (iii)
+    with G = 1 the score is a monotone function of the representative bound,
+    so retention is identical to the max rule (R2) step for step."""
+    rng = np.random.default_rng(seed)
+    for G, d, ps, S, P in ((4, 16, 4, 8, 6), (7, 8, 2, 12, 3), (2, 32, 8, 5, 9)):
+        for rank_pinned in (False, True):
+            m = oracle.Kvm(G, d, ps, S, lib=lib, aggregation=oracle.AGG_SOFTMAX_SUM, rank_pinned=rank_pinned)
+            assert m.prefill(rng.standard_normal((P, d)), rng.standard_normal((P, d))) == 0
+            for t in range(40):
+                m.decode(rng.standard_normal((G, d)) * 2.0, rng.standard_normal(d), rng.standard_normal(d),
+                         want_out=False)
+                sc, _ = m.last_scores()
+                ranked = sc[~np.isnan(sc)]
+                assert abs(ranked.sum() - G) < 1e-12 * G, (G, t, ranked.sum())
+                if ranked.size == 1:
+                    assert ranked[0] == G
+    # a lone decode page: two slots, one of them pinned
+    m = oracle.Kvm(3, 8, 4, 2, lib=lib, aggregation=oracle.AGG_SOFTMAX_SUM)
+    assert m.prefill(rng.standard_normal((4, 8)), rng.standard_normal((4, 8))) == 0
+    for t in range(9):
+        m.decode(rng.standard_normal((3, 8)), rng.standard_normal(8), rng.standard_normal(8), want_out=False)
+        sc, _ = m.last_scores()
+        assert sc[1] == 3.0 and np.isnan(sc[0]), (t, sc)
+    # G = 1: same decisions as the max rule
+    for rank_pinned in (False, True):
+        a = oracle.Kvm(1, 16, 2, 7, lib=lib, rank_pinned=rank_pinned)
+        b = oracle.Kvm(1, 16, 2, 7, lib=lib, aggregation=oracle.AGG_SOFTMAX_SUM, rank_pinned=rank_pinned)
+        K, V = rng.standard_normal((5, 16)), rng.standard_normal((5, 16))
+        assert a.prefill(K, V) == 0 and b.prefill(K, V) == 0
+        for t in range(60):
+            q, k, v = rng.standard_normal((1, 16)), rng.standard_normal(16), rng.standard_normal(16)
+            a.decode(q, k, v, want_out=False)
+            b.decode(q, k, v, want_out=False)
+            sa, sb = a.state(), b.state()
+            for key in ("page_table", "ts"):
+                assert np.array_equal(sa[key], sb[key]), (rank_pinned, t, key)
 
 
 def check_prefill_rule(lib, seed=6):
@@ -304,6 +372,8 @@ def check_budget_and_attention_set(lib, seed=7):
 
 
 ALL_CHECKS = [
+    check_rank_pinned_vs_history,
+    check_softmax_sum_invariants,
     check_dense_equivalence,
     check_single_token_and_bound,
     check_threshold_counts,

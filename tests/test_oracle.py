@@ -28,7 +28,8 @@ def test_oracle_pin(check, oracle_lib):
 # (name, [(original text, replacement)]) -- each a plausible slip in the oracle
 MUTANTS = [
     ("score_uses_min", [("acc += (a > b) ? a : b;", "acc += (a < b) ? a : b;")]),
-    ("no_softmax_scale", [("const double scale = 1.0 / sqrt((double)d);", "const double scale = 1.0;")]),
+    ("no_softmax_scale", [("const double scale = 1.0 / sqrt((double)d);\n    int n_old = 0;",
+                           "const double scale = 1.0;\n    int n_old = 0;")]),
     ("refresh_ties_at_threshold", [("m->score[s] > theta) m->ts[s] = c;", "m->score[s] >= theta) m->ts[s] = c;")]),
     ("order_statistic_off_by_one", [("theta = sorted[n - k - 1];", "theta = sorted[n - k];")]),
     ("tie_break_newest", [("m->lid[s] < m->lid[v]", "m->lid[s] > m->lid[v]")]),
@@ -41,10 +42,17 @@ MUTANTS = [
     ("kmax_not_widened", [("if (k[c] > m->kmax[(size_t)s * d + c]) m->kmax[(size_t)s * d + c] = k[c];", "")]),
     ("evicted_tail_kept", [("if (m->tail == v) m->tail = -1;", "")]),
     ("top_r_rounds_up", [("int k = (int)floor(m->r * (double)n);", "int k = (int)ceil(m->r * (double)n);")]),
-    ("pinned_pages_scored", [("        m->score[s] = NAN;\n        if (m->state[s] != EVICTABLE) continue;",
-                              "        m->score[s] = NAN;\n        if (m->state[s] == FREE) continue;")]),
+    ("pinned_pages_scored", [("#define RANKED(st) ((st) == EVICTABLE || (m->rank_pinned && (st) == PINNED))",
+                              "#define RANKED(st) ((st) == EVICTABLE || (st) == PINNED)")]),
+    ("rank_pinned_ignored", [("#define RANKED(st) ((st) == EVICTABLE || (m->rank_pinned && (st) == PINNED))",
+                              "#define RANKED(st) ((st) == EVICTABLE)")]),
+    ("softmax_sum_unnormalised", [("m->score[s] += exp(scale * (bound[(size_t)s * G + j] - mx)) / z;",
+                                   "m->score[s] += exp(scale * (bound[(size_t)s * G + j] - mx));")]),
+    ("softmax_sum_one_head", [("            for (int j = 0; j < G; ++j) {\n                double mx = -INFINITY, z = 0.0;",
+                               "            for (int j = 0; j < 1; ++j) {\n                double mx = -INFINITY, z = 0.0;")]),
     ("softmax_sign", [("double p = exp(logit[t] - mx);", "double p = exp(mx - logit[t]);")]),
-    ("gqa_last_head_only", [("if (acc > best) best = acc;", "best = acc;")]),
+    ("gqa_last_head_only", [("if (bound[(size_t)s * G + j] > best) best = bound[(size_t)s * G + j];",
+                             "best = bound[(size_t)s * G + j];")]),
 ]
 
 
