@@ -43,6 +43,9 @@ def parse():
     ap.add_argument("--seed", type=int, default=0)
     ap.add_argument("--ring", type=int, default=128, help="distinct input steps staged on device")
     ap.add_argument("--splits", type=int, default=0, help="attention splits per unit (0 = automatic)")
+    ap.add_argument("--score-aggregation", choices=("max", "softmax-sum"), default="max",
+                    help="head aggregation of the page score (default: max over the heads)")
+    ap.add_argument("--rank-pinned", action="store_true", help="rank the pinned prefill pages too")
     ap.add_argument("--cpu-seconds", type=float, default=15.0, help="budget of the CPU oracle sample")
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--copy-calibration", action="store_true",
@@ -187,7 +190,8 @@ def resident_schedule(st, ps, S, n):
 def step_bytes(w, resident, n_ev):
     """Algorithmic HBM bytes of one whole decode step, all units: K+V of the
     resident tokens; the representative keys (per-channel min and max) of the
-    evictable pages; q read once, out written once; the new K and V read once
+    n_ev scored pages (the evictable ones, plus the pinned ones when they are
+    ranked); q read once, out written once; the new K and V read once
     and stored once; the tail page's min/max read and written; per slot,
     state/timestamp/id/fill read and state/timestamp written (24 B)."""
     e = 2 if w.dtype == "bf16" else 4
@@ -196,7 +200,7 @@ def step_bytes(w, resident, n_ev):
     return per_unit.sum(axis=-1)
 
 
-def cpu_baseline(w, seed, ring_np, budget_s):
+def cpu_baseline(w, seed, ring_np, budget_s, aggregation=0, rank_pinned=False):
     """The fp64 CPU oracle on a bounded sample: a subset of units, filled to
     the budget with retention-only steps (attention skipped), then timed
     steady-state steps with attention over the same inputs."""
@@ -210,7 +214,8 @@ def cpu_baseline(w, seed, ring_np, budget_s):
     ms = []
     for u in units_idx:
         b, h = divmod(int(u), w.n_kv_heads)
-        m = oracle.Kvm(w.group, w.head_dim, w.page_size, w.slots, r=w.r)
+        m = oracle.Kvm(w.group, w.head_dim, w.page_size, w.slots, r=w.r, aggregation=aggregation,
+                       rank_pinned=rank_pinned)
         m.prefill(K[b, h].astype(np.float64), V[b, h].astype(np.float64))
         ms.append(m)
     q, k, v = ring_np
@@ -267,7 +272,9 @@ def main():
     dt = torch.bfloat16 if w.dtype == "bf16" else torch.float32
     U, S = w.batch * w.n_kv_heads, w.slots
 
-    pool = raas.Pool.for_workload(w)
+    agg = raas.SCORE_SOFTMAX_SUM if args.score_aggregation == "softmax-sum" else raas.SCORE_MAX
+    variant = agg != raas.SCORE_MAX or args.rank_pinned
+    pool = raas.Pool.for_workload(w, score_aggregation=agg, rank_pinned=args.rank_pinned)
     if args.splits:
         pool.set_attention_splits(args.splits)
     Kp, Vp = synth.prefill(w, args.seed, 0)
@@ -298,6 +305,7 @@ def main():
     st = pool.export_state(0)
     res = resident_schedule(st, w.page_size, S, args.steps)
     n_ev0 = (st["state"] == 2).sum(axis=1)
+    n_pin = (st["state"] == 1).sum(axis=1) if args.rank_pinned else 0
 
     # timed region: HIP events on the launch stream (torch's current stream)
     # around all K steps; with two kernels per step, the library also times
@@ -328,13 +336,18 @@ def main():
     # step kernel's average duration: the event span over the K launches when
     # it is the only kernel of the step, else the sampled per-kernel events
     step_avg_s = span_ms / 1e3 / args.steps if fused else step_ms / 1e3 / max(step_n, 1)
-    step_b = float(np.mean(step_bytes(w, res, n_ev0[None, :])))
+    step_b = float(np.mean(step_bytes(w, res, (n_ev0 + n_pin)[None, :])))
     # bytes of the step kernel alone: everything but what the epilogue kernel moves
     e = 2 if w.dtype == "bf16" else 4
     kernel_b = step_b if fused else step_b - U * w.group * w.head_dim * e - 24 * U * S
     achieved = kernel_b / step_avg_s / 1e9
     kname = "k_step_bf16" if w.dtype == "bf16" else "k_step_f32"
-    traffic, traffic_src = stored_traffic(kname, w.name) if fused else (None, "two kernels per step")
+    if variant:
+        traffic, traffic_src = None, "no stored counter profile for the score variants"
+    elif fused:
+        traffic, traffic_src = stored_traffic(kname, w.name)
+    else:
+        traffic, traffic_src = None, "two kernels per step"
     line = {
         "metric": "decode tokens/s per GPU at batch B, budget L; achieved HBM GB/s vs peak",
         "value": round(tokens_per_s, 1),
@@ -355,6 +368,7 @@ def main():
             "budget_tokens": w.budget, "prefill_len": w.prefill_len, "r": w.r,
             "resident_tokens_per_unit_avg": float(res.mean()),
             "attention_splits": args.splits or "auto",
+            "score_aggregation": args.score_aggregation, "rank_pinned": bool(args.rank_pinned),
         },
         "step_hbm_gbs_algorithmic": round(step_b / (elapsed / args.steps) / 1e9, 1),
         "roofline": {
@@ -375,7 +389,7 @@ def main():
     }
     assert np.all(st_end["clock"] == w.prefill_len + t_start + args.steps)
     if not args.no_cpu_baseline:
-        line["cpu_baseline"] = cpu_baseline(w, args.seed, ring_np, args.cpu_seconds)
+        line["cpu_baseline"] = cpu_baseline(w, args.seed, ring_np, args.cpu_seconds, agg, args.rank_pinned)
     print(json.dumps(line), flush=True)
 
 

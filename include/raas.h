@@ -51,7 +51,7 @@
 extern "C" {
 #endif
 
-#define RAAS_ABI_VERSION 1
+#define RAAS_ABI_VERSION 2
 
 typedef enum {
     RAAS_OK = 0,
@@ -72,6 +72,15 @@ typedef enum {
     RAAS_PREFILL_ERROR = 1     /* refuse with RAAS_E_BUDGET */
 } raas_prefill_policy;
 
+/* How the G query heads of a unit combine into one page score. The paper
+ * does not say (it keeps one decision per page); both are readings. */
+typedef enum {
+    RAAS_SCORE_MAX = 0,        /* max over the heads of the representative bound (default) */
+    RAAS_SCORE_SOFTMAX_SUM = 1 /* sum over the heads of each head's softmax, over the ranked
+                                  pages, of the bounds scaled by 1/sqrt(head_dim): scores
+                                  then sum to G */
+} raas_score_aggregation;
+
 typedef struct {
     int32_t batch;          /* sequences, >= 1; all advance together */
     int32_t n_layers;       /* >= 1; each layer has its own pool and clock */
@@ -83,6 +92,11 @@ typedef struct {
     int32_t dtype;          /* raas_dtype of q, k, v and out */
     float r;                /* fraction of evictable pages refreshed per step, in [0, 1] (0.5) */
     int32_t prefill_policy; /* raas_prefill_policy */
+    /* Variants of step 3-4 (0, 0 = the behaviour described above): */
+    int32_t score_aggregation; /* raas_score_aggregation */
+    int32_t rank_pinned;       /* 1: the pinned prefill pages are scored and ranked with the
+                                  evictable ones (n counts them) but never take timestamps;
+                                  0: only evictable pages are ranked */
 } raas_config;
 
 typedef struct raas_pool raas_pool; /* opaque */

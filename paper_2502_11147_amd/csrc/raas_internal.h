@@ -39,12 +39,14 @@ struct LayerView {
     int32_t* fill;   // [U][S] tokens in the page
     int32_t* unit;   // [U][kUnitFields]
     int32_t* err;    // device flag, nonzero after an internal inconsistency
-    double* score;   // [U][S] page scores (split path)
+    double* score;   // split path: [U][S] page scores; [U][S][G] per-head bounds when agg == 1
     float* part;     // [U][nsplit][G][D+2] partial attention (split path)
     int U, G, D, ps, S, Lcap;
     int nsplit, bps;  // attention splits per unit, 32-token blocks per split
     int rev;          // 1: this step visits blocks and page groups in descending order
     int bf16;         // 1: bf16 pool, 0: fp32 pool
+    int agg;          // head aggregation of the page score: 0 max, 1 sum of per-head softmax
+    int rank_pinned;  // 1: pinned pages are scored and ranked (never refreshed)
 };
 
 struct StepIO {
@@ -65,7 +67,8 @@ struct StepPlan {
     size_t lds;      // dynamic LDS of the step kernel
 };
 
-StepPlan plan_step(int U, int G, int D, int S, int Lcap, int ps, int pinned, bool bf16, int split_override);
+StepPlan plan_step(int U, int G, int D, int S, int Lcap, int ps, int pinned, bool bf16, int agg,
+                   int split_override);
 // Lets the step kernels use more than the default dynamic LDS.
 hipError_t allow_large_lds();
 

@@ -158,6 +158,31 @@ __global__ void k_prefill_f32(LayerView L, const float* __restrict__ k, const fl
     st4((float*)L.V + dst, ld4(v + src));
 }
 
+// Representative keys of the pinned pages, needed only when they are ranked:
+// per-channel min and max over each page's prefill tokens (Section 3.3). One
+// thread per (unit, page, channel); a wavefront reads 64 consecutive channels
+// of one token at a time.
+template <typename T>
+__global__ void k_prefill_rep(LayerView L, const T* __restrict__ k, int P, int keep_pages) {
+    const size_t tid = (size_t)blockIdx.x * blockDim.x + threadIdx.x;
+    const int D = L.D, ps = L.ps;
+    if (tid >= (size_t)L.U * keep_pages * D) return;
+    const int c = (int)(tid % D);
+    const size_t up = tid / D;
+    const int pg = (int)(up % keep_pages), u = (int)(up / keep_pages);
+    const int t0 = pg * ps, t1 = min(P, t0 + ps);  // t0 < P: the page holds a prefill token
+    const T* ku = k + (size_t)u * P * D + c;
+    T hi = ku[(size_t)t0 * D], lo = hi;
+    for (int t = t0 + 1; t < t1; ++t) {
+        const T x = ku[(size_t)t * D];
+        if (to_f(x) > to_f(hi)) hi = x;
+        if (to_f(x) < to_f(lo)) lo = x;
+    }
+    const size_t o = ((size_t)u * L.S + pg) * D + c;
+    ((T*)L.kmax)[o] = hi;
+    ((T*)L.kmin)[o] = lo;
+}
+
 // ---------------------------------------------------------------------------
 // Epilogue of a step, for one unit, run by every thread of one workgroup.
 // Slot state is in LDS with the page the step opened already marked
@@ -177,6 +202,12 @@ struct UnitRec {
     int ns, nf, clock, next_lid;
     __device__ bool opened() const { return nf == 0; }
 };
+
+// Slots that take part in the top-r order statistic: the evictable pages,
+// and the pinned ones when the pool ranks them.
+__device__ __forceinline__ bool ranked(const LayerView& L, int st) {
+    return st == kEvictable || (L.rank_pinned && st == kPinned);
+}
 
 __device__ __forceinline__ UnitRec read_unit(const LayerView& L, int u) {
     const int32_t* U4 = L.unit + (size_t)u * kUnitFields;
@@ -253,7 +284,7 @@ __device__ __forceinline__ void score_issue(const LayerView& L, int u, int p, in
 template <int D>
 __device__ __forceinline__ double score_finish(const LayerView& L, int u, int p, int part, bool act,
                                                ScoreFrag<D>& f, bool is_tail, bool opened,
-                                               const uint16_t* k_new, const double* qd) {
+                                               const uint16_t* k_new, const double* qd, double* hb) {
     constexpr int SV = ScoreFrag<D>::SV;
     const int G = L.G;
     if (act && is_tail) {
@@ -313,6 +344,7 @@ __device__ __forceinline__ double score_finish(const LayerView& L, int u, int p,
         a += __shfl_xor(a, 2);
         a += __shfl_xor(a, 4);
         best = a > best ? a : best;
+        if (hb != nullptr && part == 0) hb[j] = a;  // per-head bounds, for the softmax aggregation
     }
     return best;
 }
@@ -323,26 +355,59 @@ struct RetShared {
     int victim, evicted, next_slot, next_fill, tail_after, errs;
 };
 
+// Page scores of the softmax aggregation, by one wavefront: for each query
+// head j, a softmax over the ranked pages of the head's bounds b_j (scale
+// 1/sqrt(D), shifted by the head's largest bound M_j), summed over the heads
+// in head order: score(p) = sum_j exp(c (b_j(p) - M_j)) / Z_j. hb[p*G + j]
+// holds b_j(p) for every ranked page p.
+__device__ void softmax_sum_scores(const LayerView& L, const double* hb, const int* s_state, double* s_score) {
+    const int S = L.S, G = L.G, lane = threadIdx.x & 63;
+    const double c = 1.0 / sqrt((double)L.D);
+    for (int p = lane; p < S; p += 64)
+        if (ranked(L, s_state[p])) s_score[p] = 0.0;
+    for (int j = 0; j < G; ++j) {
+        double mx = -INFINITY;
+        for (int p = lane; p < S; p += 64)
+            if (ranked(L, s_state[p])) mx = fmax(mx, hb[(size_t)p * G + j]);
+#pragma unroll
+        for (int off = 32; off >= 1; off >>= 1) mx = fmax(mx, __shfl_xor(mx, off));
+        double z = 0.0;
+        for (int p = lane; p < S; p += 64)
+            if (ranked(L, s_state[p])) z += exp(c * (hb[(size_t)p * G + j] - mx));
+#pragma unroll
+        for (int off = 32; off >= 1; off >>= 1) z += __shfl_xor(z, off);
+        for (int p = lane; p < S; p += 64)
+            if (ranked(L, s_state[p])) s_score[p] += exp(c * (hb[(size_t)p * G + j] - mx)) / z;
+    }
+    // every lane's scores are read by the ranking below
+    __atomic_signal_fence(__ATOMIC_SEQ_CST);
+    __builtin_amdgcn_wave_barrier();
+}
+
 // Retention policy of one unit, run by one wavefront (Algorithm 1,
 // store_cache; Sections 3.2-3.3) on the slot state in LDS, the opened page
-// already marked evictable and s_score holding every evictable page's score
-// (+inf elsewhere):
-//  - top-r refresh: with n evictable pages and k = floor(r*n), page p gets
-//    ts = clock when at least n-k evictable pages score strictly less, i.e.
-//    exactly the pages above the (n-k)-th smallest score;
+// already marked evictable and s_score holding every ranked page's score
+// (+inf elsewhere), or, with the softmax aggregation, hb holding the ranked
+// pages' per-head bounds:
+//  - top-r refresh: with n ranked pages and k = floor(r*n), an evictable
+//    page p gets ts = clock when at least n-k ranked pages score strictly
+//    less, i.e. exactly the pages above the (n-k)-th smallest score (the
+//    ranked pages are the evictable ones, plus the pinned ones when the pool
+//    ranks them; pinned pages never take a timestamp);
 //  - eviction ("if kvm.is_full(): evict KVs with the oldest timestamps"):
 //    when the tail page is full and no slot is free, the evictable page with
 //    the smallest (timestamp, logical id) is freed;
 //  - the next token's target: the tail page if it has room, else the lowest
 //    free slot (a fresh page).
-__device__ void retention_wave(const LayerView& L, const UnitRec& ur, double r, const double* s_score,
-                               int* s_state, int* s_ts, const int* s_lid, RetShared& out) {
+__device__ void retention_wave(const LayerView& L, const UnitRec& ur, double r, double* s_score,
+                               int* s_state, int* s_ts, const int* s_lid, RetShared& out, const double* hb) {
     const int S = L.S, ps = L.ps, lane = threadIdx.x & 63;
+    if (hb != nullptr) softmax_sum_scores(L, hb, s_state, s_score);
     int n = 0, nfree = 0;
     for (int s0 = 0; s0 < S; s0 += 64) {
         const int s = s0 + lane;
         const int st = s < S ? s_state[s] : -1;
-        n += __popcll(__ballot(st == kEvictable));
+        n += __popcll(__ballot(st >= 0 && ranked(L, st)));
         nfree += __popcll(__ballot(st == kFree));
     }
     const int k = (int)floor(r * (double)n);
@@ -528,7 +593,9 @@ __device__ __forceinline__ void attend_block(const u32x4 (&kr)[2][D / 32], const
 // claiming blocks. The state reaches the pool only after the attention has
 // read it; the wavefronts' partial outputs merge at the end.
 
-template <int D, int NW>
+// AGG: the softmax aggregation of the page scores (a separate instance, so
+// that the default one carries none of its registers).
+template <int D, int NW, bool AGG>
 __global__ __launch_bounds__(NW * 64) __attribute__((amdgpu_waves_per_eu(1, 2))) void k_step_bf16(
     LayerView L, StepIO io, float scale_log2, double r, int fused) {
     constexpr int KS = D / 32, NB = D / 16, BLK = 32 * D;
@@ -544,7 +611,8 @@ __global__ __launch_bounds__(NW * 64) __attribute__((amdgpu_waves_per_eu(1, 2)))
     double* s_qd = reinterpret_cast<double*>(smem);  // [G][D+16] q in fp64, padded: qpad_index
     float* s_o = reinterpret_cast<float*>(s_qd + (size_t)G * qpad_row(D));  // [NW][G][D+4]
     double* s_score = reinterpret_cast<double*>(s_o + (size_t)NW * G * (D + 4));  // [S], fused only
-    int* s_state = reinterpret_cast<int*>(s_score + S);  // [S], fused only
+    double* s_hb = s_score + S;  // [S][G] per-head bounds, fused softmax aggregation only
+    int* s_state = reinterpret_cast<int*>(s_hb + (AGG ? (size_t)S * G : 0));  // [S], fused only
     int* s_ts = s_state + S;
     int* s_lid = s_ts + S;
 
@@ -609,8 +677,10 @@ __global__ __launch_bounds__(NW * 64) __attribute__((amdgpu_waves_per_eu(1, 2)))
     const int row_new = ns * ps + nf, b_new = row_new >> 5, tt_new = row_new & 31;
     // the block of claim index i, or b1 when none is left
     auto take = [&](int i) { return i < nown ? blk_of(i) : b1; };
-    // pages scored here: those whose first row lies in this workgroup's blocks, pinned ones excepted
-    const int sl0 = max(pinned, min(S, (32 * b0 + ps - 1) / ps)), sl1 = min(S, (32 * b1 + ps - 1) / ps);
+    // pages scored here: those whose first row lies in this workgroup's blocks, pinned ones
+    // excepted unless they are ranked
+    const int sl0 = max(L.rank_pinned ? 0 : pinned, min(S, (32 * b0 + ps - 1) / ps));
+    const int sl1 = min(S, (32 * b1 + ps - 1) / ps);
 
     // fill of the page holding this lane's 8 rows of block b (page_size % 8 == 0)
     auto row_fill = [&](int b) {
@@ -654,7 +724,7 @@ __global__ __launch_bounds__(NW * 64) __attribute__((amdgpu_waves_per_eu(1, 2)))
         const int g = pass * NW + w;
         return sl0 + 8 * (L.rev ? ngroups - 1 - g : g) + (lane >> 3);
     };
-    auto pass_act = [&](int p) { return p < sl1 && (p == ns || L.state[base + p] == kEvictable); };
+    auto pass_act = [&](int p) { return p < sl1 && (p == ns || ranked(L, L.state[base + p])); };
     const int npass = (sl1 - sl0 - 8 * w > 0) ? (sl1 - sl0 - 8 * w + 8 * NW - 1) / (8 * NW) : 0;
     const int npass_all = (sl1 - sl0 + 8 * NW - 1) / (8 * NW);  // passes of wavefront 0, the most
     int pass = 0;
@@ -662,8 +732,9 @@ __global__ __launch_bounds__(NW * 64) __attribute__((amdgpu_waves_per_eu(1, 2)))
     bool act_cur = false;
     auto score_step = [&]() {
         const int p = pass_page(pass);
-        const double sc = score_finish<D>(L, u, p, part, act_cur, frag, p == ns, opened, s_kn, s_qd);
-        if (act_cur && part == 0) {
+        double* hb = (AGG && act_cur) ? (fused ? s_hb : L.score + base * G) + (size_t)p * G : nullptr;
+        const double sc = score_finish<D>(L, u, p, part, act_cur, frag, p == ns, opened, s_kn, s_qd, hb);
+        if (act_cur && part == 0 && !AGG) {
             if (fused) s_score[p] = sc;
             else L.score[base + p] = sc;
         }
@@ -678,7 +749,7 @@ __global__ __launch_bounds__(NW * 64) __attribute__((amdgpu_waves_per_eu(1, 2)))
     bool decided = false;
     auto scores_done = [&]() {
         lds_barrier();
-        if (fused && w == 0) retention_wave(L, ur, r, s_score, s_state, s_ts, s_lid, ret);
+        if (fused && w == 0) retention_wave(L, ur, r, s_score, s_state, s_ts, s_lid, ret, AGG ? s_hb : nullptr);
         decided = true;
     };
 
@@ -744,7 +815,9 @@ __global__ __launch_bounds__(NW * 64) __attribute__((amdgpu_waves_per_eu(1, 2)))
         // this block's registers are free again
         if (it == 0) staged();
         else if (pass < npass) score_step();
-        if (it == npass_all) scores_done();
+        // (the softmax aggregation waits for the end of the loop: mid-loop, its
+        // exponentials would compete with the prefetched block for registers)
+        if (!AGG && it == npass_all) scores_done();
         ++it;
         b = bn;
     }
@@ -878,7 +951,7 @@ __global__ __launch_bounds__(64) void k_step_f32(LayerView L, StepIO io, float s
     const int sl0 = min(S, (t0 + ps - 1) / ps), sl1 = min(S, (t1 + ps - 1) / ps);
     for (int p = sl0 + lane; p < sl1; p += 64) {
         const bool tail = p == ns;
-        if (!(tail || L.state[base + p] == kEvictable)) continue;
+        if (!(tail || ranked(L, L.state[base + p]))) continue;
         float* kx = (float*)L.kmax + (base + p) * D;
         float* kn = (float*)L.kmin + (base + p) * D;
         double best = -INFINITY;
@@ -906,7 +979,13 @@ __global__ __launch_bounds__(64) void k_step_f32(LayerView L, StepIO io, float s
 #pragma unroll
         for (int j = 0; j < 16; ++j)
             if (j < G) best = accj[j] > best ? accj[j] : best;
-        L.score[base + p] = best;
+        if (L.agg) {
+#pragma unroll
+            for (int j = 0; j < 16; ++j)
+                if (j < G) L.score[(base + p) * G + j] = accj[j];
+        } else {
+            L.score[base + p] = best;
+        }
     }
 }
 
@@ -928,10 +1007,12 @@ __global__ __launch_bounds__(256) void k_epilogue(LayerView L, StepIO io, double
     const UnitRec ur = read_unit(L, u);
     load_slots(L, u, ur, s_score, s_state, s_ts, s_lid);
     __syncthreads();
-    for (int s = threadIdx.x; s < S; s += blockDim.x)
-        if (s_state[s] == kEvictable) s_score[s] = L.score[base + s];
+    if (!L.agg)
+        for (int s = threadIdx.x; s < S; s += blockDim.x)
+            if (ranked(L, s_state[s])) s_score[s] = L.score[base + s];
     __syncthreads();
-    if (threadIdx.x < 64) retention_wave(L, ur, r, s_score, s_state, s_ts, s_lid, ret);
+    if (threadIdx.x < 64)
+        retention_wave(L, ur, r, s_score, s_state, s_ts, s_lid, ret, L.agg ? L.score + base * G : nullptr);
     for (int idx = threadIdx.x; idx < G * D; idx += blockDim.x) {
         const int h = idx / D, c = idx - (idx / D) * D;
         float M = -INFINITY;
@@ -954,18 +1035,22 @@ __global__ __launch_bounds__(256) void k_epilogue(LayerView L, StepIO io, double
 inline unsigned grid1d(size_t n, int block) { return (unsigned)((n + block - 1) / block); }
 
 // LDS of the step kernel: the queries in fp64, the attention wavefronts'
-// partial outputs, and the fused epilogue's slot arrays
-size_t step_lds(int G, int D, int S, int NW, bool fused) {
+// partial outputs, and the fused epilogue's slot arrays (with the per-head
+// bounds of the softmax aggregation)
+size_t step_lds(int G, int D, int S, int NW, bool fused, int agg) {
     size_t b = (size_t)8 * G * qpad_row(D) + (size_t)NW * G * (D + 4) * 4;
-    if (fused) b += (size_t)S * 20;
+    if (fused) b += (size_t)S * 20 + (agg ? (size_t)S * G * 8 : 0);
     return b;
 }
 
 template <int D, int NW>
 hipError_t launch_step_bf16(const LayerView& L, const StepIO& io, const StepPlan& pl, float sl2, double r,
                             hipStream_t s) {
-    hipLaunchKernelGGL((k_step_bf16<D, NW>), dim3((unsigned)(L.U * pl.nsplit)), dim3(NW * 64), pl.lds, s, L, io,
-                       sl2, r, pl.fused ? 1 : 0);
+    const dim3 grid((unsigned)(L.U * pl.nsplit)), block(NW * 64);
+    if (L.agg)
+        hipLaunchKernelGGL((k_step_bf16<D, NW, true>), grid, block, pl.lds, s, L, io, sl2, r, pl.fused ? 1 : 0);
+    else
+        hipLaunchKernelGGL((k_step_bf16<D, NW, false>), grid, block, pl.lds, s, L, io, sl2, r, pl.fused ? 1 : 0);
     return hipGetLastError();
 }
 
@@ -973,7 +1058,8 @@ hipError_t launch_step_bf16(const LayerView& L, const StepIO& io, const StepPlan
 
 // ---------------------------------------------------------------------------
 
-StepPlan plan_step(int U, int G, int D, int S, int Lcap, int ps, int pinned, bool bf16, int split_override) {
+StepPlan plan_step(int U, int G, int D, int S, int Lcap, int ps, int pinned, bool bf16, int agg,
+                   int split_override) {
     (void)pinned;
     (void)ps;
     StepPlan pl{};
@@ -985,7 +1071,7 @@ StepPlan plan_step(int U, int G, int D, int S, int Lcap, int ps, int pinned, boo
     } else {
         pl.waves = 2;
         for (int nw : {8, 4, 2}) {
-            if (step_lds(G, D, S, nw, false) <= kMaxLds) {
+            if (step_lds(G, D, S, nw, false, agg) <= kMaxLds) {
                 pl.waves = nw;
                 break;
             }
@@ -1003,8 +1089,8 @@ StepPlan plan_step(int U, int G, int D, int S, int Lcap, int ps, int pinned, boo
     want = want > nblk ? nblk : want;
     pl.bps = (nblk + want - 1) / want;
     pl.nsplit = (nblk + pl.bps - 1) / pl.bps;
-    pl.fused = bf16 && pl.nsplit == 1 && step_lds(G, D, S, pl.waves, true) <= kMaxLds;
-    pl.lds = bf16 ? step_lds(G, D, S, pl.waves, pl.fused) : 0;
+    pl.fused = bf16 && pl.nsplit == 1 && step_lds(G, D, S, pl.waves, true, agg) <= kMaxLds;
+    pl.lds = bf16 ? step_lds(G, D, S, pl.waves, pl.fused, agg) : 0;
     return pl;
 }
 
@@ -1015,12 +1101,18 @@ hipError_t allow_large_lds() {
         hipError_t r = hipFuncSetAttribute(f, hipFuncAttributeMaxDynamicSharedMemorySize, bytes);
         if (r != hipSuccess) e = r;
     };
-    set((const void*)k_step_bf16<128, 8>);
-    set((const void*)k_step_bf16<128, 4>);
-    set((const void*)k_step_bf16<128, 2>);
-    set((const void*)k_step_bf16<64, 8>);
-    set((const void*)k_step_bf16<64, 4>);
-    set((const void*)k_step_bf16<64, 2>);
+    set((const void*)k_step_bf16<128, 8, false>);
+    set((const void*)k_step_bf16<128, 4, false>);
+    set((const void*)k_step_bf16<128, 2, false>);
+    set((const void*)k_step_bf16<64, 8, false>);
+    set((const void*)k_step_bf16<64, 4, false>);
+    set((const void*)k_step_bf16<64, 2, false>);
+    set((const void*)k_step_bf16<128, 8, true>);
+    set((const void*)k_step_bf16<128, 4, true>);
+    set((const void*)k_step_bf16<128, 2, true>);
+    set((const void*)k_step_bf16<64, 8, true>);
+    set((const void*)k_step_bf16<64, 4, true>);
+    set((const void*)k_step_bf16<64, 2, true>);
     return e;
 }
 
@@ -1041,6 +1133,15 @@ hipError_t launch_prefill(const LayerView& L, const void* k, const void* v, int 
             const size_t n = (size_t)L.U * keep_tok * (L.D / 4);
             hipLaunchKernelGGL(k_prefill_f32, dim3(grid1d(n, 256)), dim3(256), 0, stream, L,
                                (const float*)k, (const float*)v, P, keep_tok);
+        }
+        if (L.rank_pinned) {
+            const size_t n = (size_t)L.U * keep_pages * L.D;
+            if (L.bf16)
+                hipLaunchKernelGGL(k_prefill_rep<uint16_t>, dim3(grid1d(n, 256)), dim3(256), 0, stream, L,
+                                   (const uint16_t*)k, P, keep_pages);
+            else
+                hipLaunchKernelGGL(k_prefill_rep<float>, dim3(grid1d(n, 256)), dim3(256), 0, stream, L,
+                                   (const float*)k, P, keep_pages);
         }
     }
     return hipGetLastError();

@@ -58,7 +58,7 @@ struct raas_pool {
     int32_t* unit = nullptr;  // [Ly][U][kUnitFields]
     int32_t* err = nullptr;
     float* part = nullptr;    // [U][splits][G][D+2], scratch of one step
-    double* score = nullptr;  // [U][S], scratch of one step
+    double* score = nullptr;  // [U][S] page scores, or [U][S][G] per-head bounds, scratch of one step
     size_t bytes = 0;
     std::vector<unsigned char> prefilled;
     std::vector<int> pinned;  // pinned prefill pages of each layer
@@ -99,6 +99,8 @@ LayerView view(const raas_pool* p, int layer) {
     L.S = p->S;
     L.Lcap = p->Lcap;
     L.bf16 = p->cfg.dtype == RAAS_BF16;
+    L.agg = p->cfg.score_aggregation;
+    L.rank_pinned = p->cfg.rank_pinned;
     return L;
 }
 
@@ -129,6 +131,10 @@ raas_status validate(const raas_config* c) {
     if (!(c->r >= 0.0f && c->r <= 1.0f)) return fail(RAAS_E_INVALID, "r must lie in [0, 1]");
     if (c->prefill_policy != RAAS_PREFILL_PIN_HEAD && c->prefill_policy != RAAS_PREFILL_ERROR)
         return fail(RAAS_E_INVALID, "unknown prefill_policy %d", c->prefill_policy);
+    if (c->score_aggregation != RAAS_SCORE_MAX && c->score_aggregation != RAAS_SCORE_SOFTMAX_SUM)
+        return fail(RAAS_E_INVALID, "unknown score_aggregation %d", c->score_aggregation);
+    if (c->rank_pinned != 0 && c->rank_pinned != 1)
+        return fail(RAAS_E_INVALID, "rank_pinned must be 0 or 1 (got %d)", c->rank_pinned);
     const double units = (double)c->batch * c->n_kv_heads;
     if (units > 1e7) return fail(RAAS_E_INVALID, "batch * n_kv_heads too large");
     return RAAS_OK;
@@ -215,7 +221,8 @@ raas_status raas_create_pool(const raas_config* cfg, void* stream, raas_pool** o
         {(void**)&p->unit, Ly * p->U * kUnitFields * sizeof(int32_t)},
         {(void**)&p->err, 256},
         {(void**)&p->part, (size_t)p->U * max_split * p->G * (p->D + 2) * sizeof(float)},
-        {(void**)&p->score, (size_t)p->U * p->S * sizeof(double)},
+        {(void**)&p->score,
+         (size_t)p->U * p->S * (cfg->score_aggregation == RAAS_SCORE_SOFTMAX_SUM ? p->G : 1) * sizeof(double)},
     };
     hipStream_t s = (hipStream_t)stream;
     hipError_t ea = allow_large_lds();
@@ -297,7 +304,7 @@ raas_status raas_decode_step(raas_pool* p, int32_t layer, const void* q, const v
     StepIO io{q, k_new, v_new, out, page_table_out, timestamps_out, evicted_out};
     hipStream_t s = (hipStream_t)stream;
     const StepPlan pl = plan_step(p->U, p->G, p->D, p->S, p->Lcap, p->ps, p->pinned[layer],
-                                  p->cfg.dtype == RAAS_BF16, p->split_override);
+                                  p->cfg.dtype == RAAS_BF16, p->cfg.score_aggregation, p->split_override);
     L.nsplit = pl.nsplit;
     L.bps = pl.bps;
     // Successive steps of a layer read its pool in opposite directions, so a

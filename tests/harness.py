@@ -44,10 +44,10 @@ def to_device(a: np.ndarray, dtype: str):
     return t.cuda()
 
 
-def new_pool(w, splits=None, policy=None):
+def new_pool(w, splits=None, policy=None, aggregation=0, rank_pinned=False):
     import paper_2502_11147_amd as raas
 
-    kw = {}
+    kw = {"score_aggregation": aggregation, "rank_pinned": rank_pinned}
     if policy is not None:
         kw["prefill_policy"] = policy
     pool = raas.Pool.for_workload(w, **kw)
@@ -62,9 +62,11 @@ def unit_index(w, seq, kvh):
 
 def run_parity(w, seed: int, steps: int, layer: int = 0, units=None, out_every: int = 1,
                splits=None, chunk: int = 64, pool=None, prefill_len=None, check_invariants=True,
-               report: ParityReport | None = None) -> ParityReport:
+               report: ParityReport | None = None, aggregation: int = 0,
+               rank_pinned: bool = False) -> ParityReport:
     """Runs `steps` decode steps of workload `w` on the GPU and checks the
-    listed units (all when None) against the oracle."""
+    listed units (all when None) against the oracle. aggregation and
+    rank_pinned select the score variants on both sides."""
     import torch
 
     rep = report or ParityReport()
@@ -76,13 +78,13 @@ def run_parity(w, seed: int, steps: int, layer: int = 0, units=None, out_every: 
     tol = TOL[w.dtype]
     own_pool = pool is None
     if own_pool:
-        pool = new_pool(w, splits)
+        pool = new_pool(w, splits, aggregation=aggregation, rank_pinned=rank_pinned)
     Kp, Vp = synth.prefill(w, seed, layer, prefill_len=P)
     pool.prefill(layer, to_device(Kp, w.dtype) if P else None, to_device(Vp, w.dtype) if P else None)
     orc = {}
     for u in units:
         b, h = divmod(u, Hkv)
-        m = oracle.Kvm(G, d, ps, S, r=w.r)
+        m = oracle.Kvm(G, d, ps, S, r=w.r, aggregation=aggregation, rank_pinned=rank_pinned)
         rc = m.prefill(Kp[b, h].astype(np.float64), Vp[b, h].astype(np.float64))
         assert rc == 0, rc
         orc[u] = m

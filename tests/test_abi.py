@@ -64,8 +64,21 @@ BAD = [
     dict(n_q_heads=34, n_kv_heads=2), dict(head_dim=96), dict(head_dim=0), dict(page_size=12),
     dict(page_size=4), dict(budget_tokens=250), dict(budget_tokens=16), dict(budget_tokens=0),
     dict(budget_tokens=16 * 2049), dict(dtype=7), dict(r=-0.1), dict(r=1.5), dict(r=float("nan")),
-    dict(prefill_policy=3),
+    dict(prefill_policy=3), dict(score_aggregation=2), dict(score_aggregation=-1), dict(rank_pinned=2),
+    dict(rank_pinned=-1),
 ]
+
+
+def test_config_layout_matches_header():
+    """The binding's Config lists raas_config's fields in the header's order."""
+    import paper_2502_11147_amd as raas
+
+    text = open(HEADER).read()
+    body = re.search(r"typedef struct \{(.*?)\} raas_config;", text, re.S).group(1)
+    body = re.sub(r"/\*.*?\*/", "", body, flags=re.S)
+    fields = re.findall(r"(int32_t|float)\s+(\w+);", body)
+    want = [(n, ctypes.c_int32 if t == "int32_t" else ctypes.c_float) for t, n in fields]
+    assert [(n, t) for n, t in raas.Config._fields_] == want
 
 
 @pytest.mark.parametrize("bad", BAD, ids=[",".join("%s=%s" % kv for kv in b.items()) for b in BAD])

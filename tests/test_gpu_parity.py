@@ -277,3 +277,45 @@ def test_stress_dense_equivalence():
     rep = run_parity(w, seed=0, steps=steps, units=_sample_units(w, 4), out_every=16)
     _report(rep, w.name)
     assert rep.evictions == 0
+
+
+# Score variants (raas_config.score_aggregation and rank_pinned) against the
+# oracle switched the same way: (aggregation, rank_pinned), 1 = sum of
+# per-head softmax.
+VARIANTS = [(0, True), (1, False), (1, True)]
+VARIANT_CASES = [
+    dict(),                                                         # fused step kernel
+    dict(budget=512, prefill_len=100, decode_steps=520, splits=3),  # split path and epilogue kernel
+    dict(dtype="f32"),
+    dict(n_q_heads=28, n_kv_heads=4),                               # G = 7
+    dict(n_q_heads=2, n_kv_heads=2),                                # G = 1
+    dict(prefill_len=1000),                                         # S-1 pinned pages, one decode slot
+    dict(prefill_len=0),                                            # nothing pinned
+    dict(head_dim=64, page_size=8, budget=64, prefill_len=21),
+]
+
+
+@pytest.mark.parametrize("agg,rank", VARIANTS, ids=["agg%d-rank%d" % v for v in VARIANTS])
+@pytest.mark.parametrize("case", VARIANT_CASES, ids=[",".join("%s=%s" % kv for kv in c.items()) or "base"
+                                                     for c in VARIANT_CASES])
+def test_score_variants(agg, rank, case):
+    case = dict(case)
+    splits = case.pop("splits", None)
+    w = small(decode_steps=case.pop("decode_steps", 300), **case)
+    _say("case variant agg %d rank_pinned %d %s splits %s" % (agg, rank, case, splits))
+    rep = run_parity(w, seed=7, steps=w.decode_steps, splits=splits, aggregation=agg, rank_pinned=rank)
+    _report(rep, "variant")
+    assert rep.flagged_divergences <= rep.units_checked // 2
+
+
+@pytest.mark.parametrize("name,steps,units", [("llama8b-b32-L2048", 1024 + 320, 6),
+                                              ("llama8b-b1-L1024", 1024, 8)])
+def test_score_variants_full_size(name, steps, units):
+    """Both variants together at full size, in the benchmark's launch
+    configuration (llama8b-b1 runs split over several workgroups)."""
+    w = synth.get_workload(name)
+    _say("case variant agg 1 rank_pinned 1 %s steps %d" % (name, steps))
+    rep = run_parity(w, seed=1, steps=steps, units=_sample_units(w, units), out_every=32, chunk=128,
+                     aggregation=1, rank_pinned=True)
+    _report(rep, name + " variant")
+    assert rep.evictions > 0
