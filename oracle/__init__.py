@@ -63,6 +63,8 @@ def load(path: str | None = None) -> ctypes.CDLL:
         fp = ctypes.POINTER(ctypes.c_float)
         lib.orc_decode_batch.argtypes = [ctypes.POINTER(vp), ctypes.c_int, fp, fp, fp, dp]
         lib.orc_decode_batch.restype = ctypes.c_int
+        lib.orc_decode_group.argtypes = [ctypes.POINTER(vp), ctypes.c_int, dp, dp, dp, dp]
+        lib.orc_decode_group.restype = ctypes.c_int
         lib.orc_set_variant.argtypes = [vp, ctypes.c_int, ctypes.c_int]
         lib.orc_set_variant.restype = ctypes.c_int
         lib.orc_threads.argtypes = []
@@ -186,6 +188,23 @@ def decode_batch(units: list[Kvm], q, k, v, want_out: bool = True):
                               v.ctypes.data_as(fp), _dptr(out))
     if rc != OK:
         raise OracleError(rc, "orc_decode_batch")
+    return out
+
+
+def decode_group(units: list[Kvm], q, k, v, want_out: bool = True):
+    """One decode step of a sequence whose KV heads (units, alike) share one
+    page table (orc_decode_group). q: [n][G][d]; k, v: [n][d] (fp64).
+    Returns fp64 [n][G][d] or None."""
+    n = len(units)
+    G, d = units[0].G, units[0].d
+    arr = (ctypes.c_void_p * n)(*[u.handle for u in units])
+    q = _f64(q, (n, G, d))
+    k = _f64(k, (n, d))
+    v = _f64(v, (n, d))
+    out = np.empty((n, G, d), np.float64) if want_out else None
+    rc = units[0].lib.orc_decode_group(arr, n, _dptr(q), _dptr(k), _dptr(v), _dptr(out))
+    if rc != OK:
+        raise OracleError(rc, "orc_decode_group")
     return out
 
 

@@ -40,6 +40,9 @@
  *     the normalisation, a lone page's value and the G = 1 reduction to R2).
  *  rank_pinned 1: the pinned prompt pages are ranked together with the
  *     decode pages (n and k count them); only decode pages take timestamps.
+ * Variant of the decision scope (orc_decode_group): one page table per
+ *  (sequence, layer) shared by its KV heads, the page score aggregating all
+ *  of the sequence's query heads.
  */
 #include <math.h>
 #include <stdint.h>
@@ -219,27 +222,12 @@ static int is_full(const orc_kvm* m) {
     return 1;
 }
 
-/*
- * One decode step of one unit: attention, then kvm.store_cache(.., "decode")
- * = store K_new/V_new, give the top-r pages the latest timestamp, and evict
- * the oldest page when the cache is full (Algorithm 1, Section 3.3).
- *
- * q: [G][d]; k_new, v_new: [d]; out: [G][d] or NULL (attention skipped).
- * injected: NULL, or per-slot page scores that replace the representative
- * scores (used to drive the retention policy directly in tests).
- */
-int orc_decode(orc_kvm* m, const double* q, const double* k_new, const double* v_new, double* out,
-               const double* injected) {
-    if (!m) return ORC_E_INVALID;
-    if (!m->prefilled) return ORC_E_STATE;
-    if (!injected && (!q || !k_new || !v_new)) return ORC_E_INVALID;
-    const int G = m->G, d = m->d, S = m->S;
-    const int c = m->clock;
-
-    if (out) attention(m, q, k_new, v_new, out);
-
-    /* store K_new, V_new: into the tail page, or a fresh page taken from the
-     * lowest free slot when the tail is full or absent (Section 3.3) */
+/* store K_new, V_new: into the tail page, or a fresh page taken from the
+ * lowest free slot when the tail is full or absent (Section 3.3). Without
+ * k_new/v_new (retention-only runs) the token takes its place but no
+ * payload. */
+static int store_new_token(orc_kvm* m, const double* k_new, const double* v_new) {
+    const int S = m->S, c = m->clock;
     if (m->tail < 0 || m->fill[m->tail] == m->ps) {
         int s = -1;
         for (int i = 0; i < S; ++i)
@@ -257,60 +245,67 @@ int orc_decode(orc_kvm* m, const double* q, const double* k_new, const double* v
     } else {
         m->fill[m->tail] += 1; /* retention-only run: no payload */
     }
+    return ORC_OK;
+}
 
-    /* the ranked pages: the decode pages, and the pinned ones too when
-     * rank_pinned (R7) */
+/* the ranked pages: the decode pages, and the pinned ones too when
+ * rank_pinned (R7) */
 #define RANKED(st) ((st) == EVICTABLE || (m->rank_pinned && (st) == PINNED))
-    /* one representative score per ranked page (R1, R2) */
-    int n = 0;
-    for (int s = 0; s < S; ++s) {
-        m->score[s] = NAN;
-        if (RANKED(m->state[s])) ++n;
+
+/* per-head bounds of the ranked pages (R1): for this unit's G query heads
+ * j, bound[s*H + h0 + j] = sum_c max(q_jc*kmax_sc, q_jc*kmin_sc). */
+static void head_bounds(const orc_kvm* m, const double* q, double* bound, int H, int h0) {
+    const int G = m->G, d = m->d;
+    for (int s = 0; s < m->S; ++s) {
+        if (!RANKED(m->state[s])) continue;
+        for (int j = 0; j < G; ++j) {
+            double acc = 0.0;
+            for (int ch = 0; ch < d; ++ch) {
+                double a = q[(size_t)j * d + ch] * m->kmax[(size_t)s * d + ch];
+                double b = q[(size_t)j * d + ch] * m->kmin[(size_t)s * d + ch];
+                acc += (a > b) ? a : b;
+            }
+            bound[(size_t)s * H + h0 + j] = acc;
+        }
     }
-    if (injected) {
-        for (int s = 0; s < S; ++s)
-            if (RANKED(m->state[s])) m->score[s] = injected[s];
-    } else if (n > 0) {
-        /* per-head bounds b_j(p) = sum_c max(q_jc*kmax_pc, q_jc*kmin_pc) */
-        double* bound = (double*)malloc(sizeof(double) * (size_t)S * G);
+}
+
+/* one score per ranked page from the bounds of H query heads (R2, or the
+ * softmax variant); m->score is NaN elsewhere */
+static void aggregate(orc_kvm* m, const double* bound, int H) {
+    const int S = m->S;
+    for (int s = 0; s < S; ++s) m->score[s] = NAN;
+    if (m->aggregation == 0) { /* R2: max over the heads */
         for (int s = 0; s < S; ++s) {
             if (!RANKED(m->state[s])) continue;
-            for (int j = 0; j < G; ++j) {
-                double acc = 0.0;
-                for (int ch = 0; ch < d; ++ch) {
-                    double a = q[(size_t)j * d + ch] * m->kmax[(size_t)s * d + ch];
-                    double b = q[(size_t)j * d + ch] * m->kmin[(size_t)s * d + ch];
-                    acc += (a > b) ? a : b;
-                }
-                bound[(size_t)s * G + j] = acc;
-            }
+            double best = -INFINITY;
+            for (int j = 0; j < H; ++j)
+                if (bound[(size_t)s * H + j] > best) best = bound[(size_t)s * H + j];
+            m->score[s] = best;
         }
-        if (m->aggregation == 0) { /* R2: max over the heads */
-            for (int s = 0; s < S; ++s) {
-                if (!RANKED(m->state[s])) continue;
-                double best = -INFINITY;
-                for (int j = 0; j < G; ++j)
-                    if (bound[(size_t)s * G + j] > best) best = bound[(size_t)s * G + j];
-                m->score[s] = best;
-            }
-        } else { /* sum over the heads of each head's softmax over the ranked pages */
-            const double scale = 1.0 / sqrt((double)d);
+    } else { /* sum over the heads of each head's softmax over the ranked pages */
+        const double scale = 1.0 / sqrt((double)m->d);
+        for (int s = 0; s < S; ++s)
+            if (RANKED(m->state[s])) m->score[s] = 0.0;
+        for (int j = 0; j < H; ++j) {
+            double mx = -INFINITY, z = 0.0;
             for (int s = 0; s < S; ++s)
-                if (RANKED(m->state[s])) m->score[s] = 0.0;
-            for (int j = 0; j < G; ++j) {
-                double mx = -INFINITY, z = 0.0;
-                for (int s = 0; s < S; ++s)
-                    if (RANKED(m->state[s]) && bound[(size_t)s * G + j] > mx) mx = bound[(size_t)s * G + j];
-                for (int s = 0; s < S; ++s)
-                    if (RANKED(m->state[s])) z += exp(scale * (bound[(size_t)s * G + j] - mx));
-                for (int s = 0; s < S; ++s)
-                    if (RANKED(m->state[s])) m->score[s] += exp(scale * (bound[(size_t)s * G + j] - mx)) / z;
-            }
+                if (RANKED(m->state[s]) && bound[(size_t)s * H + j] > mx) mx = bound[(size_t)s * H + j];
+            for (int s = 0; s < S; ++s)
+                if (RANKED(m->state[s])) z += exp(scale * (bound[(size_t)s * H + j] - mx));
+            for (int s = 0; s < S; ++s)
+                if (RANKED(m->state[s])) m->score[s] += exp(scale * (bound[(size_t)s * H + j] - mx)) / z;
         }
-        free(bound);
     }
+}
 
-    /* new timestamps to the decode pages among the top-r ranked scores (R7) */
+/* new timestamps (the clock c) to the decode pages among the top-r ranked
+ * scores (R7) */
+static void refresh(orc_kvm* m, int c) {
+    const int S = m->S;
+    int n = 0;
+    for (int s = 0; s < S; ++s)
+        if (RANKED(m->state[s])) ++n;
     int k = (int)floor(m->r * (double)n);
     m->n_evictable = n;
     m->k_refreshed = k;
@@ -330,9 +325,11 @@ int orc_decode(orc_kvm* m, const double* q, const double* k_new, const double* v
         for (int s = 0; s < S; ++s)
             if (m->state[s] == EVICTABLE && m->score[s] > theta) m->ts[s] = c;
     }
-#undef RANKED
+}
 
-    /* if kvm.is_full(): evict the page with the oldest timestamp (R6, R8) */
+/* if kvm.is_full(): evict the page with the oldest timestamp (R6, R8) */
+static int evict_if_full(orc_kvm* m) {
+    const int S = m->S;
     m->evicted = -1;
     if (is_full(m)) {
         int v = -1;
@@ -348,7 +345,94 @@ int orc_decode(orc_kvm* m, const double* q, const double* k_new, const double* v
         m->fill[v] = 0;
         if (m->tail == v) m->tail = -1;
     }
+    return ORC_OK;
+}
+
+/*
+ * One decode step of one unit: attention, then kvm.store_cache(.., "decode")
+ * = store K_new/V_new, give the top-r pages the latest timestamp, and evict
+ * the oldest page when the cache is full (Algorithm 1, Section 3.3).
+ *
+ * q: [G][d]; k_new, v_new: [d]; out: [G][d] or NULL (attention skipped).
+ * injected: NULL, or per-slot page scores that replace the representative
+ * scores (used to drive the retention policy directly in tests).
+ */
+int orc_decode(orc_kvm* m, const double* q, const double* k_new, const double* v_new, double* out,
+               const double* injected) {
+    if (!m) return ORC_E_INVALID;
+    if (!m->prefilled) return ORC_E_STATE;
+    if (!injected && (!q || !k_new || !v_new)) return ORC_E_INVALID;
+    const int G = m->G, S = m->S;
+    const int c = m->clock;
+
+    if (out) attention(m, q, k_new, v_new, out);
+    int rc = store_new_token(m, k_new, v_new);
+    if (rc != ORC_OK) return rc;
+
+    if (injected) {
+        for (int s = 0; s < S; ++s) m->score[s] = RANKED(m->state[s]) ? injected[s] : NAN;
+    } else {
+        double* bound = (double*)malloc(sizeof(double) * (size_t)S * G);
+        head_bounds(m, q, bound, G, 0);
+        aggregate(m, bound, G);
+        free(bound);
+    }
+    refresh(m, c);
+    rc = evict_if_full(m);
+    if (rc != ORC_OK) return rc;
     m->clock = c + 1;
+    return ORC_OK;
+}
+#undef RANKED
+
+/*
+ * Variant of R2 with one decision per (sequence, layer): one decode step of
+ * a sequence whose n KV heads share one page table. ms[h] holds KV head h
+ * with its G query heads; every unit attends over its own keys and stores
+ * its own new token, and a page's score aggregates the bounds of all n*G
+ * query heads (the max, or the sum of per-head softmax), each head against
+ * its own KV head's representative key. The refresh and eviction are then
+ * the same for every KV head. The n units must be alike (configuration,
+ * prefill length, steps), so their slot states are identical.
+ * q: [n][G][d]; k_new, v_new: [n][d]; out: [n][G][d] or NULL.
+ */
+int orc_decode_group(orc_kvm** ms, int n, const double* q, const double* k_new, const double* v_new,
+                     double* out) {
+    if (!ms || n < 1 || !q || !k_new || !v_new) return ORC_E_INVALID;
+    const orc_kvm* a = ms[0];
+    for (int h = 0; h < n; ++h) {
+        const orc_kvm* b = ms[h];
+        if (!b) return ORC_E_INVALID;
+        if (!b->prefilled) return ORC_E_STATE;
+        if (b->G != a->G || b->d != a->d || b->ps != a->ps || b->S != a->S || b->r != a->r ||
+            b->aggregation != a->aggregation || b->rank_pinned != a->rank_pinned ||
+            b->clock != a->clock || b->tail != a->tail || b->next_lid != a->next_lid)
+            return ORC_E_INVALID;
+        for (int s = 0; s < a->S; ++s)
+            if (b->state[s] != a->state[s] || b->lid[s] != a->lid[s] || b->ts[s] != a->ts[s] ||
+                b->fill[s] != a->fill[s])
+                return ORC_E_INVALID;
+    }
+    const int G = a->G, d = a->d, S = a->S, H = n * G;
+    const int c = a->clock;
+    for (int h = 0; h < n; ++h) {
+        if (out)
+            attention(ms[h], q + (size_t)h * G * d, k_new + (size_t)h * d, v_new + (size_t)h * d,
+                      out + (size_t)h * G * d);
+        int rc = store_new_token(ms[h], k_new + (size_t)h * d, v_new + (size_t)h * d);
+        if (rc != ORC_OK) return rc;
+    }
+    double* bound = (double*)malloc(sizeof(double) * (size_t)S * H);
+    for (int h = 0; h < n; ++h) head_bounds(ms[h], q + (size_t)h * G * d, bound, H, h * G);
+    aggregate(ms[0], bound, H);
+    free(bound);
+    for (int h = 0; h < n; ++h) {
+        if (h > 0) memcpy(ms[h]->score, ms[0]->score, sizeof(double) * (size_t)S);
+        refresh(ms[h], c);
+        int rc = evict_if_full(ms[h]);
+        if (rc != ORC_OK) return rc;
+        ms[h]->clock = c + 1;
+    }
     return ORC_OK;
 }
 

@@ -371,7 +371,103 @@ def check_budget_and_attention_set(lib, seed=7):
     assert np.array_equal(out, np.stack([v] * G))
 
 
+def _ranked_slot_lids(st, ps, rank_pinned):
+    """slot -> logical id of the pages a step ranks, from the state before it"""
+    states = (oracle.EVICTABLE, oracle.PINNED) if rank_pinned else (oracle.EVICTABLE,)
+    out = {s: int(st["page_table"][s]) for s in range(len(st["state"])) if st["state"][s] in states}
+    new = _new_slot(st, ps)
+    if new is not None:
+        out[new] = st["next_lid"]
+    return out
+
+
+def check_group_single_token_pages(lib, seed=10):
+    """One page table per (sequence, layer), shared by n KV heads (scope
+    variant of R2). With one token per page the representative bound of a
+    page is the logit of its token, so a page's grouped score is exactly
+    max over the n*G query heads of q.k against the head's own KV head's key
+    (max rule), or the sum over those heads of the token's softmax
+    probability among the ranked tokens, scale 1/sqrt(d) (softmax rule).
+    Every KV head keeps the same page table, and each head's output is
+    textbook attention over its own resident tokens plus the new one."""
+    rng = np.random.default_rng(seed)
+    n, G, d, S, P = 3, 2, 8, 6, 3
+    for agg, rank_pinned in ((0, False), (1, False), (0, True), (1, True)):
+        ms = [oracle.Kvm(G, d, 1, S, lib=lib, aggregation=agg, rank_pinned=rank_pinned) for _ in range(n)]
+        keys = [list(rng.standard_normal((P, d))) for _ in range(n)]  # with page size 1, token = lid
+        vals = [list(rng.standard_normal((P, d))) for _ in range(n)]
+        for h in range(n):
+            assert ms[h].prefill(np.array(keys[h]), np.array(vals[h])) == 0
+        for t in range(40):
+            st0 = ms[0].state()
+            resident = [int(x) for x in st0["page_table"] if x >= 0]
+            ranked = _ranked_slot_lids(st0, 1, rank_pinned)
+            q = rng.standard_normal((n, G, d)) * 1.5
+            k = rng.standard_normal((n, d))
+            v = rng.standard_normal((n, d))
+            out = oracle.decode_group(ms, q, k, v)
+            for h in range(n):
+                keys[h].append(k[h])
+                vals[h].append(v[h])
+                ref = _softmax_attention(q[h], np.array([keys[h][x] for x in resident] + [k[h]]),
+                                         np.array([vals[h][x] for x in resident] + [v[h]]))
+                assert np.max(np.abs(out[h] - ref)) < 1e-12, (agg, t, h)
+            sts = [m.state() for m in ms]
+            for h in range(1, n):
+                for key in ("page_table", "ts", "state", "fill"):
+                    assert np.array_equal(sts[h][key], sts[0][key]), (agg, t, h, key)
+                assert sts[h]["evicted"] == sts[0]["evicted"]
+            sc, _ = ms[0].last_scores()
+            slots = sorted(ranked)
+            lids = [ranked[s] for s in slots]
+            logit = np.array([[[q[h, j] @ keys[h][x] for x in lids] for j in range(G)] for h in range(n)])
+            if agg == 0:
+                want = logit.max(axis=(0, 1))
+            else:
+                z = logit / math.sqrt(d)
+                z = np.exp(z - z.max(axis=2, keepdims=True))
+                want = (z / z.sum(axis=2, keepdims=True)).sum(axis=(0, 1))
+            got = sc[slots]
+            assert np.all(np.abs(got - want) <= 1e-12 * (1 + np.abs(want))), (agg, rank_pinned, t, got, want)
+            assert np.all(np.isnan(np.delete(sc, slots)))
+
+
+def check_group_vs_history(lib, seed=11, cases=30):
+    """Given the scores a grouped step computed, its refresh and eviction
+    follow the single-unit LRU rule: a history-replay LRU fed those scores
+    agrees with the shared page table at every step (n = 1, 2 and 4 KV
+    heads, random keys, several page sizes and r)."""
+    rng = np.random.default_rng(seed)
+    for _ in range(cases):
+        n = int(rng.choice([1, 2, 4]))
+        G = int(rng.integers(1, 4))
+        ps = int(rng.integers(1, 4))
+        S = int(rng.integers(3, 8))
+        P = int(rng.integers(0, (S - 1) * ps + 1))
+        r = float(rng.choice([0.5, 0.25, 0.75, 1.0, 0.0]))
+        rank_pinned = bool(rng.integers(0, 2))
+        agg = int(rng.integers(0, 2))
+        d = 4
+        ms = [oracle.Kvm(G, d, ps, S, r=r, lib=lib, aggregation=agg, rank_pinned=rank_pinned) for _ in range(n)]
+        for m in ms:
+            assert m.prefill(rng.standard_normal((P, d)), rng.standard_normal((P, d))) == 0
+        hist = HistoryLRU(ps, S, r, P, rank_pinned=rank_pinned)
+        for t in range(int(rng.integers(5, 40))):
+            ranked = _ranked_slot_lids(ms[0].state(), ps, rank_pinned)
+            oracle.decode_group(ms, rng.standard_normal((n, G, d)), rng.standard_normal((n, d)),
+                                rng.standard_normal((n, d)), want_out=False)
+            sc, _ = ms[0].last_scores()
+            score_of = {lid: sc[s] for s, lid in ranked.items()}
+            ev = hist.decode(lambda lid: score_of[lid])
+            for m in ms:
+                st = m.state()
+                assert (ev if ev is not None else -1) == st["evicted"], (t, ev, st["evicted"])
+                assert sorted(int(x) for x in st["page_table"] if x >= 0) == hist.resident_lids(), t
+
+
 ALL_CHECKS = [
+    check_group_single_token_pages,
+    check_group_vs_history,
     check_rank_pinned_vs_history,
     check_softmax_sum_invariants,
     check_dense_equivalence,

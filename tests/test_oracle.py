@@ -46,13 +46,17 @@ MUTANTS = [
                               "#define RANKED(st) ((st) == EVICTABLE || (st) == PINNED)")]),
     ("rank_pinned_ignored", [("#define RANKED(st) ((st) == EVICTABLE || (m->rank_pinned && (st) == PINNED))",
                               "#define RANKED(st) ((st) == EVICTABLE)")]),
-    ("softmax_sum_unnormalised", [("m->score[s] += exp(scale * (bound[(size_t)s * G + j] - mx)) / z;",
-                                   "m->score[s] += exp(scale * (bound[(size_t)s * G + j] - mx));")]),
-    ("softmax_sum_one_head", [("            for (int j = 0; j < G; ++j) {\n                double mx = -INFINITY, z = 0.0;",
-                               "            for (int j = 0; j < 1; ++j) {\n                double mx = -INFINITY, z = 0.0;")]),
+    ("softmax_sum_unnormalised", [("m->score[s] += exp(scale * (bound[(size_t)s * H + j] - mx)) / z;",
+                                   "m->score[s] += exp(scale * (bound[(size_t)s * H + j] - mx));")]),
+    ("softmax_sum_one_head", [("        for (int j = 0; j < H; ++j) {\n            double mx = -INFINITY, z = 0.0;",
+                               "        for (int j = 0; j < 1; ++j) {\n            double mx = -INFINITY, z = 0.0;")]),
+    ("group_heads_overlap", [("bound[(size_t)s * H + h0 + j] = acc;", "bound[(size_t)s * H + j] = acc;")]),
+    ("group_first_kv_head_refreshed", [("        refresh(ms[h], c);", "        if (h == 0) refresh(ms[h], c);")]),
+    ("group_first_kv_head_scored", [("    for (int h = 0; h < n; ++h) head_bounds(ms[h], q + (size_t)h * G * d, bound, H, h * G);",
+                                     "    for (int h = 0; h < n; ++h) head_bounds(ms[0], q, bound, H, h * G);")]),
     ("softmax_sign", [("double p = exp(logit[t] - mx);", "double p = exp(mx - logit[t]);")]),
-    ("gqa_last_head_only", [("if (bound[(size_t)s * G + j] > best) best = bound[(size_t)s * G + j];",
-                             "best = bound[(size_t)s * G + j];")]),
+    ("gqa_last_head_only", [("if (bound[(size_t)s * H + j] > best) best = bound[(size_t)s * H + j];",
+                             "best = bound[(size_t)s * H + j];")]),
 ]
 
 
