@@ -41,11 +41,14 @@ def parse():
     ap.add_argument("--warmup", type=int, default=200)
     ap.add_argument("--workload", default=None, help="default: llama8b-b32-L2048")
     ap.add_argument("--seed", type=int, default=0)
+    ap.add_argument("--r", type=float, default=None, help="fraction refreshed per step (default: the workload's)")
     ap.add_argument("--ring", type=int, default=128, help="distinct input steps staged on device")
     ap.add_argument("--splits", type=int, default=0, help="attention splits per unit (0 = automatic)")
     ap.add_argument("--score-aggregation", choices=("max", "softmax-sum"), default="max",
                     help="head aggregation of the page score (default: max over the heads)")
     ap.add_argument("--rank-pinned", action="store_true", help="rank the pinned prefill pages too")
+    ap.add_argument("--decision-scope", choices=("kv-head", "sequence"), default="kv-head",
+                    help="one page table per KV head (default) or per sequence")
     ap.add_argument("--cpu-seconds", type=float, default=15.0, help="budget of the CPU oracle sample")
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--copy-calibration", action="store_true",
@@ -267,14 +270,17 @@ def main():
 
     assert torch.cuda.is_available(), "bench.py needs a GPU"
     w = synth.get_workload(args.workload or synth.workloads.HEADLINE)
+    if args.r is not None:
+        w = w.replace(r=args.r)
     dev = torch.device("cuda", 0)
     torch.cuda.set_device(dev)
     dt = torch.bfloat16 if w.dtype == "bf16" else torch.float32
     U, S = w.batch * w.n_kv_heads, w.slots
 
     agg = raas.SCORE_SOFTMAX_SUM if args.score_aggregation == "softmax-sum" else raas.SCORE_MAX
-    variant = agg != raas.SCORE_MAX or args.rank_pinned
-    pool = raas.Pool.for_workload(w, score_aggregation=agg, rank_pinned=args.rank_pinned)
+    scope = raas.SCOPE_SEQUENCE if args.decision_scope == "sequence" else raas.SCOPE_KV_HEAD
+    variant = agg != raas.SCORE_MAX or args.rank_pinned or scope != raas.SCOPE_KV_HEAD
+    pool = raas.Pool.for_workload(w, score_aggregation=agg, rank_pinned=args.rank_pinned, decision_scope=scope)
     if args.splits:
         pool.set_attention_splits(args.splits)
     Kp, Vp = synth.prefill(w, args.seed, 0)
@@ -369,6 +375,7 @@ def main():
             "resident_tokens_per_unit_avg": float(res.mean()),
             "attention_splits": args.splits or "auto",
             "score_aggregation": args.score_aggregation, "rank_pinned": bool(args.rank_pinned),
+            "decision_scope": args.decision_scope,
         },
         "step_hbm_gbs_algorithmic": round(step_b / (elapsed / args.steps) / 1e9, 1),
         "roofline": {
@@ -389,7 +396,11 @@ def main():
     }
     assert np.all(st_end["clock"] == w.prefill_len + t_start + args.steps)
     if not args.no_cpu_baseline:
-        line["cpu_baseline"] = cpu_baseline(w, args.seed, ring_np, args.cpu_seconds, agg, args.rank_pinned)
+        if scope == raas.SCOPE_KV_HEAD:
+            line["cpu_baseline"] = cpu_baseline(w, args.seed, ring_np, args.cpu_seconds, agg, args.rank_pinned)
+        else:
+            line["cpu_baseline"] = None
+            line["cpu_baseline_note"] = "not sampled for the sequence scope (its oracle step is serial)"
     print(json.dumps(line), flush=True)
 
 

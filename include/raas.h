@@ -81,6 +81,16 @@ typedef enum {
                                   then sum to G */
 } raas_score_aggregation;
 
+/* What one retention decision covers. The paper does not say; both are
+ * readings. */
+typedef enum {
+    RAAS_SCOPE_KV_HEAD = 0, /* one page table per unit (sequence, layer, KV head) (default) */
+    RAAS_SCOPE_SEQUENCE = 1 /* one page table per (sequence, layer), shared by its KV heads:
+                               every KV head keeps its own keys and values in the same slots,
+                               and a page's score aggregates all n_q_heads (<= 1024) query heads,
+                               each against its own KV head's representative key */
+} raas_decision_scope;
+
 typedef struct {
     int32_t batch;          /* sequences, >= 1; all advance together */
     int32_t n_layers;       /* >= 1; each layer has its own pool and clock */
@@ -97,6 +107,7 @@ typedef struct {
     int32_t rank_pinned;       /* 1: the pinned prefill pages are scored and ranked with the
                                   evictable ones (n counts them) but never take timestamps;
                                   0: only evictable pages are ranked */
+    int32_t decision_scope;    /* raas_decision_scope */
 } raas_config;
 
 typedef struct raas_pool raas_pool; /* opaque */

@@ -17,6 +17,7 @@ OK, E_INVALID, E_BUDGET, E_STATE, E_HIP, E_OOM = 0, -1, -2, -3, -4, -5
 F32, BF16 = 0, 1
 PREFILL_PIN_HEAD, PREFILL_ERROR = 0, 1
 SCORE_MAX, SCORE_SOFTMAX_SUM = 0, 1
+SCOPE_KV_HEAD, SCOPE_SEQUENCE = 0, 1
 FREE, PINNED, EVICTABLE = 0, 1, 2
 KERNELS = ("append", "attention", "merge", "score")
 
@@ -48,6 +49,7 @@ class Config(ctypes.Structure):
         ("prefill_policy", ctypes.c_int32),
         ("score_aggregation", ctypes.c_int32),
         ("rank_pinned", ctypes.c_int32),
+        ("decision_scope", ctypes.c_int32),
     ]
 
 
@@ -117,11 +119,11 @@ class Pool:
     def __init__(self, batch: int, n_layers: int, n_q_heads: int, n_kv_heads: int, head_dim: int,
                  page_size: int, budget_tokens: int, dtype: str = "bf16", r: float = 0.5,
                  prefill_policy: int = PREFILL_PIN_HEAD, score_aggregation: int = SCORE_MAX,
-                 rank_pinned: bool = False, stream=None):
+                 rank_pinned: bool = False, decision_scope: int = SCOPE_KV_HEAD, stream=None):
         self.lib = load_library()
         self.cfg = Config(batch, n_layers, n_q_heads, n_kv_heads, head_dim, page_size, budget_tokens,
                           BF16 if dtype == "bf16" else F32, r, prefill_policy, score_aggregation,
-                          int(rank_pinned))
+                          int(rank_pinned), decision_scope)
         self.dtype = dtype
         self.batch, self.n_layers = batch, n_layers
         self.n_q_heads, self.n_kv_heads, self.head_dim = n_q_heads, n_kv_heads, head_dim

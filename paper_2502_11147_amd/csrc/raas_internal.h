@@ -47,6 +47,7 @@ struct LayerView {
     int bf16;         // 1: bf16 pool, 0: fp32 pool
     int agg;          // head aggregation of the page score: 0 max, 1 sum of per-head softmax
     int rank_pinned;  // 1: pinned pages are scored and ranked (never refreshed)
+    int hgrp;         // units per retention decision: 1, or n_kv_heads (units seq*hgrp .. +hgrp-1)
 };
 
 struct StepIO {
@@ -67,8 +68,9 @@ struct StepPlan {
     size_t lds;      // dynamic LDS of the step kernel
 };
 
+// grouped: retention decided per group of units, by the epilogue kernel
 StepPlan plan_step(int U, int G, int D, int S, int Lcap, int ps, int pinned, bool bf16, int agg,
-                   int split_override);
+                   bool grouped, int split_override);
 // Lets the step kernels use more than the default dynamic LDS.
 hipError_t allow_large_lds();
 
@@ -78,7 +80,8 @@ hipError_t launch_prefill(const LayerView& L, const void* k, const void* v, int 
 // The step kernel: attention, page scores, append; plus the epilogue when fused.
 hipError_t launch_step(const LayerView& L, const StepIO& io, const StepPlan& plan, double r,
                        hipStream_t stream);
-// The epilogue kernel of the split path: merge, refresh, evict, state out.
+// The epilogue kernel of the split path: merge, refresh, evict, state out;
+// one workgroup per group of L.hgrp units.
 hipError_t launch_epilogue(const LayerView& L, const StepIO& io, double r, hipStream_t stream);
 
 }  // namespace raas

@@ -355,40 +355,55 @@ struct RetShared {
     int victim, evicted, next_slot, next_fill, tail_after, errs;
 };
 
-// Page scores of the softmax aggregation, by one wavefront: for each query
-// head j, a softmax over the ranked pages of the head's bounds b_j (scale
-// 1/sqrt(D), shifted by the head's largest bound M_j), summed over the heads
-// in head order: score(p) = sum_j exp(c (b_j(p) - M_j)) / Z_j. hb[p*G + j]
-// holds b_j(p) for every ranked page p.
-__device__ void softmax_sum_scores(const LayerView& L, const double* hb, const int* s_state, double* s_score) {
-    const int S = L.S, G = L.G, lane = threadIdx.x & 63;
+// Page scores of the softmax aggregation, by a whole workgroup (every
+// thread calls it): for each query head, a softmax over the ranked pages of
+// the head's bounds b (scale c = 1/sqrt(D), shifted by the head's largest
+// bound M), summed over the heads in head order: score(p) = sum_hj
+// exp(c (b_hj(p) - M_hj)) / Z_hj. The heads are the G of each of nu units
+// deciding together; hb[((h*S) + p)*G + j] holds head j of unit h's bound of
+// page p for every ranked page p. First one wavefront per head finds M and Z
+// (into s_mz), then one thread per page sums its terms; s_score is visible
+// to the whole workgroup on return.
+__device__ void softmax_sum_block(const LayerView& L, const double* hb, int nu, const int* s_state,
+                                  double* s_score, double* s_mz, int tid, int nthreads) {
+    const int S = L.S, G = L.G, H = nu * G, lane = tid & 63, nw = nthreads >> 6;
     const double c = 1.0 / sqrt((double)L.D);
-    for (int p = lane; p < S; p += 64)
-        if (ranked(L, s_state[p])) s_score[p] = 0.0;
-    for (int j = 0; j < G; ++j) {
+    for (int hj = tid >> 6; hj < H; hj += nw) {
+        const int h = hj / G, j = hj - (hj / G) * G;
+        const double* hbj = hb + (size_t)h * S * G + j;
         double mx = -INFINITY;
         for (int p = lane; p < S; p += 64)
-            if (ranked(L, s_state[p])) mx = fmax(mx, hb[(size_t)p * G + j]);
+            if (ranked(L, s_state[p])) mx = fmax(mx, hbj[(size_t)p * G]);
 #pragma unroll
         for (int off = 32; off >= 1; off >>= 1) mx = fmax(mx, __shfl_xor(mx, off));
         double z = 0.0;
         for (int p = lane; p < S; p += 64)
-            if (ranked(L, s_state[p])) z += exp(c * (hb[(size_t)p * G + j] - mx));
+            if (ranked(L, s_state[p])) z += exp(c * (hbj[(size_t)p * G] - mx));
 #pragma unroll
         for (int off = 32; off >= 1; off >>= 1) z += __shfl_xor(z, off);
-        for (int p = lane; p < S; p += 64)
-            if (ranked(L, s_state[p])) s_score[p] += exp(c * (hb[(size_t)p * G + j] - mx)) / z;
+        if (lane == 0) {
+            s_mz[2 * hj] = mx;
+            s_mz[2 * hj + 1] = z;
+        }
     }
-    // every lane's scores are read by the ranking below
-    __atomic_signal_fence(__ATOMIC_SEQ_CST);
-    __builtin_amdgcn_wave_barrier();
+    __syncthreads();
+    for (int p = tid; p < S; p += nthreads) {
+        if (!ranked(L, s_state[p])) continue;
+        double acc = 0.0;
+#pragma unroll 8
+        for (int hj = 0; hj < H; ++hj) {
+            const int h = hj / G, j = hj - (hj / G) * G;
+            acc += exp(c * (hb[((size_t)h * S + p) * G + j] - s_mz[2 * hj])) / s_mz[2 * hj + 1];
+        }
+        s_score[p] = acc;
+    }
+    __syncthreads();
 }
 
 // Retention policy of one unit, run by one wavefront (Algorithm 1,
 // store_cache; Sections 3.2-3.3) on the slot state in LDS, the opened page
 // already marked evictable and s_score holding every ranked page's score
-// (+inf elsewhere), or, with the softmax aggregation, hb holding the ranked
-// pages' per-head bounds:
+// (+inf elsewhere):
 //  - top-r refresh: with n ranked pages and k = floor(r*n), an evictable
 //    page p gets ts = clock when at least n-k ranked pages score strictly
 //    less, i.e. exactly the pages above the (n-k)-th smallest score (the
@@ -399,10 +414,9 @@ __device__ void softmax_sum_scores(const LayerView& L, const double* hb, const i
 //    the smallest (timestamp, logical id) is freed;
 //  - the next token's target: the tail page if it has room, else the lowest
 //    free slot (a fresh page).
-__device__ void retention_wave(const LayerView& L, const UnitRec& ur, double r, double* s_score,
-                               int* s_state, int* s_ts, const int* s_lid, RetShared& out, const double* hb) {
+__device__ void retention_wave(const LayerView& L, const UnitRec& ur, double r, const double* s_score,
+                               int* s_state, int* s_ts, const int* s_lid, RetShared& out) {
     const int S = L.S, ps = L.ps, lane = threadIdx.x & 63;
-    if (hb != nullptr) softmax_sum_scores(L, hb, s_state, s_score);
     int n = 0, nfree = 0;
     for (int s0 = 0; s0 < S; s0 += 64) {
         const int s = s0 + lane;
@@ -591,7 +605,8 @@ __device__ __forceinline__ void attend_block(const u32x4 (&kr)[2][D / 32], const
 // has finished its passes (a workgroup barrier), wavefront 0 runs the
 // retention policy when one workgroup covers the unit (fused), then goes on
 // claiming blocks. The state reaches the pool only after the attention has
-// read it; the wavefronts' partial outputs merge at the end.
+// read it; the wavefronts' partial outputs merge at the end, into the output
+// when one workgroup covers the unit, else into the split's partial.
 
 // AGG: the softmax aggregation of the page scores (a separate instance, so
 // that the default one carries none of its registers).
@@ -612,7 +627,8 @@ __global__ __launch_bounds__(NW * 64) __attribute__((amdgpu_waves_per_eu(1, 2)))
     float* s_o = reinterpret_cast<float*>(s_qd + (size_t)G * qpad_row(D));  // [NW][G][D+4]
     double* s_score = reinterpret_cast<double*>(s_o + (size_t)NW * G * (D + 4));  // [S], fused only
     double* s_hb = s_score + S;  // [S][G] per-head bounds, fused softmax aggregation only
-    int* s_state = reinterpret_cast<int*>(s_hb + (AGG ? (size_t)S * G : 0));  // [S], fused only
+    double* s_mz = s_hb + (AGG ? (size_t)S * G : 0);  // [G][2] each head's M and Z, likewise
+    int* s_state = reinterpret_cast<int*>(s_mz + (AGG ? 2 * G : 0));  // [S], fused only
     int* s_ts = s_state + S;
     int* s_lid = s_ts + S;
 
@@ -749,7 +765,8 @@ __global__ __launch_bounds__(NW * 64) __attribute__((amdgpu_waves_per_eu(1, 2)))
     bool decided = false;
     auto scores_done = [&]() {
         lds_barrier();
-        if (fused && w == 0) retention_wave(L, ur, r, s_score, s_state, s_ts, s_lid, ret, AGG ? s_hb : nullptr);
+        if (AGG && fused) softmax_sum_block(L, s_hb, 1, s_state, s_score, s_mz, tid, NW * 64);
+        if (fused && w == 0) retention_wave(L, ur, r, s_score, s_state, s_ts, s_lid, ret);
         decided = true;
     };
 
@@ -853,7 +870,7 @@ __global__ __launch_bounds__(NW * 64) __attribute__((amdgpu_waves_per_eu(1, 2)))
             O += wt * s_o[((size_t)ww * G + h) * (D + 4) + c];
             Ls += wt * s_l[ww][h];
         }
-        if (fused) {
+        if (nsplit == 1) {  // the whole unit: the output itself
             ((uint16_t*)io.out)[((size_t)u * G + h) * D + c] = f2bf(O / Ls);
         } else {
             float* pp = L.part + (((size_t)u * nsplit + split) * G + h) * (D + 2);
@@ -992,29 +1009,40 @@ __global__ __launch_bounds__(64) void k_step_f32(LayerView L, StepIO io, float s
 // Epilogue kernel of the split path: merges the splits' partial attention
 // (out = sum_s 2^(M_s - M) O_s / sum_s 2^(M_s - M) L_s) while wavefront 0
 // runs the retention policy on the scores the splits wrote; then the state
-// goes out.
+// goes out. One workgroup per decision: L.hgrp units (the KV heads of a
+// sequence when they share one page table, whose slot states are then
+// identical), a page's score aggregating the bounds of all their heads.
+// merge 0: the step kernel wrote the outputs (bf16, one workgroup per unit).
 template <typename T>
-__global__ __launch_bounds__(256) void k_epilogue(LayerView L, StepIO io, double r) {
+__global__ __launch_bounds__(256) void k_epilogue(LayerView L, StepIO io, double r, int merge) {
     extern __shared__ __align__(16) unsigned char smem[];
     __shared__ RetShared ret;
-    const int S = L.S, G = L.G, D = L.D, nsplit = L.nsplit;
+    const int S = L.S, G = L.G, D = L.D, nsplit = L.nsplit, nu = L.hgrp;
     double* s_score = reinterpret_cast<double*>(smem);
-    int* s_state = reinterpret_cast<int*>(s_score + S);
+    double* s_mz = s_score + S;  // [nu*G][2], softmax aggregation only
+    int* s_state = reinterpret_cast<int*>(s_mz + (L.agg ? 2 * (size_t)nu * G : 0));
     int* s_ts = s_state + S;
     int* s_lid = s_ts + S;
-    const int u = blockIdx.x;
-    const size_t base = (size_t)u * S;
-    const UnitRec ur = read_unit(L, u);
-    load_slots(L, u, ur, s_score, s_state, s_ts, s_lid);
+    const int u0 = blockIdx.x * nu;
+    const size_t base = (size_t)u0 * S;
+    const UnitRec ur = read_unit(L, u0);
+    load_slots(L, u0, ur, s_score, s_state, s_ts, s_lid);
     __syncthreads();
     if (!L.agg)
         for (int s = threadIdx.x; s < S; s += blockDim.x)
-            if (ranked(L, s_state[s])) s_score[s] = L.score[base + s];
+            if (ranked(L, s_state[s])) {
+                double best = L.score[base + s];
+#pragma unroll 8
+                for (int h = 1; h < nu; ++h) best = fmax(best, L.score[base + (size_t)h * S + s]);
+                s_score[s] = best;
+            }
     __syncthreads();
-    if (threadIdx.x < 64)
-        retention_wave(L, ur, r, s_score, s_state, s_ts, s_lid, ret, L.agg ? L.score + base * G : nullptr);
-    for (int idx = threadIdx.x; idx < G * D; idx += blockDim.x) {
-        const int h = idx / D, c = idx - (idx / D) * D;
+    if (L.agg) softmax_sum_block(L, L.score + base * G, nu, s_state, s_score, s_mz, threadIdx.x, blockDim.x);
+    if (threadIdx.x < 64) retention_wave(L, ur, r, s_score, s_state, s_ts, s_lid, ret);
+    for (int idx = threadIdx.x; merge && idx < nu * G * D; idx += blockDim.x) {
+        const int uh = idx / (G * D), rem = idx - uh * (G * D);
+        const int u = u0 + uh;
+        const int h = rem / D, c = rem - (rem / D) * D;
         float M = -INFINITY;
         for (int s = 0; s < nsplit; ++s)
             M = fmaxf(M, L.part[(((size_t)u * nsplit + s) * G + h) * (D + 2) + D]);
@@ -1029,7 +1057,8 @@ __global__ __launch_bounds__(256) void k_epilogue(LayerView L, StepIO io, double
         ((T*)io.out)[((size_t)u * G + h) * D + c] = from_f<T>(O / Ls);
     }
     __syncthreads();
-    retention_store(L, io, u, ur, s_state, s_ts, s_lid, ret, threadIdx.x, blockDim.x);
+    for (int uh = 0; uh < nu; ++uh)
+        retention_store(L, io, u0 + uh, ur, s_state, s_ts, s_lid, ret, threadIdx.x, blockDim.x);
 }
 
 inline unsigned grid1d(size_t n, int block) { return (unsigned)((n + block - 1) / block); }
@@ -1039,7 +1068,7 @@ inline unsigned grid1d(size_t n, int block) { return (unsigned)((n + block - 1) 
 // bounds of the softmax aggregation)
 size_t step_lds(int G, int D, int S, int NW, bool fused, int agg) {
     size_t b = (size_t)8 * G * qpad_row(D) + (size_t)NW * G * (D + 4) * 4;
-    if (fused) b += (size_t)S * 20 + (agg ? (size_t)S * G * 8 : 0);
+    if (fused) b += (size_t)S * 20 + (agg ? (size_t)S * G * 8 + (size_t)G * 16 : 0);
     return b;
 }
 
@@ -1059,7 +1088,7 @@ hipError_t launch_step_bf16(const LayerView& L, const StepIO& io, const StepPlan
 // ---------------------------------------------------------------------------
 
 StepPlan plan_step(int U, int G, int D, int S, int Lcap, int ps, int pinned, bool bf16, int agg,
-                   int split_override) {
+                   bool grouped, int split_override) {
     (void)pinned;
     (void)ps;
     StepPlan pl{};
@@ -1089,7 +1118,7 @@ StepPlan plan_step(int U, int G, int D, int S, int Lcap, int ps, int pinned, boo
     want = want > nblk ? nblk : want;
     pl.bps = (nblk + want - 1) / want;
     pl.nsplit = (nblk + pl.bps - 1) / pl.bps;
-    pl.fused = bf16 && pl.nsplit == 1 && step_lds(G, D, S, pl.waves, true, agg) <= kMaxLds;
+    pl.fused = bf16 && !grouped && pl.nsplit == 1 && step_lds(G, D, S, pl.waves, true, agg) <= kMaxLds;
     pl.lds = bf16 ? step_lds(G, D, S, pl.waves, pl.fused, agg) : 0;
     return pl;
 }
@@ -1172,11 +1201,13 @@ hipError_t launch_step(const LayerView& L, const StepIO& io, const StepPlan& pl,
 }
 
 hipError_t launch_epilogue(const LayerView& L, const StepIO& io, double r, hipStream_t stream) {
-    const size_t shm = (size_t)L.S * (8 + 12);
+    const size_t shm = (size_t)L.S * (8 + 12) + (L.agg ? (size_t)L.hgrp * L.G * 16 : 0);
+    const dim3 grid((unsigned)(L.U / L.hgrp));
+    const int merge = !(L.bf16 && L.nsplit == 1);  // else the step kernel wrote the outputs
     if (L.bf16)
-        hipLaunchKernelGGL(k_epilogue<uint16_t>, dim3(L.U), dim3(256), shm, stream, L, io, r);
+        hipLaunchKernelGGL(k_epilogue<uint16_t>, grid, dim3(256), shm, stream, L, io, r, merge);
     else
-        hipLaunchKernelGGL(k_epilogue<float>, dim3(L.U), dim3(256), shm, stream, L, io, r);
+        hipLaunchKernelGGL(k_epilogue<float>, grid, dim3(256), shm, stream, L, io, r, merge);
     return hipGetLastError();
 }
 

@@ -101,6 +101,7 @@ LayerView view(const raas_pool* p, int layer) {
     L.bf16 = p->cfg.dtype == RAAS_BF16;
     L.agg = p->cfg.score_aggregation;
     L.rank_pinned = p->cfg.rank_pinned;
+    L.hgrp = p->cfg.decision_scope == RAAS_SCOPE_SEQUENCE ? p->cfg.n_kv_heads : 1;
     return L;
 }
 
@@ -135,6 +136,11 @@ raas_status validate(const raas_config* c) {
         return fail(RAAS_E_INVALID, "unknown score_aggregation %d", c->score_aggregation);
     if (c->rank_pinned != 0 && c->rank_pinned != 1)
         return fail(RAAS_E_INVALID, "rank_pinned must be 0 or 1 (got %d)", c->rank_pinned);
+    if (c->decision_scope != RAAS_SCOPE_KV_HEAD && c->decision_scope != RAAS_SCOPE_SEQUENCE)
+        return fail(RAAS_E_INVALID, "unknown decision_scope %d", c->decision_scope);
+    if (c->decision_scope == RAAS_SCOPE_SEQUENCE && c->n_q_heads > 1024)
+        return fail(RAAS_E_INVALID, "one decision per sequence covers at most 1024 query heads (got %d)",
+                    c->n_q_heads);
     const double units = (double)c->batch * c->n_kv_heads;
     if (units > 1e7) return fail(RAAS_E_INVALID, "batch * n_kv_heads too large");
     return RAAS_OK;
@@ -304,7 +310,8 @@ raas_status raas_decode_step(raas_pool* p, int32_t layer, const void* q, const v
     StepIO io{q, k_new, v_new, out, page_table_out, timestamps_out, evicted_out};
     hipStream_t s = (hipStream_t)stream;
     const StepPlan pl = plan_step(p->U, p->G, p->D, p->S, p->Lcap, p->ps, p->pinned[layer],
-                                  p->cfg.dtype == RAAS_BF16, p->cfg.score_aggregation, p->split_override);
+                                  p->cfg.dtype == RAAS_BF16, p->cfg.score_aggregation,
+                                  p->cfg.decision_scope == RAAS_SCOPE_SEQUENCE, p->split_override);
     L.nsplit = pl.nsplit;
     L.bps = pl.bps;
     // Successive steps of a layer read its pool in opposite directions, so a

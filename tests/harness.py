@@ -44,10 +44,10 @@ def to_device(a: np.ndarray, dtype: str):
     return t.cuda()
 
 
-def new_pool(w, splits=None, policy=None, aggregation=0, rank_pinned=False):
+def new_pool(w, splits=None, policy=None, aggregation=0, rank_pinned=False, scope=0):
     import paper_2502_11147_amd as raas
 
-    kw = {"score_aggregation": aggregation, "rank_pinned": rank_pinned}
+    kw = {"score_aggregation": aggregation, "rank_pinned": rank_pinned, "decision_scope": scope}
     if policy is not None:
         kw["prefill_policy"] = policy
     pool = raas.Pool.for_workload(w, **kw)
@@ -63,10 +63,12 @@ def unit_index(w, seq, kvh):
 def run_parity(w, seed: int, steps: int, layer: int = 0, units=None, out_every: int = 1,
                splits=None, chunk: int = 64, pool=None, prefill_len=None, check_invariants=True,
                report: ParityReport | None = None, aggregation: int = 0,
-               rank_pinned: bool = False) -> ParityReport:
+               rank_pinned: bool = False, scope: int = 0) -> ParityReport:
     """Runs `steps` decode steps of workload `w` on the GPU and checks the
-    listed units (all when None) against the oracle. aggregation and
-    rank_pinned select the score variants on both sides."""
+    listed units (all when None) against the oracle. aggregation,
+    rank_pinned and scope select the variants on both sides; with scope 1
+    (one page table per sequence) every KV head of a listed unit's sequence
+    is checked, the oracle stepping each sequence's units together."""
     import torch
 
     rep = report or ParityReport()
@@ -75,10 +77,12 @@ def run_parity(w, seed: int, steps: int, layer: int = 0, units=None, out_every: 
     U = B * Hkv
     P = w.prefill_len if prefill_len is None else prefill_len
     units = list(range(U)) if units is None else list(units)
+    if scope == 1:
+        units = sorted({b * Hkv + h for b in {u // Hkv for u in units} for h in range(Hkv)})
     tol = TOL[w.dtype]
     own_pool = pool is None
     if own_pool:
-        pool = new_pool(w, splits, aggregation=aggregation, rank_pinned=rank_pinned)
+        pool = new_pool(w, splits, aggregation=aggregation, rank_pinned=rank_pinned, scope=scope)
     Kp, Vp = synth.prefill(w, seed, layer, prefill_len=P)
     pool.prefill(layer, to_device(Kp, w.dtype) if P else None, to_device(Vp, w.dtype) if P else None)
     orc = {}
@@ -88,7 +92,11 @@ def run_parity(w, seed: int, steps: int, layer: int = 0, units=None, out_every: 
         rc = m.prefill(Kp[b, h].astype(np.float64), Vp[b, h].astype(np.float64))
         assert rc == 0, rc
         orc[u] = m
-    live = set(units)
+    # decision groups: the units deciding together, keyed by their first unit
+    groups = {}
+    for u in units:
+        groups.setdefault(u - u % Hkv if scope == 1 else u, []).append(u)
+    live = set(groups)
     rep.units_checked += len(units)
     dt = torch.bfloat16 if w.dtype == "bf16" else torch.float32
     for t0 in range(0, steps, chunk):
@@ -116,37 +124,44 @@ def run_parity(w, seed: int, steps: int, layer: int = 0, units=None, out_every: 
             rep.evictions += int(np.sum(ev_h[i] >= 0))
             if check_invariants:
                 _check_invariants(pt_h[i], ts_h[i], ev_h[i], clock, P, ps, S)
-            for u in sorted(live):
-                m = orc[u]
-                o = m.decode(q64[i, u], k64[i, u], v64[i, u], want_out=want_out)
-                st = m.state()
-                scores, theta = m.last_scores()
+            for g in sorted(live):
+                members = groups[g]
+                if len(members) == 1:
+                    u = members[0]
+                    outs = {u: orc[u].decode(q64[i, u], k64[i, u], v64[i, u], want_out=want_out)}
+                else:
+                    o = oracle.decode_group([orc[u] for u in members], q64[i, members], k64[i, members],
+                                            v64[i, members], want_out=want_out)
+                    outs = {u: (None if o is None else o[j]) for j, u in enumerate(members)}
+                scores, theta = orc[members[0]].last_scores()
                 flagged = _flagged_pages(scores, theta)
                 if len(flagged) >= 2:
                     rep.flagged_steps += 1
-                same_pt = np.array_equal(st["page_table"], pt_h[i, u])
-                same_ts = np.array_equal(st["ts"], ts_h[i, u])
-                same_ev = st["evicted"] == ev_h[i, u]
-                if not (same_pt and same_ts and same_ev):
-                    bad = set(np.nonzero(st["ts"] != ts_h[i, u])[0]) | set(
-                        np.nonzero(st["page_table"] != pt_h[i, u])[0])
-                    if len(flagged) >= 2 and bad <= flagged | _victims(st, pt_h[i, u]):
-                        rep.flagged_divergences += 1
-                        rep.notes.append("unit %d step %d: flagged near-tie divergence" % (u, t))
-                        live.discard(u)
-                        continue
-                    raise AssertionError(
-                        "retention mismatch: workload %s seed %d layer %d unit %d step %d\n"
-                        "oracle pt %s\n   gpu pt %s\noracle ts %s\n   gpu ts %s\noracle ev %d gpu ev %d"
-                        % (w.name, seed, layer, u, t, st["page_table"].tolist(), pt_h[i, u].tolist(),
-                           st["ts"].tolist(), ts_h[i, u].tolist(), st["evicted"], ev_h[i, u]))
-                if want_out:
-                    err = float(np.max(np.abs(out_h[i, u].astype(np.float64) - o)))
-                    rep.max_abs_err = max(rep.max_abs_err, err)
-                    rep.outputs_compared += 1
-                    if not (err <= tol):
-                        raise AssertionError("output mismatch: workload %s seed %d layer %d unit %d step %d: "
-                                             "max abs err %.3g > %g" % (w.name, seed, layer, u, t, err, tol))
+                for u in members:
+                    st = orc[u].state()
+                    same_pt = np.array_equal(st["page_table"], pt_h[i, u])
+                    same_ts = np.array_equal(st["ts"], ts_h[i, u])
+                    same_ev = st["evicted"] == ev_h[i, u]
+                    if not (same_pt and same_ts and same_ev):
+                        bad = set(np.nonzero(st["ts"] != ts_h[i, u])[0]) | set(
+                            np.nonzero(st["page_table"] != pt_h[i, u])[0])
+                        if len(flagged) >= 2 and bad <= flagged | _victims(st, pt_h[i, u]):
+                            rep.flagged_divergences += 1
+                            rep.notes.append("unit %d step %d: flagged near-tie divergence" % (u, t))
+                            live.discard(g)
+                            break
+                        raise AssertionError(
+                            "retention mismatch: workload %s seed %d layer %d unit %d step %d\n"
+                            "oracle pt %s\n   gpu pt %s\noracle ts %s\n   gpu ts %s\noracle ev %d gpu ev %d"
+                            % (w.name, seed, layer, u, t, st["page_table"].tolist(), pt_h[i, u].tolist(),
+                               st["ts"].tolist(), ts_h[i, u].tolist(), st["evicted"], ev_h[i, u]))
+                    if want_out:
+                        err = float(np.max(np.abs(out_h[i, u].astype(np.float64) - outs[u])))
+                        rep.max_abs_err = max(rep.max_abs_err, err)
+                        rep.outputs_compared += 1
+                        if not (err <= tol):
+                            raise AssertionError("output mismatch: workload %s seed %d layer %d unit %d step %d: "
+                                                 "max abs err %.3g > %g" % (w.name, seed, layer, u, t, err, tol))
         rep.steps = t0 + n
     if own_pool:
         pool.close()

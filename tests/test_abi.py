@@ -65,7 +65,8 @@ BAD = [
     dict(page_size=4), dict(budget_tokens=250), dict(budget_tokens=16), dict(budget_tokens=0),
     dict(budget_tokens=16 * 2049), dict(dtype=7), dict(r=-0.1), dict(r=1.5), dict(r=float("nan")),
     dict(prefill_policy=3), dict(score_aggregation=2), dict(score_aggregation=-1), dict(rank_pinned=2),
-    dict(rank_pinned=-1),
+    dict(rank_pinned=-1), dict(decision_scope=2), dict(decision_scope=-1),
+    dict(decision_scope=1, n_q_heads=2048, n_kv_heads=128),
 ]
 
 

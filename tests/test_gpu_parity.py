@@ -319,3 +319,44 @@ def test_score_variants_full_size(name, steps, units):
                      aggregation=1, rank_pinned=True)
     _report(rep, name + " variant")
     assert rep.evictions > 0
+
+
+# One page table per (sequence, layer) shared by its KV heads (decision
+# scope 1), against the oracle's grouped step; (aggregation, rank_pinned).
+SCOPE_VARIANTS = [(0, False), (1, False), (0, True)]
+SCOPE_CASES = [
+    dict(),                                                         # 2 KV heads per sequence
+    dict(n_q_heads=16, n_kv_heads=4, budget=512, prefill_len=100, decode_steps=520, splits=3),
+    dict(dtype="f32"),
+    dict(n_q_heads=28, n_kv_heads=4),                               # G = 7
+    dict(n_q_heads=4, n_kv_heads=1),                                # one KV head: the per-head rule
+    dict(prefill_len=1000),                                         # S-1 pinned pages
+]
+
+
+@pytest.mark.parametrize("agg,rank", SCOPE_VARIANTS, ids=["agg%d-rank%d" % v for v in SCOPE_VARIANTS])
+@pytest.mark.parametrize("case", SCOPE_CASES, ids=[",".join("%s=%s" % kv for kv in c.items()) or "base"
+                                                   for c in SCOPE_CASES])
+def test_sequence_scope(agg, rank, case):
+    case = dict(case)
+    splits = case.pop("splits", None)
+    w = small(decode_steps=case.pop("decode_steps", 300), **case)
+    _say("case sequence-scope agg %d rank_pinned %d %s splits %s" % (agg, rank, case, splits))
+    rep = run_parity(w, seed=9, steps=w.decode_steps, splits=splits, aggregation=agg, rank_pinned=rank,
+                     scope=1)
+    _report(rep, "sequence-scope")
+    assert rep.evictions > 0
+    assert rep.flagged_divergences <= rep.units_checked // 2
+
+
+def test_sequence_scope_full_size():
+    """One page table per sequence on the benchmark workload: two sampled
+    sequences (16 units), in the launch configuration the benchmark times
+    with this scope."""
+    w = synth.get_workload("llama8b-b32-L2048")
+    steps = 1024 + 320
+    _say("case sequence-scope %s steps %d" % (w.name, steps))
+    rep = run_parity(w, seed=2, steps=steps, units=[3 * w.n_kv_heads, 29 * w.n_kv_heads], out_every=32,
+                     chunk=128, scope=1)
+    _report(rep, w.name + " sequence-scope")
+    assert rep.evictions > 0 and rep.units_checked == 16
