@@ -128,6 +128,25 @@ raas_status raas_create_pool(const raas_config* cfg, void* stream, raas_pool** o
 raas_status raas_prefill(raas_pool* pool, int32_t layer, const void* k, const void* v,
                          int32_t prefill_len, void* stream);
 
+/* Ragged prefill of one layer: sequence b stores its first prefill_lens[b]
+ * tokens, as raas_prefill does for all (per-sequence clocks, pinned pages
+ * and budget rule). k, v: [batch][n_kv_heads][max_len][head_dim], rows past
+ * a sequence's length ignored (NULL allowed when no selected sequence keeps
+ * a token). prefill_lens: HOST int32 [batch], each in [0, max_len].
+ * seq_mask: optional HOST int32 [batch]; only sequences with a nonzero entry
+ * are (re)initialised, the others keep their state (NULL = all). Unlike
+ * raas_prefill it may be called again at any time: a selected sequence
+ * starts over with the new prompt (its pages freed, its clock reset), which
+ * is how a finished request's place in the batch is reused. The first
+ * prefill of a layer must cover every sequence (else RAAS_E_STATE). The
+ * lengths reach the device through a pinned buffer of the pool; a call first
+ * waits for the previous ragged prefill's copy out of it. Errors:
+ * RAAS_E_INVALID, RAAS_E_STATE, RAAS_E_BUDGET (policy RAAS_PREFILL_ERROR and
+ * a selected prompt over S-1 pages), RAAS_E_HIP. */
+raas_status raas_prefill_ragged(raas_pool* pool, int32_t layer, const void* k, const void* v,
+                                const int32_t* prefill_lens, const int32_t* seq_mask, int32_t max_len,
+                                void* stream);
+
 /* One decode step of one layer for every unit (steps 1-5 above). q
  * [batch][n_q_heads][head_dim]; k_new, v_new [batch][n_kv_heads][head_dim];
  * out [batch][n_q_heads][head_dim] receives the attention output, rounded
@@ -141,6 +160,17 @@ raas_status raas_prefill(raas_pool* pool, int32_t layer, const void* k, const vo
 raas_status raas_decode_step(raas_pool* pool, int32_t layer, const void* q, const void* k_new,
                              const void* v_new, void* out, int32_t* page_table_out,
                              int32_t* timestamps_out, int32_t* evicted_out, void* stream);
+
+/* raas_decode_step for the sequences whose entry of `active` (DEVICE int32
+ * [batch], read when the step runs) is nonzero: the others take no token
+ * this step; their state, clock, outputs (out, page_table_out,
+ * timestamps_out, evicted_out rows) are left untouched. active = NULL is
+ * raas_decode_step. Sequences thereby advance at their own pace (ragged
+ * batches). Errors as raas_decode_step. */
+raas_status raas_decode_step_masked(raas_pool* pool, int32_t layer, const void* q, const void* k_new,
+                                    const void* v_new, void* out, int32_t* page_table_out,
+                                    int32_t* timestamps_out, int32_t* evicted_out, const int32_t* active,
+                                    void* stream);
 
 /* Synchronises the pool's last stream, frees all device memory and the
  * pool. NULL is ignored. */

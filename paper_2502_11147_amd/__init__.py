@@ -25,7 +25,7 @@ KERNELS = ("append", "attention", "merge", "score")
 EXPORTS = (
     "raas_create_pool", "raas_prefill", "raas_decode_step", "raas_destroy", "raas_last_error",
     "raas_abi_version", "raas_pool_bytes", "raas_export_state", "raas_set_attention_splits",
-    "raas_profile", "raas_profile_read",
+    "raas_profile", "raas_profile_read", "raas_prefill_ragged", "raas_decode_step_masked",
 )
 
 
@@ -71,6 +71,10 @@ def load_library(path: str = LIB_PATH) -> ctypes.CDLL:
     lib.raas_prefill.restype = i32
     lib.raas_decode_step.argtypes = [vp, i32, vp, vp, vp, vp, vp, vp, vp, vp]
     lib.raas_decode_step.restype = i32
+    lib.raas_prefill_ragged.argtypes = [vp, i32, vp, vp, ip, ip, i32, vp]
+    lib.raas_prefill_ragged.restype = i32
+    lib.raas_decode_step_masked.argtypes = [vp, i32, vp, vp, vp, vp, vp, vp, vp, vp, vp]
+    lib.raas_decode_step_masked.restype = i32
     lib.raas_destroy.argtypes = [vp]
     lib.raas_destroy.restype = None
     lib.raas_last_error.argtypes = []
@@ -181,10 +185,33 @@ class Pool:
         vp = self._tensor(v, shape, "v") if P > 0 else None
         _check(self.lib.raas_prefill(self._h, layer, kp, vp, P, _stream_handle(stream)), "raas_prefill")
 
+    def prefill_ragged(self, layer: int, k, v, lens, mask=None, stream=None):
+        """Per-sequence prompt lengths (raas_prefill_ragged). k, v: [batch]
+        [n_kv_heads][max_len][head_dim] device tensors; lens, mask: host
+        sequences of batch ints (mask: the sequences to (re)initialise)."""
+        B = self.batch
+        lens = [int(x) for x in lens]
+        if len(lens) != B:
+            raise ValueError("lens must have %d entries" % B)
+        max_len = 0 if k is None else int(k.shape[2])
+        shape = (B, self.n_kv_heads, max_len, self.head_dim)
+        kp = self._tensor(k, shape, "k") if max_len > 0 else None
+        vp = self._tensor(v, shape, "v") if max_len > 0 else None
+        lens_c = (ctypes.c_int32 * B)(*lens)
+        mask_c = None
+        if mask is not None:
+            mask = [int(bool(x)) for x in mask]
+            if len(mask) != B:
+                raise ValueError("mask must have %d entries" % B)
+            mask_c = (ctypes.c_int32 * B)(*mask)
+        _check(self.lib.raas_prefill_ragged(self._h, layer, kp, vp, lens_c, mask_c, max_len,
+                                            _stream_handle(stream)), "raas_prefill_ragged")
+
     def prepare_step(self, layer: int, q, k_new, v_new, out, page_table=None, timestamps=None,
-                     evicted=None, stream=None) -> tuple:
-        """Checks and converts the arguments of one raas_decode_step call once,
-        so a loop can replay them with decode_prepared()."""
+                     evicted=None, stream=None, active=None) -> tuple:
+        """Checks and converts the arguments of one raas_decode_step_masked call
+        once, so a loop can replay them with decode_prepared(). active: None, or
+        a device int32 tensor [batch] (nonzero = the sequence takes the step)."""
         B, Hq, Hkv, d = self.batch, self.n_q_heads, self.n_kv_heads, self.head_dim
         return (
             self._h, layer,
@@ -195,11 +222,12 @@ class Pool:
             self._i32(page_table, (B, Hkv, self.slots), "page_table"),
             self._i32(timestamps, (B, Hkv, self.slots), "timestamps"),
             self._i32(evicted, (B, Hkv), "evicted"),
+            self._i32(active, (B,), "active"),
             _stream_handle(stream),
         )
 
     def decode_prepared(self, args: tuple):
-        _check(self.lib.raas_decode_step(*args), "raas_decode_step")
+        _check(self.lib.raas_decode_step_masked(*args), "raas_decode_step_masked")
 
     def decode_step(self, layer: int, q, k_new, v_new, out, page_table=None, timestamps=None,
                     evicted=None, stream=None):

@@ -48,6 +48,16 @@ struct LayerView {
     int agg;          // head aggregation of the page score: 0 max, 1 sum of per-head softmax
     int rank_pinned;  // 1: pinned pages are scored and ranked (never refreshed)
     int hgrp;         // units per retention decision: 1, or n_kv_heads (units seq*hgrp .. +hgrp-1)
+    int nkv;          // KV heads per sequence: unit u belongs to sequence u / nkv
+};
+
+// Prefill input of one layer: `stride` token rows per unit; per-sequence
+// lengths (lens, device [batch]) or one length P; an optional device mask
+// [batch] of the sequences to (re)initialise.
+struct PrefillIn {
+    const int32_t* lens;
+    const int32_t* mask;
+    int P, stride;
 };
 
 struct StepIO {
@@ -58,6 +68,7 @@ struct StepIO {
     int32_t* page_table_out;
     int32_t* timestamps_out;
     int32_t* evicted_out;
+    const int32_t* active;  // device [batch]: nonzero = the sequence takes this step; NULL = all
 };
 
 // Launch plan of one decode step.
@@ -75,7 +86,8 @@ StepPlan plan_step(int U, int G, int D, int S, int Lcap, int ps, int pinned, boo
 hipError_t allow_large_lds();
 
 // Launchers (asynchronous on `stream`; return the launch status).
-hipError_t launch_prefill(const LayerView& L, const void* k, const void* v, int P, int keep_pages,
+// max_tok: the most tokens any selected unit keeps (min(P, kept pages * ps)).
+hipError_t launch_prefill(const LayerView& L, const void* k, const void* v, const PrefillIn& in, int max_tok,
                           hipStream_t stream);
 // The step kernel: attention, page scores, append; plus the epilogue when fused.
 hipError_t launch_step(const LayerView& L, const StepIO& io, const StepPlan& plan, double r,

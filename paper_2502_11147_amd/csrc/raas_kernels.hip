@@ -87,11 +87,30 @@ __device__ __forceinline__ uint16_t u16_at(const u32x4& x, int e) {
 }
 
 // ---------------------------------------------------------------------------
-// Prefill: store the first keep_tok tokens of every unit and mark pages
-// 0..keep_pages-1 pinned (kvm.store_cache(.., "prefill"), Algorithm 1).
+// Prefill (kvm.store_cache(.., "prefill"), Algorithm 1): a unit's first
+// tokens go to pages 0, 1, ..., which are marked pinned; at most S-1 pages
+// are kept (the first ones), so one slot stays for decode pages. Lengths are
+// per sequence (in.lens) or uniform (in.P); in.mask, when given, selects the
+// sequences to (re)initialise and leaves the others as they are. The input
+// holds in.stride rows per unit.
 
-__global__ void k_prefill_meta(LayerView L, int P, int keep_pages) {
+// Prefill length of unit u, or -1 when its sequence is not selected.
+__device__ __forceinline__ int unit_prefill_len(const LayerView& L, const PrefillIn& in, int u) {
+    const int seq = u / L.nkv;
+    if (in.mask != nullptr && in.mask[seq] == 0) return -1;
+    return in.lens != nullptr ? in.lens[seq] : in.P;
+}
+
+// pages kept of a prefill of P tokens (the first min(ceil(P/ps), S-1))
+__device__ __forceinline__ int kept_pages(const LayerView& L, int P) {
+    return min((P + L.ps - 1) / L.ps, L.S - 1);
+}
+
+__global__ void k_prefill_meta(LayerView L, PrefillIn in) {
     const int u = blockIdx.x;
+    const int P = unit_prefill_len(L, in, u);
+    if (P < 0) return;
+    const int keep_pages = kept_pages(L, P);
     const size_t base = (size_t)u * L.S;
     for (int s = threadIdx.x; s < L.S; s += blockDim.x) {
         const bool pin = s < keep_pages;
@@ -112,47 +131,57 @@ __global__ void k_prefill_meta(LayerView L, int P, int keep_pages) {
     }
 }
 
+// K rows (D/8 threads per token) then V octets (D threads per 8 tokens),
+// over max_tok tokens per unit; tokens past a unit's kept ones are skipped
+// (K) or zero (the rest of V's last octet).
 template <int D>
-__global__ void k_prefill_bf16(LayerView L, const uint16_t* __restrict__ k,
-                               const uint16_t* __restrict__ v, int P, int keep_tok) {
+__global__ void k_prefill_bf16(LayerView L, const uint16_t* __restrict__ k, const uint16_t* __restrict__ v,
+                               PrefillIn in, int max_tok) {
     const size_t tid = (size_t)blockIdx.x * blockDim.x + threadIdx.x;
-    const size_t nK = (size_t)L.U * keep_tok * (D / 8);
-    const int octets = (keep_tok + 7) / 8;
+    const size_t nK = (size_t)L.U * max_tok * (D / 8);
+    const int octets = (max_tok + 7) / 8;
     const size_t nV = (size_t)L.U * octets * D;
     uint16_t* K = (uint16_t*)L.K;
     uint16_t* V = (uint16_t*)L.V;
     if (tid < nK) {
-        const int u = (int)(tid / ((size_t)keep_tok * (D / 8)));
-        const int rem = (int)(tid - (size_t)u * keep_tok * (D / 8));
+        const int u = (int)(tid / ((size_t)max_tok * (D / 8)));
+        const int rem = (int)(tid - (size_t)u * max_tok * (D / 8));
         const int t = rem / (D / 8), ch = rem % (D / 8);
-        st4(K + (size_t)u * L.Lcap * D + k_off<D>(t, ch * 8), ld4(k + ((size_t)u * P + t) * D + ch * 8));
+        const int P = unit_prefill_len(L, in, u);
+        if (t >= min(P, kept_pages(L, P) * L.ps)) return;  // also P < 0: not selected
+        st4(K + (size_t)u * L.Lcap * D + k_off<D>(t, ch * 8), ld4(k + ((size_t)u * in.stride + t) * D + ch * 8));
     } else if (tid - nK < nV) {
         const size_t r = tid - nK;
         const int u = (int)(r / ((size_t)octets * D));
         const int rem = (int)(r - (size_t)u * octets * D);
         const int g = rem / D, c = rem % D;
+        const int P = unit_prefill_len(L, in, u);
+        const int keep_tok = min(P, kept_pages(L, P) * L.ps);
+        if (8 * g >= keep_tok) return;
         uint32_t w[4];
 #pragma unroll
         for (int j = 0; j < 8; j += 2) {
             const int t0 = 8 * g + j, t1 = t0 + 1;
-            const uint32_t lo = (t0 < keep_tok) ? v[((size_t)u * P + t0) * D + c] : 0u;
-            const uint32_t hi = (t1 < keep_tok) ? v[((size_t)u * P + t1) * D + c] : 0u;
+            const uint32_t lo = (t0 < keep_tok) ? v[((size_t)u * in.stride + t0) * D + c] : 0u;
+            const uint32_t hi = (t1 < keep_tok) ? v[((size_t)u * in.stride + t1) * D + c] : 0u;
             w[j / 2] = lo | (hi << 16);
         }
         st4(V + (size_t)u * L.Lcap * D + v_off<D>(8 * g, c), u32x4{w[0], w[1], w[2], w[3]});
     }
 }
 
-__global__ void k_prefill_f32(LayerView L, const float* __restrict__ k, const float* __restrict__ v,
-                              int P, int keep_tok) {
+__global__ void k_prefill_f32(LayerView L, const float* __restrict__ k, const float* __restrict__ v, PrefillIn in,
+                              int max_tok) {
     const size_t tid = (size_t)blockIdx.x * blockDim.x + threadIdx.x;
     const int D = L.D;
-    const size_t n = (size_t)L.U * keep_tok * (D / 4);
+    const size_t n = (size_t)L.U * max_tok * (D / 4);
     if (tid >= n) return;
-    const int u = (int)(tid / ((size_t)keep_tok * (D / 4)));
-    const int rem = (int)(tid - (size_t)u * keep_tok * (D / 4));
+    const int u = (int)(tid / ((size_t)max_tok * (D / 4)));
+    const int rem = (int)(tid - (size_t)u * max_tok * (D / 4));
     const int t = rem / (D / 4), ch = rem % (D / 4);
-    const size_t src = ((size_t)u * P + t) * D + ch * 4;
+    const int P = unit_prefill_len(L, in, u);
+    if (t >= min(P, kept_pages(L, P) * L.ps)) return;
+    const size_t src = ((size_t)u * in.stride + t) * D + ch * 4;
     const size_t dst = ((size_t)u * L.Lcap + t) * D + ch * 4;
     st4((float*)L.K + dst, ld4(k + src));
     st4((float*)L.V + dst, ld4(v + src));
@@ -160,18 +189,20 @@ __global__ void k_prefill_f32(LayerView L, const float* __restrict__ k, const fl
 
 // Representative keys of the pinned pages, needed only when they are ranked:
 // per-channel min and max over each page's prefill tokens (Section 3.3). One
-// thread per (unit, page, channel); a wavefront reads 64 consecutive channels
-// of one token at a time.
+// thread per (unit, page, channel) over max_pages pages per unit; a
+// wavefront reads 64 consecutive channels of one token at a time.
 template <typename T>
-__global__ void k_prefill_rep(LayerView L, const T* __restrict__ k, int P, int keep_pages) {
+__global__ void k_prefill_rep(LayerView L, const T* __restrict__ k, PrefillIn in, int max_pages) {
     const size_t tid = (size_t)blockIdx.x * blockDim.x + threadIdx.x;
     const int D = L.D, ps = L.ps;
-    if (tid >= (size_t)L.U * keep_pages * D) return;
+    if (tid >= (size_t)L.U * max_pages * D) return;
     const int c = (int)(tid % D);
     const size_t up = tid / D;
-    const int pg = (int)(up % keep_pages), u = (int)(up / keep_pages);
-    const int t0 = pg * ps, t1 = min(P, t0 + ps);  // t0 < P: the page holds a prefill token
-    const T* ku = k + (size_t)u * P * D + c;
+    const int pg = (int)(up % max_pages), u = (int)(up / max_pages);
+    const int P = unit_prefill_len(L, in, u);
+    if (pg >= kept_pages(L, P)) return;            // also P < 0; else pg * ps < P
+    const int t0 = pg * ps, t1 = min(P, t0 + ps);
+    const T* ku = k + (size_t)u * in.stride * D + c;
     T hi = ku[(size_t)t0 * D], lo = hi;
     for (int t = t0 + 1; t < t1; ++t) {
         const T x = ku[(size_t)t * D];
@@ -636,6 +667,7 @@ __global__ __launch_bounds__(NW * 64) __attribute__((amdgpu_waves_per_eu(1, 2)))
     const int grp = lane >> 4, col = lane & 15;
     const int nsplit = L.nsplit;
     const int u = blockIdx.x / nsplit, split = blockIdx.x - (blockIdx.x / nsplit) * nsplit;
+    if (io.active != nullptr && io.active[u / L.nkv] == 0) return;  // the sequence sits this step out
     const size_t base = (size_t)u * S;
     const int nblk = L.Lcap / 32;
     const int b0 = split * L.bps;
@@ -893,6 +925,7 @@ __global__ __launch_bounds__(64) void k_step_f32(LayerView L, StepIO io, float s
     const int lane = threadIdx.x;
     const int nsplit = L.nsplit;
     const int u = blockIdx.x / nsplit, split = blockIdx.x - (blockIdx.x / nsplit) * nsplit;
+    if (io.active != nullptr && io.active[u / L.nkv] == 0) return;
     const int G = L.G, S = L.S, ps = L.ps;
     const size_t base = (size_t)u * S;
     const int32_t* U4 = L.unit + (size_t)u * kUnitFields;
@@ -1024,6 +1057,7 @@ __global__ __launch_bounds__(256) void k_epilogue(LayerView L, StepIO io, double
     int* s_ts = s_state + S;
     int* s_lid = s_ts + S;
     const int u0 = blockIdx.x * nu;
+    if (io.active != nullptr && io.active[u0 / L.nkv] == 0) return;
     const size_t base = (size_t)u0 * S;
     const UnitRec ur = read_unit(L, u0);
     load_slots(L, u0, ur, s_score, s_state, s_ts, s_lid);
@@ -1145,32 +1179,32 @@ hipError_t allow_large_lds() {
     return e;
 }
 
-hipError_t launch_prefill(const LayerView& L, const void* k, const void* v, int P, int keep_pages,
+hipError_t launch_prefill(const LayerView& L, const void* k, const void* v, const PrefillIn& in, int max_tok,
                           hipStream_t stream) {
-    hipLaunchKernelGGL(k_prefill_meta, dim3(L.U), dim3(256), 0, stream, L, P, keep_pages);
-    const int keep_tok = min(P, keep_pages * L.ps);
-    if (keep_tok > 0) {
+    hipLaunchKernelGGL(k_prefill_meta, dim3(L.U), dim3(256), 0, stream, L, in);
+    if (max_tok > 0) {
         if (L.bf16) {
-            const size_t n = (size_t)L.U * keep_tok * (L.D / 8) + (size_t)L.U * ((keep_tok + 7) / 8) * L.D;
+            const size_t n = (size_t)L.U * max_tok * (L.D / 8) + (size_t)L.U * ((max_tok + 7) / 8) * L.D;
             if (L.D == 128)
                 hipLaunchKernelGGL(k_prefill_bf16<128>, dim3(grid1d(n, 256)), dim3(256), 0, stream, L,
-                                   (const uint16_t*)k, (const uint16_t*)v, P, keep_tok);
+                                   (const uint16_t*)k, (const uint16_t*)v, in, max_tok);
             else
                 hipLaunchKernelGGL(k_prefill_bf16<64>, dim3(grid1d(n, 256)), dim3(256), 0, stream, L,
-                                   (const uint16_t*)k, (const uint16_t*)v, P, keep_tok);
+                                   (const uint16_t*)k, (const uint16_t*)v, in, max_tok);
         } else {
-            const size_t n = (size_t)L.U * keep_tok * (L.D / 4);
-            hipLaunchKernelGGL(k_prefill_f32, dim3(grid1d(n, 256)), dim3(256), 0, stream, L,
-                               (const float*)k, (const float*)v, P, keep_tok);
+            const size_t n = (size_t)L.U * max_tok * (L.D / 4);
+            hipLaunchKernelGGL(k_prefill_f32, dim3(grid1d(n, 256)), dim3(256), 0, stream, L, (const float*)k,
+                               (const float*)v, in, max_tok);
         }
         if (L.rank_pinned) {
-            const size_t n = (size_t)L.U * keep_pages * L.D;
+            const int max_pages = (max_tok + L.ps - 1) / L.ps;
+            const size_t n = (size_t)L.U * max_pages * L.D;
             if (L.bf16)
                 hipLaunchKernelGGL(k_prefill_rep<uint16_t>, dim3(grid1d(n, 256)), dim3(256), 0, stream, L,
-                                   (const uint16_t*)k, P, keep_pages);
+                                   (const uint16_t*)k, in, max_pages);
             else
                 hipLaunchKernelGGL(k_prefill_rep<float>, dim3(grid1d(n, 256)), dim3(256), 0, stream, L,
-                                   (const float*)k, P, keep_pages);
+                                   (const float*)k, in, max_pages);
         }
     }
     return hipGetLastError();

@@ -6,6 +6,7 @@
 #include <stdio.h>
 #include <string.h>
 
+#include <algorithm>
 #include <new>
 #include <string>
 #include <vector>
@@ -59,6 +60,9 @@ struct raas_pool {
     int32_t* err = nullptr;
     float* part = nullptr;    // [U][splits][G][D+2], scratch of one step
     double* score = nullptr;  // [U][S] page scores, or [U][S][G] per-head bounds, scratch of one step
+    int32_t* seqbuf = nullptr;   // [2][batch] prefill lengths and mask of a ragged prefill
+    int32_t* seqhost = nullptr;  // pinned host staging of seqbuf
+    hipEvent_t seq_copied = nullptr;  // recorded after the last staging copy
     size_t bytes = 0;
     std::vector<unsigned char> prefilled;
     std::vector<int> pinned;  // pinned prefill pages of each layer
@@ -102,6 +106,7 @@ LayerView view(const raas_pool* p, int layer) {
     L.agg = p->cfg.score_aggregation;
     L.rank_pinned = p->cfg.rank_pinned;
     L.hgrp = p->cfg.decision_scope == RAAS_SCOPE_SEQUENCE ? p->cfg.n_kv_heads : 1;
+    L.nkv = p->cfg.n_kv_heads;
     return L;
 }
 
@@ -229,6 +234,7 @@ raas_status raas_create_pool(const raas_config* cfg, void* stream, raas_pool** o
         {(void**)&p->part, (size_t)p->U * max_split * p->G * (p->D + 2) * sizeof(float)},
         {(void**)&p->score,
          (size_t)p->U * p->S * (cfg->score_aggregation == RAAS_SCORE_SOFTMAX_SUM ? p->G : 1) * sizeof(double)},
+        {(void**)&p->seqbuf, 2 * (size_t)cfg->batch * sizeof(int32_t)},
     };
     hipStream_t s = (hipStream_t)stream;
     hipError_t ea = allow_large_lds();
@@ -251,6 +257,12 @@ raas_status raas_create_pool(const raas_config* cfg, void* stream, raas_pool** o
             return hip_fail(e, "hipMemsetAsync");
         }
     }
+    hipError_t eh = hipHostMalloc((void**)&p->seqhost, 2 * (size_t)cfg->batch * sizeof(int32_t));
+    if (eh != hipSuccess) {
+        p->seqhost = nullptr;
+        raas_destroy(p);
+        return fail(RAAS_E_OOM, "hipHostMalloc: %s", hipGetErrorString(eh));
+    }
     // every slot starts free: lid = ts = -1, state = free (0), fill = 0
     hipError_t e = hipMemsetAsync(p->meta, 0xFF, 2 * Ly * p->meta_layer_elems * sizeof(int32_t), s);
     if (e != hipSuccess) {
@@ -269,9 +281,11 @@ void raas_destroy(raas_pool* p) {
         for (auto ev : t.start) hipEventDestroy(ev);
         for (auto ev : t.stop) hipEventDestroy(ev);
     }
-    void* ptrs[] = {p->K, p->V, p->kmin, p->kmax, p->meta, p->unit, p->err, p->part, p->score};
+    void* ptrs[] = {p->K, p->V, p->kmin, p->kmax, p->meta, p->unit, p->err, p->part, p->score, p->seqbuf};
     for (void* q : ptrs)
         if (q) hipFree(q);
+    if (p->seqhost) hipHostFree(p->seqhost);
+    if (p->seq_copied) hipEventDestroy(p->seq_copied);
     delete p;
 }
 
@@ -291,7 +305,8 @@ raas_status raas_prefill(raas_pool* p, int32_t layer, const void* k, const void*
         keep = p->S - 1;
     }
     hipStream_t s = (hipStream_t)stream;
-    hipError_t e = launch_prefill(view(p, layer), k, v, prefill_len, keep, s);
+    const PrefillIn in{nullptr, nullptr, prefill_len, prefill_len};
+    hipError_t e = launch_prefill(view(p, layer), k, v, in, std::min(prefill_len, keep * p->ps), s);
     if (e != hipSuccess) return hip_fail(e, "prefill launch");
     p->prefilled[layer] = 1;
     p->pinned[layer] = keep;
@@ -299,15 +314,77 @@ raas_status raas_prefill(raas_pool* p, int32_t layer, const void* k, const void*
     return RAAS_OK;
 }
 
+raas_status raas_prefill_ragged(raas_pool* p, int32_t layer, const void* k, const void* v,
+                                const int32_t* prefill_lens, const int32_t* seq_mask, int32_t max_len,
+                                void* stream) {
+    raas_status st = check_layer(p, layer);
+    if (st != RAAS_OK) return st;
+    if (!prefill_lens) return fail(RAAS_E_INVALID, "prefill_lens is NULL");
+    if (max_len < 0) return fail(RAAS_E_INVALID, "max_len must be >= 0 (got %d)", max_len);
+    const int B = p->cfg.batch;
+    int max_tok = 0, selected = 0;
+    for (int b = 0; b < B; ++b) {
+        if (seq_mask && !seq_mask[b]) continue;
+        ++selected;
+        const int P = prefill_lens[b];
+        if (P < 0 || P > max_len)
+            return fail(RAAS_E_INVALID, "prefill_lens[%d] = %d outside [0, max_len = %d]", b, P, max_len);
+        const int pages = (P + p->ps - 1) / p->ps;
+        if (pages > p->S - 1 && p->cfg.prefill_policy == RAAS_PREFILL_ERROR)
+            return fail(RAAS_E_BUDGET, "sequence %d: prefill needs %d pages but the budget leaves %d (S-1)", b,
+                        pages, p->S - 1);
+        max_tok = std::max(max_tok, std::min(P, std::min(pages, p->S - 1) * p->ps));
+    }
+    if (!p->prefilled[layer] && selected != B)
+        return fail(RAAS_E_STATE, "the first prefill of layer %d must cover every sequence", layer);
+    if (max_tok > 0 && (!k || !v)) return fail(RAAS_E_INVALID, "k or v is NULL");
+    hipStream_t s = (hipStream_t)stream;
+    // lengths and mask go to the device through the pool's pinned staging
+    // buffer, once the previous ragged prefill's copy out of it has run
+    hipError_t e = hipSuccess;
+    if (!p->seq_copied) {
+        e = hipEventCreateWithFlags(&p->seq_copied, hipEventDisableTiming);
+        if (e != hipSuccess) {
+            p->seq_copied = nullptr;
+            return hip_fail(e, "hipEventCreateWithFlags");
+        }
+    } else {
+        e = hipEventSynchronize(p->seq_copied);
+        if (e != hipSuccess) return hip_fail(e, "hipEventSynchronize");
+    }
+    for (int b = 0; b < B; ++b) {
+        p->seqhost[b] = prefill_lens[b];
+        p->seqhost[(size_t)B + b] = (seq_mask && !seq_mask[b]) ? 0 : 1;
+    }
+    e = hipMemcpyAsync(p->seqbuf, p->seqhost, 2 * (size_t)B * sizeof(int32_t), hipMemcpyHostToDevice, s);
+    if (e != hipSuccess) return hip_fail(e, "hipMemcpyAsync");
+    e = hipEventRecord(p->seq_copied, s);
+    if (e != hipSuccess) return hip_fail(e, "hipEventRecord");
+    const PrefillIn in{p->seqbuf, p->seqbuf + B, 0, max_len};
+    e = launch_prefill(view(p, layer), k, v, in, max_tok, s);
+    if (e != hipSuccess) return hip_fail(e, "prefill launch");
+    p->prefilled[layer] = 1;
+    p->last_stream = s;
+    return RAAS_OK;
+}
+
 raas_status raas_decode_step(raas_pool* p, int32_t layer, const void* q, const void* k_new,
                              const void* v_new, void* out, int32_t* page_table_out,
                              int32_t* timestamps_out, int32_t* evicted_out, void* stream) {
+    return raas_decode_step_masked(p, layer, q, k_new, v_new, out, page_table_out, timestamps_out, evicted_out,
+                                   nullptr, stream);
+}
+
+raas_status raas_decode_step_masked(raas_pool* p, int32_t layer, const void* q, const void* k_new,
+                                    const void* v_new, void* out, int32_t* page_table_out,
+                                    int32_t* timestamps_out, int32_t* evicted_out, const int32_t* active,
+                                    void* stream) {
     raas_status st = check_layer(p, layer);
     if (st != RAAS_OK) return st;
     if (!q || !k_new || !v_new || !out) return fail(RAAS_E_INVALID, "q, k_new, v_new and out must be non-NULL");
     if (!p->prefilled[layer]) return fail(RAAS_E_STATE, "layer %d has not been prefilled", layer);
     LayerView L = view(p, layer);
-    StepIO io{q, k_new, v_new, out, page_table_out, timestamps_out, evicted_out};
+    StepIO io{q, k_new, v_new, out, page_table_out, timestamps_out, evicted_out, active};
     hipStream_t s = (hipStream_t)stream;
     const StepPlan pl = plan_step(p->U, p->G, p->D, p->S, p->Lcap, p->ps, p->pinned[layer],
                                   p->cfg.dtype == RAAS_BF16, p->cfg.score_aggregation,

@@ -200,3 +200,101 @@ def _check_invariants(pt, ts, ev, clock, P, ps, S):
     assert np.all((ev == -1) | (ev >= -(-P // ps)))
     nfree = np.sum(pt == -1, axis=1)
     assert np.all(nfree[ev >= 0] >= 1)
+
+
+def run_ragged(w, seed: int, lens, steps: int, active_p: float = 0.75, reprefill=None, splits=None,
+               aggregation: int = 0, rank_pinned: bool = False, scope: int = 0) -> ParityReport:
+    """Ragged batch: per-sequence prompt lengths (raas_prefill_ragged), a
+    seeded per-step mask of the sequences that take a token
+    (raas_decode_step_masked), and prompts replaced mid-run (reprefill: step
+    -> {sequence: new length}, a re-prefill of those sequences alone before
+    that step). Every unit is checked against an oracle that steps only
+    when its sequence is active; inactive sequences' outputs must stay
+    untouched; at the end the whole exported state must agree."""
+    import torch
+
+    rep = ParityReport()
+    B, Hq, Hkv, d, G, S, ps = (w.batch, w.n_q_heads, w.n_kv_heads, w.head_dim, w.group, w.slots,
+                               w.page_size)
+    U = B * Hkv
+    reprefill = reprefill or {}
+    tol = TOL[w.dtype]
+    dt = torch.bfloat16 if w.dtype == "bf16" else torch.float32
+    rng = np.random.default_rng(seed + 17)
+    pool = new_pool(w, splits, aggregation=aggregation, rank_pinned=rank_pinned, scope=scope)
+    orc = {}
+
+    def prompt(lens_now, mask, pseed):
+        max_len = max([int(x) for x, m in zip(lens_now, mask) if m] + [0])
+        Kp, Vp = synth.prefill(w, pseed, 0, prefill_len=max_len)
+        pool.prefill_ragged(0, to_device(Kp, w.dtype) if max_len else None,
+                            to_device(Vp, w.dtype) if max_len else None, lens_now, mask)
+        for b in range(B):
+            if not mask[b]:
+                continue
+            for h in range(Hkv):
+                m = oracle.Kvm(G, d, ps, S, r=w.r, aggregation=aggregation, rank_pinned=rank_pinned)
+                P = int(lens_now[b])
+                assert m.prefill(Kp[b, h, :P].astype(np.float64), Vp[b, h, :P].astype(np.float64)) == 0
+                orc[b * Hkv + h] = m
+
+    lens_now = [int(x) for x in lens]
+    prompt(lens_now, [1] * B, seed)
+    groups = {b: [b * Hkv + h for h in range(Hkv)] for b in range(B)} if scope == 1 else {u: [u] for u in range(U)}
+    rep.units_checked = U
+    for t in range(steps):
+        if t in reprefill:
+            mask = [1 if b in reprefill[t] else 0 for b in range(B)]
+            for b, P in reprefill[t].items():
+                lens_now[b] = int(P)
+            prompt(lens_now, mask, seed + 1000 + t)
+        act = (rng.random(B) < active_p).astype(np.int32)
+        q, k, v = synth.steps(w, seed, 0, t, 1)
+        out = torch.full((B, Hq, d), 7.0, dtype=dt, device="cuda")
+        pt = torch.full((B, Hkv, S), -7, dtype=torch.int32, device="cuda")
+        ts = torch.full((B, Hkv, S), -7, dtype=torch.int32, device="cuda")
+        ev = torch.full((B, Hkv), -7, dtype=torch.int32, device="cuda")
+        pool.decode_prepared(pool.prepare_step(0, to_device(q[0], w.dtype), to_device(k[0], w.dtype),
+                                               to_device(v[0], w.dtype), out, pt, ts, ev,
+                                               active=torch.from_numpy(act).cuda()))
+        torch.cuda.synchronize()
+        out_h = out.float().cpu().numpy().reshape(U, G, d)
+        pt_h, ts_h, ev_h = (x.cpu().numpy().reshape(U, -1) for x in (pt, ts, ev))
+        q64, k64, v64 = q[0].reshape(U, G, d), k[0].reshape(U, d), v[0].reshape(U, d)
+        for g, members in groups.items():
+            b = members[0] // Hkv
+            if not act[b]:
+                for u in members:
+                    assert np.all(out_h[u] == 7.0) and np.all(pt_h[u] == -7) and np.all(ts_h[u] == -7) \
+                        and np.all(ev_h[u] == -7), "inactive sequence %d touched at step %d" % (b, t)
+                continue
+            if len(members) == 1:
+                outs = {members[0]: orc[members[0]].decode(q64[members[0]], k64[members[0]], v64[members[0]])}
+            else:
+                o = oracle.decode_group([orc[u] for u in members], q64[members], k64[members], v64[members])
+                outs = {u: o[j] for j, u in enumerate(members)}
+            scores, theta = orc[members[0]].last_scores()
+            if len(_flagged_pages(scores, theta)) >= 2:
+                rep.flagged_steps += 1
+            for u in members:
+                st = orc[u].state()
+                if not (np.array_equal(st["page_table"], pt_h[u]) and np.array_equal(st["ts"], ts_h[u])
+                        and st["evicted"] == ev_h[u, 0]):
+                    raise AssertionError("ragged retention mismatch: unit %d step %d\noracle pt %s\n   gpu pt %s\n"
+                                         "oracle ts %s\n   gpu ts %s" % (u, t, st["page_table"].tolist(),
+                                                                         pt_h[u].tolist(), st["ts"].tolist(),
+                                                                         ts_h[u].tolist()))
+                rep.evictions += int(st["evicted"] >= 0)
+                err = float(np.max(np.abs(out_h[u].astype(np.float64) - outs[u])))
+                rep.max_abs_err = max(rep.max_abs_err, err)
+                rep.outputs_compared += 1
+                if not (err <= tol):
+                    raise AssertionError("ragged output mismatch: unit %d step %d: %.3g" % (u, t, err))
+        rep.steps = t + 1
+    gs = pool.export_state(0)
+    for u in range(U):
+        st = orc[u].state()
+        assert np.array_equal(np.where(gs["state"][u] == 0, -1, gs["lid"][u]), st["page_table"]), u
+        assert gs["clock"][u] == st["clock"] and gs["tail"][u] == st["tail"], u
+    pool.close()
+    return rep

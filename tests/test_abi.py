@@ -102,6 +102,10 @@ def test_null_arguments(lib):
     assert "cfg" in lib.raas_last_error().decode()
     assert lib.raas_prefill(None, 0, None, None, 0, None) == raas.E_INVALID
     assert lib.raas_decode_step(None, 0, None, None, None, None, None, None, None, None) == raas.E_INVALID
+    assert lib.raas_decode_step_masked(None, 0, None, None, None, None, None, None, None, None,
+                                       None) == raas.E_INVALID
+    lens = (ctypes.c_int32 * 2)(1, 1)
+    assert lib.raas_prefill_ragged(None, 0, None, None, lens, None, 1, None) == raas.E_INVALID
     buf = (ctypes.c_int32 * 8)()
     assert lib.raas_export_state(None, 0, buf, 8, None) == raas.E_INVALID
     assert lib.raas_set_attention_splits(None, 1) == raas.E_INVALID

@@ -12,7 +12,7 @@ import numpy as np
 import pytest
 
 import synth
-from harness import ParityReport, new_pool, run_parity, to_device
+from harness import ParityReport, new_pool, run_parity, run_ragged, to_device
 
 pytestmark = pytest.mark.gpu
 
@@ -360,3 +360,29 @@ def test_sequence_scope_full_size():
                      chunk=128, scope=1)
     _report(rep, w.name + " sequence-scope")
     assert rep.evictions > 0 and rep.units_checked == 16
+
+
+RAGGED = [
+    dict(),
+    dict(dtype="f32"),
+    dict(splits=3, budget=512),
+    dict(scope=1),
+    dict(scope=1, aggregation=1, rank_pinned=True),
+    dict(rank_pinned=True),
+]
+
+
+@pytest.mark.parametrize("case", RAGGED, ids=[",".join("%s=%s" % kv for kv in c.items()) or "base" for c in RAGGED])
+def test_ragged_batch(case):
+    """Per-sequence prompt lengths (0, ragged, overflowing the budget), a
+    random mask of the sequences taking each step, and two prompts replaced
+    mid-run (a finished request's place reused)."""
+    case = dict(case)
+    wkw = {k: case.pop(k) for k in ("dtype", "budget") if k in case}
+    w = small(batch=4, decode_steps=260, **wkw)
+    lens = [0, 5, 40, 1000]
+    _say("case ragged %s %s lens %s" % (wkw, case, lens))
+    rep = run_ragged(w, seed=21, lens=lens, steps=w.decode_steps, reprefill={90: {1: 77}, 170: {3: 0, 0: 33}},
+                     **case)
+    _report(rep, "ragged")
+    assert rep.evictions > 0
