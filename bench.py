@@ -51,6 +51,10 @@ def parse():
                     help="one page table per KV head (default) or per sequence")
     ap.add_argument("--cpu-seconds", type=float, default=15.0, help="budget of the CPU oracle sample")
     ap.add_argument("--no-cpu-baseline", action="store_true")
+    ap.add_argument("--decode-sweep", action="store_true",
+                    help="per-step latency and resident tokens against decode length (prompt 128, batch 4, "
+                         "decode 8192) for RaaS at L = 1024 and 2048 and for a pool holding every token")
+    ap.add_argument("--sweep-window", type=int, default=256, help="decode steps per measured window")
     ap.add_argument("--copy-calibration", action="store_true",
                     help="run only a plain streaming kernel of known size (counter calibration)")
     ap.add_argument("--traffic-summary", metavar="DIR", default=None,
@@ -250,6 +254,50 @@ def cpu_baseline(w, seed, ring_np, budget_s, aggregation=0, rank_pinned=False):
     }
 
 
+def decode_sweep(args):
+    """Decode-length sweep (the setting of the paper's Fig. 6: prompt 128,
+    batch 4, decode up to 8192 tokens) on one Mistral-7B-shaped layer: per
+    window of decode steps, the mean step time (HIP events on the launch
+    stream) and the mean resident tokens per unit; the pool's device bytes,
+    fixed at creation. One JSON line per configuration."""
+    import torch
+
+    import paper_2502_11147_amd as raas
+    import synth
+
+    assert torch.cuda.is_available(), "needs a GPU"
+    dev = torch.device("cuda", 0)
+    W = max(1, args.sweep_window)
+    for name in ("mistral7b-b4-P128-L1024", "mistral7b-b4-P128-L2048", "mistral7b-b4-P128-dense"):
+        w = synth.get_workload(name)
+        pool = raas.Pool.for_workload(w)
+        K, V = synth.prefill(w, args.seed, 0)
+        pool.prefill(0, torch.from_numpy(K).to(torch.bfloat16).to(dev), torch.from_numpy(V).to(torch.bfloat16).to(dev))
+        out = torch.empty((w.batch, w.n_q_heads, w.head_dim), dtype=torch.bfloat16, device=dev)
+        ends, us, resident = [], [], []
+        ev0, ev1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+        for t0 in range(0, w.decode_steps, W):
+            n = min(W, w.decode_steps - t0)
+            q, k, v = (torch.from_numpy(a).to(torch.bfloat16).to(dev) for a in synth.steps(w, args.seed, 0, t0, n))
+            prepared = [pool.prepare_step(0, q[i], k[i], v[i], out) for i in range(n)]
+            torch.cuda.synchronize()
+            ev0.record()
+            for a in prepared:
+                pool.decode_prepared(a)
+            ev1.record()
+            torch.cuda.synchronize()
+            st = pool.export_state(0)
+            ends.append(t0 + n)
+            us.append(round(ev0.elapsed_time(ev1) * 1e3 / n, 3))
+            resident.append(float(np.where(st["state"] != 0, st["fill"], 0).sum(axis=1).mean()))
+        line = {"decode_sweep": name, "batch": w.batch, "prefill_len": w.prefill_len, "budget_tokens": w.budget,
+                "pool_bytes": pool.pool_bytes(), "window": W, "decode_len_at_window_end": ends,
+                "us_per_step": us, "resident_tokens_per_unit": resident,
+                "job_ms": round(sum(u * n for u, n in zip(us, np.diff([0] + ends))) / 1e3, 3)}
+        pool.close()
+        print(json.dumps(line), flush=True)
+
+
 def main():
     args = parse()
     if args.traffic_summary:
@@ -262,6 +310,9 @@ def main():
         sys.exit(2)
     if args.copy_calibration:
         copy_calibration()
+        return
+    if args.decode_sweep:
+        decode_sweep(args)
         return
     import torch
 

@@ -49,6 +49,7 @@ struct LayerView {
     int rank_pinned;  // 1: pinned pages are scored and ranked (never refreshed)
     int hgrp;         // units per retention decision: 1, or n_kv_heads (units seq*hgrp .. +hgrp-1)
     int nkv;          // KV heads per sequence: unit u belongs to sequence u / nkv
+    int nblk;         // 32-token blocks a step visits (from row 0): every resident row lies below
 };
 
 // Prefill input of one layer: `stride` token rows per unit; per-sequence

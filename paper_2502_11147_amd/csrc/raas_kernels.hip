@@ -445,15 +445,17 @@ __device__ void softmax_sum_block(const LayerView& L, const double* hb, int nu, 
 //    the smallest (timestamp, logical id) is freed;
 //  - the next token's target: the tail page if it has room, else the lowest
 //    free slot (a fresh page).
+__device__ void evict_wave(const LayerView& L, const UnitRec& ur, int* s_state, int* s_ts, const int* s_lid,
+                           RetShared& out);
+
 __device__ void retention_wave(const LayerView& L, const UnitRec& ur, double r, const double* s_score,
                                int* s_state, int* s_ts, const int* s_lid, RetShared& out) {
-    const int S = L.S, ps = L.ps, lane = threadIdx.x & 63;
-    int n = 0, nfree = 0;
+    const int S = L.S, lane = threadIdx.x & 63;
+    int n = 0;
     for (int s0 = 0; s0 < S; s0 += 64) {
         const int s = s0 + lane;
         const int st = s < S ? s_state[s] : -1;
         n += __popcll(__ballot(st >= 0 && ranked(L, st)));
-        nfree += __popcll(__ballot(st == kFree));
     }
     const int k = (int)floor(r * (double)n);
     if (k > 0) {
@@ -467,6 +469,19 @@ __device__ void retention_wave(const LayerView& L, const UnitRec& ur, double r, 
                 if (less >= n - k) s_ts[p] = ur.clock;
             }
         }
+    }
+    evict_wave(L, ur, s_state, s_ts, s_lid, out);
+}
+
+// Eviction and the next token's target, by one wavefront, once the refresh
+// has set the timestamps.
+__device__ void evict_wave(const LayerView& L, const UnitRec& ur, int* s_state, int* s_ts, const int* s_lid,
+                           RetShared& out) {
+    const int S = L.S, ps = L.ps, lane = threadIdx.x & 63;
+    int nfree = 0;
+    for (int s0 = 0; s0 < S; s0 += 64) {
+        const int s = s0 + lane;
+        nfree += __popcll(__ballot(s < S && s_state[s] == kFree));
     }
     const int fill_tail = ur.nf + 1;
     const bool full = fill_tail == ps && nfree == 0;
@@ -523,6 +538,106 @@ __device__ void retention_wave(const LayerView& L, const UnitRec& ur, double r, 
         s_state[victim] = kFree;
         s_ts[victim] = -1;
     }
+}
+
+// Order-preserving 64-bit key of a finite double (unsigned order = numeric
+// order, with -0 just below +0), and back.
+__device__ __forceinline__ unsigned long long order_key(double x) {
+    const unsigned long long b = (unsigned long long)__double_as_longlong(x);
+    return (b >> 63) ? ~b : (b | (1ull << 63));
+}
+__device__ __forceinline__ double from_order_key(unsigned long long k) {
+    return __longlong_as_double((long long)((k >> 63) ? (k & ~(1ull << 63)) : ~k));
+}
+
+// Top-r refresh by a whole workgroup (every thread calls it; the epilogue
+// kernel's version of the rule in retention_wave). With n ranked pages and
+// k = floor(r*n), an evictable page is refreshed when at least n-k ranked
+// pages score strictly less. Up to 256 slots this is counted directly.
+// Beyond, the workgroup finds theta, the (n-k)-th smallest ranked score, by
+// a radix select over order_key (eight 8-bit digits, most significant
+// first, a 256-bin histogram each) and refreshes the evictable pages
+// scoring above theta: the same pages, since fewer than n-k ranked scores
+// lie below theta and at least n-k lie at or below it. s_aux: 260 ints.
+__device__ void refresh_block(const LayerView& L, const UnitRec& ur, double r, const double* s_score,
+                              const int* s_state, int* s_ts, int* s_aux, int tid, int nthreads) {
+    const int S = L.S, lane = tid & 63;
+    int* s_hist = s_aux;  // [256]
+    if (tid == 0) s_aux[256] = 0;
+    __syncthreads();
+    int cnt = 0;
+    for (int p = tid; p < S; p += nthreads) cnt += ranked(L, s_state[p]) ? 1 : 0;
+#pragma unroll
+    for (int off = 32; off >= 1; off >>= 1) cnt += __shfl_xor(cnt, off);
+    if (lane == 0 && cnt) atomicAdd(&s_aux[256], cnt);
+    __syncthreads();
+    const int n = s_aux[256];
+    const int k = (int)floor(r * (double)n);
+    if (k == 0) return;
+    if (k == n) {  // every page refreshed
+        for (int p = tid; p < S; p += nthreads)
+            if (s_state[p] == kEvictable) s_ts[p] = ur.clock;
+        return;
+    }
+    if (S <= 256) {
+        for (int p = tid; p < S; p += nthreads) {
+            if (s_state[p] != kEvictable) continue;
+            const double sp = s_score[p];
+            int less = 0;
+#pragma unroll 8
+            for (int o = 0; o < S; ++o) less += s_score[o] < sp;  // unranked slots hold +inf
+            if (less >= n - k) s_ts[p] = ur.clock;
+        }
+        return;
+    }
+    unsigned long long prefix = 0;
+    int want = n - k - 1;  // 0-based rank of theta among the ranked scores
+    for (int shift = 56; shift >= 0; shift -= 8) {
+        for (int b = tid; b < 256; b += nthreads) s_hist[b] = 0;
+        __syncthreads();
+        const unsigned long long high = shift == 56 ? 0ull : (~0ull << (shift + 8));
+        for (int p = tid; p < S; p += nthreads) {
+            if (!ranked(L, s_state[p])) continue;
+            const unsigned long long key = order_key(s_score[p]);
+            if ((key & high) == prefix) atomicAdd(&s_hist[(int)((key >> shift) & 255ull)], 1);
+        }
+        __syncthreads();
+        if (tid < 64) {  // wavefront 0 scans the bins: lane l holds bins 4l .. 4l+3
+            const int c0 = s_hist[4 * lane], c1 = s_hist[4 * lane + 1], c2 = s_hist[4 * lane + 2],
+                      c3 = s_hist[4 * lane + 3];
+            const int sum = c0 + c1 + c2 + c3;
+            int incl = sum;
+#pragma unroll
+            for (int off = 1; off < 64; off <<= 1) {
+                const int v = __shfl_up(incl, off);
+                if (lane >= off) incl += v;
+            }
+            const int excl = incl - sum;
+            if (excl <= want && want < incl) {
+                int w = want - excl, b = 4 * lane;
+                if (w >= c0) {
+                    w -= c0;
+                    ++b;
+                    if (w >= c1) {
+                        w -= c1;
+                        ++b;
+                        if (w >= c2) {
+                            w -= c2;
+                            ++b;
+                        }
+                    }
+                }
+                s_aux[257] = b;
+                s_aux[258] = w;
+            }
+        }
+        __syncthreads();
+        prefix |= (unsigned long long)s_aux[257] << shift;
+        want = s_aux[258];
+    }
+    const double theta = from_order_key(prefix);
+    for (int p = tid; p < S; p += nthreads)
+        if (s_state[p] == kEvictable && s_score[p] > theta) s_ts[p] = ur.clock;
 }
 
 // Writes the step's retention results to the pool and the optional outputs.
@@ -669,9 +784,8 @@ __global__ __launch_bounds__(NW * 64) __attribute__((amdgpu_waves_per_eu(1, 2)))
     const int u = blockIdx.x / nsplit, split = blockIdx.x - (blockIdx.x / nsplit) * nsplit;
     if (io.active != nullptr && io.active[u / L.nkv] == 0) return;  // the sequence sits this step out
     const size_t base = (size_t)u * S;
-    const int nblk = L.Lcap / 32;
     const int b0 = split * L.bps;
-    const int b1 = min(nblk, b0 + L.bps);
+    const int b1 = max(b0, min(L.nblk, b0 + L.bps));
     const int nown = b1 - b0;  // blocks of this workgroup
     const uint16_t* qg = (const uint16_t*)io.q + (size_t)u * G * D;
     const uint16_t* kn_g = (const uint16_t*)io.k_new + (size_t)u * D;
@@ -933,7 +1047,7 @@ __global__ __launch_bounds__(64) void k_step_f32(LayerView L, StepIO io, float s
     const bool opened = nf == 0;
     const int row_new = ns * ps + nf;
     const int t0 = split * L.bps * 32;
-    const int t1 = min(S * ps, t0 + L.bps * 32);
+    const int t1 = max(t0, min(min(S * ps, 32 * L.nblk), t0 + L.bps * 32));
     const float* Ku = (const float*)L.K + (size_t)u * L.Lcap * D;
     const float* Vu = (const float*)L.V + (size_t)u * L.Lcap * D;
     const float* qg = (const float*)io.q + (size_t)u * G * D;
@@ -1039,21 +1153,27 @@ __global__ __launch_bounds__(64) void k_step_f32(LayerView L, StepIO io, float s
     }
 }
 
-// Epilogue kernel of the split path: merges the splits' partial attention
-// (out = sum_s 2^(M_s - M) O_s / sum_s 2^(M_s - M) L_s) while wavefront 0
-// runs the retention policy on the scores the splits wrote; then the state
-// goes out. One workgroup per decision: L.hgrp units (the KV heads of a
-// sequence when they share one page table, whose slot states are then
-// identical), a page's score aggregating the bounds of all their heads.
-// merge 0: the step kernel wrote the outputs (bf16, one workgroup per unit).
+// Epilogue kernel of the split path: the retention policy on the scores the
+// step kernel wrote, and the merge of the splits' partial attention
+// (out = sum_s 2^(M_s - M) O_s / sum_s 2^(M_s - M) L_s); then the state goes
+// out. One workgroup per decision: L.hgrp units (the KV heads of a sequence
+// when they share one page table, whose slot states are then identical), a
+// page's score aggregating the bounds of all their heads. The refresh runs
+// on the whole workgroup; wavefront 0 then evicts while the others start
+// the merge. merge 0: the step kernel wrote the outputs (bf16, one
+// workgroup per unit).
 template <typename T>
 __global__ __launch_bounds__(256) void k_epilogue(LayerView L, StepIO io, double r, int merge) {
     extern __shared__ __align__(16) unsigned char smem[];
     __shared__ RetShared ret;
+    __shared__ int s_aux[260];
     const int S = L.S, G = L.G, D = L.D, nsplit = L.nsplit, nu = L.hgrp;
+    const int tid = threadIdx.x, nth = blockDim.x;
     double* s_score = reinterpret_cast<double*>(smem);
     double* s_mz = s_score + S;  // [nu*G][2], softmax aggregation only
-    int* s_state = reinterpret_cast<int*>(s_mz + (L.agg ? 2 * (size_t)nu * G : 0));
+    float* s_ml = reinterpret_cast<float*>(s_mz + (L.agg ? 2 * (size_t)nu * G : 0));  // [nsplit][G][2], merge
+    float* s_den = s_ml + (merge ? 2 * (size_t)nsplit * G : 0);                       // [G], merge
+    int* s_state = reinterpret_cast<int*>(s_den + (merge ? G : 0));
     int* s_ts = s_state + S;
     int* s_lid = s_ts + S;
     const int u0 = blockIdx.x * nu;
@@ -1063,7 +1183,7 @@ __global__ __launch_bounds__(256) void k_epilogue(LayerView L, StepIO io, double
     load_slots(L, u0, ur, s_score, s_state, s_ts, s_lid);
     __syncthreads();
     if (!L.agg)
-        for (int s = threadIdx.x; s < S; s += blockDim.x)
+        for (int s = tid; s < S; s += nth)
             if (ranked(L, s_state[s])) {
                 double best = L.score[base + s];
 #pragma unroll 8
@@ -1071,28 +1191,44 @@ __global__ __launch_bounds__(256) void k_epilogue(LayerView L, StepIO io, double
                 s_score[s] = best;
             }
     __syncthreads();
-    if (L.agg) softmax_sum_block(L, L.score + base * G, nu, s_state, s_score, s_mz, threadIdx.x, blockDim.x);
-    if (threadIdx.x < 64) retention_wave(L, ur, r, s_score, s_state, s_ts, s_lid, ret);
-    for (int idx = threadIdx.x; merge && idx < nu * G * D; idx += blockDim.x) {
-        const int uh = idx / (G * D), rem = idx - uh * (G * D);
+    if (L.agg) softmax_sum_block(L, L.score + base * G, nu, s_state, s_score, s_mz, tid, nth);
+    refresh_block(L, ur, r, s_score, s_state, s_ts, s_aux, tid, nth);
+    __syncthreads();
+    if (tid < 64) evict_wave(L, ur, s_state, s_ts, s_lid, ret);
+    for (int uh = 0; merge && uh < nu; ++uh) {
         const int u = u0 + uh;
-        const int h = rem / D, c = rem - (rem / D) * D;
-        float M = -INFINITY;
-        for (int s = 0; s < nsplit; ++s)
-            M = fmaxf(M, L.part[(((size_t)u * nsplit + s) * G + h) * (D + 2) + D]);
-        float O = 0.0f, Ls = 0.0f;
-        for (int s = 0; s < nsplit; ++s) {
-            const float* pp = L.part + (((size_t)u * nsplit + s) * G + h) * (D + 2);
-            const float ms = pp[D];
-            const float wt = (ms == -INFINITY) ? 0.0f : __builtin_amdgcn_exp2f(ms - M);
-            O += wt * pp[c];
-            Ls += wt * pp[D + 1];
+        const float* pu = L.part + (size_t)u * nsplit * G * (D + 2);
+        // every split's running max and sum, then per head the weights' sum
+        for (int i = tid; i < nsplit * G; i += nth) {
+            s_ml[2 * i] = pu[(size_t)i * (D + 2) + D];
+            s_ml[2 * i + 1] = pu[(size_t)i * (D + 2) + D + 1];
         }
-        ((T*)io.out)[((size_t)u * G + h) * D + c] = from_f<T>(O / Ls);
+        __syncthreads();
+        for (int h = tid; h < G; h += nth) {
+            float M = -INFINITY;
+            for (int s = 0; s < nsplit; ++s) M = fmaxf(M, s_ml[2 * (s * G + h)]);
+            float Ls = 0.0f;
+            for (int s = 0; s < nsplit; ++s) {
+                const float ms = s_ml[2 * (s * G + h)];
+                const float wt = (ms == -INFINITY) ? 0.0f : __builtin_amdgcn_exp2f(ms - M);
+                s_ml[2 * (s * G + h)] = wt;  // the split's weight replaces its max
+                Ls += wt * s_ml[2 * (s * G + h) + 1];
+            }
+            s_den[h] = Ls;
+        }
+        __syncthreads();
+        for (int idx = tid; idx < G * D; idx += nth) {
+            const int h = idx / D, c = idx - (idx / D) * D;
+            float O = 0.0f;
+#pragma unroll 4
+            for (int s = 0; s < nsplit; ++s) O += s_ml[2 * (s * G + h)] * pu[((size_t)s * G + h) * (D + 2) + c];
+            ((T*)io.out)[((size_t)u * G + h) * D + c] = from_f<T>(O / s_den[h]);
+        }
+        __syncthreads();
     }
     __syncthreads();
     for (int uh = 0; uh < nu; ++uh)
-        retention_store(L, io, u0 + uh, ur, s_state, s_ts, s_lid, ret, threadIdx.x, blockDim.x);
+        retention_store(L, io, u0 + uh, ur, s_state, s_ts, s_lid, ret, tid, nth);
 }
 
 inline unsigned grid1d(size_t n, int block) { return (unsigned)((n + block - 1) / block); }
@@ -1235,9 +1371,10 @@ hipError_t launch_step(const LayerView& L, const StepIO& io, const StepPlan& pl,
 }
 
 hipError_t launch_epilogue(const LayerView& L, const StepIO& io, double r, hipStream_t stream) {
-    const size_t shm = (size_t)L.S * (8 + 12) + (L.agg ? (size_t)L.hgrp * L.G * 16 : 0);
-    const dim3 grid((unsigned)(L.U / L.hgrp));
     const int merge = !(L.bf16 && L.nsplit == 1);  // else the step kernel wrote the outputs
+    const size_t shm = (size_t)L.S * (8 + 12) + (L.agg ? (size_t)L.hgrp * L.G * 16 : 0) +
+                       (merge ? ((size_t)2 * L.nsplit * L.G + L.G) * 4 : 0);
+    const dim3 grid((unsigned)(L.U / L.hgrp));
     if (L.bf16)
         hipLaunchKernelGGL(k_epilogue<uint16_t>, grid, dim3(256), shm, stream, L, io, r, merge);
     else

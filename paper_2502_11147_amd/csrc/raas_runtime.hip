@@ -66,6 +66,14 @@ struct raas_pool {
     size_t bytes = 0;
     std::vector<unsigned char> prefilled;
     std::vector<int> pinned;  // pinned prefill pages of each layer
+    // Bound on the slots in use, per layer: pages open at the lowest free
+    // slot, and no slot is freed before every slot has been used, so a
+    // unit that kept k prompt pages and took n decode tokens since uses at
+    // most min(S, k + ceil(n / page_size)) slots. keep_max: the most prompt
+    // pages any unit of the layer has kept; steps: decode steps of the
+    // layer since its first prefill.
+    std::vector<int> keep_max;
+    std::vector<long long> steps;
     std::vector<unsigned char> descending;  // traversal direction of each layer's next step
     int split_override = 0;
     hipStream_t last_stream = nullptr;
@@ -107,6 +115,7 @@ LayerView view(const raas_pool* p, int layer) {
     L.rank_pinned = p->cfg.rank_pinned;
     L.hgrp = p->cfg.decision_scope == RAAS_SCOPE_SEQUENCE ? p->cfg.n_kv_heads : 1;
     L.nkv = p->cfg.n_kv_heads;
+    L.nblk = p->Lcap / kBlockTokens;
     return L;
 }
 
@@ -216,6 +225,8 @@ raas_status raas_create_pool(const raas_config* cfg, void* stream, raas_pool** o
     p->meta_layer_elems = (size_t)p->U * p->S;
     p->prefilled.assign((size_t)cfg->n_layers, 0);
     p->pinned.assign((size_t)cfg->n_layers, 0);
+    p->keep_max.assign((size_t)cfg->n_layers, 0);
+    p->steps.assign((size_t)cfg->n_layers, 0);
     p->descending.assign((size_t)cfg->n_layers, 0);
     const size_t Ly = (size_t)cfg->n_layers;
     const int nblk = p->Lcap / kBlockTokens;
@@ -310,6 +321,8 @@ raas_status raas_prefill(raas_pool* p, int32_t layer, const void* k, const void*
     if (e != hipSuccess) return hip_fail(e, "prefill launch");
     p->prefilled[layer] = 1;
     p->pinned[layer] = keep;
+    p->keep_max[layer] = keep;
+    p->steps[layer] = 0;
     p->last_stream = s;
     return RAAS_OK;
 }
@@ -322,7 +335,7 @@ raas_status raas_prefill_ragged(raas_pool* p, int32_t layer, const void* k, cons
     if (!prefill_lens) return fail(RAAS_E_INVALID, "prefill_lens is NULL");
     if (max_len < 0) return fail(RAAS_E_INVALID, "max_len must be >= 0 (got %d)", max_len);
     const int B = p->cfg.batch;
-    int max_tok = 0, selected = 0;
+    int max_tok = 0, selected = 0, keep_max = 0;
     for (int b = 0; b < B; ++b) {
         if (seq_mask && !seq_mask[b]) continue;
         ++selected;
@@ -334,6 +347,7 @@ raas_status raas_prefill_ragged(raas_pool* p, int32_t layer, const void* k, cons
             return fail(RAAS_E_BUDGET, "sequence %d: prefill needs %d pages but the budget leaves %d (S-1)", b,
                         pages, p->S - 1);
         max_tok = std::max(max_tok, std::min(P, std::min(pages, p->S - 1) * p->ps));
+        keep_max = std::max(keep_max, std::min(pages, p->S - 1));
     }
     if (!p->prefilled[layer] && selected != B)
         return fail(RAAS_E_STATE, "the first prefill of layer %d must cover every sequence", layer);
@@ -363,6 +377,12 @@ raas_status raas_prefill_ragged(raas_pool* p, int32_t layer, const void* k, cons
     const PrefillIn in{p->seqbuf, p->seqbuf + B, 0, max_len};
     e = launch_prefill(view(p, layer), k, v, in, max_tok, s);
     if (e != hipSuccess) return hip_fail(e, "prefill launch");
+    if (!p->prefilled[layer]) {
+        p->keep_max[layer] = keep_max;
+        p->steps[layer] = 0;
+    } else {
+        p->keep_max[layer] = std::max(p->keep_max[layer], keep_max);
+    }
     p->prefilled[layer] = 1;
     p->last_stream = s;
     return RAAS_OK;
@@ -386,7 +406,11 @@ raas_status raas_decode_step_masked(raas_pool* p, int32_t layer, const void* q, 
     LayerView L = view(p, layer);
     StepIO io{q, k_new, v_new, out, page_table_out, timestamps_out, evicted_out, active};
     hipStream_t s = (hipStream_t)stream;
-    const StepPlan pl = plan_step(p->U, p->G, p->D, p->S, p->Lcap, p->ps, p->pinned[layer],
+    // visit only the blocks that can hold resident rows (see keep_max)
+    const long long pages_opened = (p->steps[layer] + 1 + p->ps - 1) / p->ps;
+    const long long used = std::min<long long>(p->S, p->keep_max[layer] + pages_opened);
+    L.nblk = (int)std::min<long long>(p->Lcap / kBlockTokens, (used * p->ps + kBlockTokens - 1) / kBlockTokens);
+    const StepPlan pl = plan_step(p->U, p->G, p->D, p->S, L.nblk * kBlockTokens, p->ps, p->pinned[layer],
                                   p->cfg.dtype == RAAS_BF16, p->cfg.score_aggregation,
                                   p->cfg.decision_scope == RAAS_SCOPE_SEQUENCE, p->split_override);
     L.nsplit = pl.nsplit;
@@ -407,6 +431,7 @@ raas_status raas_decode_step_masked(raas_pool* p, int32_t layer, const void* q, 
         if (e != hipSuccess) return hip_fail(e, "epilogue launch");
     }
     p->descending[layer] ^= 1;
+    p->steps[layer] += 1;
     p->last_stream = s;
     return RAAS_OK;
 }

@@ -80,6 +80,15 @@ for _L in (512, 2048, 8192, 4096 + 32768):
                                 budget=_L, prefill_len=4096, decode_steps=32768, ms_period=128,
                                 ms_phase_random=True, ms_wmin=64, ms_wmax=1024, outlier_p=0.05)
 
+# decode-length sweep (Fig. 6 setting: prompt 128, batch 4, decode up to 8k
+# tokens): one Mistral-7B-shaped layer (32/8 heads, d 128), RaaS at two
+# budgets, and a pool holding every token (dense attention)
+for _L in (1024, 2048, 128 + 8192):
+    _name = "mistral7b-b4-P128-L%d" % _L if _L != 8320 else "mistral7b-b4-P128-dense"
+    WORKLOADS[_name] = Workload(_name, batch=4, n_layers=1, n_q_heads=32, n_kv_heads=8, head_dim=128,
+                                dtype="bf16", page_size=16, budget=_L, prefill_len=128, decode_steps=8192,
+                                ms_period=64, ms_phase_random=True, ms_wmin=64, ms_wmax=1024)
+
 HEADLINE = "llama8b-b32-L2048"
 
 

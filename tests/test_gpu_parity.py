@@ -91,6 +91,8 @@ EDGE = [
     dict(r=0.0), dict(r=1.0), dict(r=0.25), dict(r=0.75),
     dict(dtype="f32", head_dim=128),
     dict(dtype="f32", n_q_heads=14, n_kv_heads=2, head_dim=64, page_size=8, budget=96),
+    dict(page_size=8, budget=2400, prefill_len=2300),             # 300 slots: the epilogue's radix select
+    dict(page_size=8, budget=2400, prefill_len=2300, r=0.25),
 ]
 
 
@@ -292,6 +294,7 @@ VARIANT_CASES = [
     dict(prefill_len=1000),                                         # S-1 pinned pages, one decode slot
     dict(prefill_len=0),                                            # nothing pinned
     dict(head_dim=64, page_size=8, budget=64, prefill_len=21),
+    dict(page_size=8, budget=2400, prefill_len=2300),               # 300 slots, radix select
 ]
 
 
@@ -386,3 +389,18 @@ def test_ragged_batch(case):
                      **case)
     _report(rep, "ragged")
     assert rep.evictions > 0
+
+
+@pytest.mark.parametrize("name,steps,units", [("mistral7b-b4-P128-L1024", 1100, 6), ("mistral7b-b4-P128-dense", 300, 4)])
+def test_decode_sweep_shapes(name, steps, units):
+    """The decode-length sweep's layer (prompt 128, batch 4, split over
+    several workgroups per unit): past the budget at L = 1024; dense
+    attention over every token when the pool holds them all."""
+    w = synth.get_workload(name)
+    _say("case %s steps %d" % (name, steps))
+    rep = run_parity(w, seed=4, steps=steps, units=_sample_units(w, units), out_every=16, chunk=128)
+    _report(rep, name)
+    if "dense" in name:
+        assert rep.evictions == 0
+    else:
+        assert rep.evictions > 0
