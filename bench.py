@@ -216,6 +216,7 @@ def cpu_baseline(w, seed, ring_np, budget_s, aggregation=0, rank_pinned=False):
 
     U = w.batch * w.n_kv_heads
     n_s = min(U, 64)
+    oracle_threads_default = oracle.threads()
     units_idx = np.linspace(0, U - 1, n_s).astype(int)
     K, V = synth.prefill(w, seed, 0)
     ms = []
@@ -243,13 +244,36 @@ def cpu_baseline(w, seed, ring_np, budget_s, aggregation=0, rank_pinned=False):
         if el >= budget_s or timed >= 4096:
             break
     per_unit_step = el / (timed * n_s)
-    tokens_per_s = w.batch / (per_unit_step * U)
+    tokens_per_s = w.batch / (per_unit_step * U * w.n_layers)
     threads = min(oracle.threads(), n_s)
+    # the same steps on one core, a shorter sample
+    oracle.set_threads(1)
+    t1, timed1 = time.perf_counter(), 0
+    while True:
+        i = fill_steps + timed1
+        oracle.decode_batch(ms, qs[i % R], ks[i % R], vs[i % R], want_out=True)
+        timed1 += 1
+        el1 = time.perf_counter() - t1
+        if el1 >= budget_s / 3 or timed1 >= 4096:
+            break
+    oracle.set_threads(oracle_threads_default)
+    tokens_per_s_1 = w.batch / (el1 / (timed1 * n_s) * U * w.n_layers)
+    cpu_model = ""
+    try:
+        with open("/proc/cpuinfo") as f:
+            cpu_model = next((l.split(":", 1)[1].strip() for l in f if l.startswith("model name")), "")
+    except OSError:
+        pass
     return {
         "value": tokens_per_s, "unit": "tokens/s", "cores": int(threads), "kind": "oracle",
         "sample": "%d of %d units, %d steady-state decode steps with attention (%.1f s) after %d "
                   "retention-only fill steps; fp64 C oracle, OpenMP over units; scaled to the full "
-                  "batch as batch / (units * seconds per unit-step)" % (n_s, U, timed, el, fill_steps),
+                  "batch%s as batch / (units * seconds per unit-step%s)"
+                  % (n_s, U, timed, el, fill_steps, " and all layers" if w.n_layers > 1 else "",
+                     " * layers" if w.n_layers > 1 else ""),
+        "value_1core": tokens_per_s_1,
+        "sample_1core": "%d steps of the same units on one thread (%.1f s)" % (timed1, el1),
+        "cpu_model": cpu_model,
         "host_cores_available": len(os.sched_getaffinity(0)),
     }
 
@@ -331,22 +355,30 @@ def main():
     agg = raas.SCORE_SOFTMAX_SUM if args.score_aggregation == "softmax-sum" else raas.SCORE_MAX
     scope = raas.SCOPE_SEQUENCE if args.decision_scope == "sequence" else raas.SCOPE_KV_HEAD
     variant = agg != raas.SCORE_MAX or args.rank_pinned or scope != raas.SCOPE_KV_HEAD
+    t_run = time.perf_counter()
     pool = raas.Pool.for_workload(w, score_aggregation=agg, rank_pinned=args.rank_pinned, decision_scope=scope)
     if args.splits:
         pool.set_attention_splits(args.splits)
+    # a step is one token through every layer of the workload; the layers
+    # share one synthetic prompt and one ring of step inputs
+    nl = w.n_layers
     Kp, Vp = synth.prefill(w, args.seed, 0)
-    pool.prefill(0, torch.from_numpy(Kp).to(dt).to(dev), torch.from_numpy(Vp).to(dt).to(dev))
+    Kd, Vd = torch.from_numpy(Kp).to(dt).to(dev), torch.from_numpy(Vp).to(dt).to(dev)
     del Kp, Vp
+    for layer in range(nl):
+        pool.prefill(layer, Kd, Vd)
+    del Kd, Vd
     R = max(1, args.ring)
     ring_np = synth.steps(w, args.seed, 0, 0, R)
     qd, kd, vd = (torch.from_numpy(a).to(dt).to(dev) for a in ring_np)
     out = torch.empty((w.batch, w.n_q_heads, w.head_dim), dtype=dt, device=dev)
 
-    prepared = [pool.prepare_step(0, qd[j], kd[j], vd[j], out) for j in range(R)]
+    prepared = [[pool.prepare_step(layer, qd[j], kd[j], vd[j], out) for j in range(R)] for layer in range(nl)]
 
     def run(i0, n):
         for i in range(i0, i0 + n):
-            pool.decode_prepared(prepared[i % R])
+            for layer in range(nl):
+                pool.decode_prepared(prepared[layer][i % R])
 
     fill = max(0, w.budget - w.prefill_len) + w.page_size
     run(0, fill)
@@ -392,7 +424,7 @@ def main():
     tokens_per_s = w.batch * args.steps / elapsed
     # step kernel's average duration: the event span over the K launches when
     # it is the only kernel of the step, else the sampled per-kernel events
-    step_avg_s = span_ms / 1e3 / args.steps if fused else step_ms / 1e3 / max(step_n, 1)
+    step_avg_s = span_ms / 1e3 / (args.steps * nl) if fused else step_ms / 1e3 / max(step_n, 1)
     step_b = float(np.mean(step_bytes(w, res, (n_ev0 + n_pin)[None, :])))
     # bytes of the step kernel alone: everything but what the epilogue kernel moves
     e = 2 if w.dtype == "bf16" else 4
@@ -420,7 +452,7 @@ def main():
         "dtype": w.dtype,
         "data": "synthetic (seeded N(0,1) Q/K/V with planted milestone tokens; no datasets or weights)",
         "config": {
-            "workload": w.name, "batch": w.batch, "layers_per_step": 1, "n_q_heads": w.n_q_heads,
+            "workload": w.name, "batch": w.batch, "layers_per_step": nl, "n_q_heads": w.n_q_heads,
             "n_kv_heads": w.n_kv_heads, "head_dim": w.head_dim, "page_size": w.page_size,
             "budget_tokens": w.budget, "prefill_len": w.prefill_len, "r": w.r,
             "resident_tokens_per_unit_avg": float(res.mean()),
@@ -428,7 +460,7 @@ def main():
             "score_aggregation": args.score_aggregation, "rank_pinned": bool(args.rank_pinned),
             "decision_scope": args.decision_scope,
         },
-        "step_hbm_gbs_algorithmic": round(step_b / (elapsed / args.steps) / 1e9, 1),
+        "step_hbm_gbs_algorithmic": round(step_b * nl / (elapsed / args.steps) / 1e9, 1),
         "roofline": {
             "kernel": kname + ("" if fused else " (+k_epilogue)"),
             "bound": "hbm",
@@ -440,7 +472,7 @@ def main():
             "traffic_source": traffic_src,
             "bytes_per_launch": kernel_b,
             "avg_launch_us": round(step_avg_s * 1e6, 3),
-            "launches_timed": args.steps if fused else step_n,
+            "launches_timed": args.steps * nl if fused else step_n,
             "timing": "event span over the timed launches" if fused else "per-launch events, every 16th step",
             "epilogue_kernel_avg_us": round(epi_ms * 1e3 / epi_n, 3) if epi_n else None,
         },
@@ -452,6 +484,7 @@ def main():
         else:
             line["cpu_baseline"] = None
             line["cpu_baseline_note"] = "not sampled for the sequence scope (its oracle step is serial)"
+    line["run_wall_s"] = round(time.perf_counter() - t_run, 2)
     print(json.dumps(line), flush=True)
 
 

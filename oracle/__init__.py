@@ -42,8 +42,8 @@ def build(src: str = SRC, out: str = LIB_PATH, force: bool = False, extra=()) ->
 def load(path: str | None = None) -> ctypes.CDLL:
     path = path or LIB_PATH
     if path not in _libs:
-        if path == LIB_PATH and not os.path.exists(path):
-            build()
+        if path == LIB_PATH:
+            build()  # (re)compiles when missing or older than the source
         lib = ctypes.CDLL(path)
         vp, ip, dp = ctypes.c_void_p, ctypes.POINTER(ctypes.c_int), ctypes.POINTER(ctypes.c_double)
         lib.orc_new.argtypes = [ctypes.c_int] * 4 + [ctypes.c_double, ctypes.c_int]
@@ -67,6 +67,8 @@ def load(path: str | None = None) -> ctypes.CDLL:
         lib.orc_decode_group.restype = ctypes.c_int
         lib.orc_set_variant.argtypes = [vp, ctypes.c_int, ctypes.c_int]
         lib.orc_set_variant.restype = ctypes.c_int
+        lib.orc_set_threads.argtypes = [ctypes.c_int]
+        lib.orc_set_threads.restype = None
         lib.orc_threads.argtypes = []
         lib.orc_threads.restype = ctypes.c_int
         _libs[path] = lib
@@ -210,3 +212,8 @@ def decode_group(units: list[Kvm], q, k, v, want_out: bool = True):
 
 def threads() -> int:
     return int(load().orc_threads())
+
+
+def set_threads(n: int):
+    """OpenMP threads of the batched oracle calls."""
+    load().orc_set_threads(int(n))

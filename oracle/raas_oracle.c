@@ -499,6 +499,15 @@ int orc_decode_batch(orc_kvm** ms, int n, const float* q, const float* k, const 
     return status;
 }
 
+void orc_set_threads(int n) {
+#ifdef _OPENMP
+    extern void omp_set_num_threads(int);
+    if (n >= 1) omp_set_num_threads(n);
+#else
+    (void)n;
+#endif
+}
+
 int orc_threads(void) {
 #ifdef _OPENMP
     extern int omp_get_max_threads(void);
