@@ -65,6 +65,10 @@ def load(path: str | None = None) -> ctypes.CDLL:
         lib.orc_decode_batch.restype = ctypes.c_int
         lib.orc_decode_group.argtypes = [ctypes.POINTER(vp), ctypes.c_int, dp, dp, dp, dp]
         lib.orc_decode_group.restype = ctypes.c_int
+        lib.orc_set_prompt_selection.argtypes = [vp, ctypes.c_int, ctypes.c_int]
+        lib.orc_set_prompt_selection.restype = ctypes.c_int
+        lib.orc_last_attended.argtypes = [vp, ip]
+        lib.orc_last_attended.restype = None
         lib.orc_set_variant.argtypes = [vp, ctypes.c_int, ctypes.c_int]
         lib.orc_set_variant.restype = ctypes.c_int
         lib.orc_set_threads.argtypes = [ctypes.c_int]
@@ -101,7 +105,7 @@ class Kvm:
 
     def __init__(self, G: int, d: int, page_size: int, slots: int, r: float = 0.5,
                  policy: int = PIN_HEAD, lib: str | None = None, aggregation: int = AGG_MAX,
-                 rank_pinned: bool = False):
+                 rank_pinned: bool = False, prompt_slots: int | None = None, prompt_topk: int | None = None):
         self.lib = load(lib)
         self.G, self.d, self.ps, self.S = G, d, page_size, slots
         self._h = self.lib.orc_new(G, d, page_size, slots, float(r), policy)
@@ -110,6 +114,9 @@ class Kvm:
         if aggregation != AGG_MAX or rank_pinned:
             if self.lib.orc_set_variant(self._h, int(aggregation), int(bool(rank_pinned))) != OK:
                 raise ValueError("invalid oracle variant")
+        if prompt_topk is not None:
+            if self.lib.orc_set_prompt_selection(self._h, int(prompt_slots), int(prompt_topk)) != OK:
+                raise ValueError("invalid prompt selection")
 
     def __del__(self):
         h = getattr(self, "_h", None)
@@ -157,6 +164,12 @@ class Kvm:
         return dict(page_table=pt, ts=ts, state=st, fill=fl, tail=int(un[0]), next_lid=int(un[1]),
                     clock=int(un[2]), evicted=int(un[3]), n_evictable=int(un[4]),
                     k_refreshed=int(un[5]))
+
+    def last_attended(self):
+        """slots the last step attended to (with outputs requested), as bools"""
+        a = np.empty(self.S, np.int32)
+        self.lib.orc_last_attended(self._h, a.ctypes.data_as(ctypes.POINTER(ctypes.c_int)))
+        return a.astype(bool)
 
     def last_scores(self):
         sc = np.empty(self.S, np.float64)

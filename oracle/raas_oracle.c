@@ -43,6 +43,15 @@
  * Variant of the decision scope (orc_decode_group): one page table per
  *  (sequence, layer) shared by its KV heads, the page score aggregating all
  *  of the sequence's query heads.
+ * Variant of R3 for long prompts (orc_set_prompt_selection), the combination
+ *  the paper recommends for small budgets or long prompts (Section 4.2 and
+ *  its Limitations): Quest on the prompt pages, RaaS on the decode pages.
+ *  Readings (the paper gives no more than the recommendation): the prompt
+ *  keeps its own region of prompt_slots slots (all its pages are stored, as
+ *  Quest keeps every token), the decode pages live in the slots after it
+ *  under RaaS as above, and each step attends to the prompt_topk prompt pages
+ *  with the largest representative bound (max over the G heads, as R1/R2),
+ *  ties to the lower slot, plus every decode page and the new token.
  */
 #include <math.h>
 #include <stdint.h>
@@ -61,6 +70,8 @@ enum { POLICY_PIN_HEAD = 0, POLICY_ERROR = 1 };
 typedef struct {
     int G, d, ps, S, policy;
     int aggregation, rank_pinned; /* variants of R2 and R7, 0 by default */
+    int decode_base, prompt_topk; /* prompt selection: first decode slot, pages attended (-1: off) */
+    unsigned char* attend;        /* [S] slots the step attends to */
     double r;
     /* per page slot */
     int *state, *lid, *fill, *ts;
@@ -88,6 +99,8 @@ orc_kvm* orc_new(int G, int d, int ps, int S, double r, int policy) {
     m->kmin = (double*)calloc((size_t)S * d, sizeof(double));
     m->kmax = (double*)calloc((size_t)S * d, sizeof(double));
     m->score = (double*)calloc((size_t)S, sizeof(double));
+    m->attend = (unsigned char*)calloc((size_t)S, 1);
+    m->prompt_topk = -1;
     for (int s = 0; s < S; ++s) {
         m->state[s] = FREE;
         m->lid[s] = -1;
@@ -102,13 +115,26 @@ orc_kvm* orc_new(int G, int d, int ps, int S, double r, int policy) {
 
 int orc_set_variant(orc_kvm* m, int aggregation, int rank_pinned) {
     if (!m || aggregation < 0 || aggregation > 1 || rank_pinned < 0 || rank_pinned > 1) return ORC_E_INVALID;
+    if (rank_pinned && m->prompt_topk >= 0) return ORC_E_INVALID;
     m->aggregation = aggregation;
     m->rank_pinned = rank_pinned;
     return ORC_OK;
 }
 
+/* Quest on the prompt pages (see the header): prompt_slots slots hold the
+ * prompt, decode pages use the rest; each step attends to the topk prompt
+ * pages of largest bound. Before the prefill only; not with rank_pinned. */
+int orc_set_prompt_selection(orc_kvm* m, int prompt_slots, int topk) {
+    if (!m || m->prefilled || m->rank_pinned) return ORC_E_INVALID;
+    if (prompt_slots < 0 || prompt_slots > m->S - 1 || topk < 0) return ORC_E_INVALID;
+    m->decode_base = prompt_slots;
+    m->prompt_topk = topk;
+    return ORC_OK;
+}
+
 void orc_free(orc_kvm* m) {
     if (!m) return;
+    free(m->attend);
     free(m->state); free(m->lid); free(m->fill); free(m->ts);
     free(m->K); free(m->V); free(m->kmin); free(m->kmax); free(m->score);
     free(m);
@@ -144,9 +170,12 @@ int orc_prefill(orc_kvm* m, const double* K, const double* V, int P) {
     const int ps = m->ps;
     int pages = (P + ps - 1) / ps;
     int keep = pages;
-    if (keep > m->S - 1) { /* R3: at least one slot stays for decode pages */
+    /* R3: at least one slot stays for decode pages; with prompt selection the
+     * prompt has its own region */
+    const int cap = m->prompt_topk >= 0 ? m->decode_base : m->S - 1;
+    if (keep > cap) {
         if (m->policy == POLICY_ERROR) return ORC_E_BUDGET;
-        keep = m->S - 1;
+        keep = cap;
     }
     for (int p = 0; p < keep; ++p) {
         m->state[p] = PINNED;
@@ -173,14 +202,14 @@ static void attention(const orc_kvm* m, const double* q, const double* k_new, co
     const double scale = 1.0 / sqrt((double)d);
     int n_old = 0;
     for (int s = 0; s < m->S; ++s)
-        if (m->state[s] != FREE) n_old += m->fill[s];
+        if (m->attend[s]) n_old += m->fill[s];
     const int n = n_old + 1;
     double* Kc = (double*)malloc(sizeof(double) * (size_t)n * d);
     double* Vc = (double*)malloc(sizeof(double) * (size_t)n * d);
     double* logit = (double*)malloc(sizeof(double) * (size_t)n);
     int i = 0;
     for (int s = 0; s < m->S; ++s) { /* K_old, V_old */
-        if (m->state[s] == FREE) continue;
+        if (!m->attend[s]) continue;
         for (int t = 0; t < m->fill[s]; ++t, ++i) {
             memcpy(Kc + (size_t)i * d, m->K + ((size_t)s * ps + t) * d, sizeof(double) * d);
             memcpy(Vc + (size_t)i * d, m->V + ((size_t)s * ps + t) * d, sizeof(double) * d);
@@ -217,9 +246,46 @@ static int cmp_double(const void* a, const void* b) {
 /* kvm.is_full(): the next token has no room (R8) */
 static int is_full(const orc_kvm* m) {
     if (m->tail >= 0 && m->fill[m->tail] < m->ps) return 0;
-    for (int s = 0; s < m->S; ++s)
+    for (int s = m->decode_base; s < m->S; ++s)
         if (m->state[s] == FREE) return 0;
     return 1;
+}
+
+/* the slots a step attends to: every resident page, except that with prompt
+ * selection only the prompt_topk pinned pages of largest bound (max over the
+ * heads of sum_c max(q_c kmax_c, q_c kmin_c)) are taken, ties to the lower
+ * slot */
+static void select_attended(orc_kvm* m, const double* q) {
+    const int S = m->S, G = m->G, d = m->d;
+    int np = 0;
+    for (int s = 0; s < S; ++s) {
+        m->attend[s] = m->state[s] != FREE;
+        np += m->state[s] == PINNED;
+    }
+    if (m->prompt_topk < 0 || np <= m->prompt_topk) return;
+    double* b = (double*)malloc(sizeof(double) * (size_t)S);
+    for (int s = 0; s < S; ++s) {
+        if (m->state[s] != PINNED) continue;
+        double best = -INFINITY;
+        for (int j = 0; j < G; ++j) {
+            double acc = 0.0;
+            for (int c = 0; c < d; ++c) {
+                const double x = q[(size_t)j * d + c] * m->kmax[(size_t)s * d + c];
+                const double y = q[(size_t)j * d + c] * m->kmin[(size_t)s * d + c];
+                acc += x > y ? x : y;
+            }
+            if (acc > best) best = acc;
+        }
+        b[s] = best;
+    }
+    for (int s = 0; s < S; ++s) {
+        if (m->state[s] != PINNED) continue;
+        int above = 0;
+        for (int o = 0; o < S; ++o)
+            if (m->state[o] == PINNED && (b[o] > b[s] || (b[o] == b[s] && o < s))) ++above;
+        m->attend[s] = above < m->prompt_topk;
+    }
+    free(b);
 }
 
 /* store K_new, V_new: into the tail page, or a fresh page taken from the
@@ -230,7 +296,7 @@ static int store_new_token(orc_kvm* m, const double* k_new, const double* v_new)
     const int S = m->S, c = m->clock;
     if (m->tail < 0 || m->fill[m->tail] == m->ps) {
         int s = -1;
-        for (int i = 0; i < S; ++i)
+        for (int i = m->decode_base; i < S; ++i)
             if (m->state[i] == FREE) { s = i; break; }
         if (s < 0) return ORC_E_INTERNAL; /* eager eviction leaves a free slot */
         m->state[s] = EVICTABLE;
@@ -365,7 +431,10 @@ int orc_decode(orc_kvm* m, const double* q, const double* k_new, const double* v
     const int G = m->G, S = m->S;
     const int c = m->clock;
 
-    if (out) attention(m, q, k_new, v_new, out);
+    if (out) {
+        select_attended(m, q);
+        attention(m, q, k_new, v_new, out);
+    }
     int rc = store_new_token(m, k_new, v_new);
     if (rc != ORC_OK) return rc;
 
@@ -406,6 +475,7 @@ int orc_decode_group(orc_kvm** ms, int n, const double* q, const double* k_new, 
         if (!b->prefilled) return ORC_E_STATE;
         if (b->G != a->G || b->d != a->d || b->ps != a->ps || b->S != a->S || b->r != a->r ||
             b->aggregation != a->aggregation || b->rank_pinned != a->rank_pinned ||
+            b->decode_base != a->decode_base || b->prompt_topk != a->prompt_topk ||
             b->clock != a->clock || b->tail != a->tail || b->next_lid != a->next_lid)
             return ORC_E_INVALID;
         for (int s = 0; s < a->S; ++s)
@@ -416,9 +486,11 @@ int orc_decode_group(orc_kvm** ms, int n, const double* q, const double* k_new, 
     const int G = a->G, d = a->d, S = a->S, H = n * G;
     const int c = a->clock;
     for (int h = 0; h < n; ++h) {
-        if (out)
+        if (out) {
+            select_attended(ms[h], q + (size_t)h * G * d);
             attention(ms[h], q + (size_t)h * G * d, k_new + (size_t)h * d, v_new + (size_t)h * d,
                       out + (size_t)h * G * d);
+        }
         int rc = store_new_token(ms[h], k_new + (size_t)h * d, v_new + (size_t)h * d);
         if (rc != ORC_OK) return rc;
     }
@@ -452,6 +524,11 @@ void orc_state(const orc_kvm* m, int* page_table, int* ts, int* state, int* fill
         unit[4] = m->n_evictable;
         unit[5] = m->k_refreshed;
     }
+}
+
+/* the slots the last step attended to (1) or not (0) */
+void orc_last_attended(const orc_kvm* m, int* out) {
+    for (int s = 0; s < m->S; ++s) out[s] = m->attend[s];
 }
 
 /* per-slot scores of the last step (NaN where not evictable) and the threshold */

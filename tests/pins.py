@@ -25,12 +25,13 @@ def _softmax_attention(q, K, V):
     return w @ V
 
 
-def _new_slot(st, ps):
+def _new_slot(st, ps, base=0):
     """The slot a decode step fills with a fresh page, given the state before
-    the step (the lowest free slot when the tail page is full or absent)."""
+    the step (the lowest free slot from `base`, the first decode slot, when
+    the tail page is full or absent)."""
     if st["tail"] >= 0 and st["fill"][st["tail"]] < ps:
         return None
-    return min(s for s in range(len(st["state"])) if st["state"][s] == oracle.FREE)
+    return min(s for s in range(base, len(st["state"])) if st["state"][s] == oracle.FREE)
 
 
 def check_dense_equivalence(lib, G=3, d=16, ps=4, S=8, P=5, T=20, seed=1):
@@ -371,11 +372,11 @@ def check_budget_and_attention_set(lib, seed=7):
     assert np.array_equal(out, np.stack([v] * G))
 
 
-def _ranked_slot_lids(st, ps, rank_pinned):
+def _ranked_slot_lids(st, ps, rank_pinned, base=0):
     """slot -> logical id of the pages a step ranks, from the state before it"""
     states = (oracle.EVICTABLE, oracle.PINNED) if rank_pinned else (oracle.EVICTABLE,)
     out = {s: int(st["page_table"][s]) for s in range(len(st["state"])) if st["state"][s] in states}
-    new = _new_slot(st, ps)
+    new = _new_slot(st, ps, base)
     if new is not None:
         out[new] = st["next_lid"]
     return out
@@ -465,7 +466,77 @@ def check_group_vs_history(lib, seed=11, cases=30):
                 assert sorted(int(x) for x in st["page_table"] if x >= 0) == hist.resident_lids(), t
 
 
+def check_prompt_selection(lib, seed=12):
+    """Quest on the prompt pages, RaaS on the decode pages (the combination
+    recommended for long prompts). With one token per page a prompt page's
+    bound is its token's logit, so a step attends to exactly the k prompt
+    tokens of largest max_j q_j.k (ties, from duplicated keys, to the earlier
+    token), every resident decode token and the new one, and its output is
+    textbook attention over that set. Prompt pages stay put; decode pages use
+    only the slots after the prompt region and follow the LRU rule (history
+    replay fed the step's scores)."""
+    rng = np.random.default_rng(seed)
+    G, d, P, npr, ndec, k = 3, 8, 20, 24, 8, 5
+    for r in (0.5, 0.25):
+        m = oracle.Kvm(G, d, 1, npr + ndec, r=r, lib=lib, prompt_slots=npr, prompt_topk=k)
+        K = rng.standard_normal((P, d))
+        K[7] = K[3]  # equal bounds: the tie goes to the earlier token
+        K[11] = K[3]
+        V = rng.standard_normal((P, d))
+        assert m.prefill(K, V) == 0
+        keys, vals = list(K), list(V)
+        hist = HistoryLRU(1, ndec, r, 0)
+        for t in range(60):
+            st0 = m.state()
+            dec = sorted(int(x) for x in st0["page_table"][npr:] if x >= 0)
+            q = rng.standard_normal((G, d))
+            if t % 3 == 0:
+                q[0] = K[3] * 2.0  # draws the tied tokens into the top k
+            kn, vn = rng.standard_normal(d), rng.standard_normal(d)
+            out = m.decode(q, kn, vn)
+            keys.append(kn)
+            vals.append(vn)
+            logit = np.array([(q @ K[i]).max() for i in range(P)])
+            order = sorted(range(P), key=lambda i: (-logit[i], i))
+            chosen = sorted(order[:k])
+            att = m.last_attended()
+            assert sorted(np.nonzero(att[:npr])[0].tolist()) == chosen, (t, chosen)
+            pos = chosen + dec + [P + t]
+            ref = _softmax_attention(q, np.array([keys[i] for i in pos]), np.array([vals[i] for i in pos]))
+            assert np.max(np.abs(out - ref)) < 1e-12, t
+            st = m.state()
+            assert st["page_table"][:P].tolist() == list(range(P)) and np.all(st["page_table"][P:npr] == -1)
+            sc, _ = m.last_scores()
+            ranked = _ranked_slot_lids(st0, 1, False, base=npr)
+            assert all(s >= npr for s in ranked)
+            score_of = {lid - P: sc[s] for s, lid in ranked.items()}
+            ev = hist.decode(lambda lid: score_of[lid])
+            assert (P + ev if ev is not None else -1) == st["evicted"], t
+            assert sorted(int(x) - P for x in st["page_table"][npr:] if x >= 0) == hist.resident_lids(), t
+    # pages of 4: page 0 holds +10u and -10u (u along q), page 1 four copies
+    # of 0.5u. Any upper bound puts page 0 at >= 10|q|, above page 1's exact
+    # bound 0.5|q| (equal keys), so with k = 1 the step attends to page 0.
+    u = rng.standard_normal(8)
+    u /= np.linalg.norm(u)
+    K = np.array([10 * u, -10 * u, -10 * u, 10 * u] + [0.5 * u] * 4)
+    m = oracle.Kvm(1, 8, 4, 4, lib=lib, prompt_slots=2, prompt_topk=1)
+    assert m.prefill(K, rng.standard_normal((8, 8))) == 0
+    m.decode(u[None, :] * 3.0, rng.standard_normal(8), rng.standard_normal(8))
+    assert m.last_attended()[:2].tolist() == [True, False]
+    # k at least the prompt's pages: the default policy with the same slots
+    a = oracle.Kvm(2, 8, 4, 9, lib=lib, prompt_slots=4, prompt_topk=4)
+    b = oracle.Kvm(2, 8, 4, 9, lib=lib)
+    K, V = rng.standard_normal((14, 8)), rng.standard_normal((14, 8))
+    assert a.prefill(K, V) == 0 and b.prefill(K, V) == 0
+    for t in range(50):
+        q, kn, vn = rng.standard_normal((2, 8)), rng.standard_normal(8), rng.standard_normal(8)
+        assert np.array_equal(a.decode(q, kn, vn), b.decode(q, kn, vn)), t
+        sa, sb = a.state(), b.state()
+        assert np.array_equal(sa["page_table"], sb["page_table"]) and np.array_equal(sa["ts"], sb["ts"]), t
+
+
 ALL_CHECKS = [
+    check_prompt_selection,
     check_group_single_token_pages,
     check_group_vs_history,
     check_rank_pinned_vs_history,

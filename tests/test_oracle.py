@@ -34,11 +34,9 @@ MUTANTS = [
     ("order_statistic_off_by_one", [("theta = sorted[n - k - 1];", "theta = sorted[n - k];")]),
     ("tie_break_newest", [("m->lid[s] < m->lid[v]", "m->lid[s] > m->lid[v]")]),
     ("new_page_unstamped", [("m->ts[s] = c; /* R5 */", "m->ts[s] = -1; /* R5 */")]),
-    ("prefill_fills_cache", [("keep = m->S - 1;", "keep = m->S;")]),
-    ("pinned_not_attended", [("if (m->state[s] != FREE) n_old += m->fill[s];",
-                              "if (m->state[s] == EVICTABLE) n_old += m->fill[s];"),
-                             ("        if (m->state[s] == FREE) continue;\n        for (int t = 0; t < m->fill[s]; ++t, ++i) {",
-                              "        if (m->state[s] != EVICTABLE) continue;\n        for (int t = 0; t < m->fill[s]; ++t, ++i) {")]),
+    ("prefill_fills_cache", [("const int cap = m->prompt_topk >= 0 ? m->decode_base : m->S - 1;",
+                              "const int cap = m->prompt_topk >= 0 ? m->decode_base : m->S;")]),
+    ("pinned_not_attended", [("m->attend[s] = m->state[s] != FREE;", "m->attend[s] = m->state[s] == EVICTABLE;")]),
     ("kmax_not_widened", [("if (k[c] > m->kmax[(size_t)s * d + c]) m->kmax[(size_t)s * d + c] = k[c];", "")]),
     ("evicted_tail_kept", [("if (m->tail == v) m->tail = -1;", "")]),
     ("top_r_rounds_up", [("int k = (int)floor(m->r * (double)n);", "int k = (int)ceil(m->r * (double)n);")]),
@@ -55,6 +53,10 @@ MUTANTS = [
     ("group_first_kv_head_scored", [("    for (int h = 0; h < n; ++h) head_bounds(ms[h], q + (size_t)h * G * d, bound, H, h * G);",
                                      "    for (int h = 0; h < n; ++h) head_bounds(ms[0], q, bound, H, h * G);")]),
     ("softmax_sign", [("double p = exp(logit[t] - mx);", "double p = exp(mx - logit[t]);")]),
+    ("prompt_ties_to_later_slot", [("(b[o] == b[s] && o < s)", "(b[o] == b[s] && o > s)")]),
+    ("prompt_bound_uses_min", [("acc += x > y ? x : y;", "acc += x < y ? x : y;")]),
+    ("prompt_topk_one_more", [("m->attend[s] = above < m->prompt_topk;", "m->attend[s] = above <= m->prompt_topk;")]),
+    ("decode_page_in_prompt_region", [("for (int i = m->decode_base; i < S; ++i)", "for (int i = 0; i < S; ++i)")]),
     ("gqa_last_head_only", [("if (bound[(size_t)s * H + j] > best) best = bound[(size_t)s * H + j];",
                              "best = bound[(size_t)s * H + j];")]),
 ]
