@@ -31,7 +31,7 @@ if ROOT not in sys.path:
     sys.path.insert(0, ROOT)
 
 HBM_PEAK_GBS = 8000.0  # MI355X HBM3E
-KERNEL_STEP, KERNEL_EPILOGUE = 0, 1
+KERNEL_STEP, KERNEL_EPILOGUE, KERNEL_SELECT = 0, 1, 2
 
 
 def parse():
@@ -49,6 +49,9 @@ def parse():
     ap.add_argument("--rank-pinned", action="store_true", help="rank the pinned prefill pages too")
     ap.add_argument("--decision-scope", choices=("kv-head", "sequence"), default="kv-head",
                     help="one page table per KV head (default) or per sequence")
+    ap.add_argument("--prompt-topk", type=int, default=0,
+                    help="Quest on the prompt: keep the whole prompt in a prompt region and attend to this many "
+                         "prompt pages per step (0: off; the budget then counts decode tokens)")
     ap.add_argument("--cpu-seconds", type=float, default=15.0, help="budget of the CPU oracle sample")
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--decode-sweep", action="store_true",
@@ -194,7 +197,7 @@ def resident_schedule(st, ps, S, n):
     return out
 
 
-def step_bytes(w, resident, n_ev):
+def step_bytes(w, resident, n_ev, S=None):
     """Algorithmic HBM bytes of one whole decode step, all units: K+V of the
     resident tokens; the representative keys (per-channel min and max) of the
     n_ev scored pages (the evictable ones, plus the pinned ones when they are
@@ -202,7 +205,8 @@ def step_bytes(w, resident, n_ev):
     and stored once; the tail page's min/max read and written; per slot,
     state/timestamp/id/fill read and state/timestamp written (24 B)."""
     e = 2 if w.dtype == "bf16" else 4
-    d, G, S = w.head_dim, w.group, w.slots
+    d, G = w.head_dim, w.group
+    S = w.slots if S is None else S
     per_unit = (resident * 2 * d * e + n_ev * 2 * d * e + 2 * G * d * e + 4 * d * e + 4 * d * e + 24 * S)
     return per_unit.sum(axis=-1)
 
@@ -350,13 +354,16 @@ def main():
     dev = torch.device("cuda", 0)
     torch.cuda.set_device(dev)
     dt = torch.bfloat16 if w.dtype == "bf16" else torch.float32
-    U, S = w.batch * w.n_kv_heads, w.slots
-
     agg = raas.SCORE_SOFTMAX_SUM if args.score_aggregation == "softmax-sum" else raas.SCORE_MAX
     scope = raas.SCOPE_SEQUENCE if args.decision_scope == "sequence" else raas.SCOPE_KV_HEAD
-    variant = agg != raas.SCORE_MAX or args.rank_pinned or scope != raas.SCOPE_KV_HEAD
+    align = max(w.page_size, 32)
+    prompt_tokens = -(-w.prefill_len // align) * align if args.prompt_topk > 0 else 0
+    npr = prompt_tokens // w.page_size
+    variant = agg != raas.SCORE_MAX or args.rank_pinned or scope != raas.SCOPE_KV_HEAD or npr > 0
     t_run = time.perf_counter()
-    pool = raas.Pool.for_workload(w, score_aggregation=agg, rank_pinned=args.rank_pinned, decision_scope=scope)
+    pool = raas.Pool.for_workload(w, score_aggregation=agg, rank_pinned=args.rank_pinned, decision_scope=scope,
+                                  prompt_tokens=prompt_tokens, prompt_topk=args.prompt_topk)
+    U, S = w.batch * w.n_kv_heads, pool.slots
     if args.splits:
         pool.set_attention_splits(args.splits)
     # a step is one token through every layer of the workload; the layers
@@ -380,7 +387,7 @@ def main():
             for layer in range(nl):
                 pool.decode_prepared(prepared[layer][i % R])
 
-    fill = max(0, w.budget - w.prefill_len) + w.page_size
+    fill = (w.budget if npr else max(0, w.budget - w.prefill_len)) + w.page_size
     run(0, fill)
     run(fill, args.warmup)
     torch.cuda.synchronize()
@@ -389,12 +396,25 @@ def main():
     pool.profile(1 << KERNEL_EPILOGUE)
     run(fill + args.warmup, 1)
     fused = pool.profile_read(KERNEL_EPILOGUE)[1] == 0
+    # the event span times the step kernel alone only when it is the step's
+    # only launch (prompt selection adds a kernel in front)
+    alone = fused and npr == 0
     pool.profile(0)
     t_start = fill + args.warmup + 1
     st = pool.export_state(0)
-    res = resident_schedule(st, w.page_size, S, args.steps)
     n_ev0 = (st["state"] == 2).sum(axis=1)
     n_pin = (st["state"] == 1).sum(axis=1) if args.rank_pinned else 0
+    if npr:
+        # the decode region evolves as a pool of its own; the attention reads
+        # the chosen prompt pages (full ones) besides, and the selection
+        # reads every kept prompt page's representative keys
+        kp = (st["state"][:, :npr] == 1).sum(axis=1)
+        dec = dict(state=st["state"][:, npr:], fill=st["fill"][:, npr:],
+                   tail=np.where(st["tail"] >= 0, st["tail"] - npr, -1))
+        res = resident_schedule(dec, w.page_size, S - npr, args.steps) + np.minimum(kp, args.prompt_topk) * w.page_size
+        n_pin = kp
+    else:
+        res = resident_schedule(st, w.page_size, S, args.steps)
 
     # timed region: HIP events on the launch stream (torch's current stream)
     # around all K steps; with two kernels per step, the library also times
@@ -403,11 +423,11 @@ def main():
     torch.cuda.synchronize()
     t0 = time.perf_counter()
     ev0.record()
-    if fused:
+    if alone:
         run(t_start, args.steps)
     else:
         for i0 in range(0, args.steps, 16):
-            pool.profile((1 << KERNEL_STEP) | (1 << KERNEL_EPILOGUE))
+            pool.profile((1 << KERNEL_STEP) | (1 << KERNEL_EPILOGUE) | (1 << KERNEL_SELECT))
             run(t_start + i0, 1)
             pool.profile(0)
             run(t_start + i0 + 1, min(16, args.steps - i0) - 1)
@@ -417,6 +437,7 @@ def main():
     span_ms = ev0.elapsed_time(ev1)
     step_ms, step_n = pool.profile_read(KERNEL_STEP)
     epi_ms, epi_n = pool.profile_read(KERNEL_EPILOGUE)
+    sel_ms, sel_n = pool.profile_read(KERNEL_SELECT)
     st_end = pool.export_state(0)
     pool.close()
 
@@ -424,8 +445,8 @@ def main():
     tokens_per_s = w.batch * args.steps / elapsed
     # step kernel's average duration: the event span over the K launches when
     # it is the only kernel of the step, else the sampled per-kernel events
-    step_avg_s = span_ms / 1e3 / (args.steps * nl) if fused else step_ms / 1e3 / max(step_n, 1)
-    step_b = float(np.mean(step_bytes(w, res, (n_ev0 + n_pin)[None, :])))
+    step_avg_s = span_ms / 1e3 / (args.steps * nl) if alone else step_ms / 1e3 / max(step_n, 1)
+    step_b = float(np.mean(step_bytes(w, res, (n_ev0 + n_pin)[None, :], S)))
     # bytes of the step kernel alone: everything but what the epilogue kernel moves
     e = 2 if w.dtype == "bf16" else 4
     kernel_b = step_b if fused else step_b - U * w.group * w.head_dim * e - 24 * U * S
@@ -459,6 +480,7 @@ def main():
             "attention_splits": args.splits or "auto",
             "score_aggregation": args.score_aggregation, "rank_pinned": bool(args.rank_pinned),
             "decision_scope": args.decision_scope,
+            "prompt_tokens": prompt_tokens, "prompt_topk": args.prompt_topk,
         },
         "step_hbm_gbs_algorithmic": round(step_b * nl / (elapsed / args.steps) / 1e9, 1),
         "roofline": {
@@ -472,9 +494,10 @@ def main():
             "traffic_source": traffic_src,
             "bytes_per_launch": kernel_b,
             "avg_launch_us": round(step_avg_s * 1e6, 3),
-            "launches_timed": args.steps * nl if fused else step_n,
-            "timing": "event span over the timed launches" if fused else "per-launch events, every 16th step",
+            "launches_timed": args.steps * nl if alone else step_n,
+            "timing": "event span over the timed launches" if alone else "per-launch events, every 16th step",
             "epilogue_kernel_avg_us": round(epi_ms * 1e3 / epi_n, 3) if epi_n else None,
+            "select_kernel_avg_us": round(sel_ms * 1e3 / sel_n, 3) if sel_n else None,
         },
     }
     assert np.all(st_end["clock"] == w.prefill_len + t_start + args.steps)

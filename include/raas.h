@@ -108,6 +108,19 @@ typedef struct {
                                   evictable ones (n counts them) but never take timestamps;
                                   0: only evictable pages are ranked */
     int32_t decision_scope;    /* raas_decision_scope */
+    /* Quest on the prompt, RaaS on the decode tokens (recommended for long
+     * prompts or small budgets, Section 4.2 and Limitations): with
+     * prompt_tokens > 0 the pool keeps a prompt region of prompt_tokens
+     * tokens (a multiple of page_size and of 32) in front of the decode
+     * budget; prefill pages go there (a longer prompt: the first pages are
+     * kept under RAAS_PREFILL_PIN_HEAD, RAAS_E_BUDGET under
+     * RAAS_PREFILL_ERROR), budget_tokens then counts decode tokens only, and
+     * each step attends to the prompt_topk (>= 1) prompt pages of largest
+     * representative bound (max over the group's heads; ties to the lower
+     * page), every decode page and the new token. Not with rank_pinned.
+     * 0, 0 = off. */
+    int32_t prompt_tokens;
+    int32_t prompt_topk;
 } raas_config;
 
 typedef struct raas_pool raas_pool; /* opaque */
@@ -204,7 +217,8 @@ raas_status raas_set_attention_splits(raas_pool* pool, int32_t splits);
  * 0 the step kernel (attention, append, page scores, and the epilogue when a
  * single workgroup covers a unit), 1 the epilogue kernel (split merge,
  * refresh, eviction; launched when a unit is split over several
- * workgroups, and for fp32 pools). mask 0 turns timing off.
+ * workgroups, for fp32 pools and for the sequence scope), 2 the prompt
+ * selection kernel (with a prompt region). mask 0 turns timing off.
  * raas_profile_read returns, for kernel i, the summed duration in ms and the
  * number of timed launches since the last read (synchronising on the
  * recorded events), then resets them. Errors: RAAS_E_INVALID, RAAS_E_HIP. */

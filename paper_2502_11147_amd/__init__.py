@@ -19,7 +19,7 @@ PREFILL_PIN_HEAD, PREFILL_ERROR = 0, 1
 SCORE_MAX, SCORE_SOFTMAX_SUM = 0, 1
 SCOPE_KV_HEAD, SCOPE_SEQUENCE = 0, 1
 FREE, PINNED, EVICTABLE = 0, 1, 2
-KERNELS = ("append", "attention", "merge", "score")
+KERNELS = ("step", "epilogue", "prompt_select")  # raas_profile kernel indices
 
 # C entry points declared in include/raas.h
 EXPORTS = (
@@ -50,6 +50,8 @@ class Config(ctypes.Structure):
         ("score_aggregation", ctypes.c_int32),
         ("rank_pinned", ctypes.c_int32),
         ("decision_scope", ctypes.c_int32),
+        ("prompt_tokens", ctypes.c_int32),
+        ("prompt_topk", ctypes.c_int32),
     ]
 
 
@@ -123,16 +125,17 @@ class Pool:
     def __init__(self, batch: int, n_layers: int, n_q_heads: int, n_kv_heads: int, head_dim: int,
                  page_size: int, budget_tokens: int, dtype: str = "bf16", r: float = 0.5,
                  prefill_policy: int = PREFILL_PIN_HEAD, score_aggregation: int = SCORE_MAX,
-                 rank_pinned: bool = False, decision_scope: int = SCOPE_KV_HEAD, stream=None):
+                 rank_pinned: bool = False, decision_scope: int = SCOPE_KV_HEAD, prompt_tokens: int = 0,
+                 prompt_topk: int = 0, stream=None):
         self.lib = load_library()
         self.cfg = Config(batch, n_layers, n_q_heads, n_kv_heads, head_dim, page_size, budget_tokens,
                           BF16 if dtype == "bf16" else F32, r, prefill_policy, score_aggregation,
-                          int(rank_pinned), decision_scope)
+                          int(rank_pinned), decision_scope, prompt_tokens, prompt_topk)
         self.dtype = dtype
         self.batch, self.n_layers = batch, n_layers
         self.n_q_heads, self.n_kv_heads, self.head_dim = n_q_heads, n_kv_heads, head_dim
         self.page_size, self.budget = page_size, budget_tokens
-        self.slots = budget_tokens // page_size
+        self.slots = (budget_tokens + prompt_tokens) // page_size
         self.units = batch * n_kv_heads
         self._h = ctypes.c_void_p()
         _check(self.lib.raas_create_pool(ctypes.byref(self.cfg), _stream_handle(stream), ctypes.byref(self._h)),

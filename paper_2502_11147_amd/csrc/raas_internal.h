@@ -50,6 +50,13 @@ struct LayerView {
     int hgrp;         // units per retention decision: 1, or n_kv_heads (units seq*hgrp .. +hgrp-1)
     int nkv;          // KV heads per sequence: unit u belongs to sequence u / nkv
     int nblk;         // 32-token blocks a step visits (from row 0): every resident row lies below
+    int dbase;        // first slot decode pages may take (the prompt region's size; 0 without one)
+    int pcap;         // most prompt pages kept: S-1, or the prompt region's slots
+    int topk;         // prompt pages attended per step (Quest on the prompt), -1: all
+    int32_t* fill_att;  // [U][S] fills the attention sees: fill, or (topk >= 0) 0 for unchosen prompt pages
+    int32_t* blist;     // [U][lcap_blk] blocks a step visits (topk >= 0): chosen prompt blocks, decode blocks
+    int32_t* bcnt;      // [U][2] prompt blocks and all blocks in blist
+    int lcap_blk;       // Lcap / 32
 };
 
 // Prefill input of one layer: `stride` token rows per unit; per-sequence
@@ -80,9 +87,12 @@ struct StepPlan {
     size_t lds;      // dynamic LDS of the step kernel
 };
 
-// grouped: retention decided per group of units, by the epilogue kernel
+// grouped: retention decided per group of units, by the epilogue kernel;
+// list_ints: LDS entries of a block list (0 without prompt selection)
 StepPlan plan_step(int U, int G, int D, int S, int Lcap, int ps, int pinned, bool bf16, int agg,
-                   bool grouped, int split_override);
+                   bool grouped, int list_ints, int split_override);
+// Quest on the prompt pages: the attended fills and the block list of a step.
+hipError_t launch_prompt_select(const LayerView& L, const StepIO& io, hipStream_t stream);
 // Lets the step kernels use more than the default dynamic LDS.
 hipError_t allow_large_lds();
 

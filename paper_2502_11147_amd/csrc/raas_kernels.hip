@@ -101,9 +101,10 @@ __device__ __forceinline__ int unit_prefill_len(const LayerView& L, const Prefil
     return in.lens != nullptr ? in.lens[seq] : in.P;
 }
 
-// pages kept of a prefill of P tokens (the first min(ceil(P/ps), S-1))
+// pages kept of a prefill of P tokens: the first min(ceil(P/ps), pcap)
+// (pcap = S-1, or the prompt region's slots)
 __device__ __forceinline__ int kept_pages(const LayerView& L, int P) {
-    return min((P + L.ps - 1) / L.ps, L.S - 1);
+    return min((P + L.ps - 1) / L.ps, L.pcap);
 }
 
 __global__ void k_prefill_meta(LayerView L, PrefillIn in) {
@@ -125,7 +126,7 @@ __global__ void k_prefill_meta(LayerView L, PrefillIn in) {
         U4[kNextLid] = (P + L.ps - 1) / L.ps;
         U4[kClock] = P;
         U4[kEvicted] = -1;
-        U4[kNextSlot] = keep_pages;  // lowest free slot; decode starts a fresh page
+        U4[kNextSlot] = max(keep_pages, L.dbase);  // lowest free decode slot; decode starts a fresh page
         U4[kNextFill] = 0;
         U4[kPinnedPages] = keep_pages;
     }
@@ -478,8 +479,8 @@ __device__ void retention_wave(const LayerView& L, const UnitRec& ur, double r, 
 __device__ void evict_wave(const LayerView& L, const UnitRec& ur, int* s_state, int* s_ts, const int* s_lid,
                            RetShared& out) {
     const int S = L.S, ps = L.ps, lane = threadIdx.x & 63;
-    int nfree = 0;
-    for (int s0 = 0; s0 < S; s0 += 64) {
+    int nfree = 0;  // free decode slots
+    for (int s0 = L.dbase; s0 < S; s0 += 64) {
         const int s = s0 + lane;
         nfree += __popcll(__ballot(s < S && s_state[s] == kFree));
     }
@@ -517,7 +518,7 @@ __device__ void evict_wave(const LayerView& L, const UnitRec& ur, int* s_state, 
     int next_slot = ur.ns;
     if (need_free) {
         next_slot = S;
-        for (int s0 = 0; s0 < S; s0 += 64) {
+        for (int s0 = L.dbase; s0 < S; s0 += 64) {
             const int s = s0 + lane;
             const unsigned long long m = __ballot(s < S && (s_state[s] == kFree || s == victim));
             if (m) {
@@ -756,7 +757,9 @@ __device__ __forceinline__ void attend_block(const u32x4 (&kr)[2][D / 32], const
 
 // AGG: the softmax aggregation of the page scores (a separate instance, so
 // that the default one carries none of its registers).
-template <int D, int NW, bool AGG>
+// LIST: the blocks come from the unit's block list (the prompt blocks the
+// selection kernel chose, then the decode region's), not from a range.
+template <int D, int NW, bool AGG, bool LIST>
 __global__ __launch_bounds__(NW * 64) __attribute__((amdgpu_waves_per_eu(1, 2))) void k_step_bf16(
     LayerView L, StepIO io, float scale_log2, double r, int fused) {
     constexpr int KS = D / 32, NB = D / 16, BLK = 32 * D;
@@ -777,6 +780,7 @@ __global__ __launch_bounds__(NW * 64) __attribute__((amdgpu_waves_per_eu(1, 2)))
     int* s_state = reinterpret_cast<int*>(s_mz + (AGG ? 2 * G : 0));  // [S], fused only
     int* s_ts = s_state + S;
     int* s_lid = s_ts + S;
+    int* s_list = fused ? s_lid + S : reinterpret_cast<int*>(s_score);  // LIST: this workgroup's blocks
 
     const int tid = threadIdx.x, lane = tid & 63, w = tid >> 6;
     const int grp = lane >> 4, col = lane & 15;
@@ -784,15 +788,34 @@ __global__ __launch_bounds__(NW * 64) __attribute__((amdgpu_waves_per_eu(1, 2)))
     const int u = blockIdx.x / nsplit, split = blockIdx.x - (blockIdx.x / nsplit) * nsplit;
     if (io.active != nullptr && io.active[u / L.nkv] == 0) return;  // the sequence sits this step out
     const size_t base = (size_t)u * S;
-    const int b0 = split * L.bps;
-    const int b1 = max(b0, min(L.nblk, b0 + L.bps));
-    const int nown = b1 - b0;  // blocks of this workgroup
+    // this workgroup's claims lo .. hi-1: blocks of the unit (a range), or
+    // (LIST) entries of its block list; pages scored here: those whose first
+    // row lies in blocks sb0 .. sb1-1
+    int lo, hi, sb0, sb1;
+    if constexpr (LIST) {
+        const int nsel = L.bcnt[2 * u], ntot = L.bcnt[2 * u + 1];
+        const int per = (ntot + nsplit - 1) / nsplit;
+        lo = min(ntot, split * per);
+        hi = min(ntot, lo + per);
+        const int nbp = L.dbase * ps / 32;  // the decode region starts at this block
+        sb0 = nbp + max(lo, nsel) - nsel;
+        sb1 = nbp + max(hi, nsel) - nsel;
+        for (int i = tid; i < hi - lo; i += NW * 64) s_list[i] = L.blist[(size_t)u * L.lcap_blk + lo + i];
+        __syncthreads();
+    } else {
+        lo = split * L.bps;
+        hi = max(lo, min(L.nblk, lo + L.bps));
+        sb0 = lo;
+        sb1 = hi;
+    }
+    const int nown = hi - lo;                  // claims of this workgroup
+    const int bend = LIST ? 0x40000000 : hi;   // no block: every block index lies below
     const uint16_t* qg = (const uint16_t*)io.q + (size_t)u * G * D;
     const uint16_t* kn_g = (const uint16_t*)io.k_new + (size_t)u * D;
     const uint16_t* vn_g = (const uint16_t*)io.v_new + (size_t)u * D;
     const uint16_t* Ku = (const uint16_t*)L.K + (size_t)u * L.Lcap * D;
     const uint16_t* Vu = (const uint16_t*)L.V + (size_t)u * L.Lcap * D;
-    const int32_t* fu = L.fill + base;
+    const int32_t* fu = L.fill_att + base;  // fills the attention sees
     auto load_block = [&](int b, u32x4 (&kr)[2][KS], u32x4 (&vr)[NB]) {
         const uint16_t* Kb = Ku + (size_t)b * BLK + lane * 8;
         const uint16_t* Vb = Vu + (size_t)b * BLK + lane * 8;
@@ -813,11 +836,13 @@ __global__ __launch_bounds__(NW * 64) __attribute__((amdgpu_waves_per_eu(1, 2)))
     const int pinned = U4[kPinnedPages];
     // claim index i of the own blocks, ascending or (L.rev) descending
     auto blk_of = [&](int i) {
-        return b0 + (L.rev ? nown - 1 - i : i);
+        const int j = L.rev ? nown - 1 - i : i;
+        if constexpr (LIST) return s_list[j];
+        else return lo + j;
     };
-    int b = (w < nown) ? blk_of(w) : b1;
+    int b = (w < nown) ? blk_of(w) : bend;
     const int slot_first = (32 * b + 8 * grp) / ps;
-    const int fill_first = (b < b1 && slot_first < S) ? fu[slot_first] : 0;
+    const int fill_first = (b < bend && slot_first < S) ? fu[slot_first] : 0;
     // unconditional (clamped) reads: a read under a branch draws its first
     // use into the branch, with a wait for it ahead of the block loads
     const uint16_t q_first = qg[tid < G * D ? tid : 0];
@@ -832,17 +857,17 @@ __global__ __launch_bounds__(NW * 64) __attribute__((amdgpu_waves_per_eu(1, 2)))
         qv[ks] = __builtin_bit_cast(bf16x8, x);
     }
     u32x4 kr_next[2][KS], vr_next[NB];
-    if (b < b1) load_block(b, kr_next, vr_next);
+    if (b < bend) load_block(b, kr_next, vr_next);
 
     const int ns = ur.ns, nf = ur.nf;
     const bool opened = ur.opened();
     const int row_new = ns * ps + nf, b_new = row_new >> 5, tt_new = row_new & 31;
-    // the block of claim index i, or b1 when none is left
-    auto take = [&](int i) { return i < nown ? blk_of(i) : b1; };
+    // the block of claim index i, or bend when none is left
+    auto take = [&](int i) { return i < nown ? blk_of(i) : bend; };
     // pages scored here: those whose first row lies in this workgroup's blocks, pinned ones
     // excepted unless they are ranked
-    const int sl0 = max(L.rank_pinned ? 0 : pinned, min(S, (32 * b0 + ps - 1) / ps));
-    const int sl1 = min(S, (32 * b1 + ps - 1) / ps);
+    const int sl0 = max(L.rank_pinned ? 0 : pinned, min(S, (32 * sb0 + ps - 1) / ps));
+    const int sl1 = min(S, (32 * sb1 + ps - 1) / ps);
 
     // fill of the page holding this lane's 8 rows of block b (page_size % 8 == 0)
     auto row_fill = [&](int b) {
@@ -854,7 +879,7 @@ __global__ __launch_bounds__(NW * 64) __attribute__((amdgpu_waves_per_eu(1, 2)))
         return min(max(f - (t0 - (t0 / ps) * ps), 0), 8);
     };
     int f_next = 0;
-    if (b < b1) f_next = (w < nown) ? (slot_first < S ? (slot_first == ns ? nf + 1 : fill_first) : 0) : row_fill(b);
+    if (b < bend) f_next = (w < nown) ? (slot_first < S ? (slot_first == ns ? nf + 1 : fill_first) : 0) : row_fill(b);
 
     // staging for the scores and the epilogue
     if (tid < G * D) s_qd[qpad_index<D>(tid)] = (double)bf2f(q_first);
@@ -925,7 +950,7 @@ __global__ __launch_bounds__(NW * 64) __attribute__((amdgpu_waves_per_eu(1, 2)))
         }
     };
     int it = 0;
-    while (b < b1) {
+    while (b < bend) {
         const int f_cur = f_next;
         u32x4 kr[2][KS], vr[NB];
 #pragma unroll
@@ -934,10 +959,10 @@ __global__ __launch_bounds__(NW * 64) __attribute__((amdgpu_waves_per_eu(1, 2)))
             for (int ks = 0; ks < KS; ++ks) kr[qq][ks] = kr_next[qq][ks];
 #pragma unroll
         for (int nb = 0; nb < NB; ++nb) vr[nb] = vr_next[nb];
-        int bn = b1;
+        int bn = bend;
         if (lane == 0) bn = take(it == 0 ? w + NW : atomicAdd(&s_next, 1));  // one claim per wavefront
         bn = __builtin_amdgcn_readfirstlane(bn);
-        if (bn < b1) {
+        if (bn < bend) {
             f_next = row_fill(bn);
             load_block(bn, kr_next, vr_next);
         }
@@ -1053,7 +1078,7 @@ __global__ __launch_bounds__(64) void k_step_f32(LayerView L, StepIO io, float s
     const float* qg = (const float*)io.q + (size_t)u * G * D;
     const float* kn_g = (const float*)io.k_new + (size_t)u * D;
     const float* vn_g = (const float*)io.v_new + (size_t)u * D;
-    const int32_t* fu = L.fill + base;
+    const int32_t* fu = L.fill_att + base;  // fills the attention sees
 
     float qr[16][DPL], m[16], l[16], acc[16][DPL];
 #pragma unroll
@@ -1153,6 +1178,117 @@ __global__ __launch_bounds__(64) void k_step_f32(LayerView L, StepIO io, float s
     }
 }
 
+// Quest on the prompt pages (pools with a prompt region): for one unit, each
+// kept prompt page's representative bound against the step's queries, max
+// over the G heads of sum_c max(q_c kmax_c, q_c kmin_c) in fp64, channels
+// summed in order with one fused multiply-add each (the products are exact
+// in fp64, so each bound rounds exactly as a sequential sum); the topk pages
+// of largest bound, ties to the lower slot, are attended. Pages go through
+// LDS in chunks of kSelChunk (their kmin/kmax rows read with 16-byte loads,
+// rows padded against bank conflicts), one thread per (page, head). Writes
+// the fills the attention sees (0 for the other prompt pages) and the unit's
+// block list: the prompt blocks holding a chosen page, ascending, then every
+// block of the decode region. One workgroup of 256 threads per unit.
+constexpr int kSelChunk = 64;
+
+// element e of a 16-byte vector of T
+template <typename T>
+__device__ __forceinline__ float vec_elem(const u32x4& x, int e);
+template <>
+__device__ __forceinline__ float vec_elem<uint16_t>(const u32x4& x, int e) { return bf2f(u16_at(x, e)); }
+template <>
+__device__ __forceinline__ float vec_elem<float>(const u32x4& x, int e) { return __uint_as_float(x[e]); }
+
+template <typename T>
+__global__ __launch_bounds__(256) void k_prompt_select(LayerView L, StepIO io) {
+    extern __shared__ __align__(16) unsigned char smem[];
+    const int u = blockIdx.x, tid = threadIdx.x, lane = tid & 63, nth = blockDim.x;
+    if (io.active != nullptr && io.active[u / L.nkv] == 0) return;
+    const int S = L.S, G = L.G, D = L.D, ps = L.ps, npr = L.dbase;
+    const int row = D + 16 / (int)sizeof(T);  // padded row of a staged key, in elements
+    const size_t base = (size_t)u * S;
+    T* s_kx = reinterpret_cast<T*>(smem);                                // [kSelChunk][row], 16-byte rows
+    T* s_kn = s_kx + (size_t)kSelChunk * row;
+    double* s_q = reinterpret_cast<double*>(s_kn + (size_t)kSelChunk * row);  // [G][D]
+    double* s_b = s_q + (size_t)G * D;                                   // [npr] bounds
+    double* s_hb = s_b + npr;                                            // [kSelChunk][G] per-head bounds
+    int* s_sel = reinterpret_cast<int*>(s_hb + (size_t)kSelChunk * G);   // [npr] chosen
+    const int kp = L.unit[(size_t)u * kUnitFields + kPinnedPages];
+    const T* qg = (const T*)io.q + (size_t)u * G * D;
+    for (int i = tid; i < G * D; i += nth) s_q[i] = (double)to_f(qg[i]);
+    const bool all = kp <= L.topk;
+    constexpr int V = 16 / sizeof(T);  // elements per 16-byte load
+    for (int c0 = 0; c0 < kp && !all; c0 += kSelChunk) {
+        const int n = min(kSelChunk, kp - c0);
+        __syncthreads();  // the previous chunk's keys and bounds are consumed
+        for (int i = tid; i < n * (D / V); i += nth) {
+            const int pp = i / (D / V), v = i - pp * (D / V);
+            const size_t g = (base + c0 + pp) * D + (size_t)v * V;
+            *reinterpret_cast<u32x4*>(s_kx + (size_t)pp * row + v * V) = ld4((const T*)L.kmax + g);
+            *reinterpret_cast<u32x4*>(s_kn + (size_t)pp * row + v * V) = ld4((const T*)L.kmin + g);
+        }
+        __syncthreads();
+        for (int i = tid; i < n * G; i += nth) {
+            const int pp = i / G, j = i - pp * G;
+            const T* kx = s_kx + (size_t)pp * row;
+            const T* kn = s_kn + (size_t)pp * row;
+            const double* qj = s_q + (size_t)j * D;
+            double a = 0.0;
+            // both keys are read (no load waits on q's sign); the sum stays in channel order
+#pragma unroll 2
+            for (int c = 0; c < D; c += V) {
+                const u32x4 xv = *reinterpret_cast<const u32x4*>(kx + c);
+                const u32x4 nv = *reinterpret_cast<const u32x4*>(kn + c);
+#pragma unroll
+                for (int e = 0; e < V; ++e) {
+                    const double qc = qj[c + e];
+                    a = fma(qc, (double)(qc > 0.0 ? vec_elem<T>(xv, e) : vec_elem<T>(nv, e)), a);
+                }
+            }
+            s_hb[i] = a;
+        }
+        __syncthreads();
+        for (int pp = tid; pp < n; pp += nth) {
+            double best = -INFINITY;
+            for (int j = 0; j < G; ++j) best = fmax(best, s_hb[pp * G + j]);
+            s_b[c0 + pp] = best;
+        }
+    }
+    __syncthreads();
+    for (int p = tid; p < npr; p += nth) {
+        bool sel = p < kp;
+        if (sel && !all) {
+            const double bp = s_b[p];
+            int above = 0;
+            for (int o = 0; o < kp; ++o) above += (s_b[o] > bp || (s_b[o] == bp && o < p)) ? 1 : 0;
+            sel = above < L.topk;
+        }
+        s_sel[p] = sel ? 1 : 0;
+        L.fill_att[base + p] = sel ? L.fill[base + p] : 0;
+    }
+    for (int s = npr + tid; s < S; s += nth) L.fill_att[base + s] = L.fill[base + s];
+    __syncthreads();
+    if (tid < 64) {
+        const int nbp = npr * ps / 32;  // prompt blocks (the region is a whole number of blocks)
+        int32_t* bl = L.blist + (size_t)u * L.lcap_blk;
+        int cnt = 0;
+        for (int c0 = 0; c0 < nbp; c0 += 64) {
+            const int b = c0 + lane;
+            bool any = false;
+            if (b < nbp)
+                for (int s = 32 * b / ps; s <= (32 * b + 31) / ps; ++s) any = any || s_sel[s] != 0;
+            const unsigned long long m = __ballot(any);
+            if (any) bl[cnt + __popcll(m & ((1ull << lane) - 1ull))] = b;
+            cnt += __popcll(m);
+        }
+        for (int b = nbp + lane; b < L.nblk; b += 64) bl[cnt + b - nbp] = b;
+        if (lane == 0) {
+            L.bcnt[2 * u] = cnt;
+            L.bcnt[2 * u + 1] = cnt + max(0, L.nblk - nbp);
+        }
+    }
+}
+
 // Epilogue kernel of the split path: the retention policy on the scores the
 // step kernel wrote, and the merge of the splits' partial attention
 // (out = sum_s 2^(M_s - M) O_s / sum_s 2^(M_s - M) L_s); then the state goes
@@ -1234,23 +1370,47 @@ __global__ __launch_bounds__(256) void k_epilogue(LayerView L, StepIO io, double
 inline unsigned grid1d(size_t n, int block) { return (unsigned)((n + block - 1) / block); }
 
 // LDS of the step kernel: the queries in fp64, the attention wavefronts'
-// partial outputs, and the fused epilogue's slot arrays (with the per-head
-// bounds of the softmax aggregation)
-size_t step_lds(int G, int D, int S, int NW, bool fused, int agg) {
+// partial outputs, the fused epilogue's slot arrays (with the per-head
+// bounds of the softmax aggregation), and a block list
+size_t step_lds(int G, int D, int S, int NW, bool fused, int agg, int list_ints) {
     size_t b = (size_t)8 * G * qpad_row(D) + (size_t)NW * G * (D + 4) * 4;
     if (fused) b += (size_t)S * 20 + (agg ? (size_t)S * G * 8 + (size_t)G * 16 : 0);
-    return b;
+    return b + (size_t)list_ints * 4;
+}
+
+template <int D, int NW, bool AGG, bool LIST>
+void launch_step_inst(const LayerView& L, const StepIO& io, const StepPlan& pl, float sl2, double r,
+                      hipStream_t s) {
+    hipLaunchKernelGGL((k_step_bf16<D, NW, AGG, LIST>), dim3((unsigned)(L.U * pl.nsplit)), dim3(NW * 64), pl.lds,
+                       s, L, io, sl2, r, pl.fused ? 1 : 0);
 }
 
 template <int D, int NW>
 hipError_t launch_step_bf16(const LayerView& L, const StepIO& io, const StepPlan& pl, float sl2, double r,
                             hipStream_t s) {
-    const dim3 grid((unsigned)(L.U * pl.nsplit)), block(NW * 64);
-    if (L.agg)
-        hipLaunchKernelGGL((k_step_bf16<D, NW, true>), grid, block, pl.lds, s, L, io, sl2, r, pl.fused ? 1 : 0);
-    else
-        hipLaunchKernelGGL((k_step_bf16<D, NW, false>), grid, block, pl.lds, s, L, io, sl2, r, pl.fused ? 1 : 0);
+    const bool list = L.topk >= 0;
+    if (L.agg) {
+        if (list) launch_step_inst<D, NW, true, true>(L, io, pl, sl2, r, s);
+        else launch_step_inst<D, NW, true, false>(L, io, pl, sl2, r, s);
+    } else {
+        if (list) launch_step_inst<D, NW, false, true>(L, io, pl, sl2, r, s);
+        else launch_step_inst<D, NW, false, false>(L, io, pl, sl2, r, s);
+    }
     return hipGetLastError();
+}
+
+template <int D, int NW>
+hipError_t allow_lds_all(int bytes) {
+    hipError_t e = hipSuccess;
+    auto set = [&](const void* f) {
+        hipError_t r = hipFuncSetAttribute(f, hipFuncAttributeMaxDynamicSharedMemorySize, bytes);
+        if (r != hipSuccess) e = r;
+    };
+    set((const void*)k_step_bf16<D, NW, false, false>);
+    set((const void*)k_step_bf16<D, NW, true, false>);
+    set((const void*)k_step_bf16<D, NW, false, true>);
+    set((const void*)k_step_bf16<D, NW, true, true>);
+    return e;
 }
 
 }  // namespace
@@ -1258,7 +1418,7 @@ hipError_t launch_step_bf16(const LayerView& L, const StepIO& io, const StepPlan
 // ---------------------------------------------------------------------------
 
 StepPlan plan_step(int U, int G, int D, int S, int Lcap, int ps, int pinned, bool bf16, int agg,
-                   bool grouped, int split_override) {
+                   bool grouped, int list_ints, int split_override) {
     (void)pinned;
     (void)ps;
     StepPlan pl{};
@@ -1270,7 +1430,7 @@ StepPlan plan_step(int U, int G, int D, int S, int Lcap, int ps, int pinned, boo
     } else {
         pl.waves = 2;
         for (int nw : {8, 4, 2}) {
-            if (step_lds(G, D, S, nw, false, agg) <= kMaxLds) {
+            if (step_lds(G, D, S, nw, false, agg, list_ints) <= kMaxLds) {
                 pl.waves = nw;
                 break;
             }
@@ -1288,31 +1448,33 @@ StepPlan plan_step(int U, int G, int D, int S, int Lcap, int ps, int pinned, boo
     want = want > nblk ? nblk : want;
     pl.bps = (nblk + want - 1) / want;
     pl.nsplit = (nblk + pl.bps - 1) / pl.bps;
-    pl.fused = bf16 && !grouped && pl.nsplit == 1 && step_lds(G, D, S, pl.waves, true, agg) <= kMaxLds;
-    pl.lds = bf16 ? step_lds(G, D, S, pl.waves, pl.fused, agg) : 0;
+    pl.fused = bf16 && !grouped && pl.nsplit == 1 && step_lds(G, D, S, pl.waves, true, agg, list_ints) <= kMaxLds;
+    pl.lds = bf16 ? step_lds(G, D, S, pl.waves, pl.fused, agg, list_ints) : 0;
     return pl;
 }
 
 hipError_t allow_large_lds() {
     const int bytes = (int)kMaxLds;
     hipError_t e = hipSuccess;
-    auto set = [&](const void* f) {
+    for (hipError_t r : {allow_lds_all<128, 8>(bytes), allow_lds_all<128, 4>(bytes), allow_lds_all<128, 2>(bytes),
+                         allow_lds_all<64, 8>(bytes), allow_lds_all<64, 4>(bytes), allow_lds_all<64, 2>(bytes)})
+        if (r != hipSuccess) e = r;
+    for (const void* f : {(const void*)k_prompt_select<uint16_t>, (const void*)k_prompt_select<float>}) {
         hipError_t r = hipFuncSetAttribute(f, hipFuncAttributeMaxDynamicSharedMemorySize, bytes);
         if (r != hipSuccess) e = r;
-    };
-    set((const void*)k_step_bf16<128, 8, false>);
-    set((const void*)k_step_bf16<128, 4, false>);
-    set((const void*)k_step_bf16<128, 2, false>);
-    set((const void*)k_step_bf16<64, 8, false>);
-    set((const void*)k_step_bf16<64, 4, false>);
-    set((const void*)k_step_bf16<64, 2, false>);
-    set((const void*)k_step_bf16<128, 8, true>);
-    set((const void*)k_step_bf16<128, 4, true>);
-    set((const void*)k_step_bf16<128, 2, true>);
-    set((const void*)k_step_bf16<64, 8, true>);
-    set((const void*)k_step_bf16<64, 4, true>);
-    set((const void*)k_step_bf16<64, 2, true>);
+    }
     return e;
+}
+
+hipError_t launch_prompt_select(const LayerView& L, const StepIO& io, hipStream_t stream) {
+    const size_t esz = L.bf16 ? 2 : 4;
+    const size_t shm = 2 * (size_t)kSelChunk * (L.D * esz + 16) + (size_t)L.G * L.D * 8 + (size_t)L.dbase * 12 +
+                       (size_t)kSelChunk * L.G * 8;
+    if (L.bf16)
+        hipLaunchKernelGGL(k_prompt_select<uint16_t>, dim3(L.U), dim3(256), shm, stream, L, io);
+    else
+        hipLaunchKernelGGL(k_prompt_select<float>, dim3(L.U), dim3(256), shm, stream, L, io);
+    return hipGetLastError();
 }
 
 hipError_t launch_prefill(const LayerView& L, const void* k, const void* v, const PrefillIn& in, int max_tok,
@@ -1332,7 +1494,7 @@ hipError_t launch_prefill(const LayerView& L, const void* k, const void* v, cons
             hipLaunchKernelGGL(k_prefill_f32, dim3(grid1d(n, 256)), dim3(256), 0, stream, L, (const float*)k,
                                (const float*)v, in, max_tok);
         }
-        if (L.rank_pinned) {
+        if (L.rank_pinned || L.topk >= 0) {
             const int max_pages = (max_tok + L.ps - 1) / L.ps;
             const size_t n = (size_t)L.U * max_pages * L.D;
             if (L.bf16)

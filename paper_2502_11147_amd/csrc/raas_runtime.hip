@@ -35,7 +35,7 @@ raas_status hip_fail(hipError_t e, const char* what) {
     return fail(RAAS_E_HIP, "%s: %s", what, hipGetErrorString(e));
 }
 
-constexpr int kKernels = 2;  // step kernel, epilogue kernel
+constexpr int kKernels = 3;  // step kernel, epilogue kernel, prompt selection kernel
 constexpr size_t kProfRing = 8192;
 
 struct Timing {
@@ -60,6 +60,10 @@ struct raas_pool {
     int32_t* err = nullptr;
     float* part = nullptr;    // [U][splits][G][D+2], scratch of one step
     double* score = nullptr;  // [U][S] page scores, or [U][S][G] per-head bounds, scratch of one step
+    int32_t* fill_att = nullptr;  // [U][S] fills the attention sees (prompt selection), scratch of one step
+    int32_t* blist = nullptr;     // [U][Lcap/32] blocks a step visits (prompt selection), likewise
+    int32_t* bcnt = nullptr;      // [U][2]
+    int npr = 0;                  // prompt region's slots (0: none)
     int32_t* seqbuf = nullptr;   // [2][batch] prefill lengths and mask of a ragged prefill
     int32_t* seqhost = nullptr;  // pinned host staging of seqbuf
     hipEvent_t seq_copied = nullptr;  // recorded after the last staging copy
@@ -116,6 +120,13 @@ LayerView view(const raas_pool* p, int layer) {
     L.hgrp = p->cfg.decision_scope == RAAS_SCOPE_SEQUENCE ? p->cfg.n_kv_heads : 1;
     L.nkv = p->cfg.n_kv_heads;
     L.nblk = p->Lcap / kBlockTokens;
+    L.dbase = p->npr;
+    L.pcap = p->npr > 0 ? p->npr : p->S - 1;
+    L.topk = p->npr > 0 ? p->cfg.prompt_topk : -1;
+    L.fill_att = p->npr > 0 ? p->fill_att : L.fill;
+    L.blist = p->blist;
+    L.bcnt = p->bcnt;
+    L.lcap_blk = p->Lcap / kBlockTokens;
     return L;
 }
 
@@ -138,9 +149,19 @@ raas_status validate(const raas_config* c) {
     if (c->budget_tokens < 1 || c->budget_tokens % ps != 0)
         return fail(RAAS_E_INVALID, "budget_tokens (%d) must be a positive multiple of page_size (%d)",
                     c->budget_tokens, ps);
-    const int S = c->budget_tokens / ps;
+    if (c->prompt_tokens < 0 || c->prompt_tokens % ps != 0 || c->prompt_tokens % 32 != 0)
+        return fail(RAAS_E_INVALID, "prompt_tokens (%d) must be a non-negative multiple of page_size and of 32",
+                    c->prompt_tokens);
+    if (c->prompt_tokens > 0 && c->prompt_topk < 1)
+        return fail(RAAS_E_INVALID, "prompt_topk must be >= 1 with a prompt region (got %d)", c->prompt_topk);
+    if (c->prompt_tokens == 0 && c->prompt_topk != 0)
+        return fail(RAAS_E_INVALID, "prompt_topk needs a prompt region (prompt_tokens > 0)");
+    if (c->prompt_tokens > 0 && c->rank_pinned)
+        return fail(RAAS_E_INVALID, "rank_pinned does not combine with a prompt region");
+    const int S = (c->budget_tokens + c->prompt_tokens) / ps;
     if (S < 2 || S > 2048)
-        return fail(RAAS_E_INVALID, "budget_tokens / page_size = %d pages must lie in [2, 2048]", S);
+        return fail(RAAS_E_INVALID, "(budget_tokens + prompt_tokens) / page_size = %d pages must lie in [2, 2048]",
+                    S);
     if (c->dtype != RAAS_F32 && c->dtype != RAAS_BF16)
         return fail(RAAS_E_INVALID, "dtype must be RAAS_F32 or RAAS_BF16 (got %d)", c->dtype);
     if (!(c->r >= 0.0f && c->r <= 1.0f)) return fail(RAAS_E_INVALID, "r must lie in [0, 1]");
@@ -217,7 +238,8 @@ raas_status raas_create_pool(const raas_config* cfg, void* stream, raas_pool** o
     p->G = cfg->n_q_heads / cfg->n_kv_heads;
     p->D = cfg->head_dim;
     p->ps = cfg->page_size;
-    p->S = cfg->budget_tokens / cfg->page_size;
+    p->S = (cfg->budget_tokens + cfg->prompt_tokens) / cfg->page_size;
+    p->npr = cfg->prompt_tokens / cfg->page_size;
     p->Lcap = (p->S * p->ps + kBlockTokens - 1) / kBlockTokens * kBlockTokens;
     p->esz = cfg->dtype == RAAS_BF16 ? 2 : 4;
     p->kv_layer_elems = (size_t)p->U * p->Lcap * p->D;
@@ -246,6 +268,9 @@ raas_status raas_create_pool(const raas_config* cfg, void* stream, raas_pool** o
         {(void**)&p->score,
          (size_t)p->U * p->S * (cfg->score_aggregation == RAAS_SCORE_SOFTMAX_SUM ? p->G : 1) * sizeof(double)},
         {(void**)&p->seqbuf, 2 * (size_t)cfg->batch * sizeof(int32_t)},
+        {(void**)&p->fill_att, p->npr > 0 ? (size_t)p->U * p->S * sizeof(int32_t) : 4},
+        {(void**)&p->blist, p->npr > 0 ? (size_t)p->U * (p->Lcap / kBlockTokens) * sizeof(int32_t) : 4},
+        {(void**)&p->bcnt, p->npr > 0 ? (size_t)p->U * 2 * sizeof(int32_t) : 4},
     };
     hipStream_t s = (hipStream_t)stream;
     hipError_t ea = allow_large_lds();
@@ -292,7 +317,8 @@ void raas_destroy(raas_pool* p) {
         for (auto ev : t.start) hipEventDestroy(ev);
         for (auto ev : t.stop) hipEventDestroy(ev);
     }
-    void* ptrs[] = {p->K, p->V, p->kmin, p->kmax, p->meta, p->unit, p->err, p->part, p->score, p->seqbuf};
+    void* ptrs[] = {p->K,     p->V,     p->kmin,  p->kmax,     p->meta,  p->unit, p->err,
+                    p->part,  p->score, p->seqbuf, p->fill_att, p->blist, p->bcnt};
     for (void* q : ptrs)
         if (q) hipFree(q);
     if (p->seqhost) hipHostFree(p->seqhost);
@@ -308,12 +334,12 @@ raas_status raas_prefill(raas_pool* p, int32_t layer, const void* k, const void*
     if (prefill_len > 0 && (!k || !v)) return fail(RAAS_E_INVALID, "k or v is NULL");
     if (p->prefilled[layer]) return fail(RAAS_E_STATE, "layer %d was already prefilled", layer);
     const int pages = (prefill_len + p->ps - 1) / p->ps;
+    const int pcap = p->npr > 0 ? p->npr : p->S - 1;  // S-1: one slot stays for decode pages
     int keep = pages;
-    if (keep > p->S - 1) {
+    if (keep > pcap) {
         if (p->cfg.prefill_policy == RAAS_PREFILL_ERROR)
-            return fail(RAAS_E_BUDGET, "prefill needs %d pages but the budget leaves %d (S-1)", pages,
-                        p->S - 1);
-        keep = p->S - 1;
+            return fail(RAAS_E_BUDGET, "prefill needs %d pages but %d are available to it", pages, pcap);
+        keep = pcap;
     }
     hipStream_t s = (hipStream_t)stream;
     const PrefillIn in{nullptr, nullptr, prefill_len, prefill_len};
@@ -321,7 +347,7 @@ raas_status raas_prefill(raas_pool* p, int32_t layer, const void* k, const void*
     if (e != hipSuccess) return hip_fail(e, "prefill launch");
     p->prefilled[layer] = 1;
     p->pinned[layer] = keep;
-    p->keep_max[layer] = keep;
+    p->keep_max[layer] = std::max(keep, p->npr);  // decode pages start after the prompt region
     p->steps[layer] = 0;
     p->last_stream = s;
     return RAAS_OK;
@@ -343,11 +369,12 @@ raas_status raas_prefill_ragged(raas_pool* p, int32_t layer, const void* k, cons
         if (P < 0 || P > max_len)
             return fail(RAAS_E_INVALID, "prefill_lens[%d] = %d outside [0, max_len = %d]", b, P, max_len);
         const int pages = (P + p->ps - 1) / p->ps;
-        if (pages > p->S - 1 && p->cfg.prefill_policy == RAAS_PREFILL_ERROR)
-            return fail(RAAS_E_BUDGET, "sequence %d: prefill needs %d pages but the budget leaves %d (S-1)", b,
-                        pages, p->S - 1);
-        max_tok = std::max(max_tok, std::min(P, std::min(pages, p->S - 1) * p->ps));
-        keep_max = std::max(keep_max, std::min(pages, p->S - 1));
+        const int pcap = p->npr > 0 ? p->npr : p->S - 1;
+        if (pages > pcap && p->cfg.prefill_policy == RAAS_PREFILL_ERROR)
+            return fail(RAAS_E_BUDGET, "sequence %d: prefill needs %d pages but %d are available to it", b, pages,
+                        pcap);
+        max_tok = std::max(max_tok, std::min(P, std::min(pages, pcap) * p->ps));
+        keep_max = std::max(keep_max, std::max(std::min(pages, pcap), p->npr));
     }
     if (!p->prefilled[layer] && selected != B)
         return fail(RAAS_E_STATE, "the first prefill of layer %d must cover every sequence", layer);
@@ -412,7 +439,8 @@ raas_status raas_decode_step_masked(raas_pool* p, int32_t layer, const void* q, 
     L.nblk = (int)std::min<long long>(p->Lcap / kBlockTokens, (used * p->ps + kBlockTokens - 1) / kBlockTokens);
     const StepPlan pl = plan_step(p->U, p->G, p->D, p->S, L.nblk * kBlockTokens, p->ps, p->pinned[layer],
                                   p->cfg.dtype == RAAS_BF16, p->cfg.score_aggregation,
-                                  p->cfg.decision_scope == RAAS_SCOPE_SEQUENCE, p->split_override);
+                                  p->cfg.decision_scope == RAAS_SCOPE_SEQUENCE,
+                                  p->npr > 0 ? p->Lcap / kBlockTokens : 0, p->split_override);
     L.nsplit = pl.nsplit;
     L.bps = pl.bps;
     // Successive steps of a layer read its pool in opposite directions, so a
@@ -420,6 +448,12 @@ raas_status raas_decode_step_masked(raas_pool* p, int32_t layer, const void* q, 
     // to be still in the GPU's memory-side cache.
     L.rev = p->descending[layer];
 
+    if (p->npr > 0) {  // Quest on the prompt: which prompt pages this step attends to
+        prof_record(p, 2, true, s);
+        hipError_t e = launch_prompt_select(L, io, s);
+        prof_record(p, 2, false, s);
+        if (e != hipSuccess) return hip_fail(e, "prompt selection launch");
+    }
     prof_record(p, 0, true, s);
     hipError_t e = launch_step(L, io, pl, (double)p->cfg.r, s);
     prof_record(p, 0, false, s);

@@ -44,10 +44,12 @@ def to_device(a: np.ndarray, dtype: str):
     return t.cuda()
 
 
-def new_pool(w, splits=None, policy=None, aggregation=0, rank_pinned=False, scope=0):
+def new_pool(w, splits=None, policy=None, aggregation=0, rank_pinned=False, scope=0, prompt_tokens=0,
+             prompt_topk=0):
     import paper_2502_11147_amd as raas
 
-    kw = {"score_aggregation": aggregation, "rank_pinned": rank_pinned, "decision_scope": scope}
+    kw = {"score_aggregation": aggregation, "rank_pinned": rank_pinned, "decision_scope": scope,
+          "prompt_tokens": prompt_tokens, "prompt_topk": prompt_topk}
     if policy is not None:
         kw["prefill_policy"] = policy
     pool = raas.Pool.for_workload(w, **kw)
@@ -63,17 +65,21 @@ def unit_index(w, seq, kvh):
 def run_parity(w, seed: int, steps: int, layer: int = 0, units=None, out_every: int = 1,
                splits=None, chunk: int = 64, pool=None, prefill_len=None, check_invariants=True,
                report: ParityReport | None = None, aggregation: int = 0,
-               rank_pinned: bool = False, scope: int = 0) -> ParityReport:
+               rank_pinned: bool = False, scope: int = 0, prompt_tokens: int = 0,
+               prompt_topk: int = 0) -> ParityReport:
     """Runs `steps` decode steps of workload `w` on the GPU and checks the
     listed units (all when None) against the oracle. aggregation,
     rank_pinned and scope select the variants on both sides; with scope 1
     (one page table per sequence) every KV head of a listed unit's sequence
-    is checked, the oracle stepping each sequence's units together."""
+    is checked, the oracle stepping each sequence's units together.
+    prompt_tokens/prompt_topk select Quest on the prompt (a prompt region of
+    that many tokens, the top prompt_topk prompt pages attended per step)."""
     import torch
 
     rep = report or ParityReport()
-    B, Hq, Hkv, d, G, S, ps = (w.batch, w.n_q_heads, w.n_kv_heads, w.head_dim, w.group, w.slots,
-                               w.page_size)
+    B, Hq, Hkv, d, G, ps = w.batch, w.n_q_heads, w.n_kv_heads, w.head_dim, w.group, w.page_size
+    npr = prompt_tokens // ps
+    S = w.slots + npr
     U = B * Hkv
     P = w.prefill_len if prefill_len is None else prefill_len
     units = list(range(U)) if units is None else list(units)
@@ -82,13 +88,15 @@ def run_parity(w, seed: int, steps: int, layer: int = 0, units=None, out_every: 
     tol = TOL[w.dtype]
     own_pool = pool is None
     if own_pool:
-        pool = new_pool(w, splits, aggregation=aggregation, rank_pinned=rank_pinned, scope=scope)
+        pool = new_pool(w, splits, aggregation=aggregation, rank_pinned=rank_pinned, scope=scope,
+                        prompt_tokens=prompt_tokens, prompt_topk=prompt_topk)
     Kp, Vp = synth.prefill(w, seed, layer, prefill_len=P)
     pool.prefill(layer, to_device(Kp, w.dtype) if P else None, to_device(Vp, w.dtype) if P else None)
     orc = {}
     for u in units:
         b, h = divmod(u, Hkv)
-        m = oracle.Kvm(G, d, ps, S, r=w.r, aggregation=aggregation, rank_pinned=rank_pinned)
+        m = oracle.Kvm(G, d, ps, S, r=w.r, aggregation=aggregation, rank_pinned=rank_pinned,
+                       prompt_slots=npr if prompt_topk else None, prompt_topk=prompt_topk or None)
         rc = m.prefill(Kp[b, h].astype(np.float64), Vp[b, h].astype(np.float64))
         assert rc == 0, rc
         orc[u] = m
@@ -123,7 +131,7 @@ def run_parity(w, seed: int, steps: int, layer: int = 0, units=None, out_every: 
             want_out = (t % out_every == 0) or t == steps - 1
             rep.evictions += int(np.sum(ev_h[i] >= 0))
             if check_invariants:
-                _check_invariants(pt_h[i], ts_h[i], ev_h[i], clock, P, ps, S)
+                _check_invariants(pt_h[i], ts_h[i], ev_h[i], clock, P, ps, S, npr)
             for g in sorted(live):
                 members = groups[g]
                 if len(members) == 1:
@@ -180,9 +188,11 @@ def _victims(st, gpu_pt):
     return set(int(s) for s in np.nonzero((st["page_table"] == -1) | (gpu_pt == -1))[0])
 
 
-def _check_invariants(pt, ts, ev, clock, P, ps, S):
-    """Properties that hold for every unit at any size (Algorithm 1, Sections 3.1-3.3)."""
-    pinned = min(-(-P // ps), S - 1)
+def _check_invariants(pt, ts, ev, clock, P, ps, S, npr=0):
+    """Properties that hold for every unit at any size (Algorithm 1, Sections 3.1-3.3).
+    npr: slots of a prompt region (decode pages never enter it)."""
+    pinned = min(-(-P // ps), npr if npr else S - 1)
+    assert np.all(pt[:, pinned:npr] == -1), "a decode page in the prompt region"
     # prefill pages stay in slots 0..pinned-1 with their own ids and no timestamp
     assert np.all(pt[:, :pinned] == np.arange(pinned)[None, :]), "pinned pages moved"
     assert np.all(ts[:, :pinned] == -1)

@@ -67,6 +67,9 @@ BAD = [
     dict(prefill_policy=3), dict(score_aggregation=2), dict(score_aggregation=-1), dict(rank_pinned=2),
     dict(rank_pinned=-1), dict(decision_scope=2), dict(decision_scope=-1),
     dict(decision_scope=1, n_q_heads=2048, n_kv_heads=128),
+    dict(prompt_tokens=48, prompt_topk=2), dict(prompt_tokens=64, prompt_topk=0), dict(prompt_tokens=-32),
+    dict(prompt_topk=3), dict(prompt_tokens=64, prompt_topk=2, rank_pinned=1),
+    dict(prompt_tokens=32 * 1024, prompt_topk=2),
 ]
 
 

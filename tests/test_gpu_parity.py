@@ -404,3 +404,44 @@ def test_decode_sweep_shapes(name, steps, units):
         assert rep.evictions == 0
     else:
         assert rep.evictions > 0
+
+
+# Quest on the prompt pages, RaaS on the decode pages: a prompt region of
+# prompt_tokens tokens, the prompt_topk prompt pages of largest bound attended
+# each step (the oracle switched the same way).
+PROMPT_CASES = [
+    dict(prompt_tokens=128, prompt_topk=3, prefill_len=100),
+    dict(prompt_tokens=128, prompt_topk=3, prefill_len=1000),                      # prompt over the region
+    dict(prompt_tokens=128, prompt_topk=8, prefill_len=120),                       # every prompt page
+    dict(prompt_tokens=320, prompt_topk=5, prefill_len=300, budget=512, decode_steps=520, splits=3),
+    dict(prompt_tokens=256, prompt_topk=2, prefill_len=250, page_size=32, dtype="f32"),
+    dict(prompt_tokens=128, prompt_topk=1, prefill_len=128, page_size=64, budget=256),
+    dict(prompt_tokens=192, prompt_topk=4, prefill_len=190, n_q_heads=28, n_kv_heads=4),
+    dict(prompt_tokens=128, prompt_topk=3, prefill_len=100, aggregation=1),
+    dict(prompt_tokens=128, prompt_topk=3, prefill_len=100, scope=1),
+]
+
+
+@pytest.mark.parametrize("case", PROMPT_CASES, ids=[",".join("%s=%s" % kv for kv in c.items()) for c in PROMPT_CASES])
+def test_prompt_selection(case):
+    case = dict(case)
+    run_kw = {k: case.pop(k) for k in ("prompt_tokens", "prompt_topk", "splits", "aggregation", "scope") if k in case}
+    w = small(decode_steps=case.pop("decode_steps", 300), **case)
+    _say("case prompt-selection %s %s" % (case, run_kw))
+    rep = run_parity(w, seed=13, steps=w.decode_steps, **run_kw)
+    _report(rep, "prompt-selection")
+    assert rep.evictions > 0
+
+
+@pytest.mark.parametrize("name,topk,steps,units", [("llama8b-b128-ps32-L512", 8, 640, 8),
+                                                   ("llama8b-b128-ps32-L2048", 16, 2112, 4)])
+def test_prompt_selection_full_size(name, topk, steps, units):
+    """The long-prompt stress shapes (prompt 4096 tokens, page 32) with the
+    whole prompt kept in a prompt region, topk prompt pages attended per
+    step, and the decode budget run past full: sampled units."""
+    w = synth.get_workload(name)
+    _say("case prompt-selection %s topk %d steps %d" % (name, topk, steps))
+    rep = run_parity(w, seed=0, steps=steps, units=_sample_units(w, units), out_every=16, chunk=128,
+                     prompt_tokens=w.prefill_len, prompt_topk=topk)
+    _report(rep, name + " prompt-selection")
+    assert rep.evictions > 0
