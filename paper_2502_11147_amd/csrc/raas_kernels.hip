@@ -815,7 +815,9 @@ __global__ __launch_bounds__(NW * 64) __attribute__((amdgpu_waves_per_eu(1, 2)))
     const uint16_t* vn_g = (const uint16_t*)io.v_new + (size_t)u * D;
     const uint16_t* Ku = (const uint16_t*)L.K + (size_t)u * L.Lcap * D;
     const uint16_t* Vu = (const uint16_t*)L.V + (size_t)u * L.Lcap * D;
-    const int32_t* fu = L.fill_att + base;  // fills the attention sees
+    // fills the attention sees (the plain fill pointer where they are the
+    // same: read through it, the first block's fill arrives sooner)
+    const int32_t* fu = (LIST ? L.fill_att : L.fill) + base;
     auto load_block = [&](int b, u32x4 (&kr)[2][KS], u32x4 (&vr)[NB]) {
         const uint16_t* Kb = Ku + (size_t)b * BLK + lane * 8;
         const uint16_t* Vb = Vu + (size_t)b * BLK + lane * 8;
