@@ -23,6 +23,7 @@
 #include <math.h>
 
 #include <algorithm>
+#include <utility>
 
 #include "raas_internal.h"
 
@@ -1183,17 +1184,16 @@ __global__ __launch_bounds__(64) void k_step_f32(LayerView L, StepIO io, float s
 // Quest on the prompt pages (pools with a prompt region): for one unit, each
 // kept prompt page's representative bound against the step's queries, max
 // over the G heads of sum_c max(q_c kmax_c, q_c kmin_c) in fp64, channels
-// summed in order with one fused multiply-add each (the products are exact
-// in fp64, so each bound rounds exactly as a sequential sum); the topk pages
-// of largest bound, ties to the lower slot, are attended. Pages go through
-// LDS in chunks of kSelChunk (their kmin/kmax rows read with 16-byte loads,
-// rows padded against bank conflicts), one thread per (page, head). Writes
-// the fills the attention sees (0 for the other prompt pages) and the unit's
-// block list: the prompt blocks holding a chosen page, ascending, then every
-// block of the decode region. One workgroup of 256 threads per unit.
-constexpr int kSelChunk = 64;
-
-// element e of a 16-byte vector of T
+// summed in order; the topk pages of largest bound, ties to the lower slot,
+// are attended. One thread per page reads the page's kmin/kmax rows with
+// 16-byte loads and widens each key once for all heads; with q split into
+// q+ = max(q, 0) and q- = min(q, 0), a channel's term is
+// fma(q+, kmax, fma(q-, kmin, acc)): one of the two products is zero, which
+// adds exactly, and the other is exact in fp64, so each bound rounds as the
+// sequential sum does. Writes the fills the attention sees (0 for the other
+// prompt pages) and the unit's block list: the prompt blocks holding a
+// chosen page, ascending, then every block of the decode region. One
+// workgroup of 256 threads per unit.
 template <typename T>
 __device__ __forceinline__ float vec_elem(const u32x4& x, int e);
 template <>
@@ -1201,60 +1201,52 @@ __device__ __forceinline__ float vec_elem<uint16_t>(const u32x4& x, int e) { ret
 template <>
 __device__ __forceinline__ float vec_elem<float>(const u32x4& x, int e) { return __uint_as_float(x[e]); }
 
-template <typename T>
+// GQ: the query group size G, a compile-time constant so that the head loop
+// unrolls into straight-line fused multiply-adds.
+
+template <typename T, int GQ>
 __global__ __launch_bounds__(256) void k_prompt_select(LayerView L, StepIO io) {
     extern __shared__ __align__(16) unsigned char smem[];
     const int u = blockIdx.x, tid = threadIdx.x, lane = tid & 63, nth = blockDim.x;
     if (io.active != nullptr && io.active[u / L.nkv] == 0) return;
-    const int S = L.S, G = L.G, D = L.D, ps = L.ps, npr = L.dbase;
-    const int row = D + 16 / (int)sizeof(T);  // padded row of a staged key, in elements
+    constexpr int G = GQ;
+    const int S = L.S, D = L.D, ps = L.ps, npr = L.dbase;
     const size_t base = (size_t)u * S;
-    T* s_kx = reinterpret_cast<T*>(smem);                                // [kSelChunk][row], 16-byte rows
-    T* s_kn = s_kx + (size_t)kSelChunk * row;
-    double* s_q = reinterpret_cast<double*>(s_kn + (size_t)kSelChunk * row);  // [G][D]
-    double* s_b = s_q + (size_t)G * D;                                   // [npr] bounds
-    double* s_hb = s_b + npr;                                            // [kSelChunk][G] per-head bounds
-    int* s_sel = reinterpret_cast<int*>(s_hb + (size_t)kSelChunk * G);   // [npr] chosen
+    constexpr int V = 16 / sizeof(T);  // channels per 16-byte load
+    double2* s_qpm = reinterpret_cast<double2*>(smem);                 // [G][D] (q+, q-)
+    double* s_b = reinterpret_cast<double*>(s_qpm + (size_t)G * D);    // [npr] bounds
+    int* s_sel = reinterpret_cast<int*>(s_b + npr);                    // [npr] chosen
     const int kp = L.unit[(size_t)u * kUnitFields + kPinnedPages];
     const T* qg = (const T*)io.q + (size_t)u * G * D;
-    for (int i = tid; i < G * D; i += nth) s_q[i] = (double)to_f(qg[i]);
+    for (int i = tid; i < G * D; i += nth) {
+        const double q = (double)to_f(qg[i]);
+        s_qpm[i] = make_double2(q > 0.0 ? q : 0.0, q < 0.0 ? q : 0.0);
+    }
+    __syncthreads();
     const bool all = kp <= L.topk;
-    constexpr int V = 16 / sizeof(T);  // elements per 16-byte load
-    for (int c0 = 0; c0 < kp && !all; c0 += kSelChunk) {
-        const int n = min(kSelChunk, kp - c0);
-        __syncthreads();  // the previous chunk's keys and bounds are consumed
-        for (int i = tid; i < n * (D / V); i += nth) {
-            const int pp = i / (D / V), v = i - pp * (D / V);
-            const size_t g = (base + c0 + pp) * D + (size_t)v * V;
-            *reinterpret_cast<u32x4*>(s_kx + (size_t)pp * row + v * V) = ld4((const T*)L.kmax + g);
-            *reinterpret_cast<u32x4*>(s_kn + (size_t)pp * row + v * V) = ld4((const T*)L.kmin + g);
-        }
-        __syncthreads();
-        for (int i = tid; i < n * G; i += nth) {
-            const int pp = i / G, j = i - pp * G;
-            const T* kx = s_kx + (size_t)pp * row;
-            const T* kn = s_kn + (size_t)pp * row;
-            const double* qj = s_q + (size_t)j * D;
-            double a = 0.0;
-            // both keys are read (no load waits on q's sign); the sum stays in channel order
-#pragma unroll 2
-            for (int c = 0; c < D; c += V) {
-                const u32x4 xv = *reinterpret_cast<const u32x4*>(kx + c);
-                const u32x4 nv = *reinterpret_cast<const u32x4*>(kn + c);
+    for (int p = tid; p < kp && !all; p += nth) {
+        const T* kx = (const T*)L.kmax + (base + p) * D;
+        const T* kn = (const T*)L.kmin + (base + p) * D;
+        double acc[G];
 #pragma unroll
-                for (int e = 0; e < V; ++e) {
-                    const double qc = qj[c + e];
-                    a = fma(qc, (double)(qc > 0.0 ? vec_elem<T>(xv, e) : vec_elem<T>(nv, e)), a);
+        for (int j = 0; j < G; ++j) acc[j] = 0.0;
+#pragma unroll 4
+        for (int c = 0; c < D; c += V) {
+            const u32x4 xv = ld4(kx + c), nv = ld4(kn + c);
+#pragma unroll
+            for (int e = 0; e < V; ++e) {
+                const double hi = (double)vec_elem<T>(xv, e), lo = (double)vec_elem<T>(nv, e);
+#pragma unroll
+                for (int j = 0; j < G; ++j) {
+                    const double2 qpm = s_qpm[j * D + c + e];
+                    acc[j] = fma(qpm.x, hi, fma(qpm.y, lo, acc[j]));
                 }
             }
-            s_hb[i] = a;
         }
-        __syncthreads();
-        for (int pp = tid; pp < n; pp += nth) {
-            double best = -INFINITY;
-            for (int j = 0; j < G; ++j) best = fmax(best, s_hb[pp * G + j]);
-            s_b[c0 + pp] = best;
-        }
+        double best = -INFINITY;
+#pragma unroll
+        for (int j = 0; j < G; ++j) best = fmax(best, acc[j]);
+        s_b[p] = best;
     }
     __syncthreads();
     for (int p = tid; p < npr; p += nth) {
@@ -1461,21 +1453,28 @@ hipError_t allow_large_lds() {
     for (hipError_t r : {allow_lds_all<128, 8>(bytes), allow_lds_all<128, 4>(bytes), allow_lds_all<128, 2>(bytes),
                          allow_lds_all<64, 8>(bytes), allow_lds_all<64, 4>(bytes), allow_lds_all<64, 2>(bytes)})
         if (r != hipSuccess) e = r;
-    for (const void* f : {(const void*)k_prompt_select<uint16_t>, (const void*)k_prompt_select<float>}) {
-        hipError_t r = hipFuncSetAttribute(f, hipFuncAttributeMaxDynamicSharedMemorySize, bytes);
-        if (r != hipSuccess) e = r;
-    }
+
     return e;
 }
 
+template <typename T, int GQ>
+void launch_select_g(const LayerView& L, const StepIO& io, size_t shm, hipStream_t stream) {
+    hipLaunchKernelGGL((k_prompt_select<T, GQ>), dim3(L.U), dim3(256), shm, stream, L, io);
+}
+
+template <typename T, int... GS>
+void launch_select_t(const LayerView& L, const StepIO& io, size_t shm, hipStream_t stream,
+                     std::integer_sequence<int, GS...>) {
+    ((L.G == GS + 1 ? launch_select_g<T, GS + 1>(L, io, shm, stream) : void()), ...);
+}
+
 hipError_t launch_prompt_select(const LayerView& L, const StepIO& io, hipStream_t stream) {
-    const size_t esz = L.bf16 ? 2 : 4;
-    const size_t shm = 2 * (size_t)kSelChunk * (L.D * esz + 16) + (size_t)L.G * L.D * 8 + (size_t)L.dbase * 12 +
-                       (size_t)kSelChunk * L.G * 8;
+    // q split in two (16 B per element), the bounds and the chosen flags
+    const size_t shm = (size_t)L.G * L.D * 16 + (size_t)L.dbase * 12;
     if (L.bf16)
-        hipLaunchKernelGGL(k_prompt_select<uint16_t>, dim3(L.U), dim3(256), shm, stream, L, io);
+        launch_select_t<uint16_t>(L, io, shm, stream, std::make_integer_sequence<int, 16>{});
     else
-        hipLaunchKernelGGL(k_prompt_select<float>, dim3(L.U), dim3(256), shm, stream, L, io);
+        launch_select_t<float>(L, io, shm, stream, std::make_integer_sequence<int, 16>{});
     return hipGetLastError();
 }
 
