@@ -93,12 +93,15 @@ EDGE = [
     dict(dtype="f32", n_q_heads=14, n_kv_heads=2, head_dim=64, page_size=8, budget=96),
     dict(page_size=8, budget=2400, prefill_len=2300),             # 300 slots: the epilogue's radix select
     dict(page_size=8, budget=2400, prefill_len=2300, r=0.25),
+    dict(page_size=8, budget=16384, prefill_len=16000, decode_steps=80),  # 2048 slots, the most a pool has
+    dict(n_q_heads=32, n_kv_heads=2, head_dim=64, page_size=128, budget=1024, prefill_len=300),  # G 16, d 64, page 128
 ]
 
 
 @pytest.mark.parametrize("edge", EDGE, ids=[",".join("%s=%s" % kv for kv in e.items()) for e in EDGE])
 def test_edge_cases(edge):
-    w = small(decode_steps=200, **edge)
+    edge = dict(edge)
+    w = small(decode_steps=edge.pop("decode_steps", 200), **edge)
     _say("case edge %s" % edge)
     rep = run_parity(w, seed=5, steps=w.decode_steps)
     _report(rep, "edge")
@@ -295,6 +298,7 @@ VARIANT_CASES = [
     dict(prefill_len=0),                                            # nothing pinned
     dict(head_dim=64, page_size=8, budget=64, prefill_len=21),
     dict(page_size=8, budget=2400, prefill_len=2300),               # 300 slots, radix select
+    dict(page_size=8, budget=16384, prefill_len=16000, decode_steps=60),  # 2048 slots, 2047 of them pinned
 ]
 
 
