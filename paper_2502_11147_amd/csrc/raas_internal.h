@@ -57,6 +57,7 @@ struct LayerView {
     int32_t* blist;     // [U][lcap_blk] blocks a step visits (topk >= 0): chosen prompt blocks, decode blocks
     int32_t* bcnt;      // [U][2] prompt blocks and all blocks in blist
     int lcap_blk;       // Lcap / 32
+    int nt;             // 1: K/V blocks streamed with non-temporal loads
 };
 
 // Prefill input of one layer: `stride` token rows per unit; per-sequence

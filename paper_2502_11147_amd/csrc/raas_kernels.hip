@@ -760,7 +760,9 @@ __device__ __forceinline__ void attend_block(const u32x4 (&kr)[2][D / 32], const
 // that the default one carries none of its registers).
 // LIST: the blocks come from the unit's block list (the prompt blocks the
 // selection kernel chose, then the decode region's), not from a range.
-template <int D, int NW, bool AGG, bool LIST>
+// NT: K/V blocks are read with non-temporal loads (pools too large for the
+// memory-side cache to serve the next step).
+template <int D, int NW, bool AGG, bool LIST, bool NT = false>
 __global__ __launch_bounds__(NW * 64) __attribute__((amdgpu_waves_per_eu(1, 2))) void k_step_bf16(
     LayerView L, StepIO io, float scale_log2, double r, int fused) {
     constexpr int KS = D / 32, NB = D / 16, BLK = 32 * D;
@@ -819,15 +821,19 @@ __global__ __launch_bounds__(NW * 64) __attribute__((amdgpu_waves_per_eu(1, 2)))
     // fills the attention sees (the plain fill pointer where they are the
     // same: read through it, the first block's fill arrives sooner)
     const int32_t* fu = (LIST ? L.fill_att : L.fill) + base;
+    auto ldb = [&](const uint16_t* p) {
+        if constexpr (NT) return __builtin_nontemporal_load(reinterpret_cast<const u32x4*>(p));
+        else return ld4(p);
+    };
     auto load_block = [&](int b, u32x4 (&kr)[2][KS], u32x4 (&vr)[NB]) {
         const uint16_t* Kb = Ku + (size_t)b * BLK + lane * 8;
         const uint16_t* Vb = Vu + (size_t)b * BLK + lane * 8;
 #pragma unroll
         for (int qq = 0; qq < 2; ++qq)
 #pragma unroll
-            for (int ks = 0; ks < KS; ++ks) kr[qq][ks] = ld4(Kb + (qq * KS + ks) * 512);
+            for (int ks = 0; ks < KS; ++ks) kr[qq][ks] = ldb(Kb + (qq * KS + ks) * 512);
 #pragma unroll
-        for (int nb = 0; nb < NB; ++nb) vr[nb] = ld4(Vb + nb * 512);
+        for (int nb = 0; nb < NB; ++nb) vr[nb] = ldb(Vb + nb * 512);
     };
 
     // Loads complete in issue order, so the small reads go out first: the
@@ -1372,11 +1378,11 @@ size_t step_lds(int G, int D, int S, int NW, bool fused, int agg, int list_ints)
     return b + (size_t)list_ints * 4;
 }
 
-template <int D, int NW, bool AGG, bool LIST>
+template <int D, int NW, bool AGG, bool LIST, bool NT = false>
 void launch_step_inst(const LayerView& L, const StepIO& io, const StepPlan& pl, float sl2, double r,
                       hipStream_t s) {
-    hipLaunchKernelGGL((k_step_bf16<D, NW, AGG, LIST>), dim3((unsigned)(L.U * pl.nsplit)), dim3(NW * 64), pl.lds,
-                       s, L, io, sl2, r, pl.fused ? 1 : 0);
+    hipLaunchKernelGGL((k_step_bf16<D, NW, AGG, LIST, NT>), dim3((unsigned)(L.U * pl.nsplit)), dim3(NW * 64),
+                       pl.lds, s, L, io, sl2, r, pl.fused ? 1 : 0);
 }
 
 template <int D, int NW>
@@ -1388,6 +1394,7 @@ hipError_t launch_step_bf16(const LayerView& L, const StepIO& io, const StepPlan
         else launch_step_inst<D, NW, true, false>(L, io, pl, sl2, r, s);
     } else {
         if (list) launch_step_inst<D, NW, false, true>(L, io, pl, sl2, r, s);
+        else if (L.nt) launch_step_inst<D, NW, false, false, true>(L, io, pl, sl2, r, s);
         else launch_step_inst<D, NW, false, false>(L, io, pl, sl2, r, s);
     }
     return hipGetLastError();
@@ -1404,6 +1411,7 @@ hipError_t allow_lds_all(int bytes) {
     set((const void*)k_step_bf16<D, NW, true, false>);
     set((const void*)k_step_bf16<D, NW, false, true>);
     set((const void*)k_step_bf16<D, NW, true, true>);
+    set((const void*)k_step_bf16<D, NW, false, false, true>);
     return e;
 }
 

@@ -64,6 +64,7 @@ struct raas_pool {
     int32_t* blist = nullptr;     // [U][Lcap/32] blocks a step visits (prompt selection), likewise
     int32_t* bcnt = nullptr;      // [U][2]
     int npr = 0;                  // prompt region's slots (0: none)
+    int nt = 0;                   // K/V blocks streamed with non-temporal loads
     int32_t* seqbuf = nullptr;   // [2][batch] prefill lengths and mask of a ragged prefill
     int32_t* seqhost = nullptr;  // pinned host staging of seqbuf
     hipEvent_t seq_copied = nullptr;  // recorded after the last staging copy
@@ -127,6 +128,7 @@ LayerView view(const raas_pool* p, int layer) {
     L.blist = p->blist;
     L.bcnt = p->bcnt;
     L.lcap_blk = p->Lcap / kBlockTokens;
+    L.nt = p->nt;
     return L;
 }
 
@@ -250,6 +252,12 @@ raas_status raas_create_pool(const raas_config* cfg, void* stream, raas_pool** o
     p->keep_max.assign((size_t)cfg->n_layers, 0);
     p->steps.assign((size_t)cfg->n_layers, 0);
     p->descending.assign((size_t)cfg->n_layers, 0);
+    // A step reads a layer's whole pool; the same layer comes round again
+    // after every layer's pool has been read. When all of them exceed twice
+    // the memory-side cache (256 MB), nothing of a step's reads is left there
+    // for the next: the blocks are then read with non-temporal loads, which
+    // stream faster. Smaller pools keep ordinary loads and the cache's reuse.
+    p->nt = 2.0 * (double)cfg->n_layers * p->U * p->Lcap * p->D * p->esz > 2.0 * 256e6 ? 1 : 0;
     const size_t Ly = (size_t)cfg->n_layers;
     const int nblk = p->Lcap / kBlockTokens;
     const int max_split = nblk < kMaxSplits ? nblk : kMaxSplits;
