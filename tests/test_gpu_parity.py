@@ -315,15 +315,17 @@ def test_score_variants(agg, rank, case):
     assert rep.flagged_divergences <= rep.units_checked // 2
 
 
-@pytest.mark.parametrize("name,steps,units", [("llama8b-b32-L2048", 1024 + 320, 6),
-                                              ("llama8b-b1-L1024", 1024, 8)])
-def test_score_variants_full_size(name, steps, units):
+@pytest.mark.parametrize("name,steps,units,splits", [("llama8b-b32-L2048", 1024 + 320, 6, None),
+                                                     ("llama8b-b1-L1024", 1024, 8, None),
+                                                     ("llama8b-b1-L1024", 1024, 8, 4)])
+def test_score_variants_full_size(name, steps, units, splits):
     """Both variants together at full size, in the benchmark's launch
-    configuration (llama8b-b1 runs split over several workgroups)."""
+    configuration (one fused workgroup per unit for both), and llama8b-b1
+    split over 4 workgroups per unit (the epilogue kernel)."""
     w = synth.get_workload(name)
-    _say("case variant agg 1 rank_pinned 1 %s steps %d" % (name, steps))
+    _say("case variant agg 1 rank_pinned 1 %s steps %d splits %s" % (name, steps, splits))
     rep = run_parity(w, seed=1, steps=steps, units=_sample_units(w, units), out_every=32, chunk=128,
-                     aggregation=1, rank_pinned=True)
+                     aggregation=1, rank_pinned=True, splits=splits)
     _report(rep, name + " variant")
     assert rep.evictions > 0
 
