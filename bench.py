@@ -392,13 +392,14 @@ def main():
     run(fill, args.warmup)
     torch.cuda.synchronize()
 
-    # one kernel per step (the step kernel runs the epilogue) or two?
-    pool.profile(1 << KERNEL_EPILOGUE)
+    # one kernel per step (the step kernel runs the epilogue and, with a
+    # prompt region, the selection) or more?
+    pool.profile((1 << KERNEL_EPILOGUE) | (1 << KERNEL_SELECT))
     run(fill + args.warmup, 1)
     fused = pool.profile_read(KERNEL_EPILOGUE)[1] == 0
     # the event span times the step kernel alone only when it is the step's
-    # only launch (prompt selection adds a kernel in front)
-    alone = fused and npr == 0
+    # only launch (a separate prompt selection adds a kernel in front)
+    alone = fused and pool.profile_read(KERNEL_SELECT)[1] == 0
     pool.profile(0)
     t_start = fill + args.warmup + 1
     st = pool.export_state(0)

@@ -85,11 +85,13 @@ struct StepPlan {
     int waves;       // wavefronts per step workgroup (bf16)
     int nsplit, bps; // splits per unit and blocks per split
     bool fused;      // true: the step workgroup also runs the epilogue (nsplit == 1, bf16)
+    bool select_in_step;  // true: the step kernel chooses the prompt pages (no selection kernel)
     size_t lds;      // dynamic LDS of the step kernel
 };
 
 // grouped: retention decided per group of units, by the epilogue kernel;
-// list_ints: LDS entries of a block list (0 without prompt selection)
+// list_ints: LDS ints of a block list or of the in-step prompt selection (0
+// without a prompt region)
 StepPlan plan_step(int U, int G, int D, int S, int Lcap, int ps, int pinned, bool bf16, int agg,
                    bool grouped, int list_ints, int split_override);
 // Quest on the prompt pages: the attended fills and the block list of a step.

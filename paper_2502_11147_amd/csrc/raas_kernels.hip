@@ -452,22 +452,23 @@ __device__ void evict_wave(const LayerView& L, const UnitRec& ur, int* s_state, 
 
 __device__ void retention_wave(const LayerView& L, const UnitRec& ur, double r, const double* s_score,
                                int* s_state, int* s_ts, const int* s_lid, RetShared& out) {
-    const int S = L.S, lane = threadIdx.x & 63;
+    // slots below the decode base (a prompt region) are never ranked
+    const int S = L.S, lane = threadIdx.x & 63, s_lo = L.dbase;
     int n = 0;
-    for (int s0 = 0; s0 < S; s0 += 64) {
+    for (int s0 = s_lo; s0 < S; s0 += 64) {
         const int s = s0 + lane;
         const int st = s < S ? s_state[s] : -1;
         n += __popcll(__ballot(st >= 0 && ranked(L, st)));
     }
     const int k = (int)floor(r * (double)n);
     if (k > 0) {
-        for (int s0 = 0; s0 < S; s0 += 64) {
+        for (int s0 = s_lo; s0 < S; s0 += 64) {
             const int p = s0 + lane;
             if (p < S && s_state[p] == kEvictable) {
                 const double sp = s_score[p];
                 int less = 0;
 #pragma unroll 8
-                for (int o = 0; o < S; ++o) less += s_score[o] < sp;
+                for (int o = s_lo; o < S; ++o) less += s_score[o] < sp;
                 if (less >= n - k) s_ts[p] = ur.clock;
             }
         }
@@ -490,7 +491,7 @@ __device__ void evict_wave(const LayerView& L, const UnitRec& ur, int* s_state, 
     int victim = -1;
     if (full) {
         unsigned long long best = ~0ull;
-        for (int s0 = 0; s0 < S; s0 += 64) {
+        for (int s0 = L.dbase; s0 < S; s0 += 64) {  // no decode page lies below the decode base
             const int s = s0 + lane;
             if (s < S && s_state[s] == kEvictable) {
                 const unsigned long long key = ((unsigned long long)(uint32_t)s_ts[s] << 32) | (uint32_t)s_lid[s];
@@ -502,7 +503,7 @@ __device__ void evict_wave(const LayerView& L, const UnitRec& ur, int* s_state, 
             const unsigned long long o = __shfl_xor(best, off);
             best = o < best ? o : best;
         }
-        for (int s0 = 0; s0 < S; s0 += 64) {
+        for (int s0 = L.dbase; s0 < S; s0 += 64) {
             const int s = s0 + lane;
             const bool hit = s < S && s_state[s] == kEvictable &&
                              (uint32_t)s_lid[s] == (uint32_t)(best & 0xFFFFFFFFull);
@@ -758,12 +759,16 @@ __device__ __forceinline__ void attend_block(const u32x4 (&kr)[2][D / 32], const
 
 // AGG: the softmax aggregation of the page scores (a separate instance, so
 // that the default one carries none of its registers).
-// LIST: the blocks come from the unit's block list (the prompt blocks the
-// selection kernel chose, then the decode region's), not from a range.
+// LM, pools with a prompt region (Quest on the prompt): 1, the blocks come
+// from the unit's block list (the prompt blocks the selection kernel chose,
+// then the decode region's); 2, the workgroup covers the unit and selects the
+// prompt pages itself: its score passes also compute the kept prompt pages'
+// bounds, it streams the decode blocks first, and after the score barrier it
+// picks the top k and claims their blocks. 0: no prompt region.
 // NT: K/V blocks are read with non-temporal loads (pools too large for the
 // memory-side cache to serve the next step).
-template <int D, int NW, bool AGG, bool LIST, bool NT = false>
-__global__ __launch_bounds__(NW * 64) __attribute__((amdgpu_waves_per_eu(1, 2))) void k_step_bf16(
+template <int D, int NW, bool AGG, int LM, bool NT = false>
+__global__ __launch_bounds__(NW * 64) __attribute__((amdgpu_waves_per_eu(2, 2))) void k_step_bf16(
     LayerView L, StepIO io, float scale_log2, double r, int fused) {
     constexpr int KS = D / 32, NB = D / 16, BLK = 32 * D;
     extern __shared__ __align__(16) unsigned char smem[];
@@ -771,6 +776,7 @@ __global__ __launch_bounds__(NW * 64) __attribute__((amdgpu_waves_per_eu(1, 2)))
     __shared__ float s_l[NW][16];
     __shared__ RetShared ret;
     __shared__ int s_next;  // next unclaimed block index
+    __shared__ int s_nsel;  // LM 2: prompt blocks chosen
     __shared__ __align__(16) uint16_t s_kn[D];  // the new token's key and value, staged so that
     __shared__ __align__(16) uint16_t s_vn[D];  // no read in the block loop waits on memory
 
@@ -783,7 +789,12 @@ __global__ __launch_bounds__(NW * 64) __attribute__((amdgpu_waves_per_eu(1, 2)))
     int* s_state = reinterpret_cast<int*>(s_mz + (AGG ? 2 * G : 0));  // [S], fused only
     int* s_ts = s_state + S;
     int* s_lid = s_ts + S;
-    int* s_list = fused ? s_lid + S : reinterpret_cast<int*>(s_score);  // LIST: this workgroup's blocks
+    int* s_list = fused ? s_lid + S : reinterpret_cast<int*>(s_score);  // LM 1: this workgroup's blocks
+    // LM 2: the prompt pages' bounds and attended fills, the chosen prompt blocks
+    double* s_pb = reinterpret_cast<double*>(  // [dbase], 16-byte aligned (the smem base is)
+        reinterpret_cast<int*>(smem) + ((s_lid + S - reinterpret_cast<int*>(smem) + 3) & ~3));
+    int* s_fatt = reinterpret_cast<int*>(s_pb + L.dbase);          // [dbase]
+    int* s_plist = s_fatt + L.dbase;                               // [dbase * ps / 32]
 
     const int tid = threadIdx.x, lane = tid & 63, w = tid >> 6;
     const int grp = lane >> 4, col = lane & 15;
@@ -795,12 +806,17 @@ __global__ __launch_bounds__(NW * 64) __attribute__((amdgpu_waves_per_eu(1, 2)))
     // (LIST) entries of its block list; pages scored here: those whose first
     // row lies in blocks sb0 .. sb1-1
     int lo, hi, sb0, sb1;
-    if constexpr (LIST) {
+    const int nbp = LM ? L.dbase * ps / 32 : 0;  // LM: the decode region starts at this block
+    if constexpr (LM == 2) {
+        lo = 0;
+        hi = L.nblk - nbp;  // decode blocks, claimed first; claims beyond are prompt blocks
+        sb0 = 0;            // score passes: every page (the prompt's bounds, the decode pages' scores)
+        sb1 = L.nblk;
+    } else if constexpr (LM == 1) {
         const int nsel = L.bcnt[2 * u], ntot = L.bcnt[2 * u + 1];
         const int per = (ntot + nsplit - 1) / nsplit;
         lo = min(ntot, split * per);
         hi = min(ntot, lo + per);
-        const int nbp = L.dbase * ps / 32;  // the decode region starts at this block
         sb0 = nbp + max(lo, nsel) - nsel;
         sb1 = nbp + max(hi, nsel) - nsel;
         for (int i = tid; i < hi - lo; i += NW * 64) s_list[i] = L.blist[(size_t)u * L.lcap_blk + lo + i];
@@ -812,7 +828,9 @@ __global__ __launch_bounds__(NW * 64) __attribute__((amdgpu_waves_per_eu(1, 2)))
         sb1 = hi;
     }
     const int nown = hi - lo;                  // claims of this workgroup
-    const int bend = LIST ? 0x40000000 : hi;   // no block: every block index lies below
+    const int bend = LM ? 0x40000000 : hi;     // no block: every block index lies below
+    // LM 2: a claim of prompt block index i before the selection is held as -(i+1)
+    auto real = [&](int x) { return (LM != 2 || x >= 0) && x < bend; };
     const uint16_t* qg = (const uint16_t*)io.q + (size_t)u * G * D;
     const uint16_t* kn_g = (const uint16_t*)io.k_new + (size_t)u * D;
     const uint16_t* vn_g = (const uint16_t*)io.v_new + (size_t)u * D;
@@ -820,7 +838,7 @@ __global__ __launch_bounds__(NW * 64) __attribute__((amdgpu_waves_per_eu(1, 2)))
     const uint16_t* Vu = (const uint16_t*)L.V + (size_t)u * L.Lcap * D;
     // fills the attention sees (the plain fill pointer where they are the
     // same: read through it, the first block's fill arrives sooner)
-    const int32_t* fu = (LIST ? L.fill_att : L.fill) + base;
+    const int32_t* fu = (LM == 1 ? L.fill_att : L.fill) + base;
     auto ldb = [&](const uint16_t* p) {
         if constexpr (NT) return __builtin_nontemporal_load(reinterpret_cast<const u32x4*>(p));
         else return ld4(p);
@@ -846,12 +864,13 @@ __global__ __launch_bounds__(NW * 64) __attribute__((amdgpu_waves_per_eu(1, 2)))
     // claim index i of the own blocks, ascending or (L.rev) descending
     auto blk_of = [&](int i) {
         const int j = L.rev ? nown - 1 - i : i;
-        if constexpr (LIST) return s_list[j];
+        if constexpr (LM == 1) return s_list[j];
+        else if constexpr (LM == 2) return nbp + j;
         else return lo + j;
     };
-    int b = (w < nown) ? blk_of(w) : bend;
+    int b = (w < nown) ? blk_of(w) : (LM == 2 ? -(w + 1) : bend);
     const int slot_first = (32 * b + 8 * grp) / ps;
-    const int fill_first = (b < bend && slot_first < S) ? fu[slot_first] : 0;
+    const int fill_first = (real(b) && slot_first < S) ? fu[slot_first] : 0;
     // unconditional (clamped) reads: a read under a branch draws its first
     // use into the branch, with a wait for it ahead of the block loads
     const uint16_t q_first = qg[tid < G * D ? tid : 0];
@@ -866,21 +885,33 @@ __global__ __launch_bounds__(NW * 64) __attribute__((amdgpu_waves_per_eu(1, 2)))
         qv[ks] = __builtin_bit_cast(bf16x8, x);
     }
     u32x4 kr_next[2][KS], vr_next[NB];
-    if (b < bend) load_block(b, kr_next, vr_next);
+    if (real(b)) load_block(b, kr_next, vr_next);
 
     const int ns = ur.ns, nf = ur.nf;
     const bool opened = ur.opened();
     const int row_new = ns * ps + nf, b_new = row_new >> 5, tt_new = row_new & 31;
-    // the block of claim index i, or bend when none is left
-    auto take = [&](int i) { return i < nown ? blk_of(i) : bend; };
+    bool decided = false;  // this wavefront has passed the score barrier
+    // the block of claim index i, or bend when none is left (LM 2: a prompt
+    // block not chosen yet is held as -(i+1))
+    auto take = [&](int i) {
+        if constexpr (LM == 2) {
+            if (i < nown) return blk_of(i);
+            if (!decided) return -(i + 1);
+            return i - nown < s_nsel ? s_plist[i - nown] : bend;
+        } else {
+            return i < nown ? blk_of(i) : bend;
+        }
+    };
     // pages scored here: those whose first row lies in this workgroup's blocks, pinned ones
-    // excepted unless they are ranked
-    const int sl0 = max(L.rank_pinned ? 0 : pinned, min(S, (32 * sb0 + ps - 1) / ps));
+    // excepted unless they are ranked (LM 2: the kept prompt pages are bounded too)
+    const int sl0 = LM == 2 ? 0 : max(L.rank_pinned ? 0 : pinned, min(S, (32 * sb0 + ps - 1) / ps));
     const int sl1 = min(S, (32 * sb1 + ps - 1) / ps);
 
     // fill of the page holding this lane's 8 rows of block b (page_size % 8 == 0)
     auto row_fill = [&](int b) {
         const int slot = (32 * b + 8 * grp) / ps;
+        if constexpr (LM == 2)
+            if (slot < L.dbase) return s_fatt[slot];  // read only once the prompt pages are chosen
         return (slot < S) ? (slot == ns ? nf + 1 : fu[slot]) : 0;
     };
     auto valid_rows = [&](int b, int f) {
@@ -888,7 +919,7 @@ __global__ __launch_bounds__(NW * 64) __attribute__((amdgpu_waves_per_eu(1, 2)))
         return min(max(f - (t0 - (t0 / ps) * ps), 0), 8);
     };
     int f_next = 0;
-    if (b < bend) f_next = (w < nown) ? (slot_first < S ? (slot_first == ns ? nf + 1 : fill_first) : 0) : row_fill(b);
+    if (real(b)) f_next = (w < nown) ? (slot_first < S ? (slot_first == ns ? nf + 1 : fill_first) : 0) : row_fill(b);
 
     // staging for the scores and the epilogue
     if (tid < G * D) s_qd[qpad_index<D>(tid)] = (double)bf2f(q_first);
@@ -920,7 +951,9 @@ __global__ __launch_bounds__(NW * 64) __attribute__((amdgpu_waves_per_eu(1, 2)))
         const int g = pass * NW + w;
         return sl0 + 8 * (L.rev ? ngroups - 1 - g : g) + (lane >> 3);
     };
-    auto pass_act = [&](int p) { return p < sl1 && (p == ns || ranked(L, L.state[base + p])); };
+    auto pass_act = [&](int p) {
+        return p < sl1 && (p == ns || ranked(L, L.state[base + p]) || (LM == 2 && p < pinned));
+    };
     const int npass = (sl1 - sl0 - 8 * w > 0) ? (sl1 - sl0 - 8 * w + 8 * NW - 1) / (8 * NW) : 0;
     const int npass_all = (sl1 - sl0 + 8 * NW - 1) / (8 * NW);  // passes of wavefront 0, the most
     int pass = 0;
@@ -931,7 +964,8 @@ __global__ __launch_bounds__(NW * 64) __attribute__((amdgpu_waves_per_eu(1, 2)))
         double* hb = (AGG && act_cur) ? (fused ? s_hb : L.score + base * G) + (size_t)p * G : nullptr;
         const double sc = score_finish<D>(L, u, p, part, act_cur, frag, p == ns, opened, s_kn, s_qd, hb);
         if (act_cur && part == 0 && !AGG) {
-            if (fused) s_score[p] = sc;
+            if (LM == 2 && p < L.dbase) s_pb[p] = sc;  // a prompt page: a bound for the selection
+            else if (fused) s_score[p] = sc;
             else L.score[base + p] = sc;
         }
         ++pass;
@@ -941,10 +975,47 @@ __global__ __launch_bounds__(NW * 64) __attribute__((amdgpu_waves_per_eu(1, 2)))
             score_issue<D>(L, u, pn, part, act_cur && !(pn == ns && opened), frag);
         }
     };
-    // retention policy once every wavefront's scores are in LDS
-    bool decided = false;
+    // retention policy once every wavefront's scores are in LDS (LM 2: and
+    // the prompt pages chosen, which needs two more barriers)
     auto scores_done = [&]() {
         lds_barrier();
+        if constexpr (LM == 2) {
+            // the topk kept prompt pages of largest bound, ties to the lower slot
+            const bool all = pinned <= L.topk;
+            for (int p = tid; p < L.dbase; p += NW * 64) {
+                bool sel = p < pinned;
+                if (sel && !all) {
+                    // pages ranked above p: larger bounds, and equal ones at lower slots (two
+                    // per 16-byte read, four reads in flight; a read past the last kept page
+                    // stays inside the workgroup's LDS and is not counted)
+                    const double bp = s_pb[p];
+                    int above = 0;
+#pragma unroll 4
+                    for (int o = 0; o < pinned; o += 2) {
+                        const double2 x = *reinterpret_cast<const double2*>(s_pb + o);
+                        above += (x.x > bp || (x.x == bp && o < p)) ? 1 : 0;
+                        above += (o + 1 < pinned && (x.y > bp || (x.y == bp && o + 1 < p))) ? 1 : 0;
+                    }
+                    sel = above < L.topk;
+                }
+                s_fatt[p] = sel ? fu[p] : 0;  // kept pages hold at least one token
+            }
+            lds_barrier();
+            if (w == 0) {  // the prompt blocks holding a chosen page, ascending
+                int cnt = 0;
+                for (int c0 = 0; c0 < nbp; c0 += 64) {
+                    const int bb = c0 + lane;
+                    bool any = false;
+                    if (bb < nbp)
+                        for (int sl = 32 * bb / ps; sl <= (32 * bb + 31) / ps; ++sl) any = any || s_fatt[sl] > 0;
+                    const unsigned long long m = __ballot(any);
+                    if (any) s_plist[cnt + __popcll(m & ((1ull << lane) - 1ull))] = bb;
+                    cnt += __popcll(m);
+                }
+                if (lane == 0) s_nsel = cnt;
+            }
+            lds_barrier();
+        }
         if (AGG && fused) softmax_sum_block(L, s_hb, 1, s_state, s_score, s_mz, tid, NW * 64);
         if (fused && w == 0) retention_wave(L, ur, r, s_score, s_state, s_ts, s_lid, ret);
         decided = true;
@@ -958,6 +1029,30 @@ __global__ __launch_bounds__(NW * 64) __attribute__((amdgpu_waves_per_eu(1, 2)))
             score_issue<D>(L, u, p, part, act_cur && !(p == ns && opened), frag);
         }
     };
+    bool staged_done = false;  // LM 2: staged() has run (a held claim runs it early)
+    // LM 2: a claim held for the selection: this wavefront finishes its score
+    // passes, passes the score barrier (every wavefront holds one claim when
+    // it gets there: the decode blocks come first), then takes the chosen
+    // prompt block the claim stands for
+    auto resolve = [&](int x) {
+        if (!staged_done) {
+            staged();
+            staged_done = true;
+        }
+        while (pass < npass) score_step();
+        scores_done();
+        const int i = -x - 1 - nown;
+        return i < s_nsel ? s_plist[i] : bend;
+    };
+    if constexpr (LM == 2) {
+        if (b < 0) {  // no decode block for this wavefront (loaded late, after the staging)
+            b = resolve(b);
+            if (b < bend) {
+                f_next = row_fill(b);
+                load_block(b, kr_next, vr_next);
+            }
+        }
+    }
     int it = 0;
     while (b < bend) {
         const int f_cur = f_next;
@@ -971,6 +1066,8 @@ __global__ __launch_bounds__(NW * 64) __attribute__((amdgpu_waves_per_eu(1, 2)))
         int bn = bend;
         if (lane == 0) bn = take(it == 0 ? w + NW : atomicAdd(&s_next, 1));  // one claim per wavefront
         bn = __builtin_amdgcn_readfirstlane(bn);
+        if constexpr (LM == 2)
+            if (bn < 0) bn = resolve(bn);  // this block waits in registers meanwhile
         if (bn < bend) {
             f_next = row_fill(bn);
             load_block(bn, kr_next, vr_next);
@@ -1010,15 +1107,20 @@ __global__ __launch_bounds__(NW * 64) __attribute__((amdgpu_waves_per_eu(1, 2)))
             attend_block<D>(kr, vr, nv, qv, scale_log2, m_run, l_run, acc);
         }
         // this block's registers are free again
-        if (it == 0) staged();
-        else if (pass < npass) score_step();
-        // (the softmax aggregation waits for the end of the loop: mid-loop, its
-        // exponentials would compete with the prefetched block for registers)
-        if (!AGG && it == npass_all) scores_done();
+        if (LM == 2 ? !staged_done : it == 0) {
+            staged();
+            staged_done = true;
+        } else if (pass < npass) {
+            score_step();
+        }
+        // (the softmax aggregation and the prompt selection wait for the first
+        // held claim or the end of the loop: mid-loop, their arithmetic would
+        // compete with the prefetched block for registers)
+        if (!AGG && LM != 2 && it == npass_all) scores_done();
         ++it;
         b = bn;
     }
-    if (it == 0) staged();
+    if (LM == 2 ? !staged_done : it == 0) staged();
     while (pass < npass) score_step();  // passes left when the wavefront ran out of blocks
     if (!decided) scores_done();
 
@@ -1378,10 +1480,10 @@ size_t step_lds(int G, int D, int S, int NW, bool fused, int agg, int list_ints)
     return b + (size_t)list_ints * 4;
 }
 
-template <int D, int NW, bool AGG, bool LIST, bool NT = false>
+template <int D, int NW, bool AGG, int LM, bool NT = false>
 void launch_step_inst(const LayerView& L, const StepIO& io, const StepPlan& pl, float sl2, double r,
                       hipStream_t s) {
-    hipLaunchKernelGGL((k_step_bf16<D, NW, AGG, LIST, NT>), dim3((unsigned)(L.U * pl.nsplit)), dim3(NW * 64),
+    hipLaunchKernelGGL((k_step_bf16<D, NW, AGG, LM, NT>), dim3((unsigned)(L.U * pl.nsplit)), dim3(NW * 64),
                        pl.lds, s, L, io, sl2, r, pl.fused ? 1 : 0);
 }
 
@@ -1390,12 +1492,13 @@ hipError_t launch_step_bf16(const LayerView& L, const StepIO& io, const StepPlan
                             hipStream_t s) {
     const bool list = L.topk >= 0;
     if (L.agg) {
-        if (list) launch_step_inst<D, NW, true, true>(L, io, pl, sl2, r, s);
-        else launch_step_inst<D, NW, true, false>(L, io, pl, sl2, r, s);
+        if (list) launch_step_inst<D, NW, true, 1>(L, io, pl, sl2, r, s);
+        else launch_step_inst<D, NW, true, 0>(L, io, pl, sl2, r, s);
     } else {
-        if (list) launch_step_inst<D, NW, false, true>(L, io, pl, sl2, r, s);
-        else if (L.nt) launch_step_inst<D, NW, false, false, true>(L, io, pl, sl2, r, s);
-        else launch_step_inst<D, NW, false, false>(L, io, pl, sl2, r, s);
+        if (pl.select_in_step) launch_step_inst<D, NW, false, 2>(L, io, pl, sl2, r, s);
+        else if (list) launch_step_inst<D, NW, false, 1>(L, io, pl, sl2, r, s);
+        else if (L.nt) launch_step_inst<D, NW, false, 0, true>(L, io, pl, sl2, r, s);
+        else launch_step_inst<D, NW, false, 0>(L, io, pl, sl2, r, s);
     }
     return hipGetLastError();
 }
@@ -1407,11 +1510,12 @@ hipError_t allow_lds_all(int bytes) {
         hipError_t r = hipFuncSetAttribute(f, hipFuncAttributeMaxDynamicSharedMemorySize, bytes);
         if (r != hipSuccess) e = r;
     };
-    set((const void*)k_step_bf16<D, NW, false, false>);
-    set((const void*)k_step_bf16<D, NW, true, false>);
-    set((const void*)k_step_bf16<D, NW, false, true>);
-    set((const void*)k_step_bf16<D, NW, true, true>);
-    set((const void*)k_step_bf16<D, NW, false, false, true>);
+    set((const void*)k_step_bf16<D, NW, false, 0>);
+    set((const void*)k_step_bf16<D, NW, true, 0>);
+    set((const void*)k_step_bf16<D, NW, false, 1>);
+    set((const void*)k_step_bf16<D, NW, true, 1>);
+    set((const void*)k_step_bf16<D, NW, false, 2>);
+    set((const void*)k_step_bf16<D, NW, false, 0, true>);
     return e;
 }
 
@@ -1442,6 +1546,12 @@ StepPlan plan_step(int U, int G, int D, int S, int Lcap, int ps, int pinned, boo
                 break;
             }
         }
+        // two or more units per CU: workgroups of 4 wavefronts, two per CU,
+        // so that one unit's serial phases (staging, selection, retention)
+        // overlap another's streaming
+        if (split_override <= 0 && !grouped && U >= 512 && pl.waves == 8 &&
+            2 * step_lds(G, D, S, 4, true, agg, list_ints) <= kMaxLds)
+            pl.waves = 4;
         if (split_override > 0) {
             want = split_override;
         } else if (!grouped && nblk <= kFusedBlocksPerWave * pl.waves &&
@@ -1462,6 +1572,9 @@ StepPlan plan_step(int U, int G, int D, int S, int Lcap, int ps, int pinned, boo
     pl.bps = (nblk + want - 1) / want;
     pl.nsplit = (nblk + pl.bps - 1) / pl.bps;
     pl.fused = bf16 && !grouped && pl.nsplit == 1 && step_lds(G, D, S, pl.waves, true, agg, list_ints) <= kMaxLds;
+    // a fused workgroup covers its unit, so it can choose the prompt pages
+    // itself (the softmax aggregation keeps the selection kernel)
+    pl.select_in_step = pl.fused && list_ints > 0 && !agg;
     pl.lds = bf16 ? step_lds(G, D, S, pl.waves, pl.fused, agg, list_ints) : 0;
     return pl;
 }

@@ -88,6 +88,15 @@ struct raas_pool {
 
 namespace {
 
+// LDS ints the step kernel needs for the prompt selection: a block list of
+// the whole pool (list-driven instance), or the prompt pages' fp64 bounds
+// (two ints each, up to three more to align them to 16 bytes), attended
+// fills and blocks (in-step selection)
+int list_ints(const raas_pool* p) {
+    if (p->npr == 0) return 0;
+    return std::max(p->Lcap / kBlockTokens, 3 + 3 * p->npr + p->npr * p->ps / kBlockTokens);
+}
+
 LayerView view(const raas_pool* p, int layer) {
     LayerView L;
     const size_t kv = (size_t)layer * p->kv_layer_elems * p->esz;
@@ -448,7 +457,7 @@ raas_status raas_decode_step_masked(raas_pool* p, int32_t layer, const void* q, 
     const StepPlan pl = plan_step(p->U, p->G, p->D, p->S, L.nblk * kBlockTokens, p->ps, p->pinned[layer],
                                   p->cfg.dtype == RAAS_BF16, p->cfg.score_aggregation,
                                   p->cfg.decision_scope == RAAS_SCOPE_SEQUENCE,
-                                  p->npr > 0 ? p->Lcap / kBlockTokens : 0, p->split_override);
+                                  list_ints(p), p->split_override);
     L.nsplit = pl.nsplit;
     L.bps = pl.bps;
     // Successive steps of a layer read its pool in opposite directions, so a
@@ -456,7 +465,7 @@ raas_status raas_decode_step_masked(raas_pool* p, int32_t layer, const void* q, 
     // to be still in the GPU's memory-side cache.
     L.rev = p->descending[layer];
 
-    if (p->npr > 0) {  // Quest on the prompt: which prompt pages this step attends to
+    if (p->npr > 0 && !pl.select_in_step) {  // Quest on the prompt: which prompt pages this step attends to
         prof_record(p, 2, true, s);
         hipError_t e = launch_prompt_select(L, io, s);
         prof_record(p, 2, false, s);
