@@ -213,25 +213,30 @@ def _check_invariants(pt, ts, ev, clock, P, ps, S, npr=0):
 
 
 def run_ragged(w, seed: int, lens, steps: int, active_p: float = 0.75, reprefill=None, splits=None,
-               aggregation: int = 0, rank_pinned: bool = False, scope: int = 0) -> ParityReport:
+               aggregation: int = 0, rank_pinned: bool = False, scope: int = 0, prompt_tokens: int = 0,
+               prompt_topk: int = 0) -> ParityReport:
     """Ragged batch: per-sequence prompt lengths (raas_prefill_ragged), a
     seeded per-step mask of the sequences that take a token
     (raas_decode_step_masked), and prompts replaced mid-run (reprefill: step
     -> {sequence: new length}, a re-prefill of those sequences alone before
     that step). Every unit is checked against an oracle that steps only
     when its sequence is active; inactive sequences' outputs must stay
-    untouched; at the end the whole exported state must agree."""
+    untouched; at the end the whole exported state must agree.
+    prompt_tokens/prompt_topk: a prompt region with Quest on it, as in
+    run_parity (each sequence keeps its own number of prompt pages)."""
     import torch
 
     rep = ParityReport()
-    B, Hq, Hkv, d, G, S, ps = (w.batch, w.n_q_heads, w.n_kv_heads, w.head_dim, w.group, w.slots,
-                               w.page_size)
+    B, Hq, Hkv, d, G, ps = w.batch, w.n_q_heads, w.n_kv_heads, w.head_dim, w.group, w.page_size
+    npr = prompt_tokens // ps
+    S = w.slots + npr
     U = B * Hkv
     reprefill = reprefill or {}
     tol = TOL[w.dtype]
     dt = torch.bfloat16 if w.dtype == "bf16" else torch.float32
     rng = np.random.default_rng(seed + 17)
-    pool = new_pool(w, splits, aggregation=aggregation, rank_pinned=rank_pinned, scope=scope)
+    pool = new_pool(w, splits, aggregation=aggregation, rank_pinned=rank_pinned, scope=scope,
+                    prompt_tokens=prompt_tokens, prompt_topk=prompt_topk)
     orc = {}
 
     def prompt(lens_now, mask, pseed):
@@ -243,7 +248,8 @@ def run_ragged(w, seed: int, lens, steps: int, active_p: float = 0.75, reprefill
             if not mask[b]:
                 continue
             for h in range(Hkv):
-                m = oracle.Kvm(G, d, ps, S, r=w.r, aggregation=aggregation, rank_pinned=rank_pinned)
+                m = oracle.Kvm(G, d, ps, S, r=w.r, aggregation=aggregation, rank_pinned=rank_pinned,
+                               prompt_slots=npr if prompt_topk else None, prompt_topk=prompt_topk or None)
                 P = int(lens_now[b])
                 assert m.prefill(Kp[b, h, :P].astype(np.float64), Vp[b, h, :P].astype(np.float64)) == 0
                 orc[b * Hkv + h] = m

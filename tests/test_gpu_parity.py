@@ -378,6 +378,8 @@ RAGGED = [
     dict(scope=1),
     dict(scope=1, aggregation=1, rank_pinned=True),
     dict(rank_pinned=True),
+    dict(prompt_tokens=128, prompt_topk=3),            # prompt selection in the step kernel
+    dict(prompt_tokens=128, prompt_topk=3, splits=3),  # the selection kernel
 ]
 
 
