@@ -272,11 +272,12 @@ __device__ void load_slots(const LayerView& L, int u, const UnitRec& ur, double*
 
 // ---------------------------------------------------------------------------
 // Page scores (Section 3.3, Quest's representative keys): for each evictable
-// page, max over the G query heads of sum_c max(q_c*kmax_c, q_c*kmin_c), in
-// fp64. The larger product is q_c times kmax_c when q_c > 0 and kmin_c
-// otherwise (both are zero when q_c = 0), so each channel takes one selected
-// key and one fused multiply-add; products of bf16 values are exact in fp64,
-// so each multiply-add rounds exactly as an add of the exact product. Eight
+// page, max over the G query heads of sum_c max(q_c*kmax_c, q_c*kmin_c),
+// summed in fp64. A product of two bf16 values has at most 16 significant
+// bits, so both products are formed exactly in fp32 (q and the keys are
+// staged as fp32), the larger is widened and added in fp64: each add rounds
+// exactly as the fp64 sum of the exact product (products below fp32's normal
+// range, under 1e-38 in magnitude, would be the exception). Eight
 // lanes per page: lane part p sums D/8 consecutive channels in two chains
 // (even and odd channels), the eight parts combine through a fixed xor tree,
 // so equal pages score equal. A wavefront scores 8 pages per pass; its passes
@@ -284,15 +285,15 @@ __device__ void load_slots(const LayerView& L, int u, const UnitRec& ur, double*
 // the previous block computes. The page the step writes to has its min/max
 // widened by the new key and stored back.
 
-// LDS slot of element i = head * D + channel of the fp64 query array: a
+// LDS slot of element i = head * D + channel of the fp32 query array: a
 // 16-byte pad after each D/8 channels, so that the eight lanes scoring a
-// page, which read channel pairs D/8 apart, fall on different LDS banks and
-// every pair stays 16-byte aligned.
-constexpr int qpad_row(int D) { return D + 16; }
+// page, which read channels D/8 apart, fall on different LDS banks and every
+// group of four stays 16-byte aligned.
+constexpr int qpad_row(int D) { return D + 32; }
 template <int D>
 __device__ __forceinline__ int qpad_index(int i) {
     const int h = i / D, c = i - (i / D) * D;
-    return h * qpad_row(D) + c + 2 * (c / (D / 8));
+    return h * qpad_row(D) + c + 4 * (c / (D / 8));
 }
 
 template <int D>
@@ -317,7 +318,7 @@ __device__ __forceinline__ void score_issue(const LayerView& L, int u, int p, in
 template <int D>
 __device__ __forceinline__ double score_finish(const LayerView& L, int u, int p, int part, bool act,
                                                ScoreFrag<D>& f, bool is_tail, bool opened,
-                                               const uint16_t* k_new, const double* qd, double* hb) {
+                                               const uint16_t* k_new, const float* qf, double* hb) {
     constexpr int SV = ScoreFrag<D>::SV;
     const int G = L.G;
     if (act && is_tail) {
@@ -361,16 +362,15 @@ __device__ __forceinline__ double score_finish(const LayerView& L, int u, int p,
     double best = -INFINITY;
 #pragma unroll 1
     for (int j = 0; j < G; ++j) {
-        const double* qj = qd + (size_t)j * qpad_row(D) + c0 + 2 * part;  // see qpad_index
+        const float* qj = qf + (size_t)j * qpad_row(D) + c0 + 4 * part;  // see qpad_index
         double a0 = 0.0, a1 = 0.0;  // even and odd channels
-        // keep the fp64 widening inside the loop: hoisted, it needs twice the registers
 #pragma unroll
-        for (int c = 0; c < D / 8; ++c) asm volatile("" : "+v"(kxf[c]), "+v"(knf[c]));
-#pragma unroll
-        for (int c = 0; c < D / 8; c += 2) {
-            const double2 qq = *reinterpret_cast<const double2*>(qj + c);
-            a0 = fma(qq.x, (double)(qq.x > 0.0 ? kxf[c] : knf[c]), a0);
-            a1 = fma(qq.y, (double)(qq.y > 0.0 ? kxf[c + 1] : knf[c + 1]), a1);
+        for (int c = 0; c < D / 8; c += 4) {
+            const float4 qq = *reinterpret_cast<const float4*>(qj + c);
+            a0 += (double)fmaxf(qq.x * kxf[c], qq.x * knf[c]);
+            a1 += (double)fmaxf(qq.y * kxf[c + 1], qq.y * knf[c + 1]);
+            a0 += (double)fmaxf(qq.z * kxf[c + 2], qq.z * knf[c + 2]);
+            a1 += (double)fmaxf(qq.w * kxf[c + 3], qq.w * knf[c + 3]);
         }
         double a = a0 + a1;
         a += __shfl_xor(a, 1);
@@ -781,8 +781,8 @@ __global__ __launch_bounds__(NW * 64) __attribute__((amdgpu_waves_per_eu(2, 2)))
     __shared__ __align__(16) uint16_t s_vn[D];  // no read in the block loop waits on memory
 
     const int G = L.G, S = L.S, ps = L.ps;
-    double* s_qd = reinterpret_cast<double*>(smem);  // [G][D+16] q in fp64, padded: qpad_index
-    float* s_o = reinterpret_cast<float*>(s_qd + (size_t)G * qpad_row(D));  // [NW][G][D+4]
+    float* s_qf = reinterpret_cast<float*>(smem);  // [G][D+32] q in fp32, padded: qpad_index
+    float* s_o = s_qf + (size_t)G * qpad_row(D);   // [NW][G][D+4]
     double* s_score = reinterpret_cast<double*>(s_o + (size_t)NW * G * (D + 4));  // [S], fused only
     double* s_hb = s_score + S;  // [S][G] per-head bounds, fused softmax aggregation only
     double* s_mz = s_hb + (AGG ? (size_t)S * G : 0);  // [G][2] each head's M and Z, likewise
@@ -922,8 +922,8 @@ __global__ __launch_bounds__(NW * 64) __attribute__((amdgpu_waves_per_eu(2, 2)))
     if (real(b)) f_next = (w < nown) ? (slot_first < S ? (slot_first == ns ? nf + 1 : fill_first) : 0) : row_fill(b);
 
     // staging for the scores and the epilogue
-    if (tid < G * D) s_qd[qpad_index<D>(tid)] = (double)bf2f(q_first);
-    for (int i = tid + NW * 64; i < G * D; i += NW * 64) s_qd[qpad_index<D>(i)] = (double)bf2f(qg[i]);
+    if (tid < G * D) s_qf[qpad_index<D>(tid)] = bf2f(q_first);
+    for (int i = tid + NW * 64; i < G * D; i += NW * 64) s_qf[qpad_index<D>(i)] = bf2f(qg[i]);
     if (tid < D / 8) {
         st4(&s_kn[8 * tid], kn_first);
         st4(&s_vn[8 * tid], vn_first);
@@ -962,7 +962,7 @@ __global__ __launch_bounds__(NW * 64) __attribute__((amdgpu_waves_per_eu(2, 2)))
     auto score_step = [&]() {
         const int p = pass_page(pass);
         double* hb = (AGG && act_cur) ? (fused ? s_hb : L.score + base * G) + (size_t)p * G : nullptr;
-        const double sc = score_finish<D>(L, u, p, part, act_cur, frag, p == ns, opened, s_kn, s_qd, hb);
+        const double sc = score_finish<D>(L, u, p, part, act_cur, frag, p == ns, opened, s_kn, s_qf, hb);
         if (act_cur && part == 0 && !AGG) {
             if (LM == 2 && p < L.dbase) s_pb[p] = sc;  // a prompt page: a bound for the selection
             else if (fused) s_score[p] = sc;
@@ -1031,9 +1031,9 @@ __global__ __launch_bounds__(NW * 64) __attribute__((amdgpu_waves_per_eu(2, 2)))
     };
     bool staged_done = false;  // LM 2: staged() has run (a held claim runs it early)
     // LM 2: a claim held for the selection: this wavefront finishes its score
-    // passes, passes the score barrier (every wavefront holds one claim when
-    // it gets there: the decode blocks come first), then takes the chosen
-    // prompt block the claim stands for
+    // passes and waits at the score barrier, which every wavefront reaches
+    // the same way (its claims run past the decode blocks before they reach a
+    // prompt block), then takes the chosen prompt block the claim stands for
     auto resolve = [&](int x) {
         if (!staged_done) {
             staged();
@@ -1471,11 +1471,11 @@ __global__ __launch_bounds__(256) void k_epilogue(LayerView L, StepIO io, double
 
 inline unsigned grid1d(size_t n, int block) { return (unsigned)((n + block - 1) / block); }
 
-// LDS of the step kernel: the queries in fp64, the attention wavefronts'
+// LDS of the step kernel: the queries in fp32, the attention wavefronts'
 // partial outputs, the fused epilogue's slot arrays (with the per-head
 // bounds of the softmax aggregation), and a block list
 size_t step_lds(int G, int D, int S, int NW, bool fused, int agg, int list_ints) {
-    size_t b = (size_t)8 * G * qpad_row(D) + (size_t)NW * G * (D + 4) * 4;
+    size_t b = (size_t)4 * G * qpad_row(D) + (size_t)NW * G * (D + 4) * 4;
     if (fused) b += (size_t)S * 20 + (agg ? (size_t)S * G * 8 + (size_t)G * 16 : 0);
     return b + (size_t)list_ints * 4;
 }
