@@ -285,6 +285,28 @@ __device__ void load_slots(const LayerView& L, int u, const UnitRec& ur, double*
 // the previous block computes. The page the step writes to has its min/max
 // widened by the new key and stored back.
 
+// Cross-lane moves that stay in the VALU (no LDS round trip). dpp_f64<CTRL>:
+// a DPP move of both halves of a double; 0xB1 and 0x4E (quad_perm
+// [1,0,3,2] and [2,3,0,1]) give lane ^ 1 and lane ^ 2, 0x141 (row_half_mirror)
+// gives lane 7 - i within each group of 8. max_xor16_32: the max over lanes
+// i, i ^ 16, i ^ 32 and i ^ 48 through the two permlane swaps (a swap of a
+// value with itself leaves both 16-lane or 32-lane halves side by side).
+template <int CTRL>
+__device__ __forceinline__ double dpp_f64(double x) {
+    const unsigned long long b = __builtin_bit_cast(unsigned long long, x);
+    const unsigned lo = (unsigned)__builtin_amdgcn_update_dpp(0, (int)(unsigned)b, CTRL, 0xF, 0xF, false);
+    const unsigned hi = (unsigned)__builtin_amdgcn_update_dpp(0, (int)(unsigned)(b >> 32), CTRL, 0xF, 0xF, false);
+    return __builtin_bit_cast(double, ((unsigned long long)hi << 32) | lo);
+}
+__device__ __forceinline__ float max_xor16_32(float x) {
+    const unsigned u = __builtin_bit_cast(unsigned, x);
+    const auto a = __builtin_amdgcn_permlane16_swap(u, u, false, false);
+    const float m = fmaxf(__builtin_bit_cast(float, (unsigned)a[0]), __builtin_bit_cast(float, (unsigned)a[1]));
+    const unsigned v = __builtin_bit_cast(unsigned, m);
+    const auto b = __builtin_amdgcn_permlane32_swap(v, v, false, false);
+    return fmaxf(__builtin_bit_cast(float, (unsigned)b[0]), __builtin_bit_cast(float, (unsigned)b[1]));
+}
+
 // LDS slot of element i = head * D + channel of the fp32 query array: a
 // 16-byte pad after each D/8 channels, so that the eight lanes scoring a
 // page, which read channels D/8 apart, fall on different LDS banks and every
@@ -373,9 +395,11 @@ __device__ __forceinline__ double score_finish(const LayerView& L, int u, int p,
             a1 += (double)fmaxf(qq.w * kxf[c + 3], qq.w * knf[c + 3]);
         }
         double a = a0 + a1;
-        a += __shfl_xor(a, 1);
-        a += __shfl_xor(a, 2);
-        a += __shfl_xor(a, 4);
+        // the eight parts: pairs, then quads, then the two quads (the lanes of
+        // a quad hold equal sums by then, so the mirror partner gives lane ^ 4's)
+        a += dpp_f64<0xB1>(a);
+        a += dpp_f64<0x4E>(a);
+        a += dpp_f64<0x141>(a);
         best = a > best ? a : best;
         if (hb != nullptr && part == 0) hb[j] = a;  // per-head bounds, for the softmax aggregation
     }
@@ -709,8 +733,7 @@ __device__ __forceinline__ void attend_block(const u32x4 (&kr)[2][D / 32], const
     float mb = x[0];
 #pragma unroll
     for (int j = 1; j < 8; ++j) mb = fmaxf(mb, x[j]);
-    mb = fmaxf(mb, __shfl_xor(mb, 16));
-    mb = fmaxf(mb, __shfl_xor(mb, 32));
+    mb = max_xor16_32(mb);
     const float m_new = fmaxf(m_run, mb);
     if (__ballot(m_new > m_run) != 0ull) {
         const float alpha = __builtin_amdgcn_exp2f(m_run - m_new);
