@@ -1160,6 +1160,9 @@ __global__ __launch_bounds__(NW * 64) __attribute__((amdgpu_waves_per_eu(2, 2)))
             *reinterpret_cast<f32x4*>(&s_o[((size_t)w * G + col) * (D + 4) + 16 * nb + 4 * grp]) = acc[nb];
     }
     lds_barrier();  // partials parked, retention decided
+    // the state goes out first (every block has been read), its stores
+    // draining while the partials merge
+    if (fused) retention_store(L, io, u, ur, s_state, s_ts, s_lid, ret, tid, NW * 64);
 
     // merge the wavefronts' partial outputs
     for (int idx = tid; idx < G * D; idx += NW * 64) {
@@ -1186,7 +1189,6 @@ __global__ __launch_bounds__(NW * 64) __attribute__((amdgpu_waves_per_eu(2, 2)))
             }
         }
     }
-    if (fused) retention_store(L, io, u, ur, s_state, s_ts, s_lid, ret, tid, NW * 64);
 }
 
 // Step kernel, fp32 pools: one wavefront per (unit, split), one token at a
