@@ -218,7 +218,9 @@ raas_status raas_set_attention_splits(raas_pool* pool, int32_t splits);
  * single workgroup covers a unit), 1 the epilogue kernel (split merge,
  * refresh, eviction; launched when a unit is split over several
  * workgroups, for fp32 pools and for the sequence scope), 2 the prompt
- * selection kernel (with a prompt region). mask 0 turns timing off.
+ * selection kernel (with a prompt region, when the step kernel does not
+ * select the prompt pages itself: split plans, the softmax aggregation and
+ * fp32 pools). mask 0 turns timing off.
  * raas_profile_read returns, for kernel i, the summed duration in ms and the
  * number of timed launches since the last read (synchronising on the
  * recorded events), then resets them. Errors: RAAS_E_INVALID, RAAS_E_HIP. */
