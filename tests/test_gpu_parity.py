@@ -12,7 +12,8 @@ import numpy as np
 import pytest
 
 import synth
-from harness import ParityReport, new_pool, run_parity, run_ragged, to_device
+import oracle
+from harness import TOL, ParityReport, new_pool, run_parity, run_ragged, to_device
 
 pytestmark = pytest.mark.gpu
 
@@ -439,6 +440,61 @@ def test_prompt_selection(case):
     rep = run_parity(w, seed=13, steps=w.decode_steps, **run_kw)
     _report(rep, "prompt-selection")
     assert rep.evictions > 0
+
+
+@pytest.mark.parametrize("splits", [None, 2], ids=["in-step", "selection-kernel"])
+def test_prompt_selection_ties(splits):
+    """Prompt pages 1, 4 and 6 copy page 2's keys (scaled up so that the four
+    lead the bounds) with values of their own: their bounds are equal in any
+    summation order, so with top 3 the tie rule alone keeps slot 6 out, and a
+    wrong tie-break changes the outputs. Every unit, every step, against the
+    oracle; the oracle's own choice is checked too."""
+    import torch
+
+    w = small(batch=2, n_kv_heads=2, n_q_heads=8, decode_steps=60, prefill_len=128)
+    ps, npr, topk = w.page_size, 128 // w.page_size, 3
+    B, Hkv, G, d = w.batch, w.n_kv_heads, w.group, w.head_dim
+    U, S = B * Hkv, w.slots + npr
+    rng = np.random.default_rng(31)
+    K = rng.standard_normal((B, Hkv, 128, d)).astype(np.float32)
+    V = rng.standard_normal((B, Hkv, 128, d)).astype(np.float32)
+    K[:, :, 2 * ps:3 * ps] *= 3.0
+    for pg in (1, 4, 6):
+        K[:, :, pg * ps:(pg + 1) * ps] = K[:, :, 2 * ps:3 * ps]
+    Kb = to_device(K, "bf16")
+    Vb = to_device(V, "bf16")
+    Kr, Vr = Kb.float().cpu().numpy().astype(np.float64), Vb.float().cpu().numpy().astype(np.float64)
+    _say("case prompt-selection ties splits %s" % splits)
+    pool = new_pool(w, splits, prompt_tokens=128, prompt_topk=topk)
+    pool.prefill(0, Kb, Vb)
+    orc = []
+    for u in range(U):
+        b, h = divmod(u, Hkv)
+        m = oracle.Kvm(G, d, ps, S, r=w.r, prompt_slots=npr, prompt_topk=topk)
+        assert m.prefill(Kr[b, h], Vr[b, h]) == 0
+        orc.append(m)
+    out = torch.empty((B, w.n_q_heads, d), dtype=torch.bfloat16, device="cuda")
+    chosen_without_6 = 0
+    for t in range(w.decode_steps):
+        q = rng.standard_normal((B, w.n_q_heads, d)).astype(np.float32)
+        kn = rng.standard_normal((B, Hkv, d)).astype(np.float32)
+        vn = rng.standard_normal((B, Hkv, d)).astype(np.float32)
+        qb, kb, vb = to_device(q, "bf16"), to_device(kn, "bf16"), to_device(vn, "bf16")
+        pool.decode_step(0, qb, kb, vb, out)
+        torch.cuda.synchronize()
+        got = out.float().cpu().numpy().reshape(U, G, d)
+        q64 = qb.float().cpu().numpy().astype(np.float64).reshape(U, G, d)
+        k64 = kb.float().cpu().numpy().astype(np.float64).reshape(U, d)
+        v64 = vb.float().cpu().numpy().astype(np.float64).reshape(U, d)
+        for u in range(U):
+            want = orc[u].decode(q64[u], k64[u], v64[u])
+            att = orc[u].last_attended()[:npr]
+            if att[1] and att[2] and att[4] and not att[6]:
+                chosen_without_6 += 1
+            err = float(np.max(np.abs(got[u] - want)))
+            assert err <= TOL["bf16"], "unit %d step %d: max abs err %.3g" % (u, t, err)
+    pool.close()
+    assert chosen_without_6 > 0  # the tie decided the top 3 in some steps
 
 
 @pytest.mark.parametrize("name,topk,steps,units", [("llama8b-b128-ps32-L512", 8, 640, 8),
