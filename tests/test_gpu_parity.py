@@ -442,6 +442,68 @@ def test_prompt_selection(case):
     assert rep.evictions > 0
 
 
+@pytest.mark.parametrize("splits,page_size,budget", [(None, 16, 128), (2, 16, 128), (2, 8, 2400)],
+                         ids=["fused", "epilogue-count", "epilogue-radix"])
+def test_retention_exact_ties(splits, page_size, budget):
+    """Every decode page holds the same sixteen (or eight) keys as every
+    other page of its parity (two key sets, A for even pages and B for odd
+    ones), so the ranked scores come in two values, equal in any summation
+    order: the refresh's strict comparison with theta and the (timestamp,
+    id) eviction order meet exact ties at every step. Retention must match
+    the oracle bit for bit at every step (no near-tie allowance), on the
+    fused workgroup's retention, the epilogue's count and its radix select
+    (300 slots)."""
+    import torch
+
+    w = small(batch=2, n_kv_heads=2, n_q_heads=8, decode_steps=400, prefill_len=40, page_size=page_size,
+              budget=budget)
+    ps, B, Hkv, G, d, S = w.page_size, w.batch, w.n_kv_heads, w.group, w.head_dim, w.slots
+    U = B * Hkv
+    rng = np.random.default_rng(41)
+    K = to_device(rng.standard_normal((B, Hkv, 40, d)).astype(np.float32), "bf16")
+    V = to_device(rng.standard_normal((B, Hkv, 40, d)).astype(np.float32), "bf16")
+    sets = to_device(rng.standard_normal((2, ps, B, Hkv, d)).astype(np.float32), "bf16")
+    _say("case retention ties splits %s page %d budget %d" % (splits, ps, budget))
+    pool = new_pool(w, splits)
+    pool.prefill(0, K, V)
+    Kr = K.float().cpu().numpy().astype(np.float64)
+    Vr = V.float().cpu().numpy().astype(np.float64)
+    orc = []
+    for u in range(U):
+        b, h = divmod(u, Hkv)
+        m = oracle.Kvm(G, d, ps, S, r=w.r)
+        assert m.prefill(Kr[b, h], Vr[b, h]) == 0
+        orc.append(m)
+    out = torch.empty((B, w.n_q_heads, d), dtype=torch.bfloat16, device="cuda")
+    pt = torch.empty((B, Hkv, S), dtype=torch.int32, device="cuda")
+    ts = torch.empty((B, Hkv, S), dtype=torch.int32, device="cuda")
+    ev = torch.empty((B, Hkv), dtype=torch.int32, device="cuda")
+    evictions = 0
+    for t in range(w.decode_steps):
+        qb = to_device(rng.standard_normal((B, w.n_q_heads, d)).astype(np.float32), "bf16")
+        kb = sets[(t // ps) % 2, t % ps].contiguous()
+        vb = to_device(rng.standard_normal((B, Hkv, d)).astype(np.float32), "bf16")
+        pool.decode_step(0, qb, kb, vb, out, pt, ts, ev)
+        torch.cuda.synchronize()
+        got = out.float().cpu().numpy().reshape(U, G, d)
+        pt_h, ts_h, ev_h = pt.cpu().numpy().reshape(U, S), ts.cpu().numpy().reshape(U, S), ev.cpu().numpy().reshape(U)
+        q64 = qb.float().cpu().numpy().astype(np.float64).reshape(U, G, d)
+        k64 = kb.float().cpu().numpy().astype(np.float64).reshape(U, d)
+        v64 = vb.float().cpu().numpy().astype(np.float64).reshape(U, d)
+        for u in range(U):
+            want = orc[u].decode(q64[u], k64[u], v64[u])
+            st = orc[u].state()
+            assert np.array_equal(st["page_table"], pt_h[u]) and np.array_equal(st["ts"], ts_h[u]) \
+                and st["evicted"] == ev_h[u], "unit %d step %d:\noracle pt %s ts %s ev %d\n   gpu pt %s ts %s ev %d" % (
+                    u, t, st["page_table"].tolist(), st["ts"].tolist(), st["evicted"], pt_h[u].tolist(),
+                    ts_h[u].tolist(), ev_h[u])
+            evictions += int(st["evicted"] >= 0)
+            err = float(np.max(np.abs(got[u] - want)))
+            assert err <= TOL["bf16"], "unit %d step %d: max abs err %.3g" % (u, t, err)
+    pool.close()
+    assert evictions > 0 or budget > w.prefill_len + w.decode_steps
+
+
 @pytest.mark.parametrize("splits", [None, 2], ids=["in-step", "selection-kernel"])
 def test_prompt_selection_ties(splits):
     """Prompt pages 1, 4 and 6 copy page 2's keys (scaled up so that the four
