@@ -89,10 +89,12 @@ struct StepPlan {
     size_t lds;      // dynamic LDS of the step kernel
 };
 
-// grouped: retention decided per group of units, by the epilogue kernel;
+// work_blocks: 32-token blocks a unit's step attends (Lcap / 32 less the
+// unchosen prompt blocks); grouped: retention decided per group of units, by
+// the epilogue kernel;
 // list_ints: LDS ints of a block list or of the in-step prompt selection (0
 // without a prompt region)
-StepPlan plan_step(int U, int G, int D, int S, int Lcap, int ps, int pinned, bool bf16, int agg,
+StepPlan plan_step(int U, int G, int D, int S, int Lcap, int ps, int work_blocks, bool bf16, int agg,
                    bool grouped, int list_ints, int split_override);
 // Quest on the prompt pages: the attended fills and the block list of a step.
 hipError_t launch_prompt_select(const LayerView& L, const StepIO& io, hipStream_t stream);

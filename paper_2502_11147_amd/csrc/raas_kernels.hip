@@ -1553,9 +1553,15 @@ hipError_t allow_lds_all(int bytes) {
 // wavefronts: 14.6 against 19.2 us and 15.9 against 19.7 us per step).
 constexpr int kFusedBlocksPerWave = 6;
 
-StepPlan plan_step(int U, int G, int D, int S, int Lcap, int ps, int pinned, bool bf16, int agg,
+// Workgroups of 2 wavefronts, four per CU, from this many units on when a
+// unit's step attends at most kSmallWorkBlocks blocks (same box, batch 128,
+// page 32: L 512 45.1 -> 42.7 us, L 512 plus the top 8 prompt pages 114.4 ->
+// 101.8 us; L 2048, 64 blocks, 170.1 -> 173.4 us, so longer pools keep 4).
+constexpr int kSmallWorkUnits = 1024;
+constexpr int kSmallWorkBlocks = 32;
+
+StepPlan plan_step(int U, int G, int D, int S, int Lcap, int ps, int work_blocks, bool bf16, int agg,
                    bool grouped, int list_ints, int split_override) {
-    (void)pinned;
     (void)ps;
     StepPlan pl{};
     const int nblk = Lcap / kBlockTokens;
@@ -1577,6 +1583,11 @@ StepPlan plan_step(int U, int G, int D, int S, int Lcap, int ps, int pinned, boo
         if (split_override <= 0 && !grouped && U >= 512 && pl.waves == 8 &&
             2 * step_lds(G, D, S, 4, true, agg, list_ints) <= kMaxLds)
             pl.waves = 4;
+        // four or more units per CU, each with little to stream: four
+        // workgroups per CU overlap more units' serial phases
+        if (split_override <= 0 && !grouped && U >= kSmallWorkUnits && work_blocks <= kSmallWorkBlocks &&
+            pl.waves == 4 && 4 * step_lds(G, D, S, 2, true, agg, list_ints) <= kMaxLds)
+            pl.waves = 2;
         if (split_override > 0) {
             want = split_override;
         } else if (!grouped && nblk <= kFusedBlocksPerWave * pl.waves &&

@@ -70,7 +70,6 @@ struct raas_pool {
     hipEvent_t seq_copied = nullptr;  // recorded after the last staging copy
     size_t bytes = 0;
     std::vector<unsigned char> prefilled;
-    std::vector<int> pinned;  // pinned prefill pages of each layer
     // Bound on the slots in use, per layer: pages open at the lowest free
     // slot, and no slot is freed before every slot has been used, so a
     // unit that kept k prompt pages and took n decode tokens since uses at
@@ -257,7 +256,6 @@ raas_status raas_create_pool(const raas_config* cfg, void* stream, raas_pool** o
     p->rep_layer_elems = (size_t)p->U * p->S * p->D;
     p->meta_layer_elems = (size_t)p->U * p->S;
     p->prefilled.assign((size_t)cfg->n_layers, 0);
-    p->pinned.assign((size_t)cfg->n_layers, 0);
     p->keep_max.assign((size_t)cfg->n_layers, 0);
     p->steps.assign((size_t)cfg->n_layers, 0);
     p->descending.assign((size_t)cfg->n_layers, 0);
@@ -363,7 +361,6 @@ raas_status raas_prefill(raas_pool* p, int32_t layer, const void* k, const void*
     hipError_t e = launch_prefill(view(p, layer), k, v, in, std::min(prefill_len, keep * p->ps), s);
     if (e != hipSuccess) return hip_fail(e, "prefill launch");
     p->prefilled[layer] = 1;
-    p->pinned[layer] = keep;
     p->keep_max[layer] = std::max(keep, p->npr);  // decode pages start after the prompt region
     p->steps[layer] = 0;
     p->last_stream = s;
@@ -454,10 +451,17 @@ raas_status raas_decode_step_masked(raas_pool* p, int32_t layer, const void* q, 
     const long long pages_opened = (p->steps[layer] + 1 + p->ps - 1) / p->ps;
     const long long used = std::min<long long>(p->S, p->keep_max[layer] + pages_opened);
     L.nblk = (int)std::min<long long>(p->Lcap / kBlockTokens, (used * p->ps + kBlockTokens - 1) / kBlockTokens);
-    const StepPlan pl = plan_step(p->U, p->G, p->D, p->S, L.nblk * kBlockTokens, p->ps, p->pinned[layer],
+    // blocks the step attends: with a prompt region only the chosen prompt
+    // pages' blocks (at most topk pages, each on ceil(page_size / 32) blocks)
+    int work_blocks = L.nblk;
+    if (p->npr > 0) {
+        const int nbp = p->npr * p->ps / kBlockTokens;
+        const int per_page = std::max(1, p->ps / kBlockTokens);
+        work_blocks = L.nblk - nbp + std::min(nbp, p->cfg.prompt_topk * per_page);
+    }
+    const StepPlan pl = plan_step(p->U, p->G, p->D, p->S, L.nblk * kBlockTokens, p->ps, work_blocks,
                                   p->cfg.dtype == RAAS_BF16, p->cfg.score_aggregation,
-                                  p->cfg.decision_scope == RAAS_SCOPE_SEQUENCE,
-                                  list_ints(p), p->split_override);
+                                  p->cfg.decision_scope == RAAS_SCOPE_SEQUENCE, list_ints(p), p->split_override);
     L.nsplit = pl.nsplit;
     L.bps = pl.bps;
     // Successive steps of a layer read its pool in opposite directions, so a
