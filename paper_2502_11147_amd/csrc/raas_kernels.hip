@@ -474,10 +474,12 @@ __device__ void softmax_sum_block(const LayerView& L, const double* hb, int nu, 
 __device__ void evict_wave(const LayerView& L, const UnitRec& ur, int* s_state, int* s_ts, const int* s_lid,
                            RetShared& out);
 
+// lo: where the rank count starts, at most the first slot that a ranked
+// page can occupy (slots below the decode base, and below the unit's pinned
+// pages unless the pool ranks them, hold none).
 __device__ void retention_wave(const LayerView& L, const UnitRec& ur, double r, const double* s_score,
-                               int* s_state, int* s_ts, const int* s_lid, RetShared& out) {
-    // slots below the decode base (a prompt region) are never ranked
-    const int S = L.S, lane = threadIdx.x & 63, s_lo = L.dbase;
+                               int* s_state, int* s_ts, const int* s_lid, RetShared& out, int lo) {
+    const int S = L.S, lane = threadIdx.x & 63, s_lo = lo;
     int n = 0;
     for (int s0 = s_lo; s0 < S; s0 += 64) {
         const int s = s0 + lane;
@@ -1040,7 +1042,12 @@ __global__ __launch_bounds__(NW * 64) __attribute__((amdgpu_waves_per_eu(2, 2)))
             lds_barrier();
         }
         if (AGG && fused) softmax_sum_block(L, s_hb, 1, s_state, s_score, s_mz, tid, NW * 64);
-        if (fused && w == 0) retention_wave(L, ur, r, s_score, s_state, s_ts, s_lid, ret);
+        // (after the block loop, as with the softmax aggregation, the retention
+        // is on the critical path: its count skips the pinned pages; mid-loop
+        // it overlaps the streaming, and the narrower count measured no faster)
+        if (fused && w == 0)
+            retention_wave(L, ur, r, s_score, s_state, s_ts, s_lid, ret,
+                           AGG && !L.rank_pinned ? max(L.dbase, pinned) : L.dbase);
         decided = true;
     };
 
