@@ -1198,22 +1198,31 @@ __global__ __launch_bounds__(NW * 64) __attribute__((amdgpu_waves_per_eu(2, 2)))
     }
 }
 
-// Step kernel, fp32 pools: one wavefront per (unit, split), one token at a
-// time, lanes across channels, online softmax per head in fp32; one lane per
-// page for the scores, summing the channels in order.
-template <int D>
+// Step kernel, fp32 pools: one wavefront per (unit, split), over its rows in
+// chunks of 64 tokens. In a chunk each lane takes one token: its row of K is
+// loaded whole (the loads go out with the unit record's, before the fills
+// say which rows hold tokens) and dotted with the G queries from LDS. The
+// online softmax then updates each head across the wavefront (base 2), and
+// the value pass turns to lanes across channels, one token at a time. Rows
+// are loaded whether or not they hold a token, so that no load waits for
+// the fills; a row holding none enters the sums as zeros with weight 0.
+// Page scores: eight lanes per page, each over D/8 channels, fp32 products
+// formed exactly in fp64 and added there, then summed over the eight lanes
+// (a butterfly, so every lane of a page holds the same sum); each pass's
+// loads go out one pass ahead, the first at entry.
+template <int D, int GM>
 __global__ __launch_bounds__(64) void k_step_f32(LayerView L, StepIO io, float scale_log2) {
-    constexpr int DPL = D / 64;
+    constexpr int DPL = D / 64;  // channels per lane in the value pass
+    constexpr int CPP = D / 8;   // channels per lane in the page scores
+    constexpr int VG = GM * DPL >= 32 ? 8 : 16;  // tokens whose value rows load together
+    __shared__ __align__(16) float s_q[GM * D];
+    __shared__ float s_p[GM][64];  // the chunk's weights, per head and token
     const int lane = threadIdx.x;
     const int nsplit = L.nsplit;
     const int u = blockIdx.x / nsplit, split = blockIdx.x - (blockIdx.x / nsplit) * nsplit;
     if (io.active != nullptr && io.active[u / L.nkv] == 0) return;
     const int G = L.G, S = L.S, ps = L.ps;
     const size_t base = (size_t)u * S;
-    const int32_t* U4 = L.unit + (size_t)u * kUnitFields;
-    const int ns = U4[kNextSlot], nf = U4[kNextFill];
-    const bool opened = nf == 0;
-    const int row_new = ns * ps + nf;
     const int t0 = split * L.bps * 32;
     const int t1 = max(t0, min(min(S * ps, 32 * L.nblk), t0 + L.bps * 32));
     const float* Ku = (const float*)L.K + (size_t)u * L.Lcap * D;
@@ -1223,45 +1232,117 @@ __global__ __launch_bounds__(64) void k_step_f32(LayerView L, StepIO io, float s
     const float* vn_g = (const float*)io.v_new + (size_t)u * D;
     const int32_t* fu = L.fill_att + base;  // fills the attention sees
 
-    float qr[16][DPL], m[16], l[16], acc[16][DPL];
+    // this lane's key row; the first chunk's now (rows below t1 lie inside
+    // the unit's pool)
+    float kr[D];
+    auto load_key = [&](const float* kp) {
 #pragma unroll
-    for (int j = 0; j < 16; ++j) {
+        for (int c = 0; c < D; c += 4) {
+            const float4 x = *reinterpret_cast<const float4*>(kp + c);
+            kr[c] = x.x;
+            kr[c + 1] = x.y;
+            kr[c + 2] = x.z;
+            kr[c + 3] = x.w;
+        }
+    };
+    load_key(Ku + (size_t)min(t0 + lane, max(t1 - 1, 0)) * D);
+    // page state and representative keys of a score pass (pages pb .. pb+7,
+    // clamped into the split's pages), loaded one pass ahead
+    const int sl0 = min(S, (t0 + ps - 1) / ps), sl1 = min(S, (t1 + ps - 1) / ps);
+    const int part = lane & 7, cb = part * CPP;
+    float4 kx_nx[CPP / 4], kn_nx[CPP / 4];
+    int st_nx = kFree;
+    auto score_load = [&](int pb) {
+        const size_t p = base + min(pb + (lane >> 3), sl1 - 1);
+        st_nx = L.state[p];
+#pragma unroll
+        for (int c = 0; c < CPP; c += 4) {
+            kx_nx[c / 4] = *reinterpret_cast<const float4*>((const float*)L.kmax + p * D + cb + c);
+            kn_nx[c / 4] = *reinterpret_cast<const float4*>((const float*)L.kmin + p * D + cb + c);
+        }
+    };
+    if (sl0 < sl1) score_load(sl0);
+    const int32_t* U4 = L.unit + (size_t)u * kUnitFields;
+    const int ns = U4[kNextSlot], nf = U4[kNextFill];
+    const bool opened = nf == 0;
+    const int row_new = ns * ps + nf;
+    for (int i = lane; i < GM * D; i += 64) s_q[i] = i < G * D ? qg[i] : 0.0f;  // heads past G: zero
+    __syncthreads();
+
+    float m[GM], l[GM], acc[GM][DPL];
+#pragma unroll
+    for (int j = 0; j < GM; ++j) {
         m[j] = -INFINITY;
         l[j] = 0.0f;
 #pragma unroll
-        for (int i = 0; i < DPL; ++i) {
-            qr[j][i] = (j < G) ? qg[(size_t)j * D + lane + 64 * i] : 0.0f;
-            acc[j][i] = 0.0f;
-        }
+        for (int i = 0; i < DPL; ++i) acc[j][i] = 0.0f;
     }
-    for (int t = t0; t < t1; ++t) {
-        const int slot = t / ps;
-        const int f = (slot == ns) ? nf + 1 : fu[slot];
-        if (t - slot * ps >= f) continue;
-        float kr[DPL], vr[DPL];
-#pragma unroll
-        for (int i = 0; i < DPL; ++i) {
-            kr[i] = (t == row_new) ? kn_g[lane + 64 * i] : Ku[(size_t)t * D + lane + 64 * i];
-            vr[i] = (t == row_new) ? vn_g[lane + 64 * i] : Vu[(size_t)t * D + lane + 64 * i];
+    for (int c0 = t0; c0 < t1; c0 += 64) {
+        const int t = c0 + lane;
+        if (c0 > t0) load_key(Ku + (size_t)min(t, t1 - 1) * D);  // later chunks' key rows
+        bool valid = false;
+        if (t < t1) {
+            const int slot = t / ps;
+            const int f = (slot == ns) ? nf + 1 : fu[slot];
+            valid = t - slot * ps < f;
         }
+        const unsigned long long vmask = __ballot(valid);
+        if (vmask == 0) continue;
+        if (t == row_new) load_key(kn_g);
+        float sc[GM];
 #pragma unroll
-        for (int j = 0; j < 16; ++j) {
-            if (j >= G) break;
-            float dot = 0.0f;
+        for (int j = 0; j < GM; ++j) {
+            sc[j] = 0.0f;
 #pragma unroll
-            for (int i = 0; i < DPL; ++i) dot = fmaf(qr[j][i], kr[i], dot);
-            const float x = wave_sum(dot) * scale_log2;
-            const float m_new = fmaxf(m[j], x);
+            for (int c = 0; c < D; c += 4) {
+                const float4 q4 = *reinterpret_cast<const float4*>(s_q + j * D + c);
+                sc[j] = fmaf(q4.x, kr[c], sc[j]);
+                sc[j] = fmaf(q4.y, kr[c + 1], sc[j]);
+                sc[j] = fmaf(q4.z, kr[c + 2], sc[j]);
+                sc[j] = fmaf(q4.w, kr[c + 3], sc[j]);
+            }
+        }
+        // every head slot runs (those past G on zero queries, never written out)
+#pragma unroll
+        for (int j = 0; j < GM; ++j) {
+            const float x = valid ? sc[j] * scale_log2 : -INFINITY;
+            float mx = x;
+#pragma unroll
+            for (int off = 32; off >= 1; off >>= 1) mx = fmaxf(mx, __shfl_xor(mx, off));
+            const float m_new = fmaxf(m[j], mx);  // finite: some lane holds a token
             const float alpha = __builtin_amdgcn_exp2f(m[j] - m_new);
-            const float p = __builtin_amdgcn_exp2f(x - m_new);
-            l[j] = l[j] * alpha + p;
+            const float p = valid ? __builtin_amdgcn_exp2f(x - m_new) : 0.0f;
+            l[j] = l[j] * alpha + wave_sum(p);
 #pragma unroll
-            for (int i = 0; i < DPL; ++i) acc[j][i] = fmaf(p, vr[i], acc[j][i] * alpha);
+            for (int i = 0; i < DPL; ++i) acc[j][i] *= alpha;
+            s_p[j][lane] = p;
             m[j] = m_new;
         }
+        __syncthreads();
+#pragma unroll
+        for (int g0 = 0; g0 < 64; g0 += VG) {
+            float vr[VG][DPL];
+#pragma unroll
+            for (int e = 0; e < VG; ++e) {
+                const int tt = c0 + g0 + e;
+                const uint32_t keep = 0u - (uint32_t)((vmask >> (g0 + e)) & 1ull);  // all ones or zero
+                const float* vp = (tt == row_new) ? vn_g : Vu + (size_t)min(tt, t1 - 1) * D;
+#pragma unroll
+                for (int i = 0; i < DPL; ++i) vr[e][i] = __uint_as_float(__float_as_uint(vp[lane + 64 * i]) & keep);
+            }
+#pragma unroll
+            for (int e = 0; e < VG; ++e)
+#pragma unroll
+                for (int j = 0; j < GM; ++j) {
+                    const float p = s_p[j][g0 + e];
+#pragma unroll
+                    for (int i = 0; i < DPL; ++i) acc[j][i] = fmaf(p, vr[e][i], acc[j][i]);
+                }
+        }
+        __syncthreads();  // the weights are read before the next chunk writes them
     }
 #pragma unroll
-    for (int j = 0; j < 16; ++j) {
+    for (int j = 0; j < GM; ++j) {
         if (j >= G) break;
         float* pp = L.part + (((size_t)u * nsplit + split) * G + j) * (D + 2);
 #pragma unroll
@@ -1279,45 +1360,50 @@ __global__ __launch_bounds__(64) void k_step_f32(LayerView L, StepIO io, float s
             Vw[c] = vn_g[c];
         }
     }
-    // page scores: pages whose first row lies in this split
-    const int sl0 = min(S, (t0 + ps - 1) / ps), sl1 = min(S, (t1 + ps - 1) / ps);
-    for (int p = sl0 + lane; p < sl1; p += 64) {
+    // page scores: pages whose first row lies in this split, eight at a time
+    for (int pb = sl0; pb < sl1; pb += 8) {
+        const int p = pb + (lane >> 3);
         const bool tail = p == ns;
-        if (!(tail || ranked(L, L.state[base + p]))) continue;
-        float* kx = (float*)L.kmax + (base + p) * D;
-        float* kn = (float*)L.kmin + (base + p) * D;
+        const bool act = p < sl1 && (tail || ranked(L, st_nx));
+        float hi[CPP], lo[CPP];
+#pragma unroll
+        for (int c = 0; c < CPP; c += 4) {
+            const float4 a = kx_nx[c / 4], b = kn_nx[c / 4];
+            hi[c] = act ? a.x : 0.f, hi[c + 1] = act ? a.y : 0.f, hi[c + 2] = act ? a.z : 0.f;
+            hi[c + 3] = act ? a.w : 0.f;
+            lo[c] = act ? b.x : 0.f, lo[c + 1] = act ? b.y : 0.f, lo[c + 2] = act ? b.z : 0.f;
+            lo[c + 3] = act ? b.w : 0.f;
+        }
+        if (pb + 8 < sl1) score_load(pb + 8);
+        float* kx = (float*)L.kmax + (base + p) * D + cb;
+        float* kn = (float*)L.kmin + (base + p) * D + cb;
+        if (act && tail) {
+#pragma unroll
+            for (int c = 0; c < CPP; ++c) {
+                const float x = kn_g[cb + c];
+                hi[c] = opened ? x : fmaxf(hi[c], x);
+                lo[c] = opened ? x : fminf(lo[c], x);
+                kx[c] = hi[c];
+                kn[c] = lo[c];
+            }
+        }
         double best = -INFINITY;
-        double accj[16];
+#pragma unroll 1
+        for (int j = 0; j < G; ++j) {
+            double a = 0.0;
 #pragma unroll
-        for (int j = 0; j < 16; ++j) accj[j] = 0.0;
-        for (int c = 0; c < D; ++c) {
-            float hi = kx[c], lo = kn[c];
-            if (tail) {
-                const float x = kn_g[c];
-                hi = opened ? x : fmaxf(hi, x);
-                lo = opened ? x : fminf(lo, x);
-                kx[c] = hi;
-                kn[c] = lo;
+            for (int c = 0; c < CPP; ++c) {
+                const double qd = (double)s_q[j * D + cb + c];
+                const double x = qd * (double)hi[c], y = qd * (double)lo[c];
+                a += x > y ? x : y;
             }
-#pragma unroll
-            for (int j = 0; j < 16; ++j) {
-                if (j < G) {
-                    const double qd = (double)qg[(size_t)j * D + c];
-                    const double a = qd * (double)hi, b = qd * (double)lo;
-                    accj[j] += a > b ? a : b;
-                }
-            }
+            a += __shfl_xor(a, 1);
+            a += __shfl_xor(a, 2);
+            a += __shfl_xor(a, 4);
+            best = a > best ? a : best;
+            if (act && L.agg && part == 0) L.score[(base + p) * G + j] = a;
         }
-#pragma unroll
-        for (int j = 0; j < 16; ++j)
-            if (j < G) best = accj[j] > best ? accj[j] : best;
-        if (L.agg) {
-#pragma unroll
-            for (int j = 0; j < 16; ++j)
-                if (j < G) L.score[(base + p) * G + j] = accj[j];
-        } else {
-            L.score[base + p] = best;
-        }
+        if (act && !L.agg && part == 0) L.score[base + p] = best;
     }
 }
 
@@ -1684,14 +1770,21 @@ hipError_t launch_prefill(const LayerView& L, const void* k, const void* v, cons
     return hipGetLastError();
 }
 
+// fp32 step kernel with room for GM >= G query heads (the head loops unroll
+// GM times: a small bound keeps the kernel's code small)
+template <int D>
+void launch_step_f32(const LayerView& L, const StepIO& io, dim3 grid, float sl2, hipStream_t s) {
+    if (L.G <= 4) hipLaunchKernelGGL((k_step_f32<D, 4>), grid, dim3(64), 0, s, L, io, sl2);
+    else if (L.G <= 8) hipLaunchKernelGGL((k_step_f32<D, 8>), grid, dim3(64), 0, s, L, io, sl2);
+    else hipLaunchKernelGGL((k_step_f32<D, 16>), grid, dim3(64), 0, s, L, io, sl2);
+}
+
 hipError_t launch_step(const LayerView& L, const StepIO& io, const StepPlan& pl, double r, hipStream_t s) {
     const float sl2 = (float)(1.4426950408889634 / sqrt((double)L.D));
     if (!L.bf16) {
         const dim3 grid((unsigned)(L.U * pl.nsplit));
-        if (L.D == 128)
-            hipLaunchKernelGGL(k_step_f32<128>, grid, dim3(64), 0, s, L, io, sl2);
-        else
-            hipLaunchKernelGGL(k_step_f32<64>, grid, dim3(64), 0, s, L, io, sl2);
+        if (L.D == 128) launch_step_f32<128>(L, io, grid, sl2, s);
+        else launch_step_f32<64>(L, io, grid, sl2, s);
         return hipGetLastError();
     }
     if (L.D == 128) {
