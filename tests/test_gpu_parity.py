@@ -108,6 +108,30 @@ def test_edge_cases(edge):
     _report(rep, "edge")
 
 
+# fp32 step kernel instances (head slots GM = 4, 8, 16 at d 64 and 128) and
+# split shapes: one wavefront walking several 64-token chunks, uneven splits
+F32_SHAPES = [
+    dict(n_q_heads=32, n_kv_heads=2, head_dim=128),              # G 16, d 128
+    dict(n_q_heads=32, n_kv_heads=2, head_dim=64),               # G 16, d 64
+    dict(n_q_heads=16, n_kv_heads=2, head_dim=128),              # G 8
+    dict(n_q_heads=2, n_kv_heads=2, head_dim=128),               # G 1: three idle head slots
+    dict(budget=512, prefill_len=100, decode_steps=520, splits=1),   # eight chunks in one wavefront
+    dict(budget=512, prefill_len=100, decode_steps=520, splits=3),   # uneven splits, ragged last chunk
+    dict(budget=80, page_size=8, prefill_len=3, splits=2),       # ragged pages and chunks
+]
+
+
+@pytest.mark.parametrize("shape", F32_SHAPES, ids=[",".join("%s=%s" % kv for kv in e.items()) for e in F32_SHAPES])
+def test_f32_kernel_shapes(shape):
+    shape = dict(shape)
+    splits = shape.pop("splits", 0)
+    w = small(dtype="f32", decode_steps=shape.pop("decode_steps", 200), **shape)
+    _say("case f32 %s splits %d" % (shape, splits))
+    rep = run_parity(w, seed=11, steps=w.decode_steps, splits=splits)
+    _report(rep, "f32")
+    assert rep.outputs_compared > 0
+
+
 def test_multi_layer_independent():
     """Layers have their own pages and clocks; stepping one leaves the others."""
     import torch
