@@ -792,9 +792,12 @@ __device__ __forceinline__ void attend_block(const u32x4 (&kr)[2][D / 32], const
 // picks the top k and claims their blocks. 0: no prompt region.
 // NT: K/V blocks are read with non-temporal loads (pools too large for the
 // memory-side cache to serve the next step).
-template <int D, int NW, bool AGG, int LM, bool NT = false>
-__global__ __launch_bounds__(NW * 64) __attribute__((amdgpu_waves_per_eu(2, 2))) void k_step_bf16(
-    LayerView L, StepIO io, float scale_log2, double r, int fused) {
+// The step of work item wi = unit * nsplit + split, by one workgroup (the
+// arguments by value: as kernel arguments, they leave the registers of the
+// block loop alone).
+template <int D, int NW, bool AGG, int LM, bool NT>
+__device__ __forceinline__ void step_item(LayerView L, StepIO io, float scale_log2, double r, int fused,
+                                          const int wi) {
     constexpr int KS = D / 32, NB = D / 16, BLK = 32 * D;
     extern __shared__ __align__(16) unsigned char smem[];
     __shared__ float s_m[NW][16];
@@ -824,7 +827,8 @@ __global__ __launch_bounds__(NW * 64) __attribute__((amdgpu_waves_per_eu(2, 2)))
     const int tid = threadIdx.x, lane = tid & 63, w = tid >> 6;
     const int grp = lane >> 4, col = lane & 15;
     const int nsplit = L.nsplit;
-    const int u = blockIdx.x / nsplit, split = blockIdx.x - (blockIdx.x / nsplit) * nsplit;
+    const unsigned uwi = (unsigned)wi;  // (unsigned arithmetic, as on blockIdx.x)
+    const int u = uwi / nsplit, split = uwi - (uwi / nsplit) * nsplit;
     if (io.active != nullptr && io.active[u / L.nkv] == 0) return;  // the sequence sits this step out
     const size_t base = (size_t)u * S;
     // this workgroup's claims lo .. hi-1: blocks of the unit (a range), or
@@ -1196,6 +1200,13 @@ __global__ __launch_bounds__(NW * 64) __attribute__((amdgpu_waves_per_eu(2, 2)))
             }
         }
     }
+}
+
+// Step kernel (bf16 pools): rows a1-a6 for work item blockIdx.x.
+template <int D, int NW, bool AGG, int LM, bool NT = false>
+__global__ __launch_bounds__(NW * 64) __attribute__((amdgpu_waves_per_eu(2, 2))) void k_step_bf16(
+    LayerView L, StepIO io, float scale_log2, double r, int fused) {
+    step_item<D, NW, AGG, LM, NT>(L, io, scale_log2, r, fused, blockIdx.x);
 }
 
 // Step kernel, fp32 pools: one wavefront per (unit, split), over its rows in

@@ -424,6 +424,31 @@ def test_ragged_batch(case):
     assert rep.evictions > 0
 
 
+# 640 units in workgroups of 4 wavefronts, two per CU: 512 fit at once, so
+# the hardware starts the other 128 as the first ones finish
+def _many_units_workload(**kw):
+    return small(batch=160, n_q_heads=16, n_kv_heads=4, budget=160, prefill_len=40, decode_steps=200, **kw)
+
+
+def test_many_units_every_step():
+    """More units than workgroups that fit at once: every unit, every step."""
+    w = _many_units_workload()
+    _say("case many units %d" % (w.batch * w.n_kv_heads))
+    rep = run_parity(w, seed=13, steps=w.decode_steps)
+    _report(rep, "many units")
+    assert rep.units_checked == w.batch * w.n_kv_heads and rep.evictions > 0
+
+
+def test_many_units_ragged():
+    """The same with a mask of active sequences and prompts replaced mid-run."""
+    w = _many_units_workload()
+    lens = [(37 * i) % 300 for i in range(w.batch)]
+    _say("case many units ragged")
+    rep = run_ragged(w, seed=23, lens=lens, steps=w.decode_steps, reprefill={80: {3: 0, 77: 290}})
+    _report(rep, "many units ragged")
+    assert rep.evictions > 0
+
+
 @pytest.mark.parametrize("name,steps,units", [("mistral7b-b4-P128-L1024", 1100, 6), ("mistral7b-b4-P128-dense", 300, 4)])
 def test_decode_sweep_shapes(name, steps, units):
     """The decode-length sweep's layer (prompt 128, batch 4, split over
