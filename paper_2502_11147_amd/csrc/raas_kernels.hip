@@ -1546,17 +1546,35 @@ __global__ __launch_bounds__(256) void k_epilogue(LayerView L, StepIO io, double
     const int u0 = blockIdx.x * nu;
     if (io.active != nullptr && io.active[u0 / L.nkv] == 0) return;
     const size_t base = (size_t)u0 * S;
+    // The first pass's reads go out together with the slots': the page
+    // score of slot tid (max over the units; read whether or not the page
+    // turns out to be ranked) and the first unit's running maximum and sum
+    // of item tid of the merge.
+    double sc_first = -INFINITY;
+    if (!L.agg && tid < S) {
+        sc_first = L.score[base + tid];
+#pragma unroll 8
+        for (int h = 1; h < nu; ++h) sc_first = fmax(sc_first, L.score[base + (size_t)h * S + tid]);
+    }
+    float m_first = 0.0f, l_first = 0.0f;
+    if (merge && tid < nsplit * G) {
+        const float* pf = L.part + (size_t)u0 * nsplit * G * (D + 2) + (size_t)tid * (D + 2);
+        m_first = pf[D];
+        l_first = pf[D + 1];
+    }
     const UnitRec ur = read_unit(L, u0);
     load_slots(L, u0, ur, s_score, s_state, s_ts, s_lid);
     __syncthreads();
-    if (!L.agg)
-        for (int s = tid; s < S; s += nth)
+    if (!L.agg) {
+        if (tid < S && ranked(L, s_state[tid])) s_score[tid] = sc_first;
+        for (int s = tid + nth; s < S; s += nth)
             if (ranked(L, s_state[s])) {
                 double best = L.score[base + s];
 #pragma unroll 8
                 for (int h = 1; h < nu; ++h) best = fmax(best, L.score[base + (size_t)h * S + s]);
                 s_score[s] = best;
             }
+    }
     __syncthreads();
     if (L.agg) softmax_sum_block(L, L.score + base * G, nu, s_state, s_score, s_mz, tid, nth);
     refresh_block(L, ur, r, s_score, s_state, s_ts, s_aux, tid, nth);
@@ -1566,7 +1584,11 @@ __global__ __launch_bounds__(256) void k_epilogue(LayerView L, StepIO io, double
         const int u = u0 + uh;
         const float* pu = L.part + (size_t)u * nsplit * G * (D + 2);
         // every split's running max and sum, then per head the weights' sum
-        for (int i = tid; i < nsplit * G; i += nth) {
+        if (uh == 0 && tid < nsplit * G) {
+            s_ml[2 * tid] = m_first;
+            s_ml[2 * tid + 1] = l_first;
+        }
+        for (int i = uh == 0 ? tid + nth : tid; i < nsplit * G; i += nth) {
             s_ml[2 * i] = pu[(size_t)i * (D + 2) + D];
             s_ml[2 * i + 1] = pu[(size_t)i * (D + 2) + D + 1];
         }
