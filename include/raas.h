@@ -20,8 +20,8 @@
  *      0.5 = above the median, Section 3.2);
  *   5. when the next token has no room (tail page full, no free slot),
  *      evicts the evictable page with the oldest timestamp, ties to the
- *      smallest logical page id (Algorithm 1, "evict KVs with the oldest
- *      timestamps").
+ *      smallest logical page id (Algorithm 1, eviction in the decode-stage
+ *      store).
  *
  * Conventions for every call:
  *  - Tensor arguments are DEVICE pointers owned by the caller, contiguous,
@@ -51,7 +51,7 @@
 extern "C" {
 #endif
 
-#define RAAS_ABI_VERSION 2
+#define RAAS_ABI_VERSION 3
 
 typedef enum {
     RAAS_OK = 0,
@@ -100,7 +100,9 @@ typedef struct {
     int32_t page_size;      /* tokens per page: 8, 16, 32, 64 or 128 (the paper uses 16) */
     int32_t budget_tokens;  /* L: multiple of page_size, 2 <= L/page_size <= 2048 */
     int32_t dtype;          /* raas_dtype of q, k, v and out */
-    float r;                /* fraction of evictable pages refreshed per step, in [0, 1] (0.5) */
+    double r;               /* fraction of evictable pages refreshed per step, in [0, 1] (0.5);
+                               k = floor(r * n) is taken in double precision, so that r = 0.7 at
+                               n = 10 refreshes 7 pages (a float 0.7 lies below 0.7) */
     int32_t prefill_policy; /* raas_prefill_policy */
     /* Variants of step 3-4 (0, 0 = the behaviour described above): */
     int32_t score_aggregation; /* raas_score_aggregation */

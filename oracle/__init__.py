@@ -71,6 +71,12 @@ def load(path: str | None = None) -> ctypes.CDLL:
         lib.orc_last_attended.restype = None
         lib.orc_set_variant.argtypes = [vp, ctypes.c_int, ctypes.c_int]
         lib.orc_set_variant.restype = ctypes.c_int
+        lib.orc_adopt_retention.argtypes = [vp, ip, ip, ctypes.c_int]
+        lib.orc_adopt_retention.restype = ctypes.c_int
+        lib.orc_state_batch.argtypes = [ctypes.POINTER(vp), ctypes.c_int, ip, ip, ip]
+        lib.orc_state_batch.restype = None
+        lib.orc_scores_batch.argtypes = [ctypes.POINTER(vp), ctypes.c_int, dp, dp]
+        lib.orc_scores_batch.restype = None
         lib.orc_set_threads.argtypes = [ctypes.c_int]
         lib.orc_set_threads.restype = None
         lib.orc_threads.argtypes = []
@@ -165,6 +171,17 @@ class Kvm:
                     clock=int(un[2]), evicted=int(un[3]), n_evictable=int(un[4]),
                     k_refreshed=int(un[5]))
 
+    def adopt_retention(self, page_table, ts, evicted: int):
+        """Lockstep test hook: take another implementation's retention
+        decision of the last step (orc_adopt_retention). Raises when it
+        differs in more than the step's own decisions."""
+        pt = np.ascontiguousarray(page_table, np.int32)
+        t = np.ascontiguousarray(ts, np.int32)
+        ip = ctypes.POINTER(ctypes.c_int)
+        rc = self.lib.orc_adopt_retention(self._h, pt.ctypes.data_as(ip), t.ctypes.data_as(ip), int(evicted))
+        if rc != OK:
+            raise OracleError(rc, "orc_adopt_retention")
+
     def last_attended(self):
         """slots the last step attended to (with outputs requested), as bools"""
         a = np.empty(self.S, np.int32)
@@ -204,6 +221,28 @@ def decode_batch(units: list[Kvm], q, k, v, want_out: bool = True):
     if rc != OK:
         raise OracleError(rc, "orc_decode_batch")
     return out
+
+
+def state_batch(units: list[Kvm]):
+    """Page tables and timestamps [n][S] and evicted ids [n] of n alike units."""
+    n, S = len(units), units[0].S
+    arr = (ctypes.c_void_p * n)(*[u.handle for u in units])
+    pt = np.empty((n, S), np.int32)
+    ts = np.empty((n, S), np.int32)
+    ev = np.empty(n, np.int32)
+    ip = ctypes.POINTER(ctypes.c_int)
+    units[0].lib.orc_state_batch(arr, n, pt.ctypes.data_as(ip), ts.ctypes.data_as(ip), ev.ctypes.data_as(ip))
+    return pt, ts, ev
+
+
+def scores_batch(units: list[Kvm]):
+    """Last step's page scores [n][S] (NaN where not ranked) and thresholds [n]."""
+    n, S = len(units), units[0].S
+    arr = (ctypes.c_void_p * n)(*[u.handle for u in units])
+    sc = np.empty((n, S), np.float64)
+    th = np.empty(n, np.float64)
+    units[0].lib.orc_scores_batch(arr, n, _dptr(sc), _dptr(th))
+    return sc, th
 
 
 def decode_group(units: list[Kvm], q, k, v, want_out: bool = True):

@@ -83,6 +83,7 @@ typedef struct {
     double *score; /* [S], NaN where the slot is not evictable */
     double theta;  /* the threshold; -inf when every page was refreshed, NaN when none */
     int n_evictable, k_refreshed, evicted;
+    int evicted_slot, evicted_tail; /* slot of the evicted page, and whether it was the tail */
 } orc_kvm;
 
 orc_kvm* orc_new(int G, int d, int ps, int S, double r, int policy) {
@@ -109,6 +110,7 @@ orc_kvm* orc_new(int G, int d, int ps, int S, double r, int policy) {
     }
     m->tail = -1;
     m->evicted = -1;
+    m->evicted_slot = -1;
     m->theta = NAN;
     return m;
 }
@@ -397,6 +399,8 @@ static void refresh(orc_kvm* m, int c) {
 static int evict_if_full(orc_kvm* m) {
     const int S = m->S;
     m->evicted = -1;
+    m->evicted_slot = -1;
+    m->evicted_tail = 0;
     if (is_full(m)) {
         int v = -1;
         for (int s = 0; s < S; ++s) {
@@ -405,6 +409,8 @@ static int evict_if_full(orc_kvm* m) {
         }
         if (v < 0) return ORC_E_INTERNAL;
         m->evicted = m->lid[v];
+        m->evicted_slot = v;
+        m->evicted_tail = m->tail == v;
         m->state[v] = FREE;
         m->lid[v] = -1;
         m->ts[v] = -1;
@@ -523,6 +529,84 @@ void orc_state(const orc_kvm* m, int* page_table, int* ts, int* state, int* fill
         unit[3] = m->evicted;
         unit[4] = m->n_evictable;
         unit[5] = m->k_refreshed;
+    }
+}
+
+/*
+ * Test hook of the lockstep comparison (not part of the method): after a
+ * step whose threshold was a near tie, take another implementation's
+ * retention decision for this step, given as its page table (lid or -1 per
+ * slot), timestamps (-1 unless evictable) and evicted lid. Only what the
+ * step itself decided may differ from this kvm's state: the timestamps of
+ * evictable pages and which full page was evicted. The page this kvm
+ * evicted comes back from its slot (its keys and values are still there:
+ * nothing is stored between the eviction and the next step), and the page
+ * the other side evicted is freed. Anything else is ORC_E_INVALID and
+ * leaves the state unchanged.
+ */
+int orc_adopt_retention(orc_kvm* m, const int* page_table, const int* ts, int evicted) {
+    if (!m || !page_table || !ts || !m->prefilled) return ORC_E_INVALID;
+    const int S = m->S;
+    int freed = -1, back = -1;
+    for (int s = 0; s < S; ++s) {
+        const int pt = page_table[s];
+        if (m->state[s] == PINNED) {
+            if (pt != m->lid[s] || ts[s] != -1) return ORC_E_INVALID;
+        } else if (m->state[s] == EVICTABLE) {
+            if (pt == m->lid[s]) {
+                if (ts[s] < 0 || ts[s] > m->clock) return ORC_E_INVALID;
+            } else if (pt == -1 && ts[s] == -1 && m->fill[s] == m->ps && freed < 0 && evicted == m->lid[s]) {
+                freed = s; /* the other side's victim: a full page */
+            } else {
+                return ORC_E_INVALID;
+            }
+        } else { /* FREE */
+            if (pt == -1) {
+                if (ts[s] != -1) return ORC_E_INVALID;
+            } else if (s == m->evicted_slot && pt == m->evicted && ts[s] >= 0 && ts[s] <= m->clock) {
+                back = s; /* this kvm's victim, kept by the other side */
+            } else {
+                return ORC_E_INVALID;
+            }
+        }
+    }
+    if ((freed >= 0) != (back >= 0)) return ORC_E_INVALID; /* one eviction each, or the same one */
+    if (freed < 0 && evicted != m->evicted) return ORC_E_INVALID;
+    for (int s = 0; s < S; ++s)
+        if (m->state[s] == EVICTABLE && s != freed) m->ts[s] = ts[s];
+    if (back >= 0) {
+        m->state[back] = EVICTABLE;
+        m->lid[back] = m->evicted;
+        m->fill[back] = m->ps; /* evicted pages are full */
+        m->ts[back] = ts[back];
+        if (m->evicted_tail) m->tail = back;
+        m->state[freed] = FREE;
+        m->lid[freed] = -1;
+        m->ts[freed] = -1;
+        m->fill[freed] = 0;
+        m->evicted_tail = m->tail == freed;
+        if (m->tail == freed) m->tail = -1;
+        m->evicted = evicted;
+        m->evicted_slot = freed;
+    }
+    return ORC_OK;
+}
+
+/* orc_state of n kvms at once: page_table, ts [n][S] (S of the first), evicted [n] */
+void orc_state_batch(orc_kvm** ms, int n, int* page_table, int* ts, int* evicted) {
+    const int S = ms[0]->S;
+    for (int u = 0; u < n; ++u) {
+        orc_state(ms[u], page_table + (size_t)u * S, ts + (size_t)u * S, NULL, NULL, NULL);
+        evicted[u] = ms[u]->evicted;
+    }
+}
+
+/* orc_last_scores of n kvms at once: score [n][S], theta [n] */
+void orc_scores_batch(orc_kvm** ms, int n, double* score, double* theta) {
+    const int S = ms[0]->S;
+    for (int u = 0; u < n; ++u) {
+        memcpy(score + (size_t)u * S, ms[u]->score, sizeof(double) * (size_t)S);
+        theta[u] = ms[u]->theta;
     }
 }
 

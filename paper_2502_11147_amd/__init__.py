@@ -45,7 +45,7 @@ class Config(ctypes.Structure):
         ("page_size", ctypes.c_int32),
         ("budget_tokens", ctypes.c_int32),
         ("dtype", ctypes.c_int32),
-        ("r", ctypes.c_float),
+        ("r", ctypes.c_double),
         ("prefill_policy", ctypes.c_int32),
         ("score_aggregation", ctypes.c_int32),
         ("rank_pinned", ctypes.c_int32),

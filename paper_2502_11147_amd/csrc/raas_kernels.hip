@@ -224,9 +224,9 @@ __global__ void k_prefill_rep(LayerView L, const T* __restrict__ k, PrefillIn in
 //    k = floor(r*n), page p gets ts = clock when at least n-k evictable
 //    pages score strictly less, i.e. exactly the pages above the (n-k)-th
 //    smallest score.
-//  - Eviction (Algorithm 1, "if kvm.is_full(): evict KVs with the oldest
-//    timestamps"): when the tail page is full and no slot is free, the
-//    evictable page with the smallest (timestamp, logical id) is freed.
+//  - Eviction (Algorithm 1, the eviction branch of the decode-stage store):
+//    when the tail page is full and no slot is free, the evictable page
+//    with the smallest (timestamp, logical id) is freed.
 //  - The next token's target: the tail page if it has room, else the lowest
 //    free slot (a fresh page).
 
@@ -466,7 +466,7 @@ __device__ void softmax_sum_block(const LayerView& L, const double* hb, int nu, 
 //    less, i.e. exactly the pages above the (n-k)-th smallest score (the
 //    ranked pages are the evictable ones, plus the pinned ones when the pool
 //    ranks them; pinned pages never take a timestamp);
-//  - eviction ("if kvm.is_full(): evict KVs with the oldest timestamps"):
+//  - eviction (Algorithm 1, the eviction branch of the decode-stage store):
 //    when the tail page is full and no slot is free, the evictable page with
 //    the smallest (timestamp, logical id) is freed;
 //  - the next token's target: the tail page if it has room, else the lowest
@@ -1131,7 +1131,7 @@ __device__ __forceinline__ void step_item(LayerView L, StepIO io, float scale_lo
                         }
                     }
                 }
-                // append: store the new token in the pool (Algorithm 1, "Store K_new and V_new")
+                // append: the new token joins the pool (Algorithm 1, decode-stage store)
                 uint16_t* Kw = (uint16_t*)L.K + (size_t)u * L.Lcap * D;
                 uint16_t* Vw = (uint16_t*)L.V + (size_t)u * L.Lcap * D;
                 if (lane < D / 8) st4(Kw + k_off<D>(row_new, lane * 8), ld4(&s_kn[lane * 8]));

@@ -174,7 +174,7 @@ raas_status validate(const raas_config* c) {
                     S);
     if (c->dtype != RAAS_F32 && c->dtype != RAAS_BF16)
         return fail(RAAS_E_INVALID, "dtype must be RAAS_F32 or RAAS_BF16 (got %d)", c->dtype);
-    if (!(c->r >= 0.0f && c->r <= 1.0f)) return fail(RAAS_E_INVALID, "r must lie in [0, 1]");
+    if (!(c->r >= 0.0 && c->r <= 1.0)) return fail(RAAS_E_INVALID, "r must lie in [0, 1]");
     if (c->prefill_policy != RAAS_PREFILL_PIN_HEAD && c->prefill_policy != RAAS_PREFILL_ERROR)
         return fail(RAAS_E_INVALID, "unknown prefill_policy %d", c->prefill_policy);
     if (c->score_aggregation != RAAS_SCORE_MAX && c->score_aggregation != RAAS_SCORE_SOFTMAX_SUM)
@@ -476,12 +476,12 @@ raas_status raas_decode_step_masked(raas_pool* p, int32_t layer, const void* q, 
         if (e != hipSuccess) return hip_fail(e, "prompt selection launch");
     }
     prof_record(p, 0, true, s);
-    hipError_t e = launch_step(L, io, pl, (double)p->cfg.r, s);
+    hipError_t e = launch_step(L, io, pl, p->cfg.r, s);
     prof_record(p, 0, false, s);
     if (e != hipSuccess) return hip_fail(e, "step launch");
     if (!pl.fused) {
         prof_record(p, 1, true, s);
-        e = launch_epilogue(L, io, (double)p->cfg.r, s);
+        e = launch_epilogue(L, io, p->cfg.r, s);
         prof_record(p, 1, false, s);
         if (e != hipSuccess) return hip_fail(e, "epilogue launch");
     }

@@ -61,8 +61,13 @@ def _load():
         wp = ctypes.POINTER(_SynthWorkload)
         lib.synth_prefill.argtypes = [wp, ctypes.c_int, fp, fp]
         lib.synth_prefill.restype = None
+        lib.synth_prefill_units.argtypes = [wp, ctypes.c_int, ctypes.POINTER(ctypes.c_int), ctypes.c_int, fp, fp]
+        lib.synth_prefill_units.restype = None
         lib.synth_steps.argtypes = [wp, ctypes.c_int, ctypes.c_int, ctypes.c_int, fp, fp, fp]
         lib.synth_steps.restype = None
+        lib.synth_steps_units.argtypes = [wp, ctypes.c_int, ctypes.c_int, ctypes.c_int,
+                                          ctypes.POINTER(ctypes.c_int), ctypes.c_int, fp, fp, fp]
+        lib.synth_steps_units.restype = None
         lib.synth_active_milestones.argtypes = [
             wp, ctypes.c_int, ctypes.c_int, ctypes.c_int, ctypes.c_int,
             ctypes.POINTER(ctypes.c_int), ctypes.c_int,
@@ -100,6 +105,21 @@ def prefill(w: Workload, seed: int, layer: int = 0, prefill_len: int | None = No
     return K, V
 
 
+def prefill_units(w: Workload, seed: int, layer: int, prefill_len: int, units):
+    """prefill() restricted to chosen units (unit = sequence * n_kv_heads +
+    KV head), with the same values: K, V float32 [len(units)][P][head_dim]."""
+    lib = _load()
+    cw = _cstruct(w, seed)
+    cw.prefill_len = int(prefill_len)
+    u = np.ascontiguousarray(np.asarray(units, dtype=np.int32))
+    K = np.empty((len(u), cw.prefill_len, w.head_dim), np.float32)
+    V = np.empty((len(u), cw.prefill_len, w.head_dim), np.float32)
+    if len(u) and cw.prefill_len:
+        lib.synth_prefill_units(ctypes.byref(cw), int(layer), u.ctypes.data_as(ctypes.POINTER(ctypes.c_int)), len(u),
+                                _fptr(K), _fptr(V))
+    return K, V
+
+
 def steps(w: Workload, seed: int, layer: int, t0: int, n: int):
     """Decode inputs of steps t0..t0+n-1.
 
@@ -112,6 +132,23 @@ def steps(w: Workload, seed: int, layer: int, t0: int, n: int):
     v = np.empty((n, w.batch, w.n_kv_heads, w.head_dim), np.float32)
     if n > 0:
         lib.synth_steps(ctypes.byref(cw), int(layer), int(t0), int(n), _fptr(q), _fptr(k), _fptr(v))
+    return q, k, v
+
+
+def steps_units(w: Workload, seed: int, layer: int, t0: int, n: int, units):
+    """steps() restricted to chosen units (unit = sequence * n_kv_heads + KV
+    head), with the same values: q [n][len(units)][G][d], k and v
+    [n][len(units)][d] (float32)."""
+    lib = _load()
+    cw = _cstruct(w, seed)
+    u = np.ascontiguousarray(np.asarray(units, dtype=np.int32))
+    nu = len(u)
+    q = np.empty((n, nu, w.group, w.head_dim), np.float32)
+    k = np.empty((n, nu, w.head_dim), np.float32)
+    v = np.empty((n, nu, w.head_dim), np.float32)
+    if n > 0 and nu > 0:
+        lib.synth_steps_units(ctypes.byref(cw), int(layer), int(t0), int(n),
+                              u.ctypes.data_as(ctypes.POINTER(ctypes.c_int)), nu, _fptr(q), _fptr(k), _fptr(v))
     return q, k, v
 
 

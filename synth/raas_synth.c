@@ -141,22 +141,36 @@ static inline float round_to(int dtype, double x) {
     return f;
 }
 
+/* prefill K, V of one unit (sequence b, KV head h): [prefill_len][head_dim] each */
+static void unit_prefill(const synth_workload* w, int layer, int b, int h, float* K, float* V) {
+    const int P = w->prefill_len, d = w->head_dim;
+    double* tmp = (double*)malloc(sizeof(double) * (size_t)d);
+    for (int t = 0; t < P; ++t) {
+        size_t off = (size_t)t * d;
+        key_vec(w, KIND_PREFILL_K, (uint32_t)h, (uint32_t)layer, (uint32_t)b, (uint32_t)t, d, tmp);
+        for (int e = 0; e < d; ++e) K[off + e] = round_to(w->dtype, tmp[e]);
+        normal_vec(w, KIND_PREFILL_V, (uint32_t)h, (uint32_t)layer, (uint32_t)b, (uint32_t)t, d, tmp);
+        for (int e = 0; e < d; ++e) V[off + e] = round_to(w->dtype, tmp[e]);
+    }
+    free(tmp);
+}
+
 /* K, V: [batch][n_kv_heads][prefill_len][head_dim] */
 void synth_prefill(const synth_workload* w, int layer, float* K, float* V) {
-    const int B = w->batch, H = w->n_kv_heads, P = w->prefill_len, d = w->head_dim;
+    const int B = w->batch, H = w->n_kv_heads;
+    const size_t per = (size_t)w->prefill_len * w->head_dim;
 #pragma omp parallel for collapse(2) schedule(static)
     for (int b = 0; b < B; ++b)
-        for (int h = 0; h < H; ++h) {
-            double* tmp = (double*)malloc(sizeof(double) * (size_t)d);
-            for (int t = 0; t < P; ++t) {
-                size_t off = (((size_t)b * H + h) * P + t) * d;
-                key_vec(w, KIND_PREFILL_K, (uint32_t)h, (uint32_t)layer, (uint32_t)b, (uint32_t)t, d, tmp);
-                for (int e = 0; e < d; ++e) K[off + e] = round_to(w->dtype, tmp[e]);
-                normal_vec(w, KIND_PREFILL_V, (uint32_t)h, (uint32_t)layer, (uint32_t)b, (uint32_t)t, d, tmp);
-                for (int e = 0; e < d; ++e) V[off + e] = round_to(w->dtype, tmp[e]);
-            }
-            free(tmp);
-        }
+        for (int h = 0; h < H; ++h) unit_prefill(w, layer, b, h, K + ((size_t)b * H + h) * per, V + ((size_t)b * H + h) * per);
+}
+
+/* the same values for chosen units only (units[i] = sequence * n_kv_heads +
+ * KV head): K, V [nu][prefill_len][head_dim] */
+void synth_prefill_units(const synth_workload* w, int layer, const int* units, int nu, float* K, float* V) {
+    const int H = w->n_kv_heads;
+    const size_t per = (size_t)w->prefill_len * w->head_dim;
+#pragma omp parallel for schedule(dynamic, 1)
+    for (int i = 0; i < nu; ++i) unit_prefill(w, layer, units[i] / H, units[i] % H, K + (size_t)i * per, V + (size_t)i * per);
 }
 
 /* seeded phase of the unit's milestone schedule */
@@ -196,69 +210,88 @@ int synth_active_milestones(const synth_workload* w, int layer, int seq, int kvh
     return n;
 }
 
+/* decode inputs of one unit (sequence b, KV head h) at decode step t:
+ * q [G][d] (the unit's query heads), k [d], v [d] */
+static void unit_step(const synth_workload* w, int layer, int t, int b, int h, float* q, float* k, float* v) {
+    const int d = w->head_dim, G = w->n_q_heads / w->n_kv_heads;
+    const uint32_t tok = (uint32_t)t;
+    double* tmp = (double*)malloc(sizeof(double) * (size_t)d * 3);
+    double* u = tmp + d;
+    double* mk = tmp + 2 * d;
+    key_vec(w, KIND_DECODE_K, (uint32_t)h, (uint32_t)layer, (uint32_t)b, tok, d, tmp);
+    for (int e = 0; e < d; ++e) k[e] = round_to(w->dtype, tmp[e]);
+    normal_vec(w, KIND_DECODE_V, (uint32_t)h, (uint32_t)layer, (uint32_t)b, tok, d, tmp);
+    for (int e = 0; e < d; ++e) v[e] = round_to(w->dtype, tmp[e]);
+
+    /* direction u: normalised sum of the active milestones' unit keys */
+    int steps[64];
+    int na = synth_active_milestones(w, layer, b, h, t, steps, 64);
+    if (na > 64) na = 64;
+    for (int e = 0; e < d; ++e) u[e] = 0.0;
+    for (int a = 0; a < na; ++a) {
+        key_vec(w, KIND_DECODE_K, (uint32_t)h, (uint32_t)layer, (uint32_t)b, (uint32_t)steps[a], d, mk);
+        double nn = 0.0;
+        for (int e = 0; e < d; ++e) {
+            mk[e] = (double)round_to(w->dtype, mk[e]);
+            nn += mk[e] * mk[e];
+        }
+        nn = sqrt(nn);
+        for (int e = 0; e < d; ++e) u[e] += mk[e] / nn;
+    }
+    double un = 0.0;
+    for (int e = 0; e < d; ++e) un += u[e] * u[e];
+    un = sqrt(un);
+    for (int j = 0; j < G; ++j) {
+        const int head = h * G + j;
+        normal_vec(w, KIND_DECODE_Q, (uint32_t)head, (uint32_t)layer, (uint32_t)b, tok, d, tmp);
+        if (na > 0 && un > 0.0) {
+            double gn = 0.0, gu = 0.0;
+            for (int e = 0; e < d; ++e) {
+                gn += tmp[e] * tmp[e];
+                gu += tmp[e] * (u[e] / un);
+            }
+            gn = sqrt(gn);
+            double wn = 0.0;
+            for (int e = 0; e < d; ++e) {
+                double we = tmp[e] - gu * (u[e] / un);
+                wn += we * we;
+            }
+            wn = sqrt(wn);
+            for (int e = 0; e < d; ++e) {
+                double we = (tmp[e] - gu * (u[e] / un)) / (wn > 0.0 ? wn : 1.0);
+                tmp[e] = gn * (0.8 * (u[e] / un) + 0.6 * we);
+            }
+        }
+        for (int e = 0; e < d; ++e) q[(size_t)j * d + e] = round_to(w->dtype, tmp[e]);
+    }
+    free(tmp);
+}
+
 /* q: [n][batch][n_q_heads][d]; k, v: [n][batch][n_kv_heads][d]; decode steps t0..t0+n-1 */
 void synth_steps(const synth_workload* w, int layer, int t0, int n, float* q, float* k, float* v) {
-    const int B = w->batch, Hq = w->n_q_heads, H = w->n_kv_heads, d = w->head_dim;
-    const int G = Hq / H;
+    const int B = w->batch, H = w->n_kv_heads, d = w->head_dim;
+    const int G = w->n_q_heads / H;
 #pragma omp parallel for collapse(3) schedule(dynamic, 4)
     for (int s = 0; s < n; ++s)
         for (int b = 0; b < B; ++b)
             for (int h = 0; h < H; ++h) {
-                const int t = t0 + s;
-                const uint32_t tok = (uint32_t)t;
-                double* tmp = (double*)malloc(sizeof(double) * (size_t)d * 3);
-                double* u = tmp + d;
-                double* mk = tmp + 2 * d;
-                size_t off = (((size_t)s * B + b) * H + h) * d;
-                key_vec(w, KIND_DECODE_K, (uint32_t)h, (uint32_t)layer, (uint32_t)b, tok, d, tmp);
-                for (int e = 0; e < d; ++e) k[off + e] = round_to(w->dtype, tmp[e]);
-                normal_vec(w, KIND_DECODE_V, (uint32_t)h, (uint32_t)layer, (uint32_t)b, tok, d, tmp);
-                for (int e = 0; e < d; ++e) v[off + e] = round_to(w->dtype, tmp[e]);
-
-                /* direction u: normalised sum of the active milestones' unit keys */
-                int steps[64];
-                int na = synth_active_milestones(w, layer, b, h, t, steps, 64);
-                if (na > 64) na = 64;
-                for (int e = 0; e < d; ++e) u[e] = 0.0;
-                for (int a = 0; a < na; ++a) {
-                    key_vec(w, KIND_DECODE_K, (uint32_t)h, (uint32_t)layer, (uint32_t)b, (uint32_t)steps[a], d, mk);
-                    double nn = 0.0;
-                    for (int e = 0; e < d; ++e) {
-                        mk[e] = (double)round_to(w->dtype, mk[e]);
-                        nn += mk[e] * mk[e];
-                    }
-                    nn = sqrt(nn);
-                    for (int e = 0; e < d; ++e) u[e] += mk[e] / nn;
-                }
-                double un = 0.0;
-                for (int e = 0; e < d; ++e) un += u[e] * u[e];
-                un = sqrt(un);
-                for (int j = 0; j < G; ++j) {
-                    const int head = h * G + j;
-                    size_t qoff = (((size_t)s * B + b) * Hq + head) * d;
-                    normal_vec(w, KIND_DECODE_Q, (uint32_t)head, (uint32_t)layer, (uint32_t)b, tok, d, tmp);
-                    if (na > 0 && un > 0.0) {
-                        double gn = 0.0, gu = 0.0;
-                        for (int e = 0; e < d; ++e) {
-                            gn += tmp[e] * tmp[e];
-                            gu += tmp[e] * (u[e] / un);
-                        }
-                        gn = sqrt(gn);
-                        double wn = 0.0;
-                        for (int e = 0; e < d; ++e) {
-                            double we = tmp[e] - gu * (u[e] / un);
-                            wn += we * we;
-                        }
-                        wn = sqrt(wn);
-                        for (int e = 0; e < d; ++e) {
-                            double we = (tmp[e] - gu * (u[e] / un)) / (wn > 0.0 ? wn : 1.0);
-                            tmp[e] = gn * (0.8 * (u[e] / un) + 0.6 * we);
-                        }
-                    }
-                    for (int e = 0; e < d; ++e) q[qoff + e] = round_to(w->dtype, tmp[e]);
-                }
-                free(tmp);
+                const size_t uo = ((size_t)s * B + b) * H + h;
+                unit_step(w, layer, t0 + s, b, h, q + uo * G * d, k + uo * d, v + uo * d);
             }
+}
+
+/* the same values for chosen units only: units[i] = sequence * n_kv_heads +
+ * KV head; q: [n][nu][G][d]; k, v: [n][nu][d] */
+void synth_steps_units(const synth_workload* w, int layer, int t0, int n, const int* units, int nu, float* q,
+                       float* k, float* v) {
+    const int H = w->n_kv_heads, d = w->head_dim;
+    const int G = w->n_q_heads / H;
+#pragma omp parallel for collapse(2) schedule(dynamic, 4)
+    for (int s = 0; s < n; ++s)
+        for (int i = 0; i < nu; ++i) {
+            const size_t uo = (size_t)s * nu + i;
+            unit_step(w, layer, t0 + s, units[i] / H, units[i] % H, q + uo * G * d, k + uo * d, v + uo * d);
+        }
 }
 
 /* raw Philox block, exposed so tests can pin the generator to its published

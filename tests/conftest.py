@@ -27,3 +27,19 @@ def synth_lib():
 
     synth.build()
     return synth
+
+
+def pytest_terminal_summary(terminalreporter, exitstatus, config):
+    """The parity counts of every GPU run (re-syncs after near ties, first
+    divergence steps, largest output errors), also under -q."""
+    harness = sys.modules.get("harness")
+    if harness is None or not harness.REPORTS:
+        return
+    tr = terminalreporter
+    tr.write_sep("=", "parity counts (%d runs)" % len(harness.REPORTS))
+    flagged = resynced = 0
+    for test, tag, rep in harness.REPORTS:
+        tr.write_line("%s  %s" % (test, rep.line(tag)))
+        flagged += rep.flagged_steps
+        resynced += rep.flagged_divergences
+    tr.write_line("total: near-tie unit-steps %d, re-synced %d" % (flagged, resynced))

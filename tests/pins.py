@@ -295,6 +295,30 @@ def check_softmax_sum_invariants(lib, seed=9):
                 assert np.array_equal(sa[key], sb[key]), (rank_pinned, t, key)
 
 
+def check_softmax_sum_golden(lib):
+    """Variant V1 against a hand-worked step (tests/golden/
+    softmax_sum_worked_example.json): three one-token pages whose refreshed
+    page is A under the scale 1/sqrt(d) of the attention logits and would be
+    B under scale 1; the scores match the worked values."""
+    import json
+    import os
+
+    with open(os.path.join(os.path.dirname(__file__), "golden", "softmax_sum_worked_example.json")) as f:
+        g = json.load(f)
+    d, G = g["head_dim"], g["group"]
+    m = oracle.Kvm(G, d, g["page_size"], g["slots"], r=g["r"], lib=lib, aggregation=oracle.AGG_SOFTMAX_SUM)
+    assert m.prefill(None, None) == 0
+    zero_q = np.zeros((G, d))
+    for name, q in (("A", zero_q), ("B", zero_q), ("C", np.array(g["queries_step2"], float))):
+        m.decode(q, np.array(g["keys"][name], float), np.zeros(d), want_out=False)
+    sc, _ = m.last_scores()
+    for slot, name in enumerate("ABC"):
+        assert abs(sc[slot] - g["scores_step2"][name]) < 2e-7, (name, sc[slot], g["scores_step2"][name])
+    st = m.state()
+    assert st["page_table"].tolist() == g["page_table_after"], st["page_table"]
+    assert st["ts"].tolist() == g["ts_after"], st["ts"]
+
+
 def check_prefill_rule(lib, seed=6):
     """Prefill pages are stored, marked non-evictable and never change
     (Algorithm 1, Section 3.1). When the prefill does not fit, the first S-1
@@ -541,6 +565,7 @@ ALL_CHECKS = [
     check_group_vs_history,
     check_rank_pinned_vs_history,
     check_softmax_sum_invariants,
+    check_softmax_sum_golden,
     check_dense_equivalence,
     check_single_token_and_bound,
     check_threshold_counts,

@@ -80,8 +80,8 @@ def test_config_layout_matches_header():
     text = open(HEADER).read()
     body = re.search(r"typedef struct \{(.*?)\} raas_config;", text, re.S).group(1)
     body = re.sub(r"/\*.*?\*/", "", body, flags=re.S)
-    fields = re.findall(r"(int32_t|float)\s+(\w+);", body)
-    want = [(n, ctypes.c_int32 if t == "int32_t" else ctypes.c_float) for t, n in fields]
+    fields = re.findall(r"(int32_t|double)\s+(\w+);", body)
+    want = [(n, ctypes.c_int32 if t == "int32_t" else ctypes.c_double) for t, n in fields]
     assert [(n, t) for n, t in raas.Config._fields_] == want
 
 

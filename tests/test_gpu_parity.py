@@ -13,14 +13,11 @@ import pytest
 
 import synth
 import oracle
-from harness import TOL, ParityReport, new_pool, run_parity, run_ragged, to_device
+from harness import TOL, ParityReport, compare_outputs, new_pool, record, run_parity, run_ragged, say, to_device
 
 pytestmark = pytest.mark.gpu
 
-
-def _say(msg):
-    print(msg, flush=True)
-    sys.stdout.flush()
+_say = say
 
 
 @pytest.fixture(scope="module", autouse=True)
@@ -41,11 +38,13 @@ def small(**kw):
     return synth.Workload(**base)
 
 
-def _report(rep: ParityReport, tag):
-    _say("%s: steps %d units %d outputs %d max_abs_err %.3g evictions %d flagged %d/%d"
-          % (tag, rep.steps, rep.units_checked, rep.outputs_compared, rep.max_abs_err, rep.evictions,
-             rep.flagged_steps, rep.flagged_divergences))
-    assert rep.flagged_divergences == 0 or rep.flagged_divergences <= rep.flagged_steps
+def _report(rep: ParityReport, tag, resync_bound=0):
+    """Records the run's counts (printed again in the session summary) and
+    checks the re-syncs: with fp64 scores on both sides a near tie that the
+    two sides decide differently needs two pages within rounding (about
+    1e-13) of each other at the threshold, so none is expected."""
+    record(rep, tag)
+    assert rep.flagged_divergences <= resync_bound, rep.line(tag)
 
 
 def test_tiny_f32_full_run():
@@ -90,6 +89,10 @@ EDGE = [
     dict(n_q_heads=32, n_kv_heads=2),             # G = 16
     dict(head_dim=64),
     dict(r=0.0), dict(r=1.0), dict(r=0.25), dict(r=0.75),
+    # r not exact in binary: floor(r * n) at n a multiple of 10 evictable pages
+    # (3 pinned + 10 or 20 decode pages) is 7 and 18, one more than a float r gives
+    dict(r=0.7, budget=16 * 13), dict(r=0.9, budget=16 * 23), dict(r=0.7, budget=16 * 13, dtype="f32"),
+    dict(r=0.9, page_size=8, budget=8 * 308, prefill_len=2300),   # 288 pinned + 20, the epilogue's radix select
     dict(dtype="f32", head_dim=128),
     dict(dtype="f32", n_q_heads=14, n_kv_heads=2, head_dim=64, page_size=8, budget=96),
     dict(page_size=8, budget=2400, prefill_len=2300),             # 300 slots: the epilogue's radix select
@@ -187,10 +190,17 @@ def test_state_errors_and_budget_policy():
     strict.close()
 
 
+def _bf16_ulp(x):
+    """spacing of bf16 values at |x| (8 significant bits)"""
+    e = np.floor(np.log2(np.maximum(np.abs(x), 2.0 ** -126)))
+    return 2.0 ** (e - 7)
+
+
 def test_deterministic():
     """Same inputs twice: bitwise-identical retention state; outputs equal up
-    to the order in which partial sums merge (the wavefronts of a workgroup
-    claim blocks dynamically)."""
+    to the order in which the wavefronts' partial softmax states merge (they
+    claim blocks dynamically): the fp32 partials then differ by rounding,
+    so a bf16 output can land one unit in the last place apart, never more."""
     import torch
 
     w = small(decode_steps=260)
@@ -206,9 +216,14 @@ def test_deterministic():
         for i in range(w.decode_steps):
             pool.decode_step(0, qd[i], kd[i], vd[i], o[i])
         st = pool.export_state(0)
-        outs.append((o.float().cpu().numpy(), st))
+        outs.append((o.float().cpu().numpy().astype(np.float64), st))
         pool.close()
-    assert np.max(np.abs(outs[0][0] - outs[1][0])) <= 2e-2
+    a, b = outs[0][0], outs[1][0]
+    ulp = _bf16_ulp(np.maximum(np.abs(a), np.abs(b)))
+    diff = np.abs(a - b)
+    _say("deterministic: %d of %d outputs differ, largest by %.3g ulp" % (int(np.sum(diff > 0)), diff.size,
+                                                                        float(np.max(diff / ulp))))
+    assert np.all(diff <= ulp)
     for key in ("lid", "ts", "state", "fill", "clock", "next_lid"):
         assert np.array_equal(outs[0][1][key], outs[1][1][key])
 
@@ -257,56 +272,66 @@ def test_llama8b_b1_full_run():
     assert rep.evictions > 0
 
 
-def test_llama8b_b32_serving_shape():
-    """Batch-32 Llama-3.1-8B layer, L=2048 (the benchmark workload): fills the
-    budget after 1024 decode steps, then evicts; 12 sampled units checked
-    step by step, every unit checked against the invariants."""
+def test_llama8b_b32_full_run():
+    """Batch-32 Llama-3.1-8B layer, L=2048 (the benchmark workload), the
+    whole run: all 256 units, all 16384 decode steps, in the launch
+    configuration the benchmark times. The budget fills after 1024 decode
+    steps; retention is compared for every unit at every step, outputs of
+    every unit every 256th step."""
     w = synth.get_workload("llama8b-b32-L2048")
-    steps = 1024 + 640
-    _say("case %s steps %d" % (w.name, steps))
-    rep = run_parity(w, seed=0, steps=steps, units=_sample_units(w, 12), out_every=32, chunk=128)
+    steps = w.decode_steps
+    _say("case %s steps %d all units" % (w.name, steps))
+    rep = run_parity(w, seed=0, steps=steps, out_every=256, chunk=256)
     _report(rep, w.name)
-    assert rep.evictions > 0
+    assert rep.evictions > 0 and rep.units_checked == 256 and rep.steps == steps
 
 
-def test_qwen7b_28_layer_stack_last_layer():
-    """Qwen2.5-7B-shaped stack (28 layers, 28/4 heads, batch 64, L=4096): the
-    full 28-layer pool, its last layer run past the budget; 8 sampled
-    units."""
+@pytest.mark.parametrize("layer", [0, 13, 27])
+def test_qwen7b_28_layer_stack(layer):
+    """Qwen2.5-7B-shaped stack (28 layers, 28/4 heads, batch 64, L=4096):
+    the full 28-layer pool, one layer run past the budget (2048 prompt
+    tokens pin 128 of the 256 pages; the rest fill after 2048 decode
+    steps); 8 sampled units checked step by step."""
     w = synth.get_workload("qwen7b-28L-b64-L4096")
-    steps = 2048 + 256
-    _say("case %s layer 27 steps %d" % (w.name, steps))
+    steps = 2048 + 512
+    _say("case %s layer %d steps %d" % (w.name, layer, steps))
     pool = new_pool(w)
-    rep = run_parity(w, seed=0, steps=steps, layer=27, units=_sample_units(w, 8), out_every=64,
-                     chunk=128, pool=pool)
+    rep = run_parity(w, seed=0, steps=steps, layer=layer, units=_sample_units(w, 8, seed=layer), out_every=64,
+                     chunk=256, pool=pool, others="ring", inv_every=16)
     pool.close()
-    _report(rep, w.name)
+    _report(rep, "%s layer %d" % (w.name, layer))
     assert rep.evictions > 0
 
 
-@pytest.mark.parametrize("name,steps", [("llama8b-b128-ps32-L512", 200), ("llama8b-b128-ps32-L2048", 200),
-                                        ("llama8b-b128-ps32-L8192", 160)])
+@pytest.mark.parametrize("name,steps", [("llama8b-b128-ps32-L512", 600), ("llama8b-b128-ps32-L2048", 600),
+                                        ("llama8b-b128-ps32-L8192", 4096 + 512)])
 def test_stress_sweep(name, steps):
-    """Batch 128, page 32, prefill 4096, heavy-tailed keys. At L=512 and
-    2048 the prefill overflows the budget: S-1 pages pinned, each decode
-    page evicted once full."""
+    """Batch 128, page 32, prefill 4096, heavy-tailed keys, 8 sampled units.
+    At L=512 and 2048 the prefill overflows the budget: S-1 pages pinned,
+    each decode page evicted once full. At L=8192 the prompt pins 128 of the
+    256 pages and the decode pages fill the rest after 4096 steps: the run
+    goes 512 steps past that point."""
     w = synth.get_workload(name)
     _say("case %s steps %d" % (name, steps))
-    rep = run_parity(w, seed=0, steps=steps, units=_sample_units(w, 8), out_every=8)
+    units = _sample_units(w, 8)
+    rep = run_parity(w, seed=0, steps=steps, units=units, out_every=8 if steps < 1000 else 64, chunk=128,
+                     others="ring", inv_every=8)
     _report(rep, name)
-    if w.budget < w.prefill_len:
-        assert rep.evictions > 0
+    assert rep.evictions > 0
 
 
 def test_stress_dense_equivalence():
-    """L = N (36864 tokens): nothing is ever evicted and the output is dense
-    attention over every token (the oracle is exactly that at L >= N)."""
+    """L = N (36864 tokens), the whole run of 32768 decode steps: nothing is
+    ever evicted and the output is dense attention over every token (the
+    oracle is exactly that at L >= N); 4 sampled units, outputs every 512th
+    step, the last at 36864 resident tokens."""
     w = synth.get_workload("llama8b-b128-ps32-dense")
-    steps = 96
+    steps = w.decode_steps
     _say("case %s steps %d" % (w.name, steps))
-    rep = run_parity(w, seed=0, steps=steps, units=_sample_units(w, 4), out_every=16)
+    rep = run_parity(w, seed=0, steps=steps, units=_sample_units(w, 4), out_every=512, chunk=64, others="ring",
+                     inv_every=1024)
     _report(rep, w.name)
-    assert rep.evictions == 0
+    assert rep.evictions == 0 and rep.steps == steps
 
 
 # Score variants (raas_config.score_aggregation and rank_pinned) against the
@@ -337,7 +362,6 @@ def test_score_variants(agg, rank, case):
     _say("case variant agg %d rank_pinned %d %s splits %s" % (agg, rank, case, splits))
     rep = run_parity(w, seed=7, steps=w.decode_steps, splits=splits, aggregation=agg, rank_pinned=rank)
     _report(rep, "variant")
-    assert rep.flagged_divergences <= rep.units_checked // 2
 
 
 @pytest.mark.parametrize("name,steps,units,splits", [("llama8b-b32-L2048", 1024 + 320, 6, None),
@@ -380,7 +404,6 @@ def test_sequence_scope(agg, rank, case):
                      scope=1)
     _report(rep, "sequence-scope")
     assert rep.evictions > 0
-    assert rep.flagged_divergences <= rep.units_checked // 2
 
 
 def test_sequence_scope_full_size():
@@ -528,6 +551,7 @@ def test_retention_exact_ties(splits, page_size, budget):
     ts = torch.empty((B, Hkv, S), dtype=torch.int32, device="cuda")
     ev = torch.empty((B, Hkv), dtype=torch.int32, device="cuda")
     evictions = 0
+    rep = ParityReport(units_checked=U)
     for t in range(w.decode_steps):
         qb = to_device(rng.standard_normal((B, w.n_q_heads, d)).astype(np.float32), "bf16")
         kb = sets[(t // ps) % 2, t % ps].contiguous()
@@ -547,9 +571,11 @@ def test_retention_exact_ties(splits, page_size, budget):
                     u, t, st["page_table"].tolist(), st["ts"].tolist(), st["evicted"], pt_h[u].tolist(),
                     ts_h[u].tolist(), ev_h[u])
             evictions += int(st["evicted"] >= 0)
-            err = float(np.max(np.abs(got[u] - want)))
-            assert err <= TOL["bf16"], "unit %d step %d: max abs err %.3g" % (u, t, err)
+            compare_outputs(got[u][None], want[None], "bf16", "unit %d step %d" % (u, t), rep)
+        rep.steps = t + 1
     pool.close()
+    rep.evictions = evictions
+    record(rep, "retention ties")
     assert evictions > 0 or budget > w.prefill_len + w.decode_steps
 
 
@@ -586,6 +612,7 @@ def test_prompt_selection_ties(splits):
         orc.append(m)
     out = torch.empty((B, w.n_q_heads, d), dtype=torch.bfloat16, device="cuda")
     chosen_without_6 = 0
+    rep = ParityReport(units_checked=U)
     for t in range(w.decode_steps):
         q = rng.standard_normal((B, w.n_q_heads, d)).astype(np.float32)
         kn = rng.standard_normal((B, Hkv, d)).astype(np.float32)
@@ -602,9 +629,10 @@ def test_prompt_selection_ties(splits):
             att = orc[u].last_attended()[:npr]
             if att[1] and att[2] and att[4] and not att[6]:
                 chosen_without_6 += 1
-            err = float(np.max(np.abs(got[u] - want)))
-            assert err <= TOL["bf16"], "unit %d step %d: max abs err %.3g" % (u, t, err)
+            compare_outputs(got[u][None], want[None], "bf16", "unit %d step %d" % (u, t), rep)
+        rep.steps = t + 1
     pool.close()
+    record(rep, "prompt-selection ties")
     assert chosen_without_6 > 0  # the tie decided the top 3 in some steps
 
 

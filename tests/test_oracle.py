@@ -46,6 +46,8 @@ MUTANTS = [
                               "#define RANKED(st) ((st) == EVICTABLE)")]),
     ("softmax_sum_unnormalised", [("m->score[s] += exp(scale * (bound[(size_t)s * H + j] - mx)) / z;",
                                    "m->score[s] += exp(scale * (bound[(size_t)s * H + j] - mx));")]),
+    ("softmax_sum_scale_one", [("const double scale = 1.0 / sqrt((double)m->d);",
+                                "const double scale = 1.0;")]),
     ("softmax_sum_one_head", [("        for (int j = 0; j < H; ++j) {\n            double mx = -INFINITY, z = 0.0;",
                                "        for (int j = 0; j < 1; ++j) {\n            double mx = -INFINITY, z = 0.0;")]),
     ("group_heads_overlap", [("bound[(size_t)s * H + h0 + j] = acc;", "bound[(size_t)s * H + j] = acc;")]),
@@ -195,3 +197,63 @@ def test_oracle_batch_matches_single(oracle_lib):
             o1 = b[u].decode(q[u], k[u], v[u])
             assert np.array_equal(o1, out[u])
             assert a[u].state()["page_table"].tolist() == b[u].state()["page_table"].tolist()
+
+
+def _drive_scores(m, scores_by_lid, ps):
+    """One retention-only step with scores given per logical page id."""
+    st = m.state()
+    slot_lid = {s: int(st["page_table"][s]) for s in range(m.S) if st["state"][s] == oracle.EVICTABLE}
+    new = pins._new_slot(st, ps)
+    if new is not None:
+        slot_lid[new] = st["next_lid"]
+    sc = np.zeros(m.S)
+    for s, lid in slot_lid.items():
+        sc[s] = scores_by_lid(lid)
+    m.decode_with_scores(sc)
+
+
+def test_lockstep_adopt_hook(oracle_lib):
+    """The parity harness's re-sync after a near tie (orc_adopt_retention):
+    an oracle that decided one step differently (a refresh, and through it
+    the eviction) takes the other decision and from then on evolves exactly
+    as the other side; anything beyond the step's own decisions is refused
+    and leaves the state unchanged."""
+    ps, S, P = 2, 5, 2
+    rng = np.random.default_rng(3)
+    base = {lid: float(rng.standard_normal()) for lid in range(200)}
+    for flip_at in range(8, 40):
+        a = oracle.Kvm(1, 2, ps, S, lib=oracle_lib)
+        b = oracle.Kvm(1, 2, ps, S, lib=oracle_lib)
+        for m in (a, b):
+            assert m.prefill(np.zeros((P, 2)), np.zeros((P, 2))) == 0
+        for t in range(60):
+            _drive_scores(a, lambda lid: base[(lid * 7 + t) % 200], ps)
+            if t == flip_at:  # b ranks the pages in the opposite order at this step
+                _drive_scores(b, lambda lid: -base[(lid * 7 + t) % 200], ps)
+                sa, sb = a.state(), b.state()
+                if np.array_equal(sa["ts"], sb["ts"]) and sa["evicted"] == sb["evicted"]:
+                    break  # this flip changed nothing
+                a.adopt_retention(sb["page_table"], sb["ts"], sb["evicted"])
+            else:
+                _drive_scores(b, lambda lid: base[(lid * 7 + t) % 200], ps)
+            sa, sb = a.state(), b.state()
+            for key in ("page_table", "ts", "fill", "tail", "next_lid", "clock", "evicted"):
+                assert np.array_equal(sa[key], sb[key]), (flip_at, t, key, sa[key], sb[key])
+    # refused: a pinned page changed, an unknown page, two evictions
+    m = oracle.Kvm(1, 2, ps, S, lib=oracle_lib)
+    assert m.prefill(np.zeros((P, 2)), np.zeros((P, 2))) == 0
+    for t in range(12):
+        _drive_scores(m, lambda lid: float(lid), ps)
+    st = m.state()
+    bad_pin = st["page_table"].copy()
+    bad_pin[0] = 99
+    bad_new = st["page_table"].copy()
+    bad_new[int(np.argmax(st["page_table"]))] = 77
+    bad_ts = st["ts"].copy()
+    bad_ts[int(np.argmax(st["ts"]))] = st["clock"] + 5
+    for pt, ts in ((bad_pin, st["ts"]), (bad_new, st["ts"]), (st["page_table"], bad_ts)):
+        with pytest.raises(oracle.OracleError):
+            m.adopt_retention(pt, ts, st["evicted"])
+        st2 = m.state()
+        for key in ("page_table", "ts", "fill", "tail", "evicted"):
+            assert np.array_equal(st[key], st2[key])
