@@ -50,6 +50,7 @@ class ParityReport:
     flagged_divergences: int = 0    # of those, where the GPU decided differently (oracle re-synced)
     first_divergence: dict = dataclasses.field(default_factory=dict)  # unit -> step of its first re-sync
     evictions: int = 0
+    first_eviction_step: int = -1   # earliest step at which any unit evicted (-1: none)
     invariant_checks: int = 0       # steps whose every unit was checked against the invariants
     notes: list = dataclasses.field(default_factory=list)
 
@@ -303,7 +304,10 @@ def run_parity(w, seed: int, steps: int, layer: int = 0, units=None, out_every: 
         t0, n = h["t0"], h["n"]
         out_h = h["out"].float().numpy()
         pt_h, ts_h, ev_h = h["pt"].numpy(), h["ts"].numpy(), h["ev"].numpy()
+        ev_any = np.nonzero(np.any(h["ev_all"].numpy() >= 0, axis=1))[0]
         rep.evictions += int(np.sum(h["ev_all"].numpy() >= 0))
+        if len(ev_any) and rep.first_eviction_step < 0:
+            rep.first_eviction_step = int(t0 + ev_any[0])
         for j, i in enumerate(h["inv"]):
             _check_invariants(h["pt_all"][j].numpy(), h["ts_all"][j].numpy(), h["ev_all"][i].numpy(),
                               P + t0 + i, P, ps, S, npr)

@@ -190,20 +190,19 @@ def test_state_errors_and_budget_policy():
     strict.close()
 
 
-def _bf16_ulp(x):
-    """spacing of bf16 values at |x| (8 significant bits)"""
-    e = np.floor(np.log2(np.maximum(np.abs(x), 2.0 ** -126)))
-    return 2.0 ** (e - 7)
-
-
 def test_deterministic():
-    """Same inputs twice: bitwise-identical retention state; outputs equal up
-    to the order in which the wavefronts' partial softmax states merge (they
-    claim blocks dynamically): the fp32 partials then differ by rounding,
-    so a bf16 output can land one unit in the last place apart, never more."""
+    """Same inputs twice: bitwise-identical retention state. Outputs may
+    differ: the wavefronts of a workgroup claim attention blocks
+    dynamically, so a wavefront's running softmax maximum, under which its
+    probabilities are rounded to bf16 for the PV product, depends on which
+    blocks it took. Each run is within the parity bounds of the oracle, so
+    the two are within twice those bounds; the test holds them to one."""
     import torch
 
-    w = small(decode_steps=260)
+    from harness import TOL_REL
+
+    # 32 blocks per unit over 8 wavefronts: 16 claimed dynamically
+    w = small(budget=1024, prefill_len=500, decode_steps=260)
     outs = []
     for _ in range(2):
         pool = new_pool(w)
@@ -219,11 +218,10 @@ def test_deterministic():
         outs.append((o.float().cpu().numpy().astype(np.float64), st))
         pool.close()
     a, b = outs[0][0], outs[1][0]
-    ulp = _bf16_ulp(np.maximum(np.abs(a), np.abs(b)))
-    diff = np.abs(a - b)
-    _say("deterministic: %d of %d outputs differ, largest by %.3g ulp" % (int(np.sum(diff > 0)), diff.size,
-                                                                        float(np.max(diff / ulp))))
-    assert np.all(diff <= ulp)
+    rel = np.linalg.norm(a - b, axis=-1) / np.linalg.norm(a, axis=-1)
+    _say("deterministic: %d of %d outputs differ; largest relative L2 difference of a head %.3g"
+         % (int(np.sum(a != b)), a.size, float(rel.max())))
+    assert np.all(rel <= TOL_REL["bf16"])
     for key in ("lid", "ts", "state", "fill", "clock", "next_lid"):
         assert np.array_equal(outs[0][1][key], outs[1][1][key])
 
@@ -321,17 +319,20 @@ def test_stress_sweep(name, steps):
 
 
 def test_stress_dense_equivalence():
-    """L = N (36864 tokens), the whole run of 32768 decode steps: nothing is
-    ever evicted and the output is dense attention over every token (the
-    oracle is exactly that at L >= N); 4 sampled units, outputs every 512th
-    step, the last at 36864 resident tokens."""
+    """L = N (36864 tokens), the whole run of 32768 decode steps: the output
+    is dense attention over every token (the oracle is exactly that at
+    L >= N); 4 sampled units, outputs every 512th step, the last at 36864
+    resident tokens. The budget is exactly full after the last token, so the
+    eager eviction of Algorithm 1 frees one page of every unit at the last
+    step (after its attention) and at no earlier step."""
     w = synth.get_workload("llama8b-b128-ps32-dense")
     steps = w.decode_steps
     _say("case %s steps %d" % (w.name, steps))
     rep = run_parity(w, seed=0, steps=steps, units=_sample_units(w, 4), out_every=512, chunk=64, others="ring",
                      inv_every=1024)
     _report(rep, w.name)
-    assert rep.evictions == 0 and rep.steps == steps
+    assert rep.steps == steps
+    assert rep.first_eviction_step == steps - 1 and rep.evictions == w.batch * w.n_kv_heads
 
 
 # Score variants (raas_config.score_aggregation and rank_pinned) against the
