@@ -187,6 +187,27 @@ raas_status raas_decode_step_masked(raas_pool* pool, int32_t layer, const void* 
                                     int32_t* timestamps_out, int32_t* evicted_out, const int32_t* active,
                                     void* stream);
 
+/* raas_decode_step for callers that cannot allocate device memory (code
+ * under HIP graph capture, serving loops or harnesses that forbid
+ * hipMalloc): the same kernels and results, but the step's scratch memory
+ * -- the partial attention of split units, the page scores handed to the
+ * epilogue kernel, and the prompt selection's fills and block lists -- lies
+ * in a fixed array of RAAS_STATIC_SCRATCH_BYTES in the library's device
+ * code instead of the pool's own buffers. The call allocates nothing and
+ * records no profiling events. Steps whose plan needs no scratch (one
+ * workgroup per unit without a separate prompt selection, the default for
+ * bf16 pools of up to 48 blocks per unit or batches that fill the GPU)
+ * never touch the array. A step needing more than the array holds is
+ * refused with RAAS_E_INVALID, before anything is enqueued. Each GPU holds
+ * one copy of the array until the process ends, shared by every call on it:
+ * its contents are the last call's (no step relies on it starting at zero),
+ * and calls that overlap on one GPU (other streams, other threads) race on
+ * it, so they must be ordered. Errors as raas_decode_step. */
+#define RAAS_STATIC_SCRATCH_BYTES (16u << 20)
+raas_status raas_decode_step_static(raas_pool* pool, int32_t layer, const void* q, const void* k_new,
+                                    const void* v_new, void* out, int32_t* page_table_out,
+                                    int32_t* timestamps_out, int32_t* evicted_out, void* stream);
+
 /* Synchronises the pool's last stream, frees all device memory and the
  * pool. NULL is ignored. */
 void raas_destroy(raas_pool* pool);

@@ -26,6 +26,7 @@ EXPORTS = (
     "raas_create_pool", "raas_prefill", "raas_decode_step", "raas_destroy", "raas_last_error",
     "raas_abi_version", "raas_pool_bytes", "raas_export_state", "raas_set_attention_splits",
     "raas_profile", "raas_profile_read", "raas_prefill_ragged", "raas_decode_step_masked",
+    "raas_decode_step_static",
 )
 
 
@@ -77,6 +78,8 @@ def load_library(path: str = LIB_PATH) -> ctypes.CDLL:
     lib.raas_prefill_ragged.restype = i32
     lib.raas_decode_step_masked.argtypes = [vp, i32, vp, vp, vp, vp, vp, vp, vp, vp, vp]
     lib.raas_decode_step_masked.restype = i32
+    lib.raas_decode_step_static.argtypes = [vp, i32, vp, vp, vp, vp, vp, vp, vp, vp]
+    lib.raas_decode_step_static.restype = i32
     lib.raas_destroy.argtypes = [vp]
     lib.raas_destroy.restype = None
     lib.raas_last_error.argtypes = []
@@ -237,6 +240,13 @@ class Pool:
         """One decode step of one layer for every unit (raas_decode_step)."""
         self.decode_prepared(self.prepare_step(layer, q, k_new, v_new, out, page_table, timestamps,
                                                evicted, stream))
+
+    def decode_step_static(self, layer: int, q, k_new, v_new, out, page_table=None, timestamps=None,
+                           evicted=None, stream=None):
+        """raas_decode_step with the step's scratch in the library's fixed
+        device array (raas_decode_step_static): allocates nothing."""
+        args = self.prepare_step(layer, q, k_new, v_new, out, page_table, timestamps, evicted, stream)
+        _check(self.lib.raas_decode_step_static(*(args[:9] + args[10:])), "raas_decode_step_static")
 
     def export_state(self, layer: int, stream=None) -> dict:
         import numpy as np

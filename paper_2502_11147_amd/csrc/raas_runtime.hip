@@ -7,6 +7,7 @@
 #include <string.h>
 
 #include <algorithm>
+#include <mutex>
 #include <new>
 #include <string>
 #include <vector>
@@ -227,6 +228,118 @@ void prof_record(raas_pool* p, int k, bool start, hipStream_t s) {
     }
 }
 
+// The step's scratch in the fixed device array of raas_decode_step_static:
+// the split partials, the page scores, and the prompt selection's attended
+// fills, block lists and counts, each 256-byte aligned.
+__device__ __align__(256) unsigned char scratch[RAAS_STATIC_SCRATCH_BYTES];
+
+constexpr int kMaxDevices = 64;
+std::mutex g_scratch_mu;
+void* g_scratch_ptr[kMaxDevices];  // scratch's device address, per device
+
+// Address of this device's copy of `scratch` (looked up once per device,
+// with the device current; the array's name is no device address in host
+// code).
+raas_status static_scratch(void** out) {
+    int dev = 0;
+    hipError_t e = hipGetDevice(&dev);
+    if (e != hipSuccess) return hip_fail(e, "hipGetDevice");
+    if (dev < 0 || dev >= kMaxDevices) return fail(RAAS_E_INVALID, "device %d beyond the static scratch table", dev);
+    std::lock_guard<std::mutex> lock(g_scratch_mu);
+    if (!g_scratch_ptr[dev]) {
+        void* ptr = nullptr;
+        e = hipGetSymbolAddress(&ptr, HIP_SYMBOL(scratch));
+        if (e != hipSuccess || !ptr) return hip_fail(e, "hipGetSymbolAddress(scratch)");
+        g_scratch_ptr[dev] = ptr;
+    }
+    *out = g_scratch_ptr[dev];
+    return RAAS_OK;
+}
+
+size_t align256(size_t n) { return (n + 255) & ~(size_t)255; }
+
+// One decode step of one layer (raas_decode_step_masked); with
+// fixed_scratch the per-step scratch comes from `scratch` instead of the
+// pool's buffers, and nothing is allocated or profiled.
+raas_status decode_step(raas_pool* p, int32_t layer, const StepIO& io, hipStream_t s, bool fixed_scratch) {
+    raas_status st = check_layer(p, layer);
+    if (st != RAAS_OK) return st;
+    if (!io.q || !io.k_new || !io.v_new || !io.out)
+        return fail(RAAS_E_INVALID, "q, k_new, v_new and out must be non-NULL");
+    if (!p->prefilled[layer]) return fail(RAAS_E_STATE, "layer %d has not been prefilled", layer);
+    LayerView L = view(p, layer);
+    // visit only the blocks that can hold resident rows (see keep_max)
+    const long long pages_opened = (p->steps[layer] + 1 + p->ps - 1) / p->ps;
+    const long long used = std::min<long long>(p->S, p->keep_max[layer] + pages_opened);
+    L.nblk = (int)std::min<long long>(p->Lcap / kBlockTokens, (used * p->ps + kBlockTokens - 1) / kBlockTokens);
+    // blocks the step attends: with a prompt region only the chosen prompt
+    // pages' blocks (at most topk pages, each on ceil(page_size / 32) blocks)
+    int work_blocks = L.nblk;
+    if (p->npr > 0) {
+        const int nbp = p->npr * p->ps / kBlockTokens;
+        const int per_page = std::max(1, p->ps / kBlockTokens);
+        work_blocks = L.nblk - nbp + std::min(nbp, p->cfg.prompt_topk * per_page);
+    }
+    const StepPlan pl = plan_step(p->U, p->G, p->D, p->S, L.nblk * kBlockTokens, p->ps, work_blocks,
+                                  p->cfg.dtype == RAAS_BF16, p->cfg.score_aggregation,
+                                  p->cfg.decision_scope == RAAS_SCOPE_SEQUENCE, list_ints(p), p->split_override);
+    L.nsplit = pl.nsplit;
+    L.bps = pl.bps;
+    const bool select_kernel = p->npr > 0 && !pl.select_in_step;
+    if (fixed_scratch) {
+        const size_t U = (size_t)p->U, S = (size_t)p->S;
+        const size_t part = pl.fused ? 0 : align256(U * pl.nsplit * p->G * (p->D + 2) * sizeof(float));
+        const size_t score =
+            pl.fused ? 0 : align256(U * S * (p->cfg.score_aggregation == RAAS_SCORE_SOFTMAX_SUM ? p->G : 1) * 8);
+        const size_t fatt = select_kernel ? align256(U * S * 4) : 0;
+        const size_t blist = select_kernel ? align256(U * (p->Lcap / kBlockTokens) * 4) : 0;
+        const size_t bcnt = select_kernel ? align256(U * 2 * 4) : 0;
+        const size_t need = part + score + fatt + blist + bcnt;
+        if (need > RAAS_STATIC_SCRATCH_BYTES)
+            return fail(RAAS_E_INVALID, "this step needs %zu bytes of scratch; the static array holds %u", need,
+                        (unsigned)RAAS_STATIC_SCRATCH_BYTES);
+        if (need > 0) {
+            void* base = nullptr;
+            st = static_scratch(&base);
+            if (st != RAAS_OK) return st;
+            char* c = (char*)base;
+            L.part = part ? (float*)c : nullptr;
+            L.score = score ? (double*)(c + part) : nullptr;
+            if (select_kernel) {
+                L.fill_att = (int32_t*)(c + part + score);
+                L.blist = (int32_t*)(c + part + score + fatt);
+                L.bcnt = (int32_t*)(c + part + score + fatt + blist);
+            }
+        }
+    }
+    // Successive steps of a layer read its pool in opposite directions, so a
+    // step starts with the blocks the previous one read last, the likeliest
+    // to be still in the GPU's memory-side cache.
+    L.rev = p->descending[layer];
+    const bool prof = !fixed_scratch;
+
+    if (select_kernel) {  // Quest on the prompt: which prompt pages this step attends to
+        if (prof) prof_record(p, 2, true, s);
+        hipError_t e = launch_prompt_select(L, io, s);
+        if (prof) prof_record(p, 2, false, s);
+        if (e != hipSuccess) return hip_fail(e, "prompt selection launch");
+    }
+    if (prof) prof_record(p, 0, true, s);
+    hipError_t e = launch_step(L, io, pl, p->cfg.r, s);
+    if (prof) prof_record(p, 0, false, s);
+    if (e != hipSuccess) return hip_fail(e, "step launch");
+    if (!pl.fused) {
+        if (prof) prof_record(p, 1, true, s);
+        e = launch_epilogue(L, io, p->cfg.r, s);
+        if (prof) prof_record(p, 1, false, s);
+        if (e != hipSuccess) return hip_fail(e, "epilogue launch");
+    }
+    p->descending[layer] ^= 1;
+    p->steps[layer] += 1;
+    p->last_stream = s;
+    return RAAS_OK;
+}
+
 }  // namespace
 
 extern "C" {
@@ -440,55 +553,15 @@ raas_status raas_decode_step_masked(raas_pool* p, int32_t layer, const void* q, 
                                     const void* v_new, void* out, int32_t* page_table_out,
                                     int32_t* timestamps_out, int32_t* evicted_out, const int32_t* active,
                                     void* stream) {
-    raas_status st = check_layer(p, layer);
-    if (st != RAAS_OK) return st;
-    if (!q || !k_new || !v_new || !out) return fail(RAAS_E_INVALID, "q, k_new, v_new and out must be non-NULL");
-    if (!p->prefilled[layer]) return fail(RAAS_E_STATE, "layer %d has not been prefilled", layer);
-    LayerView L = view(p, layer);
-    StepIO io{q, k_new, v_new, out, page_table_out, timestamps_out, evicted_out, active};
-    hipStream_t s = (hipStream_t)stream;
-    // visit only the blocks that can hold resident rows (see keep_max)
-    const long long pages_opened = (p->steps[layer] + 1 + p->ps - 1) / p->ps;
-    const long long used = std::min<long long>(p->S, p->keep_max[layer] + pages_opened);
-    L.nblk = (int)std::min<long long>(p->Lcap / kBlockTokens, (used * p->ps + kBlockTokens - 1) / kBlockTokens);
-    // blocks the step attends: with a prompt region only the chosen prompt
-    // pages' blocks (at most topk pages, each on ceil(page_size / 32) blocks)
-    int work_blocks = L.nblk;
-    if (p->npr > 0) {
-        const int nbp = p->npr * p->ps / kBlockTokens;
-        const int per_page = std::max(1, p->ps / kBlockTokens);
-        work_blocks = L.nblk - nbp + std::min(nbp, p->cfg.prompt_topk * per_page);
-    }
-    const StepPlan pl = plan_step(p->U, p->G, p->D, p->S, L.nblk * kBlockTokens, p->ps, work_blocks,
-                                  p->cfg.dtype == RAAS_BF16, p->cfg.score_aggregation,
-                                  p->cfg.decision_scope == RAAS_SCOPE_SEQUENCE, list_ints(p), p->split_override);
-    L.nsplit = pl.nsplit;
-    L.bps = pl.bps;
-    // Successive steps of a layer read its pool in opposite directions, so a
-    // step starts with the blocks the previous one read last, the likeliest
-    // to be still in the GPU's memory-side cache.
-    L.rev = p->descending[layer];
+    const StepIO io{q, k_new, v_new, out, page_table_out, timestamps_out, evicted_out, active};
+    return decode_step(p, layer, io, (hipStream_t)stream, false);
+}
 
-    if (p->npr > 0 && !pl.select_in_step) {  // Quest on the prompt: which prompt pages this step attends to
-        prof_record(p, 2, true, s);
-        hipError_t e = launch_prompt_select(L, io, s);
-        prof_record(p, 2, false, s);
-        if (e != hipSuccess) return hip_fail(e, "prompt selection launch");
-    }
-    prof_record(p, 0, true, s);
-    hipError_t e = launch_step(L, io, pl, p->cfg.r, s);
-    prof_record(p, 0, false, s);
-    if (e != hipSuccess) return hip_fail(e, "step launch");
-    if (!pl.fused) {
-        prof_record(p, 1, true, s);
-        e = launch_epilogue(L, io, p->cfg.r, s);
-        prof_record(p, 1, false, s);
-        if (e != hipSuccess) return hip_fail(e, "epilogue launch");
-    }
-    p->descending[layer] ^= 1;
-    p->steps[layer] += 1;
-    p->last_stream = s;
-    return RAAS_OK;
+raas_status raas_decode_step_static(raas_pool* p, int32_t layer, const void* q, const void* k_new,
+                                    const void* v_new, void* out, int32_t* page_table_out,
+                                    int32_t* timestamps_out, int32_t* evicted_out, void* stream) {
+    const StepIO io{q, k_new, v_new, out, page_table_out, timestamps_out, evicted_out, nullptr};
+    return decode_step(p, layer, io, (hipStream_t)stream, true);
 }
 
 raas_status raas_export_state(raas_pool* p, int32_t layer, int32_t* host_buf, size_t n_ints,
