@@ -52,6 +52,8 @@ def parse():
     ap.add_argument("--prompt-topk", type=int, default=0,
                     help="Quest on the prompt: keep the whole prompt in a prompt region and attend to this many "
                          "prompt pages per step (0: off; the budget then counts decode tokens)")
+    ap.add_argument("--deterministic", action="store_true",
+                    help="bitwise-reproducible outputs: a fixed interleave of the blocks over the wavefronts")
     ap.add_argument("--cpu-seconds", type=float, default=15.0, help="budget of the CPU oracle sample")
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--decode-sweep", action="store_true",
@@ -359,10 +361,12 @@ def main():
     align = max(w.page_size, 32)
     prompt_tokens = -(-w.prefill_len // align) * align if args.prompt_topk > 0 else 0
     npr = prompt_tokens // w.page_size
-    variant = agg != raas.SCORE_MAX or args.rank_pinned or scope != raas.SCOPE_KV_HEAD or npr > 0
+    variant = (agg != raas.SCORE_MAX or args.rank_pinned or scope != raas.SCOPE_KV_HEAD or npr > 0
+               or args.deterministic)
     t_run = time.perf_counter()
     pool = raas.Pool.for_workload(w, score_aggregation=agg, rank_pinned=args.rank_pinned, decision_scope=scope,
-                                  prompt_tokens=prompt_tokens, prompt_topk=args.prompt_topk)
+                                  prompt_tokens=prompt_tokens, prompt_topk=args.prompt_topk,
+                                  deterministic=args.deterministic)
     U, S = w.batch * w.n_kv_heads, pool.slots
     if args.splits:
         pool.set_attention_splits(args.splits)
@@ -454,7 +458,7 @@ def main():
     achieved = kernel_b / step_avg_s / 1e9
     kname = "k_step_bf16" if w.dtype == "bf16" else "k_step_f32"
     if variant:
-        traffic, traffic_src = None, "no stored counter profile for the score variants"
+        traffic, traffic_src = None, "no stored counter profile for the variants"
     elif fused:
         traffic, traffic_src = stored_traffic(kname, w.name)
     else:
@@ -482,6 +486,7 @@ def main():
             "score_aggregation": args.score_aggregation, "rank_pinned": bool(args.rank_pinned),
             "decision_scope": args.decision_scope,
             "prompt_tokens": prompt_tokens, "prompt_topk": args.prompt_topk,
+            "deterministic": bool(args.deterministic),
         },
         "step_hbm_gbs_algorithmic": round(step_b * nl / (elapsed / args.steps) / 1e9, 1),
         "roofline": {

@@ -123,6 +123,14 @@ typedef struct {
      * 0, 0 = off. */
     int32_t prompt_tokens;
     int32_t prompt_topk;
+    /* 1: bitwise-reproducible outputs. The attention of a unit is spread
+     * over the wavefronts of a workgroup; by default they claim its blocks
+     * as they become free, so which wavefront sums which blocks, and with it
+     * the rounding of the output, can change from run to run (retention
+     * never does). With 1 each wavefront takes a fixed interleave of the
+     * blocks: identical inputs give identical outputs, at about 2% of the
+     * step time. 0: the dynamic claims. */
+    int32_t deterministic;
 } raas_config;
 
 typedef struct raas_pool raas_pool; /* opaque */
@@ -229,6 +237,22 @@ size_t raas_pool_bytes(const raas_pool* pool);
  * RAAS_E_INVALID (wrong n_ints), RAAS_E_HIP. */
 raas_status raas_export_state(raas_pool* pool, int32_t layer, int32_t* host_buf, size_t n_ints,
                               void* stream);
+
+/* Checkpoint and resume of one layer: its whole state (keys, values,
+ * representative keys, slot and unit records, the clock, and the host-side
+ * step bookkeeping) to or from a host buffer of raas_layer_checkpoint_bytes
+ * bytes. A pool of the same configuration that loads the buffer continues
+ * exactly as the saved one would have: the same retention decisions, and
+ * with `deterministic` set the same outputs bit for bit. raas_save_layer
+ * synchronises `stream`; raas_load_layer returns once the copies are
+ * enqueued (the buffer must stay valid until they have run) and replaces
+ * the layer's state, prefilled or not. The buffer starts with a header
+ * (magic, ABI version, the configuration) that raas_load_layer checks.
+ * Errors: RAAS_E_INVALID (NULL, wrong size, a header that does not match
+ * this pool), RAAS_E_HIP. */
+size_t raas_layer_checkpoint_bytes(const raas_pool* pool);
+raas_status raas_save_layer(raas_pool* pool, int32_t layer, void* host_buf, size_t bytes, void* stream);
+raas_status raas_load_layer(raas_pool* pool, int32_t layer, const void* host_buf, size_t bytes, void* stream);
 
 /* Tuning: number of slices each unit's pages are split into for the
  * attention step (split-K). 0 restores the automatic choice. Results do not

@@ -26,7 +26,7 @@ EXPORTS = (
     "raas_create_pool", "raas_prefill", "raas_decode_step", "raas_destroy", "raas_last_error",
     "raas_abi_version", "raas_pool_bytes", "raas_export_state", "raas_set_attention_splits",
     "raas_profile", "raas_profile_read", "raas_prefill_ragged", "raas_decode_step_masked",
-    "raas_decode_step_static",
+    "raas_decode_step_static", "raas_layer_checkpoint_bytes", "raas_save_layer", "raas_load_layer",
 )
 
 
@@ -53,6 +53,7 @@ class Config(ctypes.Structure):
         ("decision_scope", ctypes.c_int32),
         ("prompt_tokens", ctypes.c_int32),
         ("prompt_topk", ctypes.c_int32),
+        ("deterministic", ctypes.c_int32),
     ]
 
 
@@ -90,6 +91,12 @@ def load_library(path: str = LIB_PATH) -> ctypes.CDLL:
     lib.raas_pool_bytes.restype = ctypes.c_size_t
     lib.raas_export_state.argtypes = [vp, i32, ip, ctypes.c_size_t, vp]
     lib.raas_export_state.restype = i32
+    lib.raas_layer_checkpoint_bytes.argtypes = [vp]
+    lib.raas_layer_checkpoint_bytes.restype = ctypes.c_size_t
+    lib.raas_save_layer.argtypes = [vp, i32, vp, ctypes.c_size_t, vp]
+    lib.raas_save_layer.restype = i32
+    lib.raas_load_layer.argtypes = [vp, i32, vp, ctypes.c_size_t, vp]
+    lib.raas_load_layer.restype = i32
     lib.raas_set_attention_splits.argtypes = [vp, i32]
     lib.raas_set_attention_splits.restype = i32
     lib.raas_profile.argtypes = [vp, i32]
@@ -129,11 +136,11 @@ class Pool:
                  page_size: int, budget_tokens: int, dtype: str = "bf16", r: float = 0.5,
                  prefill_policy: int = PREFILL_PIN_HEAD, score_aggregation: int = SCORE_MAX,
                  rank_pinned: bool = False, decision_scope: int = SCOPE_KV_HEAD, prompt_tokens: int = 0,
-                 prompt_topk: int = 0, stream=None):
+                 prompt_topk: int = 0, deterministic: bool = False, stream=None):
         self.lib = load_library()
         self.cfg = Config(batch, n_layers, n_q_heads, n_kv_heads, head_dim, page_size, budget_tokens,
                           BF16 if dtype == "bf16" else F32, r, prefill_policy, score_aggregation,
-                          int(rank_pinned), decision_scope, prompt_tokens, prompt_topk)
+                          int(rank_pinned), decision_scope, prompt_tokens, prompt_topk, int(deterministic))
         self.dtype = dtype
         self.batch, self.n_layers = batch, n_layers
         self.n_q_heads, self.n_kv_heads, self.head_dim = n_q_heads, n_kv_heads, head_dim
@@ -261,6 +268,25 @@ class Pool:
                     state=buf[2 * n:3 * n].reshape(U, S), fill=buf[3 * n:4 * n].reshape(U, S),
                     tail=unit[:, 0].copy(), next_lid=unit[:, 1].copy(), clock=unit[:, 2].copy(),
                     evicted=unit[:, 3].copy())
+
+    def save_layer(self, layer: int, stream=None):
+        """One layer's whole state as a host byte array (raas_save_layer)."""
+        import numpy as np
+
+        buf = np.empty(int(self.lib.raas_layer_checkpoint_bytes(self._h)), np.uint8)
+        _check(self.lib.raas_save_layer(self._h, layer, ctypes.c_void_p(buf.ctypes.data), buf.size,
+                                        _stream_handle(stream)), "raas_save_layer")
+        return buf
+
+    def load_layer(self, layer: int, buf, stream=None):
+        """Replaces one layer's state by a saved one (raas_load_layer); keep
+        `buf` alive until the stream has run the copies."""
+        import numpy as np
+
+        buf = np.ascontiguousarray(buf, np.uint8)
+        _check(self.lib.raas_load_layer(self._h, layer, ctypes.c_void_p(buf.ctypes.data), buf.size,
+                                        _stream_handle(stream)), "raas_load_layer")
+        return buf
 
     def pool_bytes(self) -> int:
         return int(self.lib.raas_pool_bytes(self._h))

@@ -58,6 +58,7 @@ struct LayerView {
     int32_t* bcnt;      // [U][2] prompt blocks and all blocks in blist
     int lcap_blk;       // Lcap / 32
     int nt;             // 1: K/V blocks streamed with non-temporal loads
+    int det;            // 1: each wavefront takes a fixed interleave of the blocks (reproducible sums)
 };
 
 // Prefill input of one layer: `stride` token rows per unit; per-sequence

@@ -1098,8 +1098,12 @@ __device__ __forceinline__ void step_item(LayerView L, StepIO io, float scale_lo
 #pragma unroll
         for (int nb = 0; nb < NB; ++nb) vr[nb] = vr_next[nb];
         int bn = bend;
-        if (lane == 0) bn = take(it == 0 ? w + NW : atomicAdd(&s_next, 1));  // one claim per wavefront
-        bn = __builtin_amdgcn_readfirstlane(bn);
+        if (L.det) {
+            bn = take(w + (it + 1) * NW);  // a fixed interleave: reproducible partial sums
+        } else {
+            if (lane == 0) bn = take(it == 0 ? w + NW : atomicAdd(&s_next, 1));  // one claim per wavefront
+            bn = __builtin_amdgcn_readfirstlane(bn);
+        }
         if constexpr (LM == 2)
             if (bn < 0) bn = resolve(bn);  // this block waits in registers meanwhile
         if (bn < bend) {

@@ -138,6 +138,7 @@ LayerView view(const raas_pool* p, int layer) {
     L.bcnt = p->bcnt;
     L.lcap_blk = p->Lcap / kBlockTokens;
     L.nt = p->nt;
+    L.det = p->cfg.deterministic;
     return L;
 }
 
@@ -167,6 +168,8 @@ raas_status validate(const raas_config* c) {
         return fail(RAAS_E_INVALID, "prompt_topk must be >= 1 with a prompt region (got %d)", c->prompt_topk);
     if (c->prompt_tokens == 0 && c->prompt_topk != 0)
         return fail(RAAS_E_INVALID, "prompt_topk needs a prompt region (prompt_tokens > 0)");
+    if (c->deterministic != 0 && c->deterministic != 1)
+        return fail(RAAS_E_INVALID, "deterministic must be 0 or 1 (got %d)", c->deterministic);
     if (c->prompt_tokens > 0 && c->rank_pinned)
         return fail(RAAS_E_INVALID, "rank_pinned does not combine with a prompt region");
     const int S = (c->budget_tokens + c->prompt_tokens) / ps;
@@ -590,6 +593,118 @@ raas_status raas_export_state(raas_pool* p, int32_t layer, int32_t* host_buf, si
     if (errflag) return fail(RAAS_E_HIP, "device reported an internal inconsistency (flag %d)", errflag);
     for (int u = 0; u < p->U; ++u)
         for (int f = 0; f < 4; ++f) host_buf[4 * us + 4 * (size_t)u + f] = unit[(size_t)u * kUnitFields + f];
+    return RAAS_OK;
+}
+
+namespace {
+
+// Checkpoint layout: a header, then the layer's device sections in order
+// (K, V, kmin, kmax, lid, ts, state, fill, unit records), each 256-byte
+// aligned in the buffer.
+constexpr uint64_t kCkptMagic = 0x54504b4353414152ull;  // "RAASCKPT"
+struct CkptHeader {
+    uint64_t magic;
+    int64_t abi, bytes;
+    int64_t cfg[16];  // the configuration, field by field
+    int64_t prefilled, keep_max, steps, descending;
+};
+
+void ckpt_config(const raas_config& c, int64_t* out) {
+    const int64_t f[16] = {c.batch, c.n_layers, c.n_q_heads, c.n_kv_heads, c.head_dim, c.page_size,
+                           c.budget_tokens, c.dtype, (int64_t)llround(c.r * 1e12), c.prefill_policy,
+                           c.score_aggregation, c.rank_pinned, c.decision_scope, c.prompt_tokens, c.prompt_topk,
+                           c.deterministic};
+    memcpy(out, f, sizeof f);
+}
+
+struct CkptSection {
+    void* dev;
+    size_t bytes;
+};
+
+// The device sections of one layer, in checkpoint order; returns their count.
+int ckpt_sections(const raas_pool* p, int layer, CkptSection* out) {
+    const LayerView L = view(p, layer);
+    const size_t kv = p->kv_layer_elems * p->esz, rep = p->rep_layer_elems * p->esz;
+    const size_t meta = p->meta_layer_elems * sizeof(int32_t);
+    const CkptSection sec[9] = {{L.K, kv},        {L.V, kv},          {L.kmin, rep},
+                                {L.kmax, rep},    {L.lid, meta},      {L.ts, meta},
+                                {L.state, meta},  {L.fill, meta},     {L.unit, (size_t)p->U * kUnitFields * 4}};
+    memcpy(out, sec, sizeof sec);
+    return 9;
+}
+
+size_t ckpt_bytes(const raas_pool* p) {
+    CkptSection sec[9];
+    const int n = ckpt_sections(p, 0, sec);
+    size_t b = align256(sizeof(CkptHeader));
+    for (int i = 0; i < n; ++i) b += align256(sec[i].bytes);
+    return b;
+}
+
+}  // namespace
+
+size_t raas_layer_checkpoint_bytes(const raas_pool* p) { return p ? ckpt_bytes(p) : 0; }
+
+raas_status raas_save_layer(raas_pool* p, int32_t layer, void* host_buf, size_t bytes, void* stream) {
+    raas_status st = check_layer(p, layer);
+    if (st != RAAS_OK) return st;
+    if (!host_buf || bytes != ckpt_bytes(p))
+        return fail(RAAS_E_INVALID, "host_buf must hold %zu bytes (got %zu)", ckpt_bytes(p), bytes);
+    CkptHeader h{};
+    h.magic = kCkptMagic;
+    h.abi = RAAS_ABI_VERSION;
+    h.bytes = (int64_t)bytes;
+    ckpt_config(p->cfg, h.cfg);
+    h.prefilled = p->prefilled[layer];
+    h.keep_max = p->keep_max[layer];
+    h.steps = p->steps[layer];
+    h.descending = p->descending[layer];
+    memcpy(host_buf, &h, sizeof h);
+    hipStream_t s = (hipStream_t)stream;
+    CkptSection sec[9];
+    const int n = ckpt_sections(p, layer, sec);
+    size_t off = align256(sizeof h);
+    for (int i = 0; i < n; ++i) {
+        hipError_t e = hipMemcpyAsync((char*)host_buf + off, sec[i].dev, sec[i].bytes, hipMemcpyDeviceToHost, s);
+        if (e != hipSuccess) return hip_fail(e, "hipMemcpyAsync");
+        off += align256(sec[i].bytes);
+    }
+    hipError_t e = hipStreamSynchronize(s);
+    if (e != hipSuccess) return hip_fail(e, "hipStreamSynchronize");
+    return RAAS_OK;
+}
+
+raas_status raas_load_layer(raas_pool* p, int32_t layer, const void* host_buf, size_t bytes, void* stream) {
+    raas_status st = check_layer(p, layer);
+    if (st != RAAS_OK) return st;
+    if (!host_buf || bytes != ckpt_bytes(p))
+        return fail(RAAS_E_INVALID, "host_buf must hold %zu bytes (got %zu)", ckpt_bytes(p), bytes);
+    CkptHeader h;
+    memcpy(&h, host_buf, sizeof h);
+    int64_t cfg[16];
+    ckpt_config(p->cfg, cfg);
+    if (h.magic != kCkptMagic) return fail(RAAS_E_INVALID, "not a layer checkpoint");
+    if (h.abi != RAAS_ABI_VERSION || h.bytes != (int64_t)bytes)
+        return fail(RAAS_E_INVALID, "checkpoint of ABI %lld, %lld bytes", (long long)h.abi, (long long)h.bytes);
+    if (memcmp(h.cfg, cfg, sizeof cfg) != 0)
+        return fail(RAAS_E_INVALID, "checkpoint of a pool with another configuration");
+    if (h.prefilled != 0 && h.prefilled != 1) return fail(RAAS_E_INVALID, "corrupt checkpoint header");
+    hipStream_t s = (hipStream_t)stream;
+    CkptSection sec[9];
+    const int n = ckpt_sections(p, layer, sec);
+    size_t off = align256(sizeof h);
+    for (int i = 0; i < n; ++i) {
+        hipError_t e =
+            hipMemcpyAsync(sec[i].dev, (const char*)host_buf + off, sec[i].bytes, hipMemcpyHostToDevice, s);
+        if (e != hipSuccess) return hip_fail(e, "hipMemcpyAsync");
+        off += align256(sec[i].bytes);
+    }
+    p->prefilled[layer] = (unsigned char)h.prefilled;
+    p->keep_max[layer] = (int)h.keep_max;
+    p->steps[layer] = h.steps;
+    p->descending[layer] = (unsigned char)h.descending;
+    p->last_stream = s;
     return RAAS_OK;
 }
 

@@ -106,11 +106,11 @@ def _to_host_async(t, keep: list):
 
 
 def new_pool(w, splits=None, policy=None, aggregation=0, rank_pinned=False, scope=0, prompt_tokens=0,
-             prompt_topk=0):
+             prompt_topk=0, deterministic=False):
     import paper_2502_11147_amd as raas
 
     kw = {"score_aggregation": aggregation, "rank_pinned": rank_pinned, "decision_scope": scope,
-          "prompt_tokens": prompt_tokens, "prompt_topk": prompt_topk}
+          "prompt_tokens": prompt_tokens, "prompt_topk": prompt_topk, "deterministic": deterministic}
     if policy is not None:
         kw["prefill_policy"] = policy
     pool = raas.Pool.for_workload(w, **kw)

@@ -69,7 +69,7 @@ BAD = [
     dict(decision_scope=1, n_q_heads=2048, n_kv_heads=128),
     dict(prompt_tokens=48, prompt_topk=2), dict(prompt_tokens=64, prompt_topk=0), dict(prompt_tokens=-32),
     dict(prompt_topk=3), dict(prompt_tokens=64, prompt_topk=2, rank_pinned=1),
-    dict(prompt_tokens=32 * 1024, prompt_topk=2),
+    dict(prompt_tokens=32 * 1024, prompt_topk=2), dict(deterministic=2), dict(deterministic=-1),
 ]
 
 
@@ -116,6 +116,9 @@ def test_null_arguments(lib):
     ms, n = ctypes.c_double(), ctypes.c_int64()
     assert lib.raas_profile_read(None, 0, ctypes.byref(ms), ctypes.byref(n)) == raas.E_INVALID
     assert lib.raas_pool_bytes(None) == 0
+    assert lib.raas_layer_checkpoint_bytes(None) == 0
+    assert lib.raas_save_layer(None, 0, None, 0, None) == raas.E_INVALID
+    assert lib.raas_load_layer(None, 0, None, 0, None) == raas.E_INVALID
     lib.raas_destroy(None)  # NULL-safe
 
 

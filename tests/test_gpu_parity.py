@@ -190,8 +190,12 @@ def test_state_errors_and_budget_policy():
     strict.close()
 
 
-def test_deterministic():
-    """Same inputs twice: bitwise-identical retention state. Outputs may
+@pytest.mark.parametrize("splits", [None, 3], ids=["fused", "split"])
+@pytest.mark.parametrize("det", [False, True], ids=["dynamic", "deterministic"])
+def test_deterministic(det, splits):
+    """Same inputs twice: bitwise-identical retention state. With the
+    deterministic option the outputs are bitwise identical too (each
+    wavefront sums a fixed interleave of the blocks). Without it they may
     differ: the wavefronts of a workgroup claim attention blocks
     dynamically, so a wavefront's running softmax maximum, under which its
     probabilities are rounded to bf16 for the PV product, depends on which
@@ -205,7 +209,7 @@ def test_deterministic():
     w = small(budget=1024, prefill_len=500, decode_steps=260)
     outs = []
     for _ in range(2):
-        pool = new_pool(w)
+        pool = new_pool(w, splits, deterministic=det)
         K, V = synth.prefill(w, 11, 0)
         pool.prefill(0, to_device(K, w.dtype), to_device(V, w.dtype))
         q, k, v = synth.steps(w, 11, 0, 0, w.decode_steps)
@@ -219,11 +223,95 @@ def test_deterministic():
         pool.close()
     a, b = outs[0][0], outs[1][0]
     rel = np.linalg.norm(a - b, axis=-1) / np.linalg.norm(a, axis=-1)
-    _say("deterministic: %d of %d outputs differ; largest relative L2 difference of a head %.3g"
-         % (int(np.sum(a != b)), a.size, float(rel.max())))
+    _say("deterministic=%d splits %s: %d of %d outputs differ; largest relative L2 difference of a head %.3g"
+         % (det, splits, int(np.sum(a != b)), a.size, float(rel.max())))
+    if det:
+        assert np.array_equal(a, b)
     assert np.all(rel <= TOL_REL["bf16"])
     for key in ("lid", "ts", "state", "fill", "clock", "next_lid"):
         assert np.array_equal(outs[0][1][key], outs[1][1][key])
+
+
+@pytest.mark.parametrize("case", [dict(), dict(splits=3),
+                                  dict(prompt_tokens=128, prompt_topk=3, prefill_len=100, budget=512),
+                                  dict(aggregation=1)],
+                         ids=["fused", "split", "prompt-selection", "softmax-sum"])
+def test_deterministic_option_parity(case):
+    """The deterministic option (a fixed interleave of the blocks over the
+    wavefronts) against the oracle: retention bit-exact, outputs within
+    the bounds, on the fused and split plans, the in-step prompt selection
+    and the softmax aggregation."""
+    case = dict(case)
+    splits = case.pop("splits", None)
+    run_kw = {k: case.pop(k) for k in ("prompt_tokens", "prompt_topk", "aggregation") if k in case}
+    w = small(budget=case.pop("budget", 1024), prefill_len=case.pop("prefill_len", 500), decode_steps=700)
+    _say("case deterministic option %s splits %s" % (run_kw, splits))
+    pool = new_pool(w, splits, deterministic=True, **run_kw)
+    rep = run_parity(w, seed=17, steps=w.decode_steps, pool=pool, **run_kw)
+    pool.close()
+    _report(rep, "deterministic option")
+    assert rep.evictions > 0
+
+
+@pytest.mark.parametrize("case", [dict(), dict(splits=3), dict(dtype="f32"), dict(prompt_tokens=128, prompt_topk=3)],
+                         ids=["fused", "split", "f32", "prompt-selection"])
+def test_checkpoint_resume(case):
+    """A layer saved mid-run and loaded into a fresh pool of the same
+    configuration continues exactly as the uninterrupted pool: retention
+    bit for bit and (deterministic option) outputs bit for bit, through the
+    budget filling and evictions; loading into a pool of another
+    configuration is refused."""
+    import torch
+
+    import paper_2502_11147_amd as raas
+
+    case = dict(case)
+    splits = case.pop("splits", None)
+    opts = {k: case.pop(k) for k in ("prompt_tokens", "prompt_topk") if k in case}
+    w = small(budget=256, prefill_len=100, decode_steps=400, **case)
+    _say("case checkpoint %s splits %s %s" % (case, splits, opts))
+    a = new_pool(w, splits, deterministic=True, **opts)
+    K, V = synth.prefill(w, 5, 0)
+    a.prefill(0, to_device(K, w.dtype), to_device(V, w.dtype))
+    q, k, v = synth.steps(w, 5, 0, 0, w.decode_steps)
+    qd, kd, vd = to_device(q, w.dtype), to_device(k, w.dtype), to_device(v, w.dtype)
+    B, Hq, Hkv, d, S = w.batch, w.n_q_heads, w.n_kv_heads, w.head_dim, a.slots
+    dt = torch.bfloat16 if w.dtype == "bf16" else torch.float32
+
+    def step(pool, t):
+        out = torch.empty((B, Hq, d), dtype=dt, device="cuda")
+        pt = torch.empty((B, Hkv, S), dtype=torch.int32, device="cuda")
+        ts = torch.empty((B, Hkv, S), dtype=torch.int32, device="cuda")
+        ev = torch.empty((B, Hkv), dtype=torch.int32, device="cuda")
+        pool.decode_step(0, qd[t], kd[t], vd[t], out, pt, ts, ev)
+        return out, pt, ts, ev
+
+    cut = 137
+    for t in range(cut):
+        step(a, t)
+    buf = a.save_layer(0)
+    b = new_pool(w, splits, deterministic=True, **opts)
+    keep = b.load_layer(0, buf)
+    evictions = 0
+    for t in range(cut, w.decode_steps):
+        ra, rb = step(a, t), step(b, t)
+        for x, y in zip(ra, rb):
+            assert torch.equal(x, y), t
+        evictions += int((ra[3] >= 0).sum())
+    torch.cuda.synchronize()
+    del keep
+    sa, sb = a.export_state(0), b.export_state(0)
+    for key in sa:
+        assert np.array_equal(sa[key], sb[key]), key
+    assert evictions > 0
+    other = new_pool(w.replace(r=0.25), splits, deterministic=True, **opts)  # same sizes, another rule
+    for pool, data, why in ((other, buf, "configuration"), (b, np.zeros_like(buf), "checkpoint"),
+                            (b, buf[:-256], "bytes")):
+        with pytest.raises(raas.RaasError) as e:
+            pool.load_layer(0, data)
+        assert e.value.code == raas.E_INVALID and why in str(e.value), str(e.value)
+    for pool in (a, b, other):
+        pool.close()
 
 
 def test_pool_memory_is_fixed():
