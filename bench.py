@@ -19,6 +19,7 @@ throughput on a bounded sample of the same workload.
 from __future__ import annotations
 
 import argparse
+import ctypes
 import json
 import os
 import sys
@@ -54,6 +55,8 @@ def parse():
                          "prompt pages per step (0: off; the budget then counts decode tokens)")
     ap.add_argument("--deterministic", action="store_true",
                     help="bitwise-reproducible outputs: a fixed interleave of the blocks over the wavefronts")
+    ap.add_argument("--no-cold", action="store_true",
+                    help="skip the cold-cache row (the same layer shape, four layers stepped per token)")
     ap.add_argument("--cpu-seconds", type=float, default=15.0, help="budget of the CPU oracle sample")
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--decode-sweep", action="store_true",
@@ -62,6 +65,9 @@ def parse():
     ap.add_argument("--sweep-window", type=int, default=256, help="decode steps per measured window")
     ap.add_argument("--copy-calibration", action="store_true",
                     help="run only a plain streaming kernel of known size (counter calibration)")
+    ap.add_argument("--access-probe", action="store_true",
+                    help="run only the streaming probe (libraas_probe.so): the step kernel's K/V access structure "
+                         "without arithmetic, at the workloads' pool shapes, warm and cold")
     ap.add_argument("--traffic-summary", metavar="DIR", default=None,
                     help="turn rocprofv3 --pmc output under DIR/{fetch,write,copy_fetch,copy_write} "
                          "into the stored traffic profile of --workload")
@@ -91,6 +97,49 @@ def copy_calibration():
     torch.cuda.synchronize()
     print(json.dumps({"copy_calibration": "neg", "bytes_read": COPY_BYTES, "bytes_written": COPY_BYTES,
                       "launches": 5}), flush=True)
+
+
+class _ProbeConfig(ctypes.Structure):
+    _fields_ = [(n, ctypes.c_int32) for n in
+                ("units", "tokens", "head_dim", "layers", "waves", "nontemporal", "mode", "dynamic", "alternate",
+                 "launches")]
+
+
+# (name, units, tokens per unit, waves, layers, non-temporal, mode): the pool
+# shapes of the workloads; layers > 1 read several pools in turn so that no
+# launch finds its data in the 256 MB memory-side cache
+PROBES = [
+    ("llama8b-b32-L2048 (one layer, alternating)", 256, 2048, 8, 1, 0, 0),
+    ("llama8b-b32-L2048 x4 layers, cold", 256, 2048, 8, 4, 1, 0),
+    ("llama8b-b32-L2048 x4 layers, cold, two blocks per wavefront in LDS", 256, 2048, 4, 4, 1, 1),
+    ("qwen7b-28L-b64-L4096 (28 layers, cold)", 256, 4096, 8, 28, 1, 0),
+    ("qwen7b-28L-b64-L4096, two blocks per wavefront in LDS", 256, 4096, 4, 28, 1, 1),
+    ("llama8b-b128-ps32-L8192 (4.3 GB, cold)", 1024, 8192, 4, 1, 1, 0),
+    ("llama8b-b128-ps32-L8192, two blocks per wavefront in LDS", 1024, 8192, 4, 1, 1, 1),
+]
+
+
+def access_probe():
+    """The streaming probe at the workloads' pool shapes: the rate of the
+    step kernel's K/V access structure without arithmetic (a ceiling for it
+    on the same data), one JSON line per shape."""
+    from paper_2502_11147_amd import build as hip_build
+
+    lib = ctypes.CDLL(hip_build.PROBE_LIB_PATH)
+    lib.raas_probe_stream.argtypes = [ctypes.POINTER(_ProbeConfig), ctypes.POINTER(ctypes.c_double),
+                                      ctypes.POINTER(ctypes.c_double)]
+    lib.raas_probe_stream.restype = ctypes.c_int
+    for name, units, tokens, waves, layers, nt, mode in PROBES:
+        cfg = _ProbeConfig(units, tokens, 128, layers, waves, nt, mode, 1, 1, max(200, 4 * layers))
+        us, b = ctypes.c_double(), ctypes.c_double()
+        rc = lib.raas_probe_stream(ctypes.byref(cfg), ctypes.byref(us), ctypes.byref(b))
+        if rc != 0:
+            raise SystemExit("raas_probe_stream failed (%d) for %s" % (rc, name))
+        gbs = b.value / us.value / 1e3
+        print(json.dumps({"access_probe": name, "units": units, "tokens_per_unit": tokens, "waves": waves,
+                          "layers": layers, "nontemporal": bool(nt), "mode": ["registers", "lds"][mode],
+                          "bytes_per_launch": b.value, "us_per_launch": round(us.value, 3),
+                          "GB_per_s": round(gbs, 1), "frac_of_peak": round(gbs / HBM_PEAK_GBS, 4)}), flush=True)
 
 
 def _counter_rows(d, counter):
@@ -284,6 +333,62 @@ def cpu_baseline(w, seed, ring_np, budget_s, aggregation=0, rank_pinned=False):
     }
 
 
+def cold_row(w, args, kernel_bytes, steps=500, layers=4):
+    """The step kernel on the same layer shape with `layers` layers stepped
+    per token (one launch each), so that a layer's pool has left the 256 MB
+    memory-side cache by the time its next step comes: per-launch duration
+    from HIP events over the timed launches (the step kernel is the step's
+    only kernel), against the single layer's algorithmic bytes."""
+    import torch
+
+    import paper_2502_11147_amd as raas
+    import synth
+
+    dt = torch.bfloat16 if w.dtype == "bf16" else torch.float32
+    wl = w.replace(n_layers=layers)
+    pool = raas.Pool.for_workload(wl)
+    Kp, Vp = synth.prefill(w, args.seed, 0)
+    Kd, Vd = torch.from_numpy(Kp).to(dt).cuda(), torch.from_numpy(Vp).to(dt).cuda()
+    for layer in range(layers):
+        pool.prefill(layer, Kd, Vd)
+    R = 64
+    qd, kd, vd = (torch.from_numpy(a).to(dt).cuda() for a in synth.steps(w, args.seed, 0, 0, R))
+    out = torch.empty((w.batch, w.n_q_heads, w.head_dim), dtype=dt, device="cuda")
+    prep = [[pool.prepare_step(layer, qd[j], kd[j], vd[j], out) for j in range(R)] for layer in range(layers)]
+
+    def run(i0, n):
+        for i in range(i0, i0 + n):
+            for layer in range(layers):
+                pool.decode_prepared(prep[layer][i % R])
+
+    fill = max(0, w.budget - w.prefill_len) + w.page_size
+    run(0, fill + 50)
+    pool.profile(1 << KERNEL_EPILOGUE)
+    run(fill + 50, 1)
+    assert pool.profile_read(KERNEL_EPILOGUE)[1] == 0, "expected one fused kernel per step"
+    pool.profile(0)
+    ev0, ev1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+    torch.cuda.synchronize()
+    ev0.record()
+    run(fill + 51, steps)
+    ev1.record()
+    torch.cuda.synchronize()
+    us = ev0.elapsed_time(ev1) * 1e3 / (steps * layers)
+    pool.close()
+    gbs = kernel_bytes / us / 1e3
+    return {"workload": "%s, %d layers stepped per token" % (w.name, layers), "avg_launch_us": round(us, 3),
+            "launches_timed": steps * layers, "achieved": round(gbs, 1), "frac": round(gbs / HBM_PEAK_GBS, 4),
+            "bytes_per_launch": kernel_bytes, "pools_bytes": layers * pool_kv_bytes(w),
+            "note": "each layer's pool is read once per token; the pools together exceed the memory-side "
+                    "cache, so this is the rate from HBM (the runtime reads them with non-temporal loads)"}
+
+
+def pool_kv_bytes(w):
+    e = 2 if w.dtype == "bf16" else 4
+    lcap = -(-w.slots * w.page_size // 32) * 32
+    return 2 * w.batch * w.n_kv_heads * lcap * w.head_dim * e
+
+
 def decode_sweep(args):
     """Decode-length sweep (the setting of the paper's Fig. 6: prompt 128,
     batch 4, decode up to 8192 tokens) on one Mistral-7B-shaped layer: per
@@ -340,6 +445,9 @@ def main():
         sys.exit(2)
     if args.copy_calibration:
         copy_calibration()
+        return
+    if args.access_probe:
+        access_probe()
         return
     if args.decode_sweep:
         decode_sweep(args)
@@ -456,7 +564,7 @@ def main():
     e = 2 if w.dtype == "bf16" else 4
     kernel_b = step_b if fused else step_b - U * w.group * w.head_dim * e - 24 * U * S
     achieved = kernel_b / step_avg_s / 1e9
-    kname = "k_step_bf16" if w.dtype == "bf16" else "k_step_f32"
+    kname = "k_step_bf16" if w.dtype == "bf16" else ("k_step_f32_fused" if fused else "k_step_f32")
     if variant:
         traffic, traffic_src = None, "no stored counter profile for the variants"
     elif fused:
@@ -507,6 +615,8 @@ def main():
         },
     }
     assert np.all(st_end["clock"] == w.prefill_len + t_start + args.steps)
+    if nl == 1 and fused and not variant and not args.no_cold and not args.splits:
+        line["roofline_cold"] = cold_row(w, args, kernel_b)
     if not args.no_cpu_baseline:
         if scope == raas.SCOPE_KV_HEAD:
             line["cpu_baseline"] = cpu_baseline(w, args.seed, ring_np, args.cpu_seconds, agg, args.rank_pinned)

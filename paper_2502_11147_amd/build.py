@@ -11,15 +11,18 @@ CSRC = os.path.join(HERE, "csrc")
 INCLUDE = os.path.join(ROOT, "include")
 LIB_PATH = os.path.join(HERE, "libraas.so")
 SOURCES = [os.path.join(CSRC, "raas_kernels.hip"), os.path.join(CSRC, "raas_runtime.hip")]
+# the streaming probe (measurement only) is a library of its own
+PROBE_SOURCES = [os.path.join(CSRC, "raas_probe.hip")]
+PROBE_LIB_PATH = os.path.join(HERE, "libraas_probe.so")
 ARCH = "gfx950"
 
 
-def hipcc_command(out: str) -> list[str]:
+def hipcc_command(out: str, sources=None) -> list[str]:
     return [
         "hipcc", "--offload-arch=" + ARCH, "-O3", "-std=c++17", "-fPIC", "-shared",
         # packed fp32 vector instructions stay off on this target
         "-Xclang", "-target-feature", "-Xclang", "-packed-fp32-ops",
-        "-I", INCLUDE, "-I", CSRC, *SOURCES, "-o", out,
+        "-I", INCLUDE, "-I", CSRC, *(SOURCES if sources is None else sources), "-o", out,
     ]
 
 
@@ -34,15 +37,22 @@ def kernel_digest() -> str:
     return h.hexdigest()
 
 
-def build(verbose: bool = False) -> str:
-    tmp = LIB_PATH + ".tmp%d" % os.getpid()
-    cmd = hipcc_command(tmp)
+def _compile(out: str, sources, verbose: bool):
+    tmp = out + ".tmp%d" % os.getpid()
+    cmd = hipcc_command(tmp, sources)
     res = subprocess.run(cmd, capture_output=True, text=True)
     if res.returncode != 0:
         raise RuntimeError("hipcc failed:\n" + res.stdout + res.stderr)
     if verbose:
         print(" ".join(cmd))
-    os.replace(tmp, LIB_PATH)
+    os.replace(tmp, out)
+
+
+def build(verbose: bool = False) -> str:
+    """Builds libraas.so (the decode path) and libraas_probe.so (the
+    streaming probe of the measurements)."""
+    _compile(LIB_PATH, SOURCES, verbose)
+    _compile(PROBE_LIB_PATH, PROBE_SOURCES, verbose)
     return LIB_PATH
 
 

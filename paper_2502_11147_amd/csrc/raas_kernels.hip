@@ -701,6 +701,14 @@ __device__ void retention_store(const LayerView& L, const StepIO& io, int u, con
     }
 }
 
+// Makes this wavefront's LDS writes visible to its own later LDS reads (the
+// lanes of one wavefront exchanging data through LDS; no workgroup barrier).
+__device__ __forceinline__ void wave_lds_sync() {
+    __builtin_amdgcn_fence(__ATOMIC_RELEASE, "wavefront");
+    __builtin_amdgcn_wave_barrier();
+    __builtin_amdgcn_fence(__ATOMIC_ACQUIRE, "wavefront");
+}
+
 // Workgroup barrier that waits for this wavefront's LDS traffic only: loads
 // already issued to global memory stay in flight across it.
 __device__ __forceinline__ void lds_barrier() {
@@ -1097,13 +1105,11 @@ __device__ __forceinline__ void step_item(LayerView L, StepIO io, float scale_lo
             for (int ks = 0; ks < KS; ++ks) kr[qq][ks] = kr_next[qq][ks];
 #pragma unroll
         for (int nb = 0; nb < NB; ++nb) vr[nb] = vr_next[nb];
+        // one claim per wavefront: from the LDS counter, or (L.det) a fixed
+        // interleave, whose partial sums are reproducible
         int bn = bend;
-        if (L.det) {
-            bn = take(w + (it + 1) * NW);  // a fixed interleave: reproducible partial sums
-        } else {
-            if (lane == 0) bn = take(it == 0 ? w + NW : atomicAdd(&s_next, 1));  // one claim per wavefront
-            bn = __builtin_amdgcn_readfirstlane(bn);
-        }
+        if (lane == 0) bn = take(L.det ? w + (it + 1) * NW : (it == 0 ? w + NW : atomicAdd(&s_next, 1)));
+        bn = __builtin_amdgcn_readfirstlane(bn);
         if constexpr (LM == 2)
             if (bn < 0) bn = resolve(bn);  // this block waits in registers meanwhile
         if (bn < bend) {
@@ -1213,36 +1219,35 @@ __global__ __launch_bounds__(NW * 64) __attribute__((amdgpu_waves_per_eu(2, 2)))
     step_item<D, NW, AGG, LM, NT>(L, io, scale_log2, r, fused, blockIdx.x);
 }
 
-// Step kernel, fp32 pools: one wavefront per (unit, split), over its rows in
-// chunks of 64 tokens. In a chunk each lane takes one token: its row of K is
-// loaded whole (the loads go out with the unit record's, before the fills
-// say which rows hold tokens) and dotted with the G queries from LDS. The
-// online softmax then updates each head across the wavefront (base 2), and
-// the value pass turns to lanes across channels, one token at a time. Rows
-// are loaded whether or not they hold a token, so that no load waits for
-// the fills; a row holding none enters the sums as zeros with weight 0.
-// Page scores: eight lanes per page, each over D/8 channels, fp32 products
-// formed exactly in fp64 and added there, then summed over the eight lanes
-// (a butterfly, so every lane of a page holds the same sum); each pass's
-// loads go out one pass ahead, the first at entry.
+// fp32 pools: the step of one split of a unit's rows by one wavefront, over
+// its rows in chunks of 64 tokens. In a chunk each lane takes one token: its
+// row of K is loaded whole (the loads go out with the unit record's, before
+// the fills say which rows hold tokens) and dotted with the G queries from
+// LDS. The online softmax then updates each head across the wavefront (base
+// 2), and the value pass turns to lanes across channels, one token at a
+// time. Rows are loaded whether or not they hold a token, so that no load
+// waits for the fills; a row holding none enters the sums as zeros with
+// weight 0. Page scores: eight lanes per page, each over D/8 channels, fp32
+// products formed exactly in fp64 and added there, then summed over the
+// eight lanes (a butterfly, so every lane of a page holds the same sum);
+// each pass's loads go out one pass ahead, the first at entry.
+// s_q: the unit's queries [GM][D] in LDS (heads past G zero), staged by the
+// caller; s_p: this wavefront's [GM][64] weights in LDS; partial: the split's
+// partial [G][D+2] (output, max, sum); score: the unit's [S] page scores, or
+// [S][G] per-head bounds with the softmax aggregation.
 template <int D, int GM>
-__global__ __launch_bounds__(64) void k_step_f32(LayerView L, StepIO io, float scale_log2) {
+__device__ __forceinline__ void f32_split(const LayerView& L, const StepIO& io, float scale_log2, int u, int split,
+                                          const float* s_q, float (*s_p)[64], float* partial, double* score) {
     constexpr int DPL = D / 64;  // channels per lane in the value pass
     constexpr int CPP = D / 8;   // channels per lane in the page scores
     constexpr int VG = GM * DPL >= 32 ? 8 : 16;  // tokens whose value rows load together
-    __shared__ __align__(16) float s_q[GM * D];
-    __shared__ float s_p[GM][64];  // the chunk's weights, per head and token
-    const int lane = threadIdx.x;
-    const int nsplit = L.nsplit;
-    const int u = blockIdx.x / nsplit, split = blockIdx.x - (blockIdx.x / nsplit) * nsplit;
-    if (io.active != nullptr && io.active[u / L.nkv] == 0) return;
+    const int lane = threadIdx.x & 63;
     const int G = L.G, S = L.S, ps = L.ps;
     const size_t base = (size_t)u * S;
     const int t0 = split * L.bps * 32;
     const int t1 = max(t0, min(min(S * ps, 32 * L.nblk), t0 + L.bps * 32));
     const float* Ku = (const float*)L.K + (size_t)u * L.Lcap * D;
     const float* Vu = (const float*)L.V + (size_t)u * L.Lcap * D;
-    const float* qg = (const float*)io.q + (size_t)u * G * D;
     const float* kn_g = (const float*)io.k_new + (size_t)u * D;
     const float* vn_g = (const float*)io.v_new + (size_t)u * D;
     const int32_t* fu = L.fill_att + base;  // fills the attention sees
@@ -1281,8 +1286,6 @@ __global__ __launch_bounds__(64) void k_step_f32(LayerView L, StepIO io, float s
     const int ns = U4[kNextSlot], nf = U4[kNextFill];
     const bool opened = nf == 0;
     const int row_new = ns * ps + nf;
-    for (int i = lane; i < GM * D; i += 64) s_q[i] = i < G * D ? qg[i] : 0.0f;  // heads past G: zero
-    __syncthreads();
 
     float m[GM], l[GM], acc[GM][DPL];
 #pragma unroll
@@ -1333,7 +1336,7 @@ __global__ __launch_bounds__(64) void k_step_f32(LayerView L, StepIO io, float s
             s_p[j][lane] = p;
             m[j] = m_new;
         }
-        __syncthreads();
+        wave_lds_sync();
 #pragma unroll
         for (int g0 = 0; g0 < 64; g0 += VG) {
             float vr[VG][DPL];
@@ -1354,12 +1357,12 @@ __global__ __launch_bounds__(64) void k_step_f32(LayerView L, StepIO io, float s
                     for (int i = 0; i < DPL; ++i) acc[j][i] = fmaf(p, vr[e][i], acc[j][i]);
                 }
         }
-        __syncthreads();  // the weights are read before the next chunk writes them
+        wave_lds_sync();  // the weights are read before the next chunk writes them
     }
 #pragma unroll
     for (int j = 0; j < GM; ++j) {
         if (j >= G) break;
-        float* pp = L.part + (((size_t)u * nsplit + split) * G + j) * (D + 2);
+        float* pp = partial + (size_t)j * (D + 2);
 #pragma unroll
         for (int i = 0; i < DPL; ++i) pp[lane + 64 * i] = acc[j][i];
         if (lane == 0) {
@@ -1416,10 +1419,84 @@ __global__ __launch_bounds__(64) void k_step_f32(LayerView L, StepIO io, float s
             a += __shfl_xor(a, 2);
             a += __shfl_xor(a, 4);
             best = a > best ? a : best;
-            if (act && L.agg && part == 0) L.score[(base + p) * G + j] = a;
+            if (act && L.agg && part == 0) score[(size_t)p * G + j] = a;
         }
-        if (act && !L.agg && part == 0) L.score[base + p] = best;
+        if (act && !L.agg && part == 0) score[p] = best;
     }
+}
+
+// Step kernel, fp32 pools, split plan: one wavefront per (unit, split); the
+// epilogue kernel merges the splits and runs the retention.
+template <int D, int GM>
+__global__ __launch_bounds__(64) void k_step_f32(LayerView L, StepIO io, float scale_log2) {
+    __shared__ __align__(16) float s_q[GM * D];
+    __shared__ float s_p[GM][64];  // the chunk's weights, per head and token
+    const int nsplit = L.nsplit;
+    const int u = blockIdx.x / nsplit, split = blockIdx.x - (blockIdx.x / nsplit) * nsplit;
+    if (io.active != nullptr && io.active[u / L.nkv] == 0) return;
+    const int G = L.G;
+    const float* qg = (const float*)io.q + (size_t)u * G * D;
+    for (int i = threadIdx.x; i < GM * D; i += 64) s_q[i] = i < G * D ? qg[i] : 0.0f;  // heads past G: zero
+    __syncthreads();
+    f32_split<D, GM>(L, io, scale_log2, u, split, s_q, s_p, L.part + ((size_t)u * nsplit + split) * G * (D + 2),
+                     L.score + (size_t)u * L.S * (L.agg ? G : 1));
+}
+
+// head slots of the fp32 step kernel instance for a group of G heads
+constexpr int f32_head_slots(int G) { return G <= 4 ? 4 : G <= 8 ? 8 : 16; }
+
+// LDS of the fused fp32 step kernel with nw wavefronts: the queries, each
+// wavefront's weights and partial, the slot arrays (score, state, ts, lid)
+size_t f32_fused_lds(int GM, int G, int D, int S, int nw) {
+    return (size_t)GM * D * 4 + (size_t)nw * GM * 64 * 4 + (size_t)nw * G * (D + 2) * 4 + (size_t)S * 20;
+}
+
+// Step kernel, fp32 pools of head_dim 64, one workgroup per unit (L.nsplit
+// <= 8 wavefronts, one per split): the splits' attention and page scores as
+// above, into LDS;
+// then, as the epilogue kernel does for split plans, the top-r refresh by the
+// whole workgroup, the eviction by wavefront 0 while the others merge the
+// wavefronts' partial outputs, and the state out. One launch per step.
+template <int D, int GM>
+__global__ __launch_bounds__(512) void k_step_f32_fused(LayerView L, StepIO io, float scale_log2, double r) {
+    extern __shared__ __align__(16) unsigned char smem[];
+    __shared__ RetShared ret;
+    __shared__ int s_aux[260];
+    const int u = blockIdx.x, tid = threadIdx.x, nth = blockDim.x, w = tid >> 6, nw = nth >> 6;
+    if (io.active != nullptr && io.active[u / L.nkv] == 0) return;
+    const int G = L.G, S = L.S;
+    float* s_q = reinterpret_cast<float*>(smem);                       // [GM][D]
+    float (*s_p)[64] = reinterpret_cast<float (*)[64]>(s_q + GM * D);  // [nw][GM][64]
+    float* s_part = s_q + GM * D + (size_t)nw * GM * 64;               // [nw][G][D+2]
+    double* s_score = reinterpret_cast<double*>(s_part + (size_t)nw * G * (D + 2));  // [S] (8-byte aligned)
+    int* s_state = reinterpret_cast<int*>(s_score + S);
+    int* s_ts = s_state + S;
+    int* s_lid = s_ts + S;
+    const UnitRec ur = read_unit(L, u);
+    load_slots(L, u, ur, s_score, s_state, s_ts, s_lid);  // every score +inf until its page is scored
+    const float* qg = (const float*)io.q + (size_t)u * G * D;
+    for (int i = tid; i < GM * D; i += nth) s_q[i] = i < G * D ? qg[i] : 0.0f;  // heads past G: zero
+    __syncthreads();
+    f32_split<D, GM>(L, io, scale_log2, u, w, s_q, s_p + (size_t)w * GM, s_part + (size_t)w * G * (D + 2), s_score);
+    __syncthreads();
+    refresh_block(L, ur, r, s_score, s_state, s_ts, s_aux, tid, nth);
+    __syncthreads();
+    if (tid < 64) evict_wave(L, ur, s_state, s_ts, s_lid, ret);
+    for (int idx = tid; idx < G * D; idx += nth) {  // merge: out = sum_w 2^(M_w - M) O_w / sum_w 2^(M_w - M) L_w
+        const int h = idx / D, c = idx - (idx / D) * D;
+        float M = -INFINITY;
+        for (int ww = 0; ww < nw; ++ww) M = fmaxf(M, s_part[((size_t)ww * G + h) * (D + 2) + D]);
+        float O = 0.0f, Ls = 0.0f;
+        for (int ww = 0; ww < nw; ++ww) {
+            const float* pw = s_part + ((size_t)ww * G + h) * (D + 2);
+            const float wt = (pw[D] == -INFINITY) ? 0.0f : __builtin_amdgcn_exp2f(pw[D] - M);
+            O += wt * pw[c];
+            Ls += wt * pw[D + 1];
+        }
+        ((float*)io.out)[((size_t)u * G + h) * D + c] = O / Ls;
+    }
+    __syncthreads();
+    retention_store(L, io, u, ur, s_state, s_ts, s_lid, ret, tid, nth);
 }
 
 // Quest on the prompt pages (pools with a prompt region): for one unit, each
@@ -1737,11 +1814,22 @@ StepPlan plan_step(int U, int G, int D, int S, int Lcap, int ps, int work_blocks
     want = want > nblk ? nblk : want;
     pl.bps = (nblk + want - 1) / want;
     pl.nsplit = (nblk + pl.bps - 1) / pl.bps;
-    pl.fused = bf16 && !grouped && pl.nsplit == 1 && step_lds(G, D, S, pl.waves, true, agg, list_ints) <= kMaxLds;
+    if (bf16) {
+        pl.fused = !grouped && pl.nsplit == 1 && step_lds(G, D, S, pl.waves, true, agg, list_ints) <= kMaxLds;
+        pl.lds = step_lds(G, D, S, pl.waves, pl.fused, agg, list_ints);
+    } else {
+        // fp32: one workgroup per unit with a wavefront per split (up to 8,
+        // two per SIMD at the kernel's registers), which then runs the
+        // epilogue itself; the softmax aggregation, the sequence scope, a
+        // prompt region and head_dim 128 (whose key rows would spill the
+        // fused kernel's registers) keep the epilogue kernel
+        pl.fused = D == 64 && !grouped && !agg && list_ints == 0 && pl.nsplit <= 8 &&
+                   f32_fused_lds(f32_head_slots(G), G, D, S, pl.nsplit) <= kMaxLds;
+        pl.lds = pl.fused ? f32_fused_lds(f32_head_slots(G), G, D, S, pl.nsplit) : 0;
+    }
     // a fused workgroup covers its unit, so it can choose the prompt pages
     // itself (the softmax aggregation keeps the selection kernel)
-    pl.select_in_step = pl.fused && list_ints > 0 && !agg;
-    pl.lds = bf16 ? step_lds(G, D, S, pl.waves, pl.fused, agg, list_ints) : 0;
+    pl.select_in_step = bf16 && pl.fused && list_ints > 0 && !agg;
     return pl;
 }
 
@@ -1751,6 +1839,11 @@ hipError_t allow_large_lds() {
     for (hipError_t r : {allow_lds_all<128, 8>(bytes), allow_lds_all<128, 4>(bytes), allow_lds_all<128, 2>(bytes),
                          allow_lds_all<64, 8>(bytes), allow_lds_all<64, 4>(bytes), allow_lds_all<64, 2>(bytes)})
         if (r != hipSuccess) e = r;
+    for (const void* f : {(const void*)k_step_f32_fused<64, 4>, (const void*)k_step_f32_fused<64, 8>,
+                          (const void*)k_step_f32_fused<64, 16>}) {
+        hipError_t r = hipFuncSetAttribute(f, hipFuncAttributeMaxDynamicSharedMemorySize, bytes);
+        if (r != hipSuccess) e = r;
+    }
 
     return e;
 }
@@ -1809,19 +1902,30 @@ hipError_t launch_prefill(const LayerView& L, const void* k, const void* v, cons
 
 // fp32 step kernel with room for GM >= G query heads (the head loops unroll
 // GM times: a small bound keeps the kernel's code small)
+template <int D, int GM>
+void launch_step_f32_gm(const LayerView& L, const StepIO& io, const StepPlan& pl, float sl2, double r, hipStream_t s) {
+    if constexpr (D == 64) {
+        if (pl.fused) {
+            hipLaunchKernelGGL((k_step_f32_fused<D, GM>), dim3((unsigned)L.U), dim3(64 * pl.nsplit), pl.lds, s, L, io,
+                               sl2, r);
+            return;
+        }
+    }
+    hipLaunchKernelGGL((k_step_f32<D, GM>), dim3((unsigned)(L.U * pl.nsplit)), dim3(64), 0, s, L, io, sl2);
+}
+
 template <int D>
-void launch_step_f32(const LayerView& L, const StepIO& io, dim3 grid, float sl2, hipStream_t s) {
-    if (L.G <= 4) hipLaunchKernelGGL((k_step_f32<D, 4>), grid, dim3(64), 0, s, L, io, sl2);
-    else if (L.G <= 8) hipLaunchKernelGGL((k_step_f32<D, 8>), grid, dim3(64), 0, s, L, io, sl2);
-    else hipLaunchKernelGGL((k_step_f32<D, 16>), grid, dim3(64), 0, s, L, io, sl2);
+void launch_step_f32(const LayerView& L, const StepIO& io, const StepPlan& pl, float sl2, double r, hipStream_t s) {
+    if (L.G <= 4) launch_step_f32_gm<D, 4>(L, io, pl, sl2, r, s);
+    else if (L.G <= 8) launch_step_f32_gm<D, 8>(L, io, pl, sl2, r, s);
+    else launch_step_f32_gm<D, 16>(L, io, pl, sl2, r, s);
 }
 
 hipError_t launch_step(const LayerView& L, const StepIO& io, const StepPlan& pl, double r, hipStream_t s) {
     const float sl2 = (float)(1.4426950408889634 / sqrt((double)L.D));
     if (!L.bf16) {
-        const dim3 grid((unsigned)(L.U * pl.nsplit));
-        if (L.D == 128) launch_step_f32<128>(L, io, grid, sl2, s);
-        else launch_step_f32<64>(L, io, grid, sl2, s);
+        if (L.D == 128) launch_step_f32<128>(L, io, pl, sl2, r, s);
+        else launch_step_f32<64>(L, io, pl, sl2, r, s);
         return hipGetLastError();
     }
     if (L.D == 128) {

@@ -121,6 +121,12 @@ F32_SHAPES = [
     dict(budget=512, prefill_len=100, decode_steps=520, splits=1),   # eight chunks in one wavefront
     dict(budget=512, prefill_len=100, decode_steps=520, splits=3),   # uneven splits, ragged last chunk
     dict(budget=80, page_size=8, prefill_len=3, splits=2),       # ragged pages and chunks
+    # head_dim 64: one workgroup per unit, a wavefront per split, the epilogue in the same kernel
+    dict(head_dim=64, budget=256, prefill_len=40, splits=1),     # one wavefront over four chunks
+    dict(head_dim=64, budget=256, prefill_len=40, splits=3),     # uneven splits
+    dict(head_dim=64, budget=512, prefill_len=100, decode_steps=520, splits=8),  # eight wavefronts
+    dict(head_dim=64, page_size=8, budget=80, prefill_len=3),    # ragged pages, the default plan
+    dict(head_dim=64, budget=2048, prefill_len=1500, decode_steps=600),  # 32 splits: the split path
 ]
 
 
@@ -511,6 +517,7 @@ def test_sequence_scope_full_size():
 RAGGED = [
     dict(),
     dict(dtype="f32"),
+    dict(dtype="f32", head_dim=64),                    # the fused fp32 kernel
     dict(splits=3, budget=512),
     dict(scope=1),
     dict(scope=1, aggregation=1, rank_pinned=True),
@@ -526,7 +533,7 @@ def test_ragged_batch(case):
     random mask of the sequences taking each step, and two prompts replaced
     mid-run (a finished request's place reused)."""
     case = dict(case)
-    wkw = {k: case.pop(k) for k in ("dtype", "budget") if k in case}
+    wkw = {k: case.pop(k) for k in ("dtype", "budget", "head_dim") if k in case}
     w = small(batch=4, decode_steps=260, **wkw)
     lens = [0, 5, 40, 1000]
     _say("case ragged %s %s lens %s" % (wkw, case, lens))

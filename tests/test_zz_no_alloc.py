@@ -39,6 +39,7 @@ RUNS = [
     (_w(batch=6), 3, {}),                                                  # split path: partials + scores
     (_w(batch=4, budget=128, prefill_len=300), 2, dict(prompt_tokens=320, prompt_topk=3)),  # + selection lists
     (_w(batch=3, dtype="f32"), None, {}),                                  # fp32 step + epilogue kernels
+    (_w(batch=3, dtype="f32", head_dim=64), None, {}),                     # fp32 fused: no scratch
     (_w(batch=2, n_q_heads=16, n_kv_heads=4), None, dict(scope=1)),        # one page table per sequence
     (_w(batch=2, budget=128, prefill_len=40), 2, dict(aggregation=1)),     # per-head bounds as scratch
     (_w(batch=2), None, {}),                                               # fused: no scratch at all
