@@ -173,9 +173,10 @@ def traffic_summary(args):
     for counter, sub, csub in (("FETCH_SIZE", "fetch", "copy_fetch"), ("WRITE_SIZE", "write", "copy_write")):
         rows = [r for r in _counter_rows(os.path.join(args.traffic_summary, sub), counter)
                 if kernel in r["Kernel_Name"]]
-        rows = rows[-args.steps:]
-        if len(rows) < args.steps:
-            raise SystemExit("%s: %d %s dispatches, want %d" % (counter, len(rows), kernel, args.steps))
+        want = args.steps * w.n_layers  # the timed steps' launches, one per layer
+        rows = rows[-want:]
+        if len(rows) < want:
+            raise SystemExit("%s: %d %s dispatches, want %d" % (counter, len(rows), kernel, want))
         kib = float(np.mean([float(r["Counter_Value"]) for r in rows]))
         crow = [r for r in _counter_rows(os.path.join(args.traffic_summary, csub), counter)
                 if "neg" in r["Kernel_Name"]]
@@ -190,7 +191,7 @@ def traffic_summary(args):
         out[key + "_bytes_per_launch"] = round(kib * 1024.0 * factor)
         out[key + "_launches"] = len(rows)
     out["traffic_bytes_per_launch"] = out["fetch_size_bytes_per_launch"] + out["write_size_bytes_per_launch"]
-    flags = "--workload %s --steps %d --warmup %d --no-cpu-baseline" % (w.name, args.steps, args.warmup)
+    flags = "--workload %s --steps %d --warmup %d --no-cpu-baseline --no-cold" % (w.name, args.steps, args.warmup)
     out["commands"] = [
         "timeout -s KILL 300 rocprofv3 --pmc FETCH_SIZE --output-format csv -d DIR/fetch -- python3 bench.py " + flags,
         "timeout -s KILL 300 rocprofv3 --pmc WRITE_SIZE --output-format csv -d DIR/write -- python3 bench.py " + flags,

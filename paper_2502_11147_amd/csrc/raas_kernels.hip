@@ -1266,6 +1266,20 @@ __device__ __forceinline__ void f32_split(const LayerView& L, const StepIO& io, 
         }
     };
     load_key(Ku + (size_t)min(t0 + lane, max(t1 - 1, 0)) * D);
+    // VPRE (head_dim 64, up to 8 head slots, where the registers allow): the
+    // chunk's 64 value rows (one channel per lane) load together with its key
+    // rows, before the fills and the unit record arrive, and the new token's
+    // value is substituted afterwards
+    constexpr bool VPRE = D == 64 && GM <= 8;
+    float vpre[VPRE ? 64 : 1];
+    auto load_vals = [&](int c0) {
+        if constexpr (VPRE) {
+#pragma unroll
+            for (int e = 0; e < 64; ++e) vpre[e] = Vu[(size_t)min(c0 + e, max(t1 - 1, 0)) * D + lane];
+        }
+    };
+    load_vals(t0);
+    const float vn_lane = VPRE ? vn_g[lane] : 0.0f;
     // page state and representative keys of a score pass (pages pb .. pb+7,
     // clamped into the split's pages), loaded one pass ahead
     const int sl0 = min(S, (t0 + ps - 1) / ps), sl1 = min(S, (t1 + ps - 1) / ps);
@@ -1297,7 +1311,10 @@ __device__ __forceinline__ void f32_split(const LayerView& L, const StepIO& io, 
     }
     for (int c0 = t0; c0 < t1; c0 += 64) {
         const int t = c0 + lane;
-        if (c0 > t0) load_key(Ku + (size_t)min(t, t1 - 1) * D);  // later chunks' key rows
+        if (c0 > t0) {  // later chunks' key (and value) rows
+            load_key(Ku + (size_t)min(t, t1 - 1) * D);
+            load_vals(c0);
+        }
         bool valid = false;
         if (t < t1) {
             const int slot = t / ps;
@@ -1337,6 +1354,15 @@ __device__ __forceinline__ void f32_split(const LayerView& L, const StepIO& io, 
             m[j] = m_new;
         }
         wave_lds_sync();
+        if constexpr (VPRE) {
+#pragma unroll
+            for (int e = 0; e < 64; ++e) {
+                const uint32_t keep = 0u - (uint32_t)((vmask >> e) & 1ull);  // all ones or zero
+                const float v = __uint_as_float(__float_as_uint(c0 + e == row_new ? vn_lane : vpre[e]) & keep);
+#pragma unroll
+                for (int j = 0; j < GM; ++j) acc[j][0] = fmaf(s_p[j][e], v, acc[j][0]);
+            }
+        } else {
 #pragma unroll
         for (int g0 = 0; g0 < 64; g0 += VG) {
             float vr[VG][DPL];
@@ -1356,6 +1382,7 @@ __device__ __forceinline__ void f32_split(const LayerView& L, const StepIO& io, 
 #pragma unroll
                     for (int i = 0; i < DPL; ++i) acc[j][i] = fmaf(p, vr[e][i], acc[j][i]);
                 }
+        }
         }
         wave_lds_sync();  // the weights are read before the next chunk writes them
     }

@@ -89,6 +89,11 @@ for _L in (1024, 2048, 128 + 8192):
                                 dtype="bf16", page_size=16, budget=_L, prefill_len=128, decode_steps=8192,
                                 ms_period=64, ms_phase_random=True, ms_wmin=64, ms_wmax=1024)
 
+# the serving-load layer shape with four layers stepped per token: each
+# layer's pool (268 MB) has left the 256 MB memory-side cache by the time its
+# next step comes, so every step reads from HBM
+WORKLOADS["llama8b-b32-L2048-x4"] = WORKLOADS["llama8b-b32-L2048"].replace(name="llama8b-b32-L2048-x4", n_layers=4)
+
 HEADLINE = "llama8b-b32-L2048"
 
 
