@@ -102,20 +102,25 @@ def copy_calibration():
 class _ProbeConfig(ctypes.Structure):
     _fields_ = [(n, ctypes.c_int32) for n in
                 ("units", "tokens", "head_dim", "layers", "waves", "nontemporal", "mode", "dynamic", "alternate",
-                 "launches")]
+                 "launches", "kv_interleaved")]
 
 
-# (name, units, tokens per unit, waves, layers, non-temporal, mode): the pool
-# shapes of the workloads; layers > 1 read several pools in turn so that no
-# launch finds its data in the 256 MB memory-side cache
+# (name, units, tokens per unit, waves, layers, non-temporal, mode, K and V of
+# a block adjacent): the pool shapes of the workloads; layers > 1 read
+# several pools in turn so that no launch finds its data in the 256 MB
+# memory-side cache
 PROBES = [
-    ("llama8b-b32-L2048 (one layer, alternating)", 256, 2048, 8, 1, 0, 0),
-    ("llama8b-b32-L2048 x4 layers, cold", 256, 2048, 8, 4, 1, 0),
-    ("llama8b-b32-L2048 x4 layers, cold, two blocks per wavefront in LDS", 256, 2048, 4, 4, 1, 1),
-    ("qwen7b-28L-b64-L4096 (28 layers, cold)", 256, 4096, 8, 28, 1, 0),
-    ("qwen7b-28L-b64-L4096, two blocks per wavefront in LDS", 256, 4096, 4, 28, 1, 1),
-    ("llama8b-b128-ps32-L8192 (4.3 GB, cold)", 1024, 8192, 4, 1, 1, 0),
-    ("llama8b-b128-ps32-L8192, two blocks per wavefront in LDS", 1024, 8192, 4, 1, 1, 1),
+    ("llama8b-b32-L2048 (one layer, alternating)", 256, 2048, 8, 1, 0, 0, 0),
+    ("llama8b-b32-L2048 x4 layers, cold", 256, 2048, 8, 4, 1, 0, 0),
+    ("llama8b-b32-L2048 x4 layers, cold, two blocks per wavefront in LDS", 256, 2048, 4, 4, 1, 1, 0),
+    ("llama8b-b32-L2048 x4 layers, cold, K and V of a block adjacent", 256, 2048, 8, 4, 1, 0, 1),
+    ("llama8b-b32-L2048 x4 layers, cold, ordinary loads", 256, 2048, 8, 4, 0, 0, 0),
+    ("qwen7b-28L-b64-L4096 (28 layers, cold)", 256, 4096, 8, 28, 1, 0, 0),
+    ("qwen7b-28L-b64-L4096, two blocks per wavefront in LDS", 256, 4096, 4, 28, 1, 1, 0),
+    ("qwen7b-28L-b64-L4096, K and V of a block adjacent", 256, 4096, 8, 28, 1, 0, 1),
+    ("llama8b-b128-ps32-L8192 (4.3 GB, cold)", 1024, 8192, 4, 1, 1, 0, 0),
+    ("llama8b-b128-ps32-L8192, two blocks per wavefront in LDS", 1024, 8192, 4, 1, 1, 1, 0),
+    ("llama8b-b128-ps32-L8192, K and V of a block adjacent", 1024, 8192, 4, 1, 1, 0, 1),
 ]
 
 
@@ -129,8 +134,8 @@ def access_probe():
     lib.raas_probe_stream.argtypes = [ctypes.POINTER(_ProbeConfig), ctypes.POINTER(ctypes.c_double),
                                       ctypes.POINTER(ctypes.c_double)]
     lib.raas_probe_stream.restype = ctypes.c_int
-    for name, units, tokens, waves, layers, nt, mode in PROBES:
-        cfg = _ProbeConfig(units, tokens, 128, layers, waves, nt, mode, 1, 1, max(200, 4 * layers))
+    for name, units, tokens, waves, layers, nt, mode, kvi in PROBES:
+        cfg = _ProbeConfig(units, tokens, 128, layers, waves, nt, mode, 1, 1, max(200, 4 * layers), kvi)
         us, b = ctypes.c_double(), ctypes.c_double()
         rc = lib.raas_probe_stream(ctypes.byref(cfg), ctypes.byref(us), ctypes.byref(b))
         if rc != 0:
@@ -138,6 +143,7 @@ def access_probe():
         gbs = b.value / us.value / 1e3
         print(json.dumps({"access_probe": name, "units": units, "tokens_per_unit": tokens, "waves": waves,
                           "layers": layers, "nontemporal": bool(nt), "mode": ["registers", "lds"][mode],
+                          "kv_interleaved": bool(kvi),
                           "bytes_per_launch": b.value, "us_per_launch": round(us.value, 3),
                           "GB_per_s": round(gbs, 1), "frac_of_peak": round(gbs / HBM_PEAK_GBS, 4)}), flush=True)
 

@@ -14,7 +14,9 @@
  * at most 4 wavefronts). `layers` separate pools are read in turn, one per
  * launch, so that their sum can exceed the memory-side cache; alternate = 1
  * reverses a layer's traversal on every other visit, as the decode path
- * does. The probe allocates and frees its own device memory
+ * does. kv_interleaved = 1 lays each block's K and V out back to back (one
+ * contiguous run per block) instead of in two arrays. The probe allocates
+ * and frees its own device memory
  * (units * tokens * head_dim * 4 bytes per layer) and times `launches`
  * launches with HIP events on the default stream after two untimed rounds.
  * Outputs: the average microseconds per launch and the bytes one launch
@@ -39,6 +41,8 @@ typedef struct {
     int32_t dynamic;                 /* 1: dynamic claims after the first block; 0: fixed interleave */
     int32_t alternate;               /* 1: a layer's traversal reverses on every other visit */
     int32_t launches;                /* timed launches, >= 1 */
+    int32_t kv_interleaved;          /* 1: a block's K and V halves adjacent (one contiguous run
+                                        per block) instead of K and V in separate arrays */
 } raas_probe_config;
 
 int raas_probe_stream(const raas_probe_config* cfg, double* us_per_launch, double* bytes_per_launch);

@@ -37,14 +37,16 @@ struct Blk {
 
 template <int D, int NW, bool NT, int MODE>
 __global__ __launch_bounds__(NW * 64) void k_probe(const uint16_t* __restrict__ K, const uint16_t* __restrict__ V,
-                                                   int lcap_blk, int nblk, int rev, int dyn, unsigned* sink) {
+                                                   int lcap_blk, int nblk, int rev, int dyn, int kvi, unsigned* sink) {
     constexpr int BLK = 32 * D;  // elements of K (or V) per block
     constexpr int NV = D / 16;   // 16-byte vectors per lane per array
     __shared__ int s_next;
     extern __shared__ __align__(16) unsigned char stage[];  // MODE 1: [NW][2][2 * NV * 64] 16-byte vectors
     const int lane = threadIdx.x & 63, w = threadIdx.x >> 6;
-    const uint16_t* Ku = K + (size_t)blockIdx.x * lcap_blk * BLK;
-    const uint16_t* Vu = V + (size_t)blockIdx.x * lcap_blk * BLK;
+    // kvi: block b's K at K + (u * lcap_blk + b) * 2 * BLK, its V right after (the buffer K spans both)
+    const size_t bstride = kvi ? 2 * BLK : BLK;
+    const uint16_t* Ku = K + (size_t)blockIdx.x * lcap_blk * bstride;
+    const uint16_t* Vu = kvi ? Ku + BLK : V + (size_t)blockIdx.x * lcap_blk * BLK;
     if (threadIdx.x == 0) s_next = 2 * NW;
     __syncthreads();
     auto blk_of = [&](int i) { return rev ? nblk - 1 - i : i; };
@@ -65,8 +67,8 @@ __global__ __launch_bounds__(NW * 64) void k_probe(const uint16_t* __restrict__ 
     if constexpr (MODE == 0) {
         Blk<D> nx;
         auto load = [&](int b) {
-            const uint16_t* kb = Ku + (size_t)b * BLK + lane * 8;
-            const uint16_t* vb = Vu + (size_t)b * BLK + lane * 8;
+            const uint16_t* kb = Ku + (size_t)b * bstride + lane * 8;
+            const uint16_t* vb = Vu + (size_t)b * bstride + lane * 8;
 #pragma unroll
             for (int i = 0; i < NV; ++i) nx.k[i] = ldg<NT>(kb + i * 512);
 #pragma unroll
@@ -88,8 +90,8 @@ __global__ __launch_bounds__(NW * 64) void k_probe(const uint16_t* __restrict__ 
             return reinterpret_cast<u32x4*>(stage) + (size_t)(w * 2 + s) * 2 * NV * 64;
         };
         auto issue = [&](int b, int s) {  // block b's 2 * NV wave-wide 1 KB rows into slot s
-            const uint16_t* kb = Ku + (size_t)b * BLK + lane * 8;
-            const uint16_t* vb = Vu + (size_t)b * BLK + lane * 8;
+            const uint16_t* kb = Ku + (size_t)b * bstride + lane * 8;
+            const uint16_t* vb = Vu + (size_t)b * bstride + lane * 8;
             u32x4* dst = slot(s);
 #pragma unroll
             for (int j = 0; j < NV; ++j)
@@ -136,7 +138,7 @@ void launch(const raas_probe_config& c, const uint16_t* K, const uint16_t* V, in
             unsigned* sink, hipStream_t s) {
     const size_t lds = MODE == 1 ? (size_t)NW * 2 * 2 * (D / 16) * 64 * 16 : 0;
     hipLaunchKernelGGL((k_probe<D, NW, NT, MODE>), dim3(c.units), dim3(NW * 64), lds, s, K, V, lcap_blk, nblk, rev,
-                       c.dynamic, sink);
+                       c.dynamic, c.kv_interleaved, sink);
 }
 
 template <int D, int NW>
@@ -166,6 +168,7 @@ extern "C" int raas_probe_stream(const raas_probe_config* c, double* us_per_laun
     if (c->head_dim != 64 && c->head_dim != 128) return -1;
     if (c->waves != 2 && c->waves != 4 && c->waves != 8) return -1;
     if (c->mode != 0 && c->mode != 1) return -1;
+    if (c->kv_interleaved != 0 && c->kv_interleaved != 1) return -1;
     if (c->mode == 1 && (c->head_dim != 128 || c->waves > 4)) return -1;  // two 16 KB slots per wavefront
     const int lcap_blk = c->tokens / 32, nblk = lcap_blk;
     const size_t per_layer = (size_t)c->units * c->tokens * c->head_dim;  // elements of K (or V)
@@ -173,17 +176,18 @@ extern "C" int raas_probe_stream(const raas_probe_config* c, double* us_per_laun
     unsigned* sink = nullptr;
     hipEvent_t e0 = nullptr, e1 = nullptr;
     int rc = -2;
-    if (hipMalloc(&K, per_layer * c->layers * 2) != hipSuccess) K = nullptr;
-    if (hipMalloc(&V, per_layer * c->layers * 2) != hipSuccess) V = nullptr;
+    const int kvi = c->kv_interleaved ? 1 : 0;  // K holds both halves; V is unused
+    if (hipMalloc(&K, per_layer * c->layers * 2 * (1 + kvi)) != hipSuccess) K = nullptr;
+    if (hipMalloc(&V, kvi ? 256 : per_layer * c->layers * 2) != hipSuccess) V = nullptr;
     if (hipMalloc(&sink, (size_t)c->units * 8 * sizeof(unsigned)) != hipSuccess) sink = nullptr;
-    if (K && V && sink && hipMemset(K, 0x3C, per_layer * c->layers * 2) == hipSuccess &&
-        hipMemset(V, 0x3C, per_layer * c->layers * 2) == hipSuccess && hipEventCreate(&e0) == hipSuccess &&
+    if (K && V && sink && hipMemset(K, 0x3C, per_layer * c->layers * 2 * (1 + kvi)) == hipSuccess &&
+        hipMemset(V, 0x3C, kvi ? 256 : per_layer * c->layers * 2) == hipSuccess && hipEventCreate(&e0) == hipSuccess &&
         hipEventCreate(&e1) == hipSuccess && set_lds<2>() && set_lds<4>()) {
         auto run = [&](int i) {
             const int layer = i % c->layers;
             const int rev = c->alternate ? (i / c->layers) & 1 : 0;
-            const uint16_t* Kl = K + per_layer * layer;
-            const uint16_t* Vl = V + per_layer * layer;
+            const uint16_t* Kl = K + per_layer * layer * (1 + kvi);
+            const uint16_t* Vl = kvi ? V : V + per_layer * layer;
             hipStream_t s = nullptr;
             if (c->head_dim == 128) {
                 if (c->waves == 8) launch_nw<128, 8>(*c, Kl, Vl, lcap_blk, nblk, rev, sink, s);
