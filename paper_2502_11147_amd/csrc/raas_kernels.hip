@@ -406,6 +406,106 @@ __device__ __forceinline__ double score_finish(const LayerView& L, int u, int p,
     return best;
 }
 
+// Order-preserving map of a float onto an int (for an LDS atomic minimum), and back.
+__device__ __forceinline__ int float_order(float x) {
+    const int i = __builtin_bit_cast(int, x);
+    return i >= 0 ? i : i ^ 0x7FFFFFFF;
+}
+__device__ __forceinline__ float order_float(int i) { return __builtin_bit_cast(float, i >= 0 ? i : i ^ 0x7FFFFFFF); }
+
+// Per bf16 half: the magnitude, at least the smallest normal (2^-126).
+__device__ __forceinline__ uint32_t mag_floor(uint32_t x) {
+    uint32_t lo = x & 0x7FFFu, hi = (x >> 16) & 0x7FFFu;
+    lo = lo < 0x80u ? 0x80u : lo;
+    hi = hi < 0x80u ? 0x80u : hi;
+    return lo | (hi << 16);
+}
+
+// Quest bounds of the pages in slots 0 .. npages-1 (max over the heads of
+// sum_c max(q_c kmax_c, q_c kmin_c), Section 4.2 with Quest's page
+// representatives), as intervals, on the MFMA. With q+ and q- the positive
+// and negative parts of q, a channel's term is q+ kmax + q- kmin, so per
+// tile of 16 pages the bounds of every head are the product of [kmax | kmin]
+// (pages x 2D) with [q+ ; q-] (2D x heads). The fp32 sum B of those 2D exact
+// products lies within 2D 2^-23 E of the exact one whichever way each
+// addition rounds, E the sum of their magnitudes; a product flushed for a
+// subnormal factor or result loses at most what the same product of
+// magnitudes floored at 2^-126 keeps, or 2^-126. So, with E taken over the
+// floored magnitudes (one more product on the MFMA), the exact bound lies in
+// B -+ (2^-13 E + 1e-30) at D up to 128, with room for E's own rounding.
+// Written to lo/hi, with (-inf, inf) where a sum is not finite. Each
+// wavefront takes tiles w, w + NW, ..., TPW of them loaded at once. q_ops:
+// this lane's query operands (heads as columns).
+template <int D, int NW>
+__device__ __forceinline__ void prompt_bounds(const LayerView& L, size_t base, int npages, const bf16x8 (&q_ops)[D / 32],
+                                              float* lo, float* hi) {
+    constexpr int KS = D / 32, TPW = D >= 128 ? 2 : 4;
+    const int lane = threadIdx.x & 63, w = threadIdx.x >> 6, grp = lane >> 4, col = lane & 15;
+    u32x4 qpos[KS], qneg[KS];
+#pragma unroll
+    for (int ks = 0; ks < KS; ++ks) {
+        const u32x4 x = __builtin_bit_cast(u32x4, q_ops[ks]);
+#pragma unroll
+        for (int h = 0; h < 4; ++h) {
+            const uint32_t neg = ((x[h] >> 15) & 0x00010001u) * 0xFFFFu;  // halves with the sign set
+            qneg[ks][h] = x[h] & neg;
+            qpos[ks][h] = x[h] & ~neg;
+        }
+    }
+    auto mfma = [](u32x4 a, u32x4 b, f32x4 c) {
+        return __builtin_amdgcn_mfma_f32_16x16x32_bf16(__builtin_bit_cast(bf16x8, a), __builtin_bit_cast(bf16x8, b), c,
+                                                       0, 0, 0);
+    };
+    auto floored = [](u32x4 x) { return u32x4{mag_floor(x[0]), mag_floor(x[1]), mag_floor(x[2]), mag_floor(x[3])}; };
+    const int ntile = (npages + 15) / 16;
+    for (int t0 = w; t0 < ntile; t0 += TPW * NW) {
+        // lane (grp, col) supplies page 16t + col's channels 32ks + 8grp .. +7
+        // (rows past npages, and tiles past the last, repeat the last page and
+        // are not written)
+        u32x4 ax[TPW][KS], an[TPW][KS];
+#pragma unroll
+        for (int h = 0; h < TPW; ++h) {
+            const int t = min(t0 + h * NW, ntile - 1);
+            const size_t off = (base + min(16 * t + col, npages - 1)) * D + 8 * grp;
+#pragma unroll
+            for (int ks = 0; ks < KS; ++ks) {
+                ax[h][ks] = ld4((const uint16_t*)L.kmax + off + 32 * ks);
+                an[h][ks] = ld4((const uint16_t*)L.kmin + off + 32 * ks);
+            }
+        }
+#pragma unroll
+        for (int h = 0; h < TPW; ++h) {
+            const int t = t0 + h * NW;
+            if (t >= ntile) break;  // (uniform over the wavefront)
+            f32x4 sb = {0.f, 0.f, 0.f, 0.f}, se = {0.f, 0.f, 0.f, 0.f};
+#pragma unroll
+            for (int ks = 0; ks < KS; ++ks) {
+                sb = mfma(ax[h][ks], qpos[ks], sb);
+                sb = mfma(an[h][ks], qneg[ks], sb);
+                se = mfma(floored(ax[h][ks]), floored(qpos[ks]), se);
+                se = mfma(floored(an[h][ks]), floored(qneg[ks]), se);
+            }
+            // lane (grp, col) holds head col of pages 16t + 4grp + i: the max over the heads
+#pragma unroll
+            for (int i = 0; i < 4; ++i) {
+                float bm = col < L.G ? sb[i] : -INFINITY, em = col < L.G ? se[i] : 0.0f;
+#pragma unroll
+                for (int o = 8; o >= 1; o >>= 1) {
+                    bm = fmaxf(bm, __shfl_xor(bm, o));
+                    em = fmaxf(em, __shfl_xor(em, o));
+                }
+                const int p = 16 * t + 4 * grp + i;
+                if (col == 0 && p < npages) {
+                    const float err = em * 1.220703125e-04f + 1e-30f;  // 2^-13 E + 1e-30
+                    const bool fin = __builtin_isfinite(bm) && __builtin_isfinite(err);
+                    lo[p] = fin ? bm - err : -INFINITY;
+                    hi[p] = fin ? bm + err : INFINITY;
+                }
+            }
+        }
+    }
+}
+
 // Results of the retention policy for one step, computed by the retention
 // wavefront and applied to the pool once the attention has read it.
 struct RetShared {
@@ -795,9 +895,9 @@ __device__ __forceinline__ void attend_block(const u32x4 (&kr)[2][D / 32], const
 // LM, pools with a prompt region (Quest on the prompt): 1, the blocks come
 // from the unit's block list (the prompt blocks the selection kernel chose,
 // then the decode region's); 2, the workgroup covers the unit and selects the
-// prompt pages itself: its score passes also compute the kept prompt pages'
-// bounds, it streams the decode blocks first, and after the score barrier it
-// picks the top k and claims their blocks. 0: no prompt region.
+// prompt pages itself before its block loop (bounds on the MFMA, exact ones
+// for the pages near the cut), then claims the decode blocks and the chosen
+// prompt blocks from one list. 0: no prompt region.
 // NT: K/V blocks are read with non-temporal loads (pools too large for the
 // memory-side cache to serve the next step).
 // The step of work item wi = unit * nsplit + split, by one workgroup (the
@@ -813,6 +913,8 @@ __device__ __forceinline__ void step_item(LayerView L, StepIO io, float scale_lo
     __shared__ RetShared ret;
     __shared__ int s_next;  // next unclaimed block index
     __shared__ int s_nsel;  // LM 2: prompt blocks chosen
+    __shared__ int s_lo;    // LM 2: the topk-th largest lower end of a prompt bound (ordered bits)
+    __shared__ int s_ncand; // LM 2: candidate prompt pages
     __shared__ __align__(16) uint16_t s_kn[D];  // the new token's key and value, staged so that
     __shared__ __align__(16) uint16_t s_vn[D];  // no read in the block loop waits on memory
 
@@ -826,11 +928,16 @@ __device__ __forceinline__ void step_item(LayerView L, StepIO io, float scale_lo
     int* s_ts = s_state + S;
     int* s_lid = s_ts + S;
     int* s_list = fused ? s_lid + S : reinterpret_cast<int*>(s_score);  // LM 1: this workgroup's blocks
-    // LM 2: the prompt pages' bounds and attended fills, the chosen prompt blocks
-    double* s_pb = reinterpret_cast<double*>(  // [dbase], 16-byte aligned (the smem base is)
+    // LM 2: the prompt pages' bound intervals and attended fills, the chosen
+    // prompt blocks, the candidate pages and their exact bounds
+    float* s_plo = reinterpret_cast<float*>(  // [dbase] lower ends, 16-byte aligned (the smem base is)
         reinterpret_cast<int*>(smem) + ((s_lid + S - reinterpret_cast<int*>(smem) + 3) & ~3));
-    int* s_fatt = reinterpret_cast<int*>(s_pb + L.dbase);          // [dbase]
+    float* s_phi = s_plo + L.dbase;                                // [dbase] upper ends
+    int* s_fatt = reinterpret_cast<int*>(s_phi + L.dbase);         // [dbase]
     int* s_plist = s_fatt + L.dbase;                               // [dbase * ps / 32]
+    int* s_cand = s_plist + L.dbase * ps / 32;                     // [dbase]
+    double* s_ex = reinterpret_cast<double*>(                      // [dbase], 8-byte aligned
+        reinterpret_cast<int*>(smem) + ((s_cand + L.dbase - reinterpret_cast<int*>(smem) + 1) & ~1));
 
     const int tid = threadIdx.x, lane = tid & 63, w = tid >> 6;
     const int grp = lane >> 4, col = lane & 15;
@@ -846,8 +953,8 @@ __device__ __forceinline__ void step_item(LayerView L, StepIO io, float scale_lo
     const int nbp = LM ? L.dbase * ps / 32 : 0;  // LM: the decode region starts at this block
     if constexpr (LM == 2) {
         lo = 0;
-        hi = L.nblk - nbp;  // decode blocks, claimed first; claims beyond are prompt blocks
-        sb0 = 0;            // score passes: every page (the prompt's bounds, the decode pages' scores)
+        hi = L.nblk - nbp;  // decode blocks, claimed first; claims beyond are the chosen prompt blocks
+        sb0 = nbp;          // score passes: the decode pages
         sb1 = L.nblk;
     } else if constexpr (LM == 1) {
         const int nsel = L.bcnt[2 * u], ntot = L.bcnt[2 * u + 1];
@@ -866,8 +973,7 @@ __device__ __forceinline__ void step_item(LayerView L, StepIO io, float scale_lo
     }
     const int nown = hi - lo;                  // claims of this workgroup
     const int bend = LM ? 0x40000000 : hi;     // no block: every block index lies below
-    // LM 2: a claim of prompt block index i before the selection is held as -(i+1)
-    auto real = [&](int x) { return (LM != 2 || x >= 0) && x < bend; };
+    auto real = [&](int x) { return x < bend; };
     const uint16_t* qg = (const uint16_t*)io.q + (size_t)u * G * D;
     const uint16_t* kn_g = (const uint16_t*)io.k_new + (size_t)u * D;
     const uint16_t* vn_g = (const uint16_t*)io.v_new + (size_t)u * D;
@@ -905,7 +1011,7 @@ __device__ __forceinline__ void step_item(LayerView L, StepIO io, float scale_lo
         else if constexpr (LM == 2) return nbp + j;
         else return lo + j;
     };
-    int b = (w < nown) ? blk_of(w) : (LM == 2 ? -(w + 1) : bend);
+    int b = (w < nown) ? blk_of(w) : bend;  // (LM 2: a prompt block, once they are chosen)
     const int slot_first = (32 * b + 8 * grp) / ps;
     const int fill_first = (real(b) && slot_first < S) ? fu[slot_first] : 0;
     // unconditional (clamped) reads: a read under a branch draws its first
@@ -915,6 +1021,7 @@ __device__ __forceinline__ void step_item(LayerView L, StepIO io, float scale_lo
     const u32x4 kn_first = ld4(kn_g + 8 * t_new), vn_first = ld4(vn_g + 8 * t_new);
     const int s_first = tid < S ? tid : 0;
     const int st_first = L.state[base + s_first], ts_first = L.ts[base + s_first], lid_first = L.lid[base + s_first];
+    const int pf_first = LM == 2 ? fu[tid < L.dbase ? tid : 0] : 0;  // LM 2: a prompt page's fill
     bf16x8 qv[KS];
 #pragma unroll
     for (int ks = 0; ks < KS; ++ks) {
@@ -923,25 +1030,30 @@ __device__ __forceinline__ void step_item(LayerView L, StepIO io, float scale_lo
     }
     u32x4 kr_next[2][KS], vr_next[NB];
     if (real(b)) load_block(b, kr_next, vr_next);
+    // LM 2: the prompt region's bound intervals (the selection reads those of the
+    // kept pages), their loads behind the first block's and not waiting for the
+    // unit record
+    if constexpr (LM == 2) {
+        if (L.dbase > L.topk) prompt_bounds<D, NW>(L, base, L.dbase, qv, s_plo, s_phi);
+    }
 
     const int ns = ur.ns, nf = ur.nf;
     const bool opened = ur.opened();
     const int row_new = ns * ps + nf, b_new = row_new >> 5, tt_new = row_new & 31;
     bool decided = false;  // this wavefront has passed the score barrier
-    // the block of claim index i, or bend when none is left (LM 2: a prompt
-    // block not chosen yet is held as -(i+1))
+    // the block of claim index i, or bend when none is left (LM 2: the decode
+    // blocks, then the chosen prompt blocks)
     auto take = [&](int i) {
         if constexpr (LM == 2) {
             if (i < nown) return blk_of(i);
-            if (!decided) return -(i + 1);
             return i - nown < s_nsel ? s_plist[i - nown] : bend;
         } else {
             return i < nown ? blk_of(i) : bend;
         }
     };
     // pages scored here: those whose first row lies in this workgroup's blocks, pinned ones
-    // excepted unless they are ranked (LM 2: the kept prompt pages are bounded too)
-    const int sl0 = LM == 2 ? 0 : max(L.rank_pinned ? 0 : pinned, min(S, (32 * sb0 + ps - 1) / ps));
+    // excepted unless they are ranked
+    const int sl0 = max(L.rank_pinned ? 0 : pinned, min(S, (32 * sb0 + ps - 1) / ps));
     const int sl1 = min(S, (32 * sb1 + ps - 1) / ps);
 
     // fill of the page holding this lane's 8 rows of block b (page_size % 8 == 0)
@@ -959,6 +1071,10 @@ __device__ __forceinline__ void step_item(LayerView L, StepIO io, float scale_lo
     if (real(b)) f_next = (w < nown) ? (slot_first < S ? (slot_first == ns ? nf + 1 : fill_first) : 0) : row_fill(b);
 
     // staging for the scores and the epilogue
+    if constexpr (LM == 2) {  // the kept prompt pages' fills (the selection clears those it drops)
+        if (tid < L.dbase) s_fatt[tid] = tid < pinned ? pf_first : 0;
+        for (int p = tid + NW * 64; p < L.dbase; p += NW * 64) s_fatt[p] = p < pinned ? fu[p] : 0;
+    }
     if (tid < G * D) s_qf[qpad_index<D>(tid)] = bf2f(q_first);
     for (int i = tid + NW * 64; i < G * D; i += NW * 64) s_qf[qpad_index<D>(i)] = bf2f(qg[i]);
     if (tid < D / 8) {
@@ -971,10 +1087,93 @@ __device__ __forceinline__ void step_item(LayerView L, StepIO io, float scale_lo
     }
     if (tid == 0) {
         s_next = 2 * NW;  // claims start after the two static blocks of every wavefront
+        if constexpr (LM == 2) {
+            s_lo = 0x7FFFFFFF;
+            s_ncand = 0;
+        }
     }
     // the staging is visible: the first block is still in flight, and every
     // wavefront reaches this point after the same short reads
     lds_barrier();
+
+    if constexpr (LM == 2) {
+        // the topk kept prompt pages of largest bound, ties to the lower slot
+        // (Quest on the prompt): the others' fills are cleared. Each page's
+        // exact bound lies in [s_plo, s_phi]; with lo the topk-th largest lower
+        // end, at least topk pages have bounds >= lo, so a page whose upper end
+        // is below lo ranks below all of them: the top k are among the
+        // candidates with upper end >= lo, and rank among them as among all
+        // kept pages.
+        if (pinned > L.topk && L.topk > 0) {
+            for (int p = tid; p < pinned; p += NW * 64) {
+                // lower ends above p's, four per 16-byte read (a read past the last
+                // kept page stays inside the workgroup's LDS and is not counted)
+                const float lp = s_plo[p];
+                int above = 0;
+#pragma unroll 4
+                for (int o = 0; o < pinned; o += 4) {
+                    const float4 x = *reinterpret_cast<const float4*>(s_plo + o);
+                    above += (x.x > lp ? 1 : 0) + (o + 1 < pinned && x.y > lp ? 1 : 0) +
+                             (o + 2 < pinned && x.z > lp ? 1 : 0) + (o + 3 < pinned && x.w > lp ? 1 : 0);
+                }
+                if (above < L.topk) atomicMin(&s_lo, float_order(lp));
+            }
+            lds_barrier();
+            const float lo_cut = order_float(s_lo);
+            for (int p = tid; p < pinned; p += NW * 64) {
+                if (s_phi[p] >= lo_cut) s_cand[atomicAdd(&s_ncand, 1)] = p;
+                else s_fatt[p] = 0;
+            }
+            lds_barrier();
+            // exactly topk candidates: they are the top k; more: the candidates'
+            // bounds in fp64, eight lanes per page as the decode pages' scores
+            const int nc = s_ncand;
+            if (nc > L.topk) {
+                for (int c0 = 8 * w; c0 < nc; c0 += 8 * NW) {
+                    const int c = c0 + (lane >> 3);
+                    const bool act = c < nc;
+                    const int p = act ? s_cand[c] : 0;
+                    ScoreFrag<D> f;
+                    score_issue<D>(L, u, p, lane & 7, act, f);
+                    const double sc = score_finish<D>(L, u, p, lane & 7, act, f, false, false, s_kn, s_qf, nullptr);
+                    if (act && (lane & 7) == 0) s_ex[c] = sc;
+                }
+                lds_barrier();
+                for (int c = tid; c < nc; c += NW * 64) {
+                    const int p = s_cand[c];
+                    const double e = s_ex[c];
+                    int above = 0;
+                    for (int o = 0; o < nc; ++o) {
+                        const double x = s_ex[o];
+                        above += (x > e || (x == e && s_cand[o] < p)) ? 1 : 0;
+                    }
+                    if (above >= L.topk) s_fatt[p] = 0;
+                }
+            }
+        }
+        lds_barrier();
+        if (w == 0) {  // the prompt blocks holding a chosen page, ascending
+            int cnt = 0;
+            for (int c0 = 0; c0 < nbp; c0 += 64) {
+                const int bb = c0 + lane;
+                bool any = false;
+                if (bb < nbp)
+                    for (int sl = 32 * bb / ps; sl <= (32 * bb + 31) / ps; ++sl) any = any || s_fatt[sl] > 0;
+                const unsigned long long m = __ballot(any);
+                if (any) s_plist[cnt + __popcll(m & ((1ull << lane) - 1ull))] = bb;
+                cnt += __popcll(m);
+            }
+            if (lane == 0) s_nsel = cnt;
+        }
+        lds_barrier();
+        if (w >= nown) {  // no decode block for this wavefront: its first claim is a prompt block
+            b = take(w);
+            if (b < bend) {
+                f_next = row_fill(b);
+                load_block(b, kr_next, vr_next);
+            }
+        }
+    }
 
     float m_run = -INFINITY, l_run = 0.0f;
     f32x4 acc[NB];
@@ -988,9 +1187,7 @@ __device__ __forceinline__ void step_item(LayerView L, StepIO io, float scale_lo
         const int g = pass * NW + w;
         return sl0 + 8 * (L.rev ? ngroups - 1 - g : g) + (lane >> 3);
     };
-    auto pass_act = [&](int p) {
-        return p < sl1 && (p == ns || ranked(L, L.state[base + p]) || (LM == 2 && p < pinned));
-    };
+    auto pass_act = [&](int p) { return p < sl1 && (p == ns || ranked(L, L.state[base + p])); };
     const int npass = (sl1 - sl0 - 8 * w > 0) ? (sl1 - sl0 - 8 * w + 8 * NW - 1) / (8 * NW) : 0;
     const int npass_all = (sl1 - sl0 + 8 * NW - 1) / (8 * NW);  // passes of wavefront 0, the most
     int pass = 0;
@@ -1001,8 +1198,7 @@ __device__ __forceinline__ void step_item(LayerView L, StepIO io, float scale_lo
         double* hb = (AGG && act_cur) ? (fused ? s_hb : L.score + base * G) + (size_t)p * G : nullptr;
         const double sc = score_finish<D>(L, u, p, part, act_cur, frag, p == ns, opened, s_kn, s_qf, hb);
         if (act_cur && part == 0 && !AGG) {
-            if (LM == 2 && p < L.dbase) s_pb[p] = sc;  // a prompt page: a bound for the selection
-            else if (fused) s_score[p] = sc;
+            if (fused) s_score[p] = sc;
             else L.score[base + p] = sc;
         }
         ++pass;
@@ -1012,47 +1208,9 @@ __device__ __forceinline__ void step_item(LayerView L, StepIO io, float scale_lo
             score_issue<D>(L, u, pn, part, act_cur && !(pn == ns && opened), frag);
         }
     };
-    // retention policy once every wavefront's scores are in LDS (LM 2: and
-    // the prompt pages chosen, which needs two more barriers)
+    // retention policy once every wavefront's scores are in LDS
     auto scores_done = [&]() {
         lds_barrier();
-        if constexpr (LM == 2) {
-            // the topk kept prompt pages of largest bound, ties to the lower slot
-            const bool all = pinned <= L.topk;
-            for (int p = tid; p < L.dbase; p += NW * 64) {
-                bool sel = p < pinned;
-                if (sel && !all) {
-                    // pages ranked above p: larger bounds, and equal ones at lower slots (two
-                    // per 16-byte read, four reads in flight; a read past the last kept page
-                    // stays inside the workgroup's LDS and is not counted)
-                    const double bp = s_pb[p];
-                    int above = 0;
-#pragma unroll 4
-                    for (int o = 0; o < pinned; o += 2) {
-                        const double2 x = *reinterpret_cast<const double2*>(s_pb + o);
-                        above += (x.x > bp || (x.x == bp && o < p)) ? 1 : 0;
-                        above += (o + 1 < pinned && (x.y > bp || (x.y == bp && o + 1 < p))) ? 1 : 0;
-                    }
-                    sel = above < L.topk;
-                }
-                s_fatt[p] = sel ? fu[p] : 0;  // kept pages hold at least one token
-            }
-            lds_barrier();
-            if (w == 0) {  // the prompt blocks holding a chosen page, ascending
-                int cnt = 0;
-                for (int c0 = 0; c0 < nbp; c0 += 64) {
-                    const int bb = c0 + lane;
-                    bool any = false;
-                    if (bb < nbp)
-                        for (int sl = 32 * bb / ps; sl <= (32 * bb + 31) / ps; ++sl) any = any || s_fatt[sl] > 0;
-                    const unsigned long long m = __ballot(any);
-                    if (any) s_plist[cnt + __popcll(m & ((1ull << lane) - 1ull))] = bb;
-                    cnt += __popcll(m);
-                }
-                if (lane == 0) s_nsel = cnt;
-            }
-            lds_barrier();
-        }
         if (AGG && fused) softmax_sum_block(L, s_hb, 1, s_state, s_score, s_mz, tid, NW * 64);
         // (after the block loop, as with the softmax aggregation, the retention
         // is on the critical path: its count skips the pinned pages; mid-loop
@@ -1071,30 +1229,6 @@ __device__ __forceinline__ void step_item(LayerView L, StepIO io, float scale_lo
             score_issue<D>(L, u, p, part, act_cur && !(p == ns && opened), frag);
         }
     };
-    bool staged_done = false;  // LM 2: staged() has run (a held claim runs it early)
-    // LM 2: a claim held for the selection: this wavefront finishes its score
-    // passes and waits at the score barrier, which every wavefront reaches
-    // the same way (its claims run past the decode blocks before they reach a
-    // prompt block), then takes the chosen prompt block the claim stands for
-    auto resolve = [&](int x) {
-        if (!staged_done) {
-            staged();
-            staged_done = true;
-        }
-        while (pass < npass) score_step();
-        scores_done();
-        const int i = -x - 1 - nown;
-        return i < s_nsel ? s_plist[i] : bend;
-    };
-    if constexpr (LM == 2) {
-        if (b < 0) {  // no decode block for this wavefront (loaded late, after the staging)
-            b = resolve(b);
-            if (b < bend) {
-                f_next = row_fill(b);
-                load_block(b, kr_next, vr_next);
-            }
-        }
-    }
     int it = 0;
     while (b < bend) {
         const int f_cur = f_next;
@@ -1110,8 +1244,6 @@ __device__ __forceinline__ void step_item(LayerView L, StepIO io, float scale_lo
         int bn = bend;
         if (lane == 0) bn = take(L.det ? w + (it + 1) * NW : (it == 0 ? w + NW : atomicAdd(&s_next, 1)));
         bn = __builtin_amdgcn_readfirstlane(bn);
-        if constexpr (LM == 2)
-            if (bn < 0) bn = resolve(bn);  // this block waits in registers meanwhile
         if (bn < bend) {
             f_next = row_fill(bn);
             load_block(bn, kr_next, vr_next);
@@ -1151,20 +1283,18 @@ __device__ __forceinline__ void step_item(LayerView L, StepIO io, float scale_lo
             attend_block<D>(kr, vr, nv, qv, scale_log2, m_run, l_run, acc);
         }
         // this block's registers are free again
-        if (LM == 2 ? !staged_done : it == 0) {
+        if (it == 0) {
             staged();
-            staged_done = true;
         } else if (pass < npass) {
             score_step();
         }
-        // (the softmax aggregation and the prompt selection wait for the first
-        // held claim or the end of the loop: mid-loop, their arithmetic would
-        // compete with the prefetched block for registers)
-        if (!AGG && LM != 2 && it == npass_all) scores_done();
+        // (the softmax aggregation waits for the end of the loop: mid-loop, its
+        // arithmetic would compete with the prefetched block for registers)
+        if (!AGG && it == npass_all) scores_done();
         ++it;
         b = bn;
     }
-    if (LM == 2 ? !staged_done : it == 0) staged();
+    if (it == 0) staged();
     while (pass < npass) score_step();  // passes left when the wavefront ran out of blocks
     if (!decided) scores_done();
 

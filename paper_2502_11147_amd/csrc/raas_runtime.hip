@@ -89,12 +89,14 @@ struct raas_pool {
 namespace {
 
 // LDS ints the step kernel needs for the prompt selection: a block list of
-// the whole pool (list-driven instance), or the prompt pages' fp64 bounds
-// (two ints each, up to three more to align them to 16 bytes), attended
-// fills and blocks (in-step selection)
+// the whole pool (list-driven instance), or (in-step selection) the prompt
+// pages' bound intervals (two ints each, up to three more to align them to
+// 16 bytes), attended fills and blocks, the candidates and their exact
+// bounds (two ints each, one more to align them to 8 bytes)
 int list_ints(const raas_pool* p) {
     if (p->npr == 0) return 0;
-    return std::max(p->Lcap / kBlockTokens, 3 + 3 * p->npr + p->npr * p->ps / kBlockTokens);
+    const int n = p->npr;
+    return std::max(p->Lcap / kBlockTokens, 3 + 2 * n + n + n * p->ps / kBlockTokens + n + 1 + 2 * n);
 }
 
 LayerView view(const raas_pool* p, int layer) {

@@ -596,6 +596,15 @@ PROMPT_CASES = [
     dict(prompt_tokens=192, prompt_topk=4, prefill_len=190, n_q_heads=28, n_kv_heads=4),
     dict(prompt_tokens=128, prompt_topk=3, prefill_len=100, aggregation=1),
     dict(prompt_tokens=128, prompt_topk=3, prefill_len=100, scope=1),
+    # in-step selection at more prompt pages: bound tiles over several rounds
+    # per wavefront and a partial last tile (100 pages), more candidates than
+    # one pass of eight pages per wavefront takes (top 40), head_dim 64, seven
+    # query heads per KV head, page 32 with heavy-tailed key outliers
+    dict(prompt_tokens=1600, prompt_topk=40, prefill_len=1590, decode_steps=200),
+    dict(prompt_tokens=512, prompt_topk=6, prefill_len=500, head_dim=64),
+    dict(prompt_tokens=1024, prompt_topk=10, prefill_len=1000, n_q_heads=28, n_kv_heads=4, decode_steps=200),
+    dict(prompt_tokens=2048, prompt_topk=8, prefill_len=2048, page_size=32, budget=256, outlier_p=0.05,
+         decode_steps=400),
 ]
 
 
@@ -730,6 +739,66 @@ def test_prompt_selection_ties(splits):
     pool.close()
     record(rep, "prompt-selection ties")
     assert chosen_without_6 > 0  # the tie decided the top 3 in some steps
+
+
+@pytest.mark.parametrize("splits", [None, 2], ids=["in-step", "selection-kernel"])
+def test_prompt_selection_extreme_keys(splits):
+    """Prompt pages whose bounds stress the in-step selection's intervals:
+    keys scaled by 30 and by 1/30, channels of subnormal bf16 keys, an
+    all-zero page, a page of negative zeros but one channel, and queries
+    with subnormal channels; top 3 of 8 pages, every unit and step against
+    the oracle."""
+    import torch
+
+    w = small(batch=2, n_kv_heads=2, n_q_heads=8, decode_steps=60, prefill_len=128)
+    ps, npr, topk = w.page_size, 128 // w.page_size, 3
+    B, Hkv, G, d = w.batch, w.n_kv_heads, w.group, w.head_dim
+    U, S = B * Hkv, w.slots + npr
+    rng = np.random.default_rng(37)
+    K = rng.standard_normal((B, Hkv, 128, d)).astype(np.float32)
+    V = rng.standard_normal((B, Hkv, 128, d)).astype(np.float32)
+    K[:, :, 0:ps] *= 30.0
+    K[:, :, ps:2 * ps] /= 30.0
+    K[:, :, 2 * ps:3 * ps, : d // 2] = np.float32(1e-39) * np.sign(K[:, :, 2 * ps:3 * ps, : d // 2])
+    K[:, :, 3 * ps:4 * ps] = 0.0
+    K[:, :, 4 * ps:5 * ps] = -0.0
+    K[:, :, 4 * ps:5 * ps, 7] = 1.0
+    Kb = to_device(K, "bf16")
+    Vb = to_device(V, "bf16")
+    assert (Kb[:, :, 2 * ps:3 * ps, : d // 2].abs().float().max().item()) < 1.2e-38  # subnormal in bf16
+    Kr, Vr = Kb.float().cpu().numpy().astype(np.float64), Vb.float().cpu().numpy().astype(np.float64)
+    _say("case prompt-selection extreme keys splits %s" % splits)
+    pool = new_pool(w, splits, prompt_tokens=128, prompt_topk=topk)
+    pool.prefill(0, Kb, Vb)
+    orc = []
+    for u in range(U):
+        b, h = divmod(u, Hkv)
+        m = oracle.Kvm(G, d, ps, S, r=w.r, prompt_slots=npr, prompt_topk=topk)
+        assert m.prefill(Kr[b, h], Vr[b, h]) == 0
+        orc.append(m)
+    out = torch.empty((B, w.n_q_heads, d), dtype=torch.bfloat16, device="cuda")
+    rep = ParityReport(units_checked=U)
+    chosen = np.zeros(npr, dtype=np.int64)
+    for t in range(w.decode_steps):
+        q = rng.standard_normal((B, w.n_q_heads, d)).astype(np.float32)
+        q[:, :, : d // 4] *= np.float32(1e-39) if t % 2 else np.float32(1.0)
+        kn = rng.standard_normal((B, Hkv, d)).astype(np.float32)
+        vn = rng.standard_normal((B, Hkv, d)).astype(np.float32)
+        qb, kb, vb = to_device(q, "bf16"), to_device(kn, "bf16"), to_device(vn, "bf16")
+        pool.decode_step(0, qb, kb, vb, out)
+        torch.cuda.synchronize()
+        got = out.float().cpu().numpy().reshape(U, G, d)
+        q64 = qb.float().cpu().numpy().astype(np.float64).reshape(U, G, d)
+        k64 = kb.float().cpu().numpy().astype(np.float64).reshape(U, d)
+        v64 = vb.float().cpu().numpy().astype(np.float64).reshape(U, d)
+        for u in range(U):
+            want = orc[u].decode(q64[u], k64[u], v64[u])
+            chosen += np.asarray(orc[u].last_attended()[:npr], dtype=np.int64)
+            compare_outputs(got[u][None], want[None], "bf16", "unit %d step %d" % (u, t), rep)
+        rep.steps = t + 1
+    pool.close()
+    record(rep, "prompt-selection extreme keys")
+    assert chosen.min() < U * w.decode_steps and chosen.max() > 0  # a real choice among the pages
 
 
 @pytest.mark.parametrize("name,topk,steps,units", [("llama8b-b128-ps32-L512", 8, 640, 8),
