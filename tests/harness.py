@@ -119,6 +119,51 @@ def new_pool(w, splits=None, policy=None, aggregation=0, rank_pinned=False, scop
     return pool
 
 
+def random_case(i: int) -> dict:
+    """Seeded random configuration i: every switch of the C ABI drawn
+    together (pool dtype, head_dim, group size, KV heads, batch, page size,
+    budget, prompt length below and above the budget, r, the score
+    aggregation, ranked pinned pages, the decision scope, Quest on the
+    prompt, forced attention splits, the deterministic option). The pool is
+    valid (group at most 16, budget and prompt region multiples of the page,
+    the prompt region also of 32, at most 2048 slots) and small enough for
+    the oracle to follow every unit for a few hundred steps, which run past
+    the budget."""
+    import math
+
+    rng = np.random.default_rng(1000 + i)
+    dtype = "f32" if rng.random() < 0.2 else "bf16"
+    d = int(rng.choice([64, 128]))
+    G = int(rng.choice([1, 2, 3, 4, 5, 7, 8, 16]))
+    hkv = int(rng.choice([1, 2, 4])) if G <= 8 else 1
+    batch = int(rng.integers(1, 4)) if G * hkv <= 16 else 1
+    ps = int(rng.choice([8, 16, 32, 64, 128]))
+    pages = int(rng.integers(2, max(2, 512 // ps) + 1))
+    budget = pages * ps
+    prefill = int(rng.integers(0, 2 * budget + 1))
+    r = float(rng.choice([0.0, 0.25, 0.3, 0.5, 0.7, 0.9, 1.0]))
+    agg = int(rng.random() < 0.2)
+    scope = int(rng.random() < 0.15)
+    prompt = bool(rng.random() < 0.2)
+    rank = (not prompt) and bool(rng.random() < 0.15)
+    prompt_tokens = prompt_topk = 0
+    if prompt:
+        unit = ps * 32 // math.gcd(ps, 32)
+        prompt_tokens = unit * int(rng.integers(1, max(1, 512 // unit) + 1))
+        prompt_topk = int(rng.integers(1, prompt_tokens // ps + 1))
+    splits = None if rng.random() < 0.7 else int(rng.integers(2, 6))
+    det = bool(rng.random() < 0.1)
+    kept = 0 if prompt else min(prefill, budget)
+    steps = int(min(800, max(120, budget - kept + 3 * ps + 40)))
+    return dict(workload=dict(name="random-%02d" % i, batch=batch, n_layers=1, n_q_heads=G * hkv,
+                              n_kv_heads=hkv, head_dim=d, dtype=dtype, page_size=ps, budget=budget,
+                              prefill_len=prefill, decode_steps=steps, r=r, ms_period=16,
+                              ms_phase_random=True, ms_wmin=8, ms_wmax=64),
+                variant=dict(aggregation=agg, rank_pinned=rank, scope=scope, prompt_tokens=prompt_tokens,
+                             prompt_topk=prompt_topk),
+                splits=splits, deterministic=det)
+
+
 def unit_index(w, seq, kvh):
     return seq * w.n_kv_heads + kvh
 

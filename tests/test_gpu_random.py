@@ -1,0 +1,41 @@
+"""GPU parity over seeded random configurations (harness.random_case):
+every switch of the C ABI drawn together, each run past its budget against
+the oracle, every unit at every step (evicting), under the same bounds as the
+hand-picked cases. The draws are fixed by the case index, so a failure
+names a reproducible configuration."""
+from __future__ import annotations
+
+import pytest
+
+from harness import new_pool, random_case, record, run_parity, say
+
+pytestmark = pytest.mark.gpu
+
+N_CASES = 64
+
+
+@pytest.fixture(scope="module", autouse=True)
+def _gpu():
+    torch = pytest.importorskip("torch")
+    if not torch.cuda.is_available():
+        pytest.skip("no GPU")
+    import paper_2502_11147_amd as raas
+
+    raas.load_library()  # fails loudly when the HIP library is missing
+
+
+@pytest.mark.parametrize("i", range(N_CASES), ids=["rand-%02d" % i for i in range(N_CASES)])
+def test_random_config_parity(i):
+    import synth
+
+    c = random_case(i)
+    w = synth.Workload(**c["workload"])
+    say("case %s %s splits %s deterministic %s" % (c["workload"], c["variant"], c["splits"], c["deterministic"]))
+    pool = new_pool(w, c["splits"], deterministic=c["deterministic"], **c["variant"])
+    try:
+        rep = run_parity(w, seed=50 + i, steps=w.decode_steps, pool=pool, **c["variant"])
+    finally:
+        pool.close()
+    record(rep, "random %02d" % i)
+    assert rep.flagged_divergences == 0, rep.line("random %02d" % i)
+    assert rep.evictions > 0, rep.line("random %02d" % i)  # every case runs past its budget

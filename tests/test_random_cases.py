@@ -1,0 +1,31 @@
+"""The seeded random configurations of the GPU sweep (harness.random_case)
+are valid pools and cover each switch both ways."""
+from harness import random_case
+
+from test_gpu_random import N_CASES
+
+
+def test_random_cases_are_valid_and_varied():
+    cases = [random_case(i) for i in range(N_CASES)]
+
+    def seen(f):
+        return {f(c) for c in cases}
+
+    assert seen(lambda c: c["workload"]["dtype"]) == {"bf16", "f32"}
+    assert seen(lambda c: c["workload"]["head_dim"]) == {64, 128}
+    assert seen(lambda c: c["variant"]["aggregation"]) == {0, 1}
+    assert seen(lambda c: c["variant"]["scope"]) == {0, 1}
+    assert seen(lambda c: c["variant"]["rank_pinned"]) == {False, True}
+    assert seen(lambda c: c["variant"]["prompt_tokens"] > 0) == {False, True}
+    assert seen(lambda c: c["splits"] is None) == {False, True}
+    assert seen(lambda c: c["deterministic"]) == {False, True}
+    assert len(seen(lambda c: c["workload"]["page_size"])) >= 4
+    assert seen(lambda c: c["workload"]["prefill_len"] > c["workload"]["budget"]) == {False, True}
+    for c in cases:
+        w, v = c["workload"], c["variant"]
+        assert w["n_q_heads"] % w["n_kv_heads"] == 0 and w["n_q_heads"] // w["n_kv_heads"] <= 16
+        assert w["budget"] % w["page_size"] == 0
+        assert v["prompt_tokens"] % w["page_size"] == 0 and v["prompt_tokens"] % 32 == 0
+        assert 2 <= (w["budget"] + v["prompt_tokens"]) // w["page_size"] <= 2048
+        assert not (v["rank_pinned"] and v["prompt_tokens"])
+        assert v["prompt_topk"] <= v["prompt_tokens"] // w["page_size"]
