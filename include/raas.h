@@ -249,7 +249,8 @@ raas_status raas_export_state(raas_pool* pool, int32_t layer, int32_t* host_buf,
  * the layer's state, prefilled or not. The buffer starts with a header
  * (magic, ABI version, the configuration) that raas_load_layer checks.
  * Errors: RAAS_E_INVALID (NULL, wrong size, a header that does not match
- * this pool), RAAS_E_HIP. */
+ * this pool or holds out-of-range step bookkeeping; nothing is copied
+ * then), RAAS_E_HIP. */
 size_t raas_layer_checkpoint_bytes(const raas_pool* pool);
 raas_status raas_save_layer(raas_pool* pool, int32_t layer, void* host_buf, size_t bytes, void* stream);
 raas_status raas_load_layer(raas_pool* pool, int32_t layer, const void* host_buf, size_t bytes, void* stream);

@@ -691,7 +691,9 @@ raas_status raas_load_layer(raas_pool* p, int32_t layer, const void* host_buf, s
         return fail(RAAS_E_INVALID, "checkpoint of ABI %lld, %lld bytes", (long long)h.abi, (long long)h.bytes);
     if (memcmp(h.cfg, cfg, sizeof cfg) != 0)
         return fail(RAAS_E_INVALID, "checkpoint of a pool with another configuration");
-    if (h.prefilled != 0 && h.prefilled != 1) return fail(RAAS_E_INVALID, "corrupt checkpoint header");
+    if ((h.prefilled != 0 && h.prefilled != 1) || h.keep_max < 0 || h.keep_max > p->S || h.steps < 0 ||
+        (h.descending != 0 && h.descending != 1))
+        return fail(RAAS_E_INVALID, "corrupt checkpoint header");
     hipStream_t s = (hipStream_t)stream;
     CkptSection sec[9];
     const int n = ckpt_sections(p, layer, sec);

@@ -311,8 +311,17 @@ def test_checkpoint_resume(case):
         assert np.array_equal(sa[key], sb[key]), key
     assert evictions > 0
     other = new_pool(w.replace(r=0.25), splits, deterministic=True, **opts)  # same sizes, another rule
+
+    def corrupt(off, value):  # header: magic, abi, bytes, 16 config fields, then the host bookkeeping
+        x = buf.copy()
+        x[off:off + 8] = np.frombuffer(np.int64(value).tobytes(), np.uint8)
+        return x
+
+    keep_max, steps, desc = 8 * 20, 8 * 21, 8 * 22
     for pool, data, why in ((other, buf, "configuration"), (b, np.zeros_like(buf), "checkpoint"),
-                            (b, buf[:-256], "bytes")):
+                            (b, buf[:-256], "bytes"), (b, corrupt(keep_max, -1), "corrupt"),
+                            (b, corrupt(keep_max, b.slots + 1), "corrupt"), (b, corrupt(steps, -5), "corrupt"),
+                            (b, corrupt(desc, 2), "corrupt")):
         with pytest.raises(raas.RaasError) as e:
             pool.load_layer(0, data)
         assert e.value.code == raas.E_INVALID and why in str(e.value), str(e.value)
