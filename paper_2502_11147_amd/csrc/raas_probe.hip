@@ -200,21 +200,22 @@ extern "C" int raas_probe_stream(const raas_probe_config* c, double* us_per_laun
             }
         };
         for (int i = 0; i < 2 * c->layers; ++i) run(i);  // warm-up
-        hipEventRecord(e0, nullptr);
+        const bool rec0 = hipEventRecord(e0, nullptr) == hipSuccess;
         for (int i = 0; i < c->launches; ++i) run(2 * c->layers + i);
-        hipEventRecord(e1, nullptr);
+        const bool rec1 = hipEventRecord(e1, nullptr) == hipSuccess;
         float ms = 0.f;
-        if (hipEventSynchronize(e1) == hipSuccess && hipEventElapsedTime(&ms, e0, e1) == hipSuccess &&
+        if (rec0 && rec1 && hipEventSynchronize(e1) == hipSuccess && hipEventElapsedTime(&ms, e0, e1) == hipSuccess &&
             hipGetLastError() == hipSuccess) {
             *us_per_launch = 1e3 * ms / c->launches;
             *bytes_per_launch = (double)per_layer * 2 * 2;
             rc = 0;
         }
     }
-    if (e0) hipEventDestroy(e0);
-    if (e1) hipEventDestroy(e1);
-    if (K) hipFree(K);
-    if (V) hipFree(V);
-    if (sink) hipFree(sink);
+    // release what was taken (a failure here leaves nothing more to undo)
+    if (e0) (void)hipEventDestroy(e0);
+    if (e1) (void)hipEventDestroy(e1);
+    if (K) (void)hipFree(K);
+    if (V) (void)hipFree(V);
+    if (sink) (void)hipFree(sink);
     return rc;
 }

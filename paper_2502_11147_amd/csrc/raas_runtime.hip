@@ -44,6 +44,7 @@ struct Timing {
     size_t head = 0, count = 0;           // pairs recorded since the last read
     double folded_ms = 0.0;               // time of pairs recycled before the read
     int64_t folded_n = 0;
+    bool started = false;                 // the open pair's start event was recorded
 };
 
 }  // namespace
@@ -204,32 +205,40 @@ raas_status check_layer(const raas_pool* p, int32_t layer) {
     return RAAS_OK;
 }
 
+// Timing of kernel k's launches (profiling only): a pair of events around
+// each launch, in a ring. A HIP failure here never fails the step: events
+// that cannot be created switch the kernel's timing off, and a pair whose
+// events did not both record is not counted.
 void prof_record(raas_pool* p, int k, bool start, hipStream_t s) {
     if (!(p->prof_mask & (1 << k))) return;
     Timing& t = p->timing[k];
     if (t.start.empty()) {
-        t.start.resize(kProfRing);
-        t.stop.resize(kProfRing);
+        t.start.assign(kProfRing, nullptr);
+        t.stop.assign(kProfRing, nullptr);
         for (size_t i = 0; i < kProfRing; ++i) {
-            hipEventCreate(&t.start[i]);
-            hipEventCreate(&t.stop[i]);
+            if (hipEventCreate(&t.start[i]) != hipSuccess || hipEventCreate(&t.stop[i]) != hipSuccess) {
+                (void)hipGetLastError();
+                p->prof_mask &= ~(1 << k);
+                return;  // (raas_destroy releases the events created so far)
+            }
         }
     }
     const size_t slot = (t.head + t.count) % kProfRing;
     if (start) {
         if (t.count == kProfRing) {  // recycle the oldest pair
             float ms = 0.f;
-            hipEventSynchronize(t.stop[t.head]);
-            hipEventElapsedTime(&ms, t.start[t.head], t.stop[t.head]);
-            t.folded_ms += ms;
-            t.folded_n += 1;
+            if (hipEventSynchronize(t.stop[t.head]) == hipSuccess &&
+                hipEventElapsedTime(&ms, t.start[t.head], t.stop[t.head]) == hipSuccess) {
+                t.folded_ms += ms;
+                t.folded_n += 1;
+            }
             t.head = (t.head + 1) % kProfRing;
             t.count -= 1;
         }
-        hipEventRecord(t.start[(t.head + t.count) % kProfRing], s);
+        t.started = hipEventRecord(t.start[(t.head + t.count) % kProfRing], s) == hipSuccess;
     } else {
-        hipEventRecord(t.stop[slot], s);
-        t.count += 1;
+        if (t.started && hipEventRecord(t.stop[slot], s) == hipSuccess) t.count += 1;
+        t.started = false;
     }
 }
 
@@ -445,17 +454,21 @@ raas_status raas_create_pool(const raas_config* cfg, void* stream, raas_pool** o
 
 void raas_destroy(raas_pool* p) {
     if (!p) return;
-    if (p->K || p->meta) hipStreamSynchronize(p->last_stream);
+    // the pool's work has run before its memory goes; a failure here (a
+    // device already lost) leaves nothing else to undo, so it is not reported
+    if (p->K || p->meta) (void)hipStreamSynchronize(p->last_stream);
     for (auto& t : p->timing) {
-        for (auto ev : t.start) hipEventDestroy(ev);
-        for (auto ev : t.stop) hipEventDestroy(ev);
+        for (auto ev : t.start)
+            if (ev) (void)hipEventDestroy(ev);
+        for (auto ev : t.stop)
+            if (ev) (void)hipEventDestroy(ev);
     }
     void* ptrs[] = {p->K,     p->V,     p->kmin,  p->kmax,     p->meta,  p->unit, p->err,
                     p->part,  p->score, p->seqbuf, p->fill_att, p->blist, p->bcnt};
     for (void* q : ptrs)
-        if (q) hipFree(q);
-    if (p->seqhost) hipHostFree(p->seqhost);
-    if (p->seq_copied) hipEventDestroy(p->seq_copied);
+        if (q) (void)hipFree(q);
+    if (p->seqhost) (void)hipHostFree(p->seqhost);
+    if (p->seq_copied) (void)hipEventDestroy(p->seq_copied);
     delete p;
 }
 
