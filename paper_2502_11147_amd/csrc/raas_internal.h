@@ -59,6 +59,7 @@ struct LayerView {
     int lcap_blk;       // Lcap / 32
     int nt;             // 1: K/V blocks streamed with non-temporal loads
     int det;            // 1: each wavefront takes a fixed interleave of the blocks (reproducible sums)
+    int early;          // 1: the first score pass's loads go out before the first block is attended
 };
 
 // Prefill input of one layer: `stride` token rows per unit; per-sequence

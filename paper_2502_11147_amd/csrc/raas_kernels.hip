@@ -1229,6 +1229,10 @@ __device__ __forceinline__ void step_item(LayerView L, StepIO io, float scale_lo
             score_issue<D>(L, u, p, part, act_cur && !(p == ns && opened), frag);
         }
     };
+    // the first score pass's loads go out now, behind the first blocks' (L.early),
+    // or once the first block has been attended and its registers are free
+    const int early = L.early;
+    if (early) staged();
     int it = 0;
     while (b < bend) {
         const int f_cur = f_next;
@@ -1283,18 +1287,19 @@ __device__ __forceinline__ void step_item(LayerView L, StepIO io, float scale_lo
             attend_block<D>(kr, vr, nv, qv, scale_log2, m_run, l_run, acc);
         }
         // this block's registers are free again
-        if (it == 0) {
+        if (it == 0 && !early) {
             staged();
         } else if (pass < npass) {
             score_step();
         }
         // (the softmax aggregation waits for the end of the loop: mid-loop, its
-        // arithmetic would compete with the prefetched block for registers)
-        if (!AGG && it == npass_all) scores_done();
+        // arithmetic would compete with the prefetched block for registers;
+        // wavefront 0, which has the most passes, has finished them here)
+        if (!AGG && it == npass_all - early) scores_done();
         ++it;
         b = bn;
     }
-    if (it == 0) staged();
+    if (it == 0 && !early) staged();
     while (pass < npass) score_step();  // passes left when the wavefront ran out of blocks
     if (!decided) scores_done();
 

@@ -142,6 +142,7 @@ LayerView view(const raas_pool* p, int layer) {
     L.lcap_blk = p->Lcap / kBlockTokens;
     L.nt = p->nt;
     L.det = p->cfg.deterministic;
+    L.early = 0;
     return L;
 }
 
@@ -299,6 +300,12 @@ raas_status decode_step(raas_pool* p, int32_t layer, const StepIO& io, hipStream
                                   p->cfg.decision_scope == RAAS_SCOPE_SEQUENCE, list_ints(p), p->split_override);
     L.nsplit = pl.nsplit;
     L.bps = pl.bps;
+    // the first score pass issued with the first blocks: the score barrier and
+    // the retention come a block sooner, which pays where a workgroup of 8
+    // wavefronts streams at least 8 blocks each (batch 32 at L 2048: 40.79 ->
+    // 40.38 us, the Qwen stack and L 8192 level) and not below (batch 1 at
+    // L 1024 +0.14 us; batch 128 at L 512, 2 wavefronts, +0.23 us)
+    L.early = pl.waves == 8 && L.nblk >= 8 * pl.waves ? 1 : 0;
     const bool select_kernel = p->npr > 0 && !pl.select_in_step;
     if (fixed_scratch) {
         const size_t U = (size_t)p->U, S = (size_t)p->S;
