@@ -259,6 +259,24 @@ def test_deterministic_option_parity(case):
     assert rep.evictions > 0
 
 
+@pytest.mark.parametrize("splits", [None, 1], ids=["auto-split", "fused"])
+@pytest.mark.parametrize("det", [False, True], ids=["dynamic", "deterministic"])
+def test_long_pool_small_batch(det, splits):
+    """Pools of 64 blocks and more at 4 units, whose workgroups of 8
+    wavefronts issue the first score pass with the first blocks: the plan's
+    own split over the CUs, and one fused workgroup per unit (the plan of
+    the batch-32 workload, forced here), with every unit's outputs compared
+    at every step, through the budget and 600 steps past it, with the
+    dynamic claims and the deterministic option."""
+    w = small(batch=2, n_kv_heads=2, n_q_heads=8, budget=2048, prefill_len=1000, decode_steps=1700)
+    _say("case long pool small batch deterministic %s splits %s" % (det, splits))
+    pool = new_pool(w, splits, deterministic=det)
+    rep = run_parity(w, seed=19, steps=w.decode_steps, pool=pool)
+    pool.close()
+    _report(rep, "long pool small batch")
+    assert rep.evictions > 0
+
+
 @pytest.mark.parametrize("case", [dict(), dict(splits=3), dict(dtype="f32"), dict(prompt_tokens=128, prompt_topk=3)],
                          ids=["fused", "split", "f32", "prompt-selection"])
 def test_checkpoint_resume(case):
