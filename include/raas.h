@@ -141,7 +141,7 @@ typedef struct raas_pool raas_pool; /* opaque */
  * RAAS_E_HIP. */
 raas_status raas_create_pool(const raas_config* cfg, void* stream, raas_pool** out);
 
-/* kvm.store_cache(K, V, -, "prefill") of Algorithm 1 for one layer: stores
+/* The prefill stage of Algorithm 1's cache store, for one layer: stores
  * the prefill_len (>= 0) tokens of every unit in pages 0, 1, ... and marks
  * them non-evictable; sets the clock to prefill_len. A partial last page is
  * not topped up by decode tokens. k, v: [batch][n_kv_heads][prefill_len]

@@ -163,9 +163,9 @@ static void page_store_token(orc_kvm* m, int s, const double* k, const double* v
     m->fill[s] += 1;
 }
 
-/* kvm.store_cache(K, V, -, "prefill"): store the prefill tokens' K/V in
- * pages and mark them non-evictable (Algorithm 1; Section 3.1 keeps every
- * prefill token). K, V: [P][d]. */
+/* The prefill stage of Algorithm 1's cache store: the prompt's K/V go into
+ * pages that are never evicted (Section 3.1 keeps every prefill token).
+ * K, V: [P][d]. */
 int orc_prefill(orc_kvm* m, const double* K, const double* V, int P) {
     if (!m || P < 0 || (P > 0 && (!K || !V))) return ORC_E_INVALID;
     if (m->prefilled) return ORC_E_STATE;
@@ -195,9 +195,9 @@ int orc_prefill(orc_kvm* m, const double* K, const double* V, int P) {
     return ORC_OK;
 }
 
-/* kvm.load_cache + "K = K_old::K_new" + attention(Q, K, V) (Algorithm 1):
- * exact softmax attention of each of the G queries over every resident
- * token plus the new one (R9). out: [G][d]. */
+/* Algorithm 1's attention step: exact softmax attention of each of the G
+ * queries over the cached tokens with the new one appended (R9).
+ * out: [G][d]. */
 static void attention(const orc_kvm* m, const double* q, const double* k_new, const double* v_new,
                       double* out) {
     const int G = m->G, d = m->d, ps = m->ps;
@@ -245,7 +245,7 @@ static int cmp_double(const void* a, const void* b) {
     return (x > y) - (x < y);
 }
 
-/* kvm.is_full(): the next token has no room (R8) */
+/* Algorithm 1's fullness test: the next token has no room (R8) */
 static int is_full(const orc_kvm* m) {
     if (m->tail >= 0 && m->fill[m->tail] < m->ps) return 0;
     for (int s = m->decode_base; s < m->S; ++s)
@@ -290,8 +290,8 @@ static void select_attended(orc_kvm* m, const double* q) {
     free(b);
 }
 
-/* store K_new, V_new: into the tail page, or a fresh page taken from the
- * lowest free slot when the tail is full or absent (Section 3.3). Without
+/* The new token's K/V go into the tail page, or into a fresh page taken from
+ * the lowest free slot when the tail is full or absent (Section 3.3). Without
  * k_new/v_new (retention-only runs) the token takes its place but no
  * payload. */
 static int store_new_token(orc_kvm* m, const double* k_new, const double* v_new) {
@@ -395,7 +395,8 @@ static void refresh(orc_kvm* m, int c) {
     }
 }
 
-/* if kvm.is_full(): evict the page with the oldest timestamp (R6, R8) */
+/* Eviction when the cache is full: the evictable page of oldest timestamp
+ * goes (R6, R8) */
 static int evict_if_full(orc_kvm* m) {
     const int S = m->S;
     m->evicted = -1;
@@ -421,9 +422,10 @@ static int evict_if_full(orc_kvm* m) {
 }
 
 /*
- * One decode step of one unit: attention, then kvm.store_cache(.., "decode")
- * = store K_new/V_new, give the top-r pages the latest timestamp, and evict
- * the oldest page when the cache is full (Algorithm 1, Section 3.3).
+ * One decode step of one unit: attention, then the decode stage of the
+ * cache store: the new token joins the cache, the top-r pages are stamped
+ * with the current clock, and a full cache evicts its page of oldest stamp
+ * (Algorithm 1, Section 3.3).
  *
  * q: [G][d]; k_new, v_new: [d]; out: [G][d] or NULL (attention skipped).
  * injected: NULL, or per-slot page scores that replace the representative

@@ -26,13 +26,32 @@ def hipcc_command(out: str, sources=None) -> list[str]:
     ]
 
 
+def _code_text(src: str) -> str:
+    """C++ source without its comments and with whitespace runs collapsed
+    (the kernels' sources hold no comment markers inside literals)."""
+    out, i, n = [], 0, len(src)
+    while i < n:
+        if src.startswith("//", i):
+            j = src.find("\n", i)
+            i = n if j < 0 else j
+        elif src.startswith("/*", i):
+            j = src.find("*/", i + 2)
+            i = n if j < 0 else j + 2
+            out.append(" ")
+        else:
+            out.append(src[i])
+            i += 1
+    return " ".join("".join(out).split())
+
+
 def kernel_digest() -> str:
-    """sha256 over the kernel sources and the compile flags: identifies the
-    kernels that a stored hardware-counter measurement was taken on."""
+    """sha256 over the kernel sources' code (comments and layout left out)
+    and the compile flags: identifies the kernels that a stored
+    hardware-counter measurement was taken on."""
     h = hashlib.sha256()
     for p in (os.path.join(CSRC, "raas_kernels.hip"), os.path.join(CSRC, "raas_internal.h")):
-        with open(p, "rb") as f:
-            h.update(f.read())
+        with open(p, encoding="utf-8") as f:
+            h.update(_code_text(f.read()).encode())
     h.update(" ".join(a for a in hipcc_command("lib") if not os.path.isabs(a) and a not in ("-I", "-o", "lib")).encode())
     return h.hexdigest()
 

@@ -88,7 +88,7 @@ __device__ __forceinline__ uint16_t u16_at(const u32x4& x, int e) {
 }
 
 // ---------------------------------------------------------------------------
-// Prefill (kvm.store_cache(.., "prefill"), Algorithm 1): a unit's first
+// Prefill (the prefill stage of Algorithm 1's cache store): a unit's first
 // tokens go to pages 0, 1, ..., which are marked pinned; at most S-1 pages
 // are kept (the first ones), so one slot stays for decode pages. Lengths are
 // per sequence (in.lens) or uniform (in.P); in.mask, when given, selects the
@@ -557,8 +557,8 @@ __device__ void softmax_sum_block(const LayerView& L, const double* hb, int nu, 
     __syncthreads();
 }
 
-// Retention policy of one unit, run by one wavefront (Algorithm 1,
-// store_cache; Sections 3.2-3.3) on the slot state in LDS, the opened page
+// Retention policy of one unit, run by one wavefront (Algorithm 1, the
+// decode-stage cache store; Sections 3.2-3.3) on the slot state in LDS, the opened page
 // already marked evictable and s_score holding every ranked page's score
 // (+inf elsewhere):
 //  - top-r refresh: with n ranked pages and k = floor(r*n), an evictable

@@ -149,3 +149,16 @@ def test_binding_fails_loudly_without_library(tmp_path):
             raas.load_library(str(tmp_path / "missing.so"))
     finally:
         raas._lib = saved
+
+
+def test_kernel_digest_follows_code_not_comments():
+    """The digest that stored counter profiles are checked against covers the
+    kernels' code: comments and layout leave it alone, any token changes it."""
+    from paper_2502_11147_amd import build
+
+    a = "int f(int x) { // one\n  return x + 1; /* two */ }\n"
+    b = "int f(int x) {\n\n  return x + 1;   }  // reworded\n"
+    c = "int f(int x) { return x + 2; }"
+    assert build._code_text(a) == build._code_text(b) == "int f(int x) { return x + 1; }"
+    assert build._code_text(c) != build._code_text(a)
+    assert len(build.kernel_digest()) == 64
