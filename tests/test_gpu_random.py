@@ -5,13 +5,15 @@ hand-picked cases. The draws are fixed by the case index, so a failure
 names a reproducible configuration."""
 from __future__ import annotations
 
+import os
+
 import pytest
 
 from harness import new_pool, random_case, record, run_parity, say
 
 pytestmark = pytest.mark.gpu
 
-N_CASES = 64
+N_CASES = int(os.environ.get("RAAS_RANDOM_CASES", "64"))  # more for a longer sweep
 
 
 @pytest.fixture(scope="module", autouse=True)
