@@ -164,6 +164,46 @@ def random_case(i: int) -> dict:
                 splits=splits, deterministic=det)
 
 
+def random_large_case(i: int) -> dict:
+    """Seeded random configuration i with a long pool: budgets of 1024 to
+    4096 tokens (up to 512 slots at page 8, past the 256 where the split
+    path's refresh turns to a radix select), prompt regions up to 2048
+    tokens, at most 4 units, the same switches as random_case. Outputs are
+    meant to be compared on sampled steps (retention at every step)."""
+    import math
+
+    rng = np.random.default_rng(5000 + i)
+    dtype = "f32" if rng.random() < 0.15 else "bf16"
+    d = int(rng.choice([64, 128]))
+    G = int(rng.choice([1, 2, 4, 7, 8, 16]))
+    hkv = int(rng.choice([1, 2]))
+    batch = int(rng.integers(1, 3))
+    ps = int(rng.choice([8, 16, 32, 64]))
+    budget = ps * int(rng.integers(max(2, 1024 // ps), 4096 // ps + 1))
+    prefill = int(rng.integers(0, budget + 1))
+    r = float(rng.choice([0.25, 0.5, 0.7, 0.9]))
+    agg = int(rng.random() < 0.2)
+    scope = int(rng.random() < 0.15)
+    prompt = bool(rng.random() < 0.25)
+    rank = (not prompt) and bool(rng.random() < 0.15)
+    prompt_tokens = prompt_topk = 0
+    if prompt:
+        unit = ps * 32 // math.gcd(ps, 32)
+        prompt_tokens = unit * int(rng.integers(1, max(1, 2048 // unit) + 1))
+        prompt_topk = int(rng.integers(1, prompt_tokens // ps + 1))
+    splits = None if rng.random() < 0.6 else int(rng.choice([1, 2, 5, 16, 64]))
+    det = bool(rng.random() < 0.15)
+    kept = 0 if prompt else min(prefill, budget)
+    steps = int(budget - kept + 3 * ps + 40)
+    return dict(workload=dict(name="random-large-%02d" % i, batch=batch, n_layers=1, n_q_heads=G * hkv,
+                              n_kv_heads=hkv, head_dim=d, dtype=dtype, page_size=ps, budget=budget,
+                              prefill_len=prefill, decode_steps=steps, r=r, ms_period=32,
+                              ms_phase_random=True, ms_wmin=16, ms_wmax=256),
+                variant=dict(aggregation=agg, rank_pinned=rank, scope=scope, prompt_tokens=prompt_tokens,
+                             prompt_topk=prompt_topk),
+                splits=splits, deterministic=det)
+
+
 def unit_index(w, seq, kvh):
     return seq * w.n_kv_heads + kvh
 

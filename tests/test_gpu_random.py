@@ -9,11 +9,12 @@ import os
 
 import pytest
 
-from harness import new_pool, random_case, record, run_parity, say
+from harness import new_pool, random_case, random_large_case, record, run_parity, say
 
 pytestmark = pytest.mark.gpu
 
 N_CASES = int(os.environ.get("RAAS_RANDOM_CASES", "64"))  # more for a longer sweep
+N_LARGE = int(os.environ.get("RAAS_RANDOM_LARGE_CASES", "16"))
 
 
 @pytest.fixture(scope="module", autouse=True)
@@ -41,3 +42,22 @@ def test_random_config_parity(i):
     record(rep, "random %02d" % i)
     assert rep.flagged_divergences == 0, rep.line("random %02d" % i)
     assert rep.evictions > 0, rep.line("random %02d" % i)  # every case runs past its budget
+
+
+@pytest.mark.parametrize("i", range(N_LARGE), ids=["large-%02d" % i for i in range(N_LARGE)])
+def test_random_large_config_parity(i):
+    """Long pools (harness.random_large_case): retention of every unit at
+    every step, outputs every 32nd step, past the budget."""
+    import synth
+
+    c = random_large_case(i)
+    w = synth.Workload(**c["workload"])
+    say("case %s %s splits %s deterministic %s" % (c["workload"], c["variant"], c["splits"], c["deterministic"]))
+    pool = new_pool(w, c["splits"], deterministic=c["deterministic"], **c["variant"])
+    try:
+        rep = run_parity(w, seed=90 + i, steps=w.decode_steps, pool=pool, out_every=32, **c["variant"])
+    finally:
+        pool.close()
+    record(rep, "random large %02d" % i)
+    assert rep.flagged_divergences == 0, rep.line("random large %02d" % i)
+    assert rep.evictions > 0, rep.line("random large %02d" % i)

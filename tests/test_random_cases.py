@@ -1,8 +1,8 @@
 """The seeded random configurations of the GPU sweep (harness.random_case)
 are valid pools and cover each switch both ways."""
-from harness import random_case
+from harness import random_case, random_large_case
 
-from test_gpu_random import N_CASES
+from test_gpu_random import N_CASES, N_LARGE
 
 
 def test_random_cases_are_valid_and_varied():
@@ -25,6 +25,20 @@ def test_random_cases_are_valid_and_varied():
         w, v = c["workload"], c["variant"]
         assert w["n_q_heads"] % w["n_kv_heads"] == 0 and w["n_q_heads"] // w["n_kv_heads"] <= 16
         assert w["budget"] % w["page_size"] == 0
+        assert v["prompt_tokens"] % w["page_size"] == 0 and v["prompt_tokens"] % 32 == 0
+        assert 2 <= (w["budget"] + v["prompt_tokens"]) // w["page_size"] <= 2048
+        assert not (v["rank_pinned"] and v["prompt_tokens"])
+        assert v["prompt_topk"] <= v["prompt_tokens"] // w["page_size"]
+
+
+def test_random_large_cases_are_valid():
+    cases = [random_large_case(i) for i in range(max(N_LARGE, 16))]
+    assert {c["variant"]["prompt_tokens"] > 0 for c in cases} == {False, True}
+    assert any((c["workload"]["budget"] + c["variant"]["prompt_tokens"]) // c["workload"]["page_size"] > 256
+               for c in cases)
+    for c in cases:
+        w, v = c["workload"], c["variant"]
+        assert w["n_q_heads"] // w["n_kv_heads"] <= 16 and w["budget"] % w["page_size"] == 0
         assert v["prompt_tokens"] % w["page_size"] == 0 and v["prompt_tokens"] % 32 == 0
         assert 2 <= (w["budget"] + v["prompt_tokens"]) // w["page_size"] <= 2048
         assert not (v["rank_pinned"] and v["prompt_tokens"])
