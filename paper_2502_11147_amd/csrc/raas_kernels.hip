@@ -436,9 +436,9 @@ __device__ __forceinline__ uint32_t mag_floor(uint32_t x) {
 // Written to lo/hi, with (-inf, inf) where a sum is not finite. Each
 // wavefront takes tiles w, w + NW, ..., TPW of them loaded at once. q_ops:
 // this lane's query operands (heads as columns).
-template <int D, int NW>
+template <int D, int NW, class Issue>
 __device__ __forceinline__ void prompt_bounds(const LayerView& L, size_t base, int npages, const bf16x8 (&q_ops)[D / 32],
-                                              float* lo, float* hi) {
+                                              float* lo, float* hi, Issue&& issue) {
     constexpr int KS = D / 32, TPW = D >= 128 ? 2 : 4;
     const int lane = threadIdx.x & 63, w = threadIdx.x >> 6, grp = lane >> 4, col = lane & 15;
     u32x4 qpos[KS], qneg[KS];
@@ -458,11 +458,12 @@ __device__ __forceinline__ void prompt_bounds(const LayerView& L, size_t base, i
     };
     auto floored = [](u32x4 x) { return u32x4{mag_floor(x[0]), mag_floor(x[1]), mag_floor(x[2]), mag_floor(x[3])}; };
     const int ntile = (npages + 15) / 16;
-    for (int t0 = w; t0 < ntile; t0 += TPW * NW) {
-        // lane (grp, col) supplies page 16t + col's channels 32ks + 8grp .. +7
-        // (rows past npages, and tiles past the last, repeat the last page and
-        // are not written)
-        u32x4 ax[TPW][KS], an[TPW][KS];
+    constexpr int RT = TPW * NW;  // tiles per round of the workgroup
+    const int nround = w < ntile ? (ntile - w + RT - 1) / RT : 0;  // rounds of this wavefront
+    // lane (grp, col) supplies page 16t + col's channels 32ks + 8grp .. +7
+    // (rows past npages, and tiles past the last, repeat the last page and
+    // are not written)
+    auto load = [&](int t0, u32x4 (&ax)[TPW][KS], u32x4 (&an)[TPW][KS]) {
 #pragma unroll
         for (int h = 0; h < TPW; ++h) {
             const int t = min(t0 + h * NW, ntile - 1);
@@ -473,10 +474,11 @@ __device__ __forceinline__ void prompt_bounds(const LayerView& L, size_t base, i
                 an[h][ks] = ld4((const uint16_t*)L.kmin + off + 32 * ks);
             }
         }
+    };
+    auto bound = [&](int t0, const u32x4 (&ax)[TPW][KS], const u32x4 (&an)[TPW][KS]) {
 #pragma unroll
         for (int h = 0; h < TPW; ++h) {
-            const int t = t0 + h * NW;
-            if (t >= ntile) break;  // (uniform over the wavefront)
+            const int t = t0 + h * NW;  // (a tile past the last is computed and not written)
             f32x4 sb = {0.f, 0.f, 0.f, 0.f}, se = {0.f, 0.f, 0.f, 0.f};
 #pragma unroll
             for (int ks = 0; ks < KS; ++ks) {
@@ -503,7 +505,22 @@ __device__ __forceinline__ void prompt_bounds(const LayerView& L, size_t base, i
                 }
             }
         }
+    };
+    for (int r = 0; r + 1 < nround; ++r) {
+        u32x4 ax[TPW][KS], an[TPW][KS];
+        load(w + r * RT, ax, an);
+        bound(w + r * RT, ax, an);
     }
+    // the last round: its tiles, then the caller's loads, which the wait for
+    // the tiles leaves in flight (loads complete in issue order); a wavefront
+    // with no tile loads the last one and writes nothing
+    const int tl = w + max(nround - 1, 0) * RT;
+    u32x4 ax[TPW][KS], an[TPW][KS];
+    load(tl, ax, an);
+    __builtin_amdgcn_sched_barrier(0);  // (the caller's loads stay behind the tiles')
+    issue();
+    __builtin_amdgcn_sched_barrier(0);
+    bound(tl, ax, an);
 }
 
 // Results of the retention policy for one step, computed by the retention
@@ -809,6 +826,9 @@ __device__ __forceinline__ void wave_lds_sync() {
     __builtin_amdgcn_fence(__ATOMIC_ACQUIRE, "wavefront");
 }
 
+// Waits for every vector-memory load in flight (vmcnt(0); expcnt and lgkmcnt left at their maxima).
+__device__ __forceinline__ void vm_drain() { __builtin_amdgcn_s_waitcnt(0x0F70); }
+
 // Workgroup barrier that waits for this wavefront's LDS traffic only: loads
 // already issued to global memory stay in flight across it.
 __device__ __forceinline__ void lds_barrier() {
@@ -1000,7 +1020,8 @@ __device__ __forceinline__ void step_item(LayerView L, StepIO io, float scale_lo
     // Loads complete in issue order, so the small reads go out first: the
     // unit record, this thread's staging elements and slot, the first
     // block's fill and the queries; then the first block (its index w is
-    // static), which the staging below no longer waits for.
+    // static), which the staging below no longer waits for (LM 2: the
+    // staging, then the bound tiles, then the first block).
     const int32_t* U4 = L.unit + (size_t)u * kUnitFields;
     const UnitRec ur{U4[kNextSlot], U4[kNextFill], U4[kClock], U4[kNextLid]};
     const int pinned = U4[kPinnedPages];
@@ -1022,6 +1043,15 @@ __device__ __forceinline__ void step_item(LayerView L, StepIO io, float scale_lo
     const int s_first = tid < S ? tid : 0;
     const int st_first = L.state[base + s_first], ts_first = L.ts[base + s_first], lid_first = L.lid[base + s_first];
     const int pf_first = LM == 2 ? fu[tid < L.dbase ? tid : 0] : 0;  // LM 2: a prompt page's fill
+    // LM 2: a second slot and prompt page per thread, with the reads above
+    const int sl_sec = tid + NW * 64 < S ? tid + NW * 64 : 0, pg_sec = tid + NW * 64 < L.dbase ? tid + NW * 64 : 0;
+    int st_sec = 0, ts_sec = 0, lid_sec = 0, pf_sec = 0;
+    if constexpr (LM == 2) {
+        st_sec = L.state[base + sl_sec];
+        ts_sec = L.ts[base + sl_sec];
+        lid_sec = L.lid[base + sl_sec];
+        pf_sec = fu[pg_sec];
+    }
     bf16x8 qv[KS];
 #pragma unroll
     for (int ks = 0; ks < KS; ++ks) {
@@ -1029,12 +1059,58 @@ __device__ __forceinline__ void step_item(LayerView L, StepIO io, float scale_lo
         qv[ks] = __builtin_bit_cast(bf16x8, x);
     }
     u32x4 kr_next[2][KS], vr_next[NB];
-    if (real(b)) load_block(b, kr_next, vr_next);
-    // LM 2: the prompt region's bound intervals (the selection reads those of the
-    // kept pages), their loads behind the first block's and not waiting for the
-    // unit record
+    int f_first = 0;  // LM 2: the first block's fill
     if constexpr (LM == 2) {
-        if (L.dbase > L.topk) prompt_bounds<D, NW>(L, base, L.dbase, qv, s_plo, s_phi);
+        // The staging first (the other instances stage below, behind the first
+        // block's loads), so that none of its reads waits behind the bound
+        // tiles or the block: they go out about when the tiles would, which
+        // wait for the queries anyway.
+        if (tid < L.dbase) s_fatt[tid] = tid < pinned ? pf_first : 0;  // the kept prompt pages' fills
+        if (tid + NW * 64 < L.dbase) s_fatt[tid + NW * 64] = tid + NW * 64 < pinned ? pf_sec : 0;
+        for (int p = tid + 2 * NW * 64; p < L.dbase; p += NW * 64) s_fatt[p] = p < pinned ? fu[p] : 0;
+        // q in fp32 from the query operands: lane (grp, col < G) holds head
+        // col's channels 32 ks + 8 grp .. +7, one padded row segment; the
+        // wavefronts take turns over ks
+#pragma unroll
+        for (int ks = 0; ks < KS; ++ks) {
+            if (ks % NW == w && col < G) {
+                const u32x4 x = __builtin_bit_cast(u32x4, qv[ks]);
+                float* d = s_qf + qpad_index<D>(col * D + 32 * ks + 8 * grp);
+#pragma unroll
+                for (int h = 0; h < 4; ++h) {
+                    d[2 * h] = __uint_as_float(x[h] << 16);
+                    d[2 * h + 1] = __uint_as_float(x[h] & 0xFFFF0000u);
+                }
+            }
+        }
+        if (tid < D / 8) {
+            st4(&s_kn[8 * tid], kn_first);
+            st4(&s_vn[8 * tid], vn_first);
+        }
+        if (fused) {  // (always, with LM 2)
+            if (tid < S) stage_slot(ur, tid, st_first, ts_first, lid_first, s_score, s_state, s_ts, s_lid);
+            if (tid + NW * 64 < S) stage_slot(ur, tid + NW * 64, st_sec, ts_sec, lid_sec, s_score, s_state, s_ts, s_lid);
+            load_slots(L, u, ur, s_score, s_state, s_ts, s_lid, 2 * NW * 64);
+        }
+        if (tid == 0) {
+            s_next = 2 * NW;  // claims start after the two static blocks of every wavefront
+            s_lo = 0x7FFFFFFF;
+            s_ncand = 0;
+        }
+        if (w < nown) f_first = slot_first < S ? (slot_first == ur.ns ? ur.nf + 1 : fill_first) : 0;
+        // nothing else is in flight yet: every read has landed from here on,
+        // also to the compiler, which loses count of loads issued in loops
+        vm_drain();
+        // the prompt region's bound intervals (the selection reads those of the
+        // kept pages), and behind their last loads the first block, which
+        // streams during the selection; a wavefront with no decode block reads
+        // block 0 and drops it (loads on every path keep the waits for the
+        // tiles short of the block)
+        auto first = [&]() { load_block(real(b) ? b : 0, kr_next, vr_next); };
+        if (L.dbase > L.topk) prompt_bounds<D, NW>(L, base, L.dbase, qv, s_plo, s_phi, first);
+        else first();
+    } else {
+        if (real(b)) load_block(b, kr_next, vr_next);
     }
 
     const int ns = ur.ns, nf = ur.nf;
@@ -1067,30 +1143,22 @@ __device__ __forceinline__ void step_item(LayerView L, StepIO io, float scale_lo
         const int t0 = 32 * b + 8 * grp;
         return min(max(f - (t0 - (t0 / ps) * ps), 0), 8);
     };
-    int f_next = 0;
-    if (real(b)) f_next = (w < nown) ? (slot_first < S ? (slot_first == ns ? nf + 1 : fill_first) : 0) : row_fill(b);
+    int f_next = f_first;
+    if constexpr (LM != 2) {
+        if (real(b)) f_next = (w < nown) ? (slot_first < S ? (slot_first == ns ? nf + 1 : fill_first) : 0) : row_fill(b);
 
-    // staging for the scores and the epilogue
-    if constexpr (LM == 2) {  // the kept prompt pages' fills (the selection clears those it drops)
-        if (tid < L.dbase) s_fatt[tid] = tid < pinned ? pf_first : 0;
-        for (int p = tid + NW * 64; p < L.dbase; p += NW * 64) s_fatt[p] = p < pinned ? fu[p] : 0;
-    }
-    if (tid < G * D) s_qf[qpad_index<D>(tid)] = bf2f(q_first);
-    for (int i = tid + NW * 64; i < G * D; i += NW * 64) s_qf[qpad_index<D>(i)] = bf2f(qg[i]);
-    if (tid < D / 8) {
-        st4(&s_kn[8 * tid], kn_first);
-        st4(&s_vn[8 * tid], vn_first);
-    }
-    if (fused) {
-        if (tid < S) stage_slot(ur, tid, st_first, ts_first, lid_first, s_score, s_state, s_ts, s_lid);
-        load_slots(L, u, ur, s_score, s_state, s_ts, s_lid, NW * 64);
-    }
-    if (tid == 0) {
-        s_next = 2 * NW;  // claims start after the two static blocks of every wavefront
-        if constexpr (LM == 2) {
-            s_lo = 0x7FFFFFFF;
-            s_ncand = 0;
+        // staging for the scores and the epilogue
+        if (tid < G * D) s_qf[qpad_index<D>(tid)] = bf2f(q_first);
+        for (int i = tid + NW * 64; i < G * D; i += NW * 64) s_qf[qpad_index<D>(i)] = bf2f(qg[i]);
+        if (tid < D / 8) {
+            st4(&s_kn[8 * tid], kn_first);
+            st4(&s_vn[8 * tid], vn_first);
         }
+        if (fused) {
+            if (tid < S) stage_slot(ur, tid, st_first, ts_first, lid_first, s_score, s_state, s_ts, s_lid);
+            load_slots(L, u, ur, s_score, s_state, s_ts, s_lid, NW * 64);
+        }
+        if (tid == 0) s_next = 2 * NW;  // claims start after the two static blocks of every wavefront
     }
     // the staging is visible: the first block is still in flight, and every
     // wavefront reaches this point after the same short reads
@@ -1105,17 +1173,17 @@ __device__ __forceinline__ void step_item(LayerView L, StepIO io, float scale_lo
         // candidates with upper end >= lo, and rank among them as among all
         // kept pages.
         if (pinned > L.topk && L.topk > 0) {
+            const int pin4 = pinned & ~3;
             for (int p = tid; p < pinned; p += NW * 64) {
-                // lower ends above p's, four per 16-byte read (a read past the last
-                // kept page stays inside the workgroup's LDS and is not counted)
+                // lower ends above p's: four per 16-byte read, then the last few
                 const float lp = s_plo[p];
                 int above = 0;
 #pragma unroll 4
-                for (int o = 0; o < pinned; o += 4) {
+                for (int o = 0; o < pin4; o += 4) {
                     const float4 x = *reinterpret_cast<const float4*>(s_plo + o);
-                    above += (x.x > lp ? 1 : 0) + (o + 1 < pinned && x.y > lp ? 1 : 0) +
-                             (o + 2 < pinned && x.z > lp ? 1 : 0) + (o + 3 < pinned && x.w > lp ? 1 : 0);
+                    above += (x.x > lp ? 1 : 0) + (x.y > lp ? 1 : 0) + (x.z > lp ? 1 : 0) + (x.w > lp ? 1 : 0);
                 }
+                for (int o = pin4; o < pinned; ++o) above += s_plo[o] > lp ? 1 : 0;
                 if (above < L.topk) atomicMin(&s_lo, float_order(lp));
             }
             lds_barrier();
