@@ -828,6 +828,23 @@ def test_prompt_selection_extreme_keys(splits):
     assert chosen.min() < U * w.decode_steps and chosen.max() > 0  # a real choice among the pages
 
 
+@pytest.mark.parametrize("batch,prompt", [(128, 3072), (64, 4608)], ids=["1024-units", "512-units"])
+def test_prompt_selection_large_region(batch, prompt):
+    """Prompt regions of more pages than twice a workgroup's threads (page 8:
+    384 kept pages at batch 128, whose 1024 units run in workgroups of 2
+    wavefronts, four per CU; 576 at batch 64, 512 units in workgroups of 4),
+    and slots likewise (416 and 608): the in-step selection stages fills and
+    slot records past the two each thread reads with its first loads. The
+    decode budget (256 tokens) runs past full; sampled units."""
+    w = synth.get_workload("llama8b-b128-ps32-L512").replace(
+        name="prompt-region-%d" % prompt, batch=batch, page_size=8, budget=256, prefill_len=prompt)
+    _say("case prompt-selection large region batch %d prompt %d" % (batch, prompt))
+    rep = run_parity(w, seed=0, steps=400, units=_sample_units(w, 4), out_every=16, chunk=128,
+                     prompt_tokens=prompt, prompt_topk=12)
+    _report(rep, "prompt-selection large region")
+    assert rep.evictions > 0
+
+
 @pytest.mark.parametrize("name,topk,steps,units", [("llama8b-b128-ps32-L512", 8, 640, 8),
                                                    ("llama8b-b128-ps32-L2048", 16, 2112, 4)])
 def test_prompt_selection_full_size(name, topk, steps, units):
