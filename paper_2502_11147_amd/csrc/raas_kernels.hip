@@ -435,7 +435,8 @@ __device__ __forceinline__ uint32_t mag_floor(uint32_t x) {
 // B -+ (2^-13 E + 1e-30) at D up to 128, with room for E's own rounding.
 // Written to lo/hi, with (-inf, inf) where a sum is not finite. Each
 // wavefront takes tiles w, w + NW, ..., TPW of them loaded at once. q_ops:
-// this lane's query operands (heads as columns).
+// this lane's query operands (heads as columns). issue: the caller's loads,
+// issued behind the last round of tiles on every wavefront.
 template <int D, int NW, class Issue>
 __device__ __forceinline__ void prompt_bounds(const LayerView& L, size_t base, int npages, const bf16x8 (&q_ops)[D / 32],
                                               float* lo, float* hi, Issue&& issue) {
