@@ -35,9 +35,11 @@
  *     head's softmax probability over the ranked pages, the representative
  *     bound standing for the page's logit: sum_j exp(scale*(b_j(p) - M_j)) /
  *     sum_p' exp(scale*(b_j(p') - M_j)), M_j the head's largest bound,
- *     scale 1/sqrt(d). The paper names no such aggregation; the scale in
- *     particular is a reading and its value is parity unpinned (the pins fix
- *     the normalisation, a lone page's value and the G = 1 reduction to R2).
+ *     scale 1/sqrt(d). The paper names no such aggregation: the scale in
+ *     particular is a reading, not a value the paper fixes. The pins hold
+ *     the normalisation, a lone page's value, the G = 1 reduction to R2 and,
+ *     through a step worked by hand (tests/golden), the scale the oracle
+ *     uses: under scale 1 that step would refresh another page.
  *  rank_pinned 1: the pinned prompt pages are ranked together with the
  *     decode pages (n and k count them); only decode pages take timestamps.
  * Variant of the decision scope (orc_decode_group): one page table per
