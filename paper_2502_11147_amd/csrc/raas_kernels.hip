@@ -437,7 +437,7 @@ __device__ __forceinline__ uint32_t mag_floor(uint32_t x) {
 // wavefront takes tiles w, w + NW, ..., TPW of them loaded at once. q_ops:
 // this lane's query operands (heads as columns). issue: the caller's loads,
 // issued behind the last round of tiles on every wavefront.
-template <int D, int NW, class Issue>
+template <int D, int NW, bool NT, class Issue>
 __device__ __forceinline__ void prompt_bounds(const LayerView& L, size_t base, int npages, const bf16x8 (&q_ops)[D / 32],
                                               float* lo, float* hi, Issue&& issue) {
     constexpr int KS = D / 32, TPW = D >= 128 ? 2 : 4;
@@ -471,8 +471,15 @@ __device__ __forceinline__ void prompt_bounds(const LayerView& L, size_t base, i
             const size_t off = (base + min(16 * t + col, npages - 1)) * D + 8 * grp;
 #pragma unroll
             for (int ks = 0; ks < KS; ++ks) {
-                ax[h][ks] = ld4((const uint16_t*)L.kmax + off + 32 * ks);
-                an[h][ks] = ld4((const uint16_t*)L.kmin + off + 32 * ks);
+                const uint16_t* px = (const uint16_t*)L.kmax + off + 32 * ks;
+                const uint16_t* pn = (const uint16_t*)L.kmin + off + 32 * ks;
+                if constexpr (NT) {
+                    ax[h][ks] = __builtin_nontemporal_load(reinterpret_cast<const u32x4*>(px));
+                    an[h][ks] = __builtin_nontemporal_load(reinterpret_cast<const u32x4*>(pn));
+                } else {
+                    ax[h][ks] = ld4(px);
+                    an[h][ks] = ld4(pn);
+                }
             }
         }
     };
@@ -1108,7 +1115,7 @@ __device__ __forceinline__ void step_item(LayerView L, StepIO io, float scale_lo
         // block 0 and drops it (loads on every path keep the waits for the
         // tiles short of the block)
         auto first = [&]() { load_block(real(b) ? b : 0, kr_next, vr_next); };
-        if (L.dbase > L.topk) prompt_bounds<D, NW>(L, base, L.dbase, qv, s_plo, s_phi, first);
+        if (L.dbase > L.topk) prompt_bounds<D, NW, NT>(L, base, L.dbase, qv, s_plo, s_phi, first);
         else first();
     } else {
         if (real(b)) load_block(b, kr_next, vr_next);
@@ -1955,10 +1962,14 @@ hipError_t launch_step_bf16(const LayerView& L, const StepIO& io, const StepPlan
                             hipStream_t s) {
     const bool list = L.topk >= 0;
     if (L.agg) {
-        if (list) launch_step_inst<D, NW, true, 1>(L, io, pl, sl2, r, s);
+        if (list && L.nt) launch_step_inst<D, NW, true, 1, true>(L, io, pl, sl2, r, s);
+        else if (list) launch_step_inst<D, NW, true, 1>(L, io, pl, sl2, r, s);
+        else if (L.nt) launch_step_inst<D, NW, true, 0, true>(L, io, pl, sl2, r, s);
         else launch_step_inst<D, NW, true, 0>(L, io, pl, sl2, r, s);
     } else {
-        if (pl.select_in_step) launch_step_inst<D, NW, false, 2>(L, io, pl, sl2, r, s);
+        if (pl.select_in_step && L.nt) launch_step_inst<D, NW, false, 2, true>(L, io, pl, sl2, r, s);
+        else if (pl.select_in_step) launch_step_inst<D, NW, false, 2>(L, io, pl, sl2, r, s);
+        else if (list && L.nt) launch_step_inst<D, NW, false, 1, true>(L, io, pl, sl2, r, s);
         else if (list) launch_step_inst<D, NW, false, 1>(L, io, pl, sl2, r, s);
         else if (L.nt) launch_step_inst<D, NW, false, 0, true>(L, io, pl, sl2, r, s);
         else launch_step_inst<D, NW, false, 0>(L, io, pl, sl2, r, s);
@@ -1979,6 +1990,10 @@ hipError_t allow_lds_all(int bytes) {
     set((const void*)k_step_bf16<D, NW, true, 1>);
     set((const void*)k_step_bf16<D, NW, false, 2>);
     set((const void*)k_step_bf16<D, NW, false, 0, true>);
+    set((const void*)k_step_bf16<D, NW, false, 2, true>);
+    set((const void*)k_step_bf16<D, NW, true, 0, true>);
+    set((const void*)k_step_bf16<D, NW, false, 1, true>);
+    set((const void*)k_step_bf16<D, NW, true, 1, true>);
     return e;
 }
 

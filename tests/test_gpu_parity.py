@@ -439,6 +439,25 @@ def test_stress_sweep(name, steps):
     assert rep.evictions > 0
 
 
+@pytest.mark.parametrize("name,kw,steps", [
+    ("llama8b-b128-ps32-L2048", dict(aggregation=1), 300),
+    ("llama8b-b128-ps32-L512", dict(prompt_tokens=4096, prompt_topk=8, splits=2), 640),
+    ("llama8b-b128-ps32-L512", dict(prompt_tokens=4096, prompt_topk=8, aggregation=1), 640),
+], ids=["softmax-sum", "selection-kernel", "selection-kernel-softmax-sum"])
+def test_stress_variants(name, kw, steps):
+    """Variants on the batch-128 stress pools (1 GB and more, beyond the
+    memory-side cache, so read with non-temporal loads): the softmax
+    aggregation on the fused workgroup, and Quest on the prompt through the
+    selection kernel and the list-driven step (a split plan, and the
+    softmax aggregation); 4 sampled units, past the budget."""
+    w = synth.get_workload(name)
+    _say("case %s %s steps %d" % (name, kw, steps))
+    rep = run_parity(w, seed=0, steps=steps, units=_sample_units(w, 4), out_every=16, chunk=128,
+                     others="ring", inv_every=8, **kw)
+    _report(rep, "%s %s" % (name, kw))
+    assert rep.evictions > 0
+
+
 def test_stress_dense_equivalence():
     """L = N (36864 tokens), the whole run of 32768 decode steps: the output
     is dense attention over every token (the oracle is exactly that at
