@@ -77,12 +77,6 @@ __device__ __forceinline__ size_t v_off(int t, int c) {
 __device__ __forceinline__ u32x4 ld4(const void* p) { return *reinterpret_cast<const u32x4*>(p); }
 __device__ __forceinline__ void st4(void* p, u32x4 x) { *reinterpret_cast<u32x4*>(p) = x; }
 
-__device__ __forceinline__ float wave_sum(float v) {
-#pragma unroll
-    for (int off = 32; off >= 1; off >>= 1) v += __shfl_xor(v, off);
-    return v;
-}
-
 __device__ __forceinline__ uint16_t u16_at(const u32x4& x, int e) {
     return (uint16_t)((x[e >> 1] >> ((e & 1) * 16)) & 0xFFFFu);
 }
@@ -305,6 +299,34 @@ __device__ __forceinline__ float max_xor16_32(float x) {
     const unsigned v = __builtin_bit_cast(unsigned, m);
     const auto b = __builtin_amdgcn_permlane32_swap(v, v, false, false);
     return fmaxf(__builtin_bit_cast(float, (unsigned)b[0]), __builtin_bit_cast(float, (unsigned)b[1]));
+}
+// Whole-wavefront max and sum of a float with no LDS round trip: lane ^ 1
+// and lane ^ 2 by quad permutes, then the mirrors within 8 and within 16
+// lanes (every lane of a quad, then of an 8-lane half, holds the same value
+// by then), then the two permlane swaps. Every lane ends with the result,
+// the sum in the same order on every lane.
+template <int CTRL>
+__device__ __forceinline__ float dpp_f32(float x) {
+    return __builtin_bit_cast(float, __builtin_amdgcn_update_dpp(0, __builtin_bit_cast(int, x), CTRL, 0xF, 0xF, false));
+}
+__device__ __forceinline__ float wave_max_dpp(float x) {
+    x = fmaxf(x, dpp_f32<0xB1>(x));
+    x = fmaxf(x, dpp_f32<0x4E>(x));
+    x = fmaxf(x, dpp_f32<0x141>(x));
+    x = fmaxf(x, dpp_f32<0x140>(x));
+    return max_xor16_32(x);
+}
+__device__ __forceinline__ float wave_sum_dpp(float x) {
+    x += dpp_f32<0xB1>(x);
+    x += dpp_f32<0x4E>(x);
+    x += dpp_f32<0x141>(x);
+    x += dpp_f32<0x140>(x);
+    const unsigned u = __builtin_bit_cast(unsigned, x);
+    const auto a = __builtin_amdgcn_permlane16_swap(u, u, false, false);
+    x = __builtin_bit_cast(float, (unsigned)a[0]) + __builtin_bit_cast(float, (unsigned)a[1]);
+    const unsigned v = __builtin_bit_cast(unsigned, x);
+    const auto b = __builtin_amdgcn_permlane32_swap(v, v, false, false);
+    return __builtin_bit_cast(float, (unsigned)b[0]) + __builtin_bit_cast(float, (unsigned)b[1]);
 }
 
 // LDS slot of element i = head * D + channel of the fp32 query array: a
@@ -1448,7 +1470,8 @@ __global__ __launch_bounds__(NW * 64) __attribute__((amdgpu_waves_per_eu(2, 2)))
 // [S][G] per-head bounds with the softmax aggregation.
 template <int D, int GM>
 __device__ __forceinline__ void f32_split(const LayerView& L, const StepIO& io, float scale_log2, int u, int split,
-                                          const float* s_q, float (*s_p)[64], float* partial, double* score) {
+                                          const float* s_q, const float* s_kn, const float* s_vn, float (*s_p)[64],
+                                          float* partial, double* score) {
     constexpr int DPL = D / 64;  // channels per lane in the value pass
     constexpr int CPP = D / 8;   // channels per lane in the page scores
     constexpr int VG = GM * DPL >= 32 ? 8 : 16;  // tokens whose value rows load together
@@ -1459,9 +1482,12 @@ __device__ __forceinline__ void f32_split(const LayerView& L, const StepIO& io, 
     const int t1 = max(t0, min(min(S * ps, 32 * L.nblk), t0 + L.bps * 32));
     const float* Ku = (const float*)L.K + (size_t)u * L.Lcap * D;
     const float* Vu = (const float*)L.V + (size_t)u * L.Lcap * D;
-    const float* kn_g = (const float*)io.k_new + (size_t)u * D;
-    const float* vn_g = (const float*)io.v_new + (size_t)u * D;
     const int32_t* fu = L.fill_att + base;  // fills the attention sees
+    // the small reads first (loads complete in issue order): the unit record
+    // and the first chunk's fills, then the key and value rows
+    const int32_t* U4 = L.unit + (size_t)u * kUnitFields;
+    const int ns = U4[kNextSlot], nf = U4[kNextFill];
+    int f_pre = fu[min(t0 + lane, max(t1 - 1, 0)) / ps];
 
     // this lane's key row; the first chunk's now (rows below t1 lie inside
     // the unit's pool)
@@ -1490,7 +1516,7 @@ __device__ __forceinline__ void f32_split(const LayerView& L, const StepIO& io, 
         }
     };
     load_vals(t0);
-    const float vn_lane = VPRE ? vn_g[lane] : 0.0f;
+    const float vn_lane = VPRE ? s_vn[lane] : 0.0f;
     // page state and representative keys of a score pass (pages pb .. pb+7,
     // clamped into the split's pages), loaded one pass ahead
     const int sl0 = min(S, (t0 + ps - 1) / ps), sl1 = min(S, (t1 + ps - 1) / ps);
@@ -1507,8 +1533,6 @@ __device__ __forceinline__ void f32_split(const LayerView& L, const StepIO& io, 
         }
     };
     if (sl0 < sl1) score_load(sl0);
-    const int32_t* U4 = L.unit + (size_t)u * kUnitFields;
-    const int ns = U4[kNextSlot], nf = U4[kNextFill];
     const bool opened = nf == 0;
     const int row_new = ns * ps + nf;
 
@@ -1522,25 +1546,28 @@ __device__ __forceinline__ void f32_split(const LayerView& L, const StepIO& io, 
     }
     for (int c0 = t0; c0 < t1; c0 += 64) {
         const int t = c0 + lane;
-        if (c0 > t0) {  // later chunks' key (and value) rows
+        if (c0 > t0) {  // later chunks' fills, key (and value) rows
+            f_pre = fu[min(t, t1 - 1) / ps];
             load_key(Ku + (size_t)min(t, t1 - 1) * D);
             load_vals(c0);
         }
         bool valid = false;
         if (t < t1) {
             const int slot = t / ps;
-            const int f = (slot == ns) ? nf + 1 : fu[slot];
+            const int f = (slot == ns) ? nf + 1 : f_pre;
             valid = t - slot * ps < f;
         }
         const unsigned long long vmask = __ballot(valid);
         if (vmask == 0) continue;
-        if (t == row_new) load_key(kn_g);
+        if (t == row_new) load_key(s_kn);
+        // the heads' sums side by side (each in channel order)
         float sc[GM];
 #pragma unroll
-        for (int j = 0; j < GM; ++j) {
-            sc[j] = 0.0f;
+        for (int j = 0; j < GM; ++j) sc[j] = 0.0f;
 #pragma unroll
-            for (int c = 0; c < D; c += 4) {
+        for (int c = 0; c < D; c += 4) {
+#pragma unroll
+            for (int j = 0; j < GM; ++j) {
                 const float4 q4 = *reinterpret_cast<const float4*>(s_q + j * D + c);
                 sc[j] = fmaf(q4.x, kr[c], sc[j]);
                 sc[j] = fmaf(q4.y, kr[c + 1], sc[j]);
@@ -1552,13 +1579,11 @@ __device__ __forceinline__ void f32_split(const LayerView& L, const StepIO& io, 
 #pragma unroll
         for (int j = 0; j < GM; ++j) {
             const float x = valid ? sc[j] * scale_log2 : -INFINITY;
-            float mx = x;
-#pragma unroll
-            for (int off = 32; off >= 1; off >>= 1) mx = fmaxf(mx, __shfl_xor(mx, off));
+            const float mx = wave_max_dpp(x);
             const float m_new = fmaxf(m[j], mx);  // finite: some lane holds a token
             const float alpha = __builtin_amdgcn_exp2f(m[j] - m_new);
             const float p = valid ? __builtin_amdgcn_exp2f(x - m_new) : 0.0f;
-            l[j] = l[j] * alpha + wave_sum(p);
+            l[j] = l[j] * alpha + wave_sum_dpp(p);
 #pragma unroll
             for (int i = 0; i < DPL; ++i) acc[j][i] *= alpha;
             s_p[j][lane] = p;
@@ -1581,9 +1606,12 @@ __device__ __forceinline__ void f32_split(const LayerView& L, const StepIO& io, 
             for (int e = 0; e < VG; ++e) {
                 const int tt = c0 + g0 + e;
                 const uint32_t keep = 0u - (uint32_t)((vmask >> (g0 + e)) & 1ull);  // all ones or zero
-                const float* vp = (tt == row_new) ? vn_g : Vu + (size_t)min(tt, t1 - 1) * D;
+                const float* vp = Vu + (size_t)min(tt, t1 - 1) * D;
 #pragma unroll
-                for (int i = 0; i < DPL; ++i) vr[e][i] = __uint_as_float(__float_as_uint(vp[lane + 64 * i]) & keep);
+                for (int i = 0; i < DPL; ++i) {
+                    const float x = tt == row_new ? s_vn[lane + 64 * i] : vp[lane + 64 * i];
+                    vr[e][i] = __uint_as_float(__float_as_uint(x) & keep);
+                }
             }
 #pragma unroll
             for (int e = 0; e < VG; ++e)
@@ -1612,8 +1640,8 @@ __device__ __forceinline__ void f32_split(const LayerView& L, const StepIO& io, 
         float* Kw = (float*)L.K + ((size_t)u * L.Lcap + row_new) * D;
         float* Vw = (float*)L.V + ((size_t)u * L.Lcap + row_new) * D;
         for (int c = lane; c < D; c += 64) {
-            Kw[c] = kn_g[c];
-            Vw[c] = vn_g[c];
+            Kw[c] = s_kn[c];
+            Vw[c] = s_vn[c];
         }
     }
     // page scores: pages whose first row lies in this split, eight at a time
@@ -1636,7 +1664,7 @@ __device__ __forceinline__ void f32_split(const LayerView& L, const StepIO& io, 
         if (act && tail) {
 #pragma unroll
             for (int c = 0; c < CPP; ++c) {
-                const float x = kn_g[cb + c];
+                const float x = s_kn[cb + c];
                 hi[c] = opened ? x : fmaxf(hi[c], x);
                 lo[c] = opened ? x : fminf(lo[c], x);
                 kx[c] = hi[c];
@@ -1668,6 +1696,7 @@ __device__ __forceinline__ void f32_split(const LayerView& L, const StepIO& io, 
 template <int D, int GM>
 __global__ __launch_bounds__(64) void k_step_f32(LayerView L, StepIO io, float scale_log2) {
     __shared__ __align__(16) float s_q[GM * D];
+    __shared__ __align__(16) float s_kn[D], s_vn[D];  // the new token's key and value
     __shared__ float s_p[GM][64];  // the chunk's weights, per head and token
     const int nsplit = L.nsplit;
     const int u = blockIdx.x / nsplit, split = blockIdx.x - (blockIdx.x / nsplit) * nsplit;
@@ -1675,9 +1704,13 @@ __global__ __launch_bounds__(64) void k_step_f32(LayerView L, StepIO io, float s
     const int G = L.G;
     const float* qg = (const float*)io.q + (size_t)u * G * D;
     for (int i = threadIdx.x; i < GM * D; i += 64) s_q[i] = i < G * D ? qg[i] : 0.0f;  // heads past G: zero
+    for (int i = threadIdx.x; i < D; i += 64) {
+        s_kn[i] = ((const float*)io.k_new)[(size_t)u * D + i];
+        s_vn[i] = ((const float*)io.v_new)[(size_t)u * D + i];
+    }
     __syncthreads();
-    f32_split<D, GM>(L, io, scale_log2, u, split, s_q, s_p, L.part + ((size_t)u * nsplit + split) * G * (D + 2),
-                     L.score + (size_t)u * L.S * (L.agg ? G : 1));
+    f32_split<D, GM>(L, io, scale_log2, u, split, s_q, s_kn, s_vn, s_p,
+                     L.part + ((size_t)u * nsplit + split) * G * (D + 2), L.score + (size_t)u * L.S * (L.agg ? G : 1));
 }
 
 // head slots of the fp32 step kernel instance for a group of G heads
@@ -1686,7 +1719,7 @@ constexpr int f32_head_slots(int G) { return G <= 4 ? 4 : G <= 8 ? 8 : 16; }
 // LDS of the fused fp32 step kernel with nw wavefronts: the queries, each
 // wavefront's weights and partial, the slot arrays (score, state, ts, lid)
 size_t f32_fused_lds(int GM, int G, int D, int S, int nw) {
-    return (size_t)GM * D * 4 + (size_t)nw * GM * 64 * 4 + (size_t)nw * G * (D + 2) * 4 + (size_t)S * 20;
+    return (size_t)(GM + 2) * D * 4 + (size_t)nw * GM * 64 * 4 + (size_t)nw * G * (D + 2) * 4 + (size_t)S * 20;
 }
 
 // Step kernel, fp32 pools of head_dim 64, one workgroup per unit (L.nsplit
@@ -1704,8 +1737,10 @@ __global__ __launch_bounds__(512) void k_step_f32_fused(LayerView L, StepIO io, 
     if (io.active != nullptr && io.active[u / L.nkv] == 0) return;
     const int G = L.G, S = L.S;
     float* s_q = reinterpret_cast<float*>(smem);                       // [GM][D]
-    float (*s_p)[64] = reinterpret_cast<float (*)[64]>(s_q + GM * D);  // [nw][GM][64]
-    float* s_part = s_q + GM * D + (size_t)nw * GM * 64;               // [nw][G][D+2]
+    float* s_kn = s_q + GM * D;                                        // [D] the new token's key
+    float* s_vn = s_kn + D;                                            // [D] and value
+    float (*s_p)[64] = reinterpret_cast<float (*)[64]>(s_vn + D);      // [nw][GM][64]
+    float* s_part = s_vn + D + (size_t)nw * GM * 64;                   // [nw][G][D+2]
     double* s_score = reinterpret_cast<double*>(s_part + (size_t)nw * G * (D + 2));  // [S] (8-byte aligned)
     int* s_state = reinterpret_cast<int*>(s_score + S);
     int* s_ts = s_state + S;
@@ -1714,8 +1749,13 @@ __global__ __launch_bounds__(512) void k_step_f32_fused(LayerView L, StepIO io, 
     load_slots(L, u, ur, s_score, s_state, s_ts, s_lid);  // every score +inf until its page is scored
     const float* qg = (const float*)io.q + (size_t)u * G * D;
     for (int i = tid; i < GM * D; i += nth) s_q[i] = i < G * D ? qg[i] : 0.0f;  // heads past G: zero
+    for (int i = tid; i < D; i += nth) {
+        s_kn[i] = ((const float*)io.k_new)[(size_t)u * D + i];
+        s_vn[i] = ((const float*)io.v_new)[(size_t)u * D + i];
+    }
     __syncthreads();
-    f32_split<D, GM>(L, io, scale_log2, u, w, s_q, s_p + (size_t)w * GM, s_part + (size_t)w * G * (D + 2), s_score);
+    f32_split<D, GM>(L, io, scale_log2, u, w, s_q, s_kn, s_vn, s_p + (size_t)w * GM, s_part + (size_t)w * G * (D + 2),
+                     s_score);
     __syncthreads();
     refresh_block(L, ur, r, s_score, s_state, s_ts, s_aux, tid, nth);
     __syncthreads();
