@@ -435,6 +435,14 @@ __device__ __forceinline__ int float_order(float x) {
 }
 __device__ __forceinline__ float order_float(int i) { return __builtin_bit_cast(float, i >= 0 ? i : i ^ 0x7FFFFFFF); }
 
+// Order-preserving unsigned key of a float (unsigned order = numeric order,
+// -0 just below +0), and back.
+__device__ __forceinline__ unsigned ukey_f32(float x) {
+    const unsigned b = __float_as_uint(x);
+    return (b >> 31) ? ~b : (b | 0x80000000u);
+}
+__device__ __forceinline__ float from_ukey_f32(unsigned k) { return __uint_as_float((k >> 31) ? (k & 0x7FFFFFFFu) : ~k); }
+
 // Per bf16 half: the magnitude, at least the smallest normal (2^-126).
 __device__ __forceinline__ uint32_t mag_floor(uint32_t x) {
     uint32_t lo = x & 0x7FFFu, hi = (x >> 16) & 0x7FFFu;
@@ -868,6 +876,62 @@ __device__ __forceinline__ void lds_barrier() {
     __atomic_signal_fence(__ATOMIC_SEQ_CST);
 }
 
+// The k-th largest of x[0 .. n-1] (1 <= k <= n, counted with multiplicity),
+// by a whole workgroup of NT threads (every thread calls it and gets the
+// value): a radix select over ukey_f32, four 8-bit digits from the most
+// significant, a 256-bin histogram of the keys that match the digits found
+// so far in each pass; wavefront 0 scans the bins from the top for the one
+// holding the k-th key. hist: 258 ints of LDS.
+template <int NT>
+__device__ float kth_largest_wg(const float* x, int n, int k, int* hist, int tid) {
+    const int lane = tid & 63;
+    unsigned prefix = 0;
+    int want = k;  // rank from the top among the keys that match prefix, 1-based
+    for (int shift = 24; shift >= 0; shift -= 8) {
+        for (int b = tid; b < 256; b += NT) hist[b] = 0;
+        lds_barrier();
+        const unsigned high = shift == 24 ? 0u : ~0u << (shift + 8);
+        for (int p = tid; p < n; p += NT) {
+            const unsigned key = ukey_f32(x[p]);
+            if ((key & high) == prefix) atomicAdd(&hist[(key >> shift) & 255u], 1);
+        }
+        lds_barrier();
+        if (tid < 64) {  // lane l holds bins 255-4l .. 252-4l
+            const int c0 = hist[255 - 4 * lane], c1 = hist[254 - 4 * lane], c2 = hist[253 - 4 * lane],
+                      c3 = hist[252 - 4 * lane];
+            const int sum = c0 + c1 + c2 + c3;
+            int incl = sum;
+#pragma unroll
+            for (int off = 1; off < 64; off <<= 1) {
+                const int v = __shfl_up(incl, off);
+                if (lane >= off) incl += v;
+            }
+            const int excl = incl - sum;
+            if (excl < want && want <= incl) {
+                int r = want - excl, b = 255 - 4 * lane;
+                if (r > c0) {
+                    r -= c0;
+                    --b;
+                    if (r > c1) {
+                        r -= c1;
+                        --b;
+                        if (r > c2) {
+                            r -= c2;
+                            --b;
+                        }
+                    }
+                }
+                hist[256] = b;
+                hist[257] = r;
+            }
+        }
+        lds_barrier();
+        prefix |= (unsigned)hist[256] << shift;
+        want = hist[257];
+    }
+    return from_ukey_f32(prefix);
+}
+
 // One 32-token block of attention for the GQA group held by this wavefront:
 // QK^T as two 16x16x32 bf16 MFMA tiles per 32 channels (rows = tokens,
 // columns = query heads), online softmax in base 2 with one cross-lane max,
@@ -1203,21 +1267,28 @@ __device__ __forceinline__ void step_item(LayerView L, StepIO io, float scale_lo
         // candidates with upper end >= lo, and rank among them as among all
         // kept pages.
         if (pinned > L.topk && L.topk > 0) {
-            const int pin4 = pinned & ~3;
-            for (int p = tid; p < pinned; p += NW * 64) {
-                // lower ends above p's: four per 16-byte read, then the last few
-                const float lp = s_plo[p];
-                int above = 0;
+            float lo_cut;
+            if (pinned > 2 * NW * 64) {
+                // many kept pages: lo by a radix select (the count below is
+                // quadratic in them); s_ex is free until the candidates' bounds
+                lo_cut = kth_largest_wg<NW * 64>(s_plo, pinned, L.topk, reinterpret_cast<int*>(s_ex), tid);
+            } else {
+                const int pin4 = pinned & ~3;
+                for (int p = tid; p < pinned; p += NW * 64) {
+                    // lower ends above p's: four per 16-byte read, then the last few
+                    const float lp = s_plo[p];
+                    int above = 0;
 #pragma unroll 4
-                for (int o = 0; o < pin4; o += 4) {
-                    const float4 x = *reinterpret_cast<const float4*>(s_plo + o);
-                    above += (x.x > lp ? 1 : 0) + (x.y > lp ? 1 : 0) + (x.z > lp ? 1 : 0) + (x.w > lp ? 1 : 0);
+                    for (int o = 0; o < pin4; o += 4) {
+                        const float4 x = *reinterpret_cast<const float4*>(s_plo + o);
+                        above += (x.x > lp ? 1 : 0) + (x.y > lp ? 1 : 0) + (x.z > lp ? 1 : 0) + (x.w > lp ? 1 : 0);
+                    }
+                    for (int o = pin4; o < pinned; ++o) above += s_plo[o] > lp ? 1 : 0;
+                    if (above < L.topk) atomicMin(&s_lo, float_order(lp));
                 }
-                for (int o = pin4; o < pinned; ++o) above += s_plo[o] > lp ? 1 : 0;
-                if (above < L.topk) atomicMin(&s_lo, float_order(lp));
+                lds_barrier();
+                lo_cut = order_float(s_lo);
             }
-            lds_barrier();
-            const float lo_cut = order_float(s_lo);
             for (int p = tid; p < pinned; p += NW * 64) {
                 if (s_phi[p] >= lo_cut) s_cand[atomicAdd(&s_ncand, 1)] = p;
                 else s_fatt[p] = 0;

@@ -787,6 +787,67 @@ def test_prompt_selection_ties(splits):
     assert chosen_without_6 > 0  # the tie decided the top 3 in some steps
 
 
+def test_prompt_selection_ties_large_region():
+    """The tie case where the in-step selection finds its cut by a radix
+    select: 512 units (workgroups of 4 wavefronts, 256 threads) with a
+    4608-token prompt region at page 8, 576 kept pages, more than twice the
+    threads. In every unit prompt pages 1, 4 and 6 copy page 2's keys,
+    scaled so that the four lead the bounds: with top 3 the cut is the bound
+    the four share, and the tie rule alone keeps slot 6 out. Keys are drawn
+    on the GPU; four sampled units against the oracle at every step."""
+    import torch
+
+    B, Hkv, Hq, d, ps, P, topk, budget, steps = 64, 8, 32, 128, 8, 4608, 3, 256, 40
+    w = synth.get_workload("llama8b-b128-ps32-L512").replace(
+        name="prompt-ties-large-region", batch=B, page_size=ps, budget=budget, prefill_len=P)
+    G, U, npr = Hq // Hkv, B * Hkv, P // ps
+    S = budget // ps + npr
+    gen = torch.Generator(device="cuda")
+    gen.manual_seed(37)
+    K = torch.randn((B, Hkv, P, d), generator=gen, device="cuda")
+    V = torch.randn((B, Hkv, P, d), generator=gen, device="cuda")
+    K[:, :, 2 * ps:3 * ps] *= 3.0
+    for pg in (1, 4, 6):
+        K[:, :, pg * ps:(pg + 1) * ps] = K[:, :, 2 * ps:3 * ps]
+    Kb, Vb = K.to(torch.bfloat16).contiguous(), V.to(torch.bfloat16).contiguous()
+    del K, V
+    units = _sample_units(w, 4)
+    _say("case prompt-selection ties, large region: units %s" % units)
+    pool = new_pool(w, None, prompt_tokens=P, prompt_topk=topk)
+    pool.prefill(0, Kb, Vb)
+    orc = {}
+    for u in units:
+        b, h = divmod(u, Hkv)
+        m = oracle.Kvm(G, d, ps, S, r=w.r, prompt_slots=npr, prompt_topk=topk)
+        assert m.prefill(Kb[b, h].float().cpu().numpy().astype(np.float64),
+                         Vb[b, h].float().cpu().numpy().astype(np.float64)) == 0
+        orc[u] = m
+    del Kb, Vb
+    out = torch.empty((B, Hq, d), dtype=torch.bfloat16, device="cuda")
+    chosen_without_6 = 0
+    rep = ParityReport(units_checked=len(units))
+    for t in range(steps):
+        qb = torch.randn((B, Hq, d), generator=gen, device="cuda").to(torch.bfloat16)
+        kb = torch.randn((B, Hkv, d), generator=gen, device="cuda").to(torch.bfloat16)
+        vb = torch.randn((B, Hkv, d), generator=gen, device="cuda").to(torch.bfloat16)
+        pool.decode_step(0, qb, kb, vb, out)
+        torch.cuda.synchronize()
+        got = out.float().cpu().numpy().reshape(U, G, d)
+        q64 = qb.float().cpu().numpy().astype(np.float64).reshape(U, G, d)
+        k64 = kb.float().cpu().numpy().astype(np.float64).reshape(U, d)
+        v64 = vb.float().cpu().numpy().astype(np.float64).reshape(U, d)
+        for u in units:
+            want = orc[u].decode(q64[u], k64[u], v64[u])
+            att = orc[u].last_attended()[:npr]
+            if att[1] and att[2] and att[4] and not att[6]:
+                chosen_without_6 += 1
+            compare_outputs(got[u][None], want[None], "bf16", "unit %d step %d" % (u, t), rep)
+        rep.steps = t + 1
+    pool.close()
+    record(rep, "prompt-selection ties, large region")
+    assert chosen_without_6 == len(units) * steps  # the four lead at every step; the tie decides
+
+
 @pytest.mark.parametrize("splits", [None, 2], ids=["in-step", "selection-kernel"])
 def test_prompt_selection_extreme_keys(splits):
     """Prompt pages whose bounds stress the in-step selection's intervals:
