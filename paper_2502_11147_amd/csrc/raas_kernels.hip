@@ -443,6 +443,40 @@ __device__ __forceinline__ unsigned ukey_f32(float x) {
 }
 __device__ __forceinline__ float from_ukey_f32(unsigned k) { return __uint_as_float((k >> 31) ? (k & 0x7FFFFFFFu) : ~k); }
 
+// Wavefront 0's part of a pass of a radix select from the top: hist[0 .. 255]
+// holds the counts of one digit among the keys still in play; finds the bin
+// holding the want-th largest of them (1-based) and the rank within that bin,
+// into hist[256] and hist[257]. Lane l scans bins 255-4l .. 252-4l.
+__device__ __forceinline__ void radix_pick_top(int* hist, int want, int lane) {
+    const int c0 = hist[255 - 4 * lane], c1 = hist[254 - 4 * lane], c2 = hist[253 - 4 * lane],
+              c3 = hist[252 - 4 * lane];
+    const int sum = c0 + c1 + c2 + c3;
+    int incl = sum;
+#pragma unroll
+    for (int off = 1; off < 64; off <<= 1) {
+        const int v = __shfl_up(incl, off);
+        if (lane >= off) incl += v;
+    }
+    const int excl = incl - sum;
+    if (excl < want && want <= incl) {
+        int r = want - excl, b = 255 - 4 * lane;
+        if (r > c0) {
+            r -= c0;
+            --b;
+            if (r > c1) {
+                r -= c1;
+                --b;
+                if (r > c2) {
+                    r -= c2;
+                    --b;
+                }
+            }
+        }
+        hist[256] = b;
+        hist[257] = r;
+    }
+}
+
 // Per bf16 half: the magnitude, at least the smallest normal (2^-126).
 __device__ __forceinline__ uint32_t mag_floor(uint32_t x) {
     uint32_t lo = x & 0x7FFFu, hi = (x >> 16) & 0x7FFFu;
@@ -734,6 +768,29 @@ __device__ __forceinline__ double from_order_key(unsigned long long k) {
     return __longlong_as_double((long long)((k >> 63) ? (k & ~(1ull << 63)) : ~k));
 }
 
+// kth_largest_wg for doubles: eight 8-bit digits of order_key (-0 counted as
+// +0, which it equals), by a workgroup of nth threads. hist: 258 ints.
+__device__ double kth_largest_f64_wg(const double* x, int n, int k, int* hist, int tid, int nth) {
+    const int lane = tid & 63;
+    unsigned long long prefix = 0;
+    int want = k;
+    for (int shift = 56; shift >= 0; shift -= 8) {
+        for (int b = tid; b < 256; b += nth) hist[b] = 0;
+        __syncthreads();
+        const unsigned long long high = shift == 56 ? 0ull : ~0ull << (shift + 8);
+        for (int p = tid; p < n; p += nth) {
+            const unsigned long long key = order_key(x[p] + 0.0);
+            if ((key & high) == prefix) atomicAdd(&hist[(int)((key >> shift) & 255ull)], 1);
+        }
+        __syncthreads();
+        if (tid < 64) radix_pick_top(hist, want, lane);
+        __syncthreads();
+        prefix |= (unsigned long long)hist[256] << shift;
+        want = hist[257];
+    }
+    return from_order_key(prefix);
+}
+
 // Top-r refresh by a whole workgroup (every thread calls it; the epilogue
 // kernel's version of the rule in retention_wave). With n ranked pages and
 // k = floor(r*n), an evictable page is refreshed when at least n-k ranked
@@ -896,35 +953,7 @@ __device__ float kth_largest_wg(const float* x, int n, int k, int* hist, int tid
             if ((key & high) == prefix) atomicAdd(&hist[(key >> shift) & 255u], 1);
         }
         lds_barrier();
-        if (tid < 64) {  // lane l holds bins 255-4l .. 252-4l
-            const int c0 = hist[255 - 4 * lane], c1 = hist[254 - 4 * lane], c2 = hist[253 - 4 * lane],
-                      c3 = hist[252 - 4 * lane];
-            const int sum = c0 + c1 + c2 + c3;
-            int incl = sum;
-#pragma unroll
-            for (int off = 1; off < 64; off <<= 1) {
-                const int v = __shfl_up(incl, off);
-                if (lane >= off) incl += v;
-            }
-            const int excl = incl - sum;
-            if (excl < want && want <= incl) {
-                int r = want - excl, b = 255 - 4 * lane;
-                if (r > c0) {
-                    r -= c0;
-                    --b;
-                    if (r > c1) {
-                        r -= c1;
-                        --b;
-                        if (r > c2) {
-                            r -= c2;
-                            --b;
-                        }
-                    }
-                }
-                hist[256] = b;
-                hist[257] = r;
-            }
-        }
+        if (tid < 64) radix_pick_top(hist, want, lane);
         lds_barrier();
         prefix |= (unsigned)hist[256] << shift;
         want = hist[257];
@@ -1883,6 +1912,7 @@ __global__ __launch_bounds__(256) void k_prompt_select(LayerView L, StepIO io) {
     double2* s_qpm = reinterpret_cast<double2*>(smem);                 // [G][D] (q+, q-)
     double* s_b = reinterpret_cast<double*>(s_qpm + (size_t)G * D);    // [npr] bounds
     int* s_sel = reinterpret_cast<int*>(s_b + npr);                    // [npr] chosen
+    int* s_hist = s_sel + npr;  // [264] radix histogram, its pick, the count above theta, per-wavefront counts
     const int kp = L.unit[(size_t)u * kUnitFields + kPinnedPages];
     const T* qg = (const T*)io.q + (size_t)u * G * D;
     for (int i = tid; i < G * D; i += nth) {
@@ -1916,17 +1946,55 @@ __global__ __launch_bounds__(256) void k_prompt_select(LayerView L, StepIO io) {
         s_b[p] = best;
     }
     __syncthreads();
-    for (int p = tid; p < npr; p += nth) {
-        bool sel = p < kp;
-        if (sel && !all) {
-            const double bp = s_b[p];
-            int above = 0;
-            for (int o = 0; o < kp; ++o) above += (s_b[o] > bp || (s_b[o] == bp && o < p)) ? 1 : 0;
-            sel = above < L.topk;
+    // the topk pages of largest bound, ties to the lower slot. Up to one page
+    // per thread, each page is ranked against all others; beyond (the count
+    // is quadratic in the pages), theta, the topk-th largest bound (counted
+    // with multiplicity), by a radix select, then every page above it and,
+    // of those equal to it, the lowest slots, as many as are left (a prefix
+    // count in slot order): the same pages.
+    if (all || kp <= nth) {
+        for (int p = tid; p < npr; p += nth) {
+            bool sel = p < kp;
+            if (sel && !all) {
+                const double bp = s_b[p];
+                int above = 0;
+                for (int o = 0; o < kp; ++o) above += (s_b[o] > bp || (s_b[o] == bp && o < p)) ? 1 : 0;
+                sel = above < L.topk;
+            }
+            s_sel[p] = sel ? 1 : 0;
         }
-        s_sel[p] = sel ? 1 : 0;
-        L.fill_att[base + p] = sel ? L.fill[base + p] : 0;
+    } else {
+        const double theta = kth_largest_f64_wg(s_b, kp, L.topk, s_hist, tid, nth);
+        if (tid == 0) s_hist[258] = 0;
+        __syncthreads();
+        int gt = 0;
+        for (int p = tid; p < kp; p += nth) gt += s_b[p] > theta ? 1 : 0;
+#pragma unroll
+        for (int off = 32; off >= 1; off >>= 1) gt += __shfl_xor(gt, off);
+        if (lane == 0 && gt) atomicAdd(&s_hist[258], gt);
+        __syncthreads();
+        const int need = L.topk - s_hist[258], w = tid >> 6, nw = nth >> 6;
+        int run = 0;  // tied pages in the slots before this chunk
+        for (int c0 = 0; c0 < kp; c0 += nth) {
+            const int p = c0 + tid;
+            const bool eq = p < kp && s_b[p] == theta;
+            const unsigned long long m = __ballot(eq);
+            if (lane == 0) s_hist[259 + w] = __popcll(m);
+            __syncthreads();
+            int before = run + __popcll(m & ((1ull << lane) - 1ull)), tot = 0;
+            for (int ww = 0; ww < nw; ++ww) {
+                const int cw = s_hist[259 + ww];
+                tot += cw;
+                before += ww < w ? cw : 0;
+            }
+            if (p < kp) s_sel[p] = (s_b[p] > theta || (eq && before < need)) ? 1 : 0;
+            run += tot;
+            __syncthreads();
+        }
+        for (int p = kp + tid; p < npr; p += nth) s_sel[p] = 0;
     }
+    __syncthreads();
+    for (int p = tid; p < npr; p += nth) L.fill_att[base + p] = s_sel[p] ? L.fill[base + p] : 0;
     for (int s = npr + tid; s < S; s += nth) L.fill_att[base + s] = L.fill[base + s];
     __syncthreads();
     if (tid < 64) {
@@ -2217,8 +2285,9 @@ void launch_select_t(const LayerView& L, const StepIO& io, size_t shm, hipStream
 }
 
 hipError_t launch_prompt_select(const LayerView& L, const StepIO& io, hipStream_t stream) {
-    // q split in two (16 B per element), the bounds and the chosen flags
-    const size_t shm = (size_t)L.G * L.D * 16 + (size_t)L.dbase * 12;
+    // q split in two (16 B per element), the bounds and the chosen flags, the
+    // radix histogram and its counts
+    const size_t shm = (size_t)L.G * L.D * 16 + (size_t)L.dbase * 12 + 264 * 4;
     if (L.bf16)
         launch_select_t<uint16_t>(L, io, shm, stream, std::make_integer_sequence<int, 16>{});
     else

@@ -787,14 +787,16 @@ def test_prompt_selection_ties(splits):
     assert chosen_without_6 > 0  # the tie decided the top 3 in some steps
 
 
-def test_prompt_selection_ties_large_region():
-    """The tie case where the in-step selection finds its cut by a radix
-    select: 512 units (workgroups of 4 wavefronts, 256 threads) with a
-    4608-token prompt region at page 8, 576 kept pages, more than twice the
-    threads. In every unit prompt pages 1, 4 and 6 copy page 2's keys,
-    scaled so that the four lead the bounds: with top 3 the cut is the bound
-    the four share, and the tie rule alone keeps slot 6 out. Keys are drawn
-    on the GPU; four sampled units against the oracle at every step."""
+@pytest.mark.parametrize("splits", [None, 2], ids=["in-step", "selection-kernel"])
+def test_prompt_selection_ties_large_region(splits):
+    """The tie case where the selection goes by a radix select: 512 units
+    with a 4608-token prompt region at page 8, 576 kept pages, more than
+    twice the in-step workgroup's threads (4 wavefronts) and more than the
+    selection kernel's 256. In every unit prompt pages 1, 4 and 6 copy page
+    2's keys, scaled so that the four lead the bounds: with top 3 the cut
+    (or theta) is the bound the four share, and the tie rule alone keeps
+    slot 6 out. Keys are drawn on the GPU; four sampled units against the
+    oracle at every step."""
     import torch
 
     B, Hkv, Hq, d, ps, P, topk, budget, steps = 64, 8, 32, 128, 8, 4608, 3, 256, 40
@@ -812,8 +814,8 @@ def test_prompt_selection_ties_large_region():
     Kb, Vb = K.to(torch.bfloat16).contiguous(), V.to(torch.bfloat16).contiguous()
     del K, V
     units = _sample_units(w, 4)
-    _say("case prompt-selection ties, large region: units %s" % units)
-    pool = new_pool(w, None, prompt_tokens=P, prompt_topk=topk)
+    _say("case prompt-selection ties, large region, splits %s: units %s" % (splits, units))
+    pool = new_pool(w, splits, prompt_tokens=P, prompt_topk=topk)
     pool.prefill(0, Kb, Vb)
     orc = {}
     for u in units:
@@ -908,18 +910,21 @@ def test_prompt_selection_extreme_keys(splits):
     assert chosen.min() < U * w.decode_steps and chosen.max() > 0  # a real choice among the pages
 
 
-@pytest.mark.parametrize("batch,prompt", [(128, 3072), (64, 4608)], ids=["1024-units", "512-units"])
-def test_prompt_selection_large_region(batch, prompt):
+@pytest.mark.parametrize("batch,prompt,splits", [(128, 3072, None), (64, 4608, None), (64, 4608, 2)],
+                         ids=["1024-units", "512-units", "512-units-selection-kernel"])
+def test_prompt_selection_large_region(batch, prompt, splits):
     """Prompt regions of more pages than twice a workgroup's threads (page 8:
     384 kept pages at batch 128, whose 1024 units run in workgroups of 2
     wavefronts, four per CU; 576 at batch 64, 512 units in workgroups of 4),
     and slots likewise (416 and 608): the in-step selection stages fills and
-    slot records past the two each thread reads with its first loads. The
-    decode budget (256 tokens) runs past full; sampled units."""
+    slot records past the two each thread reads with its first loads, and
+    finds its cut by a radix select. Split in two, the selection kernel
+    chooses the pages, by its radix select beyond 256 pages. The decode
+    budget (256 tokens) runs past full; sampled units."""
     w = synth.get_workload("llama8b-b128-ps32-L512").replace(
         name="prompt-region-%d" % prompt, batch=batch, page_size=8, budget=256, prefill_len=prompt)
     _say("case prompt-selection large region batch %d prompt %d" % (batch, prompt))
-    rep = run_parity(w, seed=0, steps=400, units=_sample_units(w, 4), out_every=16, chunk=128,
+    rep = run_parity(w, seed=0, steps=400, units=_sample_units(w, 4), out_every=16, chunk=128, splits=splits,
                      prompt_tokens=prompt, prompt_topk=12)
     _report(rep, "prompt-selection large region")
     assert rep.evictions > 0
