@@ -799,15 +799,17 @@ __device__ double kth_largest_f64_wg(const double* x, int n, int k, int* hist, i
 // a radix select over order_key (eight 8-bit digits, most significant
 // first, a 256-bin histogram each) and refreshes the evictable pages
 // scoring above theta: the same pages, since fewer than n-k ranked scores
-// lie below theta and at least n-k lie at or below it. s_aux: 260 ints.
+// lie below theta and at least n-k lie at or below it. Slots below first
+// hold no ranked page (the prompt region's, when there is one). s_aux: 260
+// ints.
 __device__ void refresh_block(const LayerView& L, const UnitRec& ur, double r, const double* s_score,
-                              const int* s_state, int* s_ts, int* s_aux, int tid, int nthreads) {
+                              const int* s_state, int* s_ts, int* s_aux, int tid, int nthreads, int first) {
     const int S = L.S, lane = tid & 63;
     int* s_hist = s_aux;  // [256]
     if (tid == 0) s_aux[256] = 0;
     __syncthreads();
     int cnt = 0;
-    for (int p = tid; p < S; p += nthreads) cnt += ranked(L, s_state[p]) ? 1 : 0;
+    for (int p = first + tid; p < S; p += nthreads) cnt += ranked(L, s_state[p]) ? 1 : 0;
 #pragma unroll
     for (int off = 32; off >= 1; off >>= 1) cnt += __shfl_xor(cnt, off);
     if (lane == 0 && cnt) atomicAdd(&s_aux[256], cnt);
@@ -816,17 +818,17 @@ __device__ void refresh_block(const LayerView& L, const UnitRec& ur, double r, c
     const int k = (int)floor(r * (double)n);
     if (k == 0) return;
     if (k == n) {  // every page refreshed
-        for (int p = tid; p < S; p += nthreads)
+        for (int p = first + tid; p < S; p += nthreads)
             if (s_state[p] == kEvictable) s_ts[p] = ur.clock;
         return;
     }
-    if (S <= 256) {
-        for (int p = tid; p < S; p += nthreads) {
+    if (S - first <= 256) {
+        for (int p = first + tid; p < S; p += nthreads) {
             if (s_state[p] != kEvictable) continue;
             const double sp = s_score[p];
             int less = 0;
 #pragma unroll 8
-            for (int o = 0; o < S; ++o) less += s_score[o] < sp;  // unranked slots hold +inf
+            for (int o = first; o < S; ++o) less += s_score[o] < sp;  // unranked slots hold +inf
             if (less >= n - k) s_ts[p] = ur.clock;
         }
         return;
@@ -837,7 +839,7 @@ __device__ void refresh_block(const LayerView& L, const UnitRec& ur, double r, c
         for (int b = tid; b < 256; b += nthreads) s_hist[b] = 0;
         __syncthreads();
         const unsigned long long high = shift == 56 ? 0ull : (~0ull << (shift + 8));
-        for (int p = tid; p < S; p += nthreads) {
+        for (int p = first + tid; p < S; p += nthreads) {
             if (!ranked(L, s_state[p])) continue;
             const unsigned long long key = order_key(s_score[p]);
             if ((key & high) == prefix) atomicAdd(&s_hist[(int)((key >> shift) & 255ull)], 1);
@@ -877,7 +879,7 @@ __device__ void refresh_block(const LayerView& L, const UnitRec& ur, double r, c
         want = s_aux[258];
     }
     const double theta = from_order_key(prefix);
-    for (int p = tid; p < S; p += nthreads)
+    for (int p = first + tid; p < S; p += nthreads)
         if (s_state[p] == kEvictable && s_score[p] > theta) s_ts[p] = ur.clock;
 }
 
@@ -1857,7 +1859,7 @@ __global__ __launch_bounds__(512) void k_step_f32_fused(LayerView L, StepIO io, 
     f32_split<D, GM>(L, io, scale_log2, u, w, s_q, s_kn, s_vn, s_p + (size_t)w * GM, s_part + (size_t)w * G * (D + 2),
                      s_score);
     __syncthreads();
-    refresh_block(L, ur, r, s_score, s_state, s_ts, s_aux, tid, nth);
+    refresh_block(L, ur, r, s_score, s_state, s_ts, s_aux, tid, nth, L.dbase);
     __syncthreads();
     if (tid < 64) evict_wave(L, ur, s_state, s_ts, s_lid, ret);
     for (int idx = tid; idx < G * D; idx += nth) {  // merge: out = sum_w 2^(M_w - M) O_w / sum_w 2^(M_w - M) L_w
@@ -2075,7 +2077,7 @@ __global__ __launch_bounds__(256) void k_epilogue(LayerView L, StepIO io, double
     }
     __syncthreads();
     if (L.agg) softmax_sum_block(L, L.score + base * G, nu, s_state, s_score, s_mz, tid, nth);
-    refresh_block(L, ur, r, s_score, s_state, s_ts, s_aux, tid, nth);
+    refresh_block(L, ur, r, s_score, s_state, s_ts, s_aux, tid, nth, L.dbase);
     __syncthreads();
     if (tid < 64) evict_wave(L, ur, s_state, s_ts, s_lid, ret);
     for (int uh = 0; merge && uh < nu; ++uh) {
