@@ -1891,7 +1891,7 @@ __global__ __launch_bounds__(512) void k_step_f32_fused(LayerView L, StepIO io, 
 // sequential sum does. Writes the fills the attention sees (0 for the other
 // prompt pages) and the unit's block list: the prompt blocks holding a
 // chosen page, ascending, then every block of the decode region. One
-// workgroup of 256 threads per unit.
+// workgroup per unit: 256 threads, 1024 when there are fewer units than CUs.
 template <typename T>
 __device__ __forceinline__ float vec_elem(const u32x4& x, int e);
 template <>
@@ -1903,7 +1903,7 @@ __device__ __forceinline__ float vec_elem<float>(const u32x4& x, int e) { return
 // unrolls into straight-line fused multiply-adds.
 
 template <typename T, int GQ>
-__global__ __launch_bounds__(256) void k_prompt_select(LayerView L, StepIO io) {
+__global__ __launch_bounds__(1024) void k_prompt_select(LayerView L, StepIO io) {
     extern __shared__ __align__(16) unsigned char smem[];
     const int u = blockIdx.x, tid = threadIdx.x, lane = tid & 63, nth = blockDim.x;
     if (io.active != nullptr && io.active[u / L.nkv] == 0) return;
@@ -1914,7 +1914,7 @@ __global__ __launch_bounds__(256) void k_prompt_select(LayerView L, StepIO io) {
     double2* s_qpm = reinterpret_cast<double2*>(smem);                 // [G][D] (q+, q-)
     double* s_b = reinterpret_cast<double*>(s_qpm + (size_t)G * D);    // [npr] bounds
     int* s_sel = reinterpret_cast<int*>(s_b + npr);                    // [npr] chosen
-    int* s_hist = s_sel + npr;  // [264] radix histogram, its pick, the count above theta, per-wavefront counts
+    int* s_hist = s_sel + npr;  // [276] radix histogram, its pick, the count above theta, per-wavefront counts
     const int kp = L.unit[(size_t)u * kUnitFields + kPinnedPages];
     const T* qg = (const T*)io.q + (size_t)u * G * D;
     for (int i = tid; i < G * D; i += nth) {
@@ -1948,13 +1948,13 @@ __global__ __launch_bounds__(256) void k_prompt_select(LayerView L, StepIO io) {
         s_b[p] = best;
     }
     __syncthreads();
-    // the topk pages of largest bound, ties to the lower slot. Up to one page
-    // per thread, each page is ranked against all others; beyond (the count
-    // is quadratic in the pages), theta, the topk-th largest bound (counted
-    // with multiplicity), by a radix select, then every page above it and,
-    // of those equal to it, the lowest slots, as many as are left (a prefix
+    // the topk pages of largest bound, ties to the lower slot. Up to 256
+    // pages, each page is ranked against all others; beyond (the count is
+    // quadratic in the pages), theta, the topk-th largest bound (counted with
+    // multiplicity), by a radix select, then every page above it and, of
+    // those equal to it, the lowest slots, as many as are left (a prefix
     // count in slot order): the same pages.
-    if (all || kp <= nth) {
+    if (all || kp <= 256) {
         for (int p = tid; p < npr; p += nth) {
             bool sel = p < kp;
             if (sel && !all) {
@@ -2277,7 +2277,8 @@ hipError_t allow_large_lds() {
 
 template <typename T, int GQ>
 void launch_select_g(const LayerView& L, const StepIO& io, size_t shm, hipStream_t stream) {
-    hipLaunchKernelGGL((k_prompt_select<T, GQ>), dim3(L.U), dim3(256), shm, stream, L, io);
+    // fewer units than CUs: a unit's pages over more threads
+    hipLaunchKernelGGL((k_prompt_select<T, GQ>), dim3(L.U), dim3(L.U < 256 ? 1024 : 256), shm, stream, L, io);
 }
 
 template <typename T, int... GS>
@@ -2289,7 +2290,7 @@ void launch_select_t(const LayerView& L, const StepIO& io, size_t shm, hipStream
 hipError_t launch_prompt_select(const LayerView& L, const StepIO& io, hipStream_t stream) {
     // q split in two (16 B per element), the bounds and the chosen flags, the
     // radix histogram and its counts
-    const size_t shm = (size_t)L.G * L.D * 16 + (size_t)L.dbase * 12 + 264 * 4;
+    const size_t shm = (size_t)L.G * L.D * 16 + (size_t)L.dbase * 12 + 276 * 4;
     if (L.bf16)
         launch_select_t<uint16_t>(L, io, shm, stream, std::make_integer_sequence<int, 16>{});
     else
