@@ -2030,7 +2030,7 @@ __global__ __launch_bounds__(1024) void k_prompt_select(LayerView L, StepIO io) 
 // the merge. merge 0: the step kernel wrote the outputs (bf16, one
 // workgroup per unit).
 template <typename T>
-__global__ __launch_bounds__(256) void k_epilogue(LayerView L, StepIO io, double r, int merge) {
+__global__ __launch_bounds__(1024) void k_epilogue(LayerView L, StepIO io, double r, int merge) {
     extern __shared__ __align__(16) unsigned char smem[];
     __shared__ RetShared ret;
     __shared__ int s_aux[260];
@@ -2376,10 +2376,11 @@ hipError_t launch_epilogue(const LayerView& L, const StepIO& io, double r, hipSt
     const size_t shm = (size_t)L.S * (8 + 12) + (L.agg ? (size_t)L.hgrp * L.G * 16 : 0) +
                        (merge ? ((size_t)2 * L.nsplit * L.G + L.G) * 4 : 0);
     const dim3 grid((unsigned)(L.U / L.hgrp));
+    const dim3 block(grid.x < 256 ? 1024 : 256);  // fewer workgroups than CUs: more threads each
     if (L.bf16)
-        hipLaunchKernelGGL(k_epilogue<uint16_t>, grid, dim3(256), shm, stream, L, io, r, merge);
+        hipLaunchKernelGGL(k_epilogue<uint16_t>, grid, block, shm, stream, L, io, r, merge);
     else
-        hipLaunchKernelGGL(k_epilogue<float>, grid, dim3(256), shm, stream, L, io, r, merge);
+        hipLaunchKernelGGL(k_epilogue<float>, grid, block, shm, stream, L, io, r, merge);
     return hipGetLastError();
 }
 
