@@ -2020,6 +2020,148 @@ __global__ __launch_bounds__(1024) void k_prompt_select(LayerView L, StepIO io) 
     }
 }
 
+// The same selection for bf16 pools, on the MFMA: each kept prompt page's
+// bound as an interval (prompt_bounds), lo_cut the topk-th largest lower end,
+// and the candidates, the pages whose upper end reaches lo_cut; at least
+// topk pages have bounds >= lo_cut, so every other page ranks below all of
+// them. Only the candidates' bounds are taken exactly (fp64, as the decode
+// pages' scores), and the topk among them, ties to the lower slot, are the
+// chosen pages. Then the fills and the block list, as above, the list's
+// positions by a prefix count over the whole workgroup. One workgroup of
+// NW wavefronts per unit.
+template <int D, int NW>
+__global__ __launch_bounds__(NW * 64) void k_prompt_select_mfma(LayerView L, StepIO io) {
+    extern __shared__ __align__(16) unsigned char smem[];
+    __shared__ int s_lo, s_ncand, s_wc[NW];
+    constexpr int KS = D / 32, NT = NW * 64;
+    const int u = blockIdx.x, tid = threadIdx.x, lane = tid & 63, w = tid >> 6, grp = lane >> 4, col = lane & 15;
+    if (io.active != nullptr && io.active[u / L.nkv] == 0) return;
+    const int G = L.G, S = L.S, ps = L.ps, npr = L.dbase;
+    const size_t base = (size_t)u * S;
+    float* s_qf = reinterpret_cast<float*>(smem);     // [G][qpad_row(D)] q in fp32 (a multiple of 16 bytes)
+    float* s_plo = s_qf + (size_t)G * qpad_row(D);    // [npr] bound intervals (16-byte reads of s_plo)
+    float* s_phi = s_plo + npr;
+    double* s_ex = reinterpret_cast<double*>(s_phi + npr);  // [npr] candidates' exact bounds
+    int* s_cand = reinterpret_cast<int*>(s_ex + npr);       // [npr] candidates
+    int* s_sel = s_cand + npr;                          // [npr] chosen
+    int* s_hist = s_sel + npr;                          // [258] radix histogram and its pick
+    const int kp = L.unit[(size_t)u * kUnitFields + kPinnedPages];
+    const bool all = kp <= L.topk;
+    // lane (grp, col < G): head col's channels 32 ks + 8 grp .. +7, the MFMA's query operands
+    const uint16_t* qg = (const uint16_t*)io.q + (size_t)u * G * D;
+    bf16x8 qv[KS];
+#pragma unroll
+    for (int ks = 0; ks < KS; ++ks) {
+        const u32x4 x = (col < G) ? ld4(qg + (size_t)col * D + 32 * ks + 8 * grp) : u32x4{0u, 0u, 0u, 0u};
+        qv[ks] = __builtin_bit_cast(bf16x8, x);
+    }
+    for (int p = tid; p < npr; p += NT) s_sel[p] = p < kp ? 1 : 0;
+    if (tid == 0) {
+        s_lo = 0x7FFFFFFF;
+        s_ncand = 0;
+    }
+    if (!all) {
+        // q in fp32 for the exact bounds, the wavefronts taking turns over ks
+#pragma unroll
+        for (int ks = 0; ks < KS; ++ks) {
+            if (ks % NW == w && col < G) {
+                const u32x4 x = __builtin_bit_cast(u32x4, qv[ks]);
+                float* d = s_qf + qpad_index<D>(col * D + 32 * ks + 8 * grp);
+#pragma unroll
+                for (int h = 0; h < 4; ++h) {
+                    d[2 * h] = __uint_as_float(x[h] << 16);
+                    d[2 * h + 1] = __uint_as_float(x[h] & 0xFFFF0000u);
+                }
+            }
+        }
+        prompt_bounds<D, NW, false>(L, base, kp, qv, s_plo, s_phi, [] {});
+    }
+    __syncthreads();
+    if (!all) {
+        float lo_cut;
+        if (kp > 256) {  // (the count is quadratic in the pages)
+            lo_cut = kth_largest_wg<NT>(s_plo, kp, L.topk, s_hist, tid);
+        } else {
+            const int kp4 = kp & ~3;
+            for (int p = tid; p < kp; p += NT) {
+                const float lp = s_plo[p];
+                int above = 0;  // lower ends above p's: four per 16-byte read, then the last few
+#pragma unroll 4
+                for (int o = 0; o < kp4; o += 4) {
+                    const float4 x = *reinterpret_cast<const float4*>(s_plo + o);
+                    above += (x.x > lp ? 1 : 0) + (x.y > lp ? 1 : 0) + (x.z > lp ? 1 : 0) + (x.w > lp ? 1 : 0);
+                }
+                for (int o = kp4; o < kp; ++o) above += s_plo[o] > lp ? 1 : 0;
+                if (above < L.topk) atomicMin(&s_lo, float_order(lp));
+            }
+            __syncthreads();
+            lo_cut = order_float(s_lo);
+        }
+        for (int p = tid; p < kp; p += NT) {
+            if (s_phi[p] >= lo_cut) s_cand[atomicAdd(&s_ncand, 1)] = p;
+            else s_sel[p] = 0;
+        }
+        __syncthreads();
+        // exactly topk candidates: they are the top k; more: their bounds in
+        // fp64, eight lanes per page, and the topk of those
+        const int nc = s_ncand;
+        if (nc > L.topk) {
+            for (int c0 = 8 * w; c0 < nc; c0 += 8 * NW) {
+                const int c = c0 + (lane >> 3);
+                const bool act = c < nc;
+                const int p = act ? s_cand[c] : 0;
+                ScoreFrag<D> f;
+                score_issue<D>(L, u, p, lane & 7, act, f);
+                const double sc = score_finish<D>(L, u, p, lane & 7, act, f, false, false, nullptr, s_qf, nullptr);
+                if (act && (lane & 7) == 0) s_ex[c] = sc;
+            }
+            __syncthreads();
+            for (int c = tid; c < nc; c += NT) {
+                const int p = s_cand[c];
+                const double e = s_ex[c];
+                int above = 0;
+                for (int o = 0; o < nc; ++o) {
+                    const double x = s_ex[o];
+                    above += (x > e || (x == e && s_cand[o] < p)) ? 1 : 0;
+                }
+                if (above >= L.topk) s_sel[p] = 0;
+            }
+        }
+    }
+    __syncthreads();
+    for (int p = tid; p < npr; p += NT) L.fill_att[base + p] = s_sel[p] ? L.fill[base + p] : 0;
+    for (int sl = npr + tid; sl < S; sl += NT) L.fill_att[base + sl] = L.fill[base + sl];
+    // the prompt blocks holding a chosen page, ascending (a block's place: the
+    // chosen blocks before it, in its wavefront and in the ones before), then
+    // every block of the decode region
+    const int nbp = npr * ps / 32;
+    int32_t* bl = L.blist + (size_t)u * L.lcap_blk;
+    int run = 0;
+    for (int c0 = 0; c0 < nbp; c0 += NT) {
+        const int bb = c0 + tid;
+        bool any = false;
+        if (bb < nbp)
+            for (int sl = 32 * bb / ps; sl <= (32 * bb + 31) / ps; ++sl) any = any || s_sel[sl] != 0;
+        const unsigned long long m = __ballot(any);
+        if (lane == 0) s_wc[w] = __popcll(m);
+        __syncthreads();
+        int before = run + __popcll(m & ((1ull << lane) - 1ull)), tot = 0;
+#pragma unroll
+        for (int ww = 0; ww < NW; ++ww) {
+            tot += s_wc[ww];
+            before += ww < w ? s_wc[ww] : 0;
+        }
+        if (any) bl[before] = bb;
+        run += tot;
+        __syncthreads();
+    }
+    for (int b = nbp + tid; b < L.nblk; b += NT) bl[run + b - nbp] = b;
+    if (tid == 0) {
+        L.bcnt[2 * u] = run;
+        L.bcnt[2 * u + 1] = run + max(0, L.nblk - nbp);
+    }
+}
+
 // Epilogue kernel of the split path: the retention policy on the scores the
 // step kernel wrote, and the merge of the splits' partial attention
 // (out = sum_s 2^(M_s - M) O_s / sum_s 2^(M_s - M) L_s); then the state goes
@@ -2287,14 +2429,30 @@ void launch_select_t(const LayerView& L, const StepIO& io, size_t shm, hipStream
     ((L.G == GS + 1 ? launch_select_g<T, GS + 1>(L, io, shm, stream) : void()), ...);
 }
 
+template <int D>
+void launch_select_mfma(const LayerView& L, const StepIO& io, hipStream_t stream) {
+    // q in fp32 (padded rows), per prompt slot the interval, the exact bound,
+    // the candidate and the chosen flag, and the radix histogram
+    const size_t shm = (size_t)L.G * qpad_row(D) * 4 + (size_t)L.dbase * 24 + 258 * 4;
+    // fewer units than CUs: 8 wavefronts per unit
+    if (L.U < 256)
+        hipLaunchKernelGGL((k_prompt_select_mfma<D, 8>), dim3(L.U), dim3(512), shm, stream, L, io);
+    else
+        hipLaunchKernelGGL((k_prompt_select_mfma<D, 4>), dim3(L.U), dim3(256), shm, stream, L, io);
+}
+
 hipError_t launch_prompt_select(const LayerView& L, const StepIO& io, hipStream_t stream) {
+    if (L.bf16) {
+        if (L.D == 128)
+            launch_select_mfma<128>(L, io, stream);
+        else
+            launch_select_mfma<64>(L, io, stream);
+        return hipGetLastError();
+    }
     // q split in two (16 B per element), the bounds and the chosen flags, the
     // radix histogram and its counts
     const size_t shm = (size_t)L.G * L.D * 16 + (size_t)L.dbase * 12 + 276 * 4;
-    if (L.bf16)
-        launch_select_t<uint16_t>(L, io, shm, stream, std::make_integer_sequence<int, 16>{});
-    else
-        launch_select_t<float>(L, io, shm, stream, std::make_integer_sequence<int, 16>{});
+    launch_select_t<float>(L, io, shm, stream, std::make_integer_sequence<int, 16>{});
     return hipGetLastError();
 }
 

@@ -787,19 +787,24 @@ def test_prompt_selection_ties(splits):
     assert chosen_without_6 > 0  # the tie decided the top 3 in some steps
 
 
-@pytest.mark.parametrize("splits", [None, 2], ids=["in-step", "selection-kernel"])
-def test_prompt_selection_ties_large_region(splits):
+@pytest.mark.parametrize("splits,B,P,copies", [(None, 64, 4608, (1, 4, 6)), (2, 64, 4608, (1, 4, 6)),
+                                                (2, 2, 8192, (1, 600, 1000))],
+                         ids=["in-step", "selection-kernel", "selection-kernel-few-units"])
+def test_prompt_selection_ties_large_region(splits, B, P, copies):
     """The tie case where the selection goes by a radix select: 512 units
     with a 4608-token prompt region at page 8, 576 kept pages, more than
     twice the in-step workgroup's threads (4 wavefronts) and more than the
     selection kernel's 256. In every unit prompt pages 1, 4 and 6 copy page
     2's keys, scaled so that the four lead the bounds: with top 3 the cut
     (or theta) is the bound the four share, and the tie rule alone keeps
-    slot 6 out. Keys are drawn on the GPU; four sampled units against the
-    oracle at every step."""
+    slot 6 out. Few units: 16 units over 1024 prompt pages (the selection
+    kernel's 8-wavefront form), the copies at pages 1, 600 and 1000, and the
+    rule keeps 1000 out.
+    Keys are drawn on the GPU; four sampled units against the oracle at
+    every step."""
     import torch
 
-    B, Hkv, Hq, d, ps, P, topk, budget, steps = 64, 8, 32, 128, 8, 4608, 3, 256, 40
+    Hkv, Hq, d, ps, topk, budget, steps = 8, 32, 128, 8, 3, 256, 40
     w = synth.get_workload("llama8b-b128-ps32-L512").replace(
         name="prompt-ties-large-region", batch=B, page_size=ps, budget=budget, prefill_len=P)
     G, U, npr = Hq // Hkv, B * Hkv, P // ps
@@ -809,8 +814,9 @@ def test_prompt_selection_ties_large_region(splits):
     K = torch.randn((B, Hkv, P, d), generator=gen, device="cuda")
     V = torch.randn((B, Hkv, P, d), generator=gen, device="cuda")
     K[:, :, 2 * ps:3 * ps] *= 3.0
-    for pg in (1, 4, 6):
+    for pg in copies:
         K[:, :, pg * ps:(pg + 1) * ps] = K[:, :, 2 * ps:3 * ps]
+    tied = sorted((2,) + tuple(copies))
     Kb, Vb = K.to(torch.bfloat16).contiguous(), V.to(torch.bfloat16).contiguous()
     del K, V
     units = _sample_units(w, 4)
@@ -826,7 +832,7 @@ def test_prompt_selection_ties_large_region(splits):
         orc[u] = m
     del Kb, Vb
     out = torch.empty((B, Hq, d), dtype=torch.bfloat16, device="cuda")
-    chosen_without_6 = 0
+    chosen_without_last = 0
     rep = ParityReport(units_checked=len(units))
     for t in range(steps):
         qb = torch.randn((B, Hq, d), generator=gen, device="cuda").to(torch.bfloat16)
@@ -841,13 +847,13 @@ def test_prompt_selection_ties_large_region(splits):
         for u in units:
             want = orc[u].decode(q64[u], k64[u], v64[u])
             att = orc[u].last_attended()[:npr]
-            if att[1] and att[2] and att[4] and not att[6]:
-                chosen_without_6 += 1
+            if all(att[pg] for pg in tied[:3]) and not att[tied[3]]:
+                chosen_without_last += 1
             compare_outputs(got[u][None], want[None], "bf16", "unit %d step %d" % (u, t), rep)
         rep.steps = t + 1
     pool.close()
     record(rep, "prompt-selection ties, large region")
-    assert chosen_without_6 == len(units) * steps  # the four lead at every step; the tie decides
+    assert chosen_without_last == len(units) * steps  # the four lead at every step; the tie decides
 
 
 @pytest.mark.parametrize("splits", [None, 2], ids=["in-step", "selection-kernel"])
@@ -927,6 +933,29 @@ def test_prompt_selection_large_region(batch, prompt, splits):
     rep = run_parity(w, seed=0, steps=400, units=_sample_units(w, 4), out_every=16, chunk=128, splits=splits,
                      prompt_tokens=prompt, prompt_topk=12)
     _report(rep, "prompt-selection large region")
+    assert rep.evictions > 0
+
+
+@pytest.mark.parametrize("ragged", [False, True], ids=["uniform", "ragged"])
+def test_prompt_selection_few_units(ragged):
+    """Fewer units than CUs over a long prompt region (page 8, 1024 prompt
+    slots, 16 units, split plans): the selection kernel in its 8-wavefront
+    form, bound intervals over 64 tiles, its cut by a radix select past 256
+    pages, and the block list placed by a prefix count over 1024 prompt
+    blocks. Ragged: prompts of 0, 40 (fewer pages than topk, nothing to
+    rank), 3000 and 8192 tokens on four sequences that take steps by a
+    random mask, two of them re-prefilled mid-run. Every unit, every step."""
+    if ragged:
+        w = small(batch=4, n_q_heads=16, n_kv_heads=4, page_size=8, budget=128, decode_steps=300)
+        _say("case prompt-selection few units, ragged")
+        rep = run_ragged(w, seed=29, lens=[0, 40, 3000, 8192], steps=w.decode_steps,
+                         reprefill={100: {1: 8000}, 200: {3: 600}}, splits=3, prompt_tokens=8192, prompt_topk=5)
+    else:
+        w = small(batch=2, n_q_heads=32, n_kv_heads=8, page_size=8, budget=256, prefill_len=8192,
+                  decode_steps=300)
+        _say("case prompt-selection few units")
+        rep = run_parity(w, seed=5, steps=w.decode_steps, splits=2, prompt_tokens=8192, prompt_topk=12)
+    _report(rep, "prompt-selection few units")
     assert rep.evictions > 0
 
 
