@@ -56,6 +56,8 @@ struct LayerView {
     int32_t* fill_att;  // [U][S] fills the attention sees: fill, or (topk >= 0) 0 for unchosen prompt pages
     int32_t* blist;     // [U][lcap_blk] blocks a step visits (topk >= 0): chosen prompt blocks, decode blocks
     int32_t* bcnt;      // [U][2] prompt blocks and all blocks in blist
+    float* pivl;        // [2][U][dbase] prompt pages' bound intervals (lower, upper) from k_prompt_intervals
+    int pchunk;         // prompt pages per k_prompt_intervals workgroup; 0: the selection kernel bounds them itself
     int lcap_blk;       // Lcap / 32
     int nt;             // 1: K/V blocks streamed with non-temporal loads
     int det;            // 1: each wavefront takes a fixed interleave of the blocks (reproducible sums)

@@ -2020,6 +2020,30 @@ __global__ __launch_bounds__(1024) void k_prompt_select(LayerView L, StepIO io) 
     }
 }
 
+// The kept prompt pages' bound intervals (prompt_bounds) into L.pivl, for
+// units too few to fill the chip: one wavefront per L.pchunk pages of a
+// unit, so that the pages' representative keys stream through many CUs;
+// nothing for units with no more kept pages than topk.
+template <int D>
+__global__ __launch_bounds__(64) void k_prompt_intervals(LayerView L, StepIO io) {
+    constexpr int KS = D / 32;
+    const int nch = (L.dbase + L.pchunk - 1) / L.pchunk;
+    const int u = blockIdx.x / nch, ch = blockIdx.x - u * nch;
+    if (io.active != nullptr && io.active[u / L.nkv] == 0) return;
+    const int kp = L.unit[(size_t)u * kUnitFields + kPinnedPages], p0 = ch * L.pchunk;
+    if (kp <= L.topk || p0 >= kp) return;
+    const int n = min(L.pchunk, kp - p0), lane = threadIdx.x, grp = lane >> 4, col = lane & 15;
+    const uint16_t* qg = (const uint16_t*)io.q + (size_t)u * L.G * D;
+    bf16x8 qv[KS];
+#pragma unroll
+    for (int ks = 0; ks < KS; ++ks) {
+        const u32x4 x = (col < L.G) ? ld4(qg + (size_t)col * D + 32 * ks + 8 * grp) : u32x4{0u, 0u, 0u, 0u};
+        qv[ks] = __builtin_bit_cast(bf16x8, x);
+    }
+    float* lo = L.pivl + (size_t)u * L.dbase + p0;
+    prompt_bounds<D, 1, false>(L, (size_t)u * L.S + p0, n, qv, lo, lo + (size_t)L.U * L.dbase, [] {});
+}
+
 // The same selection for bf16 pools, on the MFMA: each kept prompt page's
 // bound as an interval (prompt_bounds), lo_cut the topk-th largest lower end,
 // and the candidates, the pages whose upper end reaches lo_cut; at least
@@ -2028,7 +2052,8 @@ __global__ __launch_bounds__(1024) void k_prompt_select(LayerView L, StepIO io) 
 // pages' scores), and the topk among them, ties to the lower slot, are the
 // chosen pages. Then the fills and the block list, as above, the list's
 // positions by a prefix count over the whole workgroup. One workgroup of
-// NW wavefronts per unit.
+// NW wavefronts per unit. With L.pchunk > 0 the intervals come from
+// k_prompt_intervals, launched just before.
 template <int D, int NW>
 __global__ __launch_bounds__(NW * 64) void k_prompt_select_mfma(LayerView L, StepIO io) {
     extern __shared__ __align__(16) unsigned char smem[];
@@ -2074,7 +2099,16 @@ __global__ __launch_bounds__(NW * 64) void k_prompt_select_mfma(LayerView L, Ste
                 }
             }
         }
-        prompt_bounds<D, NW, false>(L, base, kp, qv, s_plo, s_phi, [] {});
+        if (L.pchunk > 0) {
+            const float* glo = L.pivl + (size_t)u * npr;
+            const float* ghi = glo + (size_t)L.U * npr;
+            for (int p = tid; p < kp; p += NT) {
+                s_plo[p] = glo[p];
+                s_phi[p] = ghi[p];
+            }
+        } else {
+            prompt_bounds<D, NW, false>(L, base, kp, qv, s_plo, s_phi, [] {});
+        }
     }
     __syncthreads();
     if (!all) {
@@ -2434,6 +2468,10 @@ void launch_select_mfma(const LayerView& L, const StepIO& io, hipStream_t stream
     // q in fp32 (padded rows), per prompt slot the interval, the exact bound,
     // the candidate and the chosen flag, and the radix histogram
     const size_t shm = (size_t)L.G * qpad_row(D) * 4 + (size_t)L.dbase * 24 + 258 * 4;
+    if (L.pchunk > 0) {
+        const int nch = (L.dbase + L.pchunk - 1) / L.pchunk;
+        hipLaunchKernelGGL((k_prompt_intervals<D>), dim3(L.U * nch), dim3(64), 0, stream, L, io);
+    }
     // fewer units than CUs: 8 wavefronts per unit
     if (L.U < 256)
         hipLaunchKernelGGL((k_prompt_select_mfma<D, 8>), dim3(L.U), dim3(512), shm, stream, L, io);

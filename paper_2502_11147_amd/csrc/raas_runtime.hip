@@ -65,6 +65,7 @@ struct raas_pool {
     int32_t* fill_att = nullptr;  // [U][S] fills the attention sees (prompt selection), scratch of one step
     int32_t* blist = nullptr;     // [U][Lcap/32] blocks a step visits (prompt selection), likewise
     int32_t* bcnt = nullptr;      // [U][2]
+    float* pivl = nullptr;        // [2][U][npr] prompt bound intervals (bf16, fewer units than CUs)
     int npr = 0;                  // prompt region's slots (0: none)
     int nt = 0;                   // K/V blocks streamed with non-temporal loads
     int32_t* seqbuf = nullptr;   // [2][batch] prefill lengths and mask of a ragged prefill
@@ -139,6 +140,8 @@ LayerView view(const raas_pool* p, int layer) {
     L.fill_att = p->npr > 0 ? p->fill_att : L.fill;
     L.blist = p->blist;
     L.bcnt = p->bcnt;
+    L.pivl = p->pivl;
+    L.pchunk = 0;
     L.lcap_blk = p->Lcap / kBlockTokens;
     L.nt = p->nt;
     L.det = p->cfg.deterministic;
@@ -340,6 +343,15 @@ raas_status decode_step(raas_pool* p, int32_t layer, const StepIO& io, hipStream
     const bool prof = !fixed_scratch;
 
     if (select_kernel) {  // Quest on the prompt: which prompt pages this step attends to
+        // Fewer units than CUs and a long prompt region (bf16): the prompt
+        // pages' bound intervals first, by a kernel of about 256 workgroups
+        // of 32 or more pages each (the selection kernel would draw them on
+        // one CU per unit); not with the static scratch, which holds no
+        // intervals.
+        if (!fixed_scratch && p->cfg.dtype == RAAS_BF16 && p->U < 256 && p->npr > 256) {
+            const int per = (p->npr * p->U + 255) / 256;
+            L.pchunk = std::max(32, (per + 15) / 16 * 16);
+        }
         if (prof) prof_record(p, 2, true, s);
         hipError_t e = launch_prompt_select(L, io, s);
         if (prof) prof_record(p, 2, false, s);
@@ -420,6 +432,7 @@ raas_status raas_create_pool(const raas_config* cfg, void* stream, raas_pool** o
         {(void**)&p->fill_att, p->npr > 0 ? (size_t)p->U * p->S * sizeof(int32_t) : 4},
         {(void**)&p->blist, p->npr > 0 ? (size_t)p->U * (p->Lcap / kBlockTokens) * sizeof(int32_t) : 4},
         {(void**)&p->bcnt, p->npr > 0 ? (size_t)p->U * 2 * sizeof(int32_t) : 4},
+        {(void**)&p->pivl, p->npr > 0 ? 2 * (size_t)p->U * p->npr * sizeof(float) : 4},
     };
     hipStream_t s = (hipStream_t)stream;
     hipError_t ea = allow_large_lds();
@@ -471,7 +484,7 @@ void raas_destroy(raas_pool* p) {
             if (ev) (void)hipEventDestroy(ev);
     }
     void* ptrs[] = {p->K,     p->V,     p->kmin,  p->kmax,     p->meta,  p->unit, p->err,
-                    p->part,  p->score, p->seqbuf, p->fill_att, p->blist, p->bcnt};
+                    p->part,  p->score, p->seqbuf, p->fill_att, p->blist, p->bcnt, p->pivl};
     for (void* q : ptrs)
         if (q) (void)hipFree(q);
     if (p->seqhost) (void)hipHostFree(p->seqhost);
