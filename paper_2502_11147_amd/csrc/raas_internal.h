@@ -99,7 +99,8 @@ struct StepPlan {
 // list_ints: LDS ints of a block list or of the in-step prompt selection (0
 // without a prompt region)
 StepPlan plan_step(int U, int G, int D, int S, int Lcap, int ps, int work_blocks, bool bf16, int agg,
-                   bool grouped, int list_ints, int split_override);
+                   bool grouped, int list_ints, int split_override,
+                   int npr);
 // Quest on the prompt pages: the attended fills and the block list of a step.
 hipError_t launch_prompt_select(const LayerView& L, const StepIO& io, hipStream_t stream);
 // Lets the step kernels use more than the default dynamic LDS.

@@ -2362,6 +2362,16 @@ hipError_t allow_lds_all(int bytes) {
 // over a split (measured at batch 1 and 4, 32 blocks per unit over 8
 // wavefronts: 14.6 against 19.2 us and 15.9 against 19.7 us per step).
 constexpr int kFusedBlocksPerWave = 6;
+// With a prompt region and fewer units than CUs, fused up to this many
+// attended blocks per wavefront and prompt pages (batch 1 and 8, 128 prompt
+// pages, 72 attended blocks over 8 wavefronts: 30.3 against 36.2 and 32.2
+// against 36.2 us per step; batch 4, 512 pages, 80 blocks: 44.0 against
+// 54.4 us, the fused kernel 40.1 us and the split path's four kernels 37.5
+// to 39.1 us before their launch gaps; at 1024 prompt pages the fused
+// workgroup's own bound intervals cost more than the split path's
+// kernels: 68.8 against 45.9 us at batch 1).
+constexpr int kFusedPromptBlocksPerWave = 12;
+constexpr int kFusedPromptPages = 512;
 
 // Workgroups of 2 wavefronts, four per CU, from this many units on when a
 // unit's step attends at most kSmallWorkBlocks blocks (same box, batch 128,
@@ -2371,7 +2381,7 @@ constexpr int kSmallWorkUnits = 1024;
 constexpr int kSmallWorkBlocks = 32;
 
 StepPlan plan_step(int U, int G, int D, int S, int Lcap, int ps, int work_blocks, bool bf16, int agg,
-                   bool grouped, int list_ints, int split_override) {
+                   bool grouped, int list_ints, int split_override, int npr) {
     (void)ps;
     StepPlan pl{};
     const int nblk = Lcap / kBlockTokens;
@@ -2405,6 +2415,13 @@ StepPlan plan_step(int U, int G, int D, int S, int Lcap, int ps, int work_blocks
             // few blocks per wavefront: one workgroup per unit, which also runs
             // the epilogue, beats spreading the unit over more CUs and paying a
             // second launch (about 10 us) for the merge
+            want = 1;
+        } else if (!grouped && list_ints > 0 && !agg && U < 256 && npr <= kFusedPromptPages &&
+                   work_blocks <= kFusedPromptBlocksPerWave * pl.waves &&
+                   step_lds(G, D, S, pl.waves, true, agg, list_ints) <= kMaxLds) {
+            // a short prompt region: the fused workgroup chooses its prompt
+            // pages itself and attends the chosen blocks and the decode ones,
+            // which saves the selection kernel's launch as well
             want = 1;
         } else {
             // one workgroup per CU over the 256 CUs

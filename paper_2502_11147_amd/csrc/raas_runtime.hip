@@ -300,7 +300,7 @@ raas_status decode_step(raas_pool* p, int32_t layer, const StepIO& io, hipStream
     }
     const StepPlan pl = plan_step(p->U, p->G, p->D, p->S, L.nblk * kBlockTokens, p->ps, work_blocks,
                                   p->cfg.dtype == RAAS_BF16, p->cfg.score_aggregation,
-                                  p->cfg.decision_scope == RAAS_SCOPE_SEQUENCE, list_ints(p), p->split_override);
+                                  p->cfg.decision_scope == RAAS_SCOPE_SEQUENCE, list_ints(p), p->split_override, p->npr);
     L.nsplit = pl.nsplit;
     L.bps = pl.bps;
     // the first score pass issued with the first blocks: the score barrier and
@@ -344,12 +344,12 @@ raas_status decode_step(raas_pool* p, int32_t layer, const StepIO& io, hipStream
 
     if (select_kernel) {  // Quest on the prompt: which prompt pages this step attends to
         // Fewer units than CUs and a long prompt region (bf16): the prompt
-        // pages' bound intervals first, by a kernel of about 256 workgroups
-        // of 32 or more pages each (the selection kernel would draw them on
-        // one CU per unit); not with the static scratch, which holds no
-        // intervals.
+        // pages' bound intervals first, by a kernel of single-wavefront
+        // workgroups of 32 or more pages each, up to about eight per CU (the
+        // selection kernel would draw them on one CU per unit); not with the
+        // static scratch, which holds no intervals.
         if (!fixed_scratch && p->cfg.dtype == RAAS_BF16 && p->U < 256 && p->npr > 256) {
-            const int per = (p->npr * p->U + 255) / 256;
+            const int per = (p->npr * p->U + 2047) / 2048;
             L.pchunk = std::max(32, (per + 15) / 16 * 16);
         }
         if (prof) prof_record(p, 2, true, s);

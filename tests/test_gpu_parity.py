@@ -936,7 +936,7 @@ def test_prompt_selection_large_region(batch, prompt, splits):
     assert rep.evictions > 0
 
 
-@pytest.mark.parametrize("ragged", [False, True], ids=["uniform", "ragged"])
+@pytest.mark.parametrize("ragged", [False, True, "fused"], ids=["uniform", "ragged", "fused-512-pages"])
 def test_prompt_selection_few_units(ragged):
     """Fewer units than CUs over a long prompt region (page 8, 1024 prompt
     slots, 16 units, split plans): the selection kernel in its 8-wavefront
@@ -944,8 +944,16 @@ def test_prompt_selection_few_units(ragged):
     pages, and the block list placed by a prefix count over 1024 prompt
     blocks. Ragged: prompts of 0, 40 (fewer pages than topk, nothing to
     rank), 3000 and 8192 tokens on four sequences that take steps by a
-    random mask, two of them re-prefilled mid-run. Every unit, every step."""
-    if ragged:
+    random mask, two of them re-prefilled mid-run. Fused: 8 units over 512
+    prompt pages at page 16 with the plan's own choice, one fused workgroup
+    of 8 wavefronts per unit selecting in the step kernel (its count over
+    512 lower ends). Every unit, every step."""
+    if ragged == "fused":
+        w = small(batch=2, n_q_heads=16, n_kv_heads=4, page_size=16, budget=256, prefill_len=8192,
+                  decode_steps=300)
+        _say("case prompt-selection few units, fused, 512 prompt pages")
+        rep = run_parity(w, seed=7, steps=w.decode_steps, prompt_tokens=8192, prompt_topk=10)
+    elif ragged:
         w = small(batch=4, n_q_heads=16, n_kv_heads=4, page_size=8, budget=128, decode_steps=300)
         _say("case prompt-selection few units, ragged")
         rep = run_ragged(w, seed=29, lens=[0, 40, 3000, 8192], steps=w.decode_steps,
