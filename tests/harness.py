@@ -204,6 +204,46 @@ def random_large_case(i: int) -> dict:
                 splits=splits, deterministic=det)
 
 
+def random_prompt_case(i: int) -> dict:
+    """Seeded random configuration i with a long prompt region at a small
+    batch (at most 16 units): 128 to 1200 prompt pages at page 8, 16 or 32,
+    topk up to 40, prompts that fill a quarter of the region to more than
+    all of it, a decode budget of at most 240 tokens, which the run passes;
+    fp32 pools every sixth case, the score aggregation, the sequence scope,
+    forced splits and the deterministic option drawn as in random_case. These
+    reach the plan's choices for prompt regions at small batch: the fused
+    workgroup's own selection, the selection kernel with and without the
+    separate interval kernel, and the fp32 selection kernel."""
+    import math
+
+    rng = np.random.default_rng(9000 + i)
+    dtype = "f32" if i % 6 == 5 else "bf16"  # (every sixth: the fp32 selection kernel)
+    d = int(rng.choice([64, 128]))
+    G = int(rng.choice([1, 2, 4, 7, 8]))
+    hkv = int(rng.choice([1, 2, 4, 8]))
+    batch = int(rng.integers(1, 16 // hkv + 1))
+    ps = int(rng.choice([8, 16, 32]))
+    unit = ps * 32 // math.gcd(ps, 32)
+    prompt_tokens = unit * int(rng.integers(128 * ps // unit, min(16384, 1200 * ps) // unit + 1))
+    npr = prompt_tokens // ps
+    budget = ps * int(rng.integers(4, max(4, 240 // ps) + 1))
+    prefill = int(rng.integers(prompt_tokens // 4, prompt_tokens + budget + 1))
+    prompt_topk = int(rng.integers(1, min(40, npr) + 1))
+    r = float(rng.choice([0.25, 0.5, 0.7, 0.9]))
+    agg = int(rng.random() < 0.2)
+    scope = int(rng.random() < 0.1)
+    splits = None if rng.random() < 0.7 else int(rng.integers(2, 6))
+    det = bool(rng.random() < 0.1)
+    steps = int(budget + 3 * ps + 40)
+    return dict(workload=dict(name="random-prompt-%02d" % i, batch=batch, n_layers=1, n_q_heads=G * hkv,
+                              n_kv_heads=hkv, head_dim=d, dtype=dtype, page_size=ps, budget=budget,
+                              prefill_len=prefill, decode_steps=steps, r=r, ms_period=16,
+                              ms_phase_random=True, ms_wmin=8, ms_wmax=64),
+                variant=dict(aggregation=agg, rank_pinned=False, scope=scope, prompt_tokens=prompt_tokens,
+                             prompt_topk=prompt_topk),
+                splits=splits, deterministic=det)
+
+
 def unit_index(w, seq, kvh):
     return seq * w.n_kv_heads + kvh
 

@@ -9,12 +9,13 @@ import os
 
 import pytest
 
-from harness import new_pool, random_case, random_large_case, record, run_parity, say
+from harness import new_pool, random_case, random_large_case, random_prompt_case, record, run_parity, say
 
 pytestmark = pytest.mark.gpu
 
 N_CASES = int(os.environ.get("RAAS_RANDOM_CASES", "64"))  # more for a longer sweep
 N_LARGE = int(os.environ.get("RAAS_RANDOM_LARGE_CASES", "16"))
+N_PROMPT = int(os.environ.get("RAAS_RANDOM_PROMPT_CASES", "24"))
 
 
 @pytest.fixture(scope="module", autouse=True)
@@ -61,3 +62,29 @@ def test_random_large_config_parity(i):
     record(rep, "random large %02d" % i)
     assert rep.flagged_divergences == 0, rep.line("random large %02d" % i)
     assert rep.evictions > 0, rep.line("random large %02d" % i)
+
+
+@pytest.mark.parametrize("i", range(N_PROMPT), ids=["prompt-%02d" % i for i in range(N_PROMPT)])
+def test_random_prompt_region_parity(i):
+    """Long prompt regions at a small batch (harness.random_prompt_case):
+    four sampled units' retention at every step and outputs every 4th,
+    past the budget; the other units replay a ring of seeded steps."""
+    import numpy as np
+
+    import synth
+
+    c = random_prompt_case(i)
+    w = synth.Workload(**c["workload"])
+    U = w.batch * w.n_kv_heads
+    units = sorted({0, U - 1} | set(int(x) for x in np.random.default_rng(i).integers(0, U, 2)))
+    say("case %s %s splits %s deterministic %s units %s" % (c["workload"], c["variant"], c["splits"],
+                                                             c["deterministic"], units))
+    pool = new_pool(w, c["splits"], deterministic=c["deterministic"], **c["variant"])
+    try:
+        rep = run_parity(w, seed=130 + i, steps=w.decode_steps, pool=pool, units=units, out_every=4,
+                         others="ring", **c["variant"])
+    finally:
+        pool.close()
+    record(rep, "random prompt %02d" % i)
+    assert rep.flagged_divergences == 0, rep.line("random prompt %02d" % i)
+    assert rep.evictions > 0, rep.line("random prompt %02d" % i)

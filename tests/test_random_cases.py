@@ -1,8 +1,8 @@
 """The seeded random configurations of the GPU sweep (harness.random_case)
 are valid pools and cover each switch both ways."""
-from harness import random_case, random_large_case
+from harness import random_case, random_large_case, random_prompt_case
 
-from test_gpu_random import N_CASES, N_LARGE
+from test_gpu_random import N_CASES, N_LARGE, N_PROMPT
 
 
 def test_random_cases_are_valid_and_varied():
@@ -43,3 +43,19 @@ def test_random_large_cases_are_valid():
         assert 2 <= (w["budget"] + v["prompt_tokens"]) // w["page_size"] <= 2048
         assert not (v["rank_pinned"] and v["prompt_tokens"])
         assert v["prompt_topk"] <= v["prompt_tokens"] // w["page_size"]
+
+
+def test_random_prompt_cases_are_valid():
+    cases = [random_prompt_case(i) for i in range(max(N_PROMPT, 16))]
+    pages = [c["variant"]["prompt_tokens"] // c["workload"]["page_size"] for c in cases]
+    assert min(pages) <= 512 < max(pages) and any(p > 256 for p in pages)
+    assert {c["workload"]["dtype"] for c in cases} == {"bf16", "f32"}
+    for c in cases:
+        w, v = c["workload"], c["variant"]
+        npr = v["prompt_tokens"] // w["page_size"]
+        assert w["batch"] * w["n_kv_heads"] <= 16 and w["n_q_heads"] // w["n_kv_heads"] <= 16
+        assert v["prompt_tokens"] % w["page_size"] == 0 and v["prompt_tokens"] % 32 == 0
+        assert 128 <= npr <= 1200 and 1 <= v["prompt_topk"] <= min(40, npr)
+        assert 2 <= (w["budget"] + v["prompt_tokens"]) // w["page_size"] <= 2048
+        assert w["budget"] % w["page_size"] == 0 and w["decode_steps"] > w["budget"] + w["page_size"]
+        assert w["batch"] * w["n_kv_heads"] * w["prefill_len"] * w["head_dim"] <= 16 * 17000 * 128
