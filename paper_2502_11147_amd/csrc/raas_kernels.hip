@@ -2360,8 +2360,11 @@ hipError_t allow_lds_all(int bytes) {
 
 // Blocks per wavefront up to which one fused workgroup per unit is chosen
 // over a split (measured at batch 1 and 4, 32 blocks per unit over 8
-// wavefronts: 14.6 against 19.2 us and 15.9 against 19.7 us per step).
-constexpr int kFusedBlocksPerWave = 6;
+// wavefronts: 14.6 against 19.2 us and 15.9 against 19.7 us per step; 64
+// blocks at batch 1, 4 and 8: the fused kernel 17.1, 17.4 and 18.0 us
+// against 17.6, 18.6 and 20.4 us for the split path's two kernels, before
+// their second launch; 128 blocks at batch 1: 23.9 against 19.0 us).
+constexpr int kFusedBlocksPerWave = 8;
 // With a prompt region and fewer units than CUs, fused up to this many
 // attended blocks per wavefront and prompt pages (batch 1 and 8, 128 prompt
 // pages, 72 attended blocks over 8 wavefronts: 30.3 against 36.2 and 32.2
