@@ -2360,11 +2360,16 @@ hipError_t allow_lds_all(int bytes) {
 
 // Blocks per wavefront up to which one fused workgroup per unit is chosen
 // over a split (measured at batch 1 and 4, 32 blocks per unit over 8
-// wavefronts: 14.6 against 19.2 us and 15.9 against 19.7 us per step; 64
-// blocks at batch 1, 4 and 8: the fused kernel 17.1, 17.4 and 18.0 us
-// against 17.6, 18.6 and 20.4 us for the split path's two kernels, before
-// their second launch; 128 blocks at batch 1: 23.9 against 19.0 us).
-constexpr int kFusedBlocksPerWave = 8;
+// wavefronts: 14.6 against 19.2 us and 15.9 against 19.7 us per step), and
+// up to kFusedBlocksPerWaveFewSlots with at most kFewSlots slots, where the
+// fused workgroup's retention (one wavefront counting over all slots) is
+// short: 64 blocks and 64 slots at batch 1, 4 and 8, the fused kernel
+// 17.1, 17.4 and 18.0 us against 17.6, 18.6 and 20.4 us for the split
+// path's two kernels before their second launch; with 128 slots (page 16)
+// fused took 22.0 against 20.3 us per step at batch 4.
+constexpr int kFusedBlocksPerWave = 6;
+constexpr int kFusedBlocksPerWaveFewSlots = 8;
+constexpr int kFewSlots = 64;
 // With a prompt region and fewer units than CUs, fused up to this many
 // attended blocks per wavefront and prompt pages (batch 1 and 8, 128 prompt
 // pages, 72 attended blocks over 8 wavefronts: 30.3 against 36.2 and 32.2
@@ -2413,7 +2418,9 @@ StepPlan plan_step(int U, int G, int D, int S, int Lcap, int ps, int work_blocks
             pl.waves = 2;
         if (split_override > 0) {
             want = split_override;
-        } else if (!grouped && nblk <= kFusedBlocksPerWave * pl.waves &&
+        } else if (!grouped &&
+                   (nblk <= kFusedBlocksPerWave * pl.waves ||
+                    (S <= kFewSlots && nblk <= kFusedBlocksPerWaveFewSlots * pl.waves)) &&
                    step_lds(G, D, S, pl.waves, true, agg, list_ints) <= kMaxLds) {
             // few blocks per wavefront: one workgroup per unit, which also runs
             // the epilogue, beats spreading the unit over more CUs and paying a

@@ -259,15 +259,15 @@ def test_deterministic_option_parity(case):
     assert rep.evictions > 0
 
 
-@pytest.mark.parametrize("splits", [8, None], ids=["split-8", "auto-fused"])
+@pytest.mark.parametrize("splits", [None, 1], ids=["auto-split", "fused"])
 @pytest.mark.parametrize("det", [False, True], ids=["dynamic", "deterministic"])
 def test_long_pool_small_batch(det, splits):
-    """Pools of 64 blocks at 4 units, whose workgroups of 8 wavefronts
-    issue the first score pass with the first blocks: split eight ways over
-    the CUs (the plan's choice before it kept 64 blocks fused), and the
-    plan's own choice, one fused workgroup per unit, with every unit's
-    outputs compared at every step, through the budget and 600 steps past
-    it, with the dynamic claims and the deterministic option."""
+    """Pools of 64 blocks and more at 4 units, whose workgroups of 8
+    wavefronts issue the first score pass with the first blocks: the plan's
+    own split over the CUs, and one fused workgroup per unit (the plan of
+    the batch-32 workload, forced here), with every unit's outputs compared
+    at every step, through the budget and 600 steps past it, with the
+    dynamic claims and the deterministic option."""
     w = small(batch=2, n_kv_heads=2, n_q_heads=8, budget=2048, prefill_len=1000, decode_steps=1700)
     _say("case long pool small batch deterministic %s splits %s" % (det, splits))
     pool = new_pool(w, splits, deterministic=det)
