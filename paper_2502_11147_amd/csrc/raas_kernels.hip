@@ -2499,11 +2499,14 @@ void launch_select_mfma(const LayerView& L, const StepIO& io, hipStream_t stream
         const int nch = (L.dbase + L.pchunk - 1) / L.pchunk;
         hipLaunchKernelGGL((k_prompt_intervals<D>), dim3(L.U * nch), dim3(64), 0, stream, L, io);
     }
-    // fewer units than CUs: 8 wavefronts per unit
+    // fewer units than CUs: 8 wavefronts per unit; four units per CU and
+    // more: 2, so that more units are resident at once
     if (L.U < 256)
         hipLaunchKernelGGL((k_prompt_select_mfma<D, 8>), dim3(L.U), dim3(512), shm, stream, L, io);
-    else
+    else if (L.U < 1024)
         hipLaunchKernelGGL((k_prompt_select_mfma<D, 4>), dim3(L.U), dim3(256), shm, stream, L, io);
+    else
+        hipLaunchKernelGGL((k_prompt_select_mfma<D, 2>), dim3(L.U), dim3(128), shm, stream, L, io);
 }
 
 hipError_t launch_prompt_select(const LayerView& L, const StepIO& io, hipStream_t stream) {
